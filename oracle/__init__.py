@@ -1,0 +1,13 @@
+"""Plain, slow, fp64 CPU oracle of the ensemble-inference hot path.
+
+TEST INFRASTRUCTURE ONLY.  Only the tests, the smoke check and the benchmark's CPU
+baseline may import this package; the product path never calls it and shares no
+code with it.
+"""
+from .reference import (to_bf16_rne, conv2d, batchnorm, relu, maxpool2d, global_avgpool, fc,
+                        embedding, conv1d_maxtime, concat, softmax, combine_mean, argmax_first,
+                        run_model, ensemble, model_macs)
+
+__all__ = ["to_bf16_rne", "conv2d", "batchnorm", "relu", "maxpool2d", "global_avgpool", "fc",
+           "embedding", "conv1d_maxtime", "concat", "softmax", "combine_mean", "argmax_first",
+           "run_model", "ensemble", "model_macs"]

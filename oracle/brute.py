@@ -1,0 +1,87 @@
+"""Scalar pure-Python loops for tiny inputs: an independent second reading of the
+layer definitions, used only to pin the vectorised oracle.
+
+TEST INFRASTRUCTURE ONLY.  Each function follows the textbook definition directly,
+one output element at a time, on nested Python lists or small numpy arrays.
+"""
+import math
+
+
+def conv2d(x, w, stride, pad, bias=None):
+    """x [N][C][H][W], w [O][C][kh][kw]: cross-correlation with zero padding."""
+    N, C, H, W = len(x), len(x[0]), len(x[0][0]), len(x[0][0][0])
+    O, kh, kw = len(w), len(w[0][0]), len(w[0][0][0])
+    Ho = (H + 2 * pad - kh) // stride + 1
+    Wo = (W + 2 * pad - kw) // stride + 1
+    out = [[[[0.0] * Wo for _ in range(Ho)] for _ in range(O)] for _ in range(N)]
+    for n in range(N):
+        for o in range(O):
+            for yy in range(Ho):
+                for xx in range(Wo):
+                    s = 0.0 if bias is None else float(bias[o])
+                    for c in range(C):
+                        for u in range(kh):
+                            for v in range(kw):
+                                iy = yy * stride + u - pad
+                                ix = xx * stride + v - pad
+                                if 0 <= iy < H and 0 <= ix < W:
+                                    s += float(w[o][c][u][v]) * float(x[n][c][iy][ix])
+                    out[n][o][yy][xx] = s
+    return out
+
+
+def maxpool2d(x, k, stride, pad):
+    N, C, H, W = len(x), len(x[0]), len(x[0][0]), len(x[0][0][0])
+    Ho = (H + 2 * pad - k) // stride + 1
+    Wo = (W + 2 * pad - k) // stride + 1
+    out = [[[[0.0] * Wo for _ in range(Ho)] for _ in range(C)] for _ in range(N)]
+    for n in range(N):
+        for c in range(C):
+            for yy in range(Ho):
+                for xx in range(Wo):
+                    m = -math.inf
+                    for u in range(k):
+                        for v in range(k):
+                            iy, ix = yy * stride + u - pad, xx * stride + v - pad
+                            if 0 <= iy < H and 0 <= ix < W:
+                                m = max(m, float(x[n][c][iy][ix]))
+                    out[n][c][yy][xx] = m
+    return out
+
+
+def fc(x, w, bias=None):
+    """x [N][I] (already flat), w [O][I]."""
+    out = []
+    for row in x:
+        out.append([(0.0 if bias is None else float(bias[o])) +
+                    sum(float(w[o][i]) * float(row[i]) for i in range(len(row))) for o in range(len(w))])
+    return out
+
+
+def conv1d_maxtime(e, w, bias, apply_relu):
+    """e [N][L][D], w [F][D][k] -> [N][F]."""
+    N, L, D = len(e), len(e[0]), len(e[0][0])
+    F, k = len(w), len(w[0][0])
+    out = []
+    for n in range(N):
+        row = []
+        for f in range(F):
+            best = -math.inf
+            for t in range(L - k + 1):
+                s = 0.0 if bias is None else float(bias[f])
+                for j in range(k):
+                    for d in range(D):
+                        s += float(e[n][t + j][d]) * float(w[f][d][j])
+                if apply_relu:
+                    s = max(s, 0.0)
+                best = max(best, s)
+            row.append(best)
+        out.append(row)
+    return out
+
+
+def softmax_row(z):
+    m = max(z)
+    ex = [math.exp(v - m) for v in z]
+    s = sum(ex)
+    return [v / s for v in ex]
