@@ -1,0 +1,155 @@
+/*
+ * rafiki_ensemble.h -- C ABI of the MI355X (gfx950) ensemble-inference hot path.
+ *
+ * The paper's inference service deploys a list of trained models as one inference
+ * job (Section 3: the SDK gets model instances -- a model name plus the names of its
+ * parameters in the parameter server -- creates the inference job with them and
+ * deploys it; workers then fetch the parameters).  Each scheduled batch of the
+ * oldest b requests is served by the forward pass m.infer(q_{0:b}) of the models
+ * selected by the binary vector v, v != 0 (Section 5.1, Algorithm "Inference";
+ * Section 5.2 and Table 2), and the selected models' results are averaged
+ * (Section 1).  This library maps those steps to:
+ *
+ *   rafiki_ensemble_create   job creation + deployment: parameters copied to HBM
+ *   rafiki_ensemble_infer    one scheduled batch with one selection vector
+ *   rafiki_ensemble_model_logits   one model's raw logits (diagnostics, tests)
+ *   rafiki_ensemble_destroy  teardown
+ *
+ * Conventions
+ * - Every function returns an int status (RAFIKI_OK or a negative code) and never
+ *   throws; rafiki_last_error() returns a thread-local message for the last failure
+ *   on the calling thread.
+ * - Host pointers: everything inside rafiki_model_desc / rafiki_layer (read during
+ *   create only; the caller may free them on return).
+ * - Device pointers: `batch`, `out_probs`, `out_labels`, `out_logits` are caller-owned,
+ *   contiguous device buffers that must stay valid until `stream` has passed the
+ *   enqueued work and must not alias each other.
+ * - infer / model_logits only enqueue work on `stream` (a hipStream_t; 0 = the null
+ *   stream) and return; kernel faults surface at the next synchronisation.
+ * - A handle owns its device weights and a workspace sized for opts.max_batch; it is
+ *   NOT safe for concurrent infer calls from several threads or streams.
+ * - Inputs are not checked on the device: token ids must lie in [0, vocab) and image
+ *   values must be finite.
+ * - Results are deterministic: the same inputs, mask and n give bitwise-identical
+ *   outputs (no unordered atomics in any reduction).
+ */
+#ifndef RAFIKI_ENSEMBLE_H
+#define RAFIKI_ENSEMBLE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes. */
+enum {
+  RAFIKI_OK = 0,
+  RAFIKI_ERR_INVALID = -1,      /* bad argument: null pointer, mask, n, malformed model */
+  RAFIKI_ERR_UNSUPPORTED = -2,  /* valid but not implemented (e.g. a layer shape) */
+  RAFIKI_ERR_NOMEM = -3,        /* device or host allocation failed */
+  RAFIKI_ERR_HIP = -4           /* a HIP runtime call failed (e.g. no device) */
+};
+
+/* Compute precision of a handle.
+ * RAFIKI_FP32: fp32 weights, activations and accumulation.
+ * RAFIKI_BF16: weights rounded once (nearest, ties to even) to bfloat16, activations
+ *   stored as bfloat16 between layers, fp32 accumulation, fp32 batch-norm fold and
+ *   epilogue, fp32 logits, softmax and combine. */
+enum { RAFIKI_FP32 = 0, RAFIKI_BF16 = 1 };
+
+/* Request kinds. */
+enum {
+  RAFIKI_INPUT_IMAGE_NCHW_F32 = 0, /* batch = float [n, c, h, w] */
+  RAFIKI_INPUT_TOKENS_I32 = 1      /* batch = int32 [n, h] token ids (h = sequence length) */
+};
+
+/* Layer operations.  A layer's output tensor id is its index in the model's layer
+ * list; id -1 is the model input.  Layers must be topologically ordered. */
+enum {
+  RAFIKI_OP_CONV2D = 1,         /* cross-correlation, zero padding, floor output size;
+                                   weight OIHW [c_out, c_in, kh, kw]; optional bias;
+                                   optional inference BN (gamma, beta, mean, var, eps);
+                                   optional residual tensor `input2` added before ReLU */
+  RAFIKI_OP_MAXPOOL2D = 2,      /* kh x kw window, stride, pad (padding never wins) */
+  RAFIKI_OP_GLOBAL_AVGPOOL = 3, /* mean over all spatial positions -> vector [c] */
+  RAFIKI_OP_FC = 4,             /* z = W x + b; weight [c_out, c_in]; a spatial input
+                                   [c, h, w] is flattened in (c, h, w) order */
+  RAFIKI_OP_EMBEDDING = 5,      /* table [c_in = vocab, c_out = dim]; input must be -1 */
+  RAFIKI_OP_CONV1D_MAXTIME = 6, /* valid conv1d over time, weight [c_out, c_in, kw],
+                                   bias, ReLU, then max over time -> vector [c_out] */
+  RAFIKI_OP_CONCAT = 7          /* vectors `input` then `input2`, joined along channels */
+};
+
+typedef struct rafiki_ensemble_s* rafiki_ensemble_t;
+
+typedef struct {
+  int op;
+  int input, input2;            /* tensor ids; input2 = residual (CONV2D) / second operand
+                                   (CONCAT), or -1 */
+  int c_in, c_out;
+  int kh, kw, stride, pad;
+  int relu;                     /* nonzero: apply ReLU last (after the residual add) */
+  const float* weight;          /* host fp32, canonical layout above; NULL for pools/concat */
+  const float* bias;            /* host fp32 [c_out] or NULL */
+  const float* bn_gamma;        /* host fp32 [c_out]; all four NULL = no batch-norm */
+  const float* bn_beta;
+  const float* bn_mean;
+  const float* bn_var;
+  float bn_eps;
+} rafiki_layer;
+
+typedef struct {
+  int n_layers;
+  const rafiki_layer* layers;   /* the last layer produces the logits [n_classes] */
+  int n_classes;
+} rafiki_model_desc;
+
+typedef struct {
+  int input_kind;               /* RAFIKI_INPUT_* */
+  int c, h, w;                  /* image shape; for tokens h = sequence length, c = w = 1 */
+  int vocab;                    /* token vocabulary size (tokens only) */
+  int precision;                /* RAFIKI_FP32 or RAFIKI_BF16 */
+  int max_batch;                /* largest n accepted by infer; the workspace is sized for it */
+} rafiki_ensemble_opts;
+
+/* Create an ensemble of `n_models` (1..32) models sharing the input shape and
+ * n_classes.  Validates the layer lists, folds batch-norm into a per-channel fp32
+ * scale and shift (computed in fp64), rounds weights to the compute precision,
+ * packs them for the kernels, uploads them synchronously to the current device and
+ * sizes the workspace for opts->max_batch.
+ * Errors: RAFIKI_ERR_INVALID (null pointers, n_models out of range, mismatched
+ * shapes or classes, malformed layers), RAFIKI_ERR_UNSUPPORTED, RAFIKI_ERR_NOMEM,
+ * RAFIKI_ERR_HIP.  On error *out is set to NULL. */
+int rafiki_ensemble_create(const rafiki_model_desc* models, int n_models,
+                           const rafiki_ensemble_opts* opts, rafiki_ensemble_t* out);
+
+/* Serve one batch: for every model m whose bit m is set in model_subset_mask (bit m =
+ * model m in creation order), run its forward pass over the n requests in `batch`;
+ * then out_probs[i, :] = mean over the selected models of softmax(logits_m[i, :]) and
+ * out_labels[i] = lowest class index attaining the maximum of out_probs[i, :].
+ * `batch` follows opts.input_kind; out_probs is fp32 [n, n_classes] row-major;
+ * out_labels is int32 [n].  Requires 1 <= n <= max_batch, mask != 0 and no bit at
+ * position >= n_models (else RAFIKI_ERR_INVALID).  Enqueue-only on `stream`. */
+int rafiki_ensemble_infer(rafiki_ensemble_t h, const void* batch, int n, uint32_t model_subset_mask,
+                          float* out_probs, int32_t* out_labels, void* stream);
+
+/* Run model `model` alone and write its fp32 logits [n, n_classes] to out_logits.
+ * Same argument rules as infer.  Enqueue-only on `stream`. */
+int rafiki_ensemble_model_logits(rafiki_ensemble_t h, int model, const void* batch, int n,
+                                 float* out_logits, void* stream);
+
+/* Number of models and classes of a handle (host-side query). */
+int rafiki_ensemble_info(rafiki_ensemble_t h, int* n_models, int* n_classes, int* max_batch);
+
+/* Synchronise the device, free everything the handle owns.  NULL is accepted. */
+int rafiki_ensemble_destroy(rafiki_ensemble_t h);
+
+/* Message of the last failure on this thread ("" if none). */
+const char* rafiki_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RAFIKI_ENSEMBLE_H */

@@ -1,0 +1,183 @@
+"""ctypes binding of the C ABI in ``include/rafiki_ensemble.h``.
+
+Argument marshalling only: layer lists become ``rafiki_layer`` arrays, torch CUDA
+tensors become device pointers, and the current torch stream becomes the
+``hipStream_t``.  Every step of the computation runs in the HIP library; if the
+library is missing the binding raises instead of falling back to anything else.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from typing import List, Optional, Sequence
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "librafiki_ensemble.so")
+
+RAFIKI_OK, RAFIKI_ERR_INVALID, RAFIKI_ERR_UNSUPPORTED, RAFIKI_ERR_NOMEM, RAFIKI_ERR_HIP = 0, -1, -2, -3, -4
+RAFIKI_FP32, RAFIKI_BF16 = 0, 1
+RAFIKI_INPUT_IMAGE_NCHW_F32, RAFIKI_INPUT_TOKENS_I32 = 0, 1
+EXPORTED = ("rafiki_ensemble_create", "rafiki_ensemble_infer", "rafiki_ensemble_model_logits",
+            "rafiki_ensemble_info", "rafiki_ensemble_destroy", "rafiki_last_error")
+
+_fp = C.POINTER(C.c_float)
+
+
+class RafikiLayer(C.Structure):
+    _fields_ = [("op", C.c_int), ("input", C.c_int), ("input2", C.c_int), ("c_in", C.c_int), ("c_out", C.c_int),
+                ("kh", C.c_int), ("kw", C.c_int), ("stride", C.c_int), ("pad", C.c_int), ("relu", C.c_int),
+                ("weight", _fp), ("bias", _fp), ("bn_gamma", _fp), ("bn_beta", _fp), ("bn_mean", _fp),
+                ("bn_var", _fp), ("bn_eps", C.c_float)]
+
+
+class RafikiModelDesc(C.Structure):
+    _fields_ = [("n_layers", C.c_int), ("layers", C.POINTER(RafikiLayer)), ("n_classes", C.c_int)]
+
+
+class RafikiOpts(C.Structure):
+    _fields_ = [("input_kind", C.c_int), ("c", C.c_int), ("h", C.c_int), ("w", C.c_int), ("vocab", C.c_int),
+                ("precision", C.c_int), ("max_batch", C.c_int)]
+
+
+class RafikiError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"rafiki error {code}: {msg}")
+        self.code = code
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH):
+    """Load the HIP library (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"HIP library not built: {path} (run paper_1804_06087_amd.build)")
+    lib = C.CDLL(path)
+    lib.rafiki_ensemble_create.argtypes = [C.POINTER(RafikiModelDesc), C.c_int, C.POINTER(RafikiOpts),
+                                           C.POINTER(C.c_void_p)]
+    lib.rafiki_ensemble_infer.argtypes = [C.c_void_p, C.c_void_p, C.c_int, C.c_uint32, C.c_void_p, C.c_void_p,
+                                          C.c_void_p]
+    lib.rafiki_ensemble_model_logits.argtypes = [C.c_void_p, C.c_int, C.c_void_p, C.c_int, C.c_void_p, C.c_void_p]
+    lib.rafiki_ensemble_info.argtypes = [C.c_void_p, C.POINTER(C.c_int), C.POINTER(C.c_int), C.POINTER(C.c_int)]
+    lib.rafiki_ensemble_destroy.argtypes = [C.c_void_p]
+    lib.rafiki_last_error.restype = C.c_char_p
+    for name in ("rafiki_ensemble_create", "rafiki_ensemble_infer", "rafiki_ensemble_model_logits",
+                 "rafiki_ensemble_info", "rafiki_ensemble_destroy"):
+        getattr(lib, name).restype = C.c_int
+    _lib = lib
+    return lib
+
+
+def last_error() -> str:
+    return load_library().rafiki_last_error().decode()
+
+
+def _check(rc: int):
+    if rc != RAFIKI_OK:
+        raise RafikiError(rc, last_error())
+
+
+def _fptr(a: Optional[np.ndarray], keep: list):
+    if a is None:
+        return None
+    a = np.ascontiguousarray(a, dtype=np.float32)
+    keep.append(a)
+    return a.ctypes.data_as(_fp)
+
+
+def _ptr(t) -> int:
+    """Device pointer of a torch tensor (or a raw integer address)."""
+    if t is None:
+        return 0
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _stream(stream) -> int:
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def make_layers(spec, params, keep: list):
+    """rafiki_layer array for a layer list (plain attribute access on each layer)."""
+    arr = (RafikiLayer * len(spec.layers))()
+    for i, (L, P) in enumerate(zip(spec.layers, params.layers)):
+        r = arr[i]
+        r.op, r.input, r.input2 = L.op, L.input, L.input2
+        r.c_in, r.c_out, r.kh, r.kw, r.stride, r.pad = L.c_in, L.c_out, L.kh, L.kw, L.stride, L.pad
+        r.relu = 1 if L.relu else 0
+        r.weight = _fptr(P.weight, keep)
+        r.bias = _fptr(P.bias if L.bias else None, keep)
+        if L.bn:
+            r.bn_gamma, r.bn_beta = _fptr(P.bn_gamma, keep), _fptr(P.bn_beta, keep)
+            r.bn_mean, r.bn_var = _fptr(P.bn_mean, keep), _fptr(P.bn_var, keep)
+            r.bn_eps = float(P.bn_eps)
+    keep.append(arr)
+    return arr
+
+
+class Ensemble:
+    """Handle over ``rafiki_ensemble_create`` .. ``rafiki_ensemble_destroy``."""
+
+    def __init__(self, specs: Sequence, params: Sequence, precision: str = "bf16", max_batch: int = 64):
+        lib = load_library()
+        keep: list = []
+        descs = (RafikiModelDesc * len(specs))()
+        for i, (s, p) in enumerate(zip(specs, params)):
+            arr = make_layers(s, p, keep)
+            descs[i].n_layers = len(s.layers)
+            descs[i].layers = C.cast(arr, C.POINTER(RafikiLayer))
+            descs[i].n_classes = s.n_classes
+        s0 = specs[0]
+        opts = RafikiOpts()
+        if len(s0.input_shape) == 3:
+            opts.input_kind = RAFIKI_INPUT_IMAGE_NCHW_F32
+            opts.c, opts.h, opts.w = s0.input_shape
+        else:
+            opts.input_kind = RAFIKI_INPUT_TOKENS_I32
+            opts.c, opts.h, opts.w = 1, s0.input_shape[0], 1
+            opts.vocab = s0.vocab
+        opts.precision = RAFIKI_BF16 if precision == "bf16" else RAFIKI_FP32
+        opts.max_batch = max_batch
+        h = C.c_void_p()
+        _check(lib.rafiki_ensemble_create(descs, len(specs), C.byref(opts), C.byref(h)))
+        self._h = h
+        self._lib = lib
+        self.n_models = len(specs)
+        self.n_classes = s0.n_classes
+        self.max_batch = max_batch
+
+    def infer(self, batch, n: int, mask: int, out_probs, out_labels, stream=None):
+        _check(self._lib.rafiki_ensemble_infer(self._h, _ptr(batch), n, mask, _ptr(out_probs), _ptr(out_labels),
+                                               _stream(stream)))
+
+    def model_logits(self, model: int, batch, n: int, out_logits, stream=None):
+        _check(self._lib.rafiki_ensemble_model_logits(self._h, model, _ptr(batch), n, _ptr(out_logits),
+                                                      _stream(stream)))
+
+    def close(self):
+        if getattr(self, "_h", None) is not None and self._h.value:
+            _check(self._lib.rafiki_ensemble_destroy(self._h))
+        self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()

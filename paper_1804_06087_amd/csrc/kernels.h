@@ -1,0 +1,69 @@
+// Internal interface between the host runtime and the gfx950 kernels.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace rafiki {
+
+typedef uint16_t bf16_t;   // bfloat16 storage (upper half of an IEEE float)
+
+// Implicit-GEMM convolution (also FC = 1x1 conv on a 1x1 image).
+//   out[m, co] = epilogue( sum_k X[m, k] * Wp[co, k] )
+//   m = (n, ho, wo) output pixel, k = (u, v, ci) kernel tap and input channel,
+//   X[m, k] = x[n, ho*S - P + u, wo*S - P + v, ci] (zero outside the image).
+// Epilogue: y = acc * scale[co] + shift[co] (+ res[m, co]), then ReLU if requested.
+struct ConvArgs {
+  const void* x;        // NHWC activations [N][H][W][Cs] (bf16 or fp32)
+  const void* w;        // packed weights [Co_pad][Kp], K ordered (u, v, ci), zero padded
+  const float* scale;   // [Co_pad] folded batch-norm scale (0 on padded channels)
+  const float* shift;   // [Co_pad] folded shift incl. bias (0 on padded channels)
+  const void* res;      // residual [M][ldy] (same type as x) or nullptr
+  void* y;              // output [M][ldy], bf16/fp32 activations or fp32 logits
+  float* partial;       // split-K partial sums [splits][M][Co_pad]
+  int N, H, W, Cs;      // input geometry; Cs = storage channels (multiple of 8)
+  int Ho, Wo, kh, kw, stride, pad;
+  int M, K, Kp, Co_pad; // M = N*Ho*Wo; K = kh*kw*Cs; Kp = K rounded up to the K tile
+  int c_write;          // channels written per row (<= Co_pad)
+  int ldy;              // row stride of y and res, in elements
+  int relu;
+  int out_f32;          // y is fp32 (bf16 kernels); fp32 kernels always write fp32
+  int kt_per_split;     // K tiles per split (splits = gridDim.y)
+  int n_tiles;          // channel tiles per row of the output tile grid
+};
+
+// bf16 MFMA kernel family; bm, bn in {32, 64, 128}.  Returns hipSuccess or the
+// launch error.  splits > 1 writes partial sums; finish with splitk_reduce.
+hipError_t launch_conv_bf16(const ConvArgs& a, int bm, int bn, int splits, hipStream_t s);
+hipError_t launch_splitk_reduce(const ConvArgs& a, int splits, int in_bf16, hipStream_t s);
+// fp32 direct kernel (CUDA-core style FMA loops; used by the fp32 precision mode).
+hipError_t launch_conv_f32(const ConvArgs& a, hipStream_t s);
+
+// NCHW fp32 images -> NHWC with Cs >= C storage channels (zero filled), bf16 or fp32.
+hipError_t launch_stage_images(const float* x, void* y, int N, int C, int H, int W, int Cs, int to_bf16,
+                               hipStream_t s);
+// Max-pool k x k / stride / pad over NHWC (Cs channels).
+hipError_t launch_maxpool(const void* x, void* y, int N, int H, int W, int Cs, int Ho, int Wo, int k,
+                          int stride, int pad, int bf16, hipStream_t s);
+// Global average pool NHWC [N][HW][Cs] -> [N][Cs]; also max over time when is_max.
+hipError_t launch_spatial_reduce(const void* x, void* y, int N, int HW, int Cs, int is_max, int bf16,
+                                 hipStream_t s);
+// Embedding gather: tokens [N][L] -> y [N][L][Cs] rows of table [vocab][Cs].
+hipError_t launch_embed_gather(const int32_t* tok, const void* table, void* y, int N, int L, int Cs,
+                               int bf16, hipStream_t s);
+// Concatenate vectors: y[b, 0:c1] = a[b, 0:c1], y[b, c1:c1+c2] = b[b, 0:c2], zero after.
+hipError_t launch_concat(const void* a, int ca, int lda, const void* b, int cb, int ldb, void* y, int ldy,
+                         int N, int bf16, hipStream_t s);
+
+// Ensemble combine over S selected models' fp32 logits.
+struct CombineArgs {
+  const float* logits;  // base of [n_models][ld_model] slots; model m at logits + m * ld_model
+  long long ld_model;   // elements between consecutive model slots
+  int sel[32];          // selected model indices
+  int S;                // number of selected models (>= 1)
+  int n, C;
+  float* probs;         // [n][C]
+  int32_t* labels;      // [n]
+};
+hipError_t launch_combine(const CombineArgs& a, hipStream_t s);
+
+}  // namespace rafiki

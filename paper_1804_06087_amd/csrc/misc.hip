@@ -1,0 +1,313 @@
+// Memory-bound kernels of the hot path: input staging, pooling, spatial reductions,
+// embedding gather, concatenation, the fp32 direct convolution, and the ensemble
+// combine (softmax per model, mean over the selected models, first-index argmax).
+#include "kernels.h"
+
+namespace rafiki {
+
+__device__ __forceinline__ float bf2f(uint32_t b16) { return __uint_as_float(b16 << 16); }
+__device__ __forceinline__ uint32_t f2bf(float f) {   // nearest, ties to even (finite)
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+
+// 8 consecutive channels as floats, from bf16 or fp32 storage.
+__device__ __forceinline__ void load8(const void* p, long long off, int bf16, float v[8]) {
+  if (bf16) {
+    const uint4 q = *(const uint4*)((const bf16_t*)p + off);
+    v[0] = bf2f(q.x & 0xFFFFu); v[1] = bf2f(q.x >> 16);
+    v[2] = bf2f(q.y & 0xFFFFu); v[3] = bf2f(q.y >> 16);
+    v[4] = bf2f(q.z & 0xFFFFu); v[5] = bf2f(q.z >> 16);
+    v[6] = bf2f(q.w & 0xFFFFu); v[7] = bf2f(q.w >> 16);
+  } else {
+    const float4 a = *(const float4*)((const float*)p + off);
+    const float4 b = *(const float4*)((const float*)p + off + 4);
+    v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w; v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+  }
+}
+__device__ __forceinline__ void store8(void* p, long long off, int bf16, const float v[8]) {
+  if (bf16) {
+    uint4 q;
+    q.x = f2bf(v[0]) | (f2bf(v[1]) << 16);
+    q.y = f2bf(v[2]) | (f2bf(v[3]) << 16);
+    q.z = f2bf(v[4]) | (f2bf(v[5]) << 16);
+    q.w = f2bf(v[6]) | (f2bf(v[7]) << 16);
+    *(uint4*)((bf16_t*)p + off) = q;
+  } else {
+    *(float4*)((float*)p + off) = make_float4(v[0], v[1], v[2], v[3]);
+    *(float4*)((float*)p + off + 4) = make_float4(v[4], v[5], v[6], v[7]);
+  }
+}
+
+// ---------------------------------------------------------------- input staging
+// One thread per output pixel and 8-channel group: reads C planes (coalesced along
+// w across threads), writes one 16-byte (bf16) or 32-byte (fp32) NHWC chunk.
+__global__ void stage_images_kernel(const float* __restrict__ x, void* y, int N, int C, int H, int W, int Cs,
+                                    int to_bf16) {
+  const int groups = Cs / 8;
+  const long long HW = (long long)H * W;
+  const long long total = (long long)N * HW * groups;
+  const long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= total) return;
+  const int g = (int)(idx / (N * HW));            // group-major: neighbouring threads share g
+  const long long pix = idx - (long long)g * N * HW;
+  const long long n = pix / HW, hw = pix - n * HW;
+  float v[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const int c = g * 8 + j;
+    v[j] = c < C ? x[(n * C + c) * HW + hw] : 0.f;
+  }
+  store8(y, pix * Cs + g * 8, to_bf16, v);
+}
+
+hipError_t launch_stage_images(const float* x, void* y, int N, int C, int H, int W, int Cs, int to_bf16,
+                               hipStream_t s) {
+  const long long total = (long long)N * H * W * (Cs / 8);
+  hipLaunchKernelGGL(stage_images_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, x, y, N, C, H,
+                     W, Cs, to_bf16);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- max-pool
+__global__ void maxpool_kernel(const void* __restrict__ x, void* y, int N, int H, int W, int Cs, int Ho, int Wo,
+                               int k, int stride, int pad, int bf16) {
+  const int groups = Cs / 8;
+  const long long total = (long long)N * Ho * Wo * groups;
+  const long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= total) return;
+  const int g = (int)(idx % groups);
+  const long long pix = idx / groups;
+  const int wo = (int)(pix % Wo);
+  const long long t = pix / Wo;
+  const int ho = (int)(t % Ho);
+  const long long n = t / Ho;
+  float m[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) m[j] = -INFINITY;
+  for (int u = 0; u < k; ++u) {
+    const int hi = ho * stride - pad + u;
+    if (hi < 0 || hi >= H) continue;
+    for (int v = 0; v < k; ++v) {
+      const int wi = wo * stride - pad + v;
+      if (wi < 0 || wi >= W) continue;
+      float q[8];
+      load8(x, ((n * H + hi) * W + wi) * Cs + g * 8, bf16, q);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) m[j] = fmaxf(m[j], q[j]);
+    }
+  }
+  store8(y, pix * Cs + g * 8, bf16, m);
+}
+
+hipError_t launch_maxpool(const void* x, void* y, int N, int H, int W, int Cs, int Ho, int Wo, int k, int stride,
+                          int pad, int bf16, hipStream_t s) {
+  const long long total = (long long)N * Ho * Wo * (Cs / 8);
+  hipLaunchKernelGGL(maxpool_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, x, y, N, H, W, Cs, Ho,
+                     Wo, k, stride, pad, bf16);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- GAP / max over time
+// One thread per (image, 8-channel group); positions summed in order in fp32.
+__global__ void spatial_reduce_kernel(const void* __restrict__ x, void* y, int N, int HW, int Cs, int is_max,
+                                      int bf16) {
+  const int groups = Cs / 8;
+  const long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (long long)N * groups) return;
+  const int g = (int)(idx % groups);
+  const long long n = idx / groups;
+  float acc[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) acc[j] = is_max ? -INFINITY : 0.f;
+  for (int p = 0; p < HW; ++p) {
+    float q[8];
+    load8(x, (n * HW + p) * Cs + g * 8, bf16, q);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[j] = is_max ? fmaxf(acc[j], q[j]) : acc[j] + q[j];
+  }
+  if (!is_max) {
+    const float inv = 1.0f / (float)HW;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[j] = acc[j] * inv;
+  }
+  store8(y, n * Cs + g * 8, bf16, acc);
+}
+
+hipError_t launch_spatial_reduce(const void* x, void* y, int N, int HW, int Cs, int is_max, int bf16,
+                                 hipStream_t s) {
+  const long long total = (long long)N * (Cs / 8);
+  hipLaunchKernelGGL(spatial_reduce_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, x, y, N, HW,
+                     Cs, is_max, bf16);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- embedding gather
+__global__ void embed_gather_kernel(const int32_t* __restrict__ tok, const void* __restrict__ table, void* y,
+                                    int N, int L, int Cs, int bf16) {
+  const int groups = Cs / 8;
+  const long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (long long)N * L * groups) return;
+  const int g = (int)(idx % groups);
+  const long long pos = idx / groups;
+  const long long row = tok[pos];
+  if (bf16) {
+    *((uint4*)((bf16_t*)y + pos * Cs) + g) = *((const uint4*)((const bf16_t*)table + row * Cs) + g);
+  } else {
+    const float4* src = (const float4*)((const float*)table + row * Cs + g * 8);
+    float4* dst = (float4*)((float*)y + pos * Cs + g * 8);
+    dst[0] = src[0];
+    dst[1] = src[1];
+  }
+}
+
+hipError_t launch_embed_gather(const int32_t* tok, const void* table, void* y, int N, int L, int Cs, int bf16,
+                               hipStream_t s) {
+  const long long total = (long long)N * L * (Cs / 8);
+  hipLaunchKernelGGL(embed_gather_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, tok, table, y, N,
+                     L, Cs, bf16);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- concat
+__global__ void concat_kernel(const void* a, int ca, int lda, const void* b, int cb, int ldb, void* y, int ldy,
+                              int N, int bf16) {
+  const long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (long long)N * ldy) return;
+  const long long n = idx / ldy;
+  const int c = (int)(idx - n * ldy);
+  if (bf16) {
+    bf16_t v = 0;
+    if (c < ca) v = ((const bf16_t*)a)[n * lda + c];
+    else if (c < ca + cb) v = ((const bf16_t*)b)[n * ldb + (c - ca)];
+    ((bf16_t*)y)[idx] = v;
+  } else {
+    float v = 0.f;
+    if (c < ca) v = ((const float*)a)[n * lda + c];
+    else if (c < ca + cb) v = ((const float*)b)[n * ldb + (c - ca)];
+    ((float*)y)[idx] = v;
+  }
+}
+
+hipError_t launch_concat(const void* a, int ca, int lda, const void* b, int cb, int ldb, void* y, int ldy, int N,
+                         int bf16, hipStream_t s) {
+  const long long total = (long long)N * ldy;
+  hipLaunchKernelGGL(concat_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, a, ca, lda, b, cb, ldb,
+                     y, ldy, N, bf16);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- fp32 direct conv
+// One thread per (pixel, output channel); taps outer, channels inner (fp32 FMA).
+__global__ void conv_f32_kernel(ConvArgs a) {
+  const long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (long long)a.M * a.c_write) return;
+  const int m = (int)(idx / a.c_write);
+  const int co = (int)(idx - (long long)m * a.c_write);
+  const int HoWo = a.Ho * a.Wo;
+  const int n = m / HoWo, r = m - n * HoWo;
+  const int ho = r / a.Wo, wo = r - ho * a.Wo;
+  const float* X = (const float*)a.x;
+  const float* Wt = (const float*)a.w + (long long)co * a.Kp;
+  float s = 0.f;
+  for (int u = 0; u < a.kh; ++u) {
+    const int hi = ho * a.stride - a.pad + u;
+    if (hi < 0 || hi >= a.H) continue;
+    for (int v = 0; v < a.kw; ++v) {
+      const int wi = wo * a.stride - a.pad + v;
+      if (wi < 0 || wi >= a.W) continue;
+      const float* xp = X + (((long long)n * a.H + hi) * a.W + wi) * a.Cs;
+      const float* wp = Wt + (u * a.kw + v) * a.Cs;
+      for (int ci = 0; ci < a.Cs; ++ci) s = fmaf(xp[ci], wp[ci], s);
+    }
+  }
+  float y = s * a.scale[co] + a.shift[co];
+  const long long o = (long long)m * a.ldy + co;
+  if (a.res) y += ((const float*)a.res)[o];
+  if (a.relu) y = fmaxf(y, 0.f);
+  ((float*)a.y)[o] = y;
+}
+
+hipError_t launch_conv_f32(const ConvArgs& a, hipStream_t s) {
+  const long long total = (long long)a.M * a.c_write;
+  hipLaunchKernelGGL(conv_f32_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- ensemble combine
+// One wavefront per request row.  For each selected model: row max and sum of
+// exp(z - max) by butterfly reductions (fixed order, deterministic), p = e / sum
+// accumulated into the lane's registers; then the mean over models and the argmax
+// (largest value, lowest index on ties) by a second butterfly.
+constexpr int kCombineMaxPerLane = 16;   // C <= 64 * 16 = 1024 classes
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+__global__ __launch_bounds__(256) void combine_kernel(CombineArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= a.n) return;
+  const int per = (a.C + 63) / 64;
+  float acc[kCombineMaxPerLane];
+#pragma unroll
+  for (int i = 0; i < kCombineMaxPerLane; ++i) acc[i] = 0.f;
+  for (int s = 0; s < a.S; ++s) {
+    const float* z = a.logits + a.sel[s] * a.ld_model + (long long)row * a.C;
+    float v[kCombineMaxPerLane];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < kCombineMaxPerLane; ++i) {
+      const int c = i * 64 + lane;
+      v[i] = (i < per && c < a.C) ? z[c] : -INFINITY;
+      mx = fmaxf(mx, v[i]);
+    }
+    mx = wave_max(mx);
+    float sum = 0.f;
+#pragma unroll
+    for (int i = 0; i < kCombineMaxPerLane; ++i) {
+      v[i] = (i < per && i * 64 + lane < a.C) ? expf(v[i] - mx) : 0.f;
+      sum += v[i];
+    }
+    sum = wave_sum(sum);
+    const float inv = 1.0f / sum;
+#pragma unroll
+    for (int i = 0; i < kCombineMaxPerLane; ++i) acc[i] += v[i] * inv;
+  }
+  const float invS = 1.0f / (float)a.S;
+  float best = -INFINITY;
+  int bidx = 0x7fffffff;
+#pragma unroll
+  for (int i = 0; i < kCombineMaxPerLane; ++i) {
+    const int c = i * 64 + lane;
+    if (i < per && c < a.C) {
+      const float p = acc[i] * invS;
+      a.probs[(long long)row * a.C + c] = p;
+      if (p > best) { best = p; bidx = c; }     // c increases with i: keeps the first max
+    }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float ob = __shfl_xor(best, o, 64);
+    const int oi = __shfl_xor(bidx, o, 64);
+    if (ob > best || (ob == best && oi < bidx)) { best = ob; bidx = oi; }
+  }
+  if (lane == 0) a.labels[row] = bidx;
+}
+
+hipError_t launch_combine(const CombineArgs& a, hipStream_t s) {
+  if (a.C > 64 * kCombineMaxPerLane || a.S < 1) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(combine_kernel, dim3((a.n + 3) / 4), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace rafiki

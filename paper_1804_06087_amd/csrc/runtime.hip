@@ -1,0 +1,647 @@
+// Host runtime and C ABI of the ensemble-inference library.
+//
+// create: validate the layer lists, infer tensor shapes, fold batch-norm into a
+//   per-channel fp32 (scale, shift) computed in fp64, round weights to the compute
+//   precision, pack them in the kernels' [Co_pad][Kp] (u, v, ci) order, upload, and
+//   plan each model's activation workspace by liveness for max_batch requests.
+// infer: stage the request batch once (NCHW fp32 -> NHWC), run the forward pass of
+//   every selected model on the caller's stream into its logits slot, then combine.
+#include "rafiki_ensemble.h"
+#include "kernels.h"
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <memory>
+#include <string>
+#include <vector>
+
+using namespace rafiki;
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const std::string& msg) {
+  g_err = msg;
+  return code;
+}
+
+inline int round_up(int x, int m) { return (x + m - 1) / m * m; }
+inline size_t round_up_sz(size_t x, size_t m) { return (x + m - 1) / m * m; }
+
+// Host float -> bf16 bits, nearest with ties to even (finite values).
+inline uint16_t host_f2bf(float f) {
+  uint32_t u;
+  std::memcpy(&u, &f, 4);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+enum TKind { T_IMG = 0, T_VEC = 1, T_SEQ = 2, T_TOK = 3 };
+
+struct Tensor {
+  int kind = T_IMG;
+  int c = 0, h = 1, w = 1, Cs = 0;   // logical channels, spatial size, storage channels
+  size_t off = 0;                    // byte offset in the model arena
+  int last_use = -1;
+  bool is_logits = false;
+  size_t item_elems() const { return (size_t)h * w * Cs; }
+};
+
+enum OpKind { O_CONV = 0, O_MAXPOOL, O_GAP, O_EMBED, O_CONV1D, O_CONCAT };
+
+struct Op {
+  int kind = O_CONV;
+  int in = -1, in2 = -1, out = -1;
+  // GEMM-like ops (conv2d, FC, conv1d)
+  int H = 1, W = 1, Cs_in = 0, Ho = 1, Wo = 1, kh = 1, kw = 1, stride = 1, pad = 0, relu = 0;
+  int K = 0, Kp = 0, Co_pad = 0, c_out = 0, bn = 128;
+  void* d_w = nullptr;
+  float* d_scale = nullptr;
+  float* d_shift = nullptr;
+  // pooling
+  int k = 1;
+  // conv1d: pre-max scratch [n][T][Cs_out] in the arena
+  size_t tmp_off = 0;
+  // concat
+  int ca = 0, cb = 0;
+};
+
+struct Model {
+  std::vector<Op> ops;
+  std::vector<Tensor> tensors;
+  char* d_arena = nullptr;
+  size_t arena_bytes = 0;
+};
+
+struct FreeList {
+  struct B { size_t off, size; };
+  std::vector<B> free;
+  size_t top = 0;
+  size_t alloc(size_t n) {
+    n = round_up_sz(std::max<size_t>(n, 1), 256);
+    for (size_t i = 0; i < free.size(); ++i) {
+      if (free[i].size >= n) {
+        size_t off = free[i].off;
+        free[i].off += n;
+        free[i].size -= n;
+        if (free[i].size == 0) free.erase(free.begin() + i);
+        return off;
+      }
+    }
+    size_t off = top;
+    top += n;
+    return off;
+  }
+  void release(size_t off, size_t n) {
+    n = round_up_sz(std::max<size_t>(n, 1), 256);
+    free.push_back({off, n});
+    std::sort(free.begin(), free.end(), [](const B& a, const B& b) { return a.off < b.off; });
+    std::vector<B> merged;
+    for (auto& b : free) {
+      if (!merged.empty() && merged.back().off + merged.back().size == b.off) merged.back().size += b.size;
+      else merged.push_back(b);
+    }
+    free.swap(merged);
+  }
+};
+
+}  // namespace
+
+struct rafiki_ensemble_s {
+  int n_models = 0, n_classes = 0, precision = 0, max_batch = 0;
+  int input_kind = 0, C = 0, H = 0, W = 0, vocab = 0, in_Cs = 0;
+  int device = 0;
+  bool dry = false;   // validation pass: shapes only, no packing, no device calls
+  std::vector<Model> models;
+  void* d_staged = nullptr;
+  float* d_logits = nullptr;
+  float* d_partial = nullptr;
+  size_t partial_bytes = 0;
+  std::vector<void*> allocs;
+  size_t esz() const { return precision == RAFIKI_BF16 ? 2 : 4; }
+  ~rafiki_ensemble_s() {
+    for (void* p : allocs) (void)hipFree(p);
+  }
+};
+
+namespace {
+
+int dev_alloc(rafiki_ensemble_s* e, void** p, size_t bytes) {
+  *p = nullptr;
+  if (e->dry) return RAFIKI_OK;
+  if (bytes == 0) bytes = 256;
+  hipError_t st = hipMalloc(p, bytes);
+  if (st != hipSuccess) {
+    *p = nullptr;
+    (void)hipGetLastError();
+    return fail(st == hipErrorOutOfMemory ? RAFIKI_ERR_NOMEM : RAFIKI_ERR_HIP,
+                std::string("hipMalloc of ") + std::to_string(bytes) + " bytes failed: " + hipGetErrorString(st));
+  }
+  e->allocs.push_back(*p);
+  return RAFIKI_OK;
+}
+
+int upload(rafiki_ensemble_s* e, void** dst, const void* src, size_t bytes) {
+  int rc = dev_alloc(e, dst, bytes);
+  if (rc || e->dry) return rc;
+  hipError_t st = hipMemcpy(*dst, src, bytes, hipMemcpyHostToDevice);
+  if (st != hipSuccess) return fail(RAFIKI_ERR_HIP, std::string("hipMemcpy failed: ") + hipGetErrorString(st));
+  return RAFIKI_OK;
+}
+
+// Tile choices of the bf16 MFMA kernel.
+int choose_bn(int c_out) { return c_out <= 32 ? 32 : (c_out <= 64 ? 64 : 128); }
+int choose_bm(int M) { return M <= 32 ? 32 : (M <= 64 ? 64 : 128); }
+// Split K when the output tile grid alone cannot fill the 256 compute units.
+int choose_splits(int M, int bm, int n_tiles, int ktiles) {
+  const int tiles = ((M + bm - 1) / bm) * n_tiles;
+  if (tiles >= 256) return 1;
+  int s = std::min((512 + tiles - 1) / tiles, ktiles / 4);
+  s = std::max(1, std::min(s, 64));
+  const int per = (ktiles + s - 1) / s;
+  return (ktiles + per - 1) / per;
+}
+
+// Pack a GEMM-like weight into [Co_pad][Kp] with K index (u, v, ci) over Cs_in
+// storage channels.  `src_index(co, ci, u, v)` gives the canonical flat index.
+template <class F>
+std::vector<float> pack_weight(int c_out, int c_in, int kh, int kw, int Cs_in, int Co_pad, int Kp, F src_index,
+                               const float* w) {
+  std::vector<float> out((size_t)Co_pad * Kp, 0.f);
+  for (int co = 0; co < c_out; ++co)
+    for (int u = 0; u < kh; ++u)
+      for (int v = 0; v < kw; ++v)
+        for (int ci = 0; ci < c_in; ++ci)
+          out[(size_t)co * Kp + (size_t)(u * kw + v) * Cs_in + ci] = w[src_index(co, ci, u, v)];
+  return out;
+}
+
+int upload_weights(rafiki_ensemble_s* e, Op& op, const std::vector<float>& packed) {
+  if (e->precision == RAFIKI_BF16) {
+    std::vector<uint16_t> b(packed.size());
+    for (size_t i = 0; i < packed.size(); ++i) b[i] = host_f2bf(packed[i]);
+    return upload(e, &op.d_w, b.data(), b.size() * 2);
+  }
+  return upload(e, &op.d_w, packed.data(), packed.size() * 4);
+}
+
+// Fold inference batch-norm and bias: y = s * conv + t, s = gamma / sqrt(var + eps),
+// t = beta - mean * s + s * bias, evaluated in fp64 and rounded once to fp32.
+int upload_fold(rafiki_ensemble_s* e, Op& op, const rafiki_layer& L) {
+  std::vector<float> s(op.Co_pad, 0.f), t(op.Co_pad, 0.f);
+  const bool bn = L.bn_gamma != nullptr;
+  for (int c = 0; c < L.c_out; ++c) {
+    const double b = L.bias ? (double)L.bias[c] : 0.0;
+    if (bn) {
+      const double sc = (double)L.bn_gamma[c] / std::sqrt((double)L.bn_var[c] + (double)L.bn_eps);
+      s[c] = (float)sc;
+      t[c] = (float)((double)L.bn_beta[c] - (double)L.bn_mean[c] * sc + sc * b);
+    } else {
+      s[c] = 1.f;
+      t[c] = (float)b;
+    }
+  }
+  int rc = upload(e, (void**)&op.d_scale, s.data(), s.size() * 4);
+  if (rc) return rc;
+  return upload(e, (void**)&op.d_shift, t.data(), t.size() * 4);
+}
+
+std::string lname(int m, int i) { return "model " + std::to_string(m) + " layer " + std::to_string(i) + ": "; }
+
+// Validate one model, infer shapes, build its ops and upload its parameters.
+int build_model(rafiki_ensemble_s* e, int mi, const rafiki_model_desc& md, Model& M) {
+  if (md.n_layers < 1 || !md.layers) return fail(RAFIKI_ERR_INVALID, "model " + std::to_string(mi) + ": no layers");
+  if (md.n_classes < 1) return fail(RAFIKI_ERR_INVALID, "model " + std::to_string(mi) + ": n_classes < 1");
+  Tensor in;
+  if (e->input_kind == RAFIKI_INPUT_IMAGE_NCHW_F32) {
+    in.kind = T_IMG; in.c = e->C; in.h = e->H; in.w = e->W; in.Cs = e->in_Cs;
+  } else {
+    in.kind = T_TOK; in.c = 1; in.h = 1; in.w = e->H; in.Cs = 1;
+  }
+  const bool bf = e->precision == RAFIKI_BF16;
+  auto tin = [&](int id) -> const Tensor& { return id < 0 ? in : M.tensors[id]; };
+  M.tensors.resize(md.n_layers);
+  for (int i = 0; i < md.n_layers; ++i) {
+    const rafiki_layer& L = md.layers[i];
+    const std::string ln = lname(mi, i);
+    if (L.input < -1 || L.input >= i) return fail(RAFIKI_ERR_INVALID, ln + "input id out of range");
+    if (L.input2 < -1 || L.input2 >= i) return fail(RAFIKI_ERR_INVALID, ln + "input2 id out of range");
+    const Tensor& x = tin(L.input);
+    Tensor& y = M.tensors[i];
+    Op op;
+    op.in = L.input; op.in2 = L.input2; op.out = i; op.relu = L.relu ? 1 : 0;
+    const bool has_bn = L.bn_gamma || L.bn_beta || L.bn_mean || L.bn_var;
+    if (has_bn && !(L.bn_gamma && L.bn_beta && L.bn_mean && L.bn_var))
+      return fail(RAFIKI_ERR_INVALID, ln + "batch-norm needs all of gamma, beta, mean, var");
+    if (has_bn && !(L.bn_eps >= 0.f)) return fail(RAFIKI_ERR_INVALID, ln + "bn_eps must be >= 0");
+    switch (L.op) {
+      case RAFIKI_OP_CONV2D: {
+        if (x.kind != T_IMG) return fail(RAFIKI_ERR_INVALID, ln + "conv2d needs an image tensor");
+        if (L.c_in != x.c || L.c_out < 1) return fail(RAFIKI_ERR_INVALID, ln + "conv2d channel mismatch");
+        if (L.kh < 1 || L.kw < 1 || L.stride < 1 || L.pad < 0 || !L.weight)
+          return fail(RAFIKI_ERR_INVALID, ln + "conv2d geometry or weight invalid");
+        const int Ho = (x.h + 2 * L.pad - L.kh) / L.stride + 1, Wo = (x.w + 2 * L.pad - L.kw) / L.stride + 1;
+        if (x.h + 2 * L.pad < L.kh || x.w + 2 * L.pad < L.kw || Ho < 1 || Wo < 1)
+          return fail(RAFIKI_ERR_INVALID, ln + "conv2d output would be empty");
+        y.kind = T_IMG; y.c = L.c_out; y.h = Ho; y.w = Wo; y.Cs = round_up(L.c_out, 8);
+        if (L.input2 >= 0) {
+          const Tensor& r = M.tensors[L.input2];
+          if (r.kind != T_IMG || r.c != y.c || r.h != y.h || r.w != y.w)
+            return fail(RAFIKI_ERR_INVALID, ln + "residual shape differs from the conv output");
+        }
+        op.kind = O_CONV;
+        op.H = x.h; op.W = x.w; op.Cs_in = x.Cs; op.Ho = Ho; op.Wo = Wo;
+        op.kh = L.kh; op.kw = L.kw; op.stride = L.stride; op.pad = L.pad; op.c_out = L.c_out;
+        const int c_in = L.c_in, kh = L.kh, kw = L.kw;
+        op.K = kh * kw * x.Cs;
+        op.bn = bf ? choose_bn(L.c_out) : 32;
+        op.Co_pad = round_up(L.c_out, op.bn);
+        op.Kp = bf ? round_up(op.K, 64) : op.K;
+        if (e->dry) break;
+        auto packed = pack_weight(L.c_out, c_in, kh, kw, x.Cs, op.Co_pad, op.Kp,
+                                  [=](int co, int ci, int u, int v) {
+                                    return (((size_t)co * c_in + ci) * kh + u) * kw + v;
+                                  }, L.weight);
+        int rc = upload_weights(e, op, packed);
+        if (!rc) rc = upload_fold(e, op, L);
+        if (rc) return rc;
+        break;
+      }
+      case RAFIKI_OP_MAXPOOL2D: {
+        if (x.kind != T_IMG) return fail(RAFIKI_ERR_INVALID, ln + "maxpool needs an image tensor");
+        if (L.kh < 1 || L.kh != L.kw || L.stride < 1 || L.pad < 0 || L.pad >= L.kh)
+          return fail(RAFIKI_ERR_INVALID, ln + "maxpool geometry invalid (square window, pad < k)");
+        const int Ho = (x.h + 2 * L.pad - L.kh) / L.stride + 1, Wo = (x.w + 2 * L.pad - L.kw) / L.stride + 1;
+        if (x.h + 2 * L.pad < L.kh || x.w + 2 * L.pad < L.kw || Ho < 1 || Wo < 1)
+          return fail(RAFIKI_ERR_INVALID, ln + "maxpool output would be empty");
+        y = x; y.h = Ho; y.w = Wo; y.off = 0; y.last_use = -1;
+        op.kind = O_MAXPOOL; op.H = x.h; op.W = x.w; op.Cs_in = x.Cs; op.Ho = Ho; op.Wo = Wo;
+        op.k = L.kh; op.stride = L.stride; op.pad = L.pad;
+        break;
+      }
+      case RAFIKI_OP_GLOBAL_AVGPOOL: {
+        if (x.kind != T_IMG) return fail(RAFIKI_ERR_INVALID, ln + "global average pool needs an image tensor");
+        y.kind = T_VEC; y.c = x.c; y.h = 1; y.w = 1; y.Cs = x.Cs;
+        op.kind = O_GAP; op.H = x.h; op.W = x.w; op.Cs_in = x.Cs;
+        break;
+      }
+      case RAFIKI_OP_FC: {
+        if (x.kind != T_IMG && x.kind != T_VEC) return fail(RAFIKI_ERR_INVALID, ln + "FC needs an image or vector");
+        if ((long long)x.c * x.h * x.w != L.c_in || L.c_out < 1 || !L.weight)
+          return fail(RAFIKI_ERR_INVALID, ln + "FC c_in must equal the flattened input size");
+        if (has_bn) return fail(RAFIKI_ERR_UNSUPPORTED, ln + "batch-norm after FC is not supported");
+        y.kind = T_VEC; y.c = L.c_out; y.h = 1; y.w = 1; y.Cs = round_up(L.c_out, 8);
+        op.kind = O_CONV;
+        op.H = 1; op.W = 1; op.Cs_in = x.h * x.w * x.Cs; op.Ho = 1; op.Wo = 1;
+        op.kh = op.kw = op.stride = 1; op.pad = 0; op.c_out = L.c_out;
+        op.K = op.Cs_in;
+        op.bn = bf ? choose_bn(L.c_out) : 32;
+        op.Co_pad = round_up(L.c_out, op.bn);
+        op.Kp = bf ? round_up(op.K, 64) : op.K;
+        if (e->dry) break;
+        const int xc = x.c, xh = x.h, xw = x.w, xCs = x.Cs, cin = L.c_in;
+        // K index (yy, xx, c) over storage channels <- canonical column c*h*w + yy*w + xx
+        std::vector<float> packed((size_t)op.Co_pad * op.Kp, 0.f);
+        for (int co = 0; co < L.c_out; ++co)
+          for (int yy = 0; yy < xh; ++yy)
+            for (int xx = 0; xx < xw; ++xx)
+              for (int c = 0; c < xc; ++c)
+                packed[(size_t)co * op.Kp + (size_t)(yy * xw + xx) * xCs + c] =
+                    L.weight[(size_t)co * cin + (size_t)c * xh * xw + yy * xw + xx];
+        int rc = upload_weights(e, op, packed);
+        if (!rc) rc = upload_fold(e, op, L);
+        if (rc) return rc;
+        break;
+      }
+      case RAFIKI_OP_EMBEDDING: {
+        if (L.input != -1 || x.kind != T_TOK) return fail(RAFIKI_ERR_INVALID, ln + "embedding must read the token input");
+        if (L.c_in != e->vocab || L.c_out < 1 || !L.weight)
+          return fail(RAFIKI_ERR_INVALID, ln + "embedding table must be [vocab, dim]");
+        y.kind = T_SEQ; y.c = L.c_out; y.h = 1; y.w = x.w; y.Cs = round_up(L.c_out, 8);
+        op.kind = O_EMBED; op.Cs_in = y.Cs; op.W = x.w;
+        if (e->dry) break;
+        std::vector<float> packed((size_t)L.c_in * y.Cs, 0.f);
+        for (int r = 0; r < L.c_in; ++r)
+          for (int c = 0; c < L.c_out; ++c) packed[(size_t)r * y.Cs + c] = L.weight[(size_t)r * L.c_out + c];
+        int rc = upload_weights(e, op, packed);
+        if (rc) return rc;
+        break;
+      }
+      case RAFIKI_OP_CONV1D_MAXTIME: {
+        if (x.kind != T_SEQ || L.c_in != x.c || L.c_out < 1 || L.kw < 1 || L.kw > x.w || !L.weight)
+          return fail(RAFIKI_ERR_INVALID, ln + "conv1d needs a sequence input with c_in channels and kw <= length");
+        y.kind = T_VEC; y.c = L.c_out; y.h = 1; y.w = 1; y.Cs = round_up(L.c_out, 8);
+        op.kind = O_CONV1D;
+        op.H = 1; op.W = x.w; op.Cs_in = x.Cs; op.Ho = 1; op.Wo = x.w - L.kw + 1;
+        op.kh = 1; op.kw = L.kw; op.stride = 1; op.pad = 0; op.c_out = L.c_out;
+        op.K = L.kw * x.Cs;
+        op.bn = bf ? choose_bn(L.c_out) : 32;
+        op.Co_pad = round_up(L.c_out, op.bn);
+        op.Kp = bf ? round_up(op.K, 64) : op.K;
+        if (e->dry) break;
+        const int cin = L.c_in, kw = L.kw;
+        auto packed = pack_weight(L.c_out, cin, 1, kw, x.Cs, op.Co_pad, op.Kp,
+                                  [=](int co, int ci, int, int v) { return ((size_t)co * cin + ci) * kw + v; },
+                                  L.weight);
+        int rc = upload_weights(e, op, packed);
+        if (!rc) rc = upload_fold(e, op, L);
+        if (rc) return rc;
+        break;
+      }
+      case RAFIKI_OP_CONCAT: {
+        if (L.input2 < 0) return fail(RAFIKI_ERR_INVALID, ln + "concat needs input2");
+        const Tensor& b = M.tensors[L.input2];
+        if (x.kind != T_VEC || b.kind != T_VEC) return fail(RAFIKI_ERR_INVALID, ln + "concat joins vectors");
+        if (L.c_out != x.c + b.c) return fail(RAFIKI_ERR_INVALID, ln + "concat c_out must be the sum of inputs");
+        y.kind = T_VEC; y.c = L.c_out; y.h = 1; y.w = 1; y.Cs = round_up(L.c_out, 8);
+        op.kind = O_CONCAT; op.ca = x.c; op.cb = b.c;
+        break;
+      }
+      default:
+        return fail(RAFIKI_ERR_INVALID, ln + "unknown op " + std::to_string(L.op));
+    }
+    if (L.op != RAFIKI_OP_CONV2D && L.op != RAFIKI_OP_CONCAT && L.input2 != -1)
+      return fail(RAFIKI_ERR_INVALID, ln + "input2 is only meaningful for conv2d and concat");
+    if (L.op != RAFIKI_OP_CONV2D && L.op != RAFIKI_OP_FC && L.op != RAFIKI_OP_CONV1D_MAXTIME && op.relu)
+      return fail(RAFIKI_ERR_INVALID, ln + "relu is only meaningful for conv2d, FC and conv1d");
+    if (L.op != RAFIKI_OP_CONV2D && L.op != RAFIKI_OP_CONV1D_MAXTIME && has_bn && L.op != RAFIKI_OP_FC)
+      return fail(RAFIKI_ERR_INVALID, ln + "batch-norm is only meaningful for conv layers");
+    M.ops.push_back(op);
+  }
+  const rafiki_layer& last = md.layers[md.n_layers - 1];
+  if (last.op != RAFIKI_OP_FC || last.c_out != md.n_classes)
+    return fail(RAFIKI_ERR_INVALID, "model " + std::to_string(mi) + ": the last layer must be an FC with n_classes outputs");
+  M.tensors.back().is_logits = true;
+
+  // Liveness-planned arena for max_batch requests (the logits go to the ensemble's slots).
+  for (const Op& op : M.ops) {
+    if (op.in >= 0) M.tensors[op.in].last_use = std::max(M.tensors[op.in].last_use, op.out);
+    if (op.in2 >= 0) M.tensors[op.in2].last_use = std::max(M.tensors[op.in2].last_use, op.out);
+  }
+  FreeList fl;
+  const size_t es = e->esz(), nb = (size_t)e->max_batch;
+  for (size_t i = 0; i < M.ops.size(); ++i) {
+    Op& op = M.ops[i];
+    Tensor& y = M.tensors[op.out];
+    size_t tmp_bytes = 0;
+    if (op.kind == O_CONV1D) {
+      tmp_bytes = nb * op.Wo * round_up(op.c_out, 8) * es;
+      op.tmp_off = fl.alloc(tmp_bytes);
+    }
+    if (!y.is_logits) y.off = fl.alloc(nb * y.item_elems() * es);
+    if (op.kind == O_CONV1D) fl.release(op.tmp_off, tmp_bytes);
+    for (int src : {op.in, op.in2}) {
+      if (src >= 0 && M.tensors[src].last_use == (int)i && !M.tensors[src].is_logits)
+        fl.release(M.tensors[src].off, nb * M.tensors[src].item_elems() * es);
+    }
+  }
+  M.arena_bytes = std::max<size_t>(fl.top, 256);
+  return dev_alloc(e, (void**)&M.d_arena, M.arena_bytes);
+}
+
+// Largest split-K partial buffer any GEMM-like op needs for n in [1, max_batch].
+size_t partial_need(const rafiki_ensemble_s* e) {
+  if (e->precision != RAFIKI_BF16) return 0;
+  size_t need = 0;
+  for (const Model& M : e->models)
+    for (const Op& op : M.ops) {
+      if (op.kind != O_CONV && op.kind != O_CONV1D) continue;
+      for (int n = 1; n <= e->max_batch; ++n) {
+        const int Mrows = n * op.Ho * op.Wo;
+        const int bm = choose_bm(Mrows);
+        const int s = choose_splits(Mrows, bm, op.Co_pad / op.bn, op.Kp / 64);
+        if (s > 1) need = std::max(need, (size_t)s * Mrows * op.Co_pad * 4);
+      }
+    }
+  return need;
+}
+
+const void* tptr(const rafiki_ensemble_s* e, const Model& M, int id, const void* batch) {
+  if (id < 0) return e->input_kind == RAFIKI_INPUT_IMAGE_NCHW_F32 ? e->d_staged : batch;
+  return M.d_arena + M.tensors[id].off;
+}
+
+#define HIPCHK(expr)                                                                              \
+  do {                                                                                            \
+    hipError_t st_ = (expr);                                                                      \
+    if (st_ != hipSuccess) return fail(RAFIKI_ERR_HIP, std::string(#expr) + ": " + hipGetErrorString(st_)); \
+  } while (0)
+
+int run_gemm(const rafiki_ensemble_s* e, const Op& op, ConvArgs a, hipStream_t s) {
+  if (e->precision != RAFIKI_BF16) {
+    HIPCHK(launch_conv_f32(a, s));
+    return RAFIKI_OK;
+  }
+  const int bm = choose_bm(a.M);
+  const int ktiles = a.Kp / 64;
+  const int splits = choose_splits(a.M, bm, op.Co_pad / op.bn, ktiles);
+  a.kt_per_split = (ktiles + splits - 1) / splits;
+  if (splits > 1) {
+    if ((size_t)splits * a.M * a.Co_pad * 4 > e->partial_bytes)
+      return fail(RAFIKI_ERR_INVALID, "internal: split-K workspace too small");
+    a.partial = e->d_partial;
+    HIPCHK(launch_conv_bf16(a, bm, op.bn, splits, s));
+    HIPCHK(launch_splitk_reduce(a, splits, 1, s));
+  } else {
+    HIPCHK(launch_conv_bf16(a, bm, op.bn, 1, s));
+  }
+  return RAFIKI_OK;
+}
+
+// Forward pass of model `mi` over n requests; logits [n][n_classes] to `logits`.
+int run_model(const rafiki_ensemble_s* e, int mi, const void* batch, int n, float* logits, hipStream_t s) {
+  const Model& M = e->models[mi];
+  const int bf = e->precision == RAFIKI_BF16 ? 1 : 0;
+  for (const Op& op : M.ops) {
+    const Tensor& y = M.tensors[op.out];
+    void* yp = y.is_logits ? (void*)logits : (void*)(M.d_arena + y.off);
+    const void* xp = tptr(e, M, op.in, batch);
+    switch (op.kind) {
+      case O_CONV:
+      case O_CONV1D: {
+        ConvArgs a{};
+        a.x = xp; a.w = op.d_w; a.scale = op.d_scale; a.shift = op.d_shift;
+        a.res = op.in2 >= 0 ? tptr(e, M, op.in2, batch) : nullptr;
+        a.N = n; a.H = op.H; a.W = op.W; a.Cs = op.Cs_in;
+        a.Ho = op.Ho; a.Wo = op.Wo; a.kh = op.kh; a.kw = op.kw; a.stride = op.stride; a.pad = op.pad;
+        a.M = n * op.Ho * op.Wo; a.K = op.K; a.Kp = op.Kp; a.Co_pad = op.Co_pad;
+        a.relu = op.relu;
+        if (op.kind == O_CONV1D) {
+          void* tmp = M.d_arena + op.tmp_off;
+          a.y = tmp; a.c_write = round_up(op.c_out, 8); a.ldy = a.c_write; a.out_f32 = bf ? 0 : 1;
+          int rc = run_gemm(e, op, a, s);
+          if (rc) return rc;
+          HIPCHK(launch_spatial_reduce(tmp, yp, n, op.Wo, y.Cs, 1, bf, s));
+          break;
+        }
+        a.y = yp;
+        if (y.is_logits) { a.c_write = y.c; a.ldy = y.c; a.out_f32 = 1; }
+        else { a.c_write = y.Cs; a.ldy = y.Cs; a.out_f32 = bf ? 0 : 1; }
+        int rc = run_gemm(e, op, a, s);
+        if (rc) return rc;
+        break;
+      }
+      case O_MAXPOOL:
+        HIPCHK(launch_maxpool(xp, yp, n, op.H, op.W, op.Cs_in, op.Ho, op.Wo, op.k, op.stride, op.pad, bf, s));
+        break;
+      case O_GAP:
+        HIPCHK(launch_spatial_reduce(xp, yp, n, op.H * op.W, op.Cs_in, 0, bf, s));
+        break;
+      case O_EMBED:
+        HIPCHK(launch_embed_gather((const int32_t*)batch, op.d_w, yp, n, op.W, op.Cs_in, bf, s));
+        break;
+      case O_CONCAT: {
+        const Tensor& a = M.tensors[op.in];
+        const Tensor& b = M.tensors[op.in2];
+        HIPCHK(launch_concat(xp, op.ca, a.Cs, tptr(e, M, op.in2, batch), op.cb, b.Cs, yp, y.Cs, n, bf, s));
+        break;
+      }
+    }
+  }
+  return RAFIKI_OK;
+}
+
+int check_call(const rafiki_ensemble_s* h, const void* batch, int n) {
+  if (!h) return fail(RAFIKI_ERR_INVALID, "null handle");
+  if (!batch) return fail(RAFIKI_ERR_INVALID, "null batch pointer");
+  if (n < 1 || n > h->max_batch)
+    return fail(RAFIKI_ERR_INVALID, "n must be in [1, max_batch = " + std::to_string(h->max_batch) + "]");
+  return RAFIKI_OK;
+}
+
+int stage(const rafiki_ensemble_s* e, const void* batch, int n, hipStream_t s) {
+  if (e->input_kind != RAFIKI_INPUT_IMAGE_NCHW_F32) return RAFIKI_OK;
+  HIPCHK(launch_stage_images((const float*)batch, e->d_staged, n, e->C, e->H, e->W, e->in_Cs,
+                             e->precision == RAFIKI_BF16, s));
+  return RAFIKI_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int rafiki_ensemble_create(const rafiki_model_desc* models, int n_models, const rafiki_ensemble_opts* opts,
+                           rafiki_ensemble_t* out) {
+  if (out) *out = nullptr;
+  if (!models || !opts || !out) return fail(RAFIKI_ERR_INVALID, "null argument");
+  if (n_models < 1 || n_models > 32) return fail(RAFIKI_ERR_INVALID, "n_models must be in [1, 32]");
+  if (opts->precision != RAFIKI_FP32 && opts->precision != RAFIKI_BF16)
+    return fail(RAFIKI_ERR_INVALID, "unknown precision");
+  if (opts->max_batch < 1) return fail(RAFIKI_ERR_INVALID, "max_batch must be >= 1");
+  if (opts->input_kind == RAFIKI_INPUT_IMAGE_NCHW_F32) {
+    if (opts->c < 1 || opts->h < 1 || opts->w < 1) return fail(RAFIKI_ERR_INVALID, "image shape must be positive");
+  } else if (opts->input_kind == RAFIKI_INPUT_TOKENS_I32) {
+    if (opts->h < 1 || opts->vocab < 1) return fail(RAFIKI_ERR_INVALID, "sequence length and vocab must be positive");
+  } else {
+    return fail(RAFIKI_ERR_INVALID, "unknown input kind");
+  }
+  const int n_classes = models[0].n_classes;
+  for (int m = 0; m < n_models; ++m)
+    if (models[m].n_classes != n_classes)
+      return fail(RAFIKI_ERR_INVALID, "all models must have the same number of classes");
+  if (n_classes > 1024) return fail(RAFIKI_ERR_UNSUPPORTED, "at most 1024 classes are supported");
+
+  std::unique_ptr<rafiki_ensemble_s> e(new rafiki_ensemble_s());
+  e->n_models = n_models; e->n_classes = n_classes; e->precision = opts->precision;
+  e->max_batch = opts->max_batch; e->input_kind = opts->input_kind;
+  e->C = opts->c; e->H = opts->h; e->W = opts->w; e->vocab = opts->vocab;
+  if (e->input_kind == RAFIKI_INPUT_TOKENS_I32) { e->C = 1; e->W = 1; }
+  e->in_Cs = round_up(e->C, 8);
+  // Pass 1: validate every model and infer shapes without touching the device.
+  e->dry = true;
+  e->models.resize(n_models);
+  for (int m = 0; m < n_models; ++m) {
+    int rc = build_model(e.get(), m, models[m], e->models[m]);
+    if (rc) return rc;
+  }
+  int ndev = 0;
+  hipError_t st = hipGetDeviceCount(&ndev);
+  if (st != hipSuccess || ndev < 1) {
+    (void)hipGetLastError();
+    return fail(RAFIKI_ERR_HIP, std::string("no HIP device: ") + hipGetErrorString(st));
+  }
+  st = hipGetDevice(&e->device);
+  if (st != hipSuccess) return fail(RAFIKI_ERR_HIP, std::string("hipGetDevice: ") + hipGetErrorString(st));
+  // Pass 2: pack and upload.
+  e->dry = false;
+  e->models.clear();
+  e->models.resize(n_models);
+  for (int m = 0; m < n_models; ++m) {
+    int rc = build_model(e.get(), m, models[m], e->models[m]);
+    if (rc) return rc;
+  }
+  int rc;
+  if (e->input_kind == RAFIKI_INPUT_IMAGE_NCHW_F32) {
+    rc = dev_alloc(e.get(), &e->d_staged, (size_t)e->max_batch * e->H * e->W * e->in_Cs * e->esz());
+    if (rc) return rc;
+  }
+  rc = dev_alloc(e.get(), (void**)&e->d_logits, (size_t)n_models * e->max_batch * n_classes * 4);
+  if (rc) return rc;
+  e->partial_bytes = partial_need(e.get());
+  if (e->partial_bytes) {
+    rc = dev_alloc(e.get(), (void**)&e->d_partial, e->partial_bytes);
+    if (rc) return rc;
+  }
+  *out = e.release();
+  g_err.clear();
+  return RAFIKI_OK;
+}
+
+int rafiki_ensemble_infer(rafiki_ensemble_t h, const void* batch, int n, uint32_t model_subset_mask,
+                          float* out_probs, int32_t* out_labels, void* stream) {
+  int rc = check_call(h, batch, n);
+  if (rc) return rc;
+  if (!out_probs || !out_labels) return fail(RAFIKI_ERR_INVALID, "null output pointer");
+  if (model_subset_mask == 0) return fail(RAFIKI_ERR_INVALID, "model_subset_mask must select at least one model");
+  if (h->n_models < 32 && (model_subset_mask >> h->n_models) != 0)
+    return fail(RAFIKI_ERR_INVALID, "model_subset_mask selects a model that does not exist");
+  hipStream_t s = (hipStream_t)stream;
+  rc = stage(h, batch, n, s);
+  if (rc) return rc;
+  CombineArgs ca{};
+  ca.logits = h->d_logits;
+  ca.ld_model = (long long)h->max_batch * h->n_classes;
+  ca.n = n; ca.C = h->n_classes; ca.probs = out_probs; ca.labels = out_labels;
+  for (int m = 0; m < h->n_models; ++m) {
+    if (!((model_subset_mask >> m) & 1u)) continue;
+    rc = run_model(h, m, batch, n, h->d_logits + (size_t)m * ca.ld_model, s);
+    if (rc) return rc;
+    ca.sel[ca.S++] = m;
+  }
+  HIPCHK(launch_combine(ca, s));
+  return RAFIKI_OK;
+}
+
+int rafiki_ensemble_model_logits(rafiki_ensemble_t h, int model, const void* batch, int n, float* out_logits,
+                                 void* stream) {
+  int rc = check_call(h, batch, n);
+  if (rc) return rc;
+  if (!out_logits) return fail(RAFIKI_ERR_INVALID, "null output pointer");
+  if (model < 0 || model >= h->n_models) return fail(RAFIKI_ERR_INVALID, "model index out of range");
+  hipStream_t s = (hipStream_t)stream;
+  rc = stage(h, batch, n, s);
+  if (rc) return rc;
+  return run_model(h, model, batch, n, out_logits, s);
+}
+
+int rafiki_ensemble_info(rafiki_ensemble_t h, int* n_models, int* n_classes, int* max_batch) {
+  if (!h) return fail(RAFIKI_ERR_INVALID, "null handle");
+  if (n_models) *n_models = h->n_models;
+  if (n_classes) *n_classes = h->n_classes;
+  if (max_batch) *max_batch = h->max_batch;
+  return RAFIKI_OK;
+}
+
+int rafiki_ensemble_destroy(rafiki_ensemble_t h) {
+  if (!h) return RAFIKI_OK;
+  hipError_t st = hipDeviceSynchronize();
+  delete h;
+  if (st != hipSuccess) return fail(RAFIKI_ERR_HIP, std::string("hipDeviceSynchronize: ") + hipGetErrorString(st));
+  return RAFIKI_OK;
+}
+
+const char* rafiki_last_error(void) { return g_err.c_str(); }
+
+}  // extern "C"

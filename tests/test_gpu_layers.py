@@ -1,0 +1,127 @@
+"""Single-layer parity through the C ABI.
+
+Each probe model is the layer(s) under test followed by an FC whose weight is the
+identity, so the model's logits are the stored output tensor flattened in (c, h, w)
+order (with bf16 storage the identity FC is exact: one nonzero product per output,
+accumulated in fp32).  Shapes cover the edge cases of the kernels: input channels
+not a multiple of 8 or 64, odd and non-square images, stride 2, 1x1 and 7x7 kernels,
+channel counts that leave a ragged tile, residual adds, split-K FCs and a small
+TextCNN.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads as wl
+from workloads import Layer, ModelSpec, CONV2D, MAXPOOL2D, GLOBAL_AVGPOOL, FC, EMBEDDING, CONV1D_MAXTIME, CONCAT
+from paper_1804_06087_amd import Ensemble
+
+pytestmark = pytest.mark.gpu
+DEV = torch.device("cuda:0")
+
+
+def probe(layers, in_shape, out_elems, identity=True, n_out=None, seed=5, bf16=True, vocab=0):
+    L = list(layers)
+    n_out = out_elems if identity else n_out
+    L.append(Layer(op=FC, input=len(layers) - 1, c_in=out_elems, c_out=n_out, bias=True))
+    spec = ModelSpec("probe", L, n_out, in_shape, vocab=vocab)
+    params = wl.gen_params(spec, seed, bf16, "random")
+    if identity:
+        params.layers[-1].weight = np.eye(out_elems, dtype=np.float32)
+    return spec, params
+
+
+def gpu_logits(spec, params, batch, precision):
+    n = batch.shape[0]
+    with Ensemble([spec], [params], precision=precision, max_batch=n) as ens:
+        x = torch.from_numpy(batch).to(DEV)
+        out = torch.empty((n, spec.n_classes), dtype=torch.float32, device=DEV)
+        ens.model_logits(0, x, n, out)
+        torch.cuda.synchronize()
+        return out.cpu().numpy()
+
+
+def check_bf16_tensor(z, ref):
+    """bf16-stored tensors: each element within one bf16 step of the oracle's
+    (fp32 vs fp64 accumulation may round the other way), few elements differing."""
+    ref = np.asarray(ref, np.float64)
+    d = np.abs(z - ref)
+    tol = np.abs(ref) * 2.0 ** -7 + 1e-6 * np.abs(ref).max()
+    assert (d <= tol).all(), f"max excess {(d - tol).max()}"
+    assert (d > 0).mean() < 0.02, f"{(d > 0).mean():.3%} of elements differ"
+
+
+def conv(i, c_in, c_out, k, s=1, p=None, relu=True, bn=True, bias=False, res=-1):
+    return Layer(op=CONV2D, input=i, input2=res, c_in=c_in, c_out=c_out, kh=k, kw=k, stride=s,
+                 pad=k // 2 if p is None else p, relu=relu, bn=bn, bias=bias)
+
+
+CASES = {
+    # name: (layers, input (C, H, W), n, output elements)
+    "stem3x3_cin3": ([conv(-1, 3, 16, 3)], (3, 7, 7), 3, 16 * 7 * 7),
+    "s2_cin24_cout40_nonsquare": ([conv(-1, 24, 40, 3, s=2)], (24, 11, 7), 5, 40 * 6 * 4),
+    "1x1_s2_cout136": ([conv(-1, 64, 136, 1, s=2, p=0)], (64, 4, 4), 4, 136 * 2 * 2),
+    "7x7_s2_p3_stem": ([conv(-1, 3, 64, 7, s=2, p=3)], (3, 7, 7), 2, 64 * 4 * 4),
+    "residual_block": ([conv(-1, 16, 32, 1, p=0, relu=False), conv(-1, 16, 32, 3, res=0)], (16, 5, 5), 3,
+                       32 * 5 * 5),
+    "vgg_style_bias_no_bn": ([conv(-1, 8, 32, 3, bn=False, bias=True)], (8, 6, 5), 3, 32 * 6 * 5),
+    "maxpool3_s2_p1_odd": ([conv(-1, 8, 16, 3), Layer(op=MAXPOOL2D, input=0, c_in=16, c_out=16, kh=3, kw=3,
+                                                       stride=2, pad=1)], (8, 9, 9), 2, 16 * 5 * 5),
+    "maxpool2_s2": ([conv(-1, 8, 16, 3), Layer(op=MAXPOOL2D, input=0, c_in=16, c_out=16, kh=2, kw=2, stride=2)],
+                    (8, 8, 6), 2, 16 * 4 * 3),
+    "gap": ([conv(-1, 8, 48, 3), Layer(op=GLOBAL_AVGPOOL, input=0, c_in=48, c_out=48)], (8, 7, 5), 6, 48),
+    "many_tiles_ragged_m": ([conv(-1, 32, 16, 3)], (32, 7, 9), 37, 16 * 7 * 9),
+}
+
+
+@pytest.mark.parametrize("name", sorted(CASES))
+def test_layer_bf16(name):
+    layers, shape, n, out_elems = CASES[name]
+    spec, params = probe(layers, shape, out_elems)
+    batch = wl.gen_images(n, shape, "normal", True, seed=11)
+    z = gpu_logits(spec, params, batch, "bf16")
+    ref = oracle.run_model(spec, params, batch, act="bf16")
+    check_bf16_tensor(z, ref)
+
+
+@pytest.mark.parametrize("name", ["stem3x3_cin3", "s2_cin24_cout40_nonsquare", "residual_block", "maxpool3_s2_p1_odd",
+                                  "gap", "7x7_s2_p3_stem"])
+def test_layer_fp32(name):
+    layers, shape, n, out_elems = CASES[name]
+    spec, params = probe(layers, shape, out_elems, bf16=False)
+    batch = wl.gen_images(n, shape, "normal", False, seed=11)
+    z = gpu_logits(spec, params, batch, "fp32")
+    ref = oracle.run_model(spec, params, batch)
+    assert np.abs(z - ref).max() <= 1e-5 * np.abs(ref).max()
+
+
+@pytest.mark.parametrize("precision", ["bf16", "fp32"])
+def test_fc_flatten_order_and_split_k(precision):
+    """FC on a spatial input (flattened in (c, h, w) order) with a long K that the bf16
+    path splits across workgroups; random weights, fp32 logits."""
+    bf = precision == "bf16"
+    layers = [conv(-1, 16, 64, 1, p=0)]                    # -> [64, 8, 8] = 4096 features
+    spec, params = probe(layers, (16, 8, 8), 64 * 8 * 8, identity=False, n_out=100)
+    params = wl.gen_params(spec, 9, bf, "random")
+    for n in (1, 3, 70):
+        batch = wl.gen_images(n, (16, 8, 8), "normal", bf, seed=3)
+        z = gpu_logits(spec, params, batch, precision)
+        ref = oracle.run_model(spec, params, batch, act="bf16" if bf else None)
+        err = np.abs(z - ref).max() / np.abs(ref).max()
+        assert err <= (1e-4 if bf else 1e-5), (n, err)
+
+
+def test_textcnn_small():
+    spec = wl.textcnn(vocab=50, seq_len=12, dim=20, filters=5, widths=(2, 3, 5), n_classes=2)
+    for precision in ("bf16", "fp32"):
+        bf = precision == "bf16"
+        params = wl.gen_params(spec, 4, bf, "random")
+        for L, P in zip(spec.layers, params.layers):       # non-zero biases exercise the epilogue
+            if L.bias:
+                P.bias = np.linspace(-0.2, 0.3, L.c_out).astype(np.float32)
+        tok = wl.gen_tokens(9, 12, 50, seed=2)
+        z = gpu_logits(spec, params, tok, precision)
+        ref = oracle.run_model(spec, params, tok, act="bf16" if bf else None)
+        err = np.abs(z - ref).max() / np.abs(ref).max()
+        assert err <= (1e-2 if bf else 1e-5), (precision, err)

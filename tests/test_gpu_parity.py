@@ -1,0 +1,238 @@
+"""Parity of the HIP path (through the C ABI) against the fp64 oracle.
+
+Metrics (the tolerances the hot path is specified with):
+* logits: row-normwise relative error max_j |z_gpu - z_ref| / max_j |z_ref|, maximised
+  over rows; <= 1e-4 for the fp32 path, <= 2e-2 for the bf16 path;
+* labels: the GPU label must equal the oracle's, except on rows where the oracle's
+  top-2 averaged probabilities differ by < 1e-3; the bf16 path must also reach >= 99.5%
+  agreement overall (exact matches counted only);
+* probabilities: rows sum to 1 within 1e-5.
+bf16 workloads are compared with the oracle both in exact fp64 mode and in
+bf16-storage mode (every stored inter-layer tensor rounded to bf16, as specified
+for those workloads).
+"""
+import functools
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads as wl
+from paper_1804_06087_amd import Ensemble, RafikiError, RAFIKI_ERR_INVALID
+
+pytestmark = pytest.mark.gpu
+DEV = torch.device("cuda:0")
+CANARY = 7777.0
+
+
+def normwise(z, ref):
+    z = np.asarray(z, np.float64)
+    ref = np.asarray(ref, np.float64)
+    return float((np.abs(z - ref).max(1) / np.maximum(np.abs(ref).max(1), 1e-30)).max())
+
+
+def label_check(lab, p_ref, min_agree=1.0):
+    lab = np.asarray(lab)
+    srt = np.sort(p_ref, 1)
+    gap = srt[:, -1] - srt[:, -2]
+    ref = oracle.argmax_first(p_ref)
+    mism = lab != ref
+    unexcused = mism & (gap >= 1e-3)
+    agree = 1.0 - mism.mean()
+    assert not unexcused.any(), f"label mismatches with gap >= 1e-3 at rows {np.nonzero(unexcused)[0]}"
+    assert agree >= min_agree, f"agreement {agree:.4f} < {min_agree}"
+    return agree
+
+
+def run_infer(ens, batch_np, n, mask, C):
+    x = torch.from_numpy(np.ascontiguousarray(batch_np[:n])).to(DEV)
+    probs = torch.full((n * C + 64,), CANARY, dtype=torch.float32, device=DEV)
+    labels = torch.full((n + 16,), -7, dtype=torch.int32, device=DEV)
+    ens.infer(x, n, mask, probs, labels)
+    torch.cuda.synchronize()
+    p = probs.cpu().numpy()
+    lab = labels.cpu().numpy()
+    assert (p[n * C:] == CANARY).all(), "write past out_probs"
+    assert (lab[n:] == -7).all(), "write past out_labels"
+    return p[:n * C].reshape(n, C), lab[:n]
+
+
+def run_logits(ens, batch_np, n, m, C):
+    x = torch.from_numpy(np.ascontiguousarray(batch_np[:n])).to(DEV)
+    out = torch.full((n * C + 64,), CANARY, dtype=torch.float32, device=DEV)
+    ens.model_logits(m, x, n, out)
+    torch.cuda.synchronize()
+    z = out.cpu().numpy()
+    assert (z[n * C:] == CANARY).all(), "write past out_logits"
+    return z[:n * C].reshape(n, C)
+
+
+# ------------------------------------------------------------------ C1: toy fp32
+def test_c1_fp32_all_masks():
+    cfg, specs, params, batch = wl.build_config(1)
+    n, C = cfg.n, 10
+    with Ensemble(specs, params, precision="fp32", max_batch=8) as ens:
+        zs = [oracle.run_model(s, p, batch) for s, p in zip(specs, params)]
+        for m in range(2):
+            assert normwise(run_logits(ens, batch, n, m, C), zs[m]) <= 1e-4
+        for mask in (1, 2, 3):
+            p_ref, l_ref, _ = oracle.ensemble(specs, params, batch, mask, logits=zs)
+            p, lab = run_infer(ens, batch, n, mask, C)
+            assert np.abs(p - p_ref).max() <= 1e-5
+            assert np.allclose(p.sum(1), 1.0, atol=1e-5)
+            label_check(lab, p_ref)
+        # ragged smaller batch on the same handle
+        p, lab = run_infer(ens, batch, 5, 3, C)
+        p_ref, _, _ = oracle.ensemble(specs, params, batch[:5], 3, logits=[z[:5] for z in zs])
+        assert np.abs(p - p_ref).max() <= 1e-5
+        label_check(lab, p_ref)
+
+
+# ------------------------------------------------------------------ C2: ResNet-20 x 3 bf16
+@functools.lru_cache(maxsize=None)
+def _c2(n):
+    cfg, specs, params, batch = wl.build_config(2, n=n)
+    ze = [oracle.run_model(s, p, batch) for s, p in zip(specs, params)]
+    zb = [oracle.run_model(s, p, batch, act="bf16") for s, p in zip(specs, params)]
+    return cfg, specs, params, batch, ze, zb
+
+
+def test_c2_bf16_all_masks_ragged():
+    cfg, specs, params, batch, ze, zb = _c2(37)
+    n, C = 37, 10
+    with Ensemble(specs, params, precision="bf16", max_batch=48) as ens:
+        for m in range(3):
+            z = run_logits(ens, batch, n, m, C)
+            e_b, e_e = normwise(z, zb[m]), normwise(z, ze[m])
+            print(f"resnet20 model {m}: normwise vs bf16-storage oracle {e_b:.3g}, vs exact {e_e:.3g}")
+            assert e_b <= 2e-2 and e_e <= 2e-2
+        for mask in range(1, 8):
+            p, lab = run_infer(ens, batch, n, mask, C)
+            assert np.allclose(p.sum(1), 1.0, atol=1e-5)
+            for zref in (zb, ze):
+                p_ref, _, _ = oracle.ensemble(specs, params, batch, mask, logits=zref)
+                label_check(lab, p_ref, min_agree=0.995)
+
+
+def test_c2_full_batch_and_invariants():
+    """n = 128 as configured; single-model masks equal that model's softmax/argmax;
+    outputs are bitwise deterministic and independent of batch composition."""
+    cfg, specs, params, batch = wl.build_config(2)
+    n, C = cfg.n, 10
+    rows = np.arange(0, n, 9)
+    ze = [oracle.run_model(s, p, batch[rows]) for s, p in zip(specs, params)]
+    zb = [oracle.run_model(s, p, batch[rows], act="bf16") for s, p in zip(specs, params)]
+    with Ensemble(specs, params, precision="bf16", max_batch=n) as ens:
+        p, lab = run_infer(ens, batch, n, 0b111, C)
+        p2, lab2 = run_infer(ens, batch, n, 0b111, C)
+        assert np.array_equal(p, p2) and np.array_equal(lab, lab2), "not deterministic"
+        for zref in (zb, ze):
+            p_ref, _, _ = oracle.ensemble(specs, params, batch[rows], 0b111, logits=zref)
+            label_check(lab[rows], p_ref, min_agree=0.995)
+        for m in range(3):
+            z = run_logits(ens, batch, n, m, C)
+            assert normwise(z[rows], zb[m]) <= 2e-2 and normwise(z[rows], ze[m]) <= 2e-2
+            p1, lab1 = run_infer(ens, batch, n, 1 << m, C)
+            sm = oracle.softmax(z.astype(np.float64))
+            assert np.abs(p1 - sm).max() <= 1e-6
+            assert np.array_equal(lab1, oracle.argmax_first(p1))
+        p5, lab5 = run_infer(ens, batch, 5, 0b111, C)
+        assert np.array_equal(p5, p[:5]) and np.array_equal(lab5, lab[:5]), "batch composition changed results"
+
+
+def test_gpu_argument_errors():
+    cfg, specs, params, batch = wl.build_config(1)
+    with Ensemble(specs, params, precision="fp32", max_batch=8) as ens:
+        x = torch.from_numpy(batch).to(DEV)
+        probs = torch.empty((16, 10), device=DEV)
+        labels = torch.empty((16,), dtype=torch.int32, device=DEV)
+        for n, mask in ((9, 1), (0, 1), (4, 0), (4, 0b100)):
+            with pytest.raises(RafikiError) as ei:
+                ens.infer(x, n, mask, probs, labels)
+            assert ei.value.code == RAFIKI_ERR_INVALID
+        with pytest.raises(RafikiError):
+            ens.model_logits(2, x, 4, probs)
+
+
+# ------------------------------------------------------------------ C3 / C4: ImageNet-shaped
+_C3_ROWS = (0, 3, 15, 31, 63, 255)
+
+
+@functools.lru_cache(maxsize=None)
+def _c3():
+    cfg, specs, params, batch = wl.build_config(4)            # 256 images; the first 64 are config 3's batch
+    sub = batch[list(_C3_ROWS)]
+    ze = [oracle.run_model(s, p, sub, chunk=2) for s, p in zip(specs, params)]
+    zb = [oracle.run_model(s, p, sub, act="bf16", chunk=2) for s, p in zip(specs, params)]
+    return cfg, specs, params, batch, ze, zb
+
+
+@pytest.fixture(scope="module")
+def c3_ens():
+    cfg, specs, params, batch, ze, zb = _c3()
+    ens = Ensemble(specs, params, precision="bf16", max_batch=256)
+    yield ens
+    ens.close()
+
+
+def test_c3_full_batch_sampled_rows(c3_ens):
+    cfg, specs, params, batch, ze, zb = _c3()
+    n, C = 64, 1000
+    rows = [i for i, r in enumerate(_C3_ROWS) if r < n]
+    ridx = [_C3_ROWS[i] for i in rows]
+    for m in range(3):
+        z = run_logits(c3_ens, batch, n, m, C)[ridx]
+        e_b, e_e = normwise(z, zb[m][rows]), normwise(z, ze[m][rows])
+        print(f"{specs[m].name}: normwise vs bf16-storage oracle {e_b:.3g}, vs exact {e_e:.3g}")
+        assert e_b <= 2e-2 and e_e <= 2e-2
+    p, lab = run_infer(c3_ens, batch, n, 0b111, C)
+    assert np.allclose(p.sum(1), 1.0, atol=1e-5)
+    for zref in (zb, ze):
+        p_ref, _, _ = oracle.ensemble(specs, params, batch[ridx], 0b111, logits=[z[rows] for z in zref])
+        label_check(lab[ridx], p_ref)
+
+
+@pytest.mark.parametrize("n", [1, 4, 16, 64, 256])
+def test_c4_sweep(c3_ens, n):
+    cfg, specs, params, batch, ze, zb = _c3()
+    C = 1000
+    rows = [i for i, r in enumerate(_C3_ROWS) if r < n]
+    ridx = [_C3_ROWS[i] for i in rows]
+    for mask in (0b001, 0b011, 0b111):
+        p, lab = run_infer(c3_ens, batch, n, mask, C)
+        assert np.allclose(p.sum(1), 1.0, atol=1e-5)
+        for zref in (zb, ze):
+            p_ref, _, _ = oracle.ensemble(specs, params, batch[ridx], mask,
+                                          logits=[z[rows] for z in zref])
+            label_check(lab[ridx], p_ref)
+            sel = [m for m in range(3) if (mask >> m) & 1]
+            # the ensemble probabilities themselves (fp32 softmax of bf16-path logits)
+            assert np.abs(p[ridx] - p_ref).max() <= 5e-2, (mask, n)
+        del sel
+
+
+# ------------------------------------------------------------------ C5: TextCNN x 4
+def test_c5_textcnn():
+    cfg, specs, params, batch = wl.build_config(5)
+    n, C = cfg.n, 2
+    rows = np.arange(0, n, 8)
+    ze = [oracle.run_model(s, p, batch[rows]) for s, p in zip(specs, params)]
+    zb = [oracle.run_model(s, p, batch[rows], act="bf16") for s, p in zip(specs, params)]
+    with Ensemble(specs, params, precision="bf16", max_batch=n) as ens:
+        for m in range(4):
+            z = run_logits(ens, batch, n, m, C)[rows]
+            e_b, e_e = normwise(z, zb[m]), normwise(z, ze[m])
+            print(f"textcnn {m}: normwise vs bf16-storage oracle {e_b:.3g}, vs exact {e_e:.3g}")
+            assert e_b <= 2e-2 and e_e <= 2e-2
+        p, lab = run_infer(ens, batch, n, 0b1111, C)
+        assert np.allclose(p.sum(1), 1.0, atol=1e-5)
+        for zref in (zb, ze):
+            p_ref, _, _ = oracle.ensemble(specs, params, batch[rows], 0b1111, logits=zref)
+            label_check(lab[rows], p_ref, min_agree=0.995)
+        # a ragged smaller batch, every row checked
+        p, lab = run_infer(ens, batch, 67, 0b0101, C)
+        zb67 = [oracle.run_model(s, pp, batch[:67], act="bf16") if m in (0, 2) else None
+                for m, (s, pp) in enumerate(zip(specs, params))]
+        p_ref, _, _ = oracle.ensemble(specs, params, batch[:67], 0b0101, logits=zb67)
+        label_check(lab, p_ref, min_agree=0.995)
