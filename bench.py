@@ -1,0 +1,212 @@
+#!/usr/bin/env python3
+"""Ensemble-inference benchmark on one MI355X.
+
+A step is one call of the C ABI's infer over one request batch: input staging, the
+forward pass of every selected model, and the combine.  Inputs and weights are
+resident in HBM before timing starts.  Default workload: ResNet-50 + VGG-16 +
+ResNet-101, batch 64 of 3x224x224 images, bf16 with fp32 accumulation, all three
+models selected.
+
+Prints ONE JSON line: throughput (images/s or sequences/s), ms per step, p50/p99
+batch latency, the roofline of the dominant kernel class (timed live with HIP events
+on the launch stream in a separate traced pass), and the fp64 CPU oracle timed on
+a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "ensemble images/sec at batch 64 (bf16, 224²) + MFMA util %; p50 batch latency"
+PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 matrix peak
+PEAK_FP32_TFLOPS = 157.3      # MI355X fp32 vector peak
+PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
+
+WORKLOADS = {
+    # name: (config id, batch, mask, description)
+    "c3": (3, 64, 0b111, "resnet50+vgg16+resnet101 ensemble, batch 64 of 3x224x224, bf16 (fp32 accumulate)"),
+    "c2": (2, 128, 0b111, "3x resnet20 ensemble, batch 128 of 3x32x32, bf16 (fp32 accumulate)"),
+    "c1": (1, 8, 0b11, "2x toy CNN ensemble, batch 8 of 3x32x32, fp32"),
+    "c5": (5, 512, 0b1111, "4x textcnn ensemble, batch 512 of 256 tokens, bf16 (fp32 accumulate)"),
+}
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="c3", choices=sorted(WORKLOADS) + ["c4"])
+    ap.add_argument("--n", type=int, default=None, help="batch size (c4 sweep points, or override)")
+    ap.add_argument("--mask", type=int, default=None, help="model subset mask override")
+    ap.add_argument("--trace-steps", type=int, default=3)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU time of the oracle sample")
+    return ap.parse_args()
+
+
+def cpu_baseline(specs, params, batch, mask, target_s, unit):
+    """Time the fp64 oracle (as is) on the host cores over a bounded sample of the batch."""
+    import numpy as np
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:
+        cores = os.cpu_count() or 1
+    t0 = time.perf_counter()
+    oracle.ensemble(specs, params, batch[:1], mask)
+    t1 = time.perf_counter() - t0
+    k = int(max(1, min(batch.shape[0], round(target_s / max(t1, 1e-6)))))
+    t0 = time.perf_counter()
+    oracle.ensemble(specs, params, batch[:k], mask)
+    dt = time.perf_counter() - t0
+    return {"value": round(k / dt, 4), "unit": unit, "cores": int(cores), "kind": "oracle",
+            "sample": f"{k} of the {batch.shape[0]} requests, all selected models, fp64 NumPy oracle, "
+                      f"{dt:.1f} s"}
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1 "
+                                   "(sharding is described in the design notes, not implemented)"}))
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import workloads as wl
+    from paper_1804_06087_amd import Ensemble
+
+    if not torch.cuda.is_available():
+        print(json.dumps({"error": "no GPU visible"}))
+        sys.exit(1)
+    dev = torch.device("cuda:0")
+
+    if args.workload == "c4":
+        cid, n, mask, desc = 4, args.n or 64, args.mask or 0b111, None
+        desc = f"resnet50+vgg16+resnet101 subset mask {mask:#05b}, batch {n} of 3x224x224, bf16 (fp32 accumulate)"
+    else:
+        cid, n, mask, desc = WORKLOADS[args.workload]
+        if args.n:
+            n = args.n
+        if args.mask:
+            mask = args.mask
+    cfg, specs, params, batch = wl.build_config(cid, n=n)
+    precision = cfg.precision
+    tokens = cfg.input_dist == "tokens"
+    unit = "sequences/s" if tokens else "images/s"
+    C = specs[0].n_classes
+
+    ens = Ensemble(specs, params, precision=precision, max_batch=n)
+    x = torch.from_numpy(batch).to(dev)
+    probs = torch.empty((n, C), dtype=torch.float32, device=dev)
+    labels = torch.empty((n,), dtype=torch.int32, device=dev)
+    stream = torch.cuda.current_stream()
+
+    for _ in range(args.warmup):
+        ens.infer(x, n, mask, probs, labels, stream)
+    torch.cuda.synchronize()
+
+    # ---- throughput: K back-to-back steps bracketed by synchronisation
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        ens.infer(x, n, mask, probs, labels, stream)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    ms_per_step = ev0.elapsed_time(ev1) / args.steps
+
+    # ---- latency: each step on its own, events on the launch stream
+    lat = []
+    for _ in range(max(args.steps, 10)):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        ens.infer(x, n, mask, probs, labels, stream)
+        b.record(stream)
+        b.synchronize()
+        lat.append(a.elapsed_time(b))
+    lat = np.array(lat)
+
+    # ---- traced pass: per-launch HIP events around every kernel (separate from the timed steps)
+    ens.trace(True)
+    for _ in range(args.trace_steps):
+        ens.infer(x, n, mask, probs, labels, stream)
+    recs = ens.trace_read()
+    ens.trace(False)
+    torch.cuda.synchronize()
+    classes = {}
+    for r in recs:
+        c = classes.setdefault(r["kind"], {"launches": 0, "ms": 0.0, "flops": 0.0, "bytes": 0.0})
+        c["launches"] += 1
+        c["ms"] += r["ms"]
+        c["flops"] += r["flops"]
+        c["bytes"] += r["bytes"]
+    traced_step_ms = sum(c["ms"] for c in classes.values()) / args.trace_steps
+    kernels = {}
+    for k, c in classes.items():
+        ent = {"launches_per_step": c["launches"] // args.trace_steps, "ms_per_step": round(c["ms"] / args.trace_steps, 4),
+               "share": round(c["ms"] / args.trace_steps / traced_step_ms, 4)}
+        if c["flops"] > 0:
+            ent["tflops"] = round(c["flops"] / c["ms"] / 1e9, 2)
+        ent["gbs_alg"] = round(c["bytes"] / c["ms"] / 1e6, 1)
+        kernels[k] = ent
+    dom = max(classes, key=lambda k: classes[k]["ms"])
+    d = classes[dom]
+    if d["flops"] > 0:
+        peak = PEAK_BF16_TFLOPS if precision == "bf16" else PEAK_FP32_TFLOPS
+        achieved = d["flops"] / d["ms"] / 1e9
+        roof = {"bound": "mfma" if precision == "bf16" else "alu", "achieved": round(achieved, 2), "peak": peak,
+                "unit": "TFLOP/s", "frac": round(achieved / peak, 4), "traffic": None,
+                "kernel": dom, "avg_launch_ms": round(d["ms"] / d["launches"], 5),
+                "alg_flops_per_launch": round(d["flops"] / d["launches"], 1)}
+    else:
+        achieved = d["bytes"] / d["ms"] / 1e6
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None, "kernel": dom,
+                "avg_launch_ms": round(d["ms"] / d["launches"], 5),
+                "alg_bytes_per_launch": round(d["bytes"] / d["launches"], 1)}
+
+    step_flops = sum(c["flops"] for c in classes.values()) / args.trace_steps
+    value = n / (ms_per_step / 1e3)
+    out = {
+        "metric": METRIC if args.workload == "c3" else f"ensemble {unit} ({args.workload})",
+        "value": round(value, 2),
+        "unit": unit,
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if precision == "bf16" else "f32",
+        "data": "synthetic (seeded inputs and random-init weights of the named architectures)",
+        "config": {"workload": desc, "global_batch": n, "mask": mask, "n_classes": C,
+                   "input": "int32 tokens [n, 256]" if tokens else "float32 NCHW images"},
+        "p50_ms": round(float(np.percentile(lat, 50)), 4),
+        "p99_ms": round(float(np.percentile(lat, 99)), 4),
+        "mfma_util_step": round(step_flops / (ms_per_step / 1e3) / 1e12 / PEAK_BF16_TFLOPS, 4)
+        if precision == "bf16" else None,
+        "alg_tflop_per_step": round(step_flops / 1e12, 4),
+        "roofline": roof,
+        "kernels": kernels,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(specs, params, batch, mask, args.cpu_seconds, unit)
+    ens.close()
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

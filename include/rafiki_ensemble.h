@@ -142,6 +142,36 @@ int rafiki_ensemble_model_logits(rafiki_ensemble_t h, int model, const void* bat
 /* Number of models and classes of a handle (host-side query). */
 int rafiki_ensemble_info(rafiki_ensemble_t h, int* n_models, int* n_classes, int* max_batch);
 
+/* Diagnostics: per-launch timing.  Kernel classes of rafiki_trace_rec.kind: */
+enum {
+  RAFIKI_K_CONV_MFMA = 0,      /* bf16 implicit-GEMM conv / FC / conv1d on matrix cores */
+  RAFIKI_K_SPLITK_REDUCE = 1,  /* ordered sum of split-K partials + epilogue */
+  RAFIKI_K_CONV_F32 = 2,       /* fp32 direct conv / FC */
+  RAFIKI_K_STAGE = 3,          /* NCHW fp32 -> NHWC input staging */
+  RAFIKI_K_POOL = 4,           /* max-pool, global average pool, max over time */
+  RAFIKI_K_EMBED = 5,          /* embedding gather */
+  RAFIKI_K_CONCAT = 6,         /* vector concatenation */
+  RAFIKI_K_COMBINE = 7         /* softmax + ensemble mean + argmax */
+};
+typedef struct {
+  int kind;                     /* RAFIKI_K_* */
+  int model, layer;             /* -1 for staging and combine */
+  double flops;                 /* algorithmic FLOPs (2 x unpadded MACs) of the launch */
+  double bytes;                 /* algorithmic bytes: each input, weight and output once */
+  float ms;                     /* elapsed time between HIP events recorded on the launch
+                                   stream immediately before and after the kernel */
+} rafiki_trace_rec;
+
+/* Enable (1) or disable (0) per-launch event timing of subsequent infer / model_logits
+ * calls on this handle; also discards unread records.  Tracing adds two event
+ * records per launch; it does not change results. */
+int rafiki_ensemble_trace(rafiki_ensemble_t h, int enable);
+
+/* Set *count to the number of traced launches.  If cap >= *count, wait for them, copy
+ * the records (in launch order) to `out` and discard them; otherwise copy nothing and
+ * keep them (call again with a larger buffer).  Host-blocking. */
+int rafiki_ensemble_trace_read(rafiki_ensemble_t h, rafiki_trace_rec* out, int cap, int* count);
+
 /* Synchronise the device, free everything the handle owns.  NULL is accepted. */
 int rafiki_ensemble_destroy(rafiki_ensemble_t h);
 

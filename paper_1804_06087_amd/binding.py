@@ -20,7 +20,9 @@ RAFIKI_OK, RAFIKI_ERR_INVALID, RAFIKI_ERR_UNSUPPORTED, RAFIKI_ERR_NOMEM, RAFIKI_
 RAFIKI_FP32, RAFIKI_BF16 = 0, 1
 RAFIKI_INPUT_IMAGE_NCHW_F32, RAFIKI_INPUT_TOKENS_I32 = 0, 1
 EXPORTED = ("rafiki_ensemble_create", "rafiki_ensemble_infer", "rafiki_ensemble_model_logits",
-            "rafiki_ensemble_info", "rafiki_ensemble_destroy", "rafiki_last_error")
+            "rafiki_ensemble_info", "rafiki_ensemble_trace", "rafiki_ensemble_trace_read",
+            "rafiki_ensemble_destroy", "rafiki_last_error")
+KERNEL_CLASSES = ("conv_mfma", "splitk_reduce", "conv_f32", "stage", "pool", "embed", "concat", "combine")
 
 _fp = C.POINTER(C.c_float)
 
@@ -39,6 +41,11 @@ class RafikiModelDesc(C.Structure):
 class RafikiOpts(C.Structure):
     _fields_ = [("input_kind", C.c_int), ("c", C.c_int), ("h", C.c_int), ("w", C.c_int), ("vocab", C.c_int),
                 ("precision", C.c_int), ("max_batch", C.c_int)]
+
+
+class RafikiTraceRec(C.Structure):
+    _fields_ = [("kind", C.c_int), ("model", C.c_int), ("layer", C.c_int), ("flops", C.c_double),
+                ("bytes", C.c_double), ("ms", C.c_float)]
 
 
 class RafikiError(RuntimeError):
@@ -65,9 +72,12 @@ def load_library(path: str = LIB_PATH):
     lib.rafiki_ensemble_model_logits.argtypes = [C.c_void_p, C.c_int, C.c_void_p, C.c_int, C.c_void_p, C.c_void_p]
     lib.rafiki_ensemble_info.argtypes = [C.c_void_p, C.POINTER(C.c_int), C.POINTER(C.c_int), C.POINTER(C.c_int)]
     lib.rafiki_ensemble_destroy.argtypes = [C.c_void_p]
+    lib.rafiki_ensemble_trace.argtypes = [C.c_void_p, C.c_int]
+    lib.rafiki_ensemble_trace_read.argtypes = [C.c_void_p, C.POINTER(RafikiTraceRec), C.c_int, C.POINTER(C.c_int)]
     lib.rafiki_last_error.restype = C.c_char_p
     for name in ("rafiki_ensemble_create", "rafiki_ensemble_infer", "rafiki_ensemble_model_logits",
-                 "rafiki_ensemble_info", "rafiki_ensemble_destroy"):
+                 "rafiki_ensemble_info", "rafiki_ensemble_destroy", "rafiki_ensemble_trace",
+                 "rafiki_ensemble_trace_read"):
         getattr(lib, name).restype = C.c_int
     _lib = lib
     return lib
@@ -164,6 +174,18 @@ class Ensemble:
     def model_logits(self, model: int, batch, n: int, out_logits, stream=None):
         _check(self._lib.rafiki_ensemble_model_logits(self._h, model, _ptr(batch), n, _ptr(out_logits),
                                                       _stream(stream)))
+
+    def trace(self, enable: bool):
+        _check(self._lib.rafiki_ensemble_trace(self._h, 1 if enable else 0))
+
+    def trace_read(self):
+        """List of dicts {kind, model, layer, flops, bytes, ms} for the traced launches."""
+        cnt = C.c_int(0)
+        _check(self._lib.rafiki_ensemble_trace_read(self._h, None, 0, C.byref(cnt)))
+        buf = (RafikiTraceRec * max(cnt.value, 1))()
+        _check(self._lib.rafiki_ensemble_trace_read(self._h, buf, cnt.value, C.byref(cnt)))
+        return [{"kind": KERNEL_CLASSES[r.kind], "model": r.model, "layer": r.layer, "flops": r.flops,
+                 "bytes": r.bytes, "ms": r.ms} for r in buf[:cnt.value]]
 
     def close(self):
         if getattr(self, "_h", None) is not None and self._h.value:

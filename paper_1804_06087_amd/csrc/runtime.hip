@@ -57,6 +57,7 @@ struct Op {
   // GEMM-like ops (conv2d, FC, conv1d)
   int H = 1, W = 1, Cs_in = 0, Ho = 1, Wo = 1, kh = 1, kw = 1, stride = 1, pad = 0, relu = 0;
   int K = 0, Kp = 0, Co_pad = 0, c_out = 0, bn = 128;
+  int cin_l = 0;        // logical input channels (algorithmic FLOP / byte counts)
   void* d_w = nullptr;
   float* d_scale = nullptr;
   float* d_shift = nullptr;
@@ -109,8 +110,30 @@ struct FreeList {
 
 }  // namespace
 
+// Opt-in per-launch timing: HIP events recorded on the launch stream around each
+// kernel, resolved by rafiki_ensemble_trace_read.
+struct Tracer {
+  bool on = false;
+  struct Rec { int kind, model, layer; double flops, bytes; hipEvent_t a, b; };
+  std::vector<Rec> recs;
+  std::vector<hipEvent_t> pool;
+  size_t used = 0;
+  hipEvent_t next() {
+    if (used == pool.size()) {
+      hipEvent_t ev = nullptr;
+      if (hipEventCreate(&ev) != hipSuccess) return nullptr;
+      pool.push_back(ev);
+    }
+    return pool[used++];
+  }
+  ~Tracer() {
+    for (hipEvent_t ev : pool) (void)hipEventDestroy(ev);
+  }
+};
+
 struct rafiki_ensemble_s {
   int n_models = 0, n_classes = 0, precision = 0, max_batch = 0;
+  mutable Tracer trace;
   int input_kind = 0, C = 0, H = 0, W = 0, vocab = 0, in_Cs = 0;
   int device = 0;
   bool dry = false;   // validation pass: shapes only, no packing, no device calls
@@ -254,6 +277,7 @@ int build_model(rafiki_ensemble_s* e, int mi, const rafiki_model_desc& md, Model
         op.kind = O_CONV;
         op.H = x.h; op.W = x.w; op.Cs_in = x.Cs; op.Ho = Ho; op.Wo = Wo;
         op.kh = L.kh; op.kw = L.kw; op.stride = L.stride; op.pad = L.pad; op.c_out = L.c_out;
+        op.cin_l = L.c_in;
         const int c_in = L.c_in, kh = L.kh, kw = L.kw;
         op.K = kh * kw * x.Cs;
         op.bn = bf ? choose_bn(L.c_out) : 32;
@@ -277,14 +301,14 @@ int build_model(rafiki_ensemble_s* e, int mi, const rafiki_model_desc& md, Model
         if (x.h + 2 * L.pad < L.kh || x.w + 2 * L.pad < L.kw || Ho < 1 || Wo < 1)
           return fail(RAFIKI_ERR_INVALID, ln + "maxpool output would be empty");
         y = x; y.h = Ho; y.w = Wo; y.off = 0; y.last_use = -1;
-        op.kind = O_MAXPOOL; op.H = x.h; op.W = x.w; op.Cs_in = x.Cs; op.Ho = Ho; op.Wo = Wo;
+        op.kind = O_MAXPOOL; op.H = x.h; op.W = x.w; op.Cs_in = x.Cs; op.Ho = Ho; op.Wo = Wo; op.cin_l = x.c;
         op.k = L.kh; op.stride = L.stride; op.pad = L.pad;
         break;
       }
       case RAFIKI_OP_GLOBAL_AVGPOOL: {
         if (x.kind != T_IMG) return fail(RAFIKI_ERR_INVALID, ln + "global average pool needs an image tensor");
         y.kind = T_VEC; y.c = x.c; y.h = 1; y.w = 1; y.Cs = x.Cs;
-        op.kind = O_GAP; op.H = x.h; op.W = x.w; op.Cs_in = x.Cs;
+        op.kind = O_GAP; op.H = x.h; op.W = x.w; op.Cs_in = x.Cs; op.cin_l = x.c;
         break;
       }
       case RAFIKI_OP_FC: {
@@ -296,6 +320,7 @@ int build_model(rafiki_ensemble_s* e, int mi, const rafiki_model_desc& md, Model
         op.kind = O_CONV;
         op.H = 1; op.W = 1; op.Cs_in = x.h * x.w * x.Cs; op.Ho = 1; op.Wo = 1;
         op.kh = op.kw = op.stride = 1; op.pad = 0; op.c_out = L.c_out;
+        op.cin_l = L.c_in;
         op.K = op.Cs_in;
         op.bn = bf ? choose_bn(L.c_out) : 32;
         op.Co_pad = round_up(L.c_out, op.bn);
@@ -320,7 +345,7 @@ int build_model(rafiki_ensemble_s* e, int mi, const rafiki_model_desc& md, Model
         if (L.c_in != e->vocab || L.c_out < 1 || !L.weight)
           return fail(RAFIKI_ERR_INVALID, ln + "embedding table must be [vocab, dim]");
         y.kind = T_SEQ; y.c = L.c_out; y.h = 1; y.w = x.w; y.Cs = round_up(L.c_out, 8);
-        op.kind = O_EMBED; op.Cs_in = y.Cs; op.W = x.w;
+        op.kind = O_EMBED; op.Cs_in = y.Cs; op.W = x.w; op.cin_l = L.c_out;
         if (e->dry) break;
         std::vector<float> packed((size_t)L.c_in * y.Cs, 0.f);
         for (int r = 0; r < L.c_in; ++r)
@@ -336,6 +361,7 @@ int build_model(rafiki_ensemble_s* e, int mi, const rafiki_model_desc& md, Model
         op.kind = O_CONV1D;
         op.H = 1; op.W = x.w; op.Cs_in = x.Cs; op.Ho = 1; op.Wo = x.w - L.kw + 1;
         op.kh = 1; op.kw = L.kw; op.stride = 1; op.pad = 0; op.c_out = L.c_out;
+        op.cin_l = L.c_in;
         op.K = L.kw * x.Cs;
         op.bn = bf ? choose_bn(L.c_out) : 32;
         op.Co_pad = round_up(L.c_out, op.bn);
@@ -429,9 +455,32 @@ const void* tptr(const rafiki_ensemble_s* e, const Model& M, int id, const void*
     if (st_ != hipSuccess) return fail(RAFIKI_ERR_HIP, std::string(#expr) + ": " + hipGetErrorString(st_)); \
   } while (0)
 
-int run_gemm(const rafiki_ensemble_s* e, const Op& op, ConvArgs a, hipStream_t s) {
+// Launch `expr` on stream s; when tracing, bracket it with events and record the
+// launch's algorithmic FLOPs and bytes.
+#define TRACED(e, s, kind, model, layer, flops, bytes, expr)                                  \
+  do {                                                                                        \
+    hipEvent_t ta_ = nullptr, tb_ = nullptr;                                                  \
+    if ((e)->trace.on) {                                                                      \
+      ta_ = (e)->trace.next();                                                                \
+      tb_ = (e)->trace.next();                                                                \
+      if (ta_) (void)hipEventRecord(ta_, s);                                                  \
+    }                                                                                         \
+    HIPCHK(expr);                                                                             \
+    if (ta_ && tb_) {                                                                         \
+      (void)hipEventRecord(tb_, s);                                                           \
+      (e)->trace.recs.push_back({kind, model, layer, (double)(flops), (double)(bytes), ta_, tb_}); \
+    }                                                                                         \
+  } while (0)
+
+int run_gemm(const rafiki_ensemble_s* e, const Op& op, ConvArgs a, hipStream_t s, int mi = -1, int li = -1) {
+  const double es = (double)e->esz();
+  const double kalg = (double)op.kh * op.kw * op.cin_l;
+  const double flops = 2.0 * a.M * op.c_out * kalg;
+  const double in_elems = (double)a.N * a.H * a.W * op.cin_l;   // FC: H = W = 1, cin_l = flattened size
+  const double bytes = in_elems * es + (double)op.c_out * kalg * es +
+                       (double)a.M * op.c_out * (a.out_f32 ? 4.0 : es) * (a.res ? 2.0 : 1.0);
   if (e->precision != RAFIKI_BF16) {
-    HIPCHK(launch_conv_f32(a, s));
+    TRACED(e, s, RAFIKI_K_CONV_F32, mi, li, flops, bytes, launch_conv_f32(a, s));
     return RAFIKI_OK;
   }
   const int bm = choose_bm(a.M);
@@ -442,10 +491,12 @@ int run_gemm(const rafiki_ensemble_s* e, const Op& op, ConvArgs a, hipStream_t s
     if ((size_t)splits * a.M * a.Co_pad * 4 > e->partial_bytes)
       return fail(RAFIKI_ERR_INVALID, "internal: split-K workspace too small");
     a.partial = e->d_partial;
-    HIPCHK(launch_conv_bf16(a, bm, op.bn, splits, s));
-    HIPCHK(launch_splitk_reduce(a, splits, 1, s));
+    TRACED(e, s, RAFIKI_K_CONV_MFMA, mi, li, flops, bytes, launch_conv_bf16(a, bm, op.bn, splits, s));
+    TRACED(e, s, RAFIKI_K_SPLITK_REDUCE, mi, li, 0.0,
+           (double)splits * a.M * a.c_write * 4.0 + (double)a.M * a.c_write * (a.out_f32 ? 4.0 : es),
+           launch_splitk_reduce(a, splits, 1, s));
   } else {
-    HIPCHK(launch_conv_bf16(a, bm, op.bn, 1, s));
+    TRACED(e, s, RAFIKI_K_CONV_MFMA, mi, li, flops, bytes, launch_conv_bf16(a, bm, op.bn, 1, s));
   }
   return RAFIKI_OK;
 }
@@ -454,7 +505,9 @@ int run_gemm(const rafiki_ensemble_s* e, const Op& op, ConvArgs a, hipStream_t s
 int run_model(const rafiki_ensemble_s* e, int mi, const void* batch, int n, float* logits, hipStream_t s) {
   const Model& M = e->models[mi];
   const int bf = e->precision == RAFIKI_BF16 ? 1 : 0;
+  const double es = (double)e->esz();
   for (const Op& op : M.ops) {
+    const int li = op.out;
     const Tensor& y = M.tensors[op.out];
     void* yp = y.is_logits ? (void*)logits : (void*)(M.d_arena + y.off);
     const void* xp = tptr(e, M, op.in, batch);
@@ -471,31 +524,37 @@ int run_model(const rafiki_ensemble_s* e, int mi, const void* batch, int n, floa
         if (op.kind == O_CONV1D) {
           void* tmp = M.d_arena + op.tmp_off;
           a.y = tmp; a.c_write = round_up(op.c_out, 8); a.ldy = a.c_write; a.out_f32 = bf ? 0 : 1;
-          int rc = run_gemm(e, op, a, s);
+          int rc = run_gemm(e, op, a, s, mi, li);
           if (rc) return rc;
-          HIPCHK(launch_spatial_reduce(tmp, yp, n, op.Wo, y.Cs, 1, bf, s));
+          TRACED(e, s, RAFIKI_K_POOL, mi, li, 0.0, (double)n * op.Wo * op.c_out * es + (double)n * op.c_out * es,
+                 launch_spatial_reduce(tmp, yp, n, op.Wo, y.Cs, 1, bf, s));
           break;
         }
         a.y = yp;
         if (y.is_logits) { a.c_write = y.c; a.ldy = y.c; a.out_f32 = 1; }
         else { a.c_write = y.Cs; a.ldy = y.Cs; a.out_f32 = bf ? 0 : 1; }
-        int rc = run_gemm(e, op, a, s);
+        int rc = run_gemm(e, op, a, s, mi, li);
         if (rc) return rc;
         break;
       }
       case O_MAXPOOL:
-        HIPCHK(launch_maxpool(xp, yp, n, op.H, op.W, op.Cs_in, op.Ho, op.Wo, op.k, op.stride, op.pad, bf, s));
+        TRACED(e, s, RAFIKI_K_POOL, mi, li, 0.0,
+               ((double)op.H * op.W + (double)op.Ho * op.Wo) * n * op.cin_l * es,
+               launch_maxpool(xp, yp, n, op.H, op.W, op.Cs_in, op.Ho, op.Wo, op.k, op.stride, op.pad, bf, s));
         break;
       case O_GAP:
-        HIPCHK(launch_spatial_reduce(xp, yp, n, op.H * op.W, op.Cs_in, 0, bf, s));
+        TRACED(e, s, RAFIKI_K_POOL, mi, li, 0.0, ((double)op.H * op.W + 1.0) * n * op.cin_l * es,
+               launch_spatial_reduce(xp, yp, n, op.H * op.W, op.Cs_in, 0, bf, s));
         break;
       case O_EMBED:
-        HIPCHK(launch_embed_gather((const int32_t*)batch, op.d_w, yp, n, op.W, op.Cs_in, bf, s));
+        TRACED(e, s, RAFIKI_K_EMBED, mi, li, 0.0, (double)n * op.W * (4.0 + 2.0 * op.cin_l * es),
+               launch_embed_gather((const int32_t*)batch, op.d_w, yp, n, op.W, op.Cs_in, bf, s));
         break;
       case O_CONCAT: {
         const Tensor& a = M.tensors[op.in];
         const Tensor& b = M.tensors[op.in2];
-        HIPCHK(launch_concat(xp, op.ca, a.Cs, tptr(e, M, op.in2, batch), op.cb, b.Cs, yp, y.Cs, n, bf, s));
+        TRACED(e, s, RAFIKI_K_CONCAT, mi, li, 0.0, 2.0 * n * (op.ca + op.cb) * es,
+               launch_concat(xp, op.ca, a.Cs, tptr(e, M, op.in2, batch), op.cb, b.Cs, yp, y.Cs, n, bf, s));
         break;
       }
     }
@@ -513,7 +572,8 @@ int check_call(const rafiki_ensemble_s* h, const void* batch, int n) {
 
 int stage(const rafiki_ensemble_s* e, const void* batch, int n, hipStream_t s) {
   if (e->input_kind != RAFIKI_INPUT_IMAGE_NCHW_F32) return RAFIKI_OK;
-  HIPCHK(launch_stage_images((const float*)batch, e->d_staged, n, e->C, e->H, e->W, e->in_Cs,
+  TRACED(e, s, RAFIKI_K_STAGE, -1, -1, 0.0, (double)n * e->C * e->H * e->W * (4.0 + (double)e->esz()),
+         launch_stage_images((const float*)batch, e->d_staged, n, e->C, e->H, e->W, e->in_Cs,
                              e->precision == RAFIKI_BF16, s));
   return RAFIKI_OK;
 }
@@ -610,7 +670,8 @@ int rafiki_ensemble_infer(rafiki_ensemble_t h, const void* batch, int n, uint32_
     if (rc) return rc;
     ca.sel[ca.S++] = m;
   }
-  HIPCHK(launch_combine(ca, s));
+  TRACED(h, s, RAFIKI_K_COMBINE, -1, -1, 0.0, (double)n * h->n_classes * 4.0 * (ca.S + 1) + 4.0 * n,
+         launch_combine(ca, s));
   return RAFIKI_OK;
 }
 
@@ -639,6 +700,34 @@ int rafiki_ensemble_destroy(rafiki_ensemble_t h) {
   hipError_t st = hipDeviceSynchronize();
   delete h;
   if (st != hipSuccess) return fail(RAFIKI_ERR_HIP, std::string("hipDeviceSynchronize: ") + hipGetErrorString(st));
+  return RAFIKI_OK;
+}
+
+int rafiki_ensemble_trace(rafiki_ensemble_t h, int enable) {
+  if (!h) return fail(RAFIKI_ERR_INVALID, "null handle");
+  h->trace.on = enable != 0;
+  h->trace.recs.clear();
+  h->trace.used = 0;
+  return RAFIKI_OK;
+}
+
+int rafiki_ensemble_trace_read(rafiki_ensemble_t h, rafiki_trace_rec* out, int cap, int* count) {
+  if (!h || !count || (cap > 0 && !out)) return fail(RAFIKI_ERR_INVALID, "null argument");
+  const int total = (int)h->trace.recs.size();
+  *count = total;
+  if (cap < total) return RAFIKI_OK;   // too small: keep the records, report the count
+  for (int i = 0; i < total; ++i) {
+    const auto& r = h->trace.recs[i];
+    hipError_t st = hipEventSynchronize(r.b);
+    if (st != hipSuccess) return fail(RAFIKI_ERR_HIP, std::string("hipEventSynchronize: ") + hipGetErrorString(st));
+    float ms = 0.f;
+    st = hipEventElapsedTime(&ms, r.a, r.b);
+    if (st != hipSuccess) return fail(RAFIKI_ERR_HIP, std::string("hipEventElapsedTime: ") + hipGetErrorString(st));
+    out[i].kind = r.kind; out[i].model = r.model; out[i].layer = r.layer;
+    out[i].flops = r.flops; out[i].bytes = r.bytes; out[i].ms = ms;
+  }
+  h->trace.recs.clear();
+  h->trace.used = 0;
   return RAFIKI_OK;
 }
 
