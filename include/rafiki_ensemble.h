@@ -130,7 +130,11 @@ int rafiki_ensemble_create(const rafiki_model_desc* models, int n_models,
  * out_labels[i] = lowest class index attaining the maximum of out_probs[i, :].
  * `batch` follows opts.input_kind; out_probs is fp32 [n, n_classes] row-major;
  * out_labels is int32 [n].  Requires 1 <= n <= max_batch, mask != 0 and no bit at
- * position >= n_models (else RAFIKI_ERR_INVALID).  Enqueue-only on `stream`. */
+ * position >= n_models (else RAFIKI_ERR_INVALID).  Enqueue-only on `stream`, except
+ * that the first call (infer or model_logits) with a given n blocks while it times
+ * the candidate tile configurations of every layer on `stream` (set the environment
+ * variable RAFIKI_AUTOTUNE=0 to use fixed defaults instead).  The choice never
+ * changes a result: every candidate sums each output in the same order. */
 int rafiki_ensemble_infer(rafiki_ensemble_t h, const void* batch, int n, uint32_t model_subset_mask,
                           float* out_probs, int32_t* out_labels, void* stream);
 

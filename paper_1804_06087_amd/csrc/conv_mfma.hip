@@ -1,0 +1,411 @@
+// bf16 implicit-GEMM convolution / FC on gfx950 matrix cores, direct-to-LDS pipeline.
+//
+// GEMM view: out[m, co] = sum_k X[m, k] * Wp[co, k]; m = output pixel (n, ho, wo),
+// co = output channel, k = (u, v, ci) kernel tap and input channel.  X is gathered
+// on the fly from the NHWC input: a 16-byte chunk of a tile row is 8 consecutive
+// channels of one tap.
+//
+// Tiles move HBM -> LDS with buffer_load_dwordx4 ... lds (no register staging).  A
+// lane whose chunk lies outside the image or past K gets an offset beyond the
+// buffer's num_records, for which the hardware writes zeros: that is the zero
+// padding.  STAGES K tiles of 64 are in flight in an LDS ring, laid out with the
+// bank-conflict-free swizzle described at swz().  Each wave computes a (BM/WM) x (BN/WN) sub-tile with
+// v_mfma_f32_32x32x16_bf16 (weights = A operand, pixels = B operand), so a lane ends
+// with runs of 4 consecutive channels of one pixel.  Fused epilogue: fp32 scale /
+// shift (folded batch-norm + bias), residual, ReLU, bf16 store; or fp32 output;
+// or raw fp32 split-K partials.
+#include "kernels.h"
+
+namespace rafiki {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef __attribute__((address_space(3))) void lds_void;
+
+__device__ __forceinline__ float bf2f_m(uint32_t b16) { return __uint_as_float(b16 << 16); }
+__device__ __forceinline__ uint32_t f2bf_m(float f) {   // nearest, ties to even (finite)
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+
+// s_waitcnt with only the vector-memory counter constrained (gfx9 encoding).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+// LDS tile layout: row r (128 bytes = 8 chunks of 16 bytes) keeps logical chunk c in
+// slot c ^ swz(r), swz(r) = (r & 7) ^ ((r >> 3) & 1).  A 16-byte fragment read
+// serves 16 lanes at a time across 64 four-byte banks; its 16 lanes read 16
+// consecutive rows of one chunk, and swz keeps (r % 2, slot) distinct over any 16
+// rows, so the reads are bank-conflict free.
+__device__ __forceinline__ int swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
+
+// Per-thread state of the HBM -> LDS tile loader.  Wave w's load instruction j
+// fills tile rows (j * NW + w) * 8 .. +8 (64 chunks, lane l -> slot l % 8 of row
+// l / 8 of the group).  With NW even, that row's swz is (l / 8) ^ (w & 1) for every
+// j, so lane l always carries chunk (l % 8) ^ (l / 8) ^ (w & 1).
+//
+// ALIGNED (Cs % 64 == 0): K is ordered (channel block of 64, tap, channel), so K
+// tile gk is channel block gk / taps at tap gk % taps.  The taps of one channel
+// block are consecutive tiles: they re-read the same input rows while those are
+// still in L2.  Tap and channel block are wave-uniform and advanced incrementally;
+// per row only the image-bounds test and one add remain.  Otherwise (Cs % 64 != 0)
+// K is ordered (tap, channel) and each lane decodes its own (u, v, ci) with
+// multiply-high division.
+template <int BM, int BN, int NW, bool ALIGNED>
+struct Loader {
+  static constexpr int RA = BM / (8 * NW);
+  static constexpr int RB = BN / (8 * NW);
+  static constexpr int STAGE_CHUNKS = (BM + BN) * 8;
+  __amdgpu_buffer_rsrc_t xr, wr;
+  unsigned oob;
+  int chunk, wave, kt_begin;
+  int a_img[RA], a_hi[RA], a_wi[RA];   // general path: image base pixel, top-left input coords
+  int a_off[RA];                       // aligned path: byte offset of (hi0, wi0, chunk) (may be virtual)
+  unsigned b_off[RB];
+  int nu, nv, ntap, ncb;               // aligned path: tap (u, v, index) and channel block of the next tile
+
+  __device__ __forceinline__ void init(const ConvArgs& a, int m0, int n0, int wave_, int lane, int kt_begin_) {
+    wave = wave_;
+    kt_begin = kt_begin_;
+    const int lrow = lane >> 3;
+    chunk = (lane & 7) ^ lrow ^ (wave & 1);
+    xr = __builtin_amdgcn_make_buffer_rsrc((void*)a.x, (short)0, a.x_bytes, 0x00020000);
+    wr = __builtin_amdgcn_make_buffer_rsrc((void*)a.w, (short)0, a.w_bytes, 0x00020000);
+    oob = (unsigned)a.x_bytes;   // offset at num_records: the hardware returns zeros
+    const int HoWo = a.Ho * a.Wo;
+#pragma unroll
+    for (int j = 0; j < RA; ++j) {
+      const int m = m0 + (j * NW + wave) * 8 + lrow;
+      if (m < a.M) {
+        const int n = m / HoWo, r = m - n * HoWo;
+        const int ho = r / a.Wo, wo = r - ho * a.Wo;
+        a_img[j] = n * a.H * a.W;
+        a_hi[j] = ho * a.stride - a.pad;
+        a_wi[j] = wo * a.stride - a.pad;
+      } else {
+        a_img[j] = 0;
+        a_hi[j] = -(1 << 28);
+        a_wi[j] = 0;
+      }
+      a_off[j] = ((a_img[j] + a_hi[j] * a.W + a_wi[j]) * a.Cs + chunk * 8) * 2;
+    }
+#pragma unroll
+    for (int j = 0; j < RB; ++j)
+      b_off[j] = (unsigned)(((n0 + (j * NW + wave) * 8 + lrow) * a.Kp + chunk * 8) * 2);
+    if (ALIGNED) {
+      const int taps = a.kh * a.kw;
+      ncb = kt_begin / taps;
+      ntap = kt_begin - ncb * taps;
+      nu = ntap / a.kw;
+      nv = ntap - nu * a.kw;
+    }
+  }
+
+  // Issue the loads of K tile kt (relative to the split's first tile) into LDS stage
+  // `stage`.  Tiles must be issued in increasing kt order (the aligned path advances).
+  __device__ __forceinline__ void issue(const ConvArgs& a, uint4* lds, int kt, int stage) {
+    const int gk = kt_begin + kt;
+    uint4* sbase = lds + stage * STAGE_CHUNKS;
+    if (ALIGNED) {
+      const bool kvalid = gk * 64 < a.K;   // tiles past K (padding to Kp) read zeros
+      const int delta = ((nu * a.W + nv) * a.Cs + ncb * 64) * 2;
+#pragma unroll
+      for (int j = 0; j < RA; ++j) {
+        const int hi = a_hi[j] + nu, wi = a_wi[j] + nv;
+        const bool ok = kvalid && (unsigned)hi < (unsigned)a.H && (unsigned)wi < (unsigned)a.W;
+        const unsigned off = ok ? (unsigned)(a_off[j] + delta) : oob;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (lds_void*)(sbase + (j * NW + wave) * 64), 16, off, 0, 0, 0);
+      }
+      if (++ntap == a.kh * a.kw) {
+        ntap = 0; nu = 0; nv = 0; ++ncb;
+      } else if (++nv == a.kw) {
+        nv = 0; ++nu;
+      }
+    } else {
+      const unsigned k8 = (unsigned)(gk * 8 + chunk);
+      const unsigned tap = a.mag_cs8 ? __umulhi(k8, a.mag_cs8) : k8;
+      const int ci = (int)(k8 - tap * a.Cs8) * 8;
+      const unsigned u = a.mag_kw ? __umulhi(tap, a.mag_kw) : tap;
+      const int v = (int)(tap - u * a.kw);
+      const bool kvalid = (int)k8 < a.K8;
+#pragma unroll
+      for (int j = 0; j < RA; ++j) {
+        const int hi = a_hi[j] + (int)u, wi = a_wi[j] + v;
+        const bool ok = kvalid && (unsigned)hi < (unsigned)a.H && (unsigned)wi < (unsigned)a.W;
+        const unsigned off = ok ? (unsigned)((a_img[j] + hi * a.W + wi) * a.Cs + ci) * 2u : oob;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (lds_void*)(sbase + (j * NW + wave) * 64), 16, off, 0, 0, 0);
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < RB; ++j)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(wr, (lds_void*)(sbase + BM * 8 + (j * NW + wave) * 64), 16,
+                                               b_off[j], gk * 128, 0, 0);
+  }
+};
+
+// Wait until at most `n` tiles' loads (of `per` instructions each) are outstanding.
+template <int PER, int MAXN>
+__device__ __forceinline__ void wait_tiles(int n) {
+  if (MAXN >= 2 && n >= 2) wait_vmcnt<(MAXN >= 2 ? 2 * PER : 0)>();
+  else if (MAXN >= 1 && n >= 1) wait_vmcnt<(MAXN >= 1 ? PER : 0)>();
+  else wait_vmcnt<0>();
+}
+
+template <int BM, int BN, int WM, int WN, int STAGES, bool ALIGNED>
+__global__ __launch_bounds__(WM * WN * 64) void conv_mfma_kernel(ConvArgs a) {
+  constexpr int NW = WM * WN;
+  constexpr int WTM = BM / WM, WTN = BN / WN;      // wave tile: pixels x channels
+  constexpr int TM = WTM / 32, TN = WTN / 32;
+  using LoaderT = Loader<BM, BN, NW, ALIGNED>;
+  constexpr int PER = LoaderT::RA + LoaderT::RB;   // load instructions per thread per tile
+  constexpr int STAGE_CHUNKS = (BM + BN) * 8;      // 16-byte chunks per stage
+  static_assert(TM >= 1 && TN >= 1 && LoaderT::RA >= 1 && LoaderT::RB >= 1, "tile shape");
+  static_assert(NW % 2 == 0, "the loader's chunk assignment assumes an even wave count");
+  static_assert(STAGE_CHUNKS * 16 * STAGES <= 160 * 1024, "LDS budget");
+  static_assert(STAGES >= 2 && STAGES <= 4 && (STAGES - 2) * PER < 64, "pipeline depth");
+
+  __shared__ uint4 lds[STAGES * STAGE_CHUNKS];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave % WM, wn = wave / WM;
+  // Workgroups are dealt round-robin to the 8 XCDs (block b -> XCD b % 8).  Renumber
+  // so that each XCD owns a contiguous range of output tiles, walked with the channel
+  // tile fastest: the tiles sharing an input tile then run close together on one XCD
+  // and read it through that XCD's L2 once.
+  const int G = gridDim.x, b = blockIdx.x;
+  const int q = G >> 3, r8 = G & 7, xcd = b & 7, loc = b >> 3;
+  const int tile = (xcd < r8 ? xcd * (q + 1) : r8 * (q + 1) + (xcd - r8) * q) + loc;
+  const int nt = tile % a.n_tiles, mt = tile / a.n_tiles;
+  const int m0 = mt * BM, n0 = nt * BN;
+  const int ktiles = a.Kp / 64;
+  const int kt_begin = blockIdx.y * a.kt_per_split;
+  const int nk = min(a.kt_per_split, ktiles - kt_begin);
+
+  LoaderT ld;
+  ld.init(a, m0, n0, wave, lane, kt_begin);
+
+  f32x16 acc[TN][TM];
+#pragma unroll
+  for (int i = 0; i < TN; ++i)
+#pragma unroll
+    for (int j = 0; j < TM; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+  const int frow = lane & 31, fk = lane >> 5;
+  // Fragment reads: row r of a tile, 16-byte chunk kc (k-step s covers chunks 2s, 2s+1).
+  auto frag = [&](const uint4* base, int r, int kc) { return __builtin_bit_cast(bf16x8, base[r * 8 + (kc ^ swz(r))]); };
+
+  if (nk > 0) {
+#pragma unroll
+    for (int s = 0; s < STAGES; ++s)
+      if (s < nk) ld.issue(a, lds, s, s);
+    wait_tiles<PER, STAGES - 1>(min(STAGES, nk) - 1);
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+  }
+
+  bf16x8 xf[2][TM], wf[2][TN];
+  if (nk > 0) {
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm) xf[0][tm] = frag(lds, wm * WTM + tm * 32 + frow, fk);
+#pragma unroll
+    for (int tn = 0; tn < TN; ++tn) wf[0][tn] = frag(lds + BM * 8, wn * WTN + tn * 32 + frow, fk);
+  }
+
+  for (int kt = 0; kt < nk; ++kt) {
+    const int cur = kt % STAGES;
+    const uint4* As = lds + cur * STAGE_CHUNKS;
+    const uint4* Bs = As + BM * 8;
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      const int b = s & 1;
+      if (s < 3) {
+        // prefetch the fragments of k-step s + 1 of this tile; the scheduling fence
+        // keeps these reads ahead of the MFMAs below, so their latency overlaps them
+#pragma unroll
+        for (int tm = 0; tm < TM; ++tm) xf[b ^ 1][tm] = frag(As, wm * WTM + tm * 32 + frow, 2 * (s + 1) + fk);
+#pragma unroll
+        for (int tn = 0; tn < TN; ++tn) wf[b ^ 1][tn] = frag(Bs, wn * WTN + tn * 32 + frow, 2 * (s + 1) + fk);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn)
+#pragma unroll
+        for (int tm = 0; tm < TM; ++tm)
+          acc[tn][tm] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[b][tn], xf[b][tm], acc[tn][tm], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    // All of this tile's fragment reads have completed (their MFMAs consumed them).
+    // Wait for tile kt + 1, then let every wave pass: stage `cur` is free for tile
+    // kt + STAGES and tile kt + 1 is visible to all.
+    if (kt + 1 < nk) {
+      asm volatile("" ::: "memory");
+      wait_tiles<PER, STAGES - 2>(min(STAGES - 2, nk - 2 - kt));
+      __builtin_amdgcn_s_barrier();
+      asm volatile("" ::: "memory");
+      if (kt + STAGES < nk) ld.issue(a, lds, kt + STAGES, cur);
+      const uint4* An = lds + ((kt + 1) % STAGES) * STAGE_CHUNKS;
+#pragma unroll
+      for (int tm = 0; tm < TM; ++tm) xf[0][tm] = frag(An, wm * WTM + tm * 32 + frow, fk);
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn) wf[0][tn] = frag(An + BM * 8, wn * WTN + tn * 32 + frow, fk);
+    }
+  }
+
+  // ---- epilogue: lane holds channels n0 + wn*WTN + tn*32 + 8g + 4*fk + j of pixel
+  //      m0 + wm*WTM + tm*32 + frow (g, j in 0..3).
+  const bool split = gridDim.y > 1;
+#pragma unroll
+  for (int tn = 0; tn < TN; ++tn) {
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const int c = n0 + wn * WTN + tn * 32 + 8 * g + 4 * fk;
+      if (split) {
+#pragma unroll
+        for (int tm = 0; tm < TM; ++tm) {
+          const int m = m0 + wm * WTM + tm * 32 + frow;
+          if (m < a.M) {
+            float4 v = make_float4(acc[tn][tm][4 * g + 0], acc[tn][tm][4 * g + 1], acc[tn][tm][4 * g + 2],
+                                   acc[tn][tm][4 * g + 3]);
+            *(float4*)(a.partial + ((long long)blockIdx.y * a.M + m) * a.Co_pad + c) = v;
+          }
+        }
+        continue;
+      }
+      if (c >= a.c_write) continue;
+      const float4 sc = *(const float4*)(a.scale + c);
+      const float4 sh = *(const float4*)(a.shift + c);
+#pragma unroll
+      for (int tm = 0; tm < TM; ++tm) {
+        const int m = m0 + wm * WTM + tm * 32 + frow;
+        if (m >= a.M) continue;
+        float v0 = acc[tn][tm][4 * g + 0] * sc.x + sh.x;
+        float v1 = acc[tn][tm][4 * g + 1] * sc.y + sh.y;
+        float v2 = acc[tn][tm][4 * g + 2] * sc.z + sh.z;
+        float v3 = acc[tn][tm][4 * g + 3] * sc.w + sh.w;
+        const long long o = (long long)m * a.ldy + c;
+        if (a.res) {
+          const uint2 r = *(const uint2*)((const bf16_t*)a.res + o);
+          v0 += bf2f_m(r.x & 0xFFFFu);
+          v1 += bf2f_m(r.x >> 16);
+          v2 += bf2f_m(r.y & 0xFFFFu);
+          v3 += bf2f_m(r.y >> 16);
+        }
+        if (a.relu) {
+          v0 = fmaxf(v0, 0.f); v1 = fmaxf(v1, 0.f); v2 = fmaxf(v2, 0.f); v3 = fmaxf(v3, 0.f);
+        }
+        if (a.out_f32) {
+          float* y = (float*)a.y + o;
+          y[0] = v0;
+          if (c + 1 < a.c_write) y[1] = v1;
+          if (c + 2 < a.c_write) y[2] = v2;
+          if (c + 3 < a.c_write) y[3] = v3;
+        } else {
+          uint2 q;
+          q.x = f2bf_m(v0) | (f2bf_m(v1) << 16);
+          q.y = f2bf_m(v2) | (f2bf_m(v3) << 16);
+          *(uint2*)((bf16_t*)a.y + o) = q;
+        }
+      }
+    }
+  }
+}
+
+template <int BM, int BN, int WM, int WN, int STAGES>
+static hipError_t launch_mfma_cfg(const ConvArgs& a, int splits, hipStream_t s) {
+  ConvArgs b = a;
+  b.n_tiles = (a.Nc + BN - 1) / BN;
+  const int m_tiles = (a.M + BM - 1) / BM;
+  dim3 grid(m_tiles * b.n_tiles, splits);
+  if (a.Cs % 64 == 0)
+    hipLaunchKernelGGL((conv_mfma_kernel<BM, BN, WM, WN, STAGES, true>), grid, dim3(WM * WN * 64), 0, s, b);
+  else
+    hipLaunchKernelGGL((conv_mfma_kernel<BM, BN, WM, WN, STAGES, false>), grid, dim3(WM * WN * 64), 0, s, b);
+  return hipGetLastError();
+}
+
+// Sum the split-K partials in split order, then the same epilogue as the GEMM kernel.
+// One thread per (row, 4-channel group).
+__global__ void splitk_reduce_kernel(ConvArgs a, int splits, int in_bf16) {
+  const int groups = (a.c_write + 3) / 4;
+  const long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (long long)a.M * groups) return;
+  const int m = (int)(idx / groups);
+  const int c = (int)(idx - (long long)m * groups) * 4;
+  float4 s = *(const float4*)(a.partial + (long long)m * a.Co_pad + c);
+  for (int z = 1; z < splits; ++z) {
+    const float4 t = *(const float4*)(a.partial + ((long long)z * a.M + m) * a.Co_pad + c);
+    s.x += t.x; s.y += t.y; s.z += t.z; s.w += t.w;
+  }
+  const float4 sc = *(const float4*)(a.scale + c);
+  const float4 sh = *(const float4*)(a.shift + c);
+  float v[4] = {s.x * sc.x + sh.x, s.y * sc.y + sh.y, s.z * sc.z + sh.z, s.w * sc.w + sh.w};
+  const long long o = (long long)m * a.ldy + c;
+  if (a.res) {
+    for (int j = 0; j < 4; ++j) {
+      if (c + j >= a.c_write) break;
+      if (in_bf16) v[j] += bf2f_m(((const bf16_t*)a.res)[o + j]);
+      else v[j] += ((const float*)a.res)[o + j];
+    }
+  }
+  for (int j = 0; j < 4; ++j) {
+    if (c + j >= a.c_write) break;
+    float t = a.relu ? fmaxf(v[j], 0.f) : v[j];
+    if (a.out_f32) ((float*)a.y)[o + j] = t;
+    else ((bf16_t*)a.y)[o + j] = (bf16_t)f2bf_m(t);
+  }
+}
+
+// Tile configurations: id, BM x BN, waves WM x WN, pipeline stages.  Each kernel is
+// instantiated explicitly (the host pass does not always emit the launch stub of an
+// implicitly instantiated kernel template).
+#define RAFIKI_MFMA_CONFIGS(X)                                                        \
+  X(0, 256, 256, 4, 2, 2)  /* 8 waves, wave 64x128, two stages */                    \
+  X(1, 256, 256, 2, 4, 2)  /* 8 waves, wave 128x64, two stages */                    \
+  X(2, 256, 128, 2, 4, 3)  /* 8 waves, wave 128x32 */                                \
+  X(3, 128, 256, 2, 4, 3)  /* 8 waves, wave 64x64 */                                 \
+  X(4, 256, 128, 2, 2, 2)  /* wave 128x64, two stages */                             \
+  X(5, 128, 128, 2, 2, 3)  /* wave 64x64 */                                          \
+  X(6, 64, 128, 1, 4, 3)   /* wave 64x32 */                                          \
+  X(7, 128, 64, 2, 2, 3)   /* wave 64x32 */                                          \
+  X(8, 64, 64, 2, 2, 3)    /* wave 32x32 */                                          \
+  X(9, 32, 128, 1, 4, 3)   /* wave 32x32 */                                          \
+  X(10, 128, 32, 4, 1, 3)  /* wave 32x32 */                                          \
+  X(11, 256, 64, 4, 1, 3)  /* wave 64x64 */
+
+#define RAFIKI_CFG_ENTRY(id, BM, BN, WM, WN, ST) {BM, BN, WM * WN, ST},
+const MfmaConfig kMfmaConfigs[kNumMfmaConfigs] = {RAFIKI_MFMA_CONFIGS(RAFIKI_CFG_ENTRY)};
+#undef RAFIKI_CFG_ENTRY
+
+#define RAFIKI_INSTANTIATE(id, BM, BN, WM, WN, ST)                              \
+  template __global__ void conv_mfma_kernel<BM, BN, WM, WN, ST, true>(ConvArgs); \
+  template __global__ void conv_mfma_kernel<BM, BN, WM, WN, ST, false>(ConvArgs);
+RAFIKI_MFMA_CONFIGS(RAFIKI_INSTANTIATE)
+#undef RAFIKI_INSTANTIATE
+
+hipError_t launch_conv_mfma(const ConvArgs& a, int cfg, int splits, hipStream_t s) {
+  switch (cfg) {
+#define RAFIKI_CASE(id, BM, BN, WM, WN, ST) \
+    case id: return launch_mfma_cfg<BM, BN, WM, WN, ST>(a, splits, s);
+    RAFIKI_MFMA_CONFIGS(RAFIKI_CASE)
+#undef RAFIKI_CASE
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_splitk_reduce(const ConvArgs& a, int splits, int in_bf16, hipStream_t s) {
+  const long long total = (long long)a.M * ((a.c_write + 3) / 4);
+  const int threads = 256;
+  const long long blocks = (total + threads - 1) / threads;
+  hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)blocks), dim3(threads), 0, s, a, splits, in_bf16);
+  return hipGetLastError();
+}
+
+}  // namespace rafiki

@@ -23,17 +23,26 @@ struct ConvArgs {
   int N, H, W, Cs;      // input geometry; Cs = storage channels (multiple of 8)
   int Ho, Wo, kh, kw, stride, pad;
   int M, K, Kp, Co_pad; // M = N*Ho*Wo; K = kh*kw*Cs; Kp = K rounded up to the K tile
+  int Nc;               // output channels computed (tiles cover ceil(Nc / BN) * BN <= Co_pad rows)
   int c_write;          // channels written per row (<= Co_pad)
   int ldy;              // row stride of y and res, in elements
   int relu;
   int out_f32;          // y is fp32 (bf16 kernels); fp32 kernels always write fp32
   int kt_per_split;     // K tiles per split (splits = gridDim.y)
   int n_tiles;          // channel tiles per row of the output tile grid
+  // direct-to-LDS kernel: buffer sizes (bytes, < 2^31) and K decoding
+  int x_bytes, w_bytes;
+  int Cs8, K8;          // Cs / 8, K / 8
+  unsigned mag_cs8;     // floor(x / Cs8) = umulhi(x, mag_cs8) (0 when Cs8 == 1)
+  unsigned mag_kw;      // floor(x / kw)  = umulhi(x, mag_kw)  (0 when kw == 1)
 };
 
-// bf16 MFMA kernel family; bm, bn in {32, 64, 128}.  Returns hipSuccess or the
-// launch error.  splits > 1 writes partial sums; finish with splitk_reduce.
-hipError_t launch_conv_bf16(const ConvArgs& a, int bm, int bn, int splits, hipStream_t s);
+// Direct-to-LDS pipelined bf16 MFMA kernel; cfg selects the tile configuration
+// (kMfmaConfigs).  splits > 1 writes partial sums; finish with splitk_reduce.
+struct MfmaConfig { int bm, bn, waves, stages; };
+constexpr int kNumMfmaConfigs = 12;
+extern const MfmaConfig kMfmaConfigs[kNumMfmaConfigs];
+hipError_t launch_conv_mfma(const ConvArgs& a, int cfg, int splits, hipStream_t s);
 hipError_t launch_splitk_reduce(const ConvArgs& a, int splits, int in_bf16, hipStream_t s);
 // fp32 direct kernel (CUDA-core style FMA loops; used by the fp32 precision mode).
 hipError_t launch_conv_f32(const ConvArgs& a, hipStream_t s);

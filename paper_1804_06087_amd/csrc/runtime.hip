@@ -12,6 +12,8 @@
 #include <algorithm>
 #include <cmath>
 #include <cstring>
+#include <cstdlib>
+#include <map>
 #include <memory>
 #include <string>
 #include <vector>
@@ -56,7 +58,7 @@ struct Op {
   int in = -1, in2 = -1, out = -1;
   // GEMM-like ops (conv2d, FC, conv1d)
   int H = 1, W = 1, Cs_in = 0, Ho = 1, Wo = 1, kh = 1, kw = 1, stride = 1, pad = 0, relu = 0;
-  int K = 0, Kp = 0, Co_pad = 0, c_out = 0, bn = 128;
+  int K = 0, Kp = 0, Co_pad = 0, c_out = 0;
   int cin_l = 0;        // logical input channels (algorithmic FLOP / byte counts)
   void* d_w = nullptr;
   float* d_scale = nullptr;
@@ -143,6 +145,9 @@ struct rafiki_ensemble_s {
   float* d_partial = nullptr;
   size_t partial_bytes = 0;
   std::vector<void*> allocs;
+  // Tuned tile configuration per batch size, model and op (-1: not a GEMM op).
+  std::map<int, std::vector<std::vector<int>>> tuned;
+  bool autotune = true;
   size_t esz() const { return precision == RAFIKI_BF16 ? 2 : 4; }
   ~rafiki_ensemble_s() {
     for (void* p : allocs) (void)hipFree(p);
@@ -174,30 +179,48 @@ int upload(rafiki_ensemble_s* e, void** dst, const void* src, size_t bytes) {
   return RAFIKI_OK;
 }
 
-// Tile choices of the bf16 MFMA kernel.
-int choose_bn(int c_out) { return c_out <= 32 ? 32 : (c_out <= 64 ? 64 : 128); }
-int choose_bm(int M) { return M <= 32 ? 32 : (M <= 64 ? 64 : 128); }
-// Split K when the output tile grid alone cannot fill the 256 compute units.
-int choose_splits(int M, int bm, int n_tiles, int ktiles) {
-  const int tiles = ((M + bm - 1) / bm) * n_tiles;
+// bf16 GEMM tiling.  Weight rows are padded to 256 so every tile configuration fits.
+constexpr int kCoPadBf16 = 256;
+
+// Configurations whose channel tile suits c_out (at most one partly used tile row).
+bool cfg_fits(int cfg, int c_out) {
+  const int bn = kMfmaConfigs[cfg].bn;
+  if (c_out <= 32) return bn == 32;
+  if (c_out <= 64) return bn <= 64;
+  return bn <= round_up(c_out, 64) && bn >= 64;
+}
+// Split K when the output tile grid of the smallest tiles cannot fill the 256
+// compute units.  Depends only on the GEMM shape, so results do not depend on tuning.
+int choose_splits(int M, int c_out, int ktiles) {
+  const int tiles = ((M + 63) / 64) * ((c_out + 127) / 128);
   if (tiles >= 256) return 1;
   int s = std::min((512 + tiles - 1) / tiles, ktiles / 4);
   s = std::max(1, std::min(s, 64));
   const int per = (ktiles + s - 1) / s;
   return (ktiles + per - 1) / per;
 }
+// Fixed tile of split-K launches.
+int split_cfg(int c_out) { return c_out <= 32 ? 10 : (c_out <= 64 ? 8 : 6); }
+// Untuned default: the 64-pixel tiles are the most robust across shapes.
+int default_cfg(int c_out) { return c_out <= 32 ? 10 : (c_out <= 64 ? 8 : 6); }
 
-// Pack a GEMM-like weight into [Co_pad][Kp] with K index (u, v, ci) over Cs_in
-// storage channels.  `src_index(co, ci, u, v)` gives the canonical flat index.
+// Pack a GEMM-like weight into [Co_pad][Kp] over Cs_in storage channels.  K order:
+// (channel block of 64, tap, channel) when Cs_in % 64 == 0 (the kernel's aligned
+// path), else (tap, channel).  `src_index(co, ci, u, v)` gives the canonical flat index.
 template <class F>
 std::vector<float> pack_weight(int c_out, int c_in, int kh, int kw, int Cs_in, int Co_pad, int Kp, F src_index,
                                const float* w) {
   std::vector<float> out((size_t)Co_pad * Kp, 0.f);
+  const bool aligned = Cs_in % 64 == 0;
+  const int taps = kh * kw;
   for (int co = 0; co < c_out; ++co)
     for (int u = 0; u < kh; ++u)
       for (int v = 0; v < kw; ++v)
-        for (int ci = 0; ci < c_in; ++ci)
-          out[(size_t)co * Kp + (size_t)(u * kw + v) * Cs_in + ci] = w[src_index(co, ci, u, v)];
+        for (int ci = 0; ci < c_in; ++ci) {
+          const int tap = u * kw + v;
+          const size_t k = aligned ? ((size_t)(ci / 64) * taps + tap) * 64 + ci % 64 : (size_t)tap * Cs_in + ci;
+          out[(size_t)co * Kp + k] = w[src_index(co, ci, u, v)];
+        }
   return out;
 }
 
@@ -280,8 +303,7 @@ int build_model(rafiki_ensemble_s* e, int mi, const rafiki_model_desc& md, Model
         op.cin_l = L.c_in;
         const int c_in = L.c_in, kh = L.kh, kw = L.kw;
         op.K = kh * kw * x.Cs;
-        op.bn = bf ? choose_bn(L.c_out) : 32;
-        op.Co_pad = round_up(L.c_out, op.bn);
+        op.Co_pad = bf ? round_up(L.c_out, kCoPadBf16) : round_up(L.c_out, 32);
         op.Kp = bf ? round_up(op.K, 64) : op.K;
         if (e->dry) break;
         auto packed = pack_weight(L.c_out, c_in, kh, kw, x.Cs, op.Co_pad, op.Kp,
@@ -322,8 +344,7 @@ int build_model(rafiki_ensemble_s* e, int mi, const rafiki_model_desc& md, Model
         op.kh = op.kw = op.stride = 1; op.pad = 0; op.c_out = L.c_out;
         op.cin_l = L.c_in;
         op.K = op.Cs_in;
-        op.bn = bf ? choose_bn(L.c_out) : 32;
-        op.Co_pad = round_up(L.c_out, op.bn);
+        op.Co_pad = bf ? round_up(L.c_out, kCoPadBf16) : round_up(L.c_out, 32);
         op.Kp = bf ? round_up(op.K, 64) : op.K;
         if (e->dry) break;
         const int xc = x.c, xh = x.h, xw = x.w, xCs = x.Cs, cin = L.c_in;
@@ -363,8 +384,7 @@ int build_model(rafiki_ensemble_s* e, int mi, const rafiki_model_desc& md, Model
         op.kh = 1; op.kw = L.kw; op.stride = 1; op.pad = 0; op.c_out = L.c_out;
         op.cin_l = L.c_in;
         op.K = L.kw * x.Cs;
-        op.bn = bf ? choose_bn(L.c_out) : 32;
-        op.Co_pad = round_up(L.c_out, op.bn);
+        op.Co_pad = bf ? round_up(L.c_out, kCoPadBf16) : round_up(L.c_out, 32);
         op.Kp = bf ? round_up(op.K, 64) : op.K;
         if (e->dry) break;
         const int cin = L.c_in, kw = L.kw;
@@ -436,13 +456,14 @@ size_t partial_need(const rafiki_ensemble_s* e) {
       if (op.kind != O_CONV && op.kind != O_CONV1D) continue;
       for (int n = 1; n <= e->max_batch; ++n) {
         const int Mrows = n * op.Ho * op.Wo;
-        const int bm = choose_bm(Mrows);
-        const int s = choose_splits(Mrows, bm, op.Co_pad / op.bn, op.Kp / 64);
+        const int s = choose_splits(Mrows, op.c_out, op.Kp / 64);
         if (s > 1) need = std::max(need, (size_t)s * Mrows * op.Co_pad * 4);
       }
     }
   return need;
 }
+
+unsigned magic_div(int d) { return d == 1 ? 0u : (unsigned)((((unsigned long long)1 << 32) + d - 1) / d); }
 
 const void* tptr(const rafiki_ensemble_s* e, const Model& M, int id, const void* batch) {
   if (id < 0) return e->input_kind == RAFIKI_INPUT_IMAGE_NCHW_F32 ? e->d_staged : batch;
@@ -472,7 +493,7 @@ const void* tptr(const rafiki_ensemble_s* e, const Model& M, int id, const void*
     }                                                                                         \
   } while (0)
 
-int run_gemm(const rafiki_ensemble_s* e, const Op& op, ConvArgs a, hipStream_t s, int mi = -1, int li = -1) {
+int run_gemm(const rafiki_ensemble_s* e, const Op& op, ConvArgs a, hipStream_t s, int mi, int li, int cfg) {
   const double es = (double)e->esz();
   const double kalg = (double)op.kh * op.kw * op.cin_l;
   const double flops = 2.0 * a.M * op.c_out * kalg;
@@ -483,27 +504,109 @@ int run_gemm(const rafiki_ensemble_s* e, const Op& op, ConvArgs a, hipStream_t s
     TRACED(e, s, RAFIKI_K_CONV_F32, mi, li, flops, bytes, launch_conv_f32(a, s));
     return RAFIKI_OK;
   }
-  const int bm = choose_bm(a.M);
+  if ((long long)a.N * a.H * a.W * a.Cs * 2 >= (1LL << 31) || (long long)a.Co_pad * a.Kp * 2 >= (1LL << 31))
+    return fail(RAFIKI_ERR_UNSUPPORTED, "a layer's input or weights exceed 2 GiB; use a smaller max_batch");
+  if (cfg < 0) cfg = default_cfg(op.c_out);
   const int ktiles = a.Kp / 64;
-  const int splits = choose_splits(a.M, bm, op.Co_pad / op.bn, ktiles);
+  const int splits = choose_splits(a.M, op.c_out, ktiles);
   a.kt_per_split = (ktiles + splits - 1) / splits;
   if (splits > 1) {
     if ((size_t)splits * a.M * a.Co_pad * 4 > e->partial_bytes)
       return fail(RAFIKI_ERR_INVALID, "internal: split-K workspace too small");
     a.partial = e->d_partial;
-    TRACED(e, s, RAFIKI_K_CONV_MFMA, mi, li, flops, bytes, launch_conv_bf16(a, bm, op.bn, splits, s));
+    TRACED(e, s, RAFIKI_K_CONV_MFMA, mi, li, flops, bytes, launch_conv_mfma(a, split_cfg(op.c_out), splits, s));
     TRACED(e, s, RAFIKI_K_SPLITK_REDUCE, mi, li, 0.0,
            (double)splits * a.M * a.c_write * 4.0 + (double)a.M * a.c_write * (a.out_f32 ? 4.0 : es),
            launch_splitk_reduce(a, splits, 1, s));
   } else {
-    TRACED(e, s, RAFIKI_K_CONV_MFMA, mi, li, flops, bytes, launch_conv_bf16(a, bm, op.bn, 1, s));
+    TRACED(e, s, RAFIKI_K_CONV_MFMA, mi, li, flops, bytes, launch_conv_mfma(a, cfg, 1, s));
   }
+  return RAFIKI_OK;
+}
+
+// Kernel arguments of a GEMM-like op over n requests (output pointer set by the caller).
+ConvArgs gemm_args(const rafiki_ensemble_s* e, const Model& M, const Op& op, int n, const void* batch) {
+  ConvArgs a{};
+  a.x = tptr(e, M, op.in, batch); a.w = op.d_w; a.scale = op.d_scale; a.shift = op.d_shift;
+  a.res = op.in2 >= 0 ? tptr(e, M, op.in2, batch) : nullptr;
+  a.N = n; a.H = op.H; a.W = op.W; a.Cs = op.Cs_in;
+  a.Ho = op.Ho; a.Wo = op.Wo; a.kh = op.kh; a.kw = op.kw; a.stride = op.stride; a.pad = op.pad;
+  a.M = n * op.Ho * op.Wo; a.K = op.K; a.Kp = op.Kp; a.Co_pad = op.Co_pad; a.Nc = op.c_out;
+  a.relu = op.relu;
+  a.x_bytes = (int)((long long)n * op.H * op.W * op.Cs_in * (long long)e->esz());
+  a.w_bytes = (int)((long long)op.Co_pad * op.Kp * (long long)e->esz());
+  a.Cs8 = op.Cs_in / 8; a.K8 = op.K / 8;
+  a.mag_cs8 = magic_div(op.Cs_in / 8); a.mag_kw = magic_div(op.kw);
+  return a;
+}
+
+// Choose each GEMM op's tile configuration for batch size n by timing the candidates
+// on stream s (once per n; blocks the caller).  Only unsplit launches are tuned: all
+// of them sum K in the same order, so the choice never changes a result.
+int tune(rafiki_ensemble_s* e, int n, const void* batch, hipStream_t s) {
+  if (e->tuned.count(n)) return RAFIKI_OK;
+  std::vector<std::vector<int>> choice(e->models.size());
+  hipEvent_t ev[2] = {nullptr, nullptr};
+  const bool timing = e->autotune && e->precision == RAFIKI_BF16;
+  if (timing) {
+    HIPCHK(hipEventCreate(&ev[0]));
+    HIPCHK(hipEventCreate(&ev[1]));
+  }
+  int rc = RAFIKI_OK;
+  for (size_t mi = 0; mi < e->models.size() && rc == RAFIKI_OK; ++mi) {
+    const Model& M = e->models[mi];
+    choice[mi].assign(M.ops.size(), -1);
+    for (size_t oi = 0; oi < M.ops.size(); ++oi) {
+      const Op& op = M.ops[oi];
+      if (op.kind != O_CONV && op.kind != O_CONV1D) continue;
+      choice[mi][oi] = default_cfg(op.c_out);
+      if (!timing) continue;
+      ConvArgs a = gemm_args(e, M, op, n, batch);
+      if (choose_splits(a.M, op.c_out, a.Kp / 64) > 1) continue;
+      if ((long long)a.N * a.H * a.W * a.Cs * 2 >= (1LL << 31) || (long long)a.Co_pad * a.Kp * 2 >= (1LL << 31))
+        continue;   // run_gemm rejects these shapes
+      // scratch output: the op's own arena slot, or the model's logits slot
+      const Tensor& y = M.tensors[op.out];
+      a.y = y.is_logits ? (void*)(e->d_logits + mi * (size_t)e->max_batch * e->n_classes)
+                        : (void*)(op.kind == O_CONV1D ? M.d_arena + op.tmp_off : M.d_arena + y.off);
+      a.c_write = y.is_logits ? y.c : (op.kind == O_CONV1D ? round_up(op.c_out, 8) : y.Cs);
+      a.ldy = a.c_write;
+      a.out_f32 = y.is_logits ? 1 : 0;
+      a.kt_per_split = a.Kp / 64;
+      float best = 1e30f;
+      for (int cfg = 0; cfg < kNumMfmaConfigs; ++cfg) {
+        if (!cfg_fits(cfg, op.c_out)) continue;
+        if (kMfmaConfigs[cfg].bm > 2 * round_up(a.M, 32)) continue;
+        float t = 0.f;
+        for (int rep = 0; rep < 3; ++rep) {   // first launch warms caches; keep the best of two
+          if (hipEventRecord(ev[0], s) != hipSuccess || launch_conv_mfma(a, cfg, 1, s) != hipSuccess ||
+              hipEventRecord(ev[1], s) != hipSuccess || hipEventSynchronize(ev[1]) != hipSuccess) {
+            rc = fail(RAFIKI_ERR_HIP, "tile tuning launch failed");
+            break;
+          }
+          float ms = 0.f;
+          (void)hipEventElapsedTime(&ms, ev[0], ev[1]);
+          if (rep == 1 || (rep == 2 && ms < t)) t = ms;
+        }
+        if (rc) break;
+        if (t < best) { best = t; choice[mi][oi] = cfg; }
+      }
+      if (rc) break;
+    }
+  }
+  if (ev[0]) (void)hipEventDestroy(ev[0]);
+  if (ev[1]) (void)hipEventDestroy(ev[1]);
+  if (rc) return rc;
+  e->tuned[n] = std::move(choice);
   return RAFIKI_OK;
 }
 
 // Forward pass of model `mi` over n requests; logits [n][n_classes] to `logits`.
 int run_model(const rafiki_ensemble_s* e, int mi, const void* batch, int n, float* logits, hipStream_t s) {
   const Model& M = e->models[mi];
+  const auto it = e->tuned.find(n);
+  const std::vector<int> empty;
+  const std::vector<int>& cfgs = it == e->tuned.end() ? empty : it->second[mi];
   const int bf = e->precision == RAFIKI_BF16 ? 1 : 0;
   const double es = (double)e->esz();
   for (const Op& op : M.ops) {
@@ -514,17 +617,12 @@ int run_model(const rafiki_ensemble_s* e, int mi, const void* batch, int n, floa
     switch (op.kind) {
       case O_CONV:
       case O_CONV1D: {
-        ConvArgs a{};
-        a.x = xp; a.w = op.d_w; a.scale = op.d_scale; a.shift = op.d_shift;
-        a.res = op.in2 >= 0 ? tptr(e, M, op.in2, batch) : nullptr;
-        a.N = n; a.H = op.H; a.W = op.W; a.Cs = op.Cs_in;
-        a.Ho = op.Ho; a.Wo = op.Wo; a.kh = op.kh; a.kw = op.kw; a.stride = op.stride; a.pad = op.pad;
-        a.M = n * op.Ho * op.Wo; a.K = op.K; a.Kp = op.Kp; a.Co_pad = op.Co_pad;
-        a.relu = op.relu;
+        ConvArgs a = gemm_args(e, M, op, n, batch);
+        const int cfg = cfgs.empty() ? -1 : cfgs[&op - M.ops.data()];
         if (op.kind == O_CONV1D) {
           void* tmp = M.d_arena + op.tmp_off;
           a.y = tmp; a.c_write = round_up(op.c_out, 8); a.ldy = a.c_write; a.out_f32 = bf ? 0 : 1;
-          int rc = run_gemm(e, op, a, s, mi, li);
+          int rc = run_gemm(e, op, a, s, mi, li, cfg);
           if (rc) return rc;
           TRACED(e, s, RAFIKI_K_POOL, mi, li, 0.0, (double)n * op.Wo * op.c_out * es + (double)n * op.c_out * es,
                  launch_spatial_reduce(tmp, yp, n, op.Wo, y.Cs, 1, bf, s));
@@ -533,7 +631,7 @@ int run_model(const rafiki_ensemble_s* e, int mi, const void* batch, int n, floa
         a.y = yp;
         if (y.is_logits) { a.c_write = y.c; a.ldy = y.c; a.out_f32 = 1; }
         else { a.c_write = y.Cs; a.ldy = y.Cs; a.out_f32 = bf ? 0 : 1; }
-        int rc = run_gemm(e, op, a, s, mi, li);
+        int rc = run_gemm(e, op, a, s, mi, li, cfg);
         if (rc) return rc;
         break;
       }
@@ -609,6 +707,7 @@ int rafiki_ensemble_create(const rafiki_model_desc* models, int n_models, const 
   e->C = opts->c; e->H = opts->h; e->W = opts->w; e->vocab = opts->vocab;
   if (e->input_kind == RAFIKI_INPUT_TOKENS_I32) { e->C = 1; e->W = 1; }
   e->in_Cs = round_up(e->C, 8);
+  if (const char* t = std::getenv("RAFIKI_AUTOTUNE")) e->autotune = std::atoi(t) != 0;
   // Pass 1: validate every model and infer shapes without touching the device.
   e->dry = true;
   e->models.resize(n_models);
@@ -659,6 +758,7 @@ int rafiki_ensemble_infer(rafiki_ensemble_t h, const void* batch, int n, uint32_
     return fail(RAFIKI_ERR_INVALID, "model_subset_mask selects a model that does not exist");
   hipStream_t s = (hipStream_t)stream;
   rc = stage(h, batch, n, s);
+  if (!rc) rc = tune(h, n, batch, s);
   if (rc) return rc;
   CombineArgs ca{};
   ca.logits = h->d_logits;
@@ -683,6 +783,7 @@ int rafiki_ensemble_model_logits(rafiki_ensemble_t h, int model, const void* bat
   if (model < 0 || model >= h->n_models) return fail(RAFIKI_ERR_INVALID, "model index out of range");
   hipStream_t s = (hipStream_t)stream;
   rc = stage(h, batch, n, s);
+  if (!rc) rc = tune(h, n, batch, s);
   if (rc) return rc;
   return run_model(h, model, batch, n, out_logits, s);
 }
