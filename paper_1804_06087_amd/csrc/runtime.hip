@@ -76,6 +76,10 @@ struct Model {
   std::vector<Tensor> tensors;
   char* d_arena = nullptr;
   size_t arena_bytes = 0;
+  float* d_partial = nullptr;     // split-K partial sums (per model: models may run concurrently)
+  size_t partial_bytes = 0;
+  hipStream_t stream = nullptr;   // the model's own stream for concurrent ensembles
+  hipEvent_t done = nullptr;      // recorded on `stream` after the model's last kernel
 };
 
 struct FreeList {
@@ -142,14 +146,19 @@ struct rafiki_ensemble_s {
   std::vector<Model> models;
   void* d_staged = nullptr;
   float* d_logits = nullptr;
-  float* d_partial = nullptr;
-  size_t partial_bytes = 0;
+  hipEvent_t staged_ev = nullptr;   // recorded on the caller's stream after staging
+  bool concurrent = true;           // run selected models on their own streams
   std::vector<void*> allocs;
   // Tuned tile configuration per batch size, model and op (-1: not a GEMM op).
   std::map<int, std::vector<std::vector<int>>> tuned;
   bool autotune = true;
   size_t esz() const { return precision == RAFIKI_BF16 ? 2 : 4; }
   ~rafiki_ensemble_s() {
+    for (Model& M : models) {
+      if (M.done) (void)hipEventDestroy(M.done);
+      if (M.stream) (void)hipStreamDestroy(M.stream);
+    }
+    if (staged_ev) (void)hipEventDestroy(staged_ev);
     for (void* p : allocs) (void)hipFree(p);
   }
 };
@@ -447,19 +456,18 @@ int build_model(rafiki_ensemble_s* e, int mi, const rafiki_model_desc& md, Model
   return dev_alloc(e, (void**)&M.d_arena, M.arena_bytes);
 }
 
-// Largest split-K partial buffer any GEMM-like op needs for n in [1, max_batch].
-size_t partial_need(const rafiki_ensemble_s* e) {
+// Largest split-K partial buffer any GEMM-like op of model M needs for n in [1, max_batch].
+size_t partial_need(const rafiki_ensemble_s* e, const Model& M) {
   if (e->precision != RAFIKI_BF16) return 0;
   size_t need = 0;
-  for (const Model& M : e->models)
-    for (const Op& op : M.ops) {
-      if (op.kind != O_CONV && op.kind != O_CONV1D) continue;
-      for (int n = 1; n <= e->max_batch; ++n) {
-        const int Mrows = n * op.Ho * op.Wo;
-        const int s = choose_splits(Mrows, op.c_out, op.Kp / 64);
-        if (s > 1) need = std::max(need, (size_t)s * Mrows * op.Co_pad * 4);
-      }
+  for (const Op& op : M.ops) {
+    if (op.kind != O_CONV && op.kind != O_CONV1D) continue;
+    for (int n = 1; n <= e->max_batch; ++n) {
+      const int Mrows = n * op.Ho * op.Wo;
+      const int s = choose_splits(Mrows, op.c_out, op.Kp / 64);
+      if (s > 1) need = std::max(need, (size_t)s * Mrows * op.Co_pad * 4);
     }
+  }
   return need;
 }
 
@@ -511,9 +519,10 @@ int run_gemm(const rafiki_ensemble_s* e, const Op& op, ConvArgs a, hipStream_t s
   const int splits = choose_splits(a.M, op.c_out, ktiles);
   a.kt_per_split = (ktiles + splits - 1) / splits;
   if (splits > 1) {
-    if ((size_t)splits * a.M * a.Co_pad * 4 > e->partial_bytes)
+    const Model& Mo = e->models[mi];
+    if ((size_t)splits * a.M * a.Co_pad * 4 > Mo.partial_bytes)
       return fail(RAFIKI_ERR_INVALID, "internal: split-K workspace too small");
-    a.partial = e->d_partial;
+    a.partial = Mo.d_partial;
     TRACED(e, s, RAFIKI_K_CONV_MFMA, mi, li, flops, bytes, launch_conv_mfma(a, split_cfg(op.c_out), splits, s));
     TRACED(e, s, RAFIKI_K_SPLITK_REDUCE, mi, li, 0.0,
            (double)splits * a.M * a.c_write * 4.0 + (double)a.M * a.c_write * (a.out_f32 ? 4.0 : es),
@@ -708,6 +717,7 @@ int rafiki_ensemble_create(const rafiki_model_desc* models, int n_models, const 
   if (e->input_kind == RAFIKI_INPUT_TOKENS_I32) { e->C = 1; e->W = 1; }
   e->in_Cs = round_up(e->C, 8);
   if (const char* t = std::getenv("RAFIKI_AUTOTUNE")) e->autotune = std::atoi(t) != 0;
+  if (const char* t = std::getenv("RAFIKI_MODEL_STREAMS")) e->concurrent = std::atoi(t) != 0;
   // Pass 1: validate every model and infer shapes without touching the device.
   e->dry = true;
   e->models.resize(n_models);
@@ -738,10 +748,19 @@ int rafiki_ensemble_create(const rafiki_model_desc* models, int n_models, const 
   }
   rc = dev_alloc(e.get(), (void**)&e->d_logits, (size_t)n_models * e->max_batch * n_classes * 4);
   if (rc) return rc;
-  e->partial_bytes = partial_need(e.get());
-  if (e->partial_bytes) {
-    rc = dev_alloc(e.get(), (void**)&e->d_partial, e->partial_bytes);
-    if (rc) return rc;
+  for (Model& M : e->models) {
+    M.partial_bytes = partial_need(e.get(), M);
+    if (M.partial_bytes) {
+      rc = dev_alloc(e.get(), (void**)&M.d_partial, M.partial_bytes);
+      if (rc) return rc;
+    }
+    hipError_t st2 = hipStreamCreateWithFlags(&M.stream, hipStreamNonBlocking);
+    if (st2 == hipSuccess) st2 = hipEventCreateWithFlags(&M.done, hipEventDisableTiming);
+    if (st2 != hipSuccess) return fail(RAFIKI_ERR_HIP, std::string("stream/event creation: ") + hipGetErrorString(st2));
+  }
+  {
+    hipError_t st2 = hipEventCreateWithFlags(&e->staged_ev, hipEventDisableTiming);
+    if (st2 != hipSuccess) return fail(RAFIKI_ERR_HIP, std::string("event creation: ") + hipGetErrorString(st2));
   }
   *out = e.release();
   g_err.clear();
@@ -764,12 +783,24 @@ int rafiki_ensemble_infer(rafiki_ensemble_t h, const void* batch, int n, uint32_
   ca.logits = h->d_logits;
   ca.ld_model = (long long)h->max_batch * h->n_classes;
   ca.n = n; ca.C = h->n_classes; ca.probs = out_probs; ca.labels = out_labels;
-  for (int m = 0; m < h->n_models; ++m) {
-    if (!((model_subset_mask >> m) & 1u)) continue;
-    rc = run_model(h, m, batch, n, h->d_logits + (size_t)m * ca.ld_model, s);
+  for (int m = 0; m < h->n_models; ++m)
+    if ((model_subset_mask >> m) & 1u) ca.sel[ca.S++] = m;
+  // Selected models are independent until the combine: fork them onto their own
+  // streams after staging and join before the combine (sequential when tracing, so
+  // that each traced kernel has the GPU to itself).
+  const bool fork = h->concurrent && !h->trace.on && ca.S > 1;
+  if (fork) HIPCHK(hipEventRecord(h->staged_ev, s));
+  for (int i = 0; i < ca.S; ++i) {
+    const int m = ca.sel[i];
+    Model& M = h->models[m];
+    hipStream_t ms = fork ? M.stream : s;
+    if (fork) HIPCHK(hipStreamWaitEvent(ms, h->staged_ev, 0));
+    rc = run_model(h, m, batch, n, h->d_logits + (size_t)m * ca.ld_model, ms);
     if (rc) return rc;
-    ca.sel[ca.S++] = m;
+    if (fork) HIPCHK(hipEventRecord(M.done, ms));
   }
+  if (fork)
+    for (int i = 0; i < ca.S; ++i) HIPCHK(hipStreamWaitEvent(s, h->models[ca.sel[i]].done, 0));
   TRACED(h, s, RAFIKI_K_COMBINE, -1, -1, 0.0, (double)n * h->n_classes * 4.0 * (ca.S + 1) + 4.0 * n,
          launch_combine(ca, s));
   return RAFIKI_OK;

@@ -193,6 +193,19 @@ def test_c3_full_batch_sampled_rows(c3_ens):
         label_check(lab[ridx], p_ref)
 
 
+def test_c3_concurrent_models_match_single_model_runs(c3_ens):
+    """Selected models run concurrently on their own streams inside infer; the
+    ensemble must equal the combine of each model's logits computed alone."""
+    cfg, specs, params, batch, ze, zb = _c3()
+    n, C = 64, 1000
+    zs = [run_logits(c3_ens, batch, n, m, C).astype(np.float64) for m in range(3)]
+    for _ in range(2):
+        p, lab = run_infer(c3_ens, batch, n, 0b111, C)
+        p_ref = oracle.combine_mean([oracle.softmax(z) for z in zs])
+        assert np.abs(p - p_ref).max() <= 1e-6
+        assert np.array_equal(lab, oracle.argmax_first(p))
+
+
 @pytest.mark.parametrize("n", [1, 4, 16, 64, 256])
 def test_c4_sweep(c3_ens, n):
     cfg, specs, params, batch, ze, zb = _c3()
