@@ -259,62 +259,93 @@ __global__ __launch_bounds__(WM * WN * 64) void conv_mfma_kernel(ConvArgs a) {
     }
   }
 
-  // ---- epilogue: lane holds channels n0 + wn*WTN + tn*32 + 8g + 4*fk + j of pixel
-  //      m0 + wm*WTM + tm*32 + frow (g, j in 0..3).
-  const bool split = gridDim.y > 1;
+  // ---- epilogue.  Lane (frow, fk) holds, for each (tn, tm), channels
+  // n0 + wn*WTN + tn*32 + 8g + 4fk + j (g, j in 0..3) of pixel m0 + wm*WTM + tm*32 + frow.
+  if (gridDim.y > 1) {
+    // split-K: raw fp32 partial sums, 16-byte stores
 #pragma unroll
-  for (int tn = 0; tn < TN; ++tn) {
+    for (int tn = 0; tn < TN; ++tn)
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      const int c = n0 + wn * WTN + tn * 32 + 8 * g + 4 * fk;
-      if (split) {
+      for (int g = 0; g < 4; ++g) {
+        const int c = n0 + wn * WTN + tn * 32 + 8 * g + 4 * fk;
 #pragma unroll
         for (int tm = 0; tm < TM; ++tm) {
           const int m = m0 + wm * WTM + tm * 32 + frow;
-          if (m < a.M) {
-            float4 v = make_float4(acc[tn][tm][4 * g + 0], acc[tn][tm][4 * g + 1], acc[tn][tm][4 * g + 2],
-                                   acc[tn][tm][4 * g + 3]);
-            *(float4*)(a.partial + ((long long)blockIdx.y * a.M + m) * a.Co_pad + c) = v;
-          }
+          if (m < a.M)
+            *(float4*)(a.partial + ((long long)blockIdx.y * a.M + m) * a.Co_pad + c) =
+                make_float4(acc[tn][tm][4 * g + 0], acc[tn][tm][4 * g + 1], acc[tn][tm][4 * g + 2],
+                            acc[tn][tm][4 * g + 3]);
+        }
+      }
+    return;
+  }
+  // Each wave transposes its tile through a private LDS region, 32 channels at a
+  // time: the fp32 values acc * scale + shift go to LDS as [pixel][32 channels]
+  // (16-byte chunks swizzled by swz(pixel)); each lane then reads 8 channels of one
+  // pixel back, adds the residual (16-byte load), applies ReLU, rounds to bf16 and
+  // writes 16 bytes.  The residual add and the single rounding match the direct form.
+  static_assert(NW * WTM * 32 * 4 <= STAGES * STAGE_CHUNKS * 16, "epilogue staging fits in the LDS ring");
+  __syncthreads();   // every wave is done with the ring
+  float4* stg = (float4*)lds + wave * (WTM * 8);
+  const int oq = lane & 3, pl = lane >> 2;   // read phase: channel octet oq of pixel pl (+16 per pass)
+#pragma unroll
+  for (int tn = 0; tn < TN; ++tn) {
+    const int cb = n0 + wn * WTN + tn * 32;   // first channel of this 32-channel group
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const int cl = 8 * g + 4 * fk;          // local channel of this lane's 4 values
+      const float4 sc = *(const float4*)(a.scale + cb + cl);
+      const float4 sh = *(const float4*)(a.shift + cb + cl);
+#pragma unroll
+      for (int tm = 0; tm < TM; ++tm) {
+        const int p = tm * 32 + frow;
+        stg[p * 8 + ((cl >> 2) ^ swz(p))] =
+            make_float4(acc[tn][tm][4 * g + 0] * sc.x + sh.x, acc[tn][tm][4 * g + 1] * sc.y + sh.y,
+                        acc[tn][tm][4 * g + 2] * sc.z + sh.z, acc[tn][tm][4 * g + 3] * sc.w + sh.w);
+      }
+    }
+    __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): this wave's LDS writes have landed
+    __builtin_amdgcn_wave_barrier();
+    const int c = cb + 8 * oq;
+#pragma unroll
+    for (int pass = 0; pass < WTM / 16; ++pass) {
+      const int p = pass * 16 + pl;
+      const int m = m0 + wm * WTM + p;
+      const float4 lo = stg[p * 8 + ((2 * oq) ^ swz(p))];
+      const float4 hi = stg[p * 8 + ((2 * oq + 1) ^ swz(p))];
+      float v[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+      if (m >= a.M || c >= a.c_write) continue;
+      const long long o = (long long)m * a.ldy + c;
+      if (a.out_f32) {   // fp32 rows (logits): any row stride, element stores
+        float* y = (float*)a.y + o;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          if (c + j >= a.c_write) break;
+          float t = v[j] + (a.res ? bf2f_m(((const bf16_t*)a.res)[o + j]) : 0.f);
+          y[j] = a.relu ? fmaxf(t, 0.f) : t;
         }
         continue;
       }
-      if (c >= a.c_write) continue;
-      const float4 sc = *(const float4*)(a.scale + c);
-      const float4 sh = *(const float4*)(a.shift + c);
-#pragma unroll
-      for (int tm = 0; tm < TM; ++tm) {
-        const int m = m0 + wm * WTM + tm * 32 + frow;
-        if (m >= a.M) continue;
-        float v0 = acc[tn][tm][4 * g + 0] * sc.x + sh.x;
-        float v1 = acc[tn][tm][4 * g + 1] * sc.y + sh.y;
-        float v2 = acc[tn][tm][4 * g + 2] * sc.z + sh.z;
-        float v3 = acc[tn][tm][4 * g + 3] * sc.w + sh.w;
-        const long long o = (long long)m * a.ldy + c;
-        if (a.res) {
-          const uint2 r = *(const uint2*)((const bf16_t*)a.res + o);
-          v0 += bf2f_m(r.x & 0xFFFFu);
-          v1 += bf2f_m(r.x >> 16);
-          v2 += bf2f_m(r.y & 0xFFFFu);
-          v3 += bf2f_m(r.y >> 16);
-        }
-        if (a.relu) {
-          v0 = fmaxf(v0, 0.f); v1 = fmaxf(v1, 0.f); v2 = fmaxf(v2, 0.f); v3 = fmaxf(v3, 0.f);
-        }
-        if (a.out_f32) {
-          float* y = (float*)a.y + o;
-          y[0] = v0;
-          if (c + 1 < a.c_write) y[1] = v1;
-          if (c + 2 < a.c_write) y[2] = v2;
-          if (c + 3 < a.c_write) y[3] = v3;
-        } else {
-          uint2 q;
-          q.x = f2bf_m(v0) | (f2bf_m(v1) << 16);
-          q.y = f2bf_m(v2) | (f2bf_m(v3) << 16);
-          *(uint2*)((bf16_t*)a.y + o) = q;
-        }
+      if (a.res) {
+        const uint4 r = *(const uint4*)((const bf16_t*)a.res + o);
+        v[0] += bf2f_m(r.x & 0xFFFFu); v[1] += bf2f_m(r.x >> 16);
+        v[2] += bf2f_m(r.y & 0xFFFFu); v[3] += bf2f_m(r.y >> 16);
+        v[4] += bf2f_m(r.z & 0xFFFFu); v[5] += bf2f_m(r.z >> 16);
+        v[6] += bf2f_m(r.w & 0xFFFFu); v[7] += bf2f_m(r.w >> 16);
       }
+      if (a.relu) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) v[j] = fmaxf(v[j], 0.f);
+      }
+      uint4 w;
+      w.x = f2bf_m(v[0]) | (f2bf_m(v[1]) << 16);
+      w.y = f2bf_m(v[2]) | (f2bf_m(v[3]) << 16);
+      w.z = f2bf_m(v[4]) | (f2bf_m(v[5]) << 16);
+      w.w = f2bf_m(v[6]) | (f2bf_m(v[7]) << 16);
+      *(uint4*)((bf16_t*)a.y + o) = w;
     }
+    __builtin_amdgcn_s_waitcnt(0xC07F);   // reads done before the region is rewritten
+    __builtin_amdgcn_wave_barrier();
   }
 }
 
@@ -378,7 +409,13 @@ __global__ void splitk_reduce_kernel(ConvArgs a, int splits, int in_bf16) {
   X(8, 64, 64, 2, 2, 3)    /* wave 32x32 */                                          \
   X(9, 32, 128, 1, 4, 3)   /* wave 32x32 */                                          \
   X(10, 128, 32, 4, 1, 3)  /* wave 32x32 */                                          \
-  X(11, 256, 64, 4, 1, 3)  /* wave 64x64 */
+  X(11, 256, 64, 4, 1, 3)  /* wave 64x64 */                                          \
+  X(12, 64, 64, 2, 2, 2)   /* wave 32x32, two stages (short K) */                    \
+  X(13, 128, 64, 2, 2, 2)  /* wave 64x32, two stages (short K) */                    \
+  X(14, 64, 128, 1, 4, 2)  /* wave 64x32, two stages (short K) */                    \
+  X(15, 128, 128, 2, 2, 2) /* wave 64x64, two stages */                              \
+  X(16, 128, 256, 2, 4, 2) /* 8 waves, wave 64x64, two stages */                     \
+  X(17, 256, 128, 4, 2, 2) /* 8 waves, wave 64x64, two stages */
 
 #define RAFIKI_CFG_ENTRY(id, BM, BN, WM, WN, ST) {BM, BN, WM * WN, ST},
 const MfmaConfig kMfmaConfigs[kNumMfmaConfigs] = {RAFIKI_MFMA_CONFIGS(RAFIKI_CFG_ENTRY)};
