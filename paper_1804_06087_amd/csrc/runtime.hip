@@ -587,7 +587,7 @@ int tune(rafiki_ensemble_s* e, int n, const void* batch, hipStream_t s) {
         if (!cfg_fits(cfg, op.c_out)) continue;
         if (kMfmaConfigs[cfg].bm > 2 * round_up(a.M, 32)) continue;
         float t = 0.f;
-        for (int rep = 0; rep < 3; ++rep) {   // first launch warms caches; keep the best of two
+        for (int rep = 0; rep < 4; ++rep) {   // first launch warms caches; keep the best of three
           if (hipEventRecord(ev[0], s) != hipSuccess || launch_conv_mfma(a, cfg, 1, s) != hipSuccess ||
               hipEventRecord(ev[1], s) != hipSuccess || hipEventSynchronize(ev[1]) != hipSuccess) {
             rc = fail(RAFIKI_ERR_HIP, "tile tuning launch failed");
@@ -595,7 +595,7 @@ int tune(rafiki_ensemble_s* e, int n, const void* batch, hipStream_t s) {
           }
           float ms = 0.f;
           (void)hipEventElapsedTime(&ms, ev[0], ev[1]);
-          if (rep == 1 || (rep == 2 && ms < t)) t = ms;
+          if (rep == 1 || (rep > 1 && ms < t)) t = ms;
         }
         if (rc) break;
         if (t < best) { best = t; choice[mi][oi] = cfg; }

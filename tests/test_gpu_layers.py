@@ -72,6 +72,16 @@ CASES = {
                     (8, 8, 6), 2, 16 * 4 * 3),
     "gap": ([conv(-1, 8, 48, 3), Layer(op=GLOBAL_AVGPOOL, input=0, c_in=48, c_out=48)], (8, 7, 5), 6, 48),
     "many_tiles_ragged_m": ([conv(-1, 32, 16, 3)], (32, 7, 9), 37, 16 * 7 * 9),
+    # image-input convolutions with few channels (input padded to 8 storage channels)
+    "stem_3x3_cout32_ragged": ([conv(-1, 3, 32, 3)], (3, 5, 6), 7, 32 * 5 * 6),
+    "stem_7x7_s2_cout128": ([conv(-1, 3, 128, 7, s=2, p=3)], (3, 4, 4), 3, 128 * 2 * 2),
+    "stem_1ch_5x5_cout96": ([conv(-1, 1, 96, 5, p=2, bn=False, bias=True)], (1, 3, 3), 5, 96 * 3 * 3),
+    # output maps of a multiple of 128 pixels, pooled to keep the probe small
+    "stem_window_3x3": ([conv(-1, 3, 32, 3), Layer(op=MAXPOOL2D, input=0, c_in=32, c_out=32, kh=4, kw=4, stride=4)],
+                        (3, 16, 16), 3, 32 * 4 * 4),
+    "stem_window_7x7_s2": ([conv(-1, 3, 64, 7, s=2, p=3),
+                            Layer(op=MAXPOOL2D, input=0, c_in=64, c_out=64, kh=4, kw=4, stride=4)],
+                           (3, 32, 32), 2, 64 * 4 * 4),
 }
 
 
