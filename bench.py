@@ -49,7 +49,55 @@ def parse():
     ap.add_argument("--trace-steps", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU time of the oracle sample")
+    ap.add_argument("--pmc-copy-bytes", type=int, default=0,
+                    help="after warmup, copy this many bytes with a plain device copy: under rocprofv3 --pmc it "
+                         "calibrates FETCH_SIZE / WRITE_SIZE and marks where the measured steps begin")
+    ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="turn two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) of --pmc-copy-bytes into the "
+                         "per-launch HBM traffic of the conv kernel and print it as JSON")
+    ap.add_argument("--traffic-file", default=None, help="traffic JSON written by --summarize-pmc")
     return ap.parse_args()
+
+
+CONV_SOURCE = os.path.join(ROOT, "paper_1804_06087_amd", "csrc", "conv_mfma.hip")
+
+
+def kernel_source_sha() -> str:
+    import hashlib
+    return hashlib.sha256(open(CONV_SOURCE, "rb").read()).hexdigest()
+
+
+def _pmc_rows(d, counter):
+    import csv
+    import glob
+    files = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
+    if not files:
+        raise SystemExit(f"no counter_collection.csv under {d}")
+    rows = [r for r in csv.DictReader(open(files[0])) if r["Counter_Name"] == counter]
+    rows.sort(key=lambda r: int(r["Dispatch_Id"]))
+    return [(r["Kernel_Name"], float(r["Counter_Value"]) * 1024.0) for r in rows]   # KiB -> bytes
+
+
+def summarize_pmc(fetch_dir, write_dir, copy_bytes):
+    """Per-launch HBM bytes of the conv kernel in the steps after the calibration copy.
+
+    FETCH_SIZE / WRITE_SIZE are in KiB per dispatch; each is rescaled by the ratio of
+    the copy's known size to what the same counter read for the copy."""
+    out = {}
+    for name, d, counter in (("fetch", fetch_dir, "FETCH_SIZE"), ("write", write_dir, "WRITE_SIZE")):
+        rows = _pmc_rows(d, counter)
+        # the calibration kernel: the largest dispatch that is not one of the library's
+        copies = [i for i, (k, _) in enumerate(rows) if "rafiki" not in k]
+        if not copies:
+            raise SystemExit(f"calibration copy not found in {d}")
+        c = max(copies, key=lambda i: rows[i][1])
+        scale = copy_bytes / rows[c][1] if rows[c][1] > 0 else float("nan")
+        conv = [v for k, v in rows[c + 1:] if "conv_mfma_kernel" in k]
+        out[name] = {"scale": scale, "launches": len(conv), "bytes_per_launch": scale * sum(conv) / max(len(conv), 1),
+                     "copy_counter_bytes": rows[c][1]}
+    return {"kernel": "conv_mfma", "source_sha256": kernel_source_sha(), "copy_bytes": copy_bytes,
+            "fetch": out["fetch"], "write": out["write"],
+            "traffic_bytes_per_launch": out["fetch"]["bytes_per_launch"] + out["write"]["bytes_per_launch"]}
 
 
 def cpu_baseline(specs, params, batch, mask, target_s, unit):
@@ -75,6 +123,11 @@ def cpu_baseline(specs, params, batch, mask, target_s, unit):
 
 def main():
     args = parse()
+    if args.summarize_pmc:
+        if not args.pmc_copy_bytes:
+            raise SystemExit("--summarize-pmc needs --pmc-copy-bytes (the calibration copy's size)")
+        print(json.dumps(summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1], args.pmc_copy_bytes)))
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1 "
@@ -116,6 +169,14 @@ def main():
     for _ in range(args.warmup):
         ens.infer(x, n, mask, probs, labels, stream)
     torch.cuda.synchronize()
+    if args.pmc_copy_bytes:
+        # a plain elementwise kernel that reads and writes pmc_copy_bytes each
+        src = torch.empty(args.pmc_copy_bytes // 4, dtype=torch.float32, device=dev).fill_(1.0)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        torch.mul(src, 1.0, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
 
     # ---- throughput: K back-to-back steps bracketed by synchronisation
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -177,6 +238,17 @@ def main():
                 "avg_launch_ms": round(d["ms"] / d["launches"], 5),
                 "alg_bytes_per_launch": round(d["bytes"] / d["launches"], 1)}
 
+    # HBM traffic of the dominant kernel from committed counter runs, if they were
+    # taken on the current kernel source
+    tfile = args.traffic_file or os.path.join(ROOT, "profiles", f"conv_mfma_traffic_{args.workload}.json")
+    if dom == "conv_mfma" and os.path.exists(tfile):
+        try:
+            t = json.load(open(tfile))
+            if t.get("source_sha256") == kernel_source_sha():
+                roof["traffic"] = round(t["traffic_bytes_per_launch"], 1)
+                roof["traffic_unit"] = "bytes per launch (HBM, counter-based)"
+        except Exception:
+            pass
     step_flops = sum(c["flops"] for c in classes.values()) / args.trace_steps
     value = n / (ms_per_step / 1e3)
     out = {
