@@ -6,8 +6,8 @@ code with it.
 """
 from .reference import (to_bf16_rne, conv2d, batchnorm, relu, maxpool2d, global_avgpool, fc,
                         embedding, conv1d_maxtime, concat, softmax, combine_mean, argmax_first,
-                        run_model, ensemble, model_macs)
+                        run_model, ensemble, model_macs, combine_vote, ensemble_vote)
 
 __all__ = ["to_bf16_rne", "conv2d", "batchnorm", "relu", "maxpool2d", "global_avgpool", "fc",
            "embedding", "conv1d_maxtime", "concat", "softmax", "combine_mean", "argmax_first",
-           "run_model", "ensemble", "model_macs"]
+           "run_model", "ensemble", "model_macs", "combine_vote", "ensemble_vote"]

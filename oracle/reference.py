@@ -245,6 +245,48 @@ def ensemble(specs, params, batch: np.ndarray, mask: int, act: Optional[str] = N
     return p, argmax_first(p), zs
 
 
+def combine_vote(logits: Sequence[np.ndarray]):
+    """Majority vote of the selected models (Section 5.2, the ensemble experiment).
+
+    ``logits`` lists the selected models in priority order (first = highest).  Each
+    model votes for its own first-index argmax; the winning class has the most votes,
+    and a tie between classes goes to the one predicted by the highest-priority model
+    among those tied.  Returns (vote fractions [N, C], labels [N])."""
+    preds = [argmax_first(np.asarray(z, dtype=np.float64)) for z in logits]
+    n, c = np.asarray(logits[0]).shape
+    votes = np.zeros((n, c), dtype=np.float64)
+    for pr in preds:
+        votes[np.arange(n), pr] += 1.0
+    labels = np.zeros(n, dtype=np.int32)
+    for i in range(n):
+        best = votes[i].max()
+        for pr in preds:                      # priority order
+            if votes[i, pr[i]] == best:
+                labels[i] = pr[i]
+                break
+    return votes / float(len(logits)), labels
+
+
+def ensemble_vote(specs, params, batch: np.ndarray, mask: int, act: Optional[str] = None,
+                  logits: Optional[List[np.ndarray]] = None):
+    """Majority-vote ensemble over the models selected by ``mask``; model order is the
+    priority order.  Returns (vote fractions, labels, per-model logits)."""
+    if mask == 0:
+        raise ValueError("the selection vector must not be all zeros")
+    if mask >> len(specs):
+        raise ValueError("mask selects a model that does not exist")
+    zs: List[Optional[np.ndarray]] = [None] * len(specs)
+    sel = []
+    for m in range(len(specs)):
+        if not (mask >> m) & 1:
+            continue
+        z = logits[m] if logits is not None and logits[m] is not None else run_model(specs[m], params[m], batch, act)
+        zs[m] = z
+        sel.append(z)
+    v, lab = combine_vote(sel)
+    return v, lab, zs
+
+
 def model_macs(spec) -> int:
     """Algorithmic multiply-accumulates per request of one model (no padding counted)."""
     shapes: Dict[int, Tuple[int, ...]] = {}

@@ -288,3 +288,30 @@ def test_tiny_resnet_block_brute():
     ref = [[[[max(0.0, bn(b[0][c][i][j], P.layers[2], c) + x[0, c, i, j]) for j in range(4)] for i in range(4)]
             for c in range(2)]]
     assert np.allclose(got, np.array(ref), atol=1e-12)
+
+
+# ---------------------------------------------------------------- majority vote (Section 5.2)
+def test_vote_golden_example():
+    g = json.load(open(os.path.join(GOLDEN, "vote_3x4.json")))
+    logits = [np.array(z) for z in g["logits"]]
+    assert [oracle.argmax_first(z).tolist() for z in logits] == g["model_predictions"]
+    v, lab = oracle.combine_vote(logits)
+    assert np.allclose(v, g["expected_votes"], atol=1e-15)
+    assert lab.tolist() == g["expected_labels"]
+
+
+def test_vote_invariants():
+    zs = [rng.standard_normal((50, 7)) for _ in range(4)]
+    v, lab = oracle.combine_vote(zs[:1])                  # one model: its own argmax, one vote
+    assert np.array_equal(lab, np.argmax(zs[0], 1)) and np.allclose(v.sum(1), 1.0)
+    v, lab = oracle.combine_vote([zs[0], zs[0], zs[1]])   # a duplicated model is a majority
+    assert np.array_equal(lab, np.argmax(zs[0], 1))
+    v, lab = oracle.combine_vote(zs)
+    assert np.allclose(v.sum(1), 1.0, atol=1e-15)
+    # the winner always has the maximal vote count
+    assert np.all(v[np.arange(50), lab] == v.max(1))
+    # brute force over priorities: with two models that disagree, the first model wins
+    a, b = np.zeros((1, 3)), np.zeros((1, 3))
+    a[0, 2] = 1.0
+    b[0, 0] = 1.0
+    assert oracle.combine_vote([a, b])[1][0] == 2 and oracle.combine_vote([b, a])[1][0] == 0
