@@ -46,6 +46,8 @@ def parse():
     ap.add_argument("--workload", default="c3", choices=sorted(WORKLOADS) + ["c4"])
     ap.add_argument("--n", type=int, default=None, help="batch size (c4 sweep points, or override)")
     ap.add_argument("--mask", type=int, default=None, help="model subset mask override")
+    ap.add_argument("--combine", default="mean", choices=["mean", "vote"],
+                    help="ensemble combine: probability mean (default) or majority vote")
     ap.add_argument("--trace-steps", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU time of the oracle sample")
@@ -100,7 +102,7 @@ def summarize_pmc(fetch_dir, write_dir, copy_bytes):
             "traffic_bytes_per_launch": out["fetch"]["bytes_per_launch"] + out["write"]["bytes_per_launch"]}
 
 
-def cpu_baseline(specs, params, batch, mask, target_s, unit):
+def cpu_baseline(specs, params, batch, mask, target_s, unit, combine="mean"):
     """Time the fp64 oracle (as is) on the host cores over a bounded sample of the batch."""
     import numpy as np
     import oracle
@@ -109,12 +111,13 @@ def cpu_baseline(specs, params, batch, mask, target_s, unit):
         cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
     except Exception:
         cores = os.cpu_count() or 1
+    run = oracle.ensemble if combine == "mean" else oracle.ensemble_vote
     t0 = time.perf_counter()
-    oracle.ensemble(specs, params, batch[:1], mask)
+    run(specs, params, batch[:1], mask)
     t1 = time.perf_counter() - t0
     k = int(max(1, min(batch.shape[0], round(target_s / max(t1, 1e-6)))))
     t0 = time.perf_counter()
-    oracle.ensemble(specs, params, batch[:k], mask)
+    run(specs, params, batch[:k], mask)
     dt = time.perf_counter() - t0
     return {"value": round(k / dt, 4), "unit": unit, "cores": int(cores), "kind": "oracle",
             "sample": f"{k} of the {batch.shape[0]} requests, all selected models, fp64 NumPy oracle, "
@@ -165,9 +168,10 @@ def main():
     probs = torch.empty((n, C), dtype=torch.float32, device=dev)
     labels = torch.empty((n,), dtype=torch.int32, device=dev)
     stream = torch.cuda.current_stream()
+    serve = ens.infer if args.combine == "mean" else ens.infer_vote
 
     for _ in range(args.warmup):
-        ens.infer(x, n, mask, probs, labels, stream)
+        serve(x, n, mask, probs, labels, stream)
     torch.cuda.synchronize()
     if args.pmc_copy_bytes:
         # a plain elementwise kernel that reads and writes pmc_copy_bytes each
@@ -183,7 +187,7 @@ def main():
     torch.cuda.synchronize()
     ev0.record(stream)
     for _ in range(args.steps):
-        ens.infer(x, n, mask, probs, labels, stream)
+        serve(x, n, mask, probs, labels, stream)
     ev1.record(stream)
     torch.cuda.synchronize()
     ms_per_step = ev0.elapsed_time(ev1) / args.steps
@@ -193,7 +197,7 @@ def main():
     for _ in range(max(args.steps, 10)):
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         a.record(stream)
-        ens.infer(x, n, mask, probs, labels, stream)
+        serve(x, n, mask, probs, labels, stream)
         b.record(stream)
         b.synchronize()
         lat.append(a.elapsed_time(b))
@@ -202,7 +206,7 @@ def main():
     # ---- traced pass: per-launch HIP events around every kernel (separate from the timed steps)
     ens.trace(True)
     for _ in range(args.trace_steps):
-        ens.infer(x, n, mask, probs, labels, stream)
+        serve(x, n, mask, probs, labels, stream)
     recs = ens.trace_read()
     ens.trace(False)
     torch.cuda.synchronize()
@@ -252,7 +256,8 @@ def main():
     step_flops = sum(c["flops"] for c in classes.values()) / args.trace_steps
     value = n / (ms_per_step / 1e3)
     out = {
-        "metric": METRIC if args.workload == "c3" else f"ensemble {unit} ({args.workload})",
+        "metric": METRIC if args.workload == "c3" and args.combine == "mean" else
+        f"ensemble {unit} ({args.workload}, majority vote)" if args.combine == "vote" else f"ensemble {unit} ({args.workload})",
         "value": round(value, 2),
         "unit": unit,
         "n_gpus": 1,
@@ -264,7 +269,7 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16" if precision == "bf16" else "f32",
         "data": "synthetic (seeded inputs and random-init weights of the named architectures)",
-        "config": {"workload": desc, "global_batch": n, "mask": mask, "n_classes": C,
+        "config": {"workload": desc, "global_batch": n, "mask": mask, "n_classes": C, "combine": args.combine,
                    "input": "int32 tokens [n, 256]" if tokens else "float32 NCHW images"},
         "p50_ms": round(float(np.percentile(lat, 50)), 4),
         "p99_ms": round(float(np.percentile(lat, 99)), 4),
@@ -275,7 +280,8 @@ def main():
         "kernels": kernels,
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(specs, params, batch, mask, args.cpu_seconds, unit)
+        out["cpu_baseline"] = cpu_baseline(specs, params, batch, mask, args.cpu_seconds, unit,
+                                        args.combine)
     ens.close()
     print(json.dumps(out), flush=True)
 

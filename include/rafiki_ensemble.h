@@ -12,6 +12,7 @@
  *
  *   rafiki_ensemble_create   job creation + deployment: parameters copied to HBM
  *   rafiki_ensemble_infer    one scheduled batch with one selection vector
+ *   rafiki_ensemble_infer_vote     the same batch combined by majority vote (Section 5.2)
  *   rafiki_ensemble_model_logits   one model's raw logits (diagnostics, tests)
  *   rafiki_ensemble_destroy  teardown
  *
@@ -138,6 +139,19 @@ int rafiki_ensemble_create(const rafiki_model_desc* models, int n_models,
 int rafiki_ensemble_infer(rafiki_ensemble_t h, const void* batch, int n, uint32_t model_subset_mask,
                           float* out_probs, int32_t* out_labels, void* stream);
 
+/* Serve one batch like rafiki_ensemble_infer, but combine the selected models by
+ * majority vote, the aggregation of the paper's ensemble experiment (Section 5.2):
+ * each selected model votes for the lowest class index attaining the maximum of its
+ * logits; out_labels[i] is the class with the most votes, and a tie between classes
+ * goes to the class voted for by the lowest-numbered selected model (creation order is
+ * the priority order: create the models sorted from the most to the least accurate to
+ * resolve ties as the paper does).  out_votes is fp32 [n, n_classes] row-major: the
+ * fraction of the selected models voting for each class (each row sums to 1).
+ * Argument rules, errors and stream behaviour as rafiki_ensemble_infer; the result is
+ * exact (integer votes) and deterministic. */
+int rafiki_ensemble_infer_vote(rafiki_ensemble_t h, const void* batch, int n, uint32_t model_subset_mask,
+                               float* out_votes, int32_t* out_labels, void* stream);
+
 /* Run model `model` alone and write its fp32 logits [n, n_classes] to out_logits.
  * Same argument rules as infer.  Enqueue-only on `stream`. */
 int rafiki_ensemble_model_logits(rafiki_ensemble_t h, int model, const void* batch, int n,
@@ -155,7 +169,8 @@ enum {
   RAFIKI_K_POOL = 4,           /* max-pool, global average pool, max over time */
   RAFIKI_K_EMBED = 5,          /* embedding gather */
   RAFIKI_K_CONCAT = 6,         /* vector concatenation */
-  RAFIKI_K_COMBINE = 7         /* softmax + ensemble mean + argmax */
+  RAFIKI_K_COMBINE = 7,        /* softmax + ensemble mean + argmax */
+  RAFIKI_K_VOTE = 8            /* per-model argmax + majority vote */
 };
 typedef struct {
   int kind;                     /* RAFIKI_K_* */

@@ -19,10 +19,11 @@ LIB_PATH = os.path.join(_PKG, "librafiki_ensemble.so")
 RAFIKI_OK, RAFIKI_ERR_INVALID, RAFIKI_ERR_UNSUPPORTED, RAFIKI_ERR_NOMEM, RAFIKI_ERR_HIP = 0, -1, -2, -3, -4
 RAFIKI_FP32, RAFIKI_BF16 = 0, 1
 RAFIKI_INPUT_IMAGE_NCHW_F32, RAFIKI_INPUT_TOKENS_I32 = 0, 1
-EXPORTED = ("rafiki_ensemble_create", "rafiki_ensemble_infer", "rafiki_ensemble_model_logits",
+EXPORTED = ("rafiki_ensemble_create", "rafiki_ensemble_infer", "rafiki_ensemble_infer_vote",
+            "rafiki_ensemble_model_logits",
             "rafiki_ensemble_info", "rafiki_ensemble_trace", "rafiki_ensemble_trace_read",
             "rafiki_ensemble_destroy", "rafiki_last_error")
-KERNEL_CLASSES = ("conv_mfma", "splitk_reduce", "conv_f32", "stage", "pool", "embed", "concat", "combine")
+KERNEL_CLASSES = ("conv_mfma", "splitk_reduce", "conv_f32", "stage", "pool", "embed", "concat", "combine", "vote")
 
 _fp = C.POINTER(C.c_float)
 
@@ -69,15 +70,15 @@ def load_library(path: str = LIB_PATH):
                                            C.POINTER(C.c_void_p)]
     lib.rafiki_ensemble_infer.argtypes = [C.c_void_p, C.c_void_p, C.c_int, C.c_uint32, C.c_void_p, C.c_void_p,
                                           C.c_void_p]
+    lib.rafiki_ensemble_infer_vote.argtypes = [C.c_void_p, C.c_void_p, C.c_int, C.c_uint32, C.c_void_p,
+                                               C.c_void_p, C.c_void_p]
     lib.rafiki_ensemble_model_logits.argtypes = [C.c_void_p, C.c_int, C.c_void_p, C.c_int, C.c_void_p, C.c_void_p]
     lib.rafiki_ensemble_info.argtypes = [C.c_void_p, C.POINTER(C.c_int), C.POINTER(C.c_int), C.POINTER(C.c_int)]
     lib.rafiki_ensemble_destroy.argtypes = [C.c_void_p]
     lib.rafiki_ensemble_trace.argtypes = [C.c_void_p, C.c_int]
     lib.rafiki_ensemble_trace_read.argtypes = [C.c_void_p, C.POINTER(RafikiTraceRec), C.c_int, C.POINTER(C.c_int)]
     lib.rafiki_last_error.restype = C.c_char_p
-    for name in ("rafiki_ensemble_create", "rafiki_ensemble_infer", "rafiki_ensemble_model_logits",
-                 "rafiki_ensemble_info", "rafiki_ensemble_destroy", "rafiki_ensemble_trace",
-                 "rafiki_ensemble_trace_read"):
+    for name in EXPORTED[:-1]:
         getattr(lib, name).restype = C.c_int
     _lib = lib
     return lib
@@ -170,6 +171,12 @@ class Ensemble:
     def infer(self, batch, n: int, mask: int, out_probs, out_labels, stream=None):
         _check(self._lib.rafiki_ensemble_infer(self._h, _ptr(batch), n, mask, _ptr(out_probs), _ptr(out_labels),
                                                _stream(stream)))
+
+    def infer_vote(self, batch, n: int, mask: int, out_votes, out_labels, stream=None):
+        """Majority-vote combine (Section 5.2): out_votes = vote fractions, ties to the
+        lowest-numbered selected model's class."""
+        _check(self._lib.rafiki_ensemble_infer_vote(self._h, _ptr(batch), n, mask, _ptr(out_votes),
+                                                    _ptr(out_labels), _stream(stream)))
 
     def model_logits(self, model: int, batch, n: int, out_logits, stream=None):
         _check(self._lib.rafiki_ensemble_model_logits(self._h, model, _ptr(batch), n, _ptr(out_logits),

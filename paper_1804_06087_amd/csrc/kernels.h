@@ -74,5 +74,7 @@ struct CombineArgs {
   int32_t* labels;      // [n]
 };
 hipError_t launch_combine(const CombineArgs& a, hipStream_t s);
+// Majority vote over the same slots: probs <- vote fractions, labels <- winner.
+hipError_t launch_vote(const CombineArgs& a, hipStream_t s);
 
 }  // namespace rafiki

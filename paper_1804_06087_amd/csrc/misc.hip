@@ -1,6 +1,7 @@
 // Memory-bound kernels of the hot path: input staging, pooling, spatial reductions,
 // embedding gather, concatenation, the fp32 direct convolution, and the ensemble
-// combine (softmax per model, mean over the selected models, first-index argmax).
+// combine (softmax per model, mean over the selected models, first-index argmax) and
+// the majority-vote combine.
 #include "kernels.h"
 
 namespace rafiki {
@@ -307,6 +308,61 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineArgs a) {
 hipError_t launch_combine(const CombineArgs& a, hipStream_t s) {
   if (a.C > 64 * kCombineMaxPerLane || a.S < 1) return hipErrorInvalidValue;
   hipLaunchKernelGGL(combine_kernel, dim3((a.n + 3) / 4), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- majority vote
+// One wave per request row.  Each selected model's prediction is the first index of
+// the maximum of its logits; lane s keeps the prediction of selected model s (S <= 32,
+// priority = selection order).  The winner is the prediction with the most votes,
+// the tie going to the lowest s.  All integer work: exact and order independent.
+__global__ __launch_bounds__(256) void vote_kernel(CombineArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= a.n) return;
+  const int per = (a.C + 63) / 64;
+  int pred_mine = -1;
+  for (int s = 0; s < a.S; ++s) {
+    const float* z = a.logits + a.sel[s] * a.ld_model + (long long)row * a.C;
+    float best = -INFINITY;
+    int bidx = 0x7fffffff;
+    for (int i = 0; i < per; ++i) {
+      const int c = i * 64 + lane;
+      if (c < a.C) {
+        const float v = z[c];
+        if (v > best) { best = v; bidx = c; }
+      }
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const float ob = __shfl_xor(best, o, 64);
+      const int oi = __shfl_xor(bidx, o, 64);
+      if (ob > best || (ob == best && oi < bidx)) { best = ob; bidx = oi; }
+    }
+    if (bidx == 0x7fffffff) bidx = 0;        // a row with no value above -inf
+    if (lane == s) pred_mine = bidx;
+  }
+  // votes for this lane's prediction
+  int count = 0;
+  for (int t = 0; t < a.S; ++t) count += (__shfl(pred_mine, t, 64) == pred_mine) ? 1 : 0;
+  int key = lane < a.S ? count * 64 + (63 - lane) : -1;   // most votes, then lowest s
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) key = max(key, __shfl_xor(key, o, 64));
+  const int winner = 63 - (key & 63);
+  const int label = __shfl(pred_mine, winner, 64);
+  const float invS = 1.0f / (float)a.S;
+  for (int i = 0; i < per; ++i) {
+    const int c = i * 64 + lane;
+    int votes = 0;
+    for (int t = 0; t < a.S; ++t) votes += (__shfl(pred_mine, t, 64) == c) ? 1 : 0;
+    if (c < a.C) a.probs[(long long)row * a.C + c] = (float)votes * invS;
+  }
+  if (lane == 0) a.labels[row] = label;
+}
+
+hipError_t launch_vote(const CombineArgs& a, hipStream_t s) {
+  if (a.S < 1 || a.S > 32 || a.C < 1) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(vote_kernel, dim3((a.n + 3) / 4), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

@@ -767,11 +767,15 @@ int rafiki_ensemble_create(const rafiki_model_desc* models, int n_models, const 
   return RAFIKI_OK;
 }
 
-int rafiki_ensemble_infer(rafiki_ensemble_t h, const void* batch, int n, uint32_t model_subset_mask,
-                          float* out_probs, int32_t* out_labels, void* stream) {
+}  // extern "C"
+
+// One scheduled batch through the selected models, then the mean (vote = false) or
+// majority-vote (vote = true) combine into out / out_labels.
+static int serve(rafiki_ensemble_t h, const void* batch, int n, uint32_t model_subset_mask, float* out,
+                 int32_t* out_labels, void* stream, bool vote) {
   int rc = check_call(h, batch, n);
   if (rc) return rc;
-  if (!out_probs || !out_labels) return fail(RAFIKI_ERR_INVALID, "null output pointer");
+  if (!out || !out_labels) return fail(RAFIKI_ERR_INVALID, "null output pointer");
   if (model_subset_mask == 0) return fail(RAFIKI_ERR_INVALID, "model_subset_mask must select at least one model");
   if (h->n_models < 32 && (model_subset_mask >> h->n_models) != 0)
     return fail(RAFIKI_ERR_INVALID, "model_subset_mask selects a model that does not exist");
@@ -782,7 +786,7 @@ int rafiki_ensemble_infer(rafiki_ensemble_t h, const void* batch, int n, uint32_
   CombineArgs ca{};
   ca.logits = h->d_logits;
   ca.ld_model = (long long)h->max_batch * h->n_classes;
-  ca.n = n; ca.C = h->n_classes; ca.probs = out_probs; ca.labels = out_labels;
+  ca.n = n; ca.C = h->n_classes; ca.probs = out; ca.labels = out_labels;
   for (int m = 0; m < h->n_models; ++m)
     if ((model_subset_mask >> m) & 1u) ca.sel[ca.S++] = m;
   // Selected models are independent until the combine: fork them onto their own
@@ -801,9 +805,25 @@ int rafiki_ensemble_infer(rafiki_ensemble_t h, const void* batch, int n, uint32_
   }
   if (fork)
     for (int i = 0; i < ca.S; ++i) HIPCHK(hipStreamWaitEvent(s, h->models[ca.sel[i]].done, 0));
-  TRACED(h, s, RAFIKI_K_COMBINE, -1, -1, 0.0, (double)n * h->n_classes * 4.0 * (ca.S + 1) + 4.0 * n,
-         launch_combine(ca, s));
+  const double cbytes = (double)n * h->n_classes * 4.0 * (ca.S + 1) + 4.0 * n;
+  if (vote) {
+    TRACED(h, s, RAFIKI_K_VOTE, -1, -1, 0.0, cbytes, launch_vote(ca, s));
+  } else {
+    TRACED(h, s, RAFIKI_K_COMBINE, -1, -1, 0.0, cbytes, launch_combine(ca, s));
+  }
   return RAFIKI_OK;
+}
+
+extern "C" {
+
+int rafiki_ensemble_infer(rafiki_ensemble_t h, const void* batch, int n, uint32_t model_subset_mask,
+                          float* out_probs, int32_t* out_labels, void* stream) {
+  return serve(h, batch, n, model_subset_mask, out_probs, out_labels, stream, false);
+}
+
+int rafiki_ensemble_infer_vote(rafiki_ensemble_t h, const void* batch, int n, uint32_t model_subset_mask,
+                               float* out_votes, int32_t* out_labels, void* stream) {
+  return serve(h, batch, n, model_subset_mask, out_votes, out_labels, stream, true);
 }
 
 int rafiki_ensemble_model_logits(rafiki_ensemble_t h, int model, const void* batch, int n, float* out_logits,

@@ -73,6 +73,7 @@ def test_null_arguments():
     assert "null" in bd.last_error()
     assert lib.rafiki_ensemble_destroy(None) == bd.RAFIKI_OK
     assert lib.rafiki_ensemble_infer(None, None, 1, 1, None, None, None) == bd.RAFIKI_ERR_INVALID
+    assert lib.rafiki_ensemble_infer_vote(None, None, 1, 1, None, None, None) == bd.RAFIKI_ERR_INVALID
     assert lib.rafiki_ensemble_model_logits(None, 0, None, 1, None, None) == bd.RAFIKI_ERR_INVALID
     assert lib.rafiki_ensemble_info(None, None, None, None) == bd.RAFIKI_ERR_INVALID
 
