@@ -315,3 +315,12 @@ def test_vote_invariants():
     a[0, 2] = 1.0
     b[0, 0] = 1.0
     assert oracle.combine_vote([a, b])[1][0] == 2 and oracle.combine_vote([b, a])[1][0] == 0
+
+
+def test_vote_two_models_equal_the_priority_model():
+    """Section 5.2 observes that a two-model ensemble predicts exactly what its more
+    accurate member predicts: with two voters every disagreement is a tie."""
+    za, zb = rng.standard_normal((200, 10)), rng.standard_normal((200, 10))
+    assert (np.argmax(za, 1) != np.argmax(zb, 1)).sum() > 100
+    assert np.array_equal(oracle.combine_vote([za, zb])[1], np.argmax(za, 1))
+    assert np.array_equal(oracle.combine_vote([zb, za])[1], np.argmax(zb, 1))
