@@ -85,3 +85,34 @@ def softmax_row(z):
     ex = [math.exp(v - m) for v in z]
     s = sum(ex)
     return [v / s for v in ex]
+
+
+def greedy_busy_loop(arrivals, B, cost, tau, delta, t_end):
+    """The scheduling loop of Algorithm "Inference" stepped literally, one microsecond
+    per iteration, until t_end: while the model is free, test the two conditions on the
+    current queue; when busy, let time pass.  Returns (latency per request or -1,
+    dispatch list of (start, b))."""
+    n = len(arrivals)
+    lat = [-1] * n
+    disp = []
+    head, arrived, busy_until = 0, 0, -1
+    for t in range(int(arrivals[0]) if n else 0, int(t_end) + 1):
+        while arrived < n and arrivals[arrived] <= t:
+            arrived += 1
+        if t < busy_until:
+            continue
+        q = arrived - head
+        b = 0
+        if q >= max(B):
+            b = max(B)
+        elif q > 0:
+            smaller = [x for x in B if x <= q]
+            if smaller and cost[max(smaller)] + (t - arrivals[head]) + delta >= tau:
+                b = max(smaller)
+        if b:
+            disp.append((t, b))
+            for i in range(head, head + b):
+                lat[i] = t + cost[b] - arrivals[i]
+            head += b
+            busy_until = t + cost[b]
+    return lat, disp

@@ -1,0 +1,90 @@
+"""Oracle of the greedy batch-size scheduler (Section 5.1, Algorithm "Inference").
+
+TEST INFRASTRUCTURE ONLY (see the package header).
+
+One model serves a FIFO queue one batch at a time.  Whenever the model is free, the
+policy looks at the queue:
+* with at least max(B) requests queued, the oldest max(B) are served at once;
+* otherwise b is the largest candidate size not above the queue length, and the oldest
+  b are served as soon as c(b) + w(q_0) + delta >= tau, w(q_0) being the waiting time
+  of the oldest queued request; with no such b (fewer requests than min(B)) it waits.
+
+Time is kept in integer microseconds, so every comparison is exact.  A batch started
+at time t finishes at t + c(b); its requests' latency l(s) is that finish time minus
+their arrival time.  The objective of Equation (single) is the mean exceeding time
+sum(max(0, l(s) - tau)) / |S|.
+"""
+from typing import Dict, List, Sequence, Tuple
+
+import numpy as np
+
+
+def greedy_decide(B: Sequence[int], cost: Dict[int, int], queue_len: int, oldest_wait: int,
+                  tau: int, delta: int) -> int:
+    """Batch size to serve now, or 0 to keep waiting (Algorithm "Inference")."""
+    bmax = max(B)
+    if queue_len >= bmax:
+        return bmax
+    fitting = [b for b in B if b <= queue_len]
+    if not fitting:
+        return 0
+    b = max(fitting)
+    if cost[b] + oldest_wait + delta >= tau:
+        return b
+    return 0
+
+
+def simulate_greedy(arrivals: Sequence[int], B: Sequence[int], cost: Dict[int, int], tau: int, delta: int):
+    """Event-driven run of the policy over requests arriving at the given times
+    (non-decreasing, microseconds).  The decision only changes when a request arrives,
+    when the model becomes free, or when the oldest request's wait reaches
+    tau - delta - c(b); the simulation visits exactly those instants.
+
+    Returns (latency per request, -1 for requests never served, and the list of
+    dispatches (start time, batch size, queue length, oldest wait))."""
+    a = [int(x) for x in arrivals]
+    n = len(a)
+    lat = [-1] * n
+    disp: List[Tuple[int, int, int, int]] = []
+    t = a[0] if n else 0
+    head = 0        # oldest request not yet served
+    arrived = 0     # requests with arrival time <= t
+    while True:
+        while arrived < n and a[arrived] <= t:
+            arrived += 1
+        qlen = arrived - head
+        if qlen == 0:
+            if arrived == n:
+                break
+            t = a[arrived]
+            continue
+        wait = t - a[head]
+        b = greedy_decide(B, cost, qlen, wait, tau, delta)
+        if b > 0:
+            disp.append((t, b, qlen, wait))
+            done = t + cost[b]
+            for i in range(head, head + b):
+                lat[i] = done - a[i]
+            head += b
+            t = done
+            continue
+        nxt = a[arrived] if arrived < n else None
+        fitting = [x for x in B if x <= qlen]
+        if fitting:
+            deadline = a[head] + tau - delta - cost[max(fitting)]
+            nxt = deadline if nxt is None else min(nxt, deadline)
+        if nxt is None:
+            break            # fewer than min(B) requests left and none arriving
+        t = nxt
+    return lat, disp
+
+
+def serving_stats(latency: Sequence[int], tau: int) -> dict:
+    """Equation (single) objective and overdue counts over all requests (a request never
+    served counts as unserved, not in the exceeding time)."""
+    lat = np.asarray(latency, dtype=np.int64)
+    served = lat >= 0
+    exceed = np.maximum(lat[served] - tau, 0)
+    return {"requests": int(lat.size), "served": int(served.sum()),
+            "overdue": int((lat[served] > tau).sum()),
+            "mean_exceeding_us": float(exceed.sum() / max(lat.size, 1))}
