@@ -22,10 +22,25 @@ RAFIKI_INPUT_IMAGE_NCHW_F32, RAFIKI_INPUT_TOKENS_I32 = 0, 1
 EXPORTED = ("rafiki_ensemble_create", "rafiki_ensemble_infer", "rafiki_ensemble_infer_vote",
             "rafiki_ensemble_model_logits",
             "rafiki_ensemble_info", "rafiki_ensemble_trace", "rafiki_ensemble_trace_read",
-            "rafiki_ensemble_destroy", "rafiki_last_error")
+            "rafiki_ensemble_destroy", "rafiki_greedy_decide", "rafiki_greedy_simulate",
+            "rafiki_ensemble_profile", "rafiki_ensemble_serve_greedy", "rafiki_ensemble_serve_greedy_async",
+            "rafiki_last_error")
 KERNEL_CLASSES = ("conv_mfma", "splitk_reduce", "conv_f32", "stage", "pool", "embed", "concat", "combine", "vote")
 
 _fp = C.POINTER(C.c_float)
+
+
+class RafikiGreedyPolicy(C.Structure):
+    _fields_ = [("batch_sizes", C.POINTER(C.c_int32)), ("cost_us", C.POINTER(C.c_int64)), ("n_sizes", C.c_int),
+                ("tau_us", C.c_int64), ("delta_us", C.c_int64)]
+
+
+class RafikiDispatch(C.Structure):
+    _fields_ = [("start_us", C.c_int64), ("end_us", C.c_int64), ("first", C.c_int64), ("queue_len", C.c_int64),
+                ("oldest_wait_us", C.c_int64), ("b", C.c_int32), ("model", C.c_int32)]
+
+
+DISPATCH_FIELDS = ("start_us", "end_us", "first", "queue_len", "oldest_wait_us", "b", "model")
 
 
 class RafikiLayer(C.Structure):
@@ -77,6 +92,20 @@ def load_library(path: str = LIB_PATH):
     lib.rafiki_ensemble_destroy.argtypes = [C.c_void_p]
     lib.rafiki_ensemble_trace.argtypes = [C.c_void_p, C.c_int]
     lib.rafiki_ensemble_trace_read.argtypes = [C.c_void_p, C.POINTER(RafikiTraceRec), C.c_int, C.POINTER(C.c_int)]
+    P = C.POINTER
+    lib.rafiki_greedy_decide.argtypes = [P(RafikiGreedyPolicy), C.c_int64, C.c_int64, P(C.c_int32)]
+    lib.rafiki_greedy_simulate.argtypes = [P(RafikiGreedyPolicy), P(C.c_int64), C.c_int64, P(C.c_int64),
+                                           P(RafikiDispatch), C.c_int64, P(C.c_int64)]
+    lib.rafiki_ensemble_profile.argtypes = [C.c_void_p, C.c_void_p, P(C.c_int32), C.c_int, C.c_uint32, C.c_int,
+                                            C.c_void_p, C.c_void_p, P(C.c_int64), C.c_void_p]
+    lib.rafiki_ensemble_serve_greedy.argtypes = [C.c_void_p, C.c_void_p, P(C.c_int64), C.c_int64,
+                                                 P(RafikiGreedyPolicy), C.c_uint32, C.c_int, C.c_void_p, C.c_void_p,
+                                                 P(C.c_int64), P(RafikiDispatch), C.c_int64, P(C.c_int64),
+                                                 C.c_void_p]
+    lib.rafiki_ensemble_serve_greedy_async.argtypes = [C.c_void_p, C.c_void_p, P(C.c_int64), C.c_int64,
+                                                       P(RafikiGreedyPolicy), C.c_uint32, C.c_void_p, C.c_void_p,
+                                                       P(C.c_int64), P(RafikiDispatch), C.c_int64, P(C.c_int64),
+                                                       C.c_void_p]
     lib.rafiki_last_error.restype = C.c_char_p
     for name in EXPORTED[:-1]:
         getattr(lib, name).restype = C.c_int
@@ -117,6 +146,60 @@ def _stream(stream) -> int:
     if isinstance(stream, int):
         return stream
     return stream.cuda_stream
+
+
+def _i32p(a: np.ndarray):
+    return a.ctypes.data_as(C.POINTER(C.c_int32))
+
+
+def _i64p(a: np.ndarray):
+    return a.ctypes.data_as(C.POINTER(C.c_int64))
+
+
+def make_policy(batch_sizes, cost_us, tau_us: int, delta_us: int, keep: list) -> RafikiGreedyPolicy:
+    B = np.ascontiguousarray(batch_sizes, dtype=np.int32)
+    c = np.ascontiguousarray(cost_us, dtype=np.int64)
+    keep += [B, c]
+    p = RafikiGreedyPolicy()
+    p.batch_sizes, p.cost_us, p.n_sizes = _i32p(B), _i64p(c), int(B.size)
+    p.tau_us, p.delta_us = int(tau_us), int(delta_us)
+    return p
+
+
+def dispatches_to_array(disp, n: int) -> np.ndarray:
+    """Structured numpy array of the dispatch records held (at most n)."""
+    dt = np.dtype([(f, np.int64) for f in DISPATCH_FIELDS])
+    n = min(n, len(disp))
+    out = np.zeros(n, dtype=dt)
+    for i in range(n):
+        for f in DISPATCH_FIELDS:
+            out[f][i] = getattr(disp[i], f)
+    return out
+
+
+def greedy_decide(batch_sizes, cost_us, tau_us: int, delta_us: int, queue_len: int, oldest_wait_us: int) -> int:
+    lib = load_library()
+    keep = []
+    p = make_policy(batch_sizes, cost_us, tau_us, delta_us, keep)
+    b = C.c_int32(0)
+    _check(lib.rafiki_greedy_decide(C.byref(p), queue_len, oldest_wait_us, C.byref(b)))
+    return b.value
+
+
+def greedy_simulate(arrival_us, batch_sizes, cost_us, tau_us: int, delta_us: int, cap: Optional[int] = None):
+    """Host simulation of one model under the greedy policy: (latency_us, dispatches,
+    total number of dispatches); at most ``cap`` dispatch records are returned."""
+    lib = load_library()
+    keep = []
+    p = make_policy(batch_sizes, cost_us, tau_us, delta_us, keep)
+    a = np.ascontiguousarray(arrival_us, dtype=np.int64)
+    lat = np.zeros(a.size, dtype=np.int64)
+    cap = a.size + 1 if cap is None else cap
+    disp = (RafikiDispatch * max(cap, 1))()
+    nd = C.c_int64(0)
+    _check(lib.rafiki_greedy_simulate(C.byref(p), _i64p(a), a.size, _i64p(lat), disp if cap else None, cap,
+                                      C.byref(nd)))
+    return lat, dispatches_to_array(disp, min(nd.value, cap)), nd.value
 
 
 def make_layers(spec, params, keep: list):
@@ -181,6 +264,52 @@ class Ensemble:
     def model_logits(self, model: int, batch, n: int, out_logits, stream=None):
         _check(self._lib.rafiki_ensemble_model_logits(self._h, model, _ptr(batch), n, _ptr(out_logits),
                                                       _stream(stream)))
+
+    def profile(self, batch, batch_sizes, mask: int, reps: int = 10, stream=None):
+        """c(b) in microseconds for each candidate size (mask = 1 << m gives c(m, b))."""
+        import torch
+        B = np.ascontiguousarray(batch_sizes, dtype=np.int32)
+        bmax = int(B.max())
+        probs = torch.empty((bmax, self.n_classes), dtype=torch.float32, device="cuda")
+        labels = torch.empty((bmax,), dtype=torch.int32, device="cuda")
+        out = np.zeros(B.size, dtype=np.int64)
+        _check(self._lib.rafiki_ensemble_profile(self._h, _ptr(batch), _i32p(B), B.size, mask, reps, _ptr(probs),
+                                                 _ptr(labels), _i64p(out), _stream(stream)))
+        return out
+
+    def serve_greedy(self, requests, arrival_us, batch_sizes, cost_us, tau_us: int, delta_us: int, mask: int,
+                     out_probs, out_labels, combine: str = "mean", stream=None):
+        """Real-time greedy serving of resident requests; returns (latency_us, dispatches)."""
+        a = np.ascontiguousarray(arrival_us, dtype=np.int64)
+        keep = []
+        pol = make_policy(batch_sizes, cost_us, tau_us, delta_us, keep)
+        lat = np.zeros(a.size, dtype=np.int64)
+        cap = a.size + 1
+        disp = (RafikiDispatch * cap)()
+        nd = C.c_int64(0)
+        _check(self._lib.rafiki_ensemble_serve_greedy(self._h, _ptr(requests), _i64p(a), a.size, C.byref(pol), mask,
+                                                      1 if combine == "vote" else 0, _ptr(out_probs),
+                                                      _ptr(out_labels), _i64p(lat), disp, cap, C.byref(nd),
+                                                      _stream(stream)))
+        return lat, dispatches_to_array(disp, nd.value)
+
+    def serve_greedy_async(self, requests, arrival_us, policies, mask: int, out_probs, out_labels, stream=None):
+        """Asynchronous serving, one model per batch; ``policies`` maps model index ->
+        (batch_sizes, cost_us, tau_us, delta_us).  Returns (latency_us, dispatches)."""
+        a = np.ascontiguousarray(arrival_us, dtype=np.int64)
+        keep = []
+        pols = (RafikiGreedyPolicy * self.n_models)()
+        for m in range(self.n_models):
+            if m in policies:
+                pols[m] = make_policy(*policies[m], keep)
+        lat = np.zeros(a.size, dtype=np.int64)
+        cap = a.size + 1
+        disp = (RafikiDispatch * cap)()
+        nd = C.c_int64(0)
+        _check(self._lib.rafiki_ensemble_serve_greedy_async(self._h, _ptr(requests), _i64p(a), a.size, pols, mask,
+                                                            _ptr(out_probs), _ptr(out_labels), _i64p(lat), disp, cap,
+                                                            C.byref(nd), _stream(stream)))
+        return lat, dispatches_to_array(disp, nd.value)
 
     def trace(self, enable: bool):
         _check(self._lib.rafiki_ensemble_trace(self._h, 1 if enable else 0))

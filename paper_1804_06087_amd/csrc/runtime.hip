@@ -8,14 +8,18 @@
 //   every selected model on the caller's stream into its logits slot, then combine.
 #include "rafiki_ensemble.h"
 #include "kernels.h"
+#include "sched.h"
 
 #include <algorithm>
+#include <chrono>
+#include <climits>
 #include <cmath>
 #include <cstring>
 #include <cstdlib>
 #include <map>
 #include <memory>
 #include <string>
+#include <thread>
 #include <vector>
 
 using namespace rafiki;
@@ -80,6 +84,7 @@ struct Model {
   size_t partial_bytes = 0;
   hipStream_t stream = nullptr;   // the model's own stream for concurrent ensembles
   hipEvent_t done = nullptr;      // recorded on `stream` after the model's last kernel
+  void* d_staged_own = nullptr;   // the model's own staged input (asynchronous serving)
 };
 
 struct FreeList {
@@ -473,8 +478,10 @@ size_t partial_need(const rafiki_ensemble_s* e, const Model& M) {
 
 unsigned magic_div(int d) { return d == 1 ? 0u : (unsigned)((((unsigned long long)1 << 32) + d - 1) / d); }
 
-const void* tptr(const rafiki_ensemble_s* e, const Model& M, int id, const void* batch) {
-  if (id < 0) return e->input_kind == RAFIKI_INPUT_IMAGE_NCHW_F32 ? e->d_staged : batch;
+// Tensor `id` of model M; id -1 is the model input `in` (staged images or the token batch).
+const void* tptr(const rafiki_ensemble_s* e, const Model& M, int id, const void* in) {
+  (void)e;
+  if (id < 0) return in;
   return M.d_arena + M.tensors[id].off;
 }
 
@@ -534,10 +541,10 @@ int run_gemm(const rafiki_ensemble_s* e, const Op& op, ConvArgs a, hipStream_t s
 }
 
 // Kernel arguments of a GEMM-like op over n requests (output pointer set by the caller).
-ConvArgs gemm_args(const rafiki_ensemble_s* e, const Model& M, const Op& op, int n, const void* batch) {
+ConvArgs gemm_args(const rafiki_ensemble_s* e, const Model& M, const Op& op, int n, const void* in) {
   ConvArgs a{};
-  a.x = tptr(e, M, op.in, batch); a.w = op.d_w; a.scale = op.d_scale; a.shift = op.d_shift;
-  a.res = op.in2 >= 0 ? tptr(e, M, op.in2, batch) : nullptr;
+  a.x = tptr(e, M, op.in, in); a.w = op.d_w; a.scale = op.d_scale; a.shift = op.d_shift;
+  a.res = op.in2 >= 0 ? tptr(e, M, op.in2, in) : nullptr;
   a.N = n; a.H = op.H; a.W = op.W; a.Cs = op.Cs_in;
   a.Ho = op.Ho; a.Wo = op.Wo; a.kh = op.kh; a.kw = op.kw; a.stride = op.stride; a.pad = op.pad;
   a.M = n * op.Ho * op.Wo; a.K = op.K; a.Kp = op.Kp; a.Co_pad = op.Co_pad; a.Nc = op.c_out;
@@ -552,7 +559,7 @@ ConvArgs gemm_args(const rafiki_ensemble_s* e, const Model& M, const Op& op, int
 // Choose each GEMM op's tile configuration for batch size n by timing the candidates
 // on stream s (once per n; blocks the caller).  Only unsplit launches are tuned: all
 // of them sum K in the same order, so the choice never changes a result.
-int tune(rafiki_ensemble_s* e, int n, const void* batch, hipStream_t s) {
+int tune(rafiki_ensemble_s* e, int n, const void* in, hipStream_t s) {
   if (e->tuned.count(n)) return RAFIKI_OK;
   std::vector<std::vector<int>> choice(e->models.size());
   hipEvent_t ev[2] = {nullptr, nullptr};
@@ -570,7 +577,7 @@ int tune(rafiki_ensemble_s* e, int n, const void* batch, hipStream_t s) {
       if (op.kind != O_CONV && op.kind != O_CONV1D) continue;
       choice[mi][oi] = default_cfg(op.c_out);
       if (!timing) continue;
-      ConvArgs a = gemm_args(e, M, op, n, batch);
+      ConvArgs a = gemm_args(e, M, op, n, in);
       if (choose_splits(a.M, op.c_out, a.Kp / 64) > 1) continue;
       if ((long long)a.N * a.H * a.W * a.Cs * 2 >= (1LL << 31) || (long long)a.Co_pad * a.Kp * 2 >= (1LL << 31))
         continue;   // run_gemm rejects these shapes
@@ -610,8 +617,9 @@ int tune(rafiki_ensemble_s* e, int n, const void* batch, hipStream_t s) {
   return RAFIKI_OK;
 }
 
-// Forward pass of model `mi` over n requests; logits [n][n_classes] to `logits`.
-int run_model(const rafiki_ensemble_s* e, int mi, const void* batch, int n, float* logits, hipStream_t s) {
+// Forward pass of model `mi` over n requests whose model input is `in` (staged images
+// or token ids); logits [n][n_classes] to `logits`.
+int run_model(const rafiki_ensemble_s* e, int mi, const void* in, int n, float* logits, hipStream_t s) {
   const Model& M = e->models[mi];
   const auto it = e->tuned.find(n);
   const std::vector<int> empty;
@@ -622,11 +630,11 @@ int run_model(const rafiki_ensemble_s* e, int mi, const void* batch, int n, floa
     const int li = op.out;
     const Tensor& y = M.tensors[op.out];
     void* yp = y.is_logits ? (void*)logits : (void*)(M.d_arena + y.off);
-    const void* xp = tptr(e, M, op.in, batch);
+    const void* xp = tptr(e, M, op.in, in);
     switch (op.kind) {
       case O_CONV:
       case O_CONV1D: {
-        ConvArgs a = gemm_args(e, M, op, n, batch);
+        ConvArgs a = gemm_args(e, M, op, n, in);
         const int cfg = cfgs.empty() ? -1 : cfgs[&op - M.ops.data()];
         if (op.kind == O_CONV1D) {
           void* tmp = M.d_arena + op.tmp_off;
@@ -655,13 +663,13 @@ int run_model(const rafiki_ensemble_s* e, int mi, const void* batch, int n, floa
         break;
       case O_EMBED:
         TRACED(e, s, RAFIKI_K_EMBED, mi, li, 0.0, (double)n * op.W * (4.0 + 2.0 * op.cin_l * es),
-               launch_embed_gather((const int32_t*)batch, op.d_w, yp, n, op.W, op.Cs_in, bf, s));
+               launch_embed_gather((const int32_t*)in, op.d_w, yp, n, op.W, op.Cs_in, bf, s));
         break;
       case O_CONCAT: {
         const Tensor& a = M.tensors[op.in];
         const Tensor& b = M.tensors[op.in2];
         TRACED(e, s, RAFIKI_K_CONCAT, mi, li, 0.0, 2.0 * n * (op.ca + op.cb) * es,
-               launch_concat(xp, op.ca, a.Cs, tptr(e, M, op.in2, batch), op.cb, b.Cs, yp, y.Cs, n, bf, s));
+               launch_concat(xp, op.ca, a.Cs, tptr(e, M, op.in2, in), op.cb, b.Cs, yp, y.Cs, n, bf, s));
         break;
       }
     }
@@ -677,15 +685,24 @@ int check_call(const rafiki_ensemble_s* h, const void* batch, int n) {
   return RAFIKI_OK;
 }
 
-int stage(const rafiki_ensemble_s* e, const void* batch, int n, hipStream_t s) {
+// The forward passes' input: the staging buffer for images, the batch itself for tokens.
+const void* model_input(const rafiki_ensemble_s* e, const void* batch, void* staged) {
+  return e->input_kind == RAFIKI_INPUT_IMAGE_NCHW_F32 ? staged : batch;
+}
+
+int stage(const rafiki_ensemble_s* e, const void* batch, int n, hipStream_t s, void* dst) {
   if (e->input_kind != RAFIKI_INPUT_IMAGE_NCHW_F32) return RAFIKI_OK;
   TRACED(e, s, RAFIKI_K_STAGE, -1, -1, 0.0, (double)n * e->C * e->H * e->W * (4.0 + (double)e->esz()),
-         launch_stage_images((const float*)batch, e->d_staged, n, e->C, e->H, e->W, e->in_Cs,
+         launch_stage_images((const float*)batch, dst, n, e->C, e->H, e->W, e->in_Cs,
                              e->precision == RAFIKI_BF16, s));
   return RAFIKI_OK;
 }
 
 }  // namespace
+
+namespace rafiki {
+int set_error(int code, const std::string& msg) { return fail(code, msg); }
+}  // namespace rafiki
 
 extern "C" {
 
@@ -780,8 +797,9 @@ static int serve(rafiki_ensemble_t h, const void* batch, int n, uint32_t model_s
   if (h->n_models < 32 && (model_subset_mask >> h->n_models) != 0)
     return fail(RAFIKI_ERR_INVALID, "model_subset_mask selects a model that does not exist");
   hipStream_t s = (hipStream_t)stream;
-  rc = stage(h, batch, n, s);
-  if (!rc) rc = tune(h, n, batch, s);
+  const void* in = model_input(h, batch, h->d_staged);
+  rc = stage(h, batch, n, s, h->d_staged);
+  if (!rc) rc = tune(h, n, in, s);
   if (rc) return rc;
   CombineArgs ca{};
   ca.logits = h->d_logits;
@@ -799,7 +817,7 @@ static int serve(rafiki_ensemble_t h, const void* batch, int n, uint32_t model_s
     Model& M = h->models[m];
     hipStream_t ms = fork ? M.stream : s;
     if (fork) HIPCHK(hipStreamWaitEvent(ms, h->staged_ev, 0));
-    rc = run_model(h, m, batch, n, h->d_logits + (size_t)m * ca.ld_model, ms);
+    rc = run_model(h, m, in, n, h->d_logits + (size_t)m * ca.ld_model, ms);
     if (rc) return rc;
     if (fork) HIPCHK(hipEventRecord(M.done, ms));
   }
@@ -833,10 +851,11 @@ int rafiki_ensemble_model_logits(rafiki_ensemble_t h, int model, const void* bat
   if (!out_logits) return fail(RAFIKI_ERR_INVALID, "null output pointer");
   if (model < 0 || model >= h->n_models) return fail(RAFIKI_ERR_INVALID, "model index out of range");
   hipStream_t s = (hipStream_t)stream;
-  rc = stage(h, batch, n, s);
-  if (!rc) rc = tune(h, n, batch, s);
+  const void* in = model_input(h, batch, h->d_staged);
+  rc = stage(h, batch, n, s, h->d_staged);
+  if (!rc) rc = tune(h, n, in, s);
   if (rc) return rc;
-  return run_model(h, model, batch, n, out_logits, s);
+  return run_model(h, model, in, n, out_logits, s);
 }
 
 int rafiki_ensemble_info(rafiki_ensemble_t h, int* n_models, int* n_classes, int* max_batch) {
@@ -884,5 +903,299 @@ int rafiki_ensemble_trace_read(rafiki_ensemble_t h, rafiki_trace_rec* out, int c
 }
 
 const char* rafiki_last_error(void) { return g_err.c_str(); }
+
+}  // extern "C"
+
+// ---------------------------------------------------------------- serving
+namespace {
+
+using SteadyClock = std::chrono::steady_clock;
+
+// Microseconds since construction; waits sleep coarsely, then spin for the last
+// few hundred microseconds.
+struct ServeClock {
+  SteadyClock::time_point t0 = SteadyClock::now();
+  int64_t now() const {
+    return std::chrono::duration_cast<std::chrono::microseconds>(SteadyClock::now() - t0).count();
+  }
+  void wait_until(int64_t t) const {
+    for (;;) {
+      const int64_t d = t - now();
+      if (d <= 0) return;
+      if (d > 400) std::this_thread::sleep_for(std::chrono::microseconds(d - 300));
+      else std::this_thread::yield();
+    }
+  }
+};
+
+int64_t cost_of(const rafiki_greedy_policy& p, int32_t b) {
+  for (int i = 0; i < p.n_sizes; ++i)
+    if (p.batch_sizes[i] == b) return p.cost_us[i];
+  return 0;
+}
+
+size_t request_bytes(const rafiki_ensemble_s* h) { return (size_t)h->C * h->H * h->W * 4; }
+
+const void* request_row(const rafiki_ensemble_s* h, const void* requests, int64_t i) {
+  return (const char*)requests + (size_t)i * request_bytes(h);
+}
+
+int check_mask(const rafiki_ensemble_s* h, uint32_t mask) {
+  if (mask == 0) return fail(RAFIKI_ERR_INVALID, "model_subset_mask must select at least one model");
+  if (h->n_models < 32 && (mask >> h->n_models) != 0)
+    return fail(RAFIKI_ERR_INVALID, "model_subset_mask selects a model that does not exist");
+  return RAFIKI_OK;
+}
+
+int check_serve_outputs(const void* requests, int64_t n, float* probs, int32_t* labels, int64_t* lat,
+                        rafiki_dispatch* disp, int64_t cap, int64_t* ndisp) {
+  if (n > 0 && (!requests || !probs || !labels || !lat))
+    return fail(RAFIKI_ERR_INVALID, "null request or output pointer");
+  if (!ndisp || cap < 0 || (cap > 0 && !disp)) return fail(RAFIKI_ERR_INVALID, "null dispatch output or negative cap");
+  if (n > (int64_t)INT32_MAX) return fail(RAFIKI_ERR_INVALID, "too many requests");
+  return RAFIKI_OK;
+}
+
+int check_policy_fits(const rafiki_ensemble_s* h, const rafiki_greedy_policy* p) {
+  int rc = check_policy(p);
+  if (rc) return rc;
+  if (p->batch_sizes[p->n_sizes - 1] > h->max_batch)
+    return fail(RAFIKI_ERR_INVALID, "the largest batch size exceeds max_batch");
+  return RAFIKI_OK;
+}
+
+void record(rafiki_dispatch* disp, int64_t cap, int64_t& nd, const rafiki_dispatch& d) {
+  if (nd < cap) disp[nd] = d;
+  ++nd;
+}
+
+// One model's whole pipeline for asynchronous serving on its own stream: stage into
+// its own buffer, forward pass, softmax + argmax of its logits into the output rows.
+int launch_single(rafiki_ensemble_s* h, int m, const void* rows, int b, float* probs, int32_t* labels) {
+  Model& M = h->models[m];
+  const void* in = model_input(h, rows, M.d_staged_own);
+  int rc = stage(h, rows, b, M.stream, M.d_staged_own);
+  if (rc) return rc;
+  float* logits = h->d_logits + (size_t)m * h->max_batch * h->n_classes;
+  rc = run_model(h, m, in, b, logits, M.stream);
+  if (rc) return rc;
+  CombineArgs ca{};
+  ca.logits = logits;
+  ca.ld_model = 0;
+  ca.sel[0] = 0;
+  ca.S = 1;
+  ca.n = b; ca.C = h->n_classes; ca.probs = probs; ca.labels = labels;
+  HIPCHK(launch_combine(ca, M.stream));
+  HIPCHK(hipEventRecord(M.done, M.stream));
+  return RAFIKI_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int rafiki_ensemble_profile(rafiki_ensemble_t h, const void* batch, const int32_t* batch_sizes, int n_sizes,
+                            uint32_t mask, int reps, float* scratch_probs, int32_t* scratch_labels,
+                            int64_t* out_cost_us, void* stream) {
+  if (!h) return fail(RAFIKI_ERR_INVALID, "null handle");
+  if (!batch || !batch_sizes || !scratch_probs || !scratch_labels || !out_cost_us)
+    return fail(RAFIKI_ERR_INVALID, "null argument");
+  if (n_sizes < 1 || n_sizes > 64 || reps < 1 || reps > 1000)
+    return fail(RAFIKI_ERR_INVALID, "n_sizes must be in [1, 64] and reps in [1, 1000]");
+  for (int i = 0; i < n_sizes; ++i)
+    if (batch_sizes[i] < 1 || batch_sizes[i] > h->max_batch)
+      return fail(RAFIKI_ERR_INVALID, "batch sizes must be in [1, max_batch]");
+  int rc = check_mask(h, mask);
+  if (rc) return rc;
+  hipStream_t s = (hipStream_t)stream;
+  hipEvent_t ev[2] = {nullptr, nullptr};
+  HIPCHK(hipEventCreate(&ev[0]));
+  if (hipEventCreate(&ev[1]) != hipSuccess) {
+    (void)hipEventDestroy(ev[0]);
+    return fail(RAFIKI_ERR_HIP, "hipEventCreate failed");
+  }
+  std::vector<float> t(reps);
+  for (int i = 0; i < n_sizes && !rc; ++i) {
+    const int b = batch_sizes[i];
+    rc = serve(h, batch, b, mask, scratch_probs, scratch_labels, stream, false);   // untimed (tunes b)
+    for (int r = 0; r < reps && !rc; ++r) {
+      if (hipEventRecord(ev[0], s) != hipSuccess) { rc = fail(RAFIKI_ERR_HIP, "hipEventRecord failed"); break; }
+      rc = serve(h, batch, b, mask, scratch_probs, scratch_labels, stream, false);
+      if (rc) break;
+      if (hipEventRecord(ev[1], s) != hipSuccess || hipEventSynchronize(ev[1]) != hipSuccess ||
+          hipEventElapsedTime(&t[r], ev[0], ev[1]) != hipSuccess)
+        rc = fail(RAFIKI_ERR_HIP, "event timing failed");
+    }
+    if (rc) break;
+    std::sort(t.begin(), t.end());
+    out_cost_us[i] = (int64_t)std::ceil((double)t[reps / 2] * 1000.0);
+  }
+  (void)hipEventDestroy(ev[0]);
+  (void)hipEventDestroy(ev[1]);
+  return rc;
+}
+
+int rafiki_ensemble_serve_greedy(rafiki_ensemble_t h, const void* requests, const int64_t* arrival_us,
+                                 int64_t n_requests, const rafiki_greedy_policy* policy, uint32_t mask,
+                                 int combine, float* out_probs, int32_t* out_labels, int64_t* out_latency_us,
+                                 rafiki_dispatch* out_dispatch, int64_t dispatch_cap, int64_t* out_n_dispatch,
+                                 void* stream) {
+  if (!h) return fail(RAFIKI_ERR_INVALID, "null handle");
+  int rc = check_policy_fits(h, policy);
+  if (!rc) rc = check_arrivals(arrival_us, n_requests);
+  if (!rc) rc = check_mask(h, mask);
+  if (!rc) rc = check_serve_outputs(requests, n_requests, out_probs, out_labels, out_latency_us, out_dispatch,
+                                    dispatch_cap, out_n_dispatch);
+  if (rc) return rc;
+  if (combine != 0 && combine != 1) return fail(RAFIKI_ERR_INVALID, "combine must be 0 (mean) or 1 (vote)");
+  const rafiki_greedy_policy& p = *policy;
+  const bool vote = combine == 1;
+  const int64_t n = n_requests;
+  const int C = h->n_classes;
+  hipStream_t s = (hipStream_t)stream;
+  std::fill(out_latency_us, out_latency_us + n, int64_t(-1));
+  *out_n_dispatch = 0;
+  // Warm up (and tune) every candidate size before the clock starts.
+  for (int i = 0; i < p.n_sizes; ++i) {
+    const int b = p.batch_sizes[i];
+    if (b > n) break;
+    rc = serve(h, requests, b, mask, out_probs, out_labels, stream, vote);
+    if (rc) return rc;
+  }
+  HIPCHK(hipStreamSynchronize(s));
+  int64_t nd = 0, head = 0, arrived = 0;
+  const int64_t* a = arrival_us;
+  ServeClock clk;
+  while (head < n) {
+    const int64_t t = clk.now();
+    while (arrived < n && a[arrived] <= t) ++arrived;
+    const int64_t qlen = arrived - head;
+    if (qlen == 0) {
+      clk.wait_until(a[arrived]);
+      continue;
+    }
+    const int64_t wait = t - a[head];
+    const int32_t b = greedy_decide(p, qlen, wait);
+    if (b > 0) {
+      rc = serve(h, request_row(h, requests, head), b, mask, out_probs + (size_t)head * C, out_labels + head,
+                 stream, vote);
+      if (rc) return rc;
+      HIPCHK(hipStreamSynchronize(s));
+      const int64_t done = clk.now();
+      for (int64_t i = head; i < head + b; ++i) out_latency_us[i] = done - a[i];
+      record(out_dispatch, dispatch_cap, nd, {t, done, head, qlen, wait, b, -1});
+      head += b;
+      continue;
+    }
+    int64_t next = arrived < n ? a[arrived] : INT64_MAX;
+    next = std::min(next, greedy_deadline(p, qlen, a[head]));
+    if (next == INT64_MAX) break;   // fewer than min(B) left, nothing more arriving
+    clk.wait_until(next);
+  }
+  *out_n_dispatch = nd;
+  return RAFIKI_OK;
+}
+
+int rafiki_ensemble_serve_greedy_async(rafiki_ensemble_t h, const void* requests, const int64_t* arrival_us,
+                                       int64_t n_requests, const rafiki_greedy_policy* policies, uint32_t mask,
+                                       float* out_probs, int32_t* out_labels, int64_t* out_latency_us,
+                                       rafiki_dispatch* out_dispatch, int64_t dispatch_cap, int64_t* out_n_dispatch,
+                                       void* stream) {
+  if (!h) return fail(RAFIKI_ERR_INVALID, "null handle");
+  if (!policies) return fail(RAFIKI_ERR_INVALID, "null policies");
+  int rc = check_mask(h, mask);
+  if (!rc) rc = check_arrivals(arrival_us, n_requests);
+  if (!rc) rc = check_serve_outputs(requests, n_requests, out_probs, out_labels, out_latency_us, out_dispatch,
+                                    dispatch_cap, out_n_dispatch);
+  if (rc) return rc;
+  std::vector<int> sel;
+  for (int m = 0; m < h->n_models; ++m)
+    if ((mask >> m) & 1u) {
+      rc = check_policy_fits(h, &policies[m]);
+      if (rc) return rc;
+      sel.push_back(m);
+    }
+  const int64_t n = n_requests;
+  const int C = h->n_classes;
+  std::fill(out_latency_us, out_latency_us + n, int64_t(-1));
+  *out_n_dispatch = 0;
+  HIPCHK(hipStreamSynchronize((hipStream_t)stream));   // requests written on the caller's stream
+  if (h->input_kind == RAFIKI_INPUT_IMAGE_NCHW_F32)
+    for (int m : sel)
+      if (!h->models[m].d_staged_own) {
+        rc = dev_alloc(h, &h->models[m].d_staged_own,
+                       (size_t)h->max_batch * h->H * h->W * h->in_Cs * h->esz());
+        if (rc) return rc;
+      }
+  // Warm up (and tune) every model at each of its candidate sizes before the clock starts.
+  for (int m : sel) {
+    const rafiki_greedy_policy& p = policies[m];
+    for (int i = 0; i < p.n_sizes; ++i) {
+      const int b = p.batch_sizes[i];
+      if (b > n) break;
+      Model& M = h->models[m];
+      rc = stage(h, requests, b, M.stream, M.d_staged_own);
+      if (!rc) rc = tune(h, b, model_input(h, requests, M.d_staged_own), M.stream);
+      if (!rc) rc = launch_single(h, m, requests, b, out_probs, out_labels);
+      if (rc) return rc;
+      HIPCHK(hipStreamSynchronize(M.stream));
+    }
+  }
+  struct Busy { bool on = false; int64_t first = 0, b = 0, disp = -1; };
+  std::vector<Busy> busy(h->n_models);
+  std::vector<rafiki_dispatch> log;
+  int64_t head = 0, arrived = 0;
+  const int64_t* a = arrival_us;
+  ServeClock clk;
+  for (;;) {
+    // completions
+    bool any_busy = false;
+    for (int m : sel) {
+      Busy& B = busy[m];
+      if (!B.on) continue;
+      const hipError_t q = hipEventQuery(h->models[m].done);
+      if (q == hipErrorNotReady) {   // still running; clear the status so a later launch check does not see it
+        (void)hipGetLastError();
+        any_busy = true;
+        continue;
+      }
+      if (q != hipSuccess) return fail(RAFIKI_ERR_HIP, std::string("hipEventQuery: ") + hipGetErrorString(q));
+      const int64_t done = clk.now();
+      for (int64_t i = B.first; i < B.first + B.b; ++i) out_latency_us[i] = done - a[i];
+      log[B.disp].end_us = done;
+      B.on = false;
+    }
+    const int64_t t = clk.now();
+    while (arrived < n && a[arrived] <= t) ++arrived;
+    // dispatch to free models in index order
+    for (int m : sel) {
+      if (busy[m].on || arrived == head) continue;
+      const rafiki_greedy_policy& p = policies[m];
+      const int64_t qlen = arrived - head, wait = t - a[head];
+      const int32_t b = greedy_decide(p, qlen, wait);
+      if (b == 0) continue;
+      rc = launch_single(h, m, request_row(h, requests, head), b, out_probs + (size_t)head * C, out_labels + head);
+      if (rc) return rc;
+      busy[m] = {true, head, b, (int64_t)log.size()};
+      log.push_back({t, -1, head, qlen, wait, b, m});
+      any_busy = true;
+      head += b;
+    }
+    if (head == n && !any_busy) break;
+    // next instant at which a decision can change
+    int64_t next = arrived < n ? a[arrived] : INT64_MAX;
+    if (arrived > head)
+      for (int m : sel)
+        if (!busy[m].on) next = std::min(next, greedy_deadline(policies[m], arrived - head, a[head]));
+    if (any_busy) next = std::min(next, clk.now() + 20);   // poll running batches
+    if (next == INT64_MAX) break;   // nothing running, nothing servable, nothing arriving
+    clk.wait_until(next);
+  }
+  for (size_t i = 0; i < log.size(); ++i) {
+    if (i < (size_t)dispatch_cap) out_dispatch[i] = log[i];
+  }
+  *out_n_dispatch = (int64_t)log.size();
+  return RAFIKI_OK;
+}
 
 }  // extern "C"

@@ -1,0 +1,153 @@
+"""Real-time serving on the GPU with the greedy batch-size policy (Section 5.1,
+Algorithm "Inference") under the sine arrival process (Section 7.2).
+
+Timing is real, so the checks are on what the serving loop must guarantee whatever
+the clock does:
+* every decision it logged is the oracle policy's decision for the queue state it saw;
+* requests are served first-in first-out in batches from B, each request at most
+  once, and only a tail shorter than min(B) may stay unserved;
+* every batch's outputs equal a plain infer call over the same rows (bitwise: the
+  same kernels on the same inputs);
+* latencies are completion minus arrival times.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads as wl
+from paper_1804_06087_amd import Ensemble, RafikiError, RAFIKI_ERR_INVALID
+
+pytestmark = pytest.mark.gpu
+DEV = torch.device("cuda:0")
+B4 = [16, 32, 48, 64]
+N_REQ = 2048
+
+
+def arrivals(rate, tau, n, seed):
+    """n arrivals of the sine process around `rate` (requests/s), a short period of 20 tau
+    so that the requests span a few cycles."""
+    arr = wl.sine_arrivals(rate, 20 * tau, int(2.0 * n / rate * 1e6) + 20 * tau, max(tau // 10, 1), seed=seed)
+    assert arr.size >= n
+    return arr[:n]
+
+
+@pytest.fixture(scope="module")
+def c2():
+    cfg, specs, params, batch = wl.build_config(2, n=N_REQ)
+    ens = Ensemble(specs, params, precision="bf16", max_batch=64)
+    x = torch.from_numpy(batch).to(DEV)
+    yield ens, x
+    ens.close()
+
+
+def _check_fifo_and_decisions(disp, lat, arr, policies, n):
+    served = 0
+    for d in disp:
+        m = int(d["model"])
+        B, cost, tau, delta = policies[m]
+        b = int(d["b"])
+        assert b in B and d["first"] == served, d
+        assert oracle.greedy_decide(B, dict(zip(B, cost)), int(d["queue_len"]), int(d["oldest_wait_us"]), tau,
+                                    delta) == b, d
+        assert d["oldest_wait_us"] == d["start_us"] - arr[served]
+        assert arr[served + b - 1] <= d["start_us"] and d["end_us"] >= d["start_us"]
+        assert np.array_equal(lat[served:served + b], d["end_us"] - arr[served:served + b])
+        served += b
+    assert (lat[served:] == -1).all() and n - served < max(min(p[0]) for p in policies.values())
+    return served
+
+
+def _replay(ens, x, disp, probs, labels, C, mask_of):
+    for d in disp:
+        f, b = int(d["first"]), int(d["b"])
+        p = torch.empty((b, C), dtype=torch.float32, device=DEV)
+        lab = torch.empty((b,), dtype=torch.int32, device=DEV)
+        ens.infer(x[f:f + b], b, mask_of(int(d["model"])), p, lab)
+        torch.cuda.synchronize()
+        assert torch.equal(p, probs[f:f + b]) and torch.equal(lab, labels[f:f + b]), d
+
+
+def test_profile_costs(c2):
+    ens, x = c2
+    cost = ens.profile(x, B4, 0b111, reps=5)
+    assert (cost > 0).all() and cost[-1] >= cost[0]
+    for m in range(3):
+        cm = ens.profile(x, B4, 1 << m, reps=5)
+        assert (cm > 0).all() and (cm <= cost * 1.5 + 50).all()
+
+
+def test_serve_greedy_ensemble(c2):
+    ens, x = c2
+    n, C = x.shape[0], 10
+    cost = ens.profile(x, B4, 0b111, reps=5)
+    tau = int(2 * cost[-1])
+    delta = tau // 10
+    r_l = min(b / c for b, c in zip(B4, cost)) * 1e6
+    arr = arrivals(r_l, tau, n, seed=1)
+    probs = torch.full((n, C), -1.0, device=DEV)
+    labels = torch.full((n,), -1, dtype=torch.int32, device=DEV)
+    lat, disp = ens.serve_greedy(x, arr, B4, cost, tau, delta, 0b111, probs, labels)
+    pol = {-1: (B4, cost.tolist(), tau, delta)}
+    served = _check_fifo_and_decisions(disp, lat, arr, pol, n)
+    assert served >= n - 15 and len(disp) >= n // 64
+    _replay(ens, x, disp, probs, labels, C, lambda m: 0b111)
+    st = oracle.serving_stats(lat, tau)
+    print(f"sync ensemble: c(b) {cost.tolist()} us, tau {tau} us, {len(disp)} batches, {st}")
+
+
+def test_serve_greedy_vote(c2):
+    ens, x = c2
+    n, C = 256, 10
+    cost = ens.profile(x, B4, 0b101, reps=3)
+    tau = int(2 * cost[-1])
+    arr = np.zeros(n, dtype=np.int64)                      # a burst: four full batches
+    votes = torch.empty((n, C), device=DEV)
+    labels = torch.empty((n,), dtype=torch.int32, device=DEV)
+    lat, disp = ens.serve_greedy(x[:n], arr, B4, cost, tau, tau // 10, 0b101, votes, labels, combine="vote")
+    assert disp["b"].tolist() == [64] * 4 and (lat > 0).all()
+    for d in disp:
+        f = int(d["first"])
+        v = torch.empty((64, C), device=DEV)
+        lab = torch.empty((64,), dtype=torch.int32, device=DEV)
+        ens.infer_vote(x[f:f + 64], 64, 0b101, v, lab)
+        torch.cuda.synchronize()
+        assert torch.equal(v, votes[f:f + 64]) and torch.equal(lab, labels[f:f + 64])
+
+
+def test_serve_greedy_async_models(c2):
+    ens, x = c2
+    n, C = x.shape[0], 10
+    pols = {}
+    r_u = 0.0
+    for m in range(3):
+        cm = ens.profile(x, B4, 1 << m, reps=5)
+        r_u += max(b / c for b, c in zip(B4, cm)) * 1e6
+        pols[m] = (B4, cm.tolist(), 0, 0)
+    tau = int(2 * max(p[1][-1] for p in pols.values()))
+    pols = {m: (B, c, tau, tau // 10) for m, (B, c, _, _) in pols.items()}
+    arr = arrivals(r_u, tau, n, seed=2)
+    probs = torch.full((n, C), -1.0, device=DEV)
+    labels = torch.full((n,), -1, dtype=torch.int32, device=DEV)
+    lat, disp = ens.serve_greedy_async(x, arr, pols, 0b111, probs, labels)
+    served = _check_fifo_and_decisions(disp, lat, arr, pols, n)
+    assert served >= n - 15
+    assert set(disp["model"].tolist()) <= {0, 1, 2}
+    _replay(ens, x, disp, probs, labels, C, lambda m: 1 << m)
+    st = oracle.serving_stats(lat, tau)
+    print(f"async models: {len(disp)} batches, per model {np.bincount(disp['model'], minlength=3).tolist()}, {st}")
+
+
+def test_serve_argument_errors(c2):
+    ens, x = c2
+    probs = torch.empty((64, 10), device=DEV)
+    labels = torch.empty((64,), dtype=torch.int32, device=DEV)
+    arr = np.zeros(64, dtype=np.int64)
+    for B, mask in (([16, 128], 1), ([16, 64], 0), ([16, 64], 0b1000)):
+        with pytest.raises(RafikiError) as ei:
+            ens.serve_greedy(x[:64], arr, B, [10, 20], 100, 10, mask, probs, labels)
+        assert ei.value.code == RAFIKI_ERR_INVALID
+    with pytest.raises(RafikiError):
+        ens.serve_greedy(x[:64], arr[::-1] - 1, [16], [10], 100, 10, 1, probs, labels)
+    with pytest.raises(RafikiError):
+        ens.profile(x, [16, 65], 1, reps=1)
