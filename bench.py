@@ -58,6 +58,12 @@ def parse():
                     help="turn two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) of --pmc-copy-bytes into the "
                          "per-launch HBM traffic of the conv kernel and print it as JSON")
     ap.add_argument("--traffic-file", default=None, help="traffic JSON written by --summarize-pmc")
+    ap.add_argument("--serve", default=None, choices=["sync", "async"],
+                    help="instead of the step benchmark, serve a sine-rate request stream in real time with the "
+                         "greedy batch-size policy: every batch through all selected models (sync) or each model "
+                         "an independent server (async); prints one JSON line of serving statistics")
+    ap.add_argument("--cycles", type=float, default=1.0, help="serving: sine cycles of 500 tau to serve")
+    ap.add_argument("--period-taus", type=int, default=500, help="serving: sine period in units of tau")
     return ap.parse_args()
 
 
@@ -124,6 +130,87 @@ def cpu_baseline(specs, params, batch, mask, target_s, unit, combine="mean"):
                       f"{dt:.1f} s"}
 
 
+def serve_main(args, dev):
+    """Greedy serving experiment (Section 7.2) on one GPU: candidate sizes B = {16, 32,
+    48, 64}, tau = 2 c(64), delta = 0.1 tau, sine arrivals with period 500 tau around the
+    synchronous ensemble's throughput (sync) or the summed per-model throughput (async)."""
+    import numpy as np
+    import torch
+
+    import oracle
+    import workloads as wl
+    from paper_1804_06087_amd import Ensemble
+
+    cid = WORKLOADS[args.workload][0]
+    mask = args.mask or WORKLOADS[args.workload][2]
+    B = [16, 32, 48, 64]
+    cfg, specs, params, pool = wl.build_config(cid, n=1024)
+    C = specs[0].n_classes
+    ens = Ensemble(specs, params, precision=cfg.precision, max_batch=max(B))
+    xpool = torch.from_numpy(pool).to(dev)
+    sel = [m for m in range(len(specs)) if (mask >> m) & 1]
+    c_ens = ens.profile(xpool, B, mask, reps=10)
+    c_mod = {m: ens.profile(xpool, B, 1 << m, reps=10) for m in sel}
+    tau = int(2 * c_ens[-1])
+    delta = tau // 10
+    r_l = max(b / c for b, c in zip(B, c_ens)) * 1e6                       # all models on every batch
+    r_u = sum(max(b / c for b, c in zip(B, c_mod[m])) * 1e6 for m in sel)  # each model its own server
+    rate = r_l if args.serve == "sync" else r_u
+    period = args.period_taus * tau
+    arr = wl.sine_arrivals(rate, period, int(args.cycles * period), max(tau // 10, 1), seed=0)
+    n = int(arr.size)
+    req_bytes = n * xpool[0].numel() * xpool.element_size()
+    if req_bytes > 48 * 2 ** 30:
+        raise SystemExit(f"{n} requests need {req_bytes / 2 ** 30:.0f} GiB of HBM; lower --cycles or --period-taus")
+    reps = (n + xpool.shape[0] - 1) // xpool.shape[0]
+    x = xpool.repeat((reps,) + (1,) * (xpool.dim() - 1))[:n].contiguous()   # requests resident in HBM
+    probs = torch.empty((n, C), dtype=torch.float32, device=dev)
+    labels = torch.empty((n,), dtype=torch.int32, device=dev)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    if args.serve == "sync":
+        lat, disp = ens.serve_greedy(x, arr, B, c_ens, tau, delta, mask, probs, labels, combine=args.combine)
+        lat_sim, _ = oracle.simulate_greedy(arr, B, dict(zip(B, c_ens.tolist())), tau, delta)
+    else:
+        pols = {m: (B, c_mod[m], tau, delta) for m in sel}
+        lat, disp = ens.serve_greedy_async(x, arr, pols, mask, probs, labels)
+        lat_sim = None
+    wall = time.perf_counter() - t0
+    st = oracle.serving_stats(lat, tau)
+    served = lat[lat >= 0]
+    dur_s = (int(disp["end_us"].max()) if len(disp) else 0) / 1e6
+    out = {
+        "metric": f"greedy serving, {'synchronous ensemble' if args.serve == 'sync' else 'asynchronous models'}: "
+                  "overdue requests per second and mean exceeding time (Equation single)",
+        "value": round(st["overdue"] / max(dur_s, 1e-9), 2), "unit": "overdue requests/s",
+        "higher_is_better": False, "n_gpus": 1, "dtype": "bf16" if cfg.precision == "bf16" else "f32",
+        "data": "synthetic requests (a 1024-image seeded pool tiled in HBM), seeded sine arrivals",
+        "config": {"workload": WORKLOADS[args.workload][3], "mask": mask, "B": B, "tau_us": tau, "delta_us": delta,
+                   "period_us": period, "arrival_ref_rate": round(rate, 1),
+                   "arrival_ref": "r_l (synchronous ensemble throughput)" if args.serve == "sync"
+                   else "r_u (sum of per-model throughputs)", "combine": args.combine if args.serve == "sync"
+                   else "none (one model per batch)"},
+        "c_b_us": {"ensemble": c_ens.tolist(), **{f"model{m}": c_mod[m].tolist() for m in sel}},
+        "requests": st["requests"], "served": st["served"], "overdue": st["overdue"],
+        "overdue_frac": round(st["overdue"] / max(st["requests"], 1), 4),
+        "mean_exceeding_us": round(st["mean_exceeding_us"], 1),
+        "latency_p50_us": int(np.percentile(served, 50)) if served.size else None,
+        "latency_p99_us": int(np.percentile(served, 99)) if served.size else None,
+        "served_per_s": round(st["served"] / max(dur_s, 1e-9), 1), "batches": int(len(disp)),
+        "batch_sizes": {str(b): int((disp["b"] == b).sum()) for b in B},
+        "wall_s": round(wall, 2),
+    }
+    if args.serve == "async":
+        out["batches_per_model"] = {str(m): int((disp["model"] == m).sum()) for m in sel}
+    if lat_sim is not None:
+        so = oracle.serving_stats(lat_sim, tau)
+        out["oracle_simulation"] = {"overdue": so["overdue"], "mean_exceeding_us": round(so["mean_exceeding_us"], 1),
+                                    "served": so["served"],
+                                    "note": "the policy replayed by the scheduler oracle with c(b) as profiled"}
+    ens.close()
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     if args.summarize_pmc:
@@ -147,6 +234,9 @@ def main():
         print(json.dumps({"error": "no GPU visible"}))
         sys.exit(1)
     dev = torch.device("cuda:0")
+    if args.serve:
+        serve_main(args, dev)
+        return
 
     if args.workload == "c4":
         cid, n, mask, desc = 4, args.n or 64, args.mask or 0b111, None
