@@ -1,6 +1,6 @@
 // Greedy batch-size policy (Section 5.1, Algorithm "Inference") and its event-driven
 // simulation over an arrival sequence.  Host code only; integer microseconds.
-#include "sched.h"
+#include "greedy.h"
 
 #include <algorithm>
 #include <climits>

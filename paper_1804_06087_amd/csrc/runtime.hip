@@ -8,7 +8,7 @@
 //   every selected model on the caller's stream into its logits slot, then combine.
 #include "rafiki_ensemble.h"
 #include "kernels.h"
-#include "sched.h"
+#include "greedy.h"
 
 #include <algorithm>
 #include <chrono>
