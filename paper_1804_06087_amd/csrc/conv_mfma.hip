@@ -9,7 +9,7 @@
 // lane whose chunk lies outside the image or past K gets an offset beyond the
 // buffer's num_records, for which the hardware writes zeros: that is the zero
 // padding.  STAGES K tiles of 64 are in flight in an LDS ring, laid out with the
-// bank-conflict-free swizzle described at swz().  Each wave computes a (BM/WM) x (BN/WN) sub-tile with
+// bank-conflict-free swizzle described at swz<KC>().  Each wave computes a (BM/WM) x (BN/WN) sub-tile with
 // v_mfma_f32_32x32x16_bf16 (weights = A operand, pixels = B operand), so a lane ends
 // with runs of 4 consecutive channels of one pixel.  Fused epilogue: fp32 scale /
 // shift (folded batch-norm + bias), residual, ReLU, bf16 store; or fp32 output;
@@ -36,50 +36,63 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
 }
 
-// LDS tile layout: row r (128 bytes = 8 chunks of 16 bytes) keeps logical chunk c in
-// slot c ^ swz(r), swz(r) = (r & 7) ^ ((r >> 3) & 1).  A 16-byte fragment read
-// serves 16 lanes at a time across 64 four-byte banks; its 16 lanes read 16
-// consecutive rows of one chunk, and swz keeps (r % 2, slot) distinct over any 16
-// rows, so the reads are bank-conflict free.
-__device__ __forceinline__ int swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
+// LDS tile layout: a K tile is 64 (KC = 8 chunks of 16 bytes per row) or 32 (KC = 4)
+// channels wide; row r keeps logical chunk c in slot c ^ swz<KC>(r).  A 16-byte
+// fragment read serves 16 lanes at a time across 64 four-byte banks; its 16 lanes
+// read 16 consecutive rows of one chunk.
+//   KC = 8: swz(r) = (r & 7) ^ ((r >> 3) & 1) keeps (r % 2, slot) distinct over any
+//           16 rows (a 128-byte row spans half of the banks);
+//   KC = 4: swz(r) = (r >> 2) & 3 keeps (r % 4, slot) distinct over 16 rows (a
+//           64-byte row spans a quarter of the banks).
+// Either way the reads are bank-conflict free.
+template <int KC>
+__device__ __forceinline__ int swz(int r) {
+  return KC == 8 ? ((r & 7) ^ ((r >> 3) & 1)) : ((r >> 2) & 3);
+}
 
-// Per-thread state of the HBM -> LDS tile loader.  Wave w's load instruction j
-// fills tile rows (j * NW + w) * 8 .. +8 (64 chunks, lane l -> slot l % 8 of row
-// l / 8 of the group).  With NW even, that row's swz is (l / 8) ^ (w & 1) for every
-// j, so lane l always carries chunk (l % 8) ^ (l / 8) ^ (w & 1).
+// Per-thread state of the HBM -> LDS tile loader.  One load instruction moves 64
+// chunks = ROWS = 64 / KC tile rows.  Wave w's instruction j fills rows
+// (j * NW + w) * ROWS .. +ROWS, lane l -> slot l % KC of row l / KC of the group.
+//   KC = 8: with NW even that row's swz is (l / 8) ^ (w & 1) for every j, so lane l
+//           always carries chunk (l % 8) ^ (l / 8) ^ (w & 1);
+//   KC = 4: the group starts at a multiple of 16 rows, so the row's swz is l / 16 and
+//           lane l always carries chunk (l % 4) ^ (l / 16).
 //
-// ALIGNED (Cs % 64 == 0): K is ordered (channel block of 64, tap, channel), so K
-// tile gk is channel block gk / taps at tap gk % taps.  The taps of one channel
-// block are consecutive tiles: they re-read the same input rows while those are
-// still in L2.  Tap and channel block are wave-uniform and advanced incrementally;
-// per row only the image-bounds test and one add remain.  Otherwise (Cs % 64 != 0)
-// K is ordered (tap, channel) and each lane decodes its own (u, v, ci) with
-// multiply-high division.
-template <int BM, int BN, int NW, bool ALIGNED>
+// ALIGNED (Cs % 64 == 0): K is ordered (channel block of 64, tap, channel), so a
+// 64-wide K block is channel block gk / taps at tap gk % taps (a 32-wide K tile is
+// one half of such a block).  The taps of one channel block are consecutive tiles:
+// they re-read the same input rows while those are still in L2.  Tap, channel block
+// and half are wave-uniform and advanced incrementally; per row only the
+// image-bounds test and one add remain.  Otherwise (Cs % 64 != 0) K is ordered
+// (tap, channel) and each lane decodes its own (u, v, ci) with multiply-high division.
+template <int BM, int BN, int NW, bool ALIGNED, int KC>
 struct Loader {
-  static constexpr int RA = BM / (8 * NW);
-  static constexpr int RB = BN / (8 * NW);
-  static constexpr int STAGE_CHUNKS = (BM + BN) * 8;
+  static constexpr int ROWS = 64 / KC;
+  static constexpr int SUBS = 8 / KC;      // K tiles per 64-channel block
+  static constexpr int RA = BM / (ROWS * NW);
+  static constexpr int RB = BN / (ROWS * NW);
+  static constexpr int STAGE_CHUNKS = (BM + BN) * KC;
+  static_assert(KC == 8 || KC == 4, "K tile of 64 or 32 channels");
   __amdgpu_buffer_rsrc_t xr, wr;
   unsigned oob;
   int chunk, wave, kt_begin;
   int a_img[RA], a_hi[RA], a_wi[RA];   // general path: image base pixel, top-left input coords
   int a_off[RA];                       // aligned path: byte offset of (hi0, wi0, chunk) (may be virtual)
   unsigned b_off[RB];
-  int nu, nv, ntap, ncb;               // aligned path: tap (u, v, index) and channel block of the next tile
+  int nu, nv, ntap, ncb, nsub;         // aligned path: tap (u, v, index), channel block, half of the next tile
 
   __device__ __forceinline__ void init(const ConvArgs& a, int m0, int n0, int wave_, int lane, int kt_begin_) {
     wave = wave_;
     kt_begin = kt_begin_;
-    const int lrow = lane >> 3;
-    chunk = (lane & 7) ^ lrow ^ (wave & 1);
+    const int lrow = lane / KC;
+    chunk = KC == 8 ? ((lane & 7) ^ lrow ^ (wave & 1)) : ((lane & 3) ^ (lane >> 4));
     xr = __builtin_amdgcn_make_buffer_rsrc((void*)a.x, (short)0, a.x_bytes, 0x00020000);
     wr = __builtin_amdgcn_make_buffer_rsrc((void*)a.w, (short)0, a.w_bytes, 0x00020000);
     oob = (unsigned)a.x_bytes;   // offset at num_records: the hardware returns zeros
     const int HoWo = a.Ho * a.Wo;
 #pragma unroll
     for (int j = 0; j < RA; ++j) {
-      const int m = m0 + (j * NW + wave) * 8 + lrow;
+      const int m = m0 + (j * NW + wave) * ROWS + lrow;
       if (m < a.M) {
         const int n = m / HoWo, r = m - n * HoWo;
         const int ho = r / a.Wo, wo = r - ho * a.Wo;
@@ -95,45 +108,54 @@ struct Loader {
     }
 #pragma unroll
     for (int j = 0; j < RB; ++j)
-      b_off[j] = (unsigned)(((n0 + (j * NW + wave) * 8 + lrow) * a.Kp + chunk * 8) * 2);
+      b_off[j] = (unsigned)(((n0 + (j * NW + wave) * ROWS + lrow) * a.Kp + chunk * 8) * 2);
     if (ALIGNED) {
       const int taps = a.kh * a.kw;
-      ncb = kt_begin / taps;
-      ntap = kt_begin - ncb * taps;
+      const int blk = kt_begin / SUBS;
+      nsub = kt_begin - blk * SUBS;
+      ncb = blk / taps;
+      ntap = blk - ncb * taps;
       nu = ntap / a.kw;
       nv = ntap - nu * a.kw;
     }
   }
 
   // Issue the loads of K tile kt (relative to the split's first tile) into LDS stage
-  // `stage`.  Tiles must be issued in increasing kt order (the aligned path advances).
+  // `stage`, or only part P of NP of them (the loads j with j % NP == P), so that a
+  // tile's loads can be spread over the k-steps of the running tile.  The parts of a
+  // tile are issued in order, and tiles in increasing kt order (the aligned path
+  // advances its tap after the last part).
+  template <int P = 0, int NP = 1>
   __device__ __forceinline__ void issue(const ConvArgs& a, uint4* lds, int kt, int stage) {
     const int gk = kt_begin + kt;
     uint4* sbase = lds + stage * STAGE_CHUNKS;
     if (ALIGNED) {
-      const bool kvalid = gk * 64 < a.K;   // tiles past K (padding to Kp) read zeros
-      const int delta = ((nu * a.W + nv) * a.Cs + ncb * 64) * 2;
+      const bool kvalid = gk * (8 * KC) < a.K;   // tiles past K (padding to Kp) read zeros
+      const int delta = ((nu * a.W + nv) * a.Cs + ncb * 64 + nsub * (8 * KC)) * 2;
 #pragma unroll
-      for (int j = 0; j < RA; ++j) {
+      for (int j = P; j < RA; j += NP) {
         const int hi = a_hi[j] + nu, wi = a_wi[j] + nv;
         const bool ok = kvalid && (unsigned)hi < (unsigned)a.H && (unsigned)wi < (unsigned)a.W;
         const unsigned off = ok ? (unsigned)(a_off[j] + delta) : oob;
         __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (lds_void*)(sbase + (j * NW + wave) * 64), 16, off, 0, 0, 0);
       }
-      if (++ntap == a.kh * a.kw) {
-        ntap = 0; nu = 0; nv = 0; ++ncb;
-      } else if (++nv == a.kw) {
-        nv = 0; ++nu;
+      if (P == NP - 1 && ++nsub == SUBS) {
+        nsub = 0;
+        if (++ntap == a.kh * a.kw) {
+          ntap = 0; nu = 0; nv = 0; ++ncb;
+        } else if (++nv == a.kw) {
+          nv = 0; ++nu;
+        }
       }
     } else {
-      const unsigned k8 = (unsigned)(gk * 8 + chunk);
+      const unsigned k8 = (unsigned)(gk * KC + chunk);
       const unsigned tap = a.mag_cs8 ? __umulhi(k8, a.mag_cs8) : k8;
       const int ci = (int)(k8 - tap * a.Cs8) * 8;
       const unsigned u = a.mag_kw ? __umulhi(tap, a.mag_kw) : tap;
       const int v = (int)(tap - u * a.kw);
       const bool kvalid = (int)k8 < a.K8;
 #pragma unroll
-      for (int j = 0; j < RA; ++j) {
+      for (int j = P; j < RA; j += NP) {
         const int hi = a_hi[j] + (int)u, wi = a_wi[j] + v;
         const bool ok = kvalid && (unsigned)hi < (unsigned)a.H && (unsigned)wi < (unsigned)a.W;
         const unsigned off = ok ? (unsigned)((a_img[j] + hi * a.W + wi) * a.Cs + ci) * 2u : oob;
@@ -141,32 +163,40 @@ struct Loader {
       }
     }
 #pragma unroll
-    for (int j = 0; j < RB; ++j)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(wr, (lds_void*)(sbase + BM * 8 + (j * NW + wave) * 64), 16,
-                                               b_off[j], gk * 128, 0, 0);
+    for (int j = P; j < RB; j += NP)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(wr, (lds_void*)(sbase + BM * KC + (j * NW + wave) * 64), 16,
+                                               b_off[j], gk * (KC * 16), 0, 0);
   }
 };
 
 // Wait until at most `n` tiles' loads (of `per` instructions each) are outstanding.
 template <int PER, int MAXN>
 __device__ __forceinline__ void wait_tiles(int n) {
-  if (MAXN >= 2 && n >= 2) wait_vmcnt<(MAXN >= 2 ? 2 * PER : 0)>();
-  else if (MAXN >= 1 && n >= 1) wait_vmcnt<(MAXN >= 1 ? PER : 0)>();
-  else wait_vmcnt<0>();
+  if constexpr (MAXN >= 1) {
+    if (n >= MAXN) {
+      wait_vmcnt<MAXN * PER>();
+      return;
+    }
+    wait_tiles<PER, MAXN - 1>(n);
+  } else {
+    wait_vmcnt<0>();
+  }
 }
 
-template <int BM, int BN, int WM, int WN, int STAGES, bool ALIGNED>
+template <int BM, int BN, int WM, int WN, int STAGES, bool ALIGNED, int KC, bool SPLIT, bool SPREAD>
 __global__ __launch_bounds__(WM * WN * 64) void conv_mfma_kernel(ConvArgs a) {
   constexpr int NW = WM * WN;
   constexpr int WTM = BM / WM, WTN = BN / WN;      // wave tile: pixels x channels
   constexpr int TM = WTM / 32, TN = WTN / 32;
-  using LoaderT = Loader<BM, BN, NW, ALIGNED>;
+  constexpr int KS = KC / 2;                       // MFMA k-steps of 16 per K tile
+  using LoaderT = Loader<BM, BN, NW, ALIGNED, KC>;
   constexpr int PER = LoaderT::RA + LoaderT::RB;   // load instructions per thread per tile
-  constexpr int STAGE_CHUNKS = (BM + BN) * 8;      // 16-byte chunks per stage
+  constexpr int STAGE_CHUNKS = (BM + BN) * KC;     // 16-byte chunks per stage
   static_assert(TM >= 1 && TN >= 1 && LoaderT::RA >= 1 && LoaderT::RB >= 1, "tile shape");
-  static_assert(NW % 2 == 0, "the loader's chunk assignment assumes an even wave count");
+  static_assert(KC == 4 || NW % 2 == 0, "the 64-wide loader's chunk assignment assumes an even wave count");
   static_assert(STAGE_CHUNKS * 16 * STAGES <= 160 * 1024, "LDS budget");
-  static_assert(STAGES >= 2 && STAGES <= 4 && (STAGES - 2) * PER < 64, "pipeline depth");
+  static_assert(STAGES >= 2 && STAGES <= 6 && (STAGES - 2) * PER < 64, "pipeline depth");
+  static_assert(!SPREAD || KS >= 2, "a spread refill needs two k-steps");
 
   __shared__ uint4 lds[STAGES * STAGE_CHUNKS];
 
@@ -183,9 +213,10 @@ __global__ __launch_bounds__(WM * WN * 64) void conv_mfma_kernel(ConvArgs a) {
   const int tile = (xcd < r8 ? xcd * (q + 1) : r8 * (q + 1) + (xcd - r8) * q) + loc;
   const int nt = tile % a.n_tiles, mt = tile / a.n_tiles;
   const int m0 = mt * BM, n0 = nt * BN;
-  const int ktiles = a.Kp / 64;
-  const int kt_begin = blockIdx.y * a.kt_per_split;
-  const int nk = min(a.kt_per_split, ktiles - kt_begin);
+  const int ktiles = a.Kp / (8 * KC);
+  const int kps = a.kt_per_split * (8 / KC);      // kt_per_split counts 64-wide tiles
+  const int kt_begin = blockIdx.y * kps;
+  const int nk = min(kps, ktiles - kt_begin);
 
   LoaderT ld;
   ld.init(a, m0, n0, wave, lane, kt_begin);
@@ -200,7 +231,9 @@ __global__ __launch_bounds__(WM * WN * 64) void conv_mfma_kernel(ConvArgs a) {
 
   const int frow = lane & 31, fk = lane >> 5;
   // Fragment reads: row r of a tile, 16-byte chunk kc (k-step s covers chunks 2s, 2s+1).
-  auto frag = [&](const uint4* base, int r, int kc) { return __builtin_bit_cast(bf16x8, base[r * 8 + (kc ^ swz(r))]); };
+  auto frag = [&](const uint4* base, int r, int kc) {
+    return __builtin_bit_cast(bf16x8, base[r * KC + (kc ^ swz<KC>(r))]);
+  };
 
   if (nk > 0) {
 #pragma unroll
@@ -216,17 +249,27 @@ __global__ __launch_bounds__(WM * WN * 64) void conv_mfma_kernel(ConvArgs a) {
 #pragma unroll
     for (int tm = 0; tm < TM; ++tm) xf[0][tm] = frag(lds, wm * WTM + tm * 32 + frow, fk);
 #pragma unroll
-    for (int tn = 0; tn < TN; ++tn) wf[0][tn] = frag(lds + BM * 8, wn * WTN + tn * 32 + frow, fk);
+    for (int tn = 0; tn < TN; ++tn) wf[0][tn] = frag(lds + BM * KC, wn * WTN + tn * 32 + frow, fk);
   }
 
+  // Tile t always lives in stage t % STAGES.  The stage freed by tile kt - 1 takes
+  // tile kt + STAGES - 1: SPREAD = 0 issues its loads right after the barrier that
+  // frees the stage, before the next tile's first fragment reads; SPREAD = 1 issues
+  // half of them after the MFMAs of k-step 0 of tile kt and half after those of
+  // k-step 1, so that the waves of a large tile do not all stall on a full load
+  // queue before their first MFMAs.  Either way they are all issued before the end
+  // of tile kt, as the waits assume.
   for (int kt = 0; kt < nk; ++kt) {
     const int cur = kt % STAGES;
     const uint4* As = lds + cur * STAGE_CHUNKS;
-    const uint4* Bs = As + BM * 8;
+    const uint4* Bs = As + BM * KC;
+    const bool refill = SPREAD && kt >= 1 && kt + STAGES - 1 < nk;
+    const int rstage = (kt + STAGES - 1) % STAGES;
+    const int rt = kt + STAGES - 1;
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
+    for (int s = 0; s < KS; ++s) {
       const int b = s & 1;
-      if (s < 3) {
+      if (s < KS - 1) {
         // prefetch the fragments of k-step s + 1 of this tile; the scheduling fence
         // keeps these reads ahead of the MFMAs below, so their latency overlaps them
 #pragma unroll
@@ -241,6 +284,11 @@ __global__ __launch_bounds__(WM * WN * 64) void conv_mfma_kernel(ConvArgs a) {
         for (int tm = 0; tm < TM; ++tm)
           acc[tn][tm] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[b][tn], xf[b][tm], acc[tn][tm], 0, 0, 0);
       __builtin_amdgcn_sched_barrier(0);
+      if (refill) {
+        if (s == 0) ld.template issue<0, 2>(a, lds, rt, rstage);
+        if (s == 1) ld.template issue<1, 2>(a, lds, rt, rstage);
+      }
+      __builtin_amdgcn_sched_barrier(0);
     }
     // All of this tile's fragment reads have completed (their MFMAs consumed them).
     // Wait for tile kt + 1, then let every wave pass: stage `cur` is free for tile
@@ -250,18 +298,18 @@ __global__ __launch_bounds__(WM * WN * 64) void conv_mfma_kernel(ConvArgs a) {
       wait_tiles<PER, STAGES - 2>(min(STAGES - 2, nk - 2 - kt));
       __builtin_amdgcn_s_barrier();
       asm volatile("" ::: "memory");
-      if (kt + STAGES < nk) ld.issue(a, lds, kt + STAGES, cur);
+      if (!SPREAD && kt + STAGES < nk) ld.issue(a, lds, kt + STAGES, cur);
       const uint4* An = lds + ((kt + 1) % STAGES) * STAGE_CHUNKS;
 #pragma unroll
       for (int tm = 0; tm < TM; ++tm) xf[0][tm] = frag(An, wm * WTM + tm * 32 + frow, fk);
 #pragma unroll
-      for (int tn = 0; tn < TN; ++tn) wf[0][tn] = frag(An + BM * 8, wn * WTN + tn * 32 + frow, fk);
+      for (int tn = 0; tn < TN; ++tn) wf[0][tn] = frag(An + BM * KC, wn * WTN + tn * 32 + frow, fk);
     }
   }
 
   // ---- epilogue.  Lane (frow, fk) holds, for each (tn, tm), channels
   // n0 + wn*WTN + tn*32 + 8g + 4fk + j (g, j in 0..3) of pixel m0 + wm*WTM + tm*32 + frow.
-  if (gridDim.y > 1) {
+  if (SPLIT) {
     // split-K: raw fp32 partial sums, 16-byte stores
 #pragma unroll
     for (int tn = 0; tn < TN; ++tn)
@@ -290,6 +338,8 @@ __global__ __launch_bounds__(WM * WN * 64) void conv_mfma_kernel(ConvArgs a) {
   const int oq = lane & 3, pl = lane >> 2;   // read phase: channel octet oq of pixel pl (+16 per pass)
 #pragma unroll
   for (int tn = 0; tn < TN; ++tn) {
+    // one 32-channel group at a time: keeps the accumulators in place until used
+    __builtin_amdgcn_sched_barrier(0);
     const int cb = n0 + wn * WTN + tn * 32;   // first channel of this 32-channel group
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
@@ -299,7 +349,7 @@ __global__ __launch_bounds__(WM * WN * 64) void conv_mfma_kernel(ConvArgs a) {
 #pragma unroll
       for (int tm = 0; tm < TM; ++tm) {
         const int p = tm * 32 + frow;
-        stg[p * 8 + ((cl >> 2) ^ swz(p))] =
+        stg[p * 8 + ((cl >> 2) ^ swz<8>(p))] =
             make_float4(acc[tn][tm][4 * g + 0] * sc.x + sh.x, acc[tn][tm][4 * g + 1] * sc.y + sh.y,
                         acc[tn][tm][4 * g + 2] * sc.z + sh.z, acc[tn][tm][4 * g + 3] * sc.w + sh.w);
       }
@@ -311,8 +361,8 @@ __global__ __launch_bounds__(WM * WN * 64) void conv_mfma_kernel(ConvArgs a) {
     for (int pass = 0; pass < WTM / 16; ++pass) {
       const int p = pass * 16 + pl;
       const int m = m0 + wm * WTM + p;
-      const float4 lo = stg[p * 8 + ((2 * oq) ^ swz(p))];
-      const float4 hi = stg[p * 8 + ((2 * oq + 1) ^ swz(p))];
+      const float4 lo = stg[p * 8 + ((2 * oq) ^ swz<8>(p))];
+      const float4 hi = stg[p * 8 + ((2 * oq + 1) ^ swz<8>(p))];
       float v[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
       if (m >= a.M || c >= a.c_write) continue;
       const long long o = (long long)m * a.ldy + c;
@@ -349,16 +399,23 @@ __global__ __launch_bounds__(WM * WN * 64) void conv_mfma_kernel(ConvArgs a) {
   }
 }
 
-template <int BM, int BN, int WM, int WN, int STAGES>
+template <int BM, int BN, int WM, int WN, int STAGES, int KC, bool SP>
 static hipError_t launch_mfma_cfg(const ConvArgs& a, int splits, hipStream_t s) {
   ConvArgs b = a;
   b.n_tiles = (a.Nc + BN - 1) / BN;
   const int m_tiles = (a.M + BM - 1) / BM;
   dim3 grid(m_tiles * b.n_tiles, splits);
-  if (a.Cs % 64 == 0)
-    hipLaunchKernelGGL((conv_mfma_kernel<BM, BN, WM, WN, STAGES, true>), grid, dim3(WM * WN * 64), 0, s, b);
-  else
-    hipLaunchKernelGGL((conv_mfma_kernel<BM, BN, WM, WN, STAGES, false>), grid, dim3(WM * WN * 64), 0, s, b);
+  const dim3 block(WM * WN * 64);
+  if (splits > 1) {
+    if (a.Cs % 64 == 0)
+      hipLaunchKernelGGL((conv_mfma_kernel<BM, BN, WM, WN, STAGES, true, KC, true, SP>), grid, block, 0, s, b);
+    else
+      hipLaunchKernelGGL((conv_mfma_kernel<BM, BN, WM, WN, STAGES, false, KC, true, SP>), grid, block, 0, s, b);
+  } else if (a.Cs % 64 == 0) {
+    hipLaunchKernelGGL((conv_mfma_kernel<BM, BN, WM, WN, STAGES, true, KC, false, SP>), grid, block, 0, s, b);
+  } else {
+    hipLaunchKernelGGL((conv_mfma_kernel<BM, BN, WM, WN, STAGES, false, KC, false, SP>), grid, block, 0, s, b);
+  }
   return hipGetLastError();
 }
 
@@ -394,43 +451,56 @@ __global__ void splitk_reduce_kernel(ConvArgs a, int splits, int in_bf16) {
   }
 }
 
-// Tile configurations: id, BM x BN, waves WM x WN, pipeline stages.  Each kernel is
-// instantiated explicitly (the host pass does not always emit the launch stub of an
-// implicitly instantiated kernel template).
-#define RAFIKI_MFMA_CONFIGS(X)                                                        \
-  X(0, 256, 256, 4, 2, 2)  /* 8 waves, wave 64x128, two stages */                    \
-  X(1, 256, 256, 2, 4, 2)  /* 8 waves, wave 128x64, two stages */                    \
-  X(2, 256, 128, 2, 4, 3)  /* 8 waves, wave 128x32 */                                \
-  X(3, 128, 256, 2, 4, 3)  /* 8 waves, wave 64x64 */                                 \
-  X(4, 256, 128, 2, 2, 2)  /* wave 128x64, two stages */                             \
-  X(5, 128, 128, 2, 2, 3)  /* wave 64x64 */                                          \
-  X(6, 64, 128, 1, 4, 3)   /* wave 64x32 */                                          \
-  X(7, 128, 64, 2, 2, 3)   /* wave 64x32 */                                          \
-  X(8, 64, 64, 2, 2, 3)    /* wave 32x32 */                                          \
-  X(9, 32, 128, 1, 4, 3)   /* wave 32x32 */                                          \
-  X(10, 128, 32, 4, 1, 3)  /* wave 32x32 */                                          \
-  X(11, 256, 64, 4, 1, 3)  /* wave 64x64 */                                          \
-  X(12, 64, 64, 2, 2, 2)   /* wave 32x32, two stages (short K) */                    \
-  X(13, 128, 64, 2, 2, 2)  /* wave 64x32, two stages (short K) */                    \
-  X(14, 64, 128, 1, 4, 2)  /* wave 64x32, two stages (short K) */                    \
-  X(15, 128, 128, 2, 2, 2) /* wave 64x64, two stages */                              \
-  X(16, 128, 256, 2, 4, 2) /* 8 waves, wave 64x64, two stages */                     \
-  X(17, 256, 128, 4, 2, 2) /* 8 waves, wave 64x64, two stages */
+// Tile configurations: id, BM x BN, waves WM x WN, pipeline stages, 16-byte chunks
+// per row of a K tile (8: 64 channels, 4: 32 channels; a narrower K tile fits more
+// stages in the same LDS), refill schedule (SP = 1: spread over two k-steps).
+// Every configuration sums each output's K in the same MFMA order, so the choice
+// never changes a result.  Each kernel is instantiated explicitly (the host pass
+// does not always emit the launch stub of an implicitly instantiated template).
+#define RAFIKI_MFMA_CONFIGS(X)                                                         \
+  X(0, 256, 256, 4, 2, 2, 8, 0)  /* 8 waves, wave 64x128, two stages */               \
+  X(1, 256, 256, 2, 4, 2, 8, 0)  /* 8 waves, wave 128x64, two stages */               \
+  X(2, 256, 128, 2, 4, 3, 8, 0)  /* 8 waves, wave 128x32 */                           \
+  X(3, 128, 256, 2, 4, 3, 8, 0)  /* 8 waves, wave 64x64 */                            \
+  X(4, 256, 128, 2, 2, 2, 8, 0)  /* wave 128x64, two stages */                        \
+  X(5, 128, 128, 2, 2, 3, 8, 0)  /* wave 64x64 */                                     \
+  X(6, 64, 128, 1, 4, 3, 8, 0)   /* wave 64x32 */                                     \
+  X(7, 128, 64, 2, 2, 3, 8, 0)   /* wave 64x32 */                                     \
+  X(8, 64, 64, 2, 2, 3, 8, 0)    /* wave 32x32 */                                     \
+  X(9, 32, 128, 1, 4, 3, 8, 0)   /* wave 32x32 */                                     \
+  X(10, 128, 32, 4, 1, 3, 8, 0)  /* wave 32x32 */                                     \
+  X(11, 256, 64, 4, 1, 3, 8, 0)  /* wave 64x64 */                                     \
+  X(12, 64, 64, 2, 2, 2, 8, 0)   /* wave 32x32, two stages (short K) */               \
+  X(13, 128, 64, 2, 2, 2, 8, 0)  /* wave 64x32, two stages (short K) */               \
+  X(14, 64, 128, 1, 4, 2, 8, 0)  /* wave 64x32, two stages (short K) */               \
+  X(15, 128, 128, 2, 2, 2, 8, 0) /* wave 64x64, two stages */                         \
+  X(16, 128, 256, 2, 4, 2, 8, 0) /* 8 waves, wave 64x64, two stages */                \
+  X(17, 256, 128, 4, 2, 2, 8, 0) /* 8 waves, wave 64x64, two stages */                \
+  X(18, 64, 128, 1, 4, 4, 4, 0)  /* 32-wide K tiles: wave 64x32, 4 stages */          \
+  X(19, 256, 256, 4, 2, 2, 8, 1) /* as 0, spread refill */                            \
+  X(20, 256, 256, 2, 4, 2, 8, 1) /* as 1, spread refill */                            \
+  X(21, 256, 128, 2, 4, 3, 8, 1) /* as 2, spread refill */                            \
+  X(22, 128, 256, 2, 4, 3, 8, 1) /* as 3, spread refill */                            \
+  X(23, 128, 256, 2, 4, 2, 8, 1) /* as 16, spread refill */                           \
+  X(24, 256, 128, 4, 2, 2, 8, 1) /* as 17, spread refill */                           \
+  X(25, 128, 128, 2, 2, 2, 8, 1) /* as 15, spread refill */
 
-#define RAFIKI_CFG_ENTRY(id, BM, BN, WM, WN, ST) {BM, BN, WM * WN, ST},
+#define RAFIKI_CFG_ENTRY(id, BM, BN, WM, WN, ST, KC, SP) {BM, BN, WM * WN, ST, KC * 8},
 const MfmaConfig kMfmaConfigs[kNumMfmaConfigs] = {RAFIKI_MFMA_CONFIGS(RAFIKI_CFG_ENTRY)};
 #undef RAFIKI_CFG_ENTRY
 
-#define RAFIKI_INSTANTIATE(id, BM, BN, WM, WN, ST)                              \
-  template __global__ void conv_mfma_kernel<BM, BN, WM, WN, ST, true>(ConvArgs); \
-  template __global__ void conv_mfma_kernel<BM, BN, WM, WN, ST, false>(ConvArgs);
+#define RAFIKI_INSTANTIATE(id, BM, BN, WM, WN, ST, KC, SP)                                      \
+  template __global__ void conv_mfma_kernel<BM, BN, WM, WN, ST, true, KC, false, SP>(ConvArgs);  \
+  template __global__ void conv_mfma_kernel<BM, BN, WM, WN, ST, false, KC, false, SP>(ConvArgs); \
+  template __global__ void conv_mfma_kernel<BM, BN, WM, WN, ST, true, KC, true, SP>(ConvArgs);   \
+  template __global__ void conv_mfma_kernel<BM, BN, WM, WN, ST, false, KC, true, SP>(ConvArgs);
 RAFIKI_MFMA_CONFIGS(RAFIKI_INSTANTIATE)
 #undef RAFIKI_INSTANTIATE
 
 hipError_t launch_conv_mfma(const ConvArgs& a, int cfg, int splits, hipStream_t s) {
   switch (cfg) {
-#define RAFIKI_CASE(id, BM, BN, WM, WN, ST) \
-    case id: return launch_mfma_cfg<BM, BN, WM, WN, ST>(a, splits, s);
+#define RAFIKI_CASE(id, BM, BN, WM, WN, ST, KC, SP) \
+    case id: return launch_mfma_cfg<BM, BN, WM, WN, ST, KC, SP>(a, splits, s);
     RAFIKI_MFMA_CONFIGS(RAFIKI_CASE)
 #undef RAFIKI_CASE
     default: return hipErrorInvalidValue;
