@@ -15,6 +15,8 @@
  *   rafiki_greedy_decide     the policy's decision for one queue state
  *   rafiki_greedy_simulate   event-driven simulation of one model serving an arrival
  *                            sequence (host only; no device needed)
+ *   rafiki_greedy_simulate_multi   the same for several independent servers sharing
+ *                            the queue (one model each)
  *   rafiki_ensemble_profile  measures c(b) (or c(m, b)) on the device
  *   rafiki_ensemble_serve_greedy        real-time serving: every batch runs all
  *                            selected models and combines them (the synchronous
@@ -80,6 +82,17 @@ int rafiki_greedy_decide(const rafiki_greedy_policy* policy, int64_t queue_len, 
 int rafiki_greedy_simulate(const rafiki_greedy_policy* policy, const int64_t* arrival_us, int64_t n_requests,
                            int64_t* out_latency_us, rafiki_dispatch* out_dispatch, int64_t dispatch_cap,
                            int64_t* out_n_dispatch);
+
+/* Simulate n_servers independent servers (for example one model each) sharing one
+ * FIFO queue: whenever a server is free (servers visited in index order), the greedy
+ * policy policies[k] (its own c(b)) decides a batch of the oldest queued requests for
+ * it.  Decisions are re-taken exactly when a request arrives, a server becomes free
+ * or a free server's deadline is reached.  Outputs as rafiki_greedy_simulate; each
+ * dispatch's `model` is its server.  n_servers in [1, 64].  This is the host model of
+ * rafiki_ensemble_serve_greedy_async with c(m, b) as given. */
+int rafiki_greedy_simulate_multi(const rafiki_greedy_policy* policies, int n_servers, const int64_t* arrival_us,
+                                 int64_t n_requests, int64_t* out_latency_us, rafiki_dispatch* out_dispatch,
+                                 int64_t dispatch_cap, int64_t* out_n_dispatch);
 
 /* Measure c(b) on the device: for every candidate b (1 <= b <= max_batch), the median
  * over `reps` (1..1000) timed runs of rafiki_ensemble_infer(h, batch, b, mask, ...)

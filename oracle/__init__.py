@@ -8,10 +8,10 @@ code with it.
 from .reference import (to_bf16_rne, conv2d, batchnorm, relu, maxpool2d, global_avgpool, fc,
                         embedding, conv1d_maxtime, concat, softmax, combine_mean, argmax_first,
                         run_model, ensemble, model_macs, combine_vote, ensemble_vote)
-from .scheduler import greedy_decide, simulate_greedy, serving_stats
+from .scheduler import greedy_decide, simulate_greedy, simulate_greedy_multi, serving_stats
 from . import rl
 
 __all__ = ["to_bf16_rne", "conv2d", "batchnorm", "relu", "maxpool2d", "global_avgpool", "fc",
            "embedding", "conv1d_maxtime", "concat", "softmax", "combine_mean", "argmax_first",
            "run_model", "ensemble", "model_macs", "combine_vote", "ensemble_vote",
-           "greedy_decide", "simulate_greedy", "serving_stats", "rl"]
+           "greedy_decide", "simulate_greedy", "simulate_greedy_multi", "serving_stats", "rl"]

@@ -88,3 +88,46 @@ def serving_stats(latency: Sequence[int], tau: int) -> dict:
     return {"requests": int(lat.size), "served": int(served.sum()),
             "overdue": int((lat[served] > tau).sum()),
             "mean_exceeding_us": float(exceed.sum() / max(lat.size, 1))}
+
+
+def simulate_greedy_multi(arrivals: Sequence[int], policies) -> Tuple[List[int], list]:
+    """Several independent servers (one model each) sharing the FIFO queue: whenever a
+    server is free, visited in index order, its own greedy policy (B, cost dict, tau,
+    delta) decides a batch of the oldest queued requests for it.  Returns (latency
+    per request or -1, dispatches (start, batch size, queue length, oldest wait,
+    server))."""
+    a = [int(x) for x in arrivals]
+    n = len(a)
+    lat = [-1] * n
+    disp = []
+    free_at = [None] * len(policies)      # None: never used
+    t = a[0] if n else 0
+    head = arrived = 0
+    while head < n:
+        while arrived < n and a[arrived] <= t:
+            arrived += 1
+        for k, (B, cost, tau, delta) in enumerate(policies):
+            if (free_at[k] is not None and free_at[k] > t) or arrived == head:
+                continue
+            b = greedy_decide(B, cost, arrived - head, t - a[head], tau, delta)
+            if b == 0:
+                continue
+            disp.append((t, b, arrived - head, t - a[head], k))
+            for i in range(head, head + b):
+                lat[i] = t + cost[b] - a[i]
+            head += b
+            free_at[k] = t + cost[b]
+        if head >= n:
+            break
+        cands = [a[arrived]] if arrived < n else []
+        for k, (B, cost, tau, delta) in enumerate(policies):
+            if free_at[k] is not None and free_at[k] > t:
+                cands.append(free_at[k])
+            elif arrived > head:
+                fitting = [x for x in B if x <= arrived - head]
+                if fitting:
+                    cands.append(a[head] + tau - delta - cost[max(fitting)])
+        if not cands:
+            break
+        t = min(cands)
+    return lat, disp

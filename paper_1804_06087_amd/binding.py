@@ -22,9 +22,11 @@ RAFIKI_INPUT_IMAGE_NCHW_F32, RAFIKI_INPUT_TOKENS_I32 = 0, 1
 EXPORTED = ("rafiki_ensemble_create", "rafiki_ensemble_infer", "rafiki_ensemble_infer_vote",
             "rafiki_ensemble_model_logits",
             "rafiki_ensemble_info", "rafiki_ensemble_trace", "rafiki_ensemble_trace_read",
-            "rafiki_ensemble_destroy", "rafiki_greedy_decide", "rafiki_greedy_simulate",
+            "rafiki_ensemble_destroy", "rafiki_greedy_decide", "rafiki_greedy_simulate", "rafiki_greedy_simulate_multi",
             "rafiki_ensemble_profile", "rafiki_ensemble_serve_greedy", "rafiki_ensemble_serve_greedy_async",
-            "rafiki_last_error")
+            "rafiki_rl_create", "rafiki_rl_destroy", "rafiki_rl_info", "rafiki_rl_get_params", "rafiki_rl_set_params",
+            "rafiki_rl_forward", "rafiki_rl_gradient", "rafiki_rl_adam_step", "rafiki_rl_run_episode",
+            "rafiki_rl_train", "rafiki_last_error")
 KERNEL_CLASSES = ("conv_mfma", "splitk_reduce", "conv_f32", "stage", "pool", "embed", "concat", "combine", "vote")
 
 _fp = C.POINTER(C.c_float)
@@ -38,6 +40,12 @@ class RafikiGreedyPolicy(C.Structure):
 class RafikiDispatch(C.Structure):
     _fields_ = [("start_us", C.c_int64), ("end_us", C.c_int64), ("first", C.c_int64), ("queue_len", C.c_int64),
                 ("oldest_wait_us", C.c_int64), ("b", C.c_int32), ("model", C.c_int32)]
+
+
+class RafikiRLConfig(C.Structure):
+    _fields_ = [("n_models", C.c_int), ("batch_sizes", C.POINTER(C.c_int32)), ("n_sizes", C.c_int),
+                ("cost_us", C.POINTER(C.c_int64)), ("accuracy", C.POINTER(C.c_double)), ("tau_us", C.c_int64),
+                ("beta", C.c_double), ("queue_features", C.c_int), ("hidden", C.c_int)]
 
 
 DISPATCH_FIELDS = ("start_us", "end_us", "first", "queue_len", "oldest_wait_us", "b", "model")
@@ -96,6 +104,22 @@ def load_library(path: str = LIB_PATH):
     lib.rafiki_greedy_decide.argtypes = [P(RafikiGreedyPolicy), C.c_int64, C.c_int64, P(C.c_int32)]
     lib.rafiki_greedy_simulate.argtypes = [P(RafikiGreedyPolicy), P(C.c_int64), C.c_int64, P(C.c_int64),
                                            P(RafikiDispatch), C.c_int64, P(C.c_int64)]
+    lib.rafiki_greedy_simulate_multi.argtypes = [P(RafikiGreedyPolicy), C.c_int, P(C.c_int64), C.c_int64,
+                                                 P(C.c_int64), P(RafikiDispatch), C.c_int64, P(C.c_int64)]
+    D = P(C.c_double)
+    lib.rafiki_rl_create.argtypes = [P(RafikiRLConfig), C.c_uint64, P(C.c_void_p)]
+    lib.rafiki_rl_destroy.argtypes = [C.c_void_p]
+    lib.rafiki_rl_info.argtypes = [C.c_void_p, P(C.c_int), P(C.c_int), P(C.c_int64)]
+    lib.rafiki_rl_get_params.argtypes = [C.c_void_p, D, C.c_int64]
+    lib.rafiki_rl_set_params.argtypes = [C.c_void_p, D, C.c_int64]
+    lib.rafiki_rl_forward.argtypes = [C.c_void_p, D, D, D]
+    lib.rafiki_rl_gradient.argtypes = [C.c_void_p, D, P(C.c_int32), D, C.c_int64, C.c_double, C.c_double, D]
+    lib.rafiki_rl_adam_step.argtypes = [C.c_void_p, D, C.c_double]
+    lib.rafiki_rl_run_episode.argtypes = [C.c_void_p, P(C.c_int64), C.c_int64, C.c_int, P(C.c_int32), C.c_int64,
+                                          C.c_uint64, P(C.c_int32), D, D, P(C.c_int64), C.c_int64, P(C.c_int64),
+                                          P(C.c_int64)]
+    lib.rafiki_rl_train.argtypes = [C.c_void_p, P(C.c_int64), C.c_int64, C.c_int, C.c_double, C.c_double,
+                                    C.c_double, C.c_double, C.c_uint64, D]
     lib.rafiki_ensemble_profile.argtypes = [C.c_void_p, C.c_void_p, P(C.c_int32), C.c_int, C.c_uint32, C.c_int,
                                             C.c_void_p, C.c_void_p, P(C.c_int64), C.c_void_p]
     lib.rafiki_ensemble_serve_greedy.argtypes = [C.c_void_p, C.c_void_p, P(C.c_int64), C.c_int64,
@@ -200,6 +224,117 @@ def greedy_simulate(arrival_us, batch_sizes, cost_us, tau_us: int, delta_us: int
     _check(lib.rafiki_greedy_simulate(C.byref(p), _i64p(a), a.size, _i64p(lat), disp if cap else None, cap,
                                       C.byref(nd)))
     return lat, dispatches_to_array(disp, min(nd.value, cap)), nd.value
+
+
+def greedy_simulate_multi(arrival_us, policies):
+    """Host simulation of independent servers sharing the queue; ``policies`` is a list
+    of (batch_sizes, cost_us, tau_us, delta_us).  Returns (latency_us, dispatches)."""
+    lib = load_library()
+    keep = []
+    pols = (RafikiGreedyPolicy * len(policies))()
+    for k, p in enumerate(policies):
+        pols[k] = make_policy(*p, keep)
+    a = np.ascontiguousarray(arrival_us, dtype=np.int64)
+    lat = np.zeros(a.size, dtype=np.int64)
+    cap = a.size + 1
+    disp = (RafikiDispatch * cap)()
+    nd = C.c_int64(0)
+    _check(lib.rafiki_greedy_simulate_multi(pols, len(policies), _i64p(a), a.size, _i64p(lat), disp, cap,
+                                            C.byref(nd)))
+    return lat, dispatches_to_array(disp, nd.value)
+
+
+def _f64p(a: np.ndarray):
+    return a.ctypes.data_as(C.POINTER(C.c_double))
+
+
+class RLScheduler:
+    """Handle over rafiki_rl_*: the actor-critic batch-size and model-subset scheduler."""
+
+    def __init__(self, batch_sizes, cost_us, accuracy, tau_us: int, beta: float, queue_features: int = 128,
+                 hidden: int = 64, seed: int = 0):
+        lib = load_library()
+        cost = np.ascontiguousarray(cost_us, dtype=np.int64)
+        self._B = np.ascontiguousarray(batch_sizes, dtype=np.int32)
+        self._cost = np.ascontiguousarray(cost.reshape(-1))
+        self._acc = np.ascontiguousarray(accuracy, dtype=np.float64)
+        cfg = RafikiRLConfig()
+        cfg.n_models, cfg.n_sizes = cost.shape[0], self._B.size
+        cfg.batch_sizes, cfg.cost_us, cfg.accuracy = _i32p(self._B), _i64p(self._cost), _f64p(self._acc)
+        cfg.tau_us, cfg.beta, cfg.queue_features, cfg.hidden = int(tau_us), float(beta), queue_features, hidden
+        h = C.c_void_p()
+        _check(lib.rafiki_rl_create(C.byref(cfg), seed, C.byref(h)))
+        self._h, self._lib = h, lib
+        d, a, n = C.c_int(), C.c_int(), C.c_int64()
+        _check(lib.rafiki_rl_info(h, C.byref(d), C.byref(a), C.byref(n)))
+        self.state_dim, self.n_actions, self.n_params = d.value, a.value, n.value
+
+    def params(self) -> np.ndarray:
+        out = np.zeros(self.n_params)
+        _check(self._lib.rafiki_rl_get_params(self._h, _f64p(out), self.n_params))
+        return out
+
+    def set_params(self, theta):
+        t = np.ascontiguousarray(theta, dtype=np.float64)
+        _check(self._lib.rafiki_rl_set_params(self._h, _f64p(t), t.size))
+
+    def forward(self, state):
+        s = np.ascontiguousarray(state, dtype=np.float64)
+        pi = np.zeros(self.n_actions)
+        v = C.c_double()
+        _check(self._lib.rafiki_rl_forward(self._h, _f64p(s), _f64p(pi), C.byref(v)))
+        return pi, v.value
+
+    def gradient(self, states, actions, returns, c_v: float, c_e: float) -> np.ndarray:
+        S = np.ascontiguousarray(states, dtype=np.float64)
+        A = np.ascontiguousarray(actions, dtype=np.int32)
+        R = np.ascontiguousarray(returns, dtype=np.float64)
+        g = np.zeros(self.n_params)
+        _check(self._lib.rafiki_rl_gradient(self._h, _f64p(S), _i32p(A), _f64p(R), R.size, c_v, c_e, _f64p(g)))
+        return g
+
+    def adam_step(self, grad, lr: float):
+        g = np.ascontiguousarray(grad, dtype=np.float64)
+        _check(self._lib.rafiki_rl_adam_step(self._h, _f64p(g), lr))
+
+    def run_episode(self, arrival_us, mode: str = "argmax", actions=None, seed: int = 0):
+        """mode 'given' (actions), 'sample' or 'argmax'.  Returns a dict of numpy arrays:
+        actions, rewards, states, times (per decision) and latency (per request)."""
+        a = np.ascontiguousarray(arrival_us, dtype=np.int64)
+        acts_in = np.ascontiguousarray(actions if actions is not None else [], dtype=np.int32)
+        cap = a.size
+        out_a = np.zeros(cap, dtype=np.int32)
+        out_r = np.zeros(cap)
+        out_s = np.zeros((cap, self.state_dim))
+        out_t = np.zeros(cap, dtype=np.int64)
+        lat = np.zeros(a.size, dtype=np.int64)
+        steps = C.c_int64()
+        m = {"given": 0, "sample": 1, "argmax": 2}[mode]
+        _check(self._lib.rafiki_rl_run_episode(self._h, _i64p(a), a.size, m, _i32p(acts_in), acts_in.size, seed,
+                                               _i32p(out_a), _f64p(out_r), _f64p(out_s), _i64p(out_t), cap,
+                                               C.byref(steps), _i64p(lat)))
+        k = steps.value
+        return {"actions": out_a[:k], "rewards": out_r[:k], "states": out_s[:k], "times": out_t[:k],
+                "latency": lat}
+
+    def train(self, arrival_us, episodes: int, gamma: float = 0.99, lr: float = 1e-3, c_v: float = 0.5,
+              c_e: float = 0.01, seed: int = 0) -> np.ndarray:
+        a = np.ascontiguousarray(arrival_us, dtype=np.int64)
+        out = np.zeros(episodes)
+        _check(self._lib.rafiki_rl_train(self._h, _i64p(a), a.size, episodes, gamma, lr, c_v, c_e, seed,
+                                         _f64p(out)))
+        return out
+
+    def close(self):
+        if getattr(self, "_h", None) is not None and self._h.value:
+            self._lib.rafiki_rl_destroy(self._h)
+        self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
 
 
 def make_layers(spec, params, keep: list):

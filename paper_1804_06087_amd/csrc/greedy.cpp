@@ -4,6 +4,7 @@
 
 #include <algorithm>
 #include <climits>
+#include <vector>
 
 namespace rafiki {
 
@@ -116,6 +117,54 @@ int rafiki_greedy_simulate(const rafiki_greedy_policy* policy, const int64_t* ar
     int64_t next = arrived < n ? a[arrived] : INT64_MAX;
     next = std::min(next, greedy_deadline(p, qlen, a[head]));
     if (next == INT64_MAX) break;     // below min(B) with no further arrivals
+    t = next;
+  }
+  *out_n_dispatch = nd;
+  return RAFIKI_OK;
+}
+
+int rafiki_greedy_simulate_multi(const rafiki_greedy_policy* policies, int n_servers, const int64_t* arrival_us,
+                                 int64_t n_requests, int64_t* out_latency_us, rafiki_dispatch* out_dispatch,
+                                 int64_t dispatch_cap, int64_t* out_n_dispatch) {
+  if (!policies || n_servers < 1 || n_servers > 64)
+    return set_error(RAFIKI_ERR_INVALID, "null policies or n_servers outside [1, 64]");
+  for (int k = 0; k < n_servers; ++k)
+    if (int rc = check_policy(&policies[k])) return rc;
+  int rc = check_arrivals(arrival_us, n_requests);
+  if (rc) return rc;
+  if ((n_requests > 0 && !out_latency_us) || !out_n_dispatch || dispatch_cap < 0 ||
+      (dispatch_cap > 0 && !out_dispatch))
+    return set_error(RAFIKI_ERR_INVALID, "null output or negative dispatch_cap");
+  const int64_t* a = arrival_us;
+  const int64_t n = n_requests;
+  std::fill(out_latency_us, out_latency_us + n, int64_t(-1));
+  std::vector<int64_t> free_at(n_servers, INT64_MIN);
+  int64_t nd = 0, t = n ? a[0] : 0, head = 0, arrived = 0;
+  while (head < n) {
+    while (arrived < n && a[arrived] <= t) ++arrived;
+    for (int k = 0; k < n_servers; ++k) {   // free servers in index order
+      if (free_at[k] > t || arrived == head) continue;
+      const rafiki_greedy_policy& p = policies[k];
+      const int64_t qlen = arrived - head, wait = t - a[head];
+      const int32_t b = greedy_decide(p, qlen, wait);
+      if (b == 0) continue;
+      int64_t cost = 0;
+      for (int i = 0; i < p.n_sizes; ++i)
+        if (p.batch_sizes[i] == b) cost = p.cost_us[i];
+      const int64_t done = t + cost;
+      for (int64_t i = head; i < head + b; ++i) out_latency_us[i] = done - a[i];
+      if (nd < dispatch_cap) out_dispatch[nd] = {t, done, head, qlen, wait, b, k};
+      ++nd;
+      head += b;
+      free_at[k] = done;
+    }
+    if (head >= n) break;
+    int64_t next = arrived < n ? a[arrived] : INT64_MAX;
+    for (int k = 0; k < n_servers; ++k) {
+      if (free_at[k] > t) next = std::min(next, free_at[k]);
+      else if (arrived > head) next = std::min(next, greedy_deadline(policies[k], arrived - head, a[head]));
+    }
+    if (next == INT64_MAX) break;   // nothing running, nothing servable, nothing arriving
     t = next;
   }
   *out_n_dispatch = nd;
