@@ -64,6 +64,11 @@ def parse():
                          "an independent server (async); prints one JSON line of serving statistics")
     ap.add_argument("--cycles", type=float, default=1.0, help="serving: sine cycles of 500 tau to serve")
     ap.add_argument("--period-taus", type=int, default=500, help="serving: sine period in units of tau")
+    ap.add_argument("--sweep", action="store_true",
+                    help="latency/throughput trade-off of the ResNet-50 + VGG-16 + ResNet-101 subsets {R50}, "
+                         "{R50, VGG-16}, {all} at batch sizes 1, 4, 16, 64, 256: one JSON line per point with "
+                         "p50/p99 batch latency and images/s")
+    ap.add_argument("--sweep-calls", type=int, default=200, help="sweep: timed calls per point")
     return ap.parse_args()
 
 
@@ -211,6 +216,53 @@ def serve_main(args, dev):
     print(json.dumps(out), flush=True)
 
 
+def sweep_main(args, dev):
+    """Latency/accuracy trade-off grid (Section 5.2): every subset of the ImageNet-shaped
+    ensemble at every batch size, one handle (max batch 256) over one 256-image draw whose
+    prefixes are the batches.  Per point: 20 warm-up calls, then timed calls each bracketed
+    by events on the launch stream and synchronised; p50/p99 latency, images/s = n / p50."""
+    import numpy as np
+    import torch
+
+    import workloads as wl
+    from paper_1804_06087_amd import Ensemble
+
+    cfg, specs, params, pool = wl.build_config(4)
+    C = specs[0].n_classes
+    ens = Ensemble(specs, params, precision=cfg.precision, max_batch=max(cfg.batches))
+    xpool = torch.from_numpy(pool).to(dev)
+    probs = torch.empty((max(cfg.batches), C), dtype=torch.float32, device=dev)
+    labels = torch.empty((max(cfg.batches),), dtype=torch.int32, device=dev)
+    stream = torch.cuda.current_stream()
+    names = ["resnet50", "vgg16", "resnet101"]
+    for mask in cfg.masks:
+        for n in cfg.batches:
+            x = xpool[:n]
+            for _ in range(20):
+                ens.infer(x, n, mask, probs, labels, stream)
+            torch.cuda.synchronize()
+            lat = []
+            t_end = time.perf_counter() + 1.0
+            while len(lat) < args.sweep_calls or time.perf_counter() < t_end:
+                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record(stream)
+                ens.infer(x, n, mask, probs, labels, stream)
+                b.record(stream)
+                b.synchronize()
+                lat.append(a.elapsed_time(b))
+            lat = np.array(lat)
+            p50 = float(np.percentile(lat, 50))
+            print(json.dumps({
+                "metric": "ensemble images/sec and batch latency, subset/batch-size sweep",
+                "value": round(n / (p50 / 1e3), 2), "unit": "images/s", "n_gpus": 1, "higher_is_better": True,
+                "dtype": "bf16", "data": "synthetic (seeded N(0,1) images rounded to bf16, random-init weights)",
+                "config": {"workload": "+".join(names[m] for m in range(3) if (mask >> m) & 1)
+                           + f", batch {n} of 3x224x224", "mask": mask, "global_batch": n},
+                "p50_ms": round(p50, 4), "p99_ms": round(float(np.percentile(lat, 99)), 4),
+                "calls": int(lat.size)}), flush=True)
+    ens.close()
+
+
 def main():
     args = parse()
     if args.summarize_pmc:
@@ -236,6 +288,9 @@ def main():
     dev = torch.device("cuda:0")
     if args.serve:
         serve_main(args, dev)
+        return
+    if args.sweep:
+        sweep_main(args, dev)
         return
 
     if args.workload == "c4":

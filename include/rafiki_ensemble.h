@@ -191,6 +191,19 @@ int rafiki_ensemble_trace(rafiki_ensemble_t h, int enable);
  * keep them (call again with a larger buffer).  Host-blocking. */
 int rafiki_ensemble_trace_read(rafiki_ensemble_t h, rafiki_trace_rec* out, int cap, int* count);
 
+/* Diagnostics: tile configurations of the bf16 GEMM kernel.  Configuration `cfg`
+ * (0 .. count - 1) computes output tiles of bm pixels x bn channels with `waves`
+ * wavefronts, `stages` K tiles of bk channels in flight.  Every configuration sums each
+ * output's K terms in the same order, so all of them give bitwise-identical results.
+ * Returns RAFIKI_ERR_INVALID past the last configuration; null outputs are skipped. */
+int rafiki_tile_config(int cfg, int* bm, int* bn, int* waves, int* stages, int* bk);
+
+/* Diagnostics: make every subsequent unsplit bf16 GEMM launch of the handle use tile
+ * configuration `cfg` wherever its channel tile suits the layer's output channels
+ * (other layers keep their tuned choice); cfg = -1 restores the tuned choice.  Results
+ * are unchanged; only speed differs. */
+int rafiki_ensemble_force_tile(rafiki_ensemble_t h, int cfg);
+
 /* Synchronise the device, free everything the handle owns.  NULL is accepted. */
 int rafiki_ensemble_destroy(rafiki_ensemble_t h);
 

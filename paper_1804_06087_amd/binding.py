@@ -22,6 +22,7 @@ RAFIKI_INPUT_IMAGE_NCHW_F32, RAFIKI_INPUT_TOKENS_I32 = 0, 1
 EXPORTED = ("rafiki_ensemble_create", "rafiki_ensemble_infer", "rafiki_ensemble_infer_vote",
             "rafiki_ensemble_model_logits",
             "rafiki_ensemble_info", "rafiki_ensemble_trace", "rafiki_ensemble_trace_read",
+            "rafiki_tile_config", "rafiki_ensemble_force_tile",
             "rafiki_ensemble_destroy", "rafiki_greedy_decide", "rafiki_greedy_simulate", "rafiki_greedy_simulate_multi",
             "rafiki_ensemble_profile", "rafiki_ensemble_serve_greedy", "rafiki_ensemble_serve_greedy_async",
             "rafiki_rl_create", "rafiki_rl_destroy", "rafiki_rl_info", "rafiki_rl_get_params", "rafiki_rl_set_params",
@@ -100,6 +101,8 @@ def load_library(path: str = LIB_PATH):
     lib.rafiki_ensemble_destroy.argtypes = [C.c_void_p]
     lib.rafiki_ensemble_trace.argtypes = [C.c_void_p, C.c_int]
     lib.rafiki_ensemble_trace_read.argtypes = [C.c_void_p, C.POINTER(RafikiTraceRec), C.c_int, C.POINTER(C.c_int)]
+    lib.rafiki_tile_config.argtypes = [C.c_int] + [C.POINTER(C.c_int)] * 5
+    lib.rafiki_ensemble_force_tile.argtypes = [C.c_void_p, C.c_int]
     P = C.POINTER
     lib.rafiki_greedy_decide.argtypes = [P(RafikiGreedyPolicy), C.c_int64, C.c_int64, P(C.c_int32)]
     lib.rafiki_greedy_simulate.argtypes = [P(RafikiGreedyPolicy), P(C.c_int64), C.c_int64, P(C.c_int64),
@@ -355,6 +358,17 @@ def make_layers(spec, params, keep: list):
     return arr
 
 
+def tile_configs():
+    """The bf16 GEMM kernel's tile configurations: list of dicts {bm, bn, waves, stages, bk}."""
+    lib = load_library()
+    out = []
+    while True:
+        v = [C.c_int() for _ in range(5)]
+        if lib.rafiki_tile_config(len(out), *[C.byref(x) for x in v]) != RAFIKI_OK:
+            return out
+        out.append(dict(zip(("bm", "bn", "waves", "stages", "bk"), (x.value for x in v))))
+
+
 class Ensemble:
     """Handle over ``rafiki_ensemble_create`` .. ``rafiki_ensemble_destroy``."""
 
@@ -448,6 +462,10 @@ class Ensemble:
 
     def trace(self, enable: bool):
         _check(self._lib.rafiki_ensemble_trace(self._h, 1 if enable else 0))
+
+    def force_tile(self, cfg: int):
+        """Use tile configuration ``cfg`` for every unsplit bf16 GEMM it suits (-1: tuned)."""
+        _check(self._lib.rafiki_ensemble_force_tile(self._h, cfg))
 
     def trace_read(self):
         """List of dicts {kind, model, layer, flops, bytes, ms} for the traced launches."""

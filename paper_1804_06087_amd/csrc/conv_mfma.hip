@@ -483,7 +483,16 @@ __global__ void splitk_reduce_kernel(ConvArgs a, int splits, int in_bf16) {
   X(22, 128, 256, 2, 4, 3, 8, 1) /* as 3, spread refill */                            \
   X(23, 128, 256, 2, 4, 2, 8, 1) /* as 16, spread refill */                           \
   X(24, 256, 128, 4, 2, 2, 8, 1) /* as 17, spread refill */                           \
-  X(25, 128, 128, 2, 2, 2, 8, 1) /* as 15, spread refill */
+  X(25, 128, 128, 2, 2, 2, 8, 1) /* as 15, spread refill */                           \
+  X(26, 256, 256, 4, 2, 4, 4, 0) /* 8 waves, wave 64x128, 32-wide K, 4 stages */      \
+  X(27, 256, 256, 4, 2, 5, 4, 0) /* 8 waves, wave 64x128, 32-wide K, 5 stages */      \
+  X(28, 256, 128, 4, 2, 6, 4, 0) /* 8 waves, wave 64x64, 32-wide K, 6 stages */       \
+  X(29, 128, 256, 2, 4, 6, 4, 0) /* 8 waves, wave 64x64, 32-wide K, 6 stages */       \
+  X(30, 128, 128, 2, 2, 5, 8, 0) /* wave 64x64, 5 stages */                           \
+  X(31, 128, 128, 2, 2, 4, 8, 0) /* wave 64x64, 4 stages */                           \
+  X(32, 256, 256, 2, 2, 2, 8, 0) /* 4 waves, wave 128x128, two stages */              \
+  X(33, 256, 256, 2, 2, 4, 4, 0) /* 4 waves, wave 128x128, 32-wide K, 4 stages */      \
+  X(34, 256, 32, 4, 1, 3, 8, 0)  /* wave 64x32 */
 
 #define RAFIKI_CFG_ENTRY(id, BM, BN, WM, WN, ST, KC, SP) {BM, BN, WM * WN, ST, KC * 8},
 const MfmaConfig kMfmaConfigs[kNumMfmaConfigs] = {RAFIKI_MFMA_CONFIGS(RAFIKI_CFG_ENTRY)};

@@ -111,22 +111,54 @@ hipError_t launch_maxpool(const void* x, void* y, int N, int H, int W, int Cs, i
 }
 
 // ---------------------------------------------------------------- GAP / max over time
-// One thread per (image, 8-channel group); positions summed in order in fp32.
-__global__ void spatial_reduce_kernel(const void* __restrict__ x, void* y, int N, int HW, int Cs, int is_max,
-                                      int bf16) {
-  const int groups = Cs / 8;
-  const long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= (long long)N * groups) return;
-  const int g = (int)(idx % groups);
-  const long long n = idx / groups;
+// Block (image n, chunk of GB 8-channel groups); the 256 threads form P = 256 / GB
+// position slices of GB groups.  Thread (slice s, group g) reduces positions s, s + P,
+// s + 2P, ... in increasing order (four 16-byte loads in flight), then thread (0, g)
+// folds the P partial results in slice order.  The order is fixed, so results are
+// deterministic; sums are fp32.
+constexpr int kReduceThreads = 256;
+
+__global__ __launch_bounds__(kReduceThreads) void spatial_reduce_kernel(const void* __restrict__ x, void* y, int HW,
+                                                                        int Cs, int GB, int is_max, int bf16) {
+  __shared__ float part[kReduceThreads * 8];
+  const int G = Cs / 8, P = kReduceThreads / GB;
+  const int t = threadIdx.x, gl = t % GB, sl = t / GB;
+  const int g = blockIdx.y * GB + gl;
+  const long long n = blockIdx.x;
+  const float init = is_max ? -INFINITY : 0.f;
   float acc[8];
 #pragma unroll
-  for (int j = 0; j < 8; ++j) acc[j] = is_max ? -INFINITY : 0.f;
-  for (int p = 0; p < HW; ++p) {
-    float q[8];
-    load8(x, (n * HW + p) * Cs + g * 8, bf16, q);
+  for (int j = 0; j < 8; ++j) acc[j] = init;
+  auto fold = [&](const float q[8]) {
 #pragma unroll
     for (int j = 0; j < 8; ++j) acc[j] = is_max ? fmaxf(acc[j], q[j]) : acc[j] + q[j];
+  };
+  if (sl < P && g < G) {
+    const long long base = n * HW * Cs + g * 8;
+    int p = sl;
+    for (; p + 3 * P < HW; p += 4 * P) {
+      float q0[8], q1[8], q2[8], q3[8];
+      load8(x, base + (long long)p * Cs, bf16, q0);
+      load8(x, base + (long long)(p + P) * Cs, bf16, q1);
+      load8(x, base + (long long)(p + 2 * P) * Cs, bf16, q2);
+      load8(x, base + (long long)(p + 3 * P) * Cs, bf16, q3);
+      fold(q0); fold(q1); fold(q2); fold(q3);
+    }
+    for (; p < HW; p += P) {
+      float q[8];
+      load8(x, base + (long long)p * Cs, bf16, q);
+      fold(q);
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < 8; ++j) part[t * 8 + j] = acc[j];
+  __syncthreads();
+  if (sl != 0 || g >= G) return;
+  for (int r = 1; r < P; ++r) {
+    float q[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) q[j] = part[(r * GB + gl) * 8 + j];
+    fold(q);
   }
   if (!is_max) {
     const float inv = 1.0f / (float)HW;
@@ -138,9 +170,10 @@ __global__ void spatial_reduce_kernel(const void* __restrict__ x, void* y, int N
 
 hipError_t launch_spatial_reduce(const void* x, void* y, int N, int HW, int Cs, int is_max, int bf16,
                                  hipStream_t s) {
-  const long long total = (long long)N * (Cs / 8);
-  hipLaunchKernelGGL(spatial_reduce_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, x, y, N, HW,
-                     Cs, is_max, bf16);
+  const int G = Cs / 8;
+  const int GB = G < 64 ? G : 64;
+  const dim3 grid((unsigned)N, (unsigned)((G + GB - 1) / GB));
+  hipLaunchKernelGGL(spatial_reduce_kernel, grid, dim3(kReduceThreads), 0, s, x, y, HW, Cs, GB, is_max, bf16);
   return hipGetLastError();
 }
 

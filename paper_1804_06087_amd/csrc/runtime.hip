@@ -157,6 +157,7 @@ struct rafiki_ensemble_s {
   // Tuned tile configuration per batch size, model and op (-1: not a GEMM op).
   std::map<int, std::vector<std::vector<int>>> tuned;
   bool autotune = true;
+  int force_tile = -1;              // diagnostic override of the tuned configuration
   size_t esz() const { return precision == RAFIKI_BF16 ? 2 : 4; }
   ~rafiki_ensemble_s() {
     for (Model& M : models) {
@@ -635,7 +636,8 @@ int run_model(const rafiki_ensemble_s* e, int mi, const void* in, int n, float* 
       case O_CONV:
       case O_CONV1D: {
         ConvArgs a = gemm_args(e, M, op, n, in);
-        const int cfg = cfgs.empty() ? -1 : cfgs[&op - M.ops.data()];
+        int cfg = cfgs.empty() ? -1 : cfgs[&op - M.ops.data()];
+        if (e->force_tile >= 0 && cfg_fits(e->force_tile, op.c_out)) cfg = e->force_tile;
         if (op.kind == O_CONV1D) {
           void* tmp = M.d_arena + op.tmp_off;
           a.y = tmp; a.c_write = round_up(op.c_out, 8); a.ldy = a.c_write; a.out_f32 = bf ? 0 : 1;
@@ -899,6 +901,24 @@ int rafiki_ensemble_trace_read(rafiki_ensemble_t h, rafiki_trace_rec* out, int c
   }
   h->trace.recs.clear();
   h->trace.used = 0;
+  return RAFIKI_OK;
+}
+
+int rafiki_tile_config(int cfg, int* bm, int* bn, int* waves, int* stages, int* bk) {
+  if (cfg < 0 || cfg >= kNumMfmaConfigs) return fail(RAFIKI_ERR_INVALID, "no such tile configuration");
+  const MfmaConfig& c = kMfmaConfigs[cfg];
+  if (bm) *bm = c.bm;
+  if (bn) *bn = c.bn;
+  if (waves) *waves = c.waves;
+  if (stages) *stages = c.stages;
+  if (bk) *bk = c.bk;
+  return RAFIKI_OK;
+}
+
+int rafiki_ensemble_force_tile(rafiki_ensemble_t h, int cfg) {
+  if (!h) return fail(RAFIKI_ERR_INVALID, "null handle");
+  if (cfg < -1 || cfg >= kNumMfmaConfigs) return fail(RAFIKI_ERR_INVALID, "no such tile configuration");
+  h->force_tile = cfg;
   return RAFIKI_OK;
 }
 
