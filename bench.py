@@ -337,6 +337,15 @@ def main():
     torch.cuda.synchronize()
     ms_per_step = ev0.elapsed_time(ev1) / args.steps
 
+    # ---- host cost of enqueueing one step (device idle, no synchronisation inside)
+    host = []
+    for _ in range(5):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        serve(x, n, mask, probs, labels, stream)
+        host.append((time.perf_counter() - t0) * 1e3)
+    torch.cuda.synchronize()
+
     # ---- latency: each step on its own, events on the launch stream
     lat = []
     for _ in range(max(args.steps, 10)):
@@ -418,6 +427,7 @@ def main():
                    "input": "int32 tokens [n, 256]" if tokens else "float32 NCHW images"},
         "p50_ms": round(float(np.percentile(lat, 50)), 4),
         "p99_ms": round(float(np.percentile(lat, 99)), 4),
+        "host_enqueue_ms": round(float(np.median(host)), 4),
         "mfma_util_step": round(step_flops / (ms_per_step / 1e3) / 1e12 / PEAK_BF16_TFLOPS, 4)
         if precision == "bf16" else None,
         "alg_tflop_per_step": round(step_flops / 1e12, 4),

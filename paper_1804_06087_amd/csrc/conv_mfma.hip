@@ -332,33 +332,50 @@ __global__ __launch_bounds__(WM * WN * 64) void conv_mfma_kernel(ConvArgs a) {
   // (16-byte chunks swizzled by swz(pixel)); each lane then reads 8 channels of one
   // pixel back, adds the residual (16-byte load), applies ReLU, rounds to bf16 and
   // writes 16 bytes.  The residual add and the single rounding match the direct form.
+  // A group's residual, scale and shift loads are all issued before its staging
+  // writes, so their latency is paid once per group rather than once per pass.
   static_assert(NW * WTM * 32 * 4 <= STAGES * STAGE_CHUNKS * 16, "epilogue staging fits in the LDS ring");
-  __syncthreads();   // every wave is done with the ring
+  constexpr int NPASS = WTM / 16;
+  const bool bf_res = a.res != nullptr && !a.out_f32;
   float4* stg = (float4*)lds + wave * (WTM * 8);
   const int oq = lane & 3, pl = lane >> 2;   // read phase: channel octet oq of pixel pl (+16 per pass)
+  __syncthreads();   // every wave is done with the ring
 #pragma unroll
   for (int tn = 0; tn < TN; ++tn) {
     // one 32-channel group at a time: keeps the accumulators in place until used
     __builtin_amdgcn_sched_barrier(0);
     const int cb = n0 + wn * WTN + tn * 32;   // first channel of this 32-channel group
+    const int c = cb + 8 * oq;
+    uint4 rv[NPASS];
+    if (bf_res) {
+#pragma unroll
+      for (int pass = 0; pass < NPASS; ++pass) {
+        const int m = m0 + wm * WTM + pass * 16 + pl;
+        rv[pass] = (m < a.M && c < a.c_write) ? *(const uint4*)((const bf16_t*)a.res + (long long)m * a.ldy + c)
+                                              : make_uint4(0u, 0u, 0u, 0u);
+      }
+    }
+    float4 sc[4], sh[4];
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      sc[g] = *(const float4*)(a.scale + cb + 8 * g + 4 * fk);
+      sh[g] = *(const float4*)(a.shift + cb + 8 * g + 4 * fk);
+    }
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
       const int cl = 8 * g + 4 * fk;          // local channel of this lane's 4 values
-      const float4 sc = *(const float4*)(a.scale + cb + cl);
-      const float4 sh = *(const float4*)(a.shift + cb + cl);
 #pragma unroll
       for (int tm = 0; tm < TM; ++tm) {
         const int p = tm * 32 + frow;
         stg[p * 8 + ((cl >> 2) ^ swz<8>(p))] =
-            make_float4(acc[tn][tm][4 * g + 0] * sc.x + sh.x, acc[tn][tm][4 * g + 1] * sc.y + sh.y,
-                        acc[tn][tm][4 * g + 2] * sc.z + sh.z, acc[tn][tm][4 * g + 3] * sc.w + sh.w);
+            make_float4(acc[tn][tm][4 * g + 0] * sc[g].x + sh[g].x, acc[tn][tm][4 * g + 1] * sc[g].y + sh[g].y,
+                        acc[tn][tm][4 * g + 2] * sc[g].z + sh[g].z, acc[tn][tm][4 * g + 3] * sc[g].w + sh[g].w);
       }
     }
     __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): this wave's LDS writes have landed
     __builtin_amdgcn_wave_barrier();
-    const int c = cb + 8 * oq;
 #pragma unroll
-    for (int pass = 0; pass < WTM / 16; ++pass) {
+    for (int pass = 0; pass < NPASS; ++pass) {
       const int p = pass * 16 + pl;
       const int m = m0 + wm * WTM + p;
       const float4 lo = stg[p * 8 + ((2 * oq) ^ swz<8>(p))];
@@ -376,8 +393,8 @@ __global__ __launch_bounds__(WM * WN * 64) void conv_mfma_kernel(ConvArgs a) {
         }
         continue;
       }
-      if (a.res) {
-        const uint4 r = *(const uint4*)((const bf16_t*)a.res + o);
+      if (bf_res) {
+        const uint4 r = rv[pass];
         v[0] += bf2f_m(r.x & 0xFFFFu); v[1] += bf2f_m(r.x >> 16);
         v[2] += bf2f_m(r.y & 0xFFFFu); v[3] += bf2f_m(r.y >> 16);
         v[4] += bf2f_m(r.z & 0xFFFFu); v[5] += bf2f_m(r.z >> 16);
@@ -490,9 +507,7 @@ __global__ void splitk_reduce_kernel(ConvArgs a, int splits, int in_bf16) {
   X(29, 128, 256, 2, 4, 6, 4, 0) /* 8 waves, wave 64x64, 32-wide K, 6 stages */       \
   X(30, 128, 128, 2, 2, 5, 8, 0) /* wave 64x64, 5 stages */                           \
   X(31, 128, 128, 2, 2, 4, 8, 0) /* wave 64x64, 4 stages */                           \
-  X(32, 256, 256, 2, 2, 2, 8, 0) /* 4 waves, wave 128x128, two stages */              \
-  X(33, 256, 256, 2, 2, 4, 4, 0) /* 4 waves, wave 128x128, 32-wide K, 4 stages */      \
-  X(34, 256, 32, 4, 1, 3, 8, 0)  /* wave 64x32 */
+  X(32, 256, 32, 4, 1, 3, 8, 0)  /* wave 64x32 */
 
 #define RAFIKI_CFG_ENTRY(id, BM, BN, WM, WN, ST, KC, SP) {BM, BN, WM * WN, ST, KC * 8},
 const MfmaConfig kMfmaConfigs[kNumMfmaConfigs] = {RAFIKI_MFMA_CONFIGS(RAFIKI_CFG_ENTRY)};

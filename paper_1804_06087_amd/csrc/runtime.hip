@@ -620,14 +620,19 @@ int tune(rafiki_ensemble_s* e, int n, const void* in, hipStream_t s) {
 
 // Forward pass of model `mi` over n requests whose model input is `in` (staged images
 // or token ids); logits [n][n_classes] to `logits`.
-int run_model(const rafiki_ensemble_s* e, int mi, const void* in, int n, float* logits, hipStream_t s) {
+// Only ops [op_begin, op_end) are enqueued, so that the launches of several models
+// can be interleaved.
+int run_model(const rafiki_ensemble_s* e, int mi, const void* in, int n, float* logits, hipStream_t s,
+              size_t op_begin = 0, size_t op_end = SIZE_MAX) {
   const Model& M = e->models[mi];
   const auto it = e->tuned.find(n);
   const std::vector<int> empty;
   const std::vector<int>& cfgs = it == e->tuned.end() ? empty : it->second[mi];
   const int bf = e->precision == RAFIKI_BF16 ? 1 : 0;
   const double es = (double)e->esz();
-  for (const Op& op : M.ops) {
+  op_end = std::min(op_end, M.ops.size());
+  for (size_t oi = op_begin; oi < op_end; ++oi) {
+    const Op& op = M.ops[oi];
     const int li = op.out;
     const Tensor& y = M.tensors[op.out];
     void* yp = y.is_logits ? (void*)logits : (void*)(M.d_arena + y.off);
@@ -811,20 +816,37 @@ static int serve(rafiki_ensemble_t h, const void* batch, int n, uint32_t model_s
     if ((model_subset_mask >> m) & 1u) ca.sel[ca.S++] = m;
   // Selected models are independent until the combine: fork them onto their own
   // streams after staging and join before the combine (sequential when tracing, so
-  // that each traced kernel has the GPU to itself).
+  // that each traced kernel has the GPU to itself).  Forked launches are enqueued
+  // interleaved, one op of each model in turn, so that every model stream has work
+  // from the start even when enqueueing is slower than the device.
   const bool fork = h->concurrent && !h->trace.on && ca.S > 1;
-  if (fork) HIPCHK(hipEventRecord(h->staged_ev, s));
-  for (int i = 0; i < ca.S; ++i) {
-    const int m = ca.sel[i];
-    Model& M = h->models[m];
-    hipStream_t ms = fork ? M.stream : s;
-    if (fork) HIPCHK(hipStreamWaitEvent(ms, h->staged_ev, 0));
-    rc = run_model(h, m, in, n, h->d_logits + (size_t)m * ca.ld_model, ms);
-    if (rc) return rc;
-    if (fork) HIPCHK(hipEventRecord(M.done, ms));
+  if (fork) {
+    HIPCHK(hipEventRecord(h->staged_ev, s));
+    size_t rounds = 0;
+    for (int i = 0; i < ca.S; ++i) {
+      HIPCHK(hipStreamWaitEvent(h->models[ca.sel[i]].stream, h->staged_ev, 0));
+      rounds = std::max(rounds, h->models[ca.sel[i]].ops.size());
+    }
+    for (size_t oi = 0; oi < rounds; ++oi)
+      for (int i = 0; i < ca.S; ++i) {
+        const int m = ca.sel[i];
+        Model& M = h->models[m];
+        if (oi >= M.ops.size()) continue;
+        rc = run_model(h, m, in, n, h->d_logits + (size_t)m * ca.ld_model, M.stream, oi, oi + 1);
+        if (rc) return rc;
+      }
+    for (int i = 0; i < ca.S; ++i) {
+      Model& M = h->models[ca.sel[i]];
+      HIPCHK(hipEventRecord(M.done, M.stream));
+      HIPCHK(hipStreamWaitEvent(s, M.done, 0));
+    }
+  } else {
+    for (int i = 0; i < ca.S; ++i) {
+      const int m = ca.sel[i];
+      rc = run_model(h, m, in, n, h->d_logits + (size_t)m * ca.ld_model, s);
+      if (rc) return rc;
+    }
   }
-  if (fork)
-    for (int i = 0; i < ca.S; ++i) HIPCHK(hipStreamWaitEvent(s, h->models[ca.sel[i]].done, 0));
   const double cbytes = (double)n * h->n_classes * 4.0 * (ca.S + 1) + 4.0 * n;
   if (vote) {
     TRACED(h, s, RAFIKI_K_VOTE, -1, -1, 0.0, cbytes, launch_vote(ca, s));
