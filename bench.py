@@ -58,12 +58,15 @@ def parse():
                     help="turn two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) of --pmc-copy-bytes into the "
                          "per-launch HBM traffic of the conv kernel and print it as JSON")
     ap.add_argument("--traffic-file", default=None, help="traffic JSON written by --summarize-pmc")
-    ap.add_argument("--serve", default=None, choices=["sync", "async"],
+    ap.add_argument("--serve", default=None, choices=["sync", "async", "rl"],
                     help="instead of the step benchmark, serve a sine-rate request stream in real time with the "
                          "greedy batch-size policy: every batch through all selected models (sync) or each model "
-                         "an independent server (async); prints one JSON line of serving statistics")
+                         "an independent server (async); prints one JSON line of serving statistics.  rl: profile "
+                         "c(m, b) on the device, train the actor-critic subset/batch scheduler on it and compare "
+                         "its policy with fixed policies in the simulated multi-model environment")
     ap.add_argument("--cycles", type=float, default=1.0, help="serving: sine cycles of 500 tau to serve")
     ap.add_argument("--period-taus", type=int, default=500, help="serving: sine period in units of tau")
+    ap.add_argument("--rl-episodes", type=int, default=60, help="--serve rl: training episodes")
     ap.add_argument("--sweep", action="store_true",
                     help="latency/throughput trade-off of the ResNet-50 + VGG-16 + ResNet-101 subsets {R50}, "
                          "{R50, VGG-16}, {all} at batch sizes 1, 4, 16, 64, 256: one JSON line per point with "
@@ -216,6 +219,81 @@ def serve_main(args, dev):
     print(json.dumps(out), flush=True)
 
 
+def rl_main(args, dev):
+    """Multi-model scheduling (Section 5.2): c(m, b) of each ImageNet-shaped model is
+    profiled alone on the device (B = {16, 32, 48, 64}); the actor-critic agent is
+    trained on sine arrivals in the simulated environment (each model an independent
+    server); its policy (sampled, and its most probable action) is compared, on a fresh
+    arrival draw, with fixed policies: every batch through all models, or through the
+    fastest model only.  The
+    accuracy table a(M[v]) is synthetic (no trained weights or labelled data)."""
+    import numpy as np
+    import torch
+
+    import workloads as wl
+    from paper_1804_06087_amd import Ensemble, RLScheduler
+
+    B = [16, 32, 48, 64]
+    cfg, specs, params, pool = wl.build_config(3, n=64)
+    ens = Ensemble(specs, params, precision=cfg.precision, max_batch=max(B))
+    x = torch.from_numpy(pool).to(dev)
+    cost = np.stack([ens.profile(x, B, 1 << m, reps=10) for m in range(len(specs))]).astype(np.int64)
+    ens.close()
+    M = len(specs)
+    base = [0.70, 0.71, 0.72]   # synthetic single-model accuracies, in model order
+    acc = np.zeros(1 << M)
+    for v in range(1, 1 << M):
+        members = [m for m in range(M) if (v >> m) & 1]
+        acc[v] = max(base[m] for m in members) + 0.015 * (len(members) - 1)
+    tau = int(2 * cost[:, -1].max())
+    r_all = max(b / cost[:, j].max() for j, b in enumerate(B)) * 1e6       # every batch through all models
+    period = 50 * tau
+    train_arr = wl.sine_arrivals(r_all, period, 3 * period, max(tau // 10, 1), seed=1)
+    test_arr = wl.sine_arrivals(r_all, period, 3 * period, max(tau // 10, 1), seed=2)
+    agent = RLScheduler(B, cost, acc, tau, 1.0, queue_features=64, hidden=64, seed=3)
+    t0 = time.perf_counter()
+    hist = agent.train(train_arr, episodes=args.rl_episodes, lr=3e-3, seed=4)
+    train_s = time.perf_counter() - t0
+    n_acts = agent.n_actions
+
+    def evaluate(ep):
+        lat = ep["latency"]
+        served = lat >= 0
+        acts = ep["actions"]
+        sizes = [B[a % len(B)] for a in acts]
+        masks = [a // len(B) + 1 for a in acts]
+        return {"reward": round(float(ep["rewards"].sum()), 2),
+                "reward_per_request": round(float(ep["rewards"].sum()) / max(lat.size, 1), 4),
+                "served": int(served.sum()), "overdue": int((lat[served] > tau).sum()),
+                "mean_accuracy_per_batch": round(float(np.mean([acc[m] for m in masks])) if masks else 0.0, 4),
+                "decisions": int(len(acts)),
+                "mask_counts": {str(v): int(sum(1 for m in masks if m == v)) for v in range(1, 1 << M)},
+                "mean_requested_b": round(float(np.mean(sizes)) if sizes else 0.0, 1)}
+
+    res = {"rl_sampled": evaluate(agent.run_episode(test_arr, mode="sample", seed=5)),
+           "rl_argmax": evaluate(agent.run_episode(test_arr, mode="argmax"))}
+    fixed = {"all_models_b64": (len(B) * ((1 << M) - 2) + len(B) - 1),
+             "fastest_model_b64": None}
+    fastest = int(np.argmin(cost[:, -1]))
+    fixed["fastest_model_b64"] = ((1 << fastest) - 1) * len(B) + len(B) - 1
+    for name, a in fixed.items():
+        assert 0 <= a < n_acts
+        res[name] = evaluate(agent.run_episode(test_arr, mode="given", actions=[a] * test_arr.size))
+    out = {
+        "metric": "RL subset/batch scheduler on the measured c(m, b): reward per request (Equation multi_acc_reward)",
+        "value": res["rl_sampled"]["reward_per_request"], "unit": "reward/request", "higher_is_better": True,
+        "n_gpus": 1, "dtype": "bf16",
+        "data": "c(m, b) profiled on the device; seeded sine arrivals; synthetic accuracy table",
+        "config": {"workload": WORKLOADS["c3"][3], "B": B, "tau_us": tau, "beta": 1.0, "period_us": period,
+                   "arrival_ref_rate": round(r_all, 1), "accuracy_table": [round(a, 3) for a in acc.tolist()],
+                   "episodes": args.rl_episodes, "requests_per_episode": int(train_arr.size)},
+        "c_mb_us": cost.tolist(), "train_s": round(train_s, 2),
+        "train_reward_first_last": [round(float(hist[:5].mean()), 2), round(float(hist[-5:].mean()), 2)],
+        "policies": res,
+    }
+    print(json.dumps(out), flush=True)
+
+
 def sweep_main(args, dev):
     """Latency/accuracy trade-off grid (Section 5.2): every subset of the ImageNet-shaped
     ensemble at every batch size, one handle (max batch 256) over one 256-image draw whose
@@ -286,6 +364,9 @@ def main():
         print(json.dumps({"error": "no GPU visible"}))
         sys.exit(1)
     dev = torch.device("cuda:0")
+    if args.serve == "rl":
+        rl_main(args, dev)
+        return
     if args.serve:
         serve_main(args, dev)
         return

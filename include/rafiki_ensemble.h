@@ -177,8 +177,9 @@ typedef struct {
   int model, layer;             /* -1 for staging and combine */
   double flops;                 /* algorithmic FLOPs (2 x unpadded MACs) of the launch */
   double bytes;                 /* algorithmic bytes: each input, weight and output once */
-  float ms;                     /* elapsed time between HIP events recorded on the launch
-                                   stream immediately before and after the kernel */
+  float ms;                     /* kernel execution time: elapsed time between the HIP
+                                   events the launch records at the kernel's start and end
+                                   (hipExtLaunchKernelGGL start/stop events) */
 } rafiki_trace_rec;
 
 /* Enable (1) or disable (0) per-launch event timing of subsequent infer / model_logits

@@ -425,13 +425,13 @@ static hipError_t launch_mfma_cfg(const ConvArgs& a, int splits, hipStream_t s) 
   const dim3 block(WM * WN * 64);
   if (splits > 1) {
     if (a.Cs % 64 == 0)
-      hipLaunchKernelGGL((conv_mfma_kernel<BM, BN, WM, WN, STAGES, true, KC, true, SP>), grid, block, 0, s, b);
+      launch((conv_mfma_kernel<BM, BN, WM, WN, STAGES, true, KC, true, SP>), grid, block, s, b);
     else
-      hipLaunchKernelGGL((conv_mfma_kernel<BM, BN, WM, WN, STAGES, false, KC, true, SP>), grid, block, 0, s, b);
+      launch((conv_mfma_kernel<BM, BN, WM, WN, STAGES, false, KC, true, SP>), grid, block, s, b);
   } else if (a.Cs % 64 == 0) {
-    hipLaunchKernelGGL((conv_mfma_kernel<BM, BN, WM, WN, STAGES, true, KC, false, SP>), grid, block, 0, s, b);
+    launch((conv_mfma_kernel<BM, BN, WM, WN, STAGES, true, KC, false, SP>), grid, block, s, b);
   } else {
-    hipLaunchKernelGGL((conv_mfma_kernel<BM, BN, WM, WN, STAGES, false, KC, false, SP>), grid, block, 0, s, b);
+    launch((conv_mfma_kernel<BM, BN, WM, WN, STAGES, false, KC, false, SP>), grid, block, s, b);
   }
   return hipGetLastError();
 }
@@ -535,7 +535,7 @@ hipError_t launch_splitk_reduce(const ConvArgs& a, int splits, int in_bf16, hipS
   const long long total = (long long)a.M * ((a.c_write + 3) / 4);
   const int threads = 256;
   const long long blocks = (total + threads - 1) / threads;
-  hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)blocks), dim3(threads), 0, s, a, splits, in_bf16);
+  launch(splitk_reduce_kernel, dim3((unsigned)blocks), dim3(threads), s, a, splits, in_bf16);
   return hipGetLastError();
 }
 

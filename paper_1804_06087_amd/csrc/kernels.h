@@ -3,7 +3,24 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <hip/hip_ext.h>
+
 namespace rafiki {
+
+// Events the next kernel launch of this thread records at its own start and end (both
+// null: untimed).  Set by the runtime's per-launch tracing; the dispatch itself records
+// them, so the interval is the kernel's execution, not the queue around it.
+struct LaunchEvents {
+  hipEvent_t start = nullptr, stop = nullptr;
+};
+LaunchEvents& launch_events();
+
+// Every kernel of the library is launched through this, so tracing can time it.
+template <typename F, typename... Args>
+inline void launch(F kernel, dim3 grid, dim3 block, hipStream_t s, Args... args) {
+  const LaunchEvents& ev = launch_events();
+  hipExtLaunchKernelGGL(kernel, grid, block, 0, s, ev.start, ev.stop, 0, args...);
+}
 
 typedef uint16_t bf16_t;   // bfloat16 storage (upper half of an IEEE float)
 

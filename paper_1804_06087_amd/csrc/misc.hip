@@ -6,6 +6,11 @@
 
 namespace rafiki {
 
+LaunchEvents& launch_events() {
+  static thread_local LaunchEvents ev;
+  return ev;
+}
+
 __device__ __forceinline__ float bf2f(uint32_t b16) { return __uint_as_float(b16 << 16); }
 __device__ __forceinline__ uint32_t f2bf(float f) {   // nearest, ties to even (finite)
   uint32_t u = __float_as_uint(f);
@@ -66,7 +71,7 @@ __global__ void stage_images_kernel(const float* __restrict__ x, void* y, int N,
 hipError_t launch_stage_images(const float* x, void* y, int N, int C, int H, int W, int Cs, int to_bf16,
                                hipStream_t s) {
   const long long total = (long long)N * H * W * (Cs / 8);
-  hipLaunchKernelGGL(stage_images_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, x, y, N, C, H,
+  launch(stage_images_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), s, x, y, N, C, H,
                      W, Cs, to_bf16);
   return hipGetLastError();
 }
@@ -105,7 +110,7 @@ __global__ void maxpool_kernel(const void* __restrict__ x, void* y, int N, int H
 hipError_t launch_maxpool(const void* x, void* y, int N, int H, int W, int Cs, int Ho, int Wo, int k, int stride,
                           int pad, int bf16, hipStream_t s) {
   const long long total = (long long)N * Ho * Wo * (Cs / 8);
-  hipLaunchKernelGGL(maxpool_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, x, y, N, H, W, Cs, Ho,
+  launch(maxpool_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), s, x, y, N, H, W, Cs, Ho,
                      Wo, k, stride, pad, bf16);
   return hipGetLastError();
 }
@@ -173,7 +178,7 @@ hipError_t launch_spatial_reduce(const void* x, void* y, int N, int HW, int Cs, 
   const int G = Cs / 8;
   const int GB = G < 64 ? G : 64;
   const dim3 grid((unsigned)N, (unsigned)((G + GB - 1) / GB));
-  hipLaunchKernelGGL(spatial_reduce_kernel, grid, dim3(kReduceThreads), 0, s, x, y, HW, Cs, GB, is_max, bf16);
+  launch(spatial_reduce_kernel, grid, dim3(kReduceThreads), s, x, y, HW, Cs, GB, is_max, bf16);
   return hipGetLastError();
 }
 
@@ -199,7 +204,7 @@ __global__ void embed_gather_kernel(const int32_t* __restrict__ tok, const void*
 hipError_t launch_embed_gather(const int32_t* tok, const void* table, void* y, int N, int L, int Cs, int bf16,
                                hipStream_t s) {
   const long long total = (long long)N * L * (Cs / 8);
-  hipLaunchKernelGGL(embed_gather_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, tok, table, y, N,
+  launch(embed_gather_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), s, tok, table, y, N,
                      L, Cs, bf16);
   return hipGetLastError();
 }
@@ -227,7 +232,7 @@ __global__ void concat_kernel(const void* a, int ca, int lda, const void* b, int
 hipError_t launch_concat(const void* a, int ca, int lda, const void* b, int cb, int ldb, void* y, int ldy, int N,
                          int bf16, hipStream_t s) {
   const long long total = (long long)N * ldy;
-  hipLaunchKernelGGL(concat_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, a, ca, lda, b, cb, ldb,
+  launch(concat_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), s, a, ca, lda, b, cb, ldb,
                      y, ldy, N, bf16);
   return hipGetLastError();
 }
@@ -265,7 +270,7 @@ __global__ void conv_f32_kernel(ConvArgs a) {
 
 hipError_t launch_conv_f32(const ConvArgs& a, hipStream_t s) {
   const long long total = (long long)a.M * a.c_write;
-  hipLaunchKernelGGL(conv_f32_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, a);
+  launch(conv_f32_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), s, a);
   return hipGetLastError();
 }
 
@@ -340,7 +345,7 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineArgs a) {
 
 hipError_t launch_combine(const CombineArgs& a, hipStream_t s) {
   if (a.C > 64 * kCombineMaxPerLane || a.S < 1) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(combine_kernel, dim3((a.n + 3) / 4), dim3(256), 0, s, a);
+  launch(combine_kernel, dim3((a.n + 3) / 4), dim3(256), s, a);
   return hipGetLastError();
 }
 
@@ -395,7 +400,7 @@ __global__ __launch_bounds__(256) void vote_kernel(CombineArgs a) {
 
 hipError_t launch_vote(const CombineArgs& a, hipStream_t s) {
   if (a.S < 1 || a.S > 32 || a.C < 1) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(vote_kernel, dim3((a.n + 3) / 4), dim3(256), 0, s, a);
+  launch(vote_kernel, dim3((a.n + 3) / 4), dim3(256), s, a);
   return hipGetLastError();
 }
 

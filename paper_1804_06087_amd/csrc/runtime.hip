@@ -492,21 +492,22 @@ const void* tptr(const rafiki_ensemble_s* e, const Model& M, int id, const void*
     if (st_ != hipSuccess) return fail(RAFIKI_ERR_HIP, std::string(#expr) + ": " + hipGetErrorString(st_)); \
   } while (0)
 
-// Launch `expr` on stream s; when tracing, bracket it with events and record the
-// launch's algorithmic FLOPs and bytes.
+// Launch `expr` (one kernel launch) on stream s; when tracing, the launch itself records
+// a pair of events at the kernel's start and end, and the launch's algorithmic FLOPs
+// and bytes are kept with them.
 #define TRACED(e, s, kind, model, layer, flops, bytes, expr)                                  \
   do {                                                                                        \
     hipEvent_t ta_ = nullptr, tb_ = nullptr;                                                  \
     if ((e)->trace.on) {                                                                      \
       ta_ = (e)->trace.next();                                                                \
       tb_ = (e)->trace.next();                                                                \
-      if (ta_) (void)hipEventRecord(ta_, s);                                                  \
+      if (ta_ && tb_) launch_events() = {ta_, tb_};                                           \
     }                                                                                         \
-    HIPCHK(expr);                                                                             \
-    if (ta_ && tb_) {                                                                         \
-      (void)hipEventRecord(tb_, s);                                                           \
+    const hipError_t lst_ = (expr);                                                           \
+    launch_events() = {};                                                                     \
+    HIPCHK(lst_);                                                                             \
+    if (ta_ && tb_)                                                                           \
       (e)->trace.recs.push_back({kind, model, layer, (double)(flops), (double)(bytes), ta_, tb_}); \
-    }                                                                                         \
   } while (0)
 
 int run_gemm(const rafiki_ensemble_s* e, const Op& op, ConvArgs a, hipStream_t s, int mi, int li, int cfg) {
