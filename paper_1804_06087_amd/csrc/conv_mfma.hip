@@ -94,8 +94,19 @@ struct Loader {
     for (int j = 0; j < RA; ++j) {
       const int m = m0 + (j * NW + wave) * ROWS + lrow;
       if (m < a.M) {
-        const int n = m / HoWo, r = m - n * HoWo;
-        const int ho = r / a.Wo, wo = r - ho * a.Wo;
+        int n, ho, wo;
+        if (a.pool2) {   // row m: position m % 4 of 2x2 window m / 4
+          const int q = m >> 2, Wo2 = a.Wo >> 1, HW2 = (a.Ho >> 1) * Wo2;
+          n = q / HW2;
+          const int r = q - n * HW2, ho2 = r / Wo2;
+          ho = 2 * ho2 + ((m >> 1) & 1);
+          wo = 2 * (r - ho2 * Wo2) + (m & 1);
+        } else {
+          n = m / HoWo;
+          const int r = m - n * HoWo;
+          ho = r / a.Wo;
+          wo = r - ho * a.Wo;
+        }
         a_img[j] = n * a.H * a.W;
         a_hi[j] = ho * a.stride - a.pad;
         a_wi[j] = wo * a.stride - a.pad;
@@ -374,6 +385,40 @@ __global__ __launch_bounds__(WM * WN * 64) void conv_mfma_kernel(ConvArgs a) {
     }
     __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): this wave's LDS writes have landed
     __builtin_amdgcn_wave_barrier();
+    if (a.pool2) {
+      // fused 2x2 max-pool: rows 4w .. 4w + 3 of the wave tile form window w; lane
+      // (pl, oq) takes window pass * 16 + pl.  The max of the four fp32 values, then
+      // ReLU and one rounding, equals the max of the four rounded ReLU outputs.
+#pragma unroll
+      for (int pass = 0; pass < (WTM / 4 + 15) / 16; ++pass) {
+        const int wdw = pass * 16 + pl;
+        const int mb = m0 + wm * WTM + 4 * wdw;
+        if (4 * wdw >= WTM || mb >= a.M || c >= a.c_write) continue;
+        float v[8];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int p = 4 * wdw + i;
+          const float4 lo = stg[p * 8 + ((2 * oq) ^ swz<8>(p))];
+          const float4 hi = stg[p * 8 + ((2 * oq + 1) ^ swz<8>(p))];
+          const float t[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+#pragma unroll
+          for (int j = 0; j < 8; ++j) v[j] = i == 0 ? t[j] : fmaxf(v[j], t[j]);
+        }
+        if (a.relu) {
+#pragma unroll
+          for (int j = 0; j < 8; ++j) v[j] = fmaxf(v[j], 0.f);
+        }
+        uint4 w;
+        w.x = f2bf_m(v[0]) | (f2bf_m(v[1]) << 16);
+        w.y = f2bf_m(v[2]) | (f2bf_m(v[3]) << 16);
+        w.z = f2bf_m(v[4]) | (f2bf_m(v[5]) << 16);
+        w.w = f2bf_m(v[6]) | (f2bf_m(v[7]) << 16);
+        *(uint4*)((bf16_t*)a.y + (long long)(mb >> 2) * a.ldy + c) = w;
+      }
+      __builtin_amdgcn_s_waitcnt(0xC07F);   // reads done before the region is rewritten
+      __builtin_amdgcn_wave_barrier();
+      continue;
+    }
 #pragma unroll
     for (int pass = 0; pass < NPASS; ++pass) {
       const int p = pass * 16 + pl;
@@ -437,10 +482,35 @@ static hipError_t launch_mfma_cfg(const ConvArgs& a, int splits, hipStream_t s) 
 }
 
 // Sum the split-K partials in split order, then the same epilogue as the GEMM kernel.
-// One thread per (row, 4-channel group).
+// One thread per (output row, 4-channel group); with a fused 2x2 max-pool an output row
+// is window q, the max over GEMM rows 4q .. 4q + 3.
 __global__ void splitk_reduce_kernel(ConvArgs a, int splits, int in_bf16) {
   const int groups = (a.c_write + 3) / 4;
   const long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (a.pool2) {
+    if (idx >= (long long)(a.M / 4) * groups) return;
+    const int q = (int)(idx / groups);
+    const int c = (int)(idx - (long long)q * groups) * 4;
+    const float4 sc = *(const float4*)(a.scale + c);
+    const float4 sh = *(const float4*)(a.shift + c);
+    float best[4];
+    for (int i = 0; i < 4; ++i) {
+      const int m = 4 * q + i;
+      float4 s = *(const float4*)(a.partial + (long long)m * a.Co_pad + c);
+      for (int z = 1; z < splits; ++z) {
+        const float4 t = *(const float4*)(a.partial + ((long long)z * a.M + m) * a.Co_pad + c);
+        s.x += t.x; s.y += t.y; s.z += t.z; s.w += t.w;
+      }
+      const float v[4] = {s.x * sc.x + sh.x, s.y * sc.y + sh.y, s.z * sc.z + sh.z, s.w * sc.w + sh.w};
+      for (int j = 0; j < 4; ++j) best[j] = i == 0 ? v[j] : fmaxf(best[j], v[j]);
+    }
+    const long long o = (long long)q * a.ldy + c;
+    for (int j = 0; j < 4; ++j) {
+      if (c + j >= a.c_write) break;
+      ((bf16_t*)a.y)[o + j] = (bf16_t)f2bf_m(a.relu ? fmaxf(best[j], 0.f) : best[j]);
+    }
+    return;
+  }
   if (idx >= (long long)a.M * groups) return;
   const int m = (int)(idx / groups);
   const int c = (int)(idx - (long long)m * groups) * 4;
@@ -532,7 +602,7 @@ hipError_t launch_conv_mfma(const ConvArgs& a, int cfg, int splits, hipStream_t 
 }
 
 hipError_t launch_splitk_reduce(const ConvArgs& a, int splits, int in_bf16, hipStream_t s) {
-  const long long total = (long long)a.M * ((a.c_write + 3) / 4);
+  const long long total = (long long)(a.pool2 ? a.M / 4 : a.M) * ((a.c_write + 3) / 4);
   const int threads = 256;
   const long long blocks = (total + threads - 1) / threads;
   launch(splitk_reduce_kernel, dim3((unsigned)blocks), dim3(threads), s, a, splits, in_bf16);

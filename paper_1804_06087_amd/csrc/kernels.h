@@ -44,6 +44,8 @@ struct ConvArgs {
   int c_write;          // channels written per row (<= Co_pad)
   int ldy;              // row stride of y and res, in elements
   int relu;
+  int pool2;            // fused 2x2 stride-2 max-pool: GEMM row m is conv pixel (window m / 4, position
+                        // m % 4 in row-major order within the window); y holds the pooled rows m / 4
   int out_f32;          // y is fp32 (bf16 kernels); fp32 kernels always write fp32
   int kt_per_split;     // K tiles per split (splits = gridDim.y)
   int n_tiles;          // channel tiles per row of the output tile grid

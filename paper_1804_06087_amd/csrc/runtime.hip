@@ -69,6 +69,8 @@ struct Op {
   float* d_shift = nullptr;
   // pooling
   int k = 1;
+  // conv2d: a 2x2 stride-2 max-pool fused into the epilogue; `out` is the pooled tensor
+  int pool2 = 0;
   // conv1d: pre-max scratch [n][T][Cs_out] in the arena
   size_t tmp_off = 0;
   // concat
@@ -436,11 +438,39 @@ int build_model(rafiki_ensemble_s* e, int mi, const rafiki_model_desc& md, Model
     return fail(RAFIKI_ERR_INVALID, "model " + std::to_string(mi) + ": the last layer must be an FC with n_classes outputs");
   M.tensors.back().is_logits = true;
 
-  // Liveness-planned arena for max_batch requests (the logits go to the ensemble's slots).
-  for (const Op& op : M.ops) {
-    if (op.in >= 0) M.tensors[op.in].last_use = std::max(M.tensors[op.in].last_use, op.out);
-    if (op.in2 >= 0) M.tensors[op.in2].last_use = std::max(M.tensors[op.in2].last_use, op.out);
+  // A 2x2 stride-2 max-pool whose input is a bf16 conv output read by nothing else is
+  // fused into that conv: its epilogue writes the pooled tensor, and the full-size conv
+  // output is never stored.  ReLU and bf16 rounding are monotone, so the pooled values
+  // are bitwise those of the separate pool.
+  if (bf) {
+    std::vector<int> readers(M.tensors.size(), 0);
+    for (const Op& op : M.ops)
+      for (int src : {op.in, op.in2})
+        if (src >= 0) ++readers[src];
+    std::vector<Op> ops;
+    std::vector<int> writer(M.tensors.size(), -1);   // index in `ops` of the op writing each tensor
+    for (const Op& op : M.ops) {
+      if (op.kind == O_MAXPOOL && op.k == 2 && op.stride == 2 && op.pad == 0 && op.in >= 0 &&
+          readers[op.in] == 1 && writer[op.in] >= 0) {
+        Op& c = ops[writer[op.in]];
+        if (c.kind == O_CONV && c.in2 < 0 && !c.pool2 && c.Ho % 2 == 0 && c.Wo % 2 == 0) {
+          c.pool2 = 1;
+          c.out = op.out;
+          writer[op.out] = writer[op.in];
+          continue;
+        }
+      }
+      writer[op.out] = (int)ops.size();
+      ops.push_back(op);
+    }
+    M.ops.swap(ops);
   }
+
+  // Liveness-planned arena for max_batch requests (the logits go to the ensemble's slots);
+  // a tensor's last use is the index of the last op that reads it.
+  for (size_t i = 0; i < M.ops.size(); ++i)
+    for (int src : {M.ops[i].in, M.ops[i].in2})
+      if (src >= 0) M.tensors[src].last_use = std::max(M.tensors[src].last_use, (int)i);
   FreeList fl;
   const size_t es = e->esz(), nb = (size_t)e->max_batch;
   for (size_t i = 0; i < M.ops.size(); ++i) {
@@ -515,8 +545,9 @@ int run_gemm(const rafiki_ensemble_s* e, const Op& op, ConvArgs a, hipStream_t s
   const double kalg = (double)op.kh * op.kw * op.cin_l;
   const double flops = 2.0 * a.M * op.c_out * kalg;
   const double in_elems = (double)a.N * a.H * a.W * op.cin_l;   // FC: H = W = 1, cin_l = flattened size
+  const double out_rows = a.pool2 ? a.M / 4.0 : (double)a.M;
   const double bytes = in_elems * es + (double)op.c_out * kalg * es +
-                       (double)a.M * op.c_out * (a.out_f32 ? 4.0 : es) * (a.res ? 2.0 : 1.0);
+                       out_rows * op.c_out * (a.out_f32 ? 4.0 : es) * (a.res ? 2.0 : 1.0);
   if (e->precision != RAFIKI_BF16) {
     TRACED(e, s, RAFIKI_K_CONV_F32, mi, li, flops, bytes, launch_conv_f32(a, s));
     return RAFIKI_OK;
@@ -534,7 +565,7 @@ int run_gemm(const rafiki_ensemble_s* e, const Op& op, ConvArgs a, hipStream_t s
     a.partial = Mo.d_partial;
     TRACED(e, s, RAFIKI_K_CONV_MFMA, mi, li, flops, bytes, launch_conv_mfma(a, split_cfg(op.c_out), splits, s));
     TRACED(e, s, RAFIKI_K_SPLITK_REDUCE, mi, li, 0.0,
-           (double)splits * a.M * a.c_write * 4.0 + (double)a.M * a.c_write * (a.out_f32 ? 4.0 : es),
+           (double)splits * a.M * a.c_write * 4.0 + out_rows * a.c_write * (a.out_f32 ? 4.0 : es),
            launch_splitk_reduce(a, splits, 1, s));
   } else {
     TRACED(e, s, RAFIKI_K_CONV_MFMA, mi, li, flops, bytes, launch_conv_mfma(a, cfg, 1, s));
@@ -551,6 +582,7 @@ ConvArgs gemm_args(const rafiki_ensemble_s* e, const Model& M, const Op& op, int
   a.Ho = op.Ho; a.Wo = op.Wo; a.kh = op.kh; a.kw = op.kw; a.stride = op.stride; a.pad = op.pad;
   a.M = n * op.Ho * op.Wo; a.K = op.K; a.Kp = op.Kp; a.Co_pad = op.Co_pad; a.Nc = op.c_out;
   a.relu = op.relu;
+  a.pool2 = op.pool2;
   a.x_bytes = (int)((long long)n * op.H * op.W * op.Cs_in * (long long)e->esz());
   a.w_bytes = (int)((long long)op.Co_pad * op.Kp * (long long)e->esz());
   a.Cs8 = op.Cs_in / 8; a.K8 = op.K / 8;

@@ -76,6 +76,15 @@ CASES = {
     "stem_3x3_cout32_ragged": ([conv(-1, 3, 32, 3)], (3, 5, 6), 7, 32 * 5 * 6),
     "stem_7x7_s2_cout128": ([conv(-1, 3, 128, 7, s=2, p=3)], (3, 4, 4), 3, 128 * 2 * 2),
     "stem_1ch_5x5_cout96": ([conv(-1, 1, 96, 5, p=2, bn=False, bias=True)], (1, 3, 3), 5, 96 * 3 * 3),
+    # 2x2 stride-2 max-pool fused into the conv epilogue (bf16): ragged window count,
+    # 64 storage channels; a long-K conv whose tiny output is split over K (the pooled
+    # split-K reduction); an odd-sized conv output that is pooled separately (floor)
+    "pool2_fused_ragged": ([conv(-1, 64, 24, 3), Layer(op=MAXPOOL2D, input=0, c_in=24, c_out=24, kh=2, kw=2,
+                                                        stride=2)], (64, 10, 14), 3, 24 * 5 * 7),
+    "pool2_fused_split_k": ([conv(-1, 512, 64, 3), Layer(op=MAXPOOL2D, input=0, c_in=64, c_out=64, kh=2, kw=2,
+                                                          stride=2)], (512, 4, 4), 2, 64 * 2 * 2),
+    "pool2_odd_unfused": ([conv(-1, 8, 16, 3), Layer(op=MAXPOOL2D, input=0, c_in=16, c_out=16, kh=2, kw=2,
+                                                      stride=2)], (8, 7, 9), 3, 16 * 3 * 4),
     # output maps of a multiple of 128 pixels, pooled to keep the probe small
     "stem_window_3x3": ([conv(-1, 3, 32, 3), Layer(op=MAXPOOL2D, input=0, c_in=32, c_out=32, kh=4, kw=4, stride=4)],
                         (3, 16, 16), 3, 32 * 4 * 4),
