@@ -144,3 +144,19 @@ def test_textcnn_small():
         ref = oracle.run_model(spec, params, tok, act="bf16" if bf else None)
         err = np.abs(z - ref).max() / np.abs(ref).max()
         assert err <= (1e-2 if bf else 1e-5), (precision, err)
+
+
+def test_textcnn_long_sequence():
+    """Long sequences (260 tokens; 258 and 254 positions for widths 3 and 7, so a
+    position range spans several row tiles and the max over time many of them), odd
+    channel counts and a batch that is not a multiple of anything."""
+    spec = wl.textcnn(vocab=64, seq_len=260, dim=24, filters=12, widths=(3, 7), n_classes=2)
+    params = wl.gen_params(spec, 6, True, "random")
+    for L, P in zip(spec.layers, params.layers):
+        if L.bias:
+            P.bias = np.linspace(-0.3, 0.2, L.c_out).astype(np.float32)
+    tok = wl.gen_tokens(5, 260, 64, seed=8)
+    z = gpu_logits(spec, params, tok, "bf16")
+    ref = oracle.run_model(spec, params, tok, act="bf16")
+    err = np.abs(z - ref).max() / np.abs(ref).max()
+    assert err <= 1e-2, err
