@@ -36,7 +36,7 @@ def fits(bn, c_out):
 
 
 CASES = {
-    # name: (conv layers, input (C, H, W), n); output channels of the last conv
+    # name: (conv layers, input (C, H, W), n)
     # 64 storage channels: K ordered (channel block, tap, channel); ragged M
     "aligned_3x3_cout256": ([conv(-1, 64, 256, 3)], (64, 20, 20), 21),
     # 24 channels: K ordered (tap, channel) with per-lane decode; ragged N tile
@@ -46,6 +46,10 @@ CASES = {
     # residual add after a stride-2 3x3, projection shortcut
     "residual_s2_cout128": ([conv(-1, 64, 128, 1, s=2, relu=False), conv(-1, 64, 128, 3, s=2, res=0)],
                             (64, 32, 32), 65),
+    # residual add after a stride-1 3x3, rows of 18 pixels
+    "residual_s1_cout128": ([conv(-1, 64, 128, 1, relu=False), conv(-1, 64, 128, 3, res=0)], (64, 12, 18), 76),
+    # 7x7 images: every tile spans several images
+    "aligned_3x3_7x7": ([conv(-1, 128, 128, 3)], (128, 7, 7), 340),
 }
 
 
