@@ -194,8 +194,10 @@ __device__ __forceinline__ void wait_tiles(int n) {
   }
 }
 
-template <int BM, int BN, int WM, int WN, int STAGES, bool ALIGNED, int KC, bool SPLIT, bool SPREAD>
-__global__ __launch_bounds__(WM * WN * 64) void conv_mfma_kernel(ConvArgs a) {
+// OCC > 0: registers are limited so that OCC waves fit on each SIMD (more workgroups
+// per CU, at the risk of spills).
+template <int BM, int BN, int WM, int WN, int STAGES, bool ALIGNED, int KC, bool SPLIT, bool SPREAD, int OCC>
+__global__ __launch_bounds__(WM * WN * 64, OCC > 0 ? OCC : 1) void conv_mfma_kernel(ConvArgs a) {
   constexpr int NW = WM * WN;
   constexpr int WTM = BM / WM, WTN = BN / WN;      // wave tile: pixels x channels
   constexpr int TM = WTM / 32, TN = WTN / 32;
@@ -209,7 +211,9 @@ __global__ __launch_bounds__(WM * WN * 64) void conv_mfma_kernel(ConvArgs a) {
   static_assert(STAGES >= 2 && STAGES <= 6 && (STAGES - 2) * PER < 64, "pipeline depth");
   static_assert(!SPREAD || KS >= 2, "a spread refill needs two k-steps");
 
-  __shared__ uint4 lds[STAGES * STAGE_CHUNKS];
+  // the ring, or the epilogue's staging of the wave tiles if that is larger
+  constexpr int LDS_CHUNKS = STAGES * STAGE_CHUNKS > NW * WTM * 8 ? STAGES * STAGE_CHUNKS : NW * WTM * 8;
+  __shared__ uint4 lds[LDS_CHUNKS];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -345,7 +349,7 @@ __global__ __launch_bounds__(WM * WN * 64) void conv_mfma_kernel(ConvArgs a) {
   // writes 16 bytes.  The residual add and the single rounding match the direct form.
   // A group's residual, scale and shift loads are all issued before its staging
   // writes, so their latency is paid once per group rather than once per pass.
-  static_assert(NW * WTM * 32 * 4 <= STAGES * STAGE_CHUNKS * 16, "epilogue staging fits in the LDS ring");
+  static_assert(NW * WTM * 32 * 4 <= LDS_CHUNKS * 16, "epilogue staging fits in LDS");
   constexpr int NPASS = WTM / 16;
   const bool bf_res = a.res != nullptr && !a.out_f32;
   float4* stg = (float4*)lds + wave * (WTM * 8);
@@ -461,7 +465,7 @@ __global__ __launch_bounds__(WM * WN * 64) void conv_mfma_kernel(ConvArgs a) {
   }
 }
 
-template <int BM, int BN, int WM, int WN, int STAGES, int KC, bool SP>
+template <int BM, int BN, int WM, int WN, int STAGES, int KC, bool SP, int OC>
 static hipError_t launch_mfma_cfg(const ConvArgs& a, int splits, hipStream_t s) {
   ConvArgs b = a;
   b.n_tiles = (a.Nc + BN - 1) / BN;
@@ -470,13 +474,13 @@ static hipError_t launch_mfma_cfg(const ConvArgs& a, int splits, hipStream_t s) 
   const dim3 block(WM * WN * 64);
   if (splits > 1) {
     if (a.Cs % 64 == 0)
-      launch((conv_mfma_kernel<BM, BN, WM, WN, STAGES, true, KC, true, SP>), grid, block, s, b);
+      launch((conv_mfma_kernel<BM, BN, WM, WN, STAGES, true, KC, true, SP, OC>), grid, block, s, b);
     else
-      launch((conv_mfma_kernel<BM, BN, WM, WN, STAGES, false, KC, true, SP>), grid, block, s, b);
+      launch((conv_mfma_kernel<BM, BN, WM, WN, STAGES, false, KC, true, SP, OC>), grid, block, s, b);
   } else if (a.Cs % 64 == 0) {
-    launch((conv_mfma_kernel<BM, BN, WM, WN, STAGES, true, KC, false, SP>), grid, block, s, b);
+    launch((conv_mfma_kernel<BM, BN, WM, WN, STAGES, true, KC, false, SP, OC>), grid, block, s, b);
   } else {
-    launch((conv_mfma_kernel<BM, BN, WM, WN, STAGES, false, KC, false, SP>), grid, block, s, b);
+    launch((conv_mfma_kernel<BM, BN, WM, WN, STAGES, false, KC, false, SP, OC>), grid, block, s, b);
   }
   return hipGetLastError();
 }
@@ -545,56 +549,61 @@ __global__ void splitk_reduce_kernel(ConvArgs a, int splits, int in_bf16) {
 // never changes a result.  Each kernel is instantiated explicitly (the host pass
 // does not always emit the launch stub of an implicitly instantiated template).
 #define RAFIKI_MFMA_CONFIGS(X)                                                         \
-  X(0, 256, 256, 4, 2, 2, 8, 0)  /* 8 waves, wave 64x128, two stages */               \
-  X(1, 256, 256, 2, 4, 2, 8, 0)  /* 8 waves, wave 128x64, two stages */               \
-  X(2, 256, 128, 2, 4, 3, 8, 0)  /* 8 waves, wave 128x32 */                           \
-  X(3, 128, 256, 2, 4, 3, 8, 0)  /* 8 waves, wave 64x64 */                            \
-  X(4, 256, 128, 2, 2, 2, 8, 0)  /* wave 128x64, two stages */                        \
-  X(5, 128, 128, 2, 2, 3, 8, 0)  /* wave 64x64 */                                     \
-  X(6, 64, 128, 1, 4, 3, 8, 0)   /* wave 64x32 */                                     \
-  X(7, 128, 64, 2, 2, 3, 8, 0)   /* wave 64x32 */                                     \
-  X(8, 64, 64, 2, 2, 3, 8, 0)    /* wave 32x32 */                                     \
-  X(9, 32, 128, 1, 4, 3, 8, 0)   /* wave 32x32 */                                     \
-  X(10, 128, 32, 4, 1, 3, 8, 0)  /* wave 32x32 */                                     \
-  X(11, 256, 64, 4, 1, 3, 8, 0)  /* wave 64x64 */                                     \
-  X(12, 64, 64, 2, 2, 2, 8, 0)   /* wave 32x32, two stages (short K) */               \
-  X(13, 128, 64, 2, 2, 2, 8, 0)  /* wave 64x32, two stages (short K) */               \
-  X(14, 64, 128, 1, 4, 2, 8, 0)  /* wave 64x32, two stages (short K) */               \
-  X(15, 128, 128, 2, 2, 2, 8, 0) /* wave 64x64, two stages */                         \
-  X(16, 128, 256, 2, 4, 2, 8, 0) /* 8 waves, wave 64x64, two stages */                \
-  X(17, 256, 128, 4, 2, 2, 8, 0) /* 8 waves, wave 64x64, two stages */                \
-  X(18, 64, 128, 1, 4, 4, 4, 0)  /* 32-wide K tiles: wave 64x32, 4 stages */          \
-  X(19, 256, 256, 4, 2, 2, 8, 1) /* as 0, spread refill */                            \
-  X(20, 256, 256, 2, 4, 2, 8, 1) /* as 1, spread refill */                            \
-  X(21, 256, 128, 2, 4, 3, 8, 1) /* as 2, spread refill */                            \
-  X(22, 128, 256, 2, 4, 3, 8, 1) /* as 3, spread refill */                            \
-  X(23, 128, 256, 2, 4, 2, 8, 1) /* as 16, spread refill */                           \
-  X(24, 256, 128, 4, 2, 2, 8, 1) /* as 17, spread refill */                           \
-  X(25, 128, 128, 2, 2, 2, 8, 1) /* as 15, spread refill */                           \
-  X(26, 256, 256, 4, 2, 4, 4, 0) /* 8 waves, wave 64x128, 32-wide K, 4 stages */      \
-  X(27, 256, 256, 4, 2, 5, 4, 0) /* 8 waves, wave 64x128, 32-wide K, 5 stages */      \
-  X(28, 256, 128, 4, 2, 6, 4, 0) /* 8 waves, wave 64x64, 32-wide K, 6 stages */       \
-  X(29, 128, 256, 2, 4, 6, 4, 0) /* 8 waves, wave 64x64, 32-wide K, 6 stages */       \
-  X(30, 128, 128, 2, 2, 5, 8, 0) /* wave 64x64, 5 stages */                           \
-  X(31, 128, 128, 2, 2, 4, 8, 0) /* wave 64x64, 4 stages */                           \
-  X(32, 256, 32, 4, 1, 3, 8, 0)  /* wave 64x32 */
+  X(0, 256, 256, 4, 2, 2, 8, 0, 0)  /* 8 waves, wave 64x128, two stages */               \
+  X(1, 256, 256, 2, 4, 2, 8, 0, 0)  /* 8 waves, wave 128x64, two stages */               \
+  X(2, 256, 128, 2, 4, 3, 8, 0, 0)  /* 8 waves, wave 128x32 */                           \
+  X(3, 128, 256, 2, 4, 3, 8, 0, 0)  /* 8 waves, wave 64x64 */                            \
+  X(4, 256, 128, 2, 2, 2, 8, 0, 0)  /* wave 128x64, two stages */                        \
+  X(5, 128, 128, 2, 2, 3, 8, 0, 0)  /* wave 64x64 */                                     \
+  X(6, 64, 128, 1, 4, 3, 8, 0, 0)   /* wave 64x32 */                                     \
+  X(7, 128, 64, 2, 2, 3, 8, 0, 0)   /* wave 64x32 */                                     \
+  X(8, 64, 64, 2, 2, 3, 8, 0, 0)    /* wave 32x32 */                                     \
+  X(9, 32, 128, 1, 4, 3, 8, 0, 0)   /* wave 32x32 */                                     \
+  X(10, 128, 32, 4, 1, 3, 8, 0, 0)  /* wave 32x32 */                                     \
+  X(11, 256, 64, 4, 1, 3, 8, 0, 0)  /* wave 64x64 */                                     \
+  X(12, 64, 64, 2, 2, 2, 8, 0, 0)   /* wave 32x32, two stages (short K) */               \
+  X(13, 128, 64, 2, 2, 2, 8, 0, 0)  /* wave 64x32, two stages (short K) */               \
+  X(14, 64, 128, 1, 4, 2, 8, 0, 0)  /* wave 64x32, two stages (short K) */               \
+  X(15, 128, 128, 2, 2, 2, 8, 0, 0) /* wave 64x64, two stages */                         \
+  X(16, 128, 256, 2, 4, 2, 8, 0, 0) /* 8 waves, wave 64x64, two stages */                \
+  X(17, 256, 128, 4, 2, 2, 8, 0, 0) /* 8 waves, wave 64x64, two stages */                \
+  X(18, 64, 128, 1, 4, 4, 4, 0, 0)  /* 32-wide K tiles: wave 64x32, 4 stages */          \
+  X(19, 256, 256, 4, 2, 2, 8, 1, 0) /* as 0, spread refill */                            \
+  X(20, 256, 256, 2, 4, 2, 8, 1, 0) /* as 1, spread refill */                            \
+  X(21, 256, 128, 2, 4, 3, 8, 1, 0) /* as 2, spread refill */                            \
+  X(22, 128, 256, 2, 4, 3, 8, 1, 0) /* as 3, spread refill */                            \
+  X(23, 128, 256, 2, 4, 2, 8, 1, 0) /* as 16, spread refill */                           \
+  X(24, 256, 128, 4, 2, 2, 8, 1, 0) /* as 17, spread refill */                           \
+  X(25, 128, 128, 2, 2, 2, 8, 1, 0) /* as 15, spread refill */                           \
+  X(26, 256, 256, 4, 2, 4, 4, 0, 0) /* 8 waves, wave 64x128, 32-wide K, 4 stages */      \
+  X(27, 256, 256, 4, 2, 5, 4, 0, 0) /* 8 waves, wave 64x128, 32-wide K, 5 stages */      \
+  X(28, 256, 128, 4, 2, 6, 4, 0, 0) /* 8 waves, wave 64x64, 32-wide K, 6 stages */       \
+  X(29, 128, 256, 2, 4, 6, 4, 0, 0) /* 8 waves, wave 64x64, 32-wide K, 6 stages */       \
+  X(30, 128, 128, 2, 2, 5, 8, 0, 0) /* wave 64x64, 5 stages */                           \
+  X(31, 128, 128, 2, 2, 4, 8, 0, 0) /* wave 64x64, 4 stages */                           \
+  X(32, 256, 32, 4, 1, 3, 8, 0, 0)  /* wave 64x32 */                                 \
+  X(33, 128, 128, 2, 2, 2, 4, 0, 3) /* wave 64x64, 32-wide K, registers for 3 waves per SIMD */ \
+  X(34, 128, 128, 2, 2, 3, 4, 0, 3) /* as 33, three stages */                          \
+  X(35, 64, 128, 1, 4, 2, 4, 0, 4)  /* wave 64x32, 32-wide K, 4 waves per SIMD */       \
+  X(36, 128, 64, 2, 2, 2, 4, 0, 4)  /* wave 64x32, 32-wide K, 4 waves per SIMD */       \
+  X(37, 256, 128, 4, 2, 2, 4, 0, 2) /* 8 waves, wave 64x64, 32-wide K */
 
-#define RAFIKI_CFG_ENTRY(id, BM, BN, WM, WN, ST, KC, SP) {BM, BN, WM * WN, ST, KC * 8},
+#define RAFIKI_CFG_ENTRY(id, BM, BN, WM, WN, ST, KC, SP, OC) {BM, BN, WM * WN, ST, KC * 8},
 const MfmaConfig kMfmaConfigs[kNumMfmaConfigs] = {RAFIKI_MFMA_CONFIGS(RAFIKI_CFG_ENTRY)};
 #undef RAFIKI_CFG_ENTRY
 
-#define RAFIKI_INSTANTIATE(id, BM, BN, WM, WN, ST, KC, SP)                                      \
-  template __global__ void conv_mfma_kernel<BM, BN, WM, WN, ST, true, KC, false, SP>(ConvArgs);  \
-  template __global__ void conv_mfma_kernel<BM, BN, WM, WN, ST, false, KC, false, SP>(ConvArgs); \
-  template __global__ void conv_mfma_kernel<BM, BN, WM, WN, ST, true, KC, true, SP>(ConvArgs);   \
-  template __global__ void conv_mfma_kernel<BM, BN, WM, WN, ST, false, KC, true, SP>(ConvArgs);
+#define RAFIKI_INSTANTIATE(id, BM, BN, WM, WN, ST, KC, SP, OC)                                      \
+  template __global__ void conv_mfma_kernel<BM, BN, WM, WN, ST, true, KC, false, SP, OC>(ConvArgs);  \
+  template __global__ void conv_mfma_kernel<BM, BN, WM, WN, ST, false, KC, false, SP, OC>(ConvArgs); \
+  template __global__ void conv_mfma_kernel<BM, BN, WM, WN, ST, true, KC, true, SP, OC>(ConvArgs);   \
+  template __global__ void conv_mfma_kernel<BM, BN, WM, WN, ST, false, KC, true, SP, OC>(ConvArgs);
 RAFIKI_MFMA_CONFIGS(RAFIKI_INSTANTIATE)
 #undef RAFIKI_INSTANTIATE
 
 hipError_t launch_conv_mfma(const ConvArgs& a, int cfg, int splits, hipStream_t s) {
   switch (cfg) {
-#define RAFIKI_CASE(id, BM, BN, WM, WN, ST, KC, SP) \
-    case id: return launch_mfma_cfg<BM, BN, WM, WN, ST, KC, SP>(a, splits, s);
+#define RAFIKI_CASE(id, BM, BN, WM, WN, ST, KC, SP, OC) \
+    case id: return launch_mfma_cfg<BM, BN, WM, WN, ST, KC, SP, OC>(a, splits, s);
     RAFIKI_MFMA_CONFIGS(RAFIKI_CASE)
 #undef RAFIKI_CASE
     default: return hipErrorInvalidValue;
