@@ -228,7 +228,10 @@ __global__ __launch_bounds__(WM * WN * 64, OCC > 0 ? OCC : 1) void conv_mfma_ker
   const int tile = (xcd < r8 ? xcd * (q + 1) : r8 * (q + 1) + (xcd - r8) * q) + loc;
   const int nt = tile % a.n_tiles, mt = tile / a.n_tiles;
   const int m0 = mt * BM, n0 = nt * BN;
-  const int ktiles = a.Kp / (8 * KC);
+  // K tiles that hold any of the K real terms (Kp may pad K by up to 63 with zeros, a
+  // whole 32-wide tile of them when KC = 4); skipping a tile of zero products leaves
+  // every sum unchanged, bit for bit
+  const int ktiles = (a.K + 8 * KC - 1) / (8 * KC);
   const int kps = a.kt_per_split * (8 / KC);      // kt_per_split counts 64-wide tiles
   const int kt_begin = blockIdx.y * kps;
   const int nk = min(kps, ktiles - kt_begin);
