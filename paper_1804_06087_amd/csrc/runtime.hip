@@ -216,7 +216,7 @@ int choose_splits(int M, int c_out, int ktiles) {
   const int per = (ktiles + s - 1) / s;
   return (ktiles + per - 1) / per;
 }
-// Fixed tile of split-K launches.
+// Untuned tile of split-K launches.
 int split_cfg(int c_out) { return c_out <= 32 ? 10 : (c_out <= 64 ? 8 : 6); }
 // Untuned default: the 64-pixel tiles are the most robust across shapes.
 int default_cfg(int c_out) { return c_out <= 32 ? 10 : (c_out <= 64 ? 8 : 6); }
@@ -554,16 +554,16 @@ int run_gemm(const rafiki_ensemble_s* e, const Op& op, ConvArgs a, hipStream_t s
   }
   if ((long long)a.N * a.H * a.W * a.Cs * 2 >= (1LL << 31) || (long long)a.Co_pad * a.Kp * 2 >= (1LL << 31))
     return fail(RAFIKI_ERR_UNSUPPORTED, "a layer's input or weights exceed 2 GiB; use a smaller max_batch");
-  if (cfg < 0) cfg = default_cfg(op.c_out);
   const int ktiles = a.Kp / 64;
   const int splits = choose_splits(a.M, op.c_out, ktiles);
+  if (cfg < 0) cfg = splits > 1 ? split_cfg(op.c_out) : default_cfg(op.c_out);
   a.kt_per_split = (ktiles + splits - 1) / splits;
   if (splits > 1) {
     const Model& Mo = e->models[mi];
     if ((size_t)splits * a.M * a.Co_pad * 4 > Mo.partial_bytes)
       return fail(RAFIKI_ERR_INVALID, "internal: split-K workspace too small");
     a.partial = Mo.d_partial;
-    TRACED(e, s, RAFIKI_K_CONV_MFMA, mi, li, flops, bytes, launch_conv_mfma(a, split_cfg(op.c_out), splits, s));
+    TRACED(e, s, RAFIKI_K_CONV_MFMA, mi, li, flops, bytes, launch_conv_mfma(a, cfg, splits, s));
     TRACED(e, s, RAFIKI_K_SPLITK_REDUCE, mi, li, 0.0,
            (double)splits * a.M * a.c_write * 4.0 + out_rows * a.c_write * (a.out_f32 ? 4.0 : es),
            launch_splitk_reduce(a, splits, 1, s));
@@ -612,7 +612,13 @@ int tune(rafiki_ensemble_s* e, int n, const void* in, hipStream_t s) {
       choice[mi][oi] = default_cfg(op.c_out);
       if (!timing) continue;
       ConvArgs a = gemm_args(e, M, op, n, in);
-      if (choose_splits(a.M, op.c_out, a.Kp / 64) > 1) continue;
+      // Split-K launches keep the split of K that the shape fixes (so the sums do not
+      // depend on the tile either); only their tile is tuned.
+      const int splits = choose_splits(a.M, op.c_out, a.Kp / 64);
+      if (splits > 1) {
+        choice[mi][oi] = split_cfg(op.c_out);
+        a.partial = M.d_partial;
+      }
       if ((long long)a.N * a.H * a.W * a.Cs * 2 >= (1LL << 31) || (long long)a.Co_pad * a.Kp * 2 >= (1LL << 31))
         continue;   // run_gemm rejects these shapes
       // scratch output: the op's own arena slot, or the model's logits slot
@@ -622,7 +628,7 @@ int tune(rafiki_ensemble_s* e, int n, const void* in, hipStream_t s) {
       a.c_write = y.is_logits ? y.c : (op.kind == O_CONV1D ? round_up(op.c_out, 8) : y.Cs);
       a.ldy = a.c_write;
       a.out_f32 = y.is_logits ? 1 : 0;
-      a.kt_per_split = a.Kp / 64;
+      a.kt_per_split = (a.Kp / 64 + splits - 1) / splits;
       float best = 1e30f;
       for (int cfg = 0; cfg < kNumMfmaConfigs; ++cfg) {
         if (!cfg_fits(cfg, op.c_out)) continue;
@@ -630,7 +636,7 @@ int tune(rafiki_ensemble_s* e, int n, const void* in, hipStream_t s) {
         float t = 0.f;
         for (int rep = 0; rep < 4; ++rep) {   // first launch warms caches; keep the best of three
           launch_events() = {ev[0], ev[1]};
-          const hipError_t lst = launch_conv_mfma(a, cfg, 1, s);
+          const hipError_t lst = launch_conv_mfma(a, cfg, splits, s);
           launch_events() = {};
           if (lst != hipSuccess || hipEventSynchronize(ev[1]) != hipSuccess) {
             rc = fail(RAFIKI_ERR_HIP, "tile tuning launch failed");

@@ -1,8 +1,9 @@
 """Every tile configuration of the bf16 GEMM kernel gives bitwise-identical results.
 
 The tuner picks, per layer and batch size, the fastest configuration; that is only
-sound if the choice never changes a bit.  Each probe model is a convolution large
-enough to run unsplit (so the forced configuration is the one launched), followed by
+sound if the choice never changes a bit.  Each probe model is a convolution (unsplit,
+or split over K where the shape asks for it: the split itself is fixed by the shape,
+and the forced configuration is the one launched), followed by
 global average pooling and a random FC: a change of any single conv output element
 moves the pooled sum by far more than its fp32 rounding, so equal logits mean equal
 conv outputs.  The logits are also checked against the oracle.
@@ -50,6 +51,9 @@ CASES = {
     "residual_s1_cout128": ([conv(-1, 64, 128, 1, relu=False), conv(-1, 64, 128, 3, res=0)], (64, 12, 18), 76),
     # 7x7 images: every tile spans several images
     "aligned_3x3_7x7": ([conv(-1, 128, 128, 3)], (128, 7, 7), 340),
+    # few output rows and a long K: split over K (the split is fixed by the shape, the
+    # tile is not), residual added in the split-K reduction
+    "split_k_3x3_7x7_residual": ([conv(-1, 512, 256, 1, relu=False), conv(-1, 512, 256, 3, res=0)], (512, 7, 7), 4),
 }
 
 
