@@ -72,6 +72,10 @@ def parse():
                          "{R50, VGG-16}, {all} at batch sizes 1, 4, 16, 64, 256: one JSON line per point with "
                          "p50/p99 batch latency and images/s")
     ap.add_argument("--sweep-calls", type=int, default=200, help="sweep: timed calls per point")
+    ap.add_argument("--memory-kernels", action="store_true",
+                    help="HBM bandwidth of the path's memory-bound kernels called on their own (combine, vote, "
+                         "max-pool, global average pool) at ImageNet-shaped sizes, against the 8 TB/s peak and a "
+                         "plain device copy; one JSON line per kernel")
     return ap.parse_args()
 
 
@@ -294,6 +298,71 @@ def rl_main(args, dev):
     print(json.dumps(out), flush=True)
 
 
+def memory_main(args, dev):
+    """Standalone memory-bound kernels: the combine at |S| = 3, C = 1000 on a scaled
+    batch of 262,144 rows (the batch-64 combine moves about 1 MB, below launch latency),
+    the ResNet stem max-pool and the VGG-16 first max-pool at batch 64, and the global
+    average pool of ResNet's last stage (batch 64 and a scaled batch of 512).  Best of
+    10 timed calls after 3 warm-up calls; algorithmic bytes = every input and output
+    once."""
+    import torch
+
+    from paper_1804_06087_amd.binding import (combine_mean, combine_vote, maxpool_nhwc_bf16,
+                                              global_avgpool_nhwc_bf16)
+
+    def timed(fn):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        best = 1e30
+        for _ in range(10):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            fn()
+            b.record()
+            b.synchronize()
+            best = min(best, a.elapsed_time(b))
+        return best
+
+    def emit(name, shape, nbytes, ms):
+        gbs = nbytes / (ms / 1e3) / 1e9
+        print(json.dumps({"metric": f"HBM bandwidth of {name}", "value": round(gbs, 1), "unit": "GB/s",
+                          "higher_is_better": True, "n_gpus": 1, "dtype": "f32" if "combine" in name or "vote" in name
+                          else "bf16", "data": "synthetic", "config": {"kernel": name, "shape": shape},
+                          "ms": round(ms, 4), "bytes": int(nbytes),
+                          "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS,
+                                       "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4)}}), flush=True)
+
+    g = torch.Generator(device=dev)
+    g.manual_seed(0)
+    # plain device copy, for context (read + write)
+    src = torch.empty(2 ** 28, dtype=torch.float32, device=dev).normal_(generator=g)
+    dst = torch.empty_like(src)
+    emit("device copy (torch)", [2 ** 28], 2 * src.numel() * 4, timed(lambda: dst.copy_(src)))
+    del src, dst
+    S, n, C = 3, 262144, 1000
+    z = torch.empty((S, n, C), dtype=torch.float32, device=dev).normal_(generator=g)
+    p = torch.empty((n, C), dtype=torch.float32, device=dev)
+    lab = torch.empty((n,), dtype=torch.int32, device=dev)
+    nb = n * C * 4 * (S + 1) + 4 * n
+    emit("combine (softmax, mean, argmax)", [S, n, C], nb, timed(lambda: combine_mean(z, p, lab)))
+    emit("majority-vote combine", [S, n, C], nb, timed(lambda: combine_vote(z, p, lab)))
+    del z, p, lab
+    for name, (N, H, W, Cc), k, st, pd in (("max-pool 3x3/2 pad 1 (ResNet stem)", (64, 112, 112, 64), 3, 2, 1),
+                                         ("max-pool 2x2/2 (VGG-16 pool1)", (64, 224, 224, 64), 2, 2, 0)):
+        x = torch.empty((N, H, W, Cc), dtype=torch.bfloat16, device=dev).normal_(generator=g)
+        Ho, Wo = (H + 2 * pd - k) // st + 1, (W + 2 * pd - k) // st + 1
+        y = torch.empty((N, Ho, Wo, Cc), dtype=torch.bfloat16, device=dev)
+        emit(name, [N, H, W, Cc], (x.numel() + y.numel()) * 2, timed(lambda: maxpool_nhwc_bf16(x, y, k, st, pd)))
+        del x, y
+    for N in (64, 512):
+        x = torch.empty((N, 7, 7, 2048), dtype=torch.bfloat16, device=dev).normal_(generator=g)
+        y = torch.empty((N, 2048), dtype=torch.bfloat16, device=dev)
+        emit("global average pool (ResNet last stage)", [N, 7, 7, 2048], (x.numel() + y.numel()) * 2,
+             timed(lambda: global_avgpool_nhwc_bf16(x, y)))
+        del x, y
+
+
 def sweep_main(args, dev):
     """Latency/accuracy trade-off grid (Section 5.2): every subset of the ImageNet-shaped
     ensemble at every batch size, one handle (max batch 256) over one 256-image draw whose
@@ -372,6 +441,9 @@ def main():
         return
     if args.sweep:
         sweep_main(args, dev)
+        return
+    if args.memory_kernels:
+        memory_main(args, dev)
         return
 
     if args.workload == "c4":

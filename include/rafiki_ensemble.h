@@ -192,6 +192,35 @@ int rafiki_ensemble_trace(rafiki_ensemble_t h, int enable);
  * keep them (call again with a larger buffer).  Host-blocking. */
 int rafiki_ensemble_trace_read(rafiki_ensemble_t h, rafiki_trace_rec* out, int cap, int* count);
 
+/* Standalone kernels of the path, on caller-owned contiguous device buffers, enqueued on
+ * `stream` (hipStream_t as void*; 0 = the null stream).  They are the kernels infer uses,
+ * exposed for measurement and for callers that hold their own tensors (for example logits
+ * of models that ran on other GPUs and were gathered, the model-sharded layout of the
+ * paper's one-model-per-GPU deployment).  Argument errors return RAFIKI_ERR_INVALID
+ * before any device call; nothing is allocated.
+ *
+ * Ensemble combine (Section 1; Section 5.2): logits fp32 [n_models][n][n_classes]; the
+ * mean of the per-model softmax to out_probs fp32 [n][n_classes] and its first-index
+ * argmax to out_labels int32 [n].  1 <= n_models <= 32, n >= 1, 1 <= n_classes <= 1024. */
+int rafiki_combine_mean(const float* logits, int n_models, int n, int n_classes, float* out_probs,
+                        int32_t* out_labels, void* stream);
+
+/* Majority vote over the same logits (ties to the lowest model index's class; see
+ * rafiki_ensemble_infer_vote): vote fractions to out_votes [n][n_classes], winners to
+ * out_labels [n].  Same limits. */
+int rafiki_combine_vote(const float* logits, int n_models, int n, int n_classes, float* out_votes,
+                        int32_t* out_labels, void* stream);
+
+/* Max-pool k x k, stride, padding pad on each side (padding cells never win: they are -inf),
+ * over bf16 NHWC x [n][h][w][c] into y [n][ho][wo][c] with ho = (h + 2 pad - k) / stride + 1
+ * (floor; likewise wo).  c a multiple of 8; k >= 1, stride >= 1, 0 <= pad < k; ho, wo >= 1. */
+int rafiki_maxpool_nhwc_bf16(const void* x, void* y, int n, int h, int w, int c, int k, int stride, int pad,
+                             void* stream);
+
+/* Global average pool over bf16 NHWC x [n][h][w][c] into y [n][c] (fp32 sums in a fixed
+ * order, one rounding to bf16).  c a multiple of 8. */
+int rafiki_global_avgpool_nhwc_bf16(const void* x, void* y, int n, int h, int w, int c, void* stream);
+
 /* Diagnostics: tile configurations of the bf16 GEMM kernel.  Configuration `cfg`
  * (0 .. count - 1) computes output tiles of bm pixels x bn channels with `waves`
  * wavefronts, `stages` K tiles of bk channels in flight.  Every configuration sums each

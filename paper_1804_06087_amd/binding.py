@@ -22,7 +22,8 @@ RAFIKI_INPUT_IMAGE_NCHW_F32, RAFIKI_INPUT_TOKENS_I32 = 0, 1
 EXPORTED = ("rafiki_ensemble_create", "rafiki_ensemble_infer", "rafiki_ensemble_infer_vote",
             "rafiki_ensemble_model_logits",
             "rafiki_ensemble_info", "rafiki_ensemble_trace", "rafiki_ensemble_trace_read",
-            "rafiki_tile_config", "rafiki_ensemble_force_tile",
+            "rafiki_tile_config", "rafiki_ensemble_force_tile", "rafiki_combine_mean", "rafiki_combine_vote",
+            "rafiki_maxpool_nhwc_bf16", "rafiki_global_avgpool_nhwc_bf16",
             "rafiki_ensemble_destroy", "rafiki_greedy_decide", "rafiki_greedy_simulate", "rafiki_greedy_simulate_multi",
             "rafiki_ensemble_profile", "rafiki_ensemble_serve_greedy", "rafiki_ensemble_serve_greedy_async",
             "rafiki_rl_create", "rafiki_rl_destroy", "rafiki_rl_info", "rafiki_rl_get_params", "rafiki_rl_set_params",
@@ -103,6 +104,10 @@ def load_library(path: str = LIB_PATH):
     lib.rafiki_ensemble_trace_read.argtypes = [C.c_void_p, C.POINTER(RafikiTraceRec), C.c_int, C.POINTER(C.c_int)]
     lib.rafiki_tile_config.argtypes = [C.c_int] + [C.POINTER(C.c_int)] * 5
     lib.rafiki_ensemble_force_tile.argtypes = [C.c_void_p, C.c_int]
+    lib.rafiki_combine_mean.argtypes = [C.c_void_p, C.c_int, C.c_int, C.c_int, C.c_void_p, C.c_void_p, C.c_void_p]
+    lib.rafiki_combine_vote.argtypes = [C.c_void_p, C.c_int, C.c_int, C.c_int, C.c_void_p, C.c_void_p, C.c_void_p]
+    lib.rafiki_maxpool_nhwc_bf16.argtypes = [C.c_void_p, C.c_void_p] + [C.c_int] * 7 + [C.c_void_p]
+    lib.rafiki_global_avgpool_nhwc_bf16.argtypes = [C.c_void_p, C.c_void_p] + [C.c_int] * 4 + [C.c_void_p]
     P = C.POINTER
     lib.rafiki_greedy_decide.argtypes = [P(RafikiGreedyPolicy), C.c_int64, C.c_int64, P(C.c_int32)]
     lib.rafiki_greedy_simulate.argtypes = [P(RafikiGreedyPolicy), P(C.c_int64), C.c_int64, P(C.c_int64),
@@ -356,6 +361,57 @@ def make_layers(spec, params, keep: list):
             r.bn_eps = float(P.bn_eps)
     keep.append(arr)
     return arr
+
+
+def _expect(t, shape, dtype, name):
+    """Raise ValueError unless torch tensor ``t`` is a contiguous device tensor of that shape and dtype."""
+    if not t.is_cuda or t.dtype != dtype or tuple(t.shape) != tuple(shape) or not t.is_contiguous():
+        raise ValueError(f"{name}: expected a contiguous device tensor {tuple(shape)} of {dtype}, got "
+                         f"{tuple(t.shape)} {t.dtype} on {t.device}"
+                         f"{'' if t.is_contiguous() else ' (not contiguous)'}")
+
+
+def _combine_io(logits, out, labels):
+    import torch
+    if logits.dim() != 3:
+        raise ValueError("logits: expected [S, n, C]")
+    S, n, C = logits.shape
+    _expect(logits, (S, n, C), torch.float32, "logits")
+    _expect(out, (n, C), torch.float32, "output")
+    _expect(labels, (n,), torch.int32, "labels")
+    return S, n, C
+
+
+def combine_mean(logits, out_probs, out_labels, stream=None):
+    """Standalone combine: logits [S, n, C] fp32 -> mean softmax [n, C], first-index argmax [n]."""
+    S, n, C = _combine_io(logits, out_probs, out_labels)
+    _check(load_library().rafiki_combine_mean(_ptr(logits), S, n, C, _ptr(out_probs), _ptr(out_labels),
+                                              _stream(stream)))
+
+
+def combine_vote(logits, out_votes, out_labels, stream=None):
+    """Standalone majority vote over logits [S, n, C] fp32."""
+    S, n, C = _combine_io(logits, out_votes, out_labels)
+    _check(load_library().rafiki_combine_vote(_ptr(logits), S, n, C, _ptr(out_votes), _ptr(out_labels),
+                                              _stream(stream)))
+
+
+def maxpool_nhwc_bf16(x, y, k: int, stride: int, pad: int, stream=None):
+    """Standalone max-pool over a bf16 NHWC tensor x [n, h, w, c] into y [n, ho, wo, c]."""
+    import torch
+    n, h, w, c = x.shape
+    _expect(x, (n, h, w, c), torch.bfloat16, "x")
+    _expect(y, (n, (h + 2 * pad - k) // stride + 1, (w + 2 * pad - k) // stride + 1, c), torch.bfloat16, "y")
+    _check(load_library().rafiki_maxpool_nhwc_bf16(_ptr(x), _ptr(y), n, h, w, c, k, stride, pad, _stream(stream)))
+
+
+def global_avgpool_nhwc_bf16(x, y, stream=None):
+    """Standalone global average pool over a bf16 NHWC tensor x [n, h, w, c] into y [n, c]."""
+    import torch
+    n, h, w, c = x.shape
+    _expect(x, (n, h, w, c), torch.bfloat16, "x")
+    _expect(y, (n, c), torch.bfloat16, "y")
+    _check(load_library().rafiki_global_avgpool_nhwc_bf16(_ptr(x), _ptr(y), n, h, w, c, _stream(stream)))
 
 
 def tile_configs():

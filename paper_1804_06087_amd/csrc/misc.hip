@@ -292,31 +292,60 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
+// VEC = 4 (n_classes a multiple of 4): lane-contiguous float4 loads and stores, each
+// lane holding classes 4 (i * 64 + lane) + j; VEC = 1: classes i * 64 + lane.  Either way
+// the classes a lane holds increase with its register index, so keeping the first
+// maximum in a lane and the lower index across lanes gives the first-index argmax.
+template <int VEC>
+__device__ __forceinline__ int class_of(int i, int j, int lane) {
+  return VEC == 4 ? 4 * (i * 64 + lane) + j : i * 64 + lane;
+}
+
+// Loads the row's logits of one model into v (-inf past n_classes).
+template <int VEC>
+__device__ __forceinline__ void load_row(const float* z, int C, int lane, float v[kCombineMaxPerLane]) {
+  if constexpr (VEC == 4) {
+#pragma unroll
+    for (int i = 0; i < kCombineMaxPerLane / 4; ++i) {
+      const int c = 4 * (i * 64 + lane);
+      const float4 q = c < C ? *(const float4*)(z + c) : make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
+      v[4 * i + 0] = q.x; v[4 * i + 1] = q.y; v[4 * i + 2] = q.z; v[4 * i + 3] = q.w;
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < kCombineMaxPerLane; ++i) {
+      const int c = i * 64 + lane;
+      v[i] = c < C ? z[c] : -INFINITY;
+    }
+  }
+}
+
+template <int VEC>
 __global__ __launch_bounds__(256) void combine_kernel(CombineArgs a) {
   const int lane = threadIdx.x & 63;
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= a.n) return;
-  const int per = (a.C + 63) / 64;
+  constexpr int R = kCombineMaxPerLane / VEC;   // register groups of VEC classes
   float acc[kCombineMaxPerLane];
 #pragma unroll
   for (int i = 0; i < kCombineMaxPerLane; ++i) acc[i] = 0.f;
   for (int s = 0; s < a.S; ++s) {
     const float* z = a.logits + a.sel[s] * a.ld_model + (long long)row * a.C;
     float v[kCombineMaxPerLane];
+    load_row<VEC>(z, a.C, lane, v);
     float mx = -INFINITY;
 #pragma unroll
-    for (int i = 0; i < kCombineMaxPerLane; ++i) {
-      const int c = i * 64 + lane;
-      v[i] = (i < per && c < a.C) ? z[c] : -INFINITY;
-      mx = fmaxf(mx, v[i]);
-    }
+    for (int i = 0; i < kCombineMaxPerLane; ++i) mx = fmaxf(mx, v[i]);
     mx = wave_max(mx);
     float sum = 0.f;
 #pragma unroll
-    for (int i = 0; i < kCombineMaxPerLane; ++i) {
-      v[i] = (i < per && i * 64 + lane < a.C) ? expf(v[i] - mx) : 0.f;
-      sum += v[i];
-    }
+    for (int i = 0; i < R; ++i)
+#pragma unroll
+      for (int j = 0; j < VEC; ++j) {
+        const int k = i * VEC + j;
+        v[k] = class_of<VEC>(i, j, lane) < a.C ? expf(v[k] - mx) : 0.f;
+        sum += v[k];
+      }
     sum = wave_sum(sum);
     const float inv = 1.0f / sum;
 #pragma unroll
@@ -325,13 +354,20 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineArgs a) {
   const float invS = 1.0f / (float)a.S;
   float best = -INFINITY;
   int bidx = 0x7fffffff;
+  float* prow = a.probs + (long long)row * a.C;
 #pragma unroll
-  for (int i = 0; i < kCombineMaxPerLane; ++i) {
-    const int c = i * 64 + lane;
-    if (i < per && c < a.C) {
-      const float p = acc[i] * invS;
-      a.probs[(long long)row * a.C + c] = p;
-      if (p > best) { best = p; bidx = c; }     // c increases with i: keeps the first max
+  for (int i = 0; i < R; ++i) {
+    float p[VEC];
+#pragma unroll
+    for (int j = 0; j < VEC; ++j) {
+      p[j] = acc[i * VEC + j] * invS;
+      const int c = class_of<VEC>(i, j, lane);
+      if (c < a.C && p[j] > best) { best = p[j]; bidx = c; }
+    }
+    const int c0 = class_of<VEC>(i, 0, lane);
+    if (c0 < a.C) {
+      if constexpr (VEC == 4) *(float4*)(prow + c0) = make_float4(p[0], p[1], p[2], p[3]);
+      else prow[c0] = p[0];
     }
   }
 #pragma unroll
@@ -343,9 +379,16 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineArgs a) {
   if (lane == 0) a.labels[row] = bidx;
 }
 
+// The float4 path needs every row of logits and of the output on a 16-byte boundary.
+static bool vec4_ok(const CombineArgs& a) {
+  return a.C % 4 == 0 && a.ld_model % 4 == 0 &&
+         (((uintptr_t)a.logits | (uintptr_t)a.probs) & 15) == 0;
+}
+
 hipError_t launch_combine(const CombineArgs& a, hipStream_t s) {
   if (a.C > 64 * kCombineMaxPerLane || a.S < 1) return hipErrorInvalidValue;
-  launch(combine_kernel, dim3((a.n + 3) / 4), dim3(256), s, a);
+  if (vec4_ok(a)) launch(combine_kernel<4>, dim3((a.n + 3) / 4), dim3(256), s, a);
+  else launch(combine_kernel<1>, dim3((a.n + 3) / 4), dim3(256), s, a);
   return hipGetLastError();
 }
 
@@ -354,23 +397,24 @@ hipError_t launch_combine(const CombineArgs& a, hipStream_t s) {
 // the maximum of its logits; lane s keeps the prediction of selected model s (S <= 32,
 // priority = selection order).  The winner is the prediction with the most votes,
 // the tie going to the lowest s.  All integer work: exact and order independent.
+template <int VEC>
 __global__ __launch_bounds__(256) void vote_kernel(CombineArgs a) {
   const int lane = threadIdx.x & 63;
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= a.n) return;
-  const int per = (a.C + 63) / 64;
+  constexpr int R = kCombineMaxPerLane / VEC;
   int pred_mine = -1;
   for (int s = 0; s < a.S; ++s) {
     const float* z = a.logits + a.sel[s] * a.ld_model + (long long)row * a.C;
+    float v[kCombineMaxPerLane];
+    load_row<VEC>(z, a.C, lane, v);   // all of the row's loads first, then the scan
     float best = -INFINITY;
     int bidx = 0x7fffffff;
-    for (int i = 0; i < per; ++i) {
-      const int c = i * 64 + lane;
-      if (c < a.C) {
-        const float v = z[c];
-        if (v > best) { best = v; bidx = c; }
-      }
-    }
+#pragma unroll
+    for (int i = 0; i < R; ++i)
+#pragma unroll
+      for (int j = 0; j < VEC; ++j)
+        if (v[i * VEC + j] > best) { best = v[i * VEC + j]; bidx = class_of<VEC>(i, j, lane); }
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) {
       const float ob = __shfl_xor(best, o, 64);
@@ -389,18 +433,30 @@ __global__ __launch_bounds__(256) void vote_kernel(CombineArgs a) {
   const int winner = 63 - (key & 63);
   const int label = __shfl(pred_mine, winner, 64);
   const float invS = 1.0f / (float)a.S;
-  for (int i = 0; i < per; ++i) {
-    const int c = i * 64 + lane;
-    int votes = 0;
-    for (int t = 0; t < a.S; ++t) votes += (__shfl(pred_mine, t, 64) == c) ? 1 : 0;
-    if (c < a.C) a.probs[(long long)row * a.C + c] = (float)votes * invS;
+  float* prow = a.probs + (long long)row * a.C;
+#pragma unroll
+  for (int i = 0; i < R; ++i) {
+    float f[VEC];
+#pragma unroll
+    for (int j = 0; j < VEC; ++j) {
+      const int c = class_of<VEC>(i, j, lane);
+      int votes = 0;
+      for (int t = 0; t < a.S; ++t) votes += (__shfl(pred_mine, t, 64) == c) ? 1 : 0;
+      f[j] = (float)votes * invS;
+    }
+    const int c0 = class_of<VEC>(i, 0, lane);
+    if (c0 < a.C) {
+      if constexpr (VEC == 4) *(float4*)(prow + c0) = make_float4(f[0], f[1], f[2], f[3]);
+      else prow[c0] = f[0];
+    }
   }
   if (lane == 0) a.labels[row] = label;
 }
 
 hipError_t launch_vote(const CombineArgs& a, hipStream_t s) {
-  if (a.S < 1 || a.S > 32 || a.C < 1) return hipErrorInvalidValue;
-  launch(vote_kernel, dim3((a.n + 3) / 4), dim3(256), s, a);
+  if (a.S < 1 || a.S > 32 || a.C < 1 || a.C > 64 * kCombineMaxPerLane) return hipErrorInvalidValue;
+  if (vec4_ok(a)) launch(vote_kernel<4>, dim3((a.n + 3) / 4), dim3(256), s, a);
+  else launch(vote_kernel<1>, dim3((a.n + 3) / 4), dim3(256), s, a);
   return hipGetLastError();
 }
 

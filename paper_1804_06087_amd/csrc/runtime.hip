@@ -970,6 +970,52 @@ int rafiki_ensemble_trace_read(rafiki_ensemble_t h, rafiki_trace_rec* out, int c
   return RAFIKI_OK;
 }
 
+static int combine_standalone(const float* logits, int n_models, int n, int n_classes, float* out,
+                              int32_t* labels, void* stream, bool vote) {
+  if (!logits || !out || !labels) return fail(RAFIKI_ERR_INVALID, "null pointer");
+  if (n_models < 1 || n_models > 32) return fail(RAFIKI_ERR_INVALID, "n_models must be in [1, 32]");
+  if (n < 1 || n_classes < 1 || n_classes > 1024)
+    return fail(RAFIKI_ERR_INVALID, "n must be >= 1 and n_classes in [1, 1024]");
+  CombineArgs ca{};
+  ca.logits = logits;
+  ca.ld_model = (long long)n * n_classes;
+  for (int m = 0; m < n_models; ++m) ca.sel[ca.S++] = m;
+  ca.n = n; ca.C = n_classes; ca.probs = out; ca.labels = labels;
+  const hipError_t st = vote ? launch_vote(ca, (hipStream_t)stream) : launch_combine(ca, (hipStream_t)stream);
+  if (st != hipSuccess) return fail(RAFIKI_ERR_HIP, std::string("combine launch: ") + hipGetErrorString(st));
+  return RAFIKI_OK;
+}
+
+int rafiki_combine_mean(const float* logits, int n_models, int n, int n_classes, float* out_probs,
+                        int32_t* out_labels, void* stream) {
+  return combine_standalone(logits, n_models, n, n_classes, out_probs, out_labels, stream, false);
+}
+
+int rafiki_combine_vote(const float* logits, int n_models, int n, int n_classes, float* out_votes,
+                        int32_t* out_labels, void* stream) {
+  return combine_standalone(logits, n_models, n, n_classes, out_votes, out_labels, stream, true);
+}
+
+int rafiki_maxpool_nhwc_bf16(const void* x, void* y, int n, int h, int w, int c, int k, int stride, int pad,
+                             void* stream) {
+  if (!x || !y) return fail(RAFIKI_ERR_INVALID, "null pointer");
+  if (n < 1 || h < 1 || w < 1 || c < 8 || c % 8 || k < 1 || stride < 1 || pad < 0 || pad >= k)
+    return fail(RAFIKI_ERR_INVALID, "maxpool geometry invalid (c a multiple of 8, pad < k)");
+  if (h + 2 * pad < k || w + 2 * pad < k) return fail(RAFIKI_ERR_INVALID, "maxpool output would be empty");
+  const int ho = (h + 2 * pad - k) / stride + 1, wo = (w + 2 * pad - k) / stride + 1;
+  const hipError_t st = launch_maxpool(x, y, n, h, w, c, ho, wo, k, stride, pad, 1, (hipStream_t)stream);
+  if (st != hipSuccess) return fail(RAFIKI_ERR_HIP, std::string("maxpool launch: ") + hipGetErrorString(st));
+  return RAFIKI_OK;
+}
+
+int rafiki_global_avgpool_nhwc_bf16(const void* x, void* y, int n, int h, int w, int c, void* stream) {
+  if (!x || !y) return fail(RAFIKI_ERR_INVALID, "null pointer");
+  if (n < 1 || h < 1 || w < 1 || c < 8 || c % 8) return fail(RAFIKI_ERR_INVALID, "pool geometry invalid");
+  const hipError_t st = launch_spatial_reduce(x, y, n, h * w, c, 0, 1, (hipStream_t)stream);
+  if (st != hipSuccess) return fail(RAFIKI_ERR_HIP, std::string("pool launch: ") + hipGetErrorString(st));
+  return RAFIKI_OK;
+}
+
 int rafiki_tile_config(int cfg, int* bm, int* bn, int* waves, int* stages, int* bk) {
   if (cfg < 0 || cfg >= kNumMfmaConfigs) return fail(RAFIKI_ERR_INVALID, "no such tile configuration");
   const MfmaConfig& c = kMfmaConfigs[cfg];
