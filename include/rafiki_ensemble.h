@@ -234,6 +234,23 @@ int rafiki_tile_config(int cfg, int* bm, int* bn, int* waves, int* stages, int* 
  * are unchanged; only speed differs. */
 int rafiki_ensemble_force_tile(rafiki_ensemble_t h, int cfg);
 
+/* Graph replay of the forward passes (off by default; environment RAFIKI_GRAPHS=1 turns
+ * it on at create).  Measured on MI355X it is no faster than the eager launches for one
+ * model and slower for several, whose branches the replay did not overlap as well as
+ * the per-model streams do.  Once a batch size n has been tuned, infer / infer_vote capture the
+ * forward passes of (n, model_subset_mask) into a HIP graph on first use and replay it
+ * on later calls: the staging of `batch` and the combine into the caller's buffers are
+ * launched around the graph on `stream`, so results are those of the eager launches bit
+ * for bit.  At most 64 (n, mask) graphs are kept per handle; further pairs run eagerly.
+ * Token input is first copied (device to device, on `stream`) into a buffer of the
+ * handle that the graph reads.  A capture that fails disables graphs for the handle and
+ * the call runs eagerly.  Tracing (rafiki_ensemble_trace) always runs eagerly.
+ * use_graphs synchronises the device and drops every kept graph; enable = 0 turns
+ * replay off.  force_tile also drops them.  graph_stats reports the graphs kept, the
+ * replays so far and the failed captures; any output pointer may be NULL. */
+int rafiki_ensemble_use_graphs(rafiki_ensemble_t h, int enable);
+int rafiki_ensemble_graph_stats(rafiki_ensemble_t h, int* n_graphs, long long* replays, long long* failures);
+
 /* Synchronise the device, free everything the handle owns.  NULL is accepted. */
 int rafiki_ensemble_destroy(rafiki_ensemble_t h);
 

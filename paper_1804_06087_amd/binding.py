@@ -22,7 +22,8 @@ RAFIKI_INPUT_IMAGE_NCHW_F32, RAFIKI_INPUT_TOKENS_I32 = 0, 1
 EXPORTED = ("rafiki_ensemble_create", "rafiki_ensemble_infer", "rafiki_ensemble_infer_vote",
             "rafiki_ensemble_model_logits",
             "rafiki_ensemble_info", "rafiki_ensemble_trace", "rafiki_ensemble_trace_read",
-            "rafiki_tile_config", "rafiki_ensemble_force_tile", "rafiki_combine_mean", "rafiki_combine_vote",
+            "rafiki_tile_config", "rafiki_ensemble_force_tile", "rafiki_ensemble_use_graphs",
+            "rafiki_ensemble_graph_stats", "rafiki_combine_mean", "rafiki_combine_vote",
             "rafiki_maxpool_nhwc_bf16", "rafiki_global_avgpool_nhwc_bf16",
             "rafiki_ensemble_destroy", "rafiki_greedy_decide", "rafiki_greedy_simulate", "rafiki_greedy_simulate_multi",
             "rafiki_ensemble_profile", "rafiki_ensemble_serve_greedy", "rafiki_ensemble_serve_greedy_async",
@@ -104,6 +105,9 @@ def load_library(path: str = LIB_PATH):
     lib.rafiki_ensemble_trace_read.argtypes = [C.c_void_p, C.POINTER(RafikiTraceRec), C.c_int, C.POINTER(C.c_int)]
     lib.rafiki_tile_config.argtypes = [C.c_int] + [C.POINTER(C.c_int)] * 5
     lib.rafiki_ensemble_force_tile.argtypes = [C.c_void_p, C.c_int]
+    lib.rafiki_ensemble_use_graphs.argtypes = [C.c_void_p, C.c_int]
+    lib.rafiki_ensemble_graph_stats.argtypes = [C.c_void_p, C.POINTER(C.c_int), C.POINTER(C.c_longlong),
+                                                C.POINTER(C.c_longlong)]
     lib.rafiki_combine_mean.argtypes = [C.c_void_p, C.c_int, C.c_int, C.c_int, C.c_void_p, C.c_void_p, C.c_void_p]
     lib.rafiki_combine_vote.argtypes = [C.c_void_p, C.c_int, C.c_int, C.c_int, C.c_void_p, C.c_void_p, C.c_void_p]
     lib.rafiki_maxpool_nhwc_bf16.argtypes = [C.c_void_p, C.c_void_p] + [C.c_int] * 7 + [C.c_void_p]
@@ -522,6 +526,16 @@ class Ensemble:
     def force_tile(self, cfg: int):
         """Use tile configuration ``cfg`` for every unsplit bf16 GEMM it suits (-1: tuned)."""
         _check(self._lib.rafiki_ensemble_force_tile(self._h, cfg))
+
+    def use_graphs(self, enable: bool):
+        """Turn graph replay of the forward passes on or off (drops every kept graph)."""
+        _check(self._lib.rafiki_ensemble_use_graphs(self._h, 1 if enable else 0))
+
+    def graph_stats(self):
+        """(graphs kept, replays so far, failed captures)."""
+        g, r, f = C.c_int(0), C.c_longlong(0), C.c_longlong(0)
+        _check(self._lib.rafiki_ensemble_graph_stats(self._h, C.byref(g), C.byref(r), C.byref(f)))
+        return g.value, r.value, f.value
 
     def trace_read(self):
         """List of dicts {kind, model, layer, flops, bytes, ms} for the traced launches."""

@@ -15,11 +15,15 @@ struct LaunchEvents {
 };
 LaunchEvents& launch_events();
 
-// Every kernel of the library is launched through this, so tracing can time it.
+// Every kernel of the library is launched through this, so tracing can time it.  An
+// untimed launch is a plain launch, which stream capture records into a graph.
 template <typename F, typename... Args>
 inline void launch(F kernel, dim3 grid, dim3 block, hipStream_t s, Args... args) {
   const LaunchEvents& ev = launch_events();
-  hipExtLaunchKernelGGL(kernel, grid, block, 0, s, ev.start, ev.stop, 0, args...);
+  if (ev.start || ev.stop)
+    hipExtLaunchKernelGGL(kernel, grid, block, 0, s, ev.start, ev.stop, 0, args...);
+  else
+    hipLaunchKernelGGL(kernel, grid, block, 0, s, args...);
 }
 
 typedef uint16_t bf16_t;   // bfloat16 storage (upper half of an IEEE float)

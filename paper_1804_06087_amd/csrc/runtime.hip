@@ -160,8 +160,30 @@ struct rafiki_ensemble_s {
   std::map<int, std::vector<std::vector<int>>> tuned;
   bool autotune = true;
   int force_tile = -1;              // diagnostic override of the tuned configuration
+  // Forward passes replayed as HIP graphs, one per (batch size, model subset): every
+  // kernel argument inside them (weights, arenas, staged input, logits workspace,
+  // tuned tiles) is fixed once the batch size has been tuned.  Staging and the combine,
+  // which touch the caller's buffers, are launched outside the graph.
+  struct GraphExec {
+    hipGraph_t graph = nullptr;
+    hipGraphExec_t exec = nullptr;
+  };
+  bool use_graphs = false;          // opt-in: replay measured no faster than the eager launches
+  std::map<std::pair<int, uint32_t>, GraphExec> graphs;
+  hipStream_t capture_stream = nullptr;
+  void* d_tokens = nullptr;         // token ids copied here when a graph reads them
+  long long graph_replays = 0, graph_failures = 0;
   size_t esz() const { return precision == RAFIKI_BF16 ? 2 : 4; }
+  void drop_graphs() {
+    for (auto& kv : graphs) {
+      if (kv.second.exec) (void)hipGraphExecDestroy(kv.second.exec);
+      if (kv.second.graph) (void)hipGraphDestroy(kv.second.graph);
+    }
+    graphs.clear();
+  }
   ~rafiki_ensemble_s() {
+    drop_graphs();
+    if (capture_stream) (void)hipStreamDestroy(capture_stream);
     for (Model& M : models) {
       if (M.done) (void)hipEventDestroy(M.done);
       if (M.stream) (void)hipStreamDestroy(M.stream);
@@ -786,6 +808,7 @@ int rafiki_ensemble_create(const rafiki_model_desc* models, int n_models, const 
   e->in_Cs = round_up(e->C, 8);
   if (const char* t = std::getenv("RAFIKI_AUTOTUNE")) e->autotune = std::atoi(t) != 0;
   if (const char* t = std::getenv("RAFIKI_MODEL_STREAMS")) e->concurrent = std::atoi(t) != 0;
+  if (const char* t = std::getenv("RAFIKI_GRAPHS")) e->use_graphs = std::atoi(t) != 0;
   // Pass 1: validate every model and infer shapes without touching the device.
   e->dry = true;
   e->models.resize(n_models);
@@ -826,8 +849,13 @@ int rafiki_ensemble_create(const rafiki_model_desc* models, int n_models, const 
     if (st2 == hipSuccess) st2 = hipEventCreateWithFlags(&M.done, hipEventDisableTiming);
     if (st2 != hipSuccess) return fail(RAFIKI_ERR_HIP, std::string("stream/event creation: ") + hipGetErrorString(st2));
   }
+  if (e->input_kind == RAFIKI_INPUT_TOKENS_I32) {
+    rc = dev_alloc(e.get(), &e->d_tokens, (size_t)e->max_batch * e->H * 4);
+    if (rc) return rc;
+  }
   {
     hipError_t st2 = hipEventCreateWithFlags(&e->staged_ev, hipEventDisableTiming);
+    if (st2 == hipSuccess) st2 = hipStreamCreateWithFlags(&e->capture_stream, hipStreamNonBlocking);
     if (st2 != hipSuccess) return fail(RAFIKI_ERR_HIP, std::string("event creation: ") + hipGetErrorString(st2));
   }
   *out = e.release();
@@ -837,32 +865,15 @@ int rafiki_ensemble_create(const rafiki_model_desc* models, int n_models, const 
 
 }  // extern "C"
 
-// One scheduled batch through the selected models, then the mean (vote = false) or
-// majority-vote (vote = true) combine into out / out_labels.
-static int serve(rafiki_ensemble_t h, const void* batch, int n, uint32_t model_subset_mask, float* out,
-                 int32_t* out_labels, void* stream, bool vote) {
-  int rc = check_call(h, batch, n);
-  if (rc) return rc;
-  if (!out || !out_labels) return fail(RAFIKI_ERR_INVALID, "null output pointer");
-  if (model_subset_mask == 0) return fail(RAFIKI_ERR_INVALID, "model_subset_mask must select at least one model");
-  if (h->n_models < 32 && (model_subset_mask >> h->n_models) != 0)
-    return fail(RAFIKI_ERR_INVALID, "model_subset_mask selects a model that does not exist");
-  hipStream_t s = (hipStream_t)stream;
-  const void* in = model_input(h, batch, h->d_staged);
-  rc = stage(h, batch, n, s, h->d_staged);
-  if (!rc) rc = tune(h, n, in, s);
-  if (rc) return rc;
-  CombineArgs ca{};
-  ca.logits = h->d_logits;
-  ca.ld_model = (long long)h->max_batch * h->n_classes;
-  ca.n = n; ca.C = h->n_classes; ca.probs = out; ca.labels = out_labels;
-  for (int m = 0; m < h->n_models; ++m)
-    if ((model_subset_mask >> m) & 1u) ca.sel[ca.S++] = m;
-  // Selected models are independent until the combine: fork them onto their own
-  // streams after staging and join before the combine (sequential when tracing, so
-  // that each traced kernel has the GPU to itself).  Forked launches are enqueued
-  // interleaved, one op of each model in turn, so that every model stream has work
-  // from the start even when enqueueing is slower than the device.
+// Forward passes of the models ca.sel over n requests whose model input is `in`, logits
+// into the workspace, ordered after the work already on s and before what follows it.
+// Selected models are independent until the combine: they fork onto their own streams
+// and join back (sequential when tracing, so that each traced kernel has the GPU to
+// itself).  Forked launches are enqueued interleaved, one op of each model in turn, so
+// that every model stream has work from the start even when enqueueing is slower than
+// the device.
+static int forward(rafiki_ensemble_t h, const CombineArgs& ca, const void* in, int n, hipStream_t s) {
+  int rc = RAFIKI_OK;
   const bool fork = h->concurrent && !h->trace.on && ca.S > 1;
   if (fork) {
     HIPCHK(hipEventRecord(h->staged_ev, s));
@@ -890,6 +901,92 @@ static int serve(rafiki_ensemble_t h, const void* batch, int n, uint32_t model_s
       rc = run_model(h, m, in, n, h->d_logits + (size_t)m * ca.ld_model, s);
       if (rc) return rc;
     }
+  }
+  return RAFIKI_OK;
+}
+
+constexpr size_t kMaxGraphs = 64;   // (batch size, subset) pairs kept as graphs per handle
+
+// The instantiated graph of the forward passes for (n, mask), captured on first use.
+// *exec stays null when the cache is full or the capture fails; the caller then runs
+// the same launches eagerly (a failed capture is counted and disables graphs).
+static int graph_for(rafiki_ensemble_t h, int n, uint32_t mask, const CombineArgs& ca, const void* in,
+                     hipGraphExec_t* exec) {
+  *exec = nullptr;
+  const auto key = std::make_pair(n, mask);
+  const auto it = h->graphs.find(key);
+  if (it != h->graphs.end()) {
+    *exec = it->second.exec;
+    return RAFIKI_OK;
+  }
+  if (h->graphs.size() >= kMaxGraphs) return RAFIKI_OK;
+  hipStream_t cs = h->capture_stream;
+  if (hipStreamBeginCapture(cs, hipStreamCaptureModeRelaxed) != hipSuccess) {
+    (void)hipGetLastError();
+    ++h->graph_failures;
+    h->use_graphs = false;
+    return RAFIKI_OK;
+  }
+  const int frc = forward(h, ca, in, n, cs);
+  hipGraph_t g = nullptr;
+  const hipError_t est = hipStreamEndCapture(cs, &g);
+  hipGraphExec_t x = nullptr;
+  hipError_t ist = hipErrorUnknown;
+  if (frc == RAFIKI_OK && est == hipSuccess && g) ist = hipGraphInstantiate(&x, g, nullptr, nullptr, 0);
+  if (frc != RAFIKI_OK || est != hipSuccess || ist != hipSuccess) {
+    if (g) (void)hipGraphDestroy(g);
+    (void)hipGetLastError();
+    ++h->graph_failures;
+    h->use_graphs = false;
+    return RAFIKI_OK;
+  }
+  h->graphs[key] = {g, x};
+  *exec = x;
+  return RAFIKI_OK;
+}
+
+// One scheduled batch through the selected models, then the mean (vote = false) or
+// majority-vote (vote = true) combine into out / out_labels.
+static int serve(rafiki_ensemble_t h, const void* batch, int n, uint32_t model_subset_mask, float* out,
+                 int32_t* out_labels, void* stream, bool vote) {
+  int rc = check_call(h, batch, n);
+  if (rc) return rc;
+  if (!out || !out_labels) return fail(RAFIKI_ERR_INVALID, "null output pointer");
+  if (model_subset_mask == 0) return fail(RAFIKI_ERR_INVALID, "model_subset_mask must select at least one model");
+  if (h->n_models < 32 && (model_subset_mask >> h->n_models) != 0)
+    return fail(RAFIKI_ERR_INVALID, "model_subset_mask selects a model that does not exist");
+  hipStream_t s = (hipStream_t)stream;
+  CombineArgs ca{};
+  ca.logits = h->d_logits;
+  ca.ld_model = (long long)h->max_batch * h->n_classes;
+  ca.n = n; ca.C = h->n_classes; ca.probs = out; ca.labels = out_labels;
+  for (int m = 0; m < h->n_models; ++m)
+    if ((model_subset_mask >> m) & 1u) ca.sel[ca.S++] = m;
+  // With graphs on, a graph replays the forward passes once this batch size is tuned;
+  // tracing, and a batch size seen for the first time, run them eagerly.
+  const bool graph = h->use_graphs && !h->trace.on && h->tuned.count(n);
+  if (graph) {
+    const void* in = h->input_kind == RAFIKI_INPUT_IMAGE_NCHW_F32 ? h->d_staged : h->d_tokens;
+    rc = stage(h, batch, n, s, h->d_staged);
+    if (rc) return rc;
+    if (h->input_kind == RAFIKI_INPUT_TOKENS_I32)
+      HIPCHK(hipMemcpyAsync(h->d_tokens, batch, (size_t)n * h->H * 4, hipMemcpyDeviceToDevice, s));
+    hipGraphExec_t exec = nullptr;
+    rc = graph_for(h, n, model_subset_mask, ca, in, &exec);
+    if (rc) return rc;
+    if (exec) {
+      HIPCHK(hipGraphLaunch(exec, s));
+      ++h->graph_replays;
+    } else {
+      rc = forward(h, ca, in, n, s);   // capture refused: the same launches, eagerly
+      if (rc) return rc;
+    }
+  } else {
+    const void* in = model_input(h, batch, h->d_staged);
+    rc = stage(h, batch, n, s, h->d_staged);
+    if (!rc) rc = tune(h, n, in, s);
+    if (!rc) rc = forward(h, ca, in, n, s);
+    if (rc) return rc;
   }
   const double cbytes = (double)n * h->n_classes * 4.0 * (ca.S + 1) + 4.0 * n;
   if (vote) {
@@ -1030,7 +1127,27 @@ int rafiki_tile_config(int cfg, int* bm, int* bn, int* waves, int* stages, int* 
 int rafiki_ensemble_force_tile(rafiki_ensemble_t h, int cfg) {
   if (!h) return fail(RAFIKI_ERR_INVALID, "null handle");
   if (cfg < -1 || cfg >= kNumMfmaConfigs) return fail(RAFIKI_ERR_INVALID, "no such tile configuration");
+  if (cfg != h->force_tile) {
+    HIPCHK(hipDeviceSynchronize());   // graphs holding the old tiles may still be running
+    h->drop_graphs();
+  }
   h->force_tile = cfg;
+  return RAFIKI_OK;
+}
+
+int rafiki_ensemble_use_graphs(rafiki_ensemble_t h, int enable) {
+  if (!h) return fail(RAFIKI_ERR_INVALID, "null handle");
+  HIPCHK(hipDeviceSynchronize());
+  h->drop_graphs();
+  h->use_graphs = enable != 0;
+  return RAFIKI_OK;
+}
+
+int rafiki_ensemble_graph_stats(rafiki_ensemble_t h, int* n_graphs, long long* replays, long long* failures) {
+  if (!h) return fail(RAFIKI_ERR_INVALID, "null handle");
+  if (n_graphs) *n_graphs = (int)h->graphs.size();
+  if (replays) *replays = h->graph_replays;
+  if (failures) *failures = h->graph_failures;
   return RAFIKI_OK;
 }
 
