@@ -404,10 +404,26 @@ def sweep_main(args, dev):
                 "value": round(n / (p50 / 1e3), 2), "unit": "images/s", "n_gpus": 1, "higher_is_better": True,
                 "dtype": "bf16", "data": "synthetic (seeded N(0,1) images rounded to bf16, random-init weights)",
                 "config": {"workload": "+".join(names[m] for m in range(3) if (mask >> m) & 1)
-                           + f", batch {n} of 3x224x224", "mask": mask, "global_batch": n},
+                           + f", batch {n} of 3x224x224", "mask": mask, "global_batch": n,
+                           "schedule": schedule_desc(ens, n, mask, names)},
                 "p50_ms": round(p50, 4), "p99_ms": round(float(np.percentile(lat, 99)), 4),
                 "calls": int(lat.size)}), flush=True)
     ens.close()
+
+
+def schedule_desc(ens, n, mask, names):
+    """How the selected models' forward passes were scheduled for (n, mask)."""
+    members = [m for m in range(len(names)) if (mask >> m) & 1]
+    if len(members) == 1:
+        return names[members[0]]
+    try:
+        solo = ens.get_schedule(n, mask)
+    except Exception:
+        solo = -1
+    if solo < 0:
+        return "all concurrent"
+    rest = [names[m] for m in members if m != solo]
+    return f"{names[solo]} alone; {' then '.join(rest)} on a second lane (longest first)"
 
 
 def main():
@@ -577,7 +593,8 @@ def main():
         "dtype": "bf16" if precision == "bf16" else "f32",
         "data": "synthetic (seeded inputs and random-init weights of the named architectures)",
         "config": {"workload": desc, "global_batch": n, "mask": mask, "n_classes": C, "combine": args.combine,
-                   "input": "int32 tokens [n, 256]" if tokens else "float32 NCHW images"},
+                   "input": "int32 tokens [n, 256]" if tokens else "float32 NCHW images",
+                   "schedule": schedule_desc(ens, n, mask, [f"{sp.name}#{i}" for i, sp in enumerate(specs)])},
         "p50_ms": round(float(np.percentile(lat, 50)), 4),
         "p99_ms": round(float(np.percentile(lat, 99)), 4),
         "host_enqueue_ms": round(float(np.median(host)), 4),

@@ -234,6 +234,21 @@ int rafiki_tile_config(int cfg, int* bm, int* bn, int* waves, int* stages, int* 
  * are unchanged; only speed differs. */
 int rafiki_ensemble_force_tile(rafiki_ensemble_t h, int cfg);
 
+/* Schedule of the selected models' forward passes for one (n, model_subset_mask).
+ * The models are independent until the combine and run on their own streams.  With
+ * three or more selected models, the first infer / infer_vote of a (n, mask) pair times
+ * each candidate schedule on `stream` (best of three runs each; it blocks the caller
+ * once) and keeps the fastest: solo = -1, all models concurrently; solo = m, model m
+ * alone on one lane while the other selected models run one after another (longest
+ * alone time first) on a second lane.  A schedule only orders the same launches, so it
+ * never changes a result.  Environment RAFIKI_SCHEDULE_TUNING=0 at create skips the
+ * timing (solo = -1 unless set).
+ * get_schedule: the kept choice; RAFIKI_ERR_INVALID if none has been chosen yet.
+ * set_schedule: sets it (solo = -1 or a model of the subset); synchronises the device
+ * and drops any kept graphs. */
+int rafiki_ensemble_get_schedule(rafiki_ensemble_t h, int n, uint32_t model_subset_mask, int* solo);
+int rafiki_ensemble_set_schedule(rafiki_ensemble_t h, int n, uint32_t model_subset_mask, int solo);
+
 /* Graph replay of the forward passes (off by default; environment RAFIKI_GRAPHS=1 turns
  * it on at create).  Measured on MI355X it is no faster than the eager launches for one
  * model and slower for several, whose branches the replay did not overlap as well as

@@ -22,7 +22,8 @@ RAFIKI_INPUT_IMAGE_NCHW_F32, RAFIKI_INPUT_TOKENS_I32 = 0, 1
 EXPORTED = ("rafiki_ensemble_create", "rafiki_ensemble_infer", "rafiki_ensemble_infer_vote",
             "rafiki_ensemble_model_logits",
             "rafiki_ensemble_info", "rafiki_ensemble_trace", "rafiki_ensemble_trace_read",
-            "rafiki_tile_config", "rafiki_ensemble_force_tile", "rafiki_ensemble_use_graphs",
+            "rafiki_tile_config", "rafiki_ensemble_force_tile", "rafiki_ensemble_get_schedule",
+            "rafiki_ensemble_set_schedule", "rafiki_ensemble_use_graphs",
             "rafiki_ensemble_graph_stats", "rafiki_combine_mean", "rafiki_combine_vote",
             "rafiki_maxpool_nhwc_bf16", "rafiki_global_avgpool_nhwc_bf16",
             "rafiki_ensemble_destroy", "rafiki_greedy_decide", "rafiki_greedy_simulate", "rafiki_greedy_simulate_multi",
@@ -105,6 +106,8 @@ def load_library(path: str = LIB_PATH):
     lib.rafiki_ensemble_trace_read.argtypes = [C.c_void_p, C.POINTER(RafikiTraceRec), C.c_int, C.POINTER(C.c_int)]
     lib.rafiki_tile_config.argtypes = [C.c_int] + [C.POINTER(C.c_int)] * 5
     lib.rafiki_ensemble_force_tile.argtypes = [C.c_void_p, C.c_int]
+    lib.rafiki_ensemble_get_schedule.argtypes = [C.c_void_p, C.c_int, C.c_uint32, C.POINTER(C.c_int)]
+    lib.rafiki_ensemble_set_schedule.argtypes = [C.c_void_p, C.c_int, C.c_uint32, C.c_int]
     lib.rafiki_ensemble_use_graphs.argtypes = [C.c_void_p, C.c_int]
     lib.rafiki_ensemble_graph_stats.argtypes = [C.c_void_p, C.POINTER(C.c_int), C.POINTER(C.c_longlong),
                                                 C.POINTER(C.c_longlong)]
@@ -526,6 +529,15 @@ class Ensemble:
     def force_tile(self, cfg: int):
         """Use tile configuration ``cfg`` for every unsplit bf16 GEMM it suits (-1: tuned)."""
         _check(self._lib.rafiki_ensemble_force_tile(self._h, cfg))
+
+    def get_schedule(self, n: int, mask: int) -> int:
+        """Schedule kept for (n, mask): -1 all models concurrent, m model m alone on one lane."""
+        v = C.c_int(0)
+        _check(self._lib.rafiki_ensemble_get_schedule(self._h, n, mask, C.byref(v)))
+        return v.value
+
+    def set_schedule(self, n: int, mask: int, solo: int):
+        _check(self._lib.rafiki_ensemble_set_schedule(self._h, n, mask, solo))
 
     def use_graphs(self, enable: bool):
         """Turn graph replay of the forward passes on or off (drops every kept graph)."""

@@ -158,6 +158,14 @@ struct rafiki_ensemble_s {
   std::vector<void*> allocs;
   // Tuned tile configuration per batch size, model and op (-1: not a GEMM op).
   std::map<int, std::vector<std::vector<int>>> tuned;
+  // Per batch size: each model's forward time alone, estimated when tuning (sum of the
+  // chosen tiles' times; GEMM FLOPs / 1e12 when tiles are not timed).
+  std::map<int, std::vector<double>> model_ms;
+  // Per (batch size, subset): the schedule of the selected models' forward passes
+  // chosen by timing (-1: all concurrent; m: model m alone on one lane, the others
+  // one after another on a second lane).
+  std::map<std::pair<int, uint32_t>, int> schedule;
+  bool tune_schedule = true;
   bool autotune = true;
   int force_tile = -1;              // diagnostic override of the tuned configuration
   // Forward passes replayed as HIP graphs, one per (batch size, model subset): every
@@ -618,6 +626,7 @@ ConvArgs gemm_args(const rafiki_ensemble_s* e, const Model& M, const Op& op, int
 int tune(rafiki_ensemble_s* e, int n, const void* in, hipStream_t s) {
   if (e->tuned.count(n)) return RAFIKI_OK;
   std::vector<std::vector<int>> choice(e->models.size());
+  std::vector<double> est(e->models.size(), 0.0);
   hipEvent_t ev[2] = {nullptr, nullptr};
   const bool timing = e->autotune && e->precision == RAFIKI_BF16;
   if (timing) {
@@ -632,7 +641,10 @@ int tune(rafiki_ensemble_s* e, int n, const void* in, hipStream_t s) {
       const Op& op = M.ops[oi];
       if (op.kind != O_CONV && op.kind != O_CONV1D) continue;
       choice[mi][oi] = default_cfg(op.c_out);
-      if (!timing) continue;
+      if (!timing) {
+        est[mi] += 2.0 * n * op.Ho * op.Wo * (double)op.c_out * op.K / 1e12;
+        continue;
+      }
       ConvArgs a = gemm_args(e, M, op, n, in);
       // Split-K launches keep the split of K that the shape fixes (so the sums do not
       // depend on the tile either); only their tile is tuned.
@@ -675,12 +687,14 @@ int tune(rafiki_ensemble_s* e, int n, const void* in, hipStream_t s) {
         if (t < best) { best = t; choice[mi][oi] = cfg; }
       }
       if (rc) break;
+      est[mi] += best;
     }
   }
   if (ev[0]) (void)hipEventDestroy(ev[0]);
   if (ev[1]) (void)hipEventDestroy(ev[1]);
   if (rc) return rc;
   e->tuned[n] = std::move(choice);
+  e->model_ms[n] = std::move(est);
   return RAFIKI_OK;
 }
 
@@ -809,6 +823,7 @@ int rafiki_ensemble_create(const rafiki_model_desc* models, int n_models, const 
   if (const char* t = std::getenv("RAFIKI_AUTOTUNE")) e->autotune = std::atoi(t) != 0;
   if (const char* t = std::getenv("RAFIKI_MODEL_STREAMS")) e->concurrent = std::atoi(t) != 0;
   if (const char* t = std::getenv("RAFIKI_GRAPHS")) e->use_graphs = std::atoi(t) != 0;
+  if (const char* t = std::getenv("RAFIKI_SCHEDULE_TUNING")) e->tune_schedule = std::atoi(t) != 0;
   // Pass 1: validate every model and infer shapes without touching the device.
   e->dry = true;
   e->models.resize(n_models);
@@ -839,7 +854,8 @@ int rafiki_ensemble_create(const rafiki_model_desc* models, int n_models, const 
   }
   rc = dev_alloc(e.get(), (void**)&e->d_logits, (size_t)n_models * e->max_batch * n_classes * 4);
   if (rc) return rc;
-  for (Model& M : e->models) {
+  for (int mi = 0; mi < n_models; ++mi) {
+    Model& M = e->models[mi];
     M.partial_bytes = partial_need(e.get(), M);
     if (M.partial_bytes) {
       rc = dev_alloc(e.get(), (void**)&M.d_partial, M.partial_bytes);
@@ -872,29 +888,48 @@ int rafiki_ensemble_create(const rafiki_model_desc* models, int n_models, const 
 // itself).  Forked launches are enqueued interleaved, one op of each model in turn, so
 // that every model stream has work from the start even when enqueueing is slower than
 // the device.
-static int forward(rafiki_ensemble_t h, const CombineArgs& ca, const void* in, int n, hipStream_t s) {
+static int forward(rafiki_ensemble_t h, const CombineArgs& ca, const void* in, int n, hipStream_t s, int solo) {
   int rc = RAFIKI_OK;
   const bool fork = h->concurrent && !h->trace.on && ca.S > 1;
   if (fork) {
     HIPCHK(hipEventRecord(h->staged_ev, s));
+    // Lanes.  solo < 0: every model on its own lane.  solo = m: model m alone on one
+    // lane, the other selected models one after another on a second lane, longest
+    // (estimated alone) first; each waits for the previous one's done event.
+    std::vector<int> prev(h->n_models, -1);        // model this one waits for (-1: staging)
+    if (solo >= 0) {
+      std::vector<double> est(h->n_models, 1.0);
+      const auto it = h->model_ms.find(n);
+      if (it != h->model_ms.end()) est = it->second;
+      std::vector<int> rest;
+      for (int i = 0; i < ca.S; ++i)
+        if (ca.sel[i] != solo) rest.push_back(ca.sel[i]);
+      std::stable_sort(rest.begin(), rest.end(), [&](int a, int b) { return est[a] > est[b]; });
+      for (size_t k = 1; k < rest.size(); ++k) prev[rest[k]] = rest[k - 1];
+    }
+    // enqueue offsets: a model's launches are enqueued after its predecessor's last one
+    std::vector<size_t> off(h->n_models, 0);
+    for (int i = 0; i < ca.S; ++i)           // a chain's predecessors come first in it
+      for (int m = ca.sel[i]; prev[m] >= 0; m = prev[m]) off[ca.sel[i]] += h->models[prev[m]].ops.size();
     size_t rounds = 0;
     for (int i = 0; i < ca.S; ++i) {
-      HIPCHK(hipStreamWaitEvent(h->models[ca.sel[i]].stream, h->staged_ev, 0));
-      rounds = std::max(rounds, h->models[ca.sel[i]].ops.size());
+      const int m = ca.sel[i];
+      if (prev[m] < 0) HIPCHK(hipStreamWaitEvent(h->models[m].stream, h->staged_ev, 0));
+      rounds = std::max(rounds, h->models[m].ops.size() + off[m]);
     }
-    for (size_t oi = 0; oi < rounds; ++oi)
+    for (size_t r = 0; r < rounds; ++r)
       for (int i = 0; i < ca.S; ++i) {
         const int m = ca.sel[i];
         Model& M = h->models[m];
+        if (r < off[m]) continue;
+        const size_t oi = r - off[m];
         if (oi >= M.ops.size()) continue;
+        if (oi == 0 && prev[m] >= 0) HIPCHK(hipStreamWaitEvent(M.stream, h->models[prev[m]].done, 0));
         rc = run_model(h, m, in, n, h->d_logits + (size_t)m * ca.ld_model, M.stream, oi, oi + 1);
         if (rc) return rc;
+        if (oi + 1 == M.ops.size()) HIPCHK(hipEventRecord(M.done, M.stream));
       }
-    for (int i = 0; i < ca.S; ++i) {
-      Model& M = h->models[ca.sel[i]];
-      HIPCHK(hipEventRecord(M.done, M.stream));
-      HIPCHK(hipStreamWaitEvent(s, M.done, 0));
-    }
+    for (int i = 0; i < ca.S; ++i) HIPCHK(hipStreamWaitEvent(s, h->models[ca.sel[i]].done, 0));
   } else {
     for (int i = 0; i < ca.S; ++i) {
       const int m = ca.sel[i];
@@ -905,12 +940,60 @@ static int forward(rafiki_ensemble_t h, const CombineArgs& ca, const void* in, i
   return RAFIKI_OK;
 }
 
+// The schedule of (n, mask): chosen on first use by timing every candidate on stream s
+// (blocks the caller once).  Candidates: all models concurrent, and each selected model
+// alone on one lane with the others chained on a second.  A schedule only orders the
+// same launches, so the choice never changes a result.  With fewer than three models,
+// when tracing, or with model streams off, the models run as before (solo = -1).
+static int pick_schedule(rafiki_ensemble_t h, const CombineArgs& ca, const void* in, int n, uint32_t mask,
+                         hipStream_t s, int* solo) {
+  *solo = -1;
+  if (ca.S < 3 || !h->concurrent || h->trace.on) return RAFIKI_OK;
+  const auto key = std::make_pair(n, mask);
+  const auto it = h->schedule.find(key);
+  if (it != h->schedule.end()) {
+    *solo = it->second;
+    return RAFIKI_OK;
+  }
+  if (!h->tune_schedule) return RAFIKI_OK;
+  hipEvent_t ev[2] = {nullptr, nullptr};
+  HIPCHK(hipEventCreate(&ev[0]));
+  hipError_t st = hipEventCreate(&ev[1]);
+  if (st != hipSuccess) {
+    (void)hipEventDestroy(ev[0]);
+    return fail(RAFIKI_ERR_HIP, std::string("hipEventCreate: ") + hipGetErrorString(st));
+  }
+  int rc = RAFIKI_OK, best_solo = -1;
+  float best = 1e30f;
+  for (int c = -1; c < ca.S && rc == RAFIKI_OK; ++c) {
+    const int cand = c < 0 ? -1 : ca.sel[c];
+    float t = 1e30f;
+    for (int rep = 0; rep < 3 && rc == RAFIKI_OK; ++rep) {   // best of three
+      st = hipEventRecord(ev[0], s);
+      if (st == hipSuccess) rc = forward(h, ca, in, n, s, cand);
+      if (st == hipSuccess && rc == RAFIKI_OK) st = hipEventRecord(ev[1], s);
+      if (st == hipSuccess && rc == RAFIKI_OK) st = hipEventSynchronize(ev[1]);
+      float ms = 0.f;
+      if (st == hipSuccess && rc == RAFIKI_OK) st = hipEventElapsedTime(&ms, ev[0], ev[1]);
+      if (st != hipSuccess && rc == RAFIKI_OK) rc = fail(RAFIKI_ERR_HIP, std::string("schedule timing: ") + hipGetErrorString(st));
+      if (rc == RAFIKI_OK) t = std::min(t, ms);
+    }
+    if (rc == RAFIKI_OK && t < best) { best = t; best_solo = cand; }
+  }
+  (void)hipEventDestroy(ev[0]);
+  (void)hipEventDestroy(ev[1]);
+  if (rc) return rc;
+  h->schedule[key] = best_solo;
+  *solo = best_solo;
+  return RAFIKI_OK;
+}
+
 constexpr size_t kMaxGraphs = 64;   // (batch size, subset) pairs kept as graphs per handle
 
 // The instantiated graph of the forward passes for (n, mask), captured on first use.
 // *exec stays null when the cache is full or the capture fails; the caller then runs
 // the same launches eagerly (a failed capture is counted and disables graphs).
-static int graph_for(rafiki_ensemble_t h, int n, uint32_t mask, const CombineArgs& ca, const void* in,
+static int graph_for(rafiki_ensemble_t h, int n, uint32_t mask, const CombineArgs& ca, const void* in, int solo,
                      hipGraphExec_t* exec) {
   *exec = nullptr;
   const auto key = std::make_pair(n, mask);
@@ -927,7 +1010,7 @@ static int graph_for(rafiki_ensemble_t h, int n, uint32_t mask, const CombineArg
     h->use_graphs = false;
     return RAFIKI_OK;
   }
-  const int frc = forward(h, ca, in, n, cs);
+  const int frc = forward(h, ca, in, n, cs, solo);
   hipGraph_t g = nullptr;
   const hipError_t est = hipStreamEndCapture(cs, &g);
   hipGraphExec_t x = nullptr;
@@ -972,20 +1055,25 @@ static int serve(rafiki_ensemble_t h, const void* batch, int n, uint32_t model_s
     if (h->input_kind == RAFIKI_INPUT_TOKENS_I32)
       HIPCHK(hipMemcpyAsync(h->d_tokens, batch, (size_t)n * h->H * 4, hipMemcpyDeviceToDevice, s));
     hipGraphExec_t exec = nullptr;
-    rc = graph_for(h, n, model_subset_mask, ca, in, &exec);
+    int solo = -1;
+    rc = pick_schedule(h, ca, in, n, model_subset_mask, s, &solo);
+    if (rc) return rc;
+    rc = graph_for(h, n, model_subset_mask, ca, in, solo, &exec);
     if (rc) return rc;
     if (exec) {
       HIPCHK(hipGraphLaunch(exec, s));
       ++h->graph_replays;
     } else {
-      rc = forward(h, ca, in, n, s);   // capture refused: the same launches, eagerly
+      rc = forward(h, ca, in, n, s, solo);   // capture refused: the same launches, eagerly
       if (rc) return rc;
     }
   } else {
     const void* in = model_input(h, batch, h->d_staged);
     rc = stage(h, batch, n, s, h->d_staged);
     if (!rc) rc = tune(h, n, in, s);
-    if (!rc) rc = forward(h, ca, in, n, s);
+    int solo = -1;
+    if (!rc) rc = pick_schedule(h, ca, in, n, model_subset_mask, s, &solo);
+    if (!rc) rc = forward(h, ca, in, n, s, solo);
     if (rc) return rc;
   }
   const double cbytes = (double)n * h->n_classes * 4.0 * (ca.S + 1) + 4.0 * n;
@@ -1132,6 +1220,26 @@ int rafiki_ensemble_force_tile(rafiki_ensemble_t h, int cfg) {
     h->drop_graphs();
   }
   h->force_tile = cfg;
+  return RAFIKI_OK;
+}
+
+int rafiki_ensemble_get_schedule(rafiki_ensemble_t h, int n, uint32_t mask, int* solo) {
+  if (!h || !solo) return fail(RAFIKI_ERR_INVALID, "null argument");
+  const auto it = h->schedule.find(std::make_pair(n, mask));
+  if (it == h->schedule.end()) return fail(RAFIKI_ERR_INVALID, "no schedule chosen for this batch size and subset");
+  *solo = it->second;
+  return RAFIKI_OK;
+}
+
+int rafiki_ensemble_set_schedule(rafiki_ensemble_t h, int n, uint32_t mask, int solo) {
+  if (!h) return fail(RAFIKI_ERR_INVALID, "null handle");
+  if (n < 1 || n > h->max_batch || mask == 0 || (h->n_models < 32 && (mask >> h->n_models) != 0))
+    return fail(RAFIKI_ERR_INVALID, "batch size or subset mask out of range");
+  if (solo < -1 || solo >= h->n_models || (solo >= 0 && !((mask >> solo) & 1u)))
+    return fail(RAFIKI_ERR_INVALID, "solo must be -1 or a model of the subset");
+  HIPCHK(hipDeviceSynchronize());   // graphs built with the old schedule may still run
+  h->drop_graphs();
+  h->schedule[std::make_pair(n, mask)] = solo;
   return RAFIKI_OK;
 }
 
