@@ -423,7 +423,7 @@ def schedule_desc(ens, n, mask, names):
     if solo < 0:
         return "all concurrent"
     rest = [names[m] for m in members if m != solo]
-    return f"{names[solo]} alone; {' then '.join(rest)} on a second lane (longest first)"
+    return f"{names[solo]} alone; {', '.join(rest)} one after another on a second lane, longest alone time first"
 
 
 def main():
