@@ -302,9 +302,10 @@ def memory_main(args, dev):
     """Standalone memory-bound kernels: the combine at |S| = 3, C = 1000 on a scaled
     batch of 262,144 rows (the batch-64 combine moves about 1 MB, below launch latency),
     the ResNet stem max-pool and the VGG-16 first max-pool at batch 64, and the global
-    average pool of ResNet's last stage (batch 64 and a scaled batch of 512).  Best of
-    10 timed calls after 3 warm-up calls; algorithmic bytes = every input and output
-    once."""
+    average pool of ResNet's last stage (batch 64 and a scaled batch of 512).  Each
+    timing brackets enough back-to-back calls to last about a millisecond (so short
+    kernels are not dominated by the events around them); best of 10 timings after 3
+    warm-up calls; algorithmic bytes = every input and output once."""
     import torch
 
     from paper_1804_06087_amd.binding import (combine_mean, combine_vote, maxpool_nhwc_bf16,
@@ -314,14 +315,20 @@ def memory_main(args, dev):
         for _ in range(3):
             fn()
         torch.cuda.synchronize()
+        reps = 1
         best = 1e30
-        for _ in range(10):
+        for i in range(11):
             a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             a.record()
-            fn()
+            for _ in range(reps):
+                fn()
             b.record()
             b.synchronize()
-            best = min(best, a.elapsed_time(b))
+            ms = a.elapsed_time(b) / reps
+            if i == 0:      # sizing run
+                reps = max(1, min(200, int(1.0 / max(ms, 1e-3))))
+                continue
+            best = min(best, ms)
         return best
 
     def emit(name, shape, nbytes, ms):
