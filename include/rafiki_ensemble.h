@@ -180,6 +180,9 @@ typedef struct {
   float ms;                     /* kernel execution time: elapsed time between the HIP
                                    events the launch records at the kernel's start and end
                                    (hipExtLaunchKernelGGL start/stop events) */
+  int tile_cfg;                 /* bf16 GEMM launches (conv_mfma, splitk_reduce): the tile
+                                   configuration used (rafiki_tile_config); -1 otherwise */
+  int splits;                   /* the same launches: K splits (1 = unsplit); 0 otherwise */
 } rafiki_trace_rec;
 
 /* Enable (1) or disable (0) per-launch event timing of subsequent infer / model_logits

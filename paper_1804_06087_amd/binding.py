@@ -73,7 +73,7 @@ class RafikiOpts(C.Structure):
 
 class RafikiTraceRec(C.Structure):
     _fields_ = [("kind", C.c_int), ("model", C.c_int), ("layer", C.c_int), ("flops", C.c_double),
-                ("bytes", C.c_double), ("ms", C.c_float)]
+                ("bytes", C.c_double), ("ms", C.c_float), ("tile_cfg", C.c_int), ("splits", C.c_int)]
 
 
 class RafikiError(RuntimeError):
@@ -550,13 +550,14 @@ class Ensemble:
         return g.value, r.value, f.value
 
     def trace_read(self):
-        """List of dicts {kind, model, layer, flops, bytes, ms} for the traced launches."""
+        """List of dicts {kind, model, layer, flops, bytes, ms, tile_cfg, splits} for the traced launches."""
         cnt = C.c_int(0)
         _check(self._lib.rafiki_ensemble_trace_read(self._h, None, 0, C.byref(cnt)))
         buf = (RafikiTraceRec * max(cnt.value, 1))()
         _check(self._lib.rafiki_ensemble_trace_read(self._h, buf, cnt.value, C.byref(cnt)))
         return [{"kind": KERNEL_CLASSES[r.kind], "model": r.model, "layer": r.layer, "flops": r.flops,
-                 "bytes": r.bytes, "ms": r.ms} for r in buf[:cnt.value]]
+                 "bytes": r.bytes, "ms": r.ms, "tile_cfg": r.tile_cfg, "splits": r.splits}
+                for r in buf[:cnt.value]]
 
     def close(self):
         if getattr(self, "_h", None) is not None and self._h.value:

@@ -127,7 +127,7 @@ struct FreeList {
 // kernel, resolved by rafiki_ensemble_trace_read.
 struct Tracer {
   bool on = false;
-  struct Rec { int kind, model, layer; double flops, bytes; hipEvent_t a, b; };
+  struct Rec { int kind, model, layer; double flops, bytes; hipEvent_t a, b; int tile_cfg, splits; };
   std::vector<Rec> recs;
   std::vector<hipEvent_t> pool;
   size_t used = 0;
@@ -555,6 +555,13 @@ const void* tptr(const rafiki_ensemble_s* e, const Model& M, int id, const void*
 // Launch `expr` (one kernel launch) on stream s; when tracing, the launch itself records
 // a pair of events at the kernel's start and end, and the launch's algorithmic FLOPs
 // and bytes are kept with them.
+// Tile configuration and split count of the GEMM launch being traced (-1 / 0 otherwise).
+struct TraceTile { int cfg = -1, splits = 0; };
+TraceTile& trace_tile() {
+  thread_local TraceTile t;
+  return t;
+}
+
 #define TRACED(e, s, kind, model, layer, flops, bytes, expr)                                  \
   do {                                                                                        \
     hipEvent_t ta_ = nullptr, tb_ = nullptr;                                                  \
@@ -567,7 +574,8 @@ const void* tptr(const rafiki_ensemble_s* e, const Model& M, int id, const void*
     launch_events() = {};                                                                     \
     HIPCHK(lst_);                                                                             \
     if (ta_ && tb_)                                                                           \
-      (e)->trace.recs.push_back({kind, model, layer, (double)(flops), (double)(bytes), ta_, tb_}); \
+      (e)->trace.recs.push_back({kind, model, layer, (double)(flops), (double)(bytes), ta_, tb_,     \
+                                 trace_tile().cfg, trace_tile().splits});                           \
   } while (0)
 
 int run_gemm(const rafiki_ensemble_s* e, const Op& op, ConvArgs a, hipStream_t s, int mi, int li, int cfg) {
@@ -588,6 +596,10 @@ int run_gemm(const rafiki_ensemble_s* e, const Op& op, ConvArgs a, hipStream_t s
   const int splits = choose_splits(a.M, op.c_out, ktiles);
   if (cfg < 0) cfg = splits > 1 ? split_cfg(op.c_out) : default_cfg(op.c_out);
   a.kt_per_split = (ktiles + splits - 1) / splits;
+  struct TileScope {
+    TileScope(int c, int sp) { trace_tile() = {c, sp}; }
+    ~TileScope() { trace_tile() = {}; }
+  } tile_scope(cfg, splits);
   if (splits > 1) {
     const Model& Mo = e->models[mi];
     if ((size_t)splits * a.M * a.Co_pad * 4 > Mo.partial_bytes)
@@ -1149,6 +1161,7 @@ int rafiki_ensemble_trace_read(rafiki_ensemble_t h, rafiki_trace_rec* out, int c
     if (st != hipSuccess) return fail(RAFIKI_ERR_HIP, std::string("hipEventElapsedTime: ") + hipGetErrorString(st));
     out[i].kind = r.kind; out[i].model = r.model; out[i].layer = r.layer;
     out[i].flops = r.flops; out[i].bytes = r.bytes; out[i].ms = ms;
+    out[i].tile_cfg = r.tile_cfg; out[i].splits = r.splits;
   }
   h->trace.recs.clear();
   h->trace.used = 0;
