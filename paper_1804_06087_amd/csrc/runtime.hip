@@ -555,6 +555,30 @@ const void* tptr(const rafiki_ensemble_s* e, const Model& M, int id, const void*
 // Launch `expr` (one kernel launch) on stream s; when tracing, the launch itself records
 // a pair of events at the kernel's start and end, and the launch's algorithmic FLOPs
 // and bytes are kept with them.
+// Tile tuning inside forward passes: while a probe is installed on this thread, every
+// conv_mfma launch records a pair of dispatch events (its layer and tile with them).
+struct TuneProbe {
+  struct Rec { int layer, cfg; hipEvent_t a, b; };
+  std::vector<Rec> recs;
+  std::vector<hipEvent_t> pool;
+  size_t used = 0;
+  hipEvent_t next() {
+    if (used == pool.size()) {
+      hipEvent_t ev = nullptr;
+      if (hipEventCreate(&ev) != hipSuccess) return nullptr;
+      pool.push_back(ev);
+    }
+    return pool[used++];
+  }
+  ~TuneProbe() {
+    for (hipEvent_t ev : pool) (void)hipEventDestroy(ev);
+  }
+};
+TuneProbe*& tune_probe() {
+  thread_local TuneProbe* p = nullptr;
+  return p;
+}
+
 // Tile configuration and split count of the GEMM launch being traced (-1 / 0 otherwise).
 struct TraceTile { int cfg = -1, splits = 0; };
 TraceTile& trace_tile() {
@@ -564,15 +588,20 @@ TraceTile& trace_tile() {
 
 #define TRACED(e, s, kind, model, layer, flops, bytes, expr)                                  \
   do {                                                                                        \
-    hipEvent_t ta_ = nullptr, tb_ = nullptr;                                                  \
+    hipEvent_t ta_ = nullptr, tb_ = nullptr, pa_ = nullptr, pb_ = nullptr;                    \
     if ((e)->trace.on) {                                                                      \
       ta_ = (e)->trace.next();                                                                \
       tb_ = (e)->trace.next();                                                                \
       if (ta_ && tb_) launch_events() = {ta_, tb_};                                           \
+    } else if ((kind) == RAFIKI_K_CONV_MFMA && tune_probe()) {                                \
+      pa_ = tune_probe()->next();                                                             \
+      pb_ = tune_probe()->next();                                                             \
+      if (pa_ && pb_) launch_events() = {pa_, pb_};                                           \
     }                                                                                         \
     const hipError_t lst_ = (expr);                                                           \
     launch_events() = {};                                                                     \
     HIPCHK(lst_);                                                                             \
+    if (pa_ && pb_) tune_probe()->recs.push_back({(layer), trace_tile().cfg, pa_, pb_});      \
     if (ta_ && tb_)                                                                           \
       (e)->trace.recs.push_back({kind, model, layer, (double)(flops), (double)(bytes), ta_, tb_,     \
                                  trace_tile().cfg, trace_tile().splits});                           \
@@ -632,79 +661,105 @@ ConvArgs gemm_args(const rafiki_ensemble_s* e, const Model& M, const Op& op, int
   return a;
 }
 
-// Choose each GEMM op's tile configuration for batch size n by timing the candidates
-// on stream s (once per n; blocks the caller).  Only unsplit launches are tuned: all
-// of them sum K in the same order, so the choice never changes a result.
+int run_model(const rafiki_ensemble_s* e, int mi, const void* in, int n, float* logits, hipStream_t s,
+              size_t op_begin = 0, size_t op_end = SIZE_MAX);
+
+// Choose each GEMM op's tile configuration for batch size n (once per n; blocks the
+// caller).  The candidates are timed where they will run: inside forward passes of
+// the model on stream s, one model at a time.  Pass j gives every GEMM op its j-th
+// candidate; each launch records dispatch events; two rounds of passes, and each op
+// keeps the candidate with the shortest launch.  Timed this way a layer reads weights
+// that are not in cache and an input the previous layer has just written, as in
+// serving (timing a candidate by repeating it alone kept the weights in L2 and chose
+// shallow pipelines that are slower in the pass).  All candidates sum K in the same
+// order, and a split-K launch keeps the split that the shape fixes (only its tile is
+// tuned), so the choice never changes a result.
 int tune(rafiki_ensemble_s* e, int n, const void* in, hipStream_t s) {
   if (e->tuned.count(n)) return RAFIKI_OK;
-  std::vector<std::vector<int>> choice(e->models.size());
-  std::vector<double> est(e->models.size(), 0.0);
-  hipEvent_t ev[2] = {nullptr, nullptr};
+  const size_t NM = e->models.size();
+  std::vector<std::vector<int>> choice(NM);
+  std::vector<std::vector<std::vector<int>>> cand(NM);
+  std::vector<double> est(NM, 0.0);
   const bool timing = e->autotune && e->precision == RAFIKI_BF16;
-  if (timing) {
-    HIPCHK(hipEventCreate(&ev[0]));
-    HIPCHK(hipEventCreate(&ev[1]));
-  }
-  int rc = RAFIKI_OK;
-  for (size_t mi = 0; mi < e->models.size() && rc == RAFIKI_OK; ++mi) {
+  for (size_t mi = 0; mi < NM; ++mi) {
     const Model& M = e->models[mi];
     choice[mi].assign(M.ops.size(), -1);
+    cand[mi].resize(M.ops.size());
     for (size_t oi = 0; oi < M.ops.size(); ++oi) {
       const Op& op = M.ops[oi];
       if (op.kind != O_CONV && op.kind != O_CONV1D) continue;
-      choice[mi][oi] = default_cfg(op.c_out);
-      if (!timing) {
-        est[mi] += 2.0 * n * op.Ho * op.Wo * (double)op.c_out * op.K / 1e12;
-        continue;
-      }
-      ConvArgs a = gemm_args(e, M, op, n, in);
-      // Split-K launches keep the split of K that the shape fixes (so the sums do not
-      // depend on the tile either); only their tile is tuned.
-      const int splits = choose_splits(a.M, op.c_out, a.Kp / 64);
-      if (splits > 1) {
-        choice[mi][oi] = split_cfg(op.c_out);
-        a.partial = M.d_partial;
-      }
-      if ((long long)a.N * a.H * a.W * a.Cs * 2 >= (1LL << 31) || (long long)a.Co_pad * a.Kp * 2 >= (1LL << 31))
-        continue;   // run_gemm rejects these shapes
-      // scratch output: the op's own arena slot, or the model's logits slot
-      const Tensor& y = M.tensors[op.out];
-      a.y = y.is_logits ? (void*)(e->d_logits + mi * (size_t)e->max_batch * e->n_classes)
-                        : (void*)(op.kind == O_CONV1D ? M.d_arena + op.tmp_off : M.d_arena + y.off);
-      a.c_write = y.is_logits ? y.c : (op.kind == O_CONV1D ? round_up(op.c_out, 8) : y.Cs);
-      a.ldy = a.c_write;
-      a.out_f32 = y.is_logits ? 1 : 0;
-      a.kt_per_split = (a.Kp / 64 + splits - 1) / splits;
-      float best = 1e30f;
-      for (int cfg = 0; cfg < kNumMfmaConfigs; ++cfg) {
-        if (!cfg_fits(cfg, op.c_out)) continue;
-        if (kMfmaConfigs[cfg].bm > 2 * round_up(a.M, 32)) continue;
-        float t = 0.f;
-        for (int rep = 0; rep < 4; ++rep) {   // first launch warms caches; keep the best of three
-          launch_events() = {ev[0], ev[1]};
-          const hipError_t lst = launch_conv_mfma(a, cfg, splits, s);
-          launch_events() = {};
-          if (lst != hipSuccess || hipEventSynchronize(ev[1]) != hipSuccess) {
-            rc = fail(RAFIKI_ERR_HIP, "tile tuning launch failed");
-            break;
-          }
-          float ms = 0.f;
-          (void)hipEventElapsedTime(&ms, ev[0], ev[1]);
-          if (rep == 1 || (rep > 1 && ms < t)) t = ms;
-        }
-        if (rc) break;
-        // Fastest alone.  (Weighting the time by the share of compute units a launch
-        // occupies, to leave room for concurrently running models, made the concurrent
-        // ResNet-50 + VGG-16 + ResNet-101 step 12-20 % slower.)
-        if (t < best) { best = t; choice[mi][oi] = cfg; }
-      }
-      if (rc) break;
-      est[mi] += best;
+      const int M_rows = n * op.Ho * op.Wo;
+      const int splits = choose_splits(M_rows, op.c_out, op.Kp / 64);
+      choice[mi][oi] = splits > 1 ? split_cfg(op.c_out) : default_cfg(op.c_out);
+      est[mi] += 2.0 * n * op.Ho * op.Wo * (double)op.c_out * op.K / 1e12;
+      if (!timing) continue;
+      for (int cfg = 0; cfg < kNumMfmaConfigs; ++cfg)
+        if (cfg_fits(cfg, op.c_out) && kMfmaConfigs[cfg].bm <= 2 * round_up(M_rows, 32)) cand[mi][oi].push_back(cfg);
     }
   }
-  if (ev[0]) (void)hipEventDestroy(ev[0]);
-  if (ev[1]) (void)hipEventDestroy(ev[1]);
+  if (!timing) {
+    e->tuned[n] = std::move(choice);
+    e->model_ms[n] = std::move(est);
+    return RAFIKI_OK;
+  }
+  // best[mi][oi][cfg]: shortest launch seen.  A forced tile and the caller's tracing
+  // are suspended during the passes.
+  std::vector<std::vector<std::vector<float>>> best(NM);
+  TuneProbe probe;
+  int rc = RAFIKI_OK;
+  const int saved_force = e->force_tile;
+  const bool saved_trace = e->trace.on;
+  e->force_tile = -1;
+  e->trace.on = false;
+  for (size_t mi = 0; mi < NM && rc == RAFIKI_OK; ++mi) {
+    const Model& M = e->models[mi];
+    best[mi].assign(M.ops.size(), std::vector<float>(kNumMfmaConfigs, 1e30f));
+    std::vector<int> out_to_op(M.tensors.size(), -1);
+    size_t J = 0;
+    for (size_t oi = 0; oi < M.ops.size(); ++oi) {
+      out_to_op[M.ops[oi].out] = (int)oi;
+      J = std::max(J, cand[mi][oi].size());
+    }
+    float* logits = e->d_logits + mi * (size_t)e->max_batch * e->n_classes;
+    for (int round = 0; round < 2 && rc == RAFIKI_OK; ++round)
+      for (size_t j = 0; j < J && rc == RAFIKI_OK; ++j) {
+        std::vector<std::vector<int>> pass = choice;
+        for (size_t oi = 0; oi < M.ops.size(); ++oi)
+          if (!cand[mi][oi].empty()) pass[mi][oi] = cand[mi][oi][j % cand[mi][oi].size()];
+        e->tuned[n] = std::move(pass);
+        probe.recs.clear();
+        probe.used = 0;
+        tune_probe() = &probe;
+        rc = run_model(e, (int)mi, in, n, logits, s, 0, SIZE_MAX);
+        tune_probe() = nullptr;
+        if (rc) break;
+        for (const TuneProbe::Rec& r : probe.recs) {
+          float ms = 0.f;
+          hipError_t st = hipEventSynchronize(r.b);
+          if (st == hipSuccess) st = hipEventElapsedTime(&ms, r.a, r.b);
+          if (st != hipSuccess) {
+            rc = fail(RAFIKI_ERR_HIP, std::string("tile tuning timing: ") + hipGetErrorString(st));
+            break;
+          }
+          const int oi = r.layer >= 0 && r.layer < (int)out_to_op.size() ? out_to_op[r.layer] : -1;
+          if (oi >= 0 && r.cfg >= 0 && r.cfg < kNumMfmaConfigs)
+            best[mi][oi][r.cfg] = std::min(best[mi][oi][r.cfg], ms);
+        }
+      }
+  }
+  e->tuned.erase(n);
+  e->force_tile = saved_force;
+  e->trace.on = saved_trace;
   if (rc) return rc;
+  for (size_t mi = 0; mi < NM; ++mi) {
+    est[mi] = 0.0;
+    for (size_t oi = 0; oi < cand[mi].size(); ++oi) {
+      float t = 1e30f;
+      for (int cfg : cand[mi][oi])
+        if (best[mi][oi][cfg] < t) { t = best[mi][oi][cfg]; choice[mi][oi] = cfg; }
+      if (t < 1e29f) est[mi] += t;
+    }
+  }
   e->tuned[n] = std::move(choice);
   e->model_ms[n] = std::move(est);
   return RAFIKI_OK;
@@ -715,7 +770,7 @@ int tune(rafiki_ensemble_s* e, int n, const void* in, hipStream_t s) {
 // Only ops [op_begin, op_end) are enqueued, so that the launches of several models
 // can be interleaved.
 int run_model(const rafiki_ensemble_s* e, int mi, const void* in, int n, float* logits, hipStream_t s,
-              size_t op_begin = 0, size_t op_end = SIZE_MAX) {
+              size_t op_begin, size_t op_end) {
   const Model& M = e->models[mi];
   const auto it = e->tuned.find(n);
   const std::vector<int> empty;
