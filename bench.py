@@ -424,13 +424,14 @@ def schedule_desc(ens, n, mask, names):
     if len(members) == 1:
         return names[members[0]]
     try:
-        solo = ens.get_schedule(n, mask)
+        solo, asc = ens.get_schedule(n, mask)
     except Exception:
-        solo = -1
+        solo, asc = -1, 0
     if solo < 0:
         return "all concurrent"
     rest = [names[m] for m in members if m != solo]
-    return f"{names[solo]} alone; {', '.join(rest)} one after another on a second lane, longest alone time first"
+    order = "shortest" if asc else "longest"
+    return f"{names[solo]} alone; {', '.join(rest)} one after another on a second lane, {order} alone time first"
 
 
 def main():

@@ -242,15 +242,17 @@ int rafiki_ensemble_force_tile(rafiki_ensemble_t h, int cfg);
  * three or more selected models, the first infer / infer_vote of a (n, mask) pair times
  * each candidate schedule on `stream` (best of three runs each; it blocks the caller
  * once) and keeps the fastest: solo = -1, all models concurrently; solo = m, model m
- * alone on one lane while the other selected models run one after another (longest
- * alone time first) on a second lane.  A schedule only orders the same launches, so it
- * never changes a result.  Environment RAFIKI_SCHEDULE_TUNING=0 at create skips the
- * timing (solo = -1 unless set).
- * get_schedule: the kept choice; RAFIKI_ERR_INVALID if none has been chosen yet.
+ * alone on one lane while the other selected models run one after another on a second
+ * lane, longest estimated alone time first (ascending = 0) or shortest first
+ * (ascending = 1).  A schedule only orders the same launches, so it never changes a
+ * result.  Environment RAFIKI_SCHEDULE_TUNING=0 at create skips the timing (all
+ * concurrent unless set).
+ * get_schedule: the kept choice (`ascending` may be NULL); RAFIKI_ERR_INVALID if none
+ * has been chosen yet.
  * set_schedule: sets it (solo = -1 or a model of the subset); synchronises the device
  * and drops any kept graphs. */
-int rafiki_ensemble_get_schedule(rafiki_ensemble_t h, int n, uint32_t model_subset_mask, int* solo);
-int rafiki_ensemble_set_schedule(rafiki_ensemble_t h, int n, uint32_t model_subset_mask, int solo);
+int rafiki_ensemble_get_schedule(rafiki_ensemble_t h, int n, uint32_t model_subset_mask, int* solo, int* ascending);
+int rafiki_ensemble_set_schedule(rafiki_ensemble_t h, int n, uint32_t model_subset_mask, int solo, int ascending);
 
 /* Graph replay of the forward passes (off by default; environment RAFIKI_GRAPHS=1 turns
  * it on at create).  Measured on MI355X it is no faster than the eager launches for one

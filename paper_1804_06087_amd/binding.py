@@ -106,8 +106,9 @@ def load_library(path: str = LIB_PATH):
     lib.rafiki_ensemble_trace_read.argtypes = [C.c_void_p, C.POINTER(RafikiTraceRec), C.c_int, C.POINTER(C.c_int)]
     lib.rafiki_tile_config.argtypes = [C.c_int] + [C.POINTER(C.c_int)] * 5
     lib.rafiki_ensemble_force_tile.argtypes = [C.c_void_p, C.c_int]
-    lib.rafiki_ensemble_get_schedule.argtypes = [C.c_void_p, C.c_int, C.c_uint32, C.POINTER(C.c_int)]
-    lib.rafiki_ensemble_set_schedule.argtypes = [C.c_void_p, C.c_int, C.c_uint32, C.c_int]
+    lib.rafiki_ensemble_get_schedule.argtypes = [C.c_void_p, C.c_int, C.c_uint32, C.POINTER(C.c_int),
+                                                 C.POINTER(C.c_int)]
+    lib.rafiki_ensemble_set_schedule.argtypes = [C.c_void_p, C.c_int, C.c_uint32, C.c_int, C.c_int]
     lib.rafiki_ensemble_use_graphs.argtypes = [C.c_void_p, C.c_int]
     lib.rafiki_ensemble_graph_stats.argtypes = [C.c_void_p, C.POINTER(C.c_int), C.POINTER(C.c_longlong),
                                                 C.POINTER(C.c_longlong)]
@@ -530,14 +531,16 @@ class Ensemble:
         """Use tile configuration ``cfg`` for every unsplit bf16 GEMM it suits (-1: tuned)."""
         _check(self._lib.rafiki_ensemble_force_tile(self._h, cfg))
 
-    def get_schedule(self, n: int, mask: int) -> int:
-        """Schedule kept for (n, mask): -1 all models concurrent, m model m alone on one lane."""
-        v = C.c_int(0)
-        _check(self._lib.rafiki_ensemble_get_schedule(self._h, n, mask, C.byref(v)))
-        return v.value
+    def get_schedule(self, n: int, mask: int):
+        """Schedule kept for (n, mask): (solo, ascending).  solo -1: all models concurrent;
+        m: model m alone on one lane, the others chained on a second lane, longest first
+        (ascending 0) or shortest first (ascending 1)."""
+        v, a = C.c_int(0), C.c_int(0)
+        _check(self._lib.rafiki_ensemble_get_schedule(self._h, n, mask, C.byref(v), C.byref(a)))
+        return v.value, a.value
 
-    def set_schedule(self, n: int, mask: int, solo: int):
-        _check(self._lib.rafiki_ensemble_set_schedule(self._h, n, mask, solo))
+    def set_schedule(self, n: int, mask: int, solo: int, ascending: int = 0):
+        _check(self._lib.rafiki_ensemble_set_schedule(self._h, n, mask, solo, ascending))
 
     def use_graphs(self, enable: bool):
         """Turn graph replay of the forward passes on or off (drops every kept graph)."""

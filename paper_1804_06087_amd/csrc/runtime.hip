@@ -162,9 +162,13 @@ struct rafiki_ensemble_s {
   // chosen tiles' times; GEMM FLOPs / 1e12 when tiles are not timed).
   std::map<int, std::vector<double>> model_ms;
   // Per (batch size, subset): the schedule of the selected models' forward passes
-  // chosen by timing (-1: all concurrent; m: model m alone on one lane, the others
-  // one after another on a second lane).
-  std::map<std::pair<int, uint32_t>, int> schedule;
+  // chosen by timing (solo -1: all concurrent; solo m: model m alone on one lane, the
+  // others one after another on a second lane, longest estimated alone time first, or
+  // shortest first when `ascending`).
+  struct Sched {
+    int solo = -1, ascending = 0;
+  };
+  std::map<std::pair<int, uint32_t>, Sched> schedule;
   bool tune_schedule = true;
   bool autotune = true;
   int force_tile = -1;              // diagnostic override of the tuned configuration
@@ -955,14 +959,17 @@ int rafiki_ensemble_create(const rafiki_model_desc* models, int n_models, const 
 // itself).  Forked launches are enqueued interleaved, one op of each model in turn, so
 // that every model stream has work from the start even when enqueueing is slower than
 // the device.
-static int forward(rafiki_ensemble_t h, const CombineArgs& ca, const void* in, int n, hipStream_t s, int solo) {
+static int forward(rafiki_ensemble_t h, const CombineArgs& ca, const void* in, int n, hipStream_t s,
+                   rafiki_ensemble_s::Sched sched) {
+  const int solo = sched.solo;
   int rc = RAFIKI_OK;
   const bool fork = h->concurrent && !h->trace.on && ca.S > 1;
   if (fork) {
     HIPCHK(hipEventRecord(h->staged_ev, s));
     // Lanes.  solo < 0: every model on its own lane.  solo = m: model m alone on one
     // lane, the other selected models one after another on a second lane, longest
-    // (estimated alone) first; each waits for the previous one's done event.
+    // (estimated alone) first, or shortest first if sched.ascending; each waits for
+    // the previous one's done event.
     std::vector<int> prev(h->n_models, -1);        // model this one waits for (-1: staging)
     if (solo >= 0) {
       std::vector<double> est(h->n_models, 1.0);
@@ -972,6 +979,7 @@ static int forward(rafiki_ensemble_t h, const CombineArgs& ca, const void* in, i
       for (int i = 0; i < ca.S; ++i)
         if (ca.sel[i] != solo) rest.push_back(ca.sel[i]);
       std::stable_sort(rest.begin(), rest.end(), [&](int a, int b) { return est[a] > est[b]; });
+      if (sched.ascending) std::reverse(rest.begin(), rest.end());
       for (size_t k = 1; k < rest.size(); ++k) prev[rest[k]] = rest[k - 1];
     }
     // enqueue offsets: a model's launches are enqueued after its predecessor's last one
@@ -1009,20 +1017,26 @@ static int forward(rafiki_ensemble_t h, const CombineArgs& ca, const void* in, i
 
 // The schedule of (n, mask): chosen on first use by timing every candidate on stream s
 // (blocks the caller once).  Candidates: all models concurrent, and each selected model
-// alone on one lane with the others chained on a second.  A schedule only orders the
-// same launches, so the choice never changes a result.  With fewer than three models,
-// when tracing, or with model streams off, the models run as before (solo = -1).
+// alone on one lane with the others chained on a second (longest first, and, with two
+// or more chained, also shortest first).  A schedule only orders the same launches, so
+// the choice never changes a result.  With fewer than three models, when tracing, or
+// with model streams off, the models run as before (all concurrent).
 static int pick_schedule(rafiki_ensemble_t h, const CombineArgs& ca, const void* in, int n, uint32_t mask,
-                         hipStream_t s, int* solo) {
-  *solo = -1;
+                         hipStream_t s, rafiki_ensemble_s::Sched* sched) {
+  *sched = {};
   if (ca.S < 3 || !h->concurrent || h->trace.on) return RAFIKI_OK;
   const auto key = std::make_pair(n, mask);
   const auto it = h->schedule.find(key);
   if (it != h->schedule.end()) {
-    *solo = it->second;
+    *sched = it->second;
     return RAFIKI_OK;
   }
   if (!h->tune_schedule) return RAFIKI_OK;
+  std::vector<rafiki_ensemble_s::Sched> cands(1);
+  for (int i = 0; i < ca.S; ++i) {
+    cands.push_back({ca.sel[i], 0});
+    if (ca.S >= 3) cands.push_back({ca.sel[i], 1});
+  }
   hipEvent_t ev[2] = {nullptr, nullptr};
   HIPCHK(hipEventCreate(&ev[0]));
   hipError_t st = hipEventCreate(&ev[1]);
@@ -1030,10 +1044,10 @@ static int pick_schedule(rafiki_ensemble_t h, const CombineArgs& ca, const void*
     (void)hipEventDestroy(ev[0]);
     return fail(RAFIKI_ERR_HIP, std::string("hipEventCreate: ") + hipGetErrorString(st));
   }
-  int rc = RAFIKI_OK, best_solo = -1;
+  int rc = RAFIKI_OK;
+  rafiki_ensemble_s::Sched best_sched;
   float best = 1e30f;
-  for (int c = -1; c < ca.S && rc == RAFIKI_OK; ++c) {
-    const int cand = c < 0 ? -1 : ca.sel[c];
+  for (const auto& cand : cands) {
     float t = 1e30f;
     for (int rep = 0; rep < 3 && rc == RAFIKI_OK; ++rep) {   // best of three
       st = hipEventRecord(ev[0], s);
@@ -1045,13 +1059,14 @@ static int pick_schedule(rafiki_ensemble_t h, const CombineArgs& ca, const void*
       if (st != hipSuccess && rc == RAFIKI_OK) rc = fail(RAFIKI_ERR_HIP, std::string("schedule timing: ") + hipGetErrorString(st));
       if (rc == RAFIKI_OK) t = std::min(t, ms);
     }
-    if (rc == RAFIKI_OK && t < best) { best = t; best_solo = cand; }
+    if (rc) break;
+    if (t < best) { best = t; best_sched = cand; }
   }
   (void)hipEventDestroy(ev[0]);
   (void)hipEventDestroy(ev[1]);
   if (rc) return rc;
-  h->schedule[key] = best_solo;
-  *solo = best_solo;
+  h->schedule[key] = best_sched;
+  *sched = best_sched;
   return RAFIKI_OK;
 }
 
@@ -1060,8 +1075,8 @@ constexpr size_t kMaxGraphs = 64;   // (batch size, subset) pairs kept as graphs
 // The instantiated graph of the forward passes for (n, mask), captured on first use.
 // *exec stays null when the cache is full or the capture fails; the caller then runs
 // the same launches eagerly (a failed capture is counted and disables graphs).
-static int graph_for(rafiki_ensemble_t h, int n, uint32_t mask, const CombineArgs& ca, const void* in, int solo,
-                     hipGraphExec_t* exec) {
+static int graph_for(rafiki_ensemble_t h, int n, uint32_t mask, const CombineArgs& ca, const void* in,
+                     rafiki_ensemble_s::Sched sched, hipGraphExec_t* exec) {
   *exec = nullptr;
   const auto key = std::make_pair(n, mask);
   const auto it = h->graphs.find(key);
@@ -1077,7 +1092,7 @@ static int graph_for(rafiki_ensemble_t h, int n, uint32_t mask, const CombineArg
     h->use_graphs = false;
     return RAFIKI_OK;
   }
-  const int frc = forward(h, ca, in, n, cs, solo);
+  const int frc = forward(h, ca, in, n, cs, sched);
   hipGraph_t g = nullptr;
   const hipError_t est = hipStreamEndCapture(cs, &g);
   hipGraphExec_t x = nullptr;
@@ -1122,25 +1137,25 @@ static int serve(rafiki_ensemble_t h, const void* batch, int n, uint32_t model_s
     if (h->input_kind == RAFIKI_INPUT_TOKENS_I32)
       HIPCHK(hipMemcpyAsync(h->d_tokens, batch, (size_t)n * h->H * 4, hipMemcpyDeviceToDevice, s));
     hipGraphExec_t exec = nullptr;
-    int solo = -1;
-    rc = pick_schedule(h, ca, in, n, model_subset_mask, s, &solo);
+    rafiki_ensemble_s::Sched sched;
+    rc = pick_schedule(h, ca, in, n, model_subset_mask, s, &sched);
     if (rc) return rc;
-    rc = graph_for(h, n, model_subset_mask, ca, in, solo, &exec);
+    rc = graph_for(h, n, model_subset_mask, ca, in, sched, &exec);
     if (rc) return rc;
     if (exec) {
       HIPCHK(hipGraphLaunch(exec, s));
       ++h->graph_replays;
     } else {
-      rc = forward(h, ca, in, n, s, solo);   // capture refused: the same launches, eagerly
+      rc = forward(h, ca, in, n, s, sched);   // capture refused: the same launches, eagerly
       if (rc) return rc;
     }
   } else {
     const void* in = model_input(h, batch, h->d_staged);
     rc = stage(h, batch, n, s, h->d_staged);
     if (!rc) rc = tune(h, n, in, s);
-    int solo = -1;
-    if (!rc) rc = pick_schedule(h, ca, in, n, model_subset_mask, s, &solo);
-    if (!rc) rc = forward(h, ca, in, n, s, solo);
+    rafiki_ensemble_s::Sched sched;
+    if (!rc) rc = pick_schedule(h, ca, in, n, model_subset_mask, s, &sched);
+    if (!rc) rc = forward(h, ca, in, n, s, sched);
     if (rc) return rc;
   }
   const double cbytes = (double)n * h->n_classes * 4.0 * (ca.S + 1) + 4.0 * n;
@@ -1291,15 +1306,16 @@ int rafiki_ensemble_force_tile(rafiki_ensemble_t h, int cfg) {
   return RAFIKI_OK;
 }
 
-int rafiki_ensemble_get_schedule(rafiki_ensemble_t h, int n, uint32_t mask, int* solo) {
+int rafiki_ensemble_get_schedule(rafiki_ensemble_t h, int n, uint32_t mask, int* solo, int* ascending) {
   if (!h || !solo) return fail(RAFIKI_ERR_INVALID, "null argument");
   const auto it = h->schedule.find(std::make_pair(n, mask));
   if (it == h->schedule.end()) return fail(RAFIKI_ERR_INVALID, "no schedule chosen for this batch size and subset");
-  *solo = it->second;
+  *solo = it->second.solo;
+  if (ascending) *ascending = it->second.ascending;
   return RAFIKI_OK;
 }
 
-int rafiki_ensemble_set_schedule(rafiki_ensemble_t h, int n, uint32_t mask, int solo) {
+int rafiki_ensemble_set_schedule(rafiki_ensemble_t h, int n, uint32_t mask, int solo, int ascending) {
   if (!h) return fail(RAFIKI_ERR_INVALID, "null handle");
   if (n < 1 || n > h->max_batch || mask == 0 || (h->n_models < 32 && (mask >> h->n_models) != 0))
     return fail(RAFIKI_ERR_INVALID, "batch size or subset mask out of range");
@@ -1307,7 +1323,7 @@ int rafiki_ensemble_set_schedule(rafiki_ensemble_t h, int n, uint32_t mask, int 
     return fail(RAFIKI_ERR_INVALID, "solo must be -1 or a model of the subset");
   HIPCHK(hipDeviceSynchronize());   // graphs built with the old schedule may still run
   h->drop_graphs();
-  h->schedule[std::make_pair(n, mask)] = solo;
+  h->schedule[std::make_pair(n, mask)] = {solo, ascending ? 1 : 0};
   return RAFIKI_OK;
 }
 

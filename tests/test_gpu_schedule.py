@@ -31,17 +31,18 @@ def test_every_schedule_gives_the_same_bits(cid, n, mask):
     x = torch.from_numpy(batch).to(DEV)
     with Ensemble(specs, params, precision="bf16", max_batch=n) as ens:
         p0, l0 = _infer(ens, x, n, mask, C)
-        chosen = ens.get_schedule(n, mask)
+        chosen, asc = ens.get_schedule(n, mask)
         members = [m for m in range(len(specs)) if (mask >> m) & 1]
         assert chosen == -1 or chosen in members
+        assert asc in (0, 1)
         v0 = _infer(ens, x, n, mask, C, vote=True)
-        for solo in [-1] + members:
-            ens.set_schedule(n, mask, solo)
-            assert ens.get_schedule(n, mask) == solo
+        for solo, asc in [(-1, 0)] + [(m, a) for m in members for a in (0, 1)]:
+            ens.set_schedule(n, mask, solo, asc)
+            assert ens.get_schedule(n, mask) == (solo, asc)
             for _ in range(2):
                 p, lab = _infer(ens, x, n, mask, C)
-                assert np.array_equal(p, p0), f"schedule {solo}: probabilities differ"
-                assert np.array_equal(lab, l0), f"schedule {solo}: labels differ"
+                assert np.array_equal(p, p0), f"schedule {solo}/{asc}: probabilities differ"
+                assert np.array_equal(lab, l0), f"schedule {solo}/{asc}: labels differ"
             v, lv = _infer(ens, x, n, mask, C, vote=True)
             assert np.array_equal(v, v0[0]) and np.array_equal(lv, v0[1])
 
@@ -58,5 +59,5 @@ def test_schedule_arguments():
             ens.set_schedule(9, 0b111, -1)             # beyond max_batch
         with pytest.raises(RafikiError):
             ens.set_schedule(8, 0b1000, -1)            # no such model
-        ens.set_schedule(8, 0b111, 1)
-        assert ens.get_schedule(8, 0b111) == 1
+        ens.set_schedule(8, 0b111, 1, 1)
+        assert ens.get_schedule(8, 0b111) == (1, 1)
