@@ -27,8 +27,10 @@
  *   enqueued work and must not alias each other.
  * - infer / model_logits only enqueue work on `stream` (a hipStream_t; 0 = the null
  *   stream) and return; kernel faults surface at the next synchronisation.
- * - A handle owns its device weights and a workspace sized for opts.max_batch; it is
- *   NOT safe for concurrent infer calls from several threads or streams.
+ * - A handle owns its device weights and a workspace sized for opts.max_batch, which
+ *   every call shares: issue the calls on one stream, or make each call's stream wait
+ *   for the previous call's work (an event); calls from several threads at once are
+ *   not supported.
  * - Inputs are not checked on the device: token ids must lie in [0, vocab) and image
  *   values must be finite.
  * - Results are deterministic: the same inputs, mask and n give bitwise-identical
@@ -133,9 +135,12 @@ int rafiki_ensemble_create(const rafiki_model_desc* models, int n_models,
  * out_labels is int32 [n].  Requires 1 <= n <= max_batch, mask != 0 and no bit at
  * position >= n_models (else RAFIKI_ERR_INVALID).  Enqueue-only on `stream`, except
  * that the first call (infer or model_logits) with a given n blocks while it times
- * the candidate tile configurations of every layer on `stream` (set the environment
- * variable RAFIKI_AUTOTUNE=0 to use fixed defaults instead).  The choice never
- * changes a result: every candidate sums each output in the same order. */
+ * the candidate tile configurations of every layer inside forward passes on `stream`
+ * (set the environment variable RAFIKI_AUTOTUNE=0 to use fixed defaults instead), and
+ * the first infer of a (n, mask) with three or more models blocks while it times the
+ * model schedules (see rafiki_ensemble_get_schedule).  Neither choice changes a
+ * result: every tile candidate sums each output in the same order, and a schedule
+ * only orders the same launches. */
 int rafiki_ensemble_infer(rafiki_ensemble_t h, const void* batch, int n, uint32_t model_subset_mask,
                           float* out_probs, int32_t* out_labels, void* stream);
 
