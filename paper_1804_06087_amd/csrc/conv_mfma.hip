@@ -589,7 +589,9 @@ __global__ void splitk_reduce_kernel(ConvArgs a, int splits, int in_bf16) {
   X(34, 128, 128, 2, 2, 3, 4, 0, 3) /* as 33, three stages */                          \
   X(35, 64, 128, 1, 4, 2, 4, 0, 4)  /* wave 64x32, 32-wide K, 4 waves per SIMD */       \
   X(36, 128, 64, 2, 2, 2, 4, 0, 4)  /* wave 64x32, 32-wide K, 4 waves per SIMD */       \
-  X(37, 256, 128, 4, 2, 2, 4, 0, 2) /* 8 waves, wave 64x64, 32-wide K */
+  X(37, 256, 128, 4, 2, 2, 4, 0, 2) /* 8 waves, wave 64x64, 32-wide K */                 \
+  X(38, 256, 64, 2, 2, 2, 8, 0, 0)  /* wave 128x32, two stages */                        \
+  X(39, 256, 64, 2, 2, 3, 4, 0, 0)  /* wave 128x32, 32-wide K, 3 stages */
 
 #define RAFIKI_CFG_ENTRY(id, BM, BN, WM, WN, ST, KC, SP, OC) {BM, BN, WM * WN, ST, KC * 8},
 const MfmaConfig kMfmaConfigs[kNumMfmaConfigs] = {RAFIKI_MFMA_CONFIGS(RAFIKI_CFG_ENTRY)};
