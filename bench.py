@@ -76,6 +76,10 @@ def parse():
                     help="HBM bandwidth of the path's memory-bound kernels called on their own (combine, vote, "
                          "max-pool, global average pool) at ImageNet-shaped sizes, against the 8 TB/s peak and a "
                          "plain device copy; one JSON line per kernel")
+    ap.add_argument("--layers", action="store_true",
+                    help="per-launch roofline of one workload (--workload, --n): traced steps with the models "
+                         "one after another; for every launch its own bound max(FLOPs / 2.5 PFLOP/s, bytes / 8 TB/s) "
+                         "and the fraction of it achieved; a markdown table")
     return ap.parse_args()
 
 
@@ -418,6 +422,74 @@ def sweep_main(args, dev):
     ens.close()
 
 
+def layers_main(args, dev):
+    """Per-launch roofline table of one workload: every launch of three traced steps
+    (models one after another, each kernel alone on the GPU), averaged per (model,
+    layer, kernel class).  A launch's bound is max(FLOPs / bf16 peak, bytes / HBM peak)
+    with its algorithmic FLOPs and bytes; 'of bound' = that time / measured time."""
+    import numpy as np
+    import torch
+
+    import workloads as wl
+    from workloads.specs import OP_NAMES
+    from paper_1804_06087_amd import Ensemble
+
+    cid = {"c1": 1, "c2": 2, "c3": 3, "c4": 4, "c5": 5}[args.workload]
+    cfg, specs, params, batch = wl.build_config(cid, n=args.n)
+    n = batch.shape[0]
+    mask = args.mask or (1 << len(specs)) - 1
+    C = specs[0].n_classes
+    ens = Ensemble(specs, params, precision=cfg.precision, max_batch=n)
+    x = torch.from_numpy(batch).to(dev)
+    probs = torch.empty((n, C), dtype=torch.float32, device=dev)
+    labels = torch.empty((n,), dtype=torch.int32, device=dev)
+    for _ in range(3):
+        ens.infer(x, n, mask, probs, labels)
+    torch.cuda.synchronize()
+    ens.trace(True)
+    T = 3
+    for _ in range(T):
+        ens.infer(x, n, mask, probs, labels)
+    recs = ens.trace_read()
+    ens.trace(False)
+    ens.close()
+    agg = {}
+    for r in recs:
+        key = (r["model"], r["layer"], r["kind"])
+        a = agg.setdefault(key, {"ms": 0.0, "flops": r["flops"], "bytes": r["bytes"], "cfg": r["tile_cfg"],
+                                 "splits": r["splits"]})
+        a["ms"] += r["ms"] / T
+    tot_ms = sum(a["ms"] for a in agg.values())
+    tot_bound = 0.0
+    print(f"# Per-launch roofline: {cfg.name}, batch {n}, mask {mask:#b}\n")
+    print(f"Command: `python bench.py --layers --workload {args.workload}"
+          + (f" --n {args.n}" if args.n else "") + (f" --mask {args.mask}" if args.mask else "") + "`\n")
+    print("| model | layer | op | kernel | tile / splits | us | TFLOP/s | GB/s | bound | bound us | of bound |")
+    print("|---|---|---|---|---|---|---|---|---|---|---|")
+    by_kind = {}
+    for (m, li, kind), a in sorted(agg.items(), key=lambda t: (t[0][0], t[0][1])):
+        t_f = a["flops"] / (PEAK_BF16_TFLOPS * 1e12) * 1e3
+        t_b = a["bytes"] / (PEAK_HBM_GBS * 1e9) * 1e3
+        bound, tb = ("mfma", t_f) if t_f >= t_b else ("hbm", t_b)
+        tot_bound += tb
+        k = by_kind.setdefault(kind, [0.0, 0.0])
+        k[0] += a["ms"]
+        k[1] += tb
+        desc = ""
+        if m >= 0 and li >= 0:
+            L = specs[m].layers[li]
+            desc = f"{OP_NAMES[L.op]} {L.c_in}->{L.c_out} {L.kh}x{L.kw}/{L.stride}"
+        tile = f"{a['cfg']} / {a['splits']}" if a["cfg"] >= 0 else ""
+        print(f"| {specs[m].name if m >= 0 else '-'} | {li} | {desc} | {kind} | {tile} | {a['ms'] * 1e3:.1f} | "
+              f"{a['flops'] / a['ms'] / 1e9:.0f} | {a['bytes'] / a['ms'] / 1e6:.0f} | {bound} | {tb * 1e3:.1f} | "
+              f"{tb / a['ms']:.2f} |")
+    print(f"\nTotal traced time {tot_ms:.3f} ms per step; sum of the launches' roofline times {tot_bound:.3f} ms "
+          f"({tot_bound / tot_ms:.3f} of the measured time).\n")
+    print("| kernel class | ms per step | roofline ms | of bound |\n|---|---|---|---|")
+    for kind, (ms, tb) in sorted(by_kind.items(), key=lambda t: -t[1][0]):
+        print(f"| {kind} | {ms:.3f} | {tb:.3f} | {tb / ms:.2f} |")
+
+
 def schedule_desc(ens, n, mask, names):
     """How the selected models' forward passes were scheduled for (n, mask)."""
     members = [m for m in range(len(names)) if (mask >> m) & 1]
@@ -468,6 +540,9 @@ def main():
         return
     if args.memory_kernels:
         memory_main(args, dev)
+        return
+    if args.layers:
+        layers_main(args, dev)
         return
 
     if args.workload == "c4":
@@ -542,12 +617,15 @@ def main():
     ens.trace(False)
     torch.cuda.synchronize()
     classes = {}
+    flop_peak = (PEAK_BF16_TFLOPS if precision == "bf16" else PEAK_FP32_TFLOPS) * 1e12
     for r in recs:
-        c = classes.setdefault(r["kind"], {"launches": 0, "ms": 0.0, "flops": 0.0, "bytes": 0.0})
+        c = classes.setdefault(r["kind"], {"launches": 0, "ms": 0.0, "flops": 0.0, "bytes": 0.0, "bound_ms": 0.0})
         c["launches"] += 1
         c["ms"] += r["ms"]
         c["flops"] += r["flops"]
         c["bytes"] += r["bytes"]
+        # this launch's own roofline time: the larger of its FLOPs at peak and its bytes at peak
+        c["bound_ms"] += max(r["flops"] / flop_peak, r["bytes"] / (PEAK_HBM_GBS * 1e9)) * 1e3
     traced_step_ms = sum(c["ms"] for c in classes.values()) / args.trace_steps
     kernels = {}
     for k, c in classes.items():
@@ -556,6 +634,8 @@ def main():
         if c["flops"] > 0:
             ent["tflops"] = round(c["flops"] / c["ms"] / 1e9, 2)
         ent["gbs_alg"] = round(c["bytes"] / c["ms"] / 1e6, 1)
+        # time-weighted fraction of the per-launch roofline (each launch against its own bound)
+        ent["of_launch_roofline"] = round(c["bound_ms"] / c["ms"], 4)
         kernels[k] = ent
     dom = max(classes, key=lambda k: classes[k]["ms"])
     d = classes[dom]
