@@ -110,3 +110,23 @@ def test_graph_dropped_by_force_tile():
         assert np.array_equal(p, base[0]) and np.array_equal(p2, base[0])
         assert np.array_equal(lab2, base[1])
         assert ens.graph_stats()[2] == 0
+
+
+@pytest.mark.parametrize("solo,asc", [(-1, 0), (0, 0), (2, 1)])
+def test_graph_replay_under_each_schedule(solo, asc):
+    """A graph captured with a two-lane schedule (a model waiting on another's done
+    event) replays the same bits as the eager launches."""
+    cfg, specs, params, batch = wl.build_config(2, n=24)
+    C = 10
+    x = torch.from_numpy(batch).to(DEV)
+    with Ensemble(specs, params, precision="bf16", max_batch=24) as ens:
+        _infer(ens, x, 24, 0b111, C)                   # tunes n = 24
+        ens.set_schedule(24, 0b111, solo, asc)
+        ens.use_graphs(False)
+        base = _infer(ens, x, 24, 0b111, C)
+        ens.use_graphs(True)
+        for _ in range(3):
+            p, lab = _infer(ens, x, 24, 0b111, C)
+            assert np.array_equal(p, base[0]) and np.array_equal(lab, base[1])
+        g, r, f = ens.graph_stats()
+        assert g == 1 and r == 3 and f == 0
