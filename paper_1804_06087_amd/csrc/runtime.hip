@@ -4,8 +4,11 @@
 //   per-channel fp32 (scale, shift) computed in fp64, round weights to the compute
 //   precision, pack them in the kernels' [Co_pad][Kp] (u, v, ci) order, upload, and
 //   plan each model's activation workspace by liveness for max_batch requests.
-// infer: stage the request batch once (NCHW fp32 -> NHWC), run the forward pass of
-//   every selected model on the caller's stream into its logits slot, then combine.
+// infer: stage the request batch once (NCHW fp32 -> NHWC) on the caller's stream, run
+//   the forward pass of every selected model into its logits slot (on the models' own
+//   streams, in the schedule timed for this batch size and subset, or replayed as a
+//   graph), join back on the caller's stream, then combine.  The first call with a
+//   new batch size also times every GEMM op's tile candidates inside forward passes.
 #include "rafiki_ensemble.h"
 #include "kernels.h"
 #include "greedy.h"
