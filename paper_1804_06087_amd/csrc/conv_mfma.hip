@@ -591,7 +591,10 @@ __global__ void splitk_reduce_kernel(ConvArgs a, int splits, int in_bf16) {
   X(36, 128, 64, 2, 2, 2, 4, 0, 4)  /* wave 64x32, 32-wide K, 4 waves per SIMD */       \
   X(37, 256, 128, 4, 2, 2, 4, 0, 2) /* 8 waves, wave 64x64, 32-wide K */                 \
   X(38, 256, 64, 2, 2, 2, 8, 0, 0)  /* wave 128x32, two stages */                        \
-  X(39, 256, 64, 2, 2, 3, 4, 0, 0)  /* wave 128x32, 32-wide K, 3 stages */
+  X(39, 256, 64, 2, 2, 3, 4, 0, 0)  /* wave 128x32, 32-wide K, 3 stages */                \
+  X(40, 128, 128, 2, 4, 3, 8, 0, 0) /* 8 waves, wave 64x32, 3 stages */                   \
+  X(41, 128, 128, 4, 2, 4, 4, 0, 0) /* 8 waves, wave 32x64, 32-wide K, 4 stages */        \
+  X(42, 128, 128, 2, 4, 2, 8, 0, 0) /* 8 waves, wave 64x32, 2 stages */
 
 #define RAFIKI_CFG_ENTRY(id, BM, BN, WM, WN, ST, KC, SP, OC) {BM, BN, WM * WN, ST, KC * 8},
 const MfmaConfig kMfmaConfigs[kNumMfmaConfigs] = {RAFIKI_MFMA_CONFIGS(RAFIKI_CFG_ENTRY)};

@@ -63,7 +63,7 @@ struct ConvArgs {
 // Direct-to-LDS pipelined bf16 MFMA kernel; cfg selects the tile configuration
 // (kMfmaConfigs).  splits > 1 writes partial sums; finish with splitk_reduce.
 struct MfmaConfig { int bm, bn, waves, stages, bk; };
-constexpr int kNumMfmaConfigs = 40;
+constexpr int kNumMfmaConfigs = 43;
 extern const MfmaConfig kMfmaConfigs[kNumMfmaConfigs];
 hipError_t launch_conv_mfma(const ConvArgs& a, int cfg, int splits, hipStream_t s);
 hipError_t launch_splitk_reduce(const ConvArgs& a, int splits, int in_bf16, hipStream_t s);
