@@ -190,9 +190,13 @@ typedef struct {
   int splits;                   /* the same launches: K splits (1 = unsplit); 0 otherwise */
 } rafiki_trace_rec;
 
-/* Enable (1) or disable (0) per-launch event timing of subsequent infer / model_logits
- * calls on this handle; also discards unread records.  Tracing adds two event
- * records per launch; it does not change results. */
+/* Per-launch event timing of subsequent infer / model_logits calls on this handle:
+ * enable = 0 off; 1 on, with the selected models run one after another on the
+ * caller's stream (each kernel has the GPU to itself); 2 on, with the models on their
+ * own streams in their kept schedule (kernels time their share of a concurrent step;
+ * no schedule is timed while tracing).  Also discards unread records.  Tracing adds two
+ * event records per launch; it does not change results.  Other values:
+ * RAFIKI_ERR_INVALID. */
 int rafiki_ensemble_trace(rafiki_ensemble_t h, int enable);
 
 /* Set *count to the number of traced launches.  If cap >= *count, wait for them, copy

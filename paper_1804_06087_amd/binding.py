@@ -524,8 +524,10 @@ class Ensemble:
                                                             C.byref(nd), _stream(stream)))
         return lat, dispatches_to_array(disp, nd.value)
 
-    def trace(self, enable: bool):
-        _check(self._lib.rafiki_ensemble_trace(self._h, 1 if enable else 0))
+    def trace(self, enable, concurrent: bool = False):
+        """Per-launch timing on (models one after another, or concurrent=True: on their
+        own streams in their kept schedule) or off."""
+        _check(self._lib.rafiki_ensemble_trace(self._h, (2 if concurrent else 1) if enable else 0))
 
     def force_tile(self, cfg: int):
         """Use tile configuration ``cfg`` for every unsplit bf16 GEMM it suits (-1: tuned)."""

@@ -130,6 +130,7 @@ struct FreeList {
 // kernel, resolved by rafiki_ensemble_trace_read.
 struct Tracer {
   bool on = false;
+  bool concurrent = false;   // keep the models' own streams and schedule while tracing
   struct Rec { int kind, model, layer; double flops, bytes; hipEvent_t a, b; int tile_cfg, splits; };
   std::vector<Rec> recs;
   std::vector<hipEvent_t> pool;
@@ -966,7 +967,7 @@ static int forward(rafiki_ensemble_t h, const CombineArgs& ca, const void* in, i
                    rafiki_ensemble_s::Sched sched) {
   const int solo = sched.solo;
   int rc = RAFIKI_OK;
-  const bool fork = h->concurrent && !h->trace.on && ca.S > 1;
+  const bool fork = h->concurrent && (!h->trace.on || h->trace.concurrent) && ca.S > 1;
   if (fork) {
     HIPCHK(hipEventRecord(h->staged_ev, s));
     // Lanes.  solo < 0: every model on its own lane.  solo = m: model m alone on one
@@ -1027,14 +1028,14 @@ static int forward(rafiki_ensemble_t h, const CombineArgs& ca, const void* in, i
 static int pick_schedule(rafiki_ensemble_t h, const CombineArgs& ca, const void* in, int n, uint32_t mask,
                          hipStream_t s, rafiki_ensemble_s::Sched* sched) {
   *sched = {};
-  if (ca.S < 3 || !h->concurrent || h->trace.on) return RAFIKI_OK;
+  if (ca.S < 3 || !h->concurrent || (h->trace.on && !h->trace.concurrent)) return RAFIKI_OK;
   const auto key = std::make_pair(n, mask);
   const auto it = h->schedule.find(key);
   if (it != h->schedule.end()) {
     *sched = it->second;
     return RAFIKI_OK;
   }
-  if (!h->tune_schedule) return RAFIKI_OK;
+  if (!h->tune_schedule || h->trace.on) return RAFIKI_OK;   // never time candidates while tracing
   std::vector<rafiki_ensemble_s::Sched> cands(1);
   for (int i = 0; i < ca.S; ++i) {
     cands.push_back({ca.sel[i], 0});
@@ -1214,7 +1215,9 @@ int rafiki_ensemble_destroy(rafiki_ensemble_t h) {
 
 int rafiki_ensemble_trace(rafiki_ensemble_t h, int enable) {
   if (!h) return fail(RAFIKI_ERR_INVALID, "null handle");
+  if (enable < 0 || enable > 2) return fail(RAFIKI_ERR_INVALID, "trace mode must be 0, 1 or 2");
   h->trace.on = enable != 0;
+  h->trace.concurrent = enable == 2;
   h->trace.recs.clear();
   h->trace.used = 0;
   return RAFIKI_OK;

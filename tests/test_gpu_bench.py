@@ -31,6 +31,8 @@ def test_bench_line_has_the_contract_fields(monkeypatch, capsys):
         assert k in r, k
     assert r["bound"] == "mfma" and r["peak"] == 2500.0 and 0 < r["frac"] < 1
     assert abs(r["frac"] - r["achieved"] / r["peak"]) < 1e-3
+    # the same kernel timed in the concurrent schedule (three models): a longer launch
+    assert r["concurrent_avg_launch_ms"] > 0 and r["concurrent_achieved"] > 0
     c = d["cpu_baseline"]
     assert c["kind"] == "oracle" and c["value"] > 0 and c["cores"] >= 1
     for kind in d["kernels"].values():
