@@ -671,7 +671,9 @@ def main():
 
     # HBM traffic of the dominant kernel from committed counter runs, if they were
     # taken on the current kernel source
-    tfile = args.traffic_file or os.path.join(ROOT, "profiles", f"conv_mfma_traffic_{args.workload}.json")
+    traffic_names = {"c3": "r50_vgg16_r101_b64"}   # workloads whose conv traffic counters are committed
+    tfile = args.traffic_file or (os.path.join(ROOT, "profiles", f"conv_mfma_traffic_{traffic_names[args.workload]}.json")
+                                  if args.workload in traffic_names else "")
     if dom == "conv_mfma" and os.path.exists(tfile):
         try:
             t = json.load(open(tfile))
