@@ -329,10 +329,14 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineArgs a) {
   float acc[kCombineMaxPerLane];
 #pragma unroll
   for (int i = 0; i < kCombineMaxPerLane; ++i) acc[i] = 0.f;
+  // the next selected model's row is loaded while this one is reduced
+  float nxt[kCombineMaxPerLane];
+  load_row<VEC>(a.logits + a.sel[0] * a.ld_model + (long long)row * a.C, a.C, lane, nxt);
   for (int s = 0; s < a.S; ++s) {
-    const float* z = a.logits + a.sel[s] * a.ld_model + (long long)row * a.C;
     float v[kCombineMaxPerLane];
-    load_row<VEC>(z, a.C, lane, v);
+#pragma unroll
+    for (int i = 0; i < kCombineMaxPerLane; ++i) v[i] = nxt[i];
+    if (s + 1 < a.S) load_row<VEC>(a.logits + a.sel[s + 1] * a.ld_model + (long long)row * a.C, a.C, lane, nxt);
     float mx = -INFINITY;
 #pragma unroll
     for (int i = 0; i < kCombineMaxPerLane; ++i) mx = fmaxf(mx, v[i]);
@@ -404,10 +408,15 @@ __global__ __launch_bounds__(256) void vote_kernel(CombineArgs a) {
   if (row >= a.n) return;
   constexpr int R = kCombineMaxPerLane / VEC;
   int pred_mine = -1;
+  // all of a row's loads first, then the scan; the next model's row is loaded while
+  // this one is scanned
+  float nxt[kCombineMaxPerLane];
+  load_row<VEC>(a.logits + a.sel[0] * a.ld_model + (long long)row * a.C, a.C, lane, nxt);
   for (int s = 0; s < a.S; ++s) {
-    const float* z = a.logits + a.sel[s] * a.ld_model + (long long)row * a.C;
     float v[kCombineMaxPerLane];
-    load_row<VEC>(z, a.C, lane, v);   // all of the row's loads first, then the scan
+#pragma unroll
+    for (int i = 0; i < kCombineMaxPerLane; ++i) v[i] = nxt[i];
+    if (s + 1 < a.S) load_row<VEC>(a.logits + a.sel[s + 1] * a.ld_model + (long long)row * a.C, a.C, lane, nxt);
     float best = -INFINITY;
     int bidx = 0x7fffffff;
 #pragma unroll
