@@ -296,6 +296,8 @@ __device__ __forceinline__ float wave_sum(float v) {
 // lane holding classes 4 (i * 64 + lane) + j; VEC = 1: classes i * 64 + lane.  Either way
 // the classes a lane holds increase with its register index, so keeping the first
 // maximum in a lane and the lower index across lanes gives the first-index argmax.
+typedef float nt_f4 __attribute__((ext_vector_type(4)));   // streaming (non-temporal) 16-byte accesses
+
 template <int VEC>
 __device__ __forceinline__ int class_of(int i, int j, int lane) {
   return VEC == 4 ? 4 * (i * 64 + lane) + j : i * 64 + lane;
@@ -308,7 +310,8 @@ __device__ __forceinline__ void load_row(const float* z, int C, int lane, float 
 #pragma unroll
     for (int i = 0; i < kCombineMaxPerLane / 4; ++i) {
       const int c = 4 * (i * 64 + lane);
-      const float4 q = c < C ? *(const float4*)(z + c) : make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
+      const nt_f4 q = c < C ? __builtin_nontemporal_load((const nt_f4*)(z + c))
+                            : nt_f4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
       v[4 * i + 0] = q.x; v[4 * i + 1] = q.y; v[4 * i + 2] = q.z; v[4 * i + 3] = q.w;
     }
   } else {
@@ -370,7 +373,7 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineArgs a) {
     }
     const int c0 = class_of<VEC>(i, 0, lane);
     if (c0 < a.C) {
-      if constexpr (VEC == 4) *(float4*)(prow + c0) = make_float4(p[0], p[1], p[2], p[3]);
+      if constexpr (VEC == 4) __builtin_nontemporal_store(nt_f4{p[0], p[1], p[2], p[3]}, (nt_f4*)(prow + c0));
       else prow[c0] = p[0];
     }
   }
@@ -455,7 +458,7 @@ __global__ __launch_bounds__(256) void vote_kernel(CombineArgs a) {
     }
     const int c0 = class_of<VEC>(i, 0, lane);
     if (c0 < a.C) {
-      if constexpr (VEC == 4) *(float4*)(prow + c0) = make_float4(f[0], f[1], f[2], f[3]);
+      if constexpr (VEC == 4) __builtin_nontemporal_store(nt_f4{f[0], f[1], f[2], f[3]}, (nt_f4*)(prow + c0));
       else prow[c0] = f[0];
     }
   }
