@@ -32,6 +32,22 @@ __device__ __forceinline__ void load8(const void* p, long long off, int bf16, fl
     v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w; v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
   }
 }
+// load8 with streaming (non-temporal) loads, for data read exactly once
+typedef unsigned int nt_u4 __attribute__((ext_vector_type(4)));
+typedef float nt_f4v __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ void load8_stream(const void* p, long long off, int bf16, float v[8]) {
+  if (bf16) {
+    const nt_u4 q = __builtin_nontemporal_load((const nt_u4*)((const bf16_t*)p + off));
+    v[0] = bf2f(q.x & 0xFFFFu); v[1] = bf2f(q.x >> 16);
+    v[2] = bf2f(q.y & 0xFFFFu); v[3] = bf2f(q.y >> 16);
+    v[4] = bf2f(q.z & 0xFFFFu); v[5] = bf2f(q.z >> 16);
+    v[6] = bf2f(q.w & 0xFFFFu); v[7] = bf2f(q.w >> 16);
+  } else {
+    const nt_f4v a = __builtin_nontemporal_load((const nt_f4v*)((const float*)p + off));
+    const nt_f4v b = __builtin_nontemporal_load((const nt_f4v*)((const float*)p + off + 4));
+    v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w; v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+  }
+}
 __device__ __forceinline__ void store8(void* p, long long off, int bf16, const float v[8]) {
   if (bf16) {
     uint4 q;
@@ -77,8 +93,10 @@ hipError_t launch_stage_images(const float* x, void* y, int N, int C, int H, int
 }
 
 // ---------------------------------------------------------------- max-pool
+// stream = 1 (windows do not overlap, stride >= k): every input value is read once, with
+// streaming loads; overlapping windows re-read neighbours from cache and load normally.
 __global__ void maxpool_kernel(const void* __restrict__ x, void* y, int N, int H, int W, int Cs, int Ho, int Wo,
-                               int k, int stride, int pad, int bf16) {
+                               int k, int stride, int pad, int bf16, int stream) {
   const int groups = Cs / 8;
   const long long total = (long long)N * Ho * Wo * groups;
   const long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x;
@@ -99,7 +117,9 @@ __global__ void maxpool_kernel(const void* __restrict__ x, void* y, int N, int H
       const int wi = wo * stride - pad + v;
       if (wi < 0 || wi >= W) continue;
       float q[8];
-      load8(x, ((n * H + hi) * W + wi) * Cs + g * 8, bf16, q);
+      const long long off = ((n * H + hi) * W + wi) * Cs + g * 8;
+      if (stream) load8_stream(x, off, bf16, q);
+      else load8(x, off, bf16, q);
 #pragma unroll
       for (int j = 0; j < 8; ++j) m[j] = fmaxf(m[j], q[j]);
     }
@@ -111,16 +131,16 @@ hipError_t launch_maxpool(const void* x, void* y, int N, int H, int W, int Cs, i
                           int pad, int bf16, hipStream_t s) {
   const long long total = (long long)N * Ho * Wo * (Cs / 8);
   launch(maxpool_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), s, x, y, N, H, W, Cs, Ho,
-                     Wo, k, stride, pad, bf16);
+                     Wo, k, stride, pad, bf16, stride >= k ? 1 : 0);
   return hipGetLastError();
 }
 
 // ---------------------------------------------------------------- GAP / max over time
 // Block (image n, chunk of GB 8-channel groups); the 256 threads form P = 256 / GB
 // position slices of GB groups.  Thread (slice s, group g) reduces positions s, s + P,
-// s + 2P, ... in increasing order (four 16-byte loads in flight), then thread (0, g)
-// folds the P partial results in slice order.  The order is fixed, so results are
-// deterministic; sums are fp32.
+// s + 2P, ... in increasing order (four 16-byte streaming loads in flight: every input
+// value is read once), then thread (0, g) folds the P partial results in slice order.
+// The order is fixed, so results are deterministic; sums are fp32.
 constexpr int kReduceThreads = 256;
 
 __global__ __launch_bounds__(kReduceThreads) void spatial_reduce_kernel(const void* __restrict__ x, void* y, int HW,
@@ -143,15 +163,15 @@ __global__ __launch_bounds__(kReduceThreads) void spatial_reduce_kernel(const vo
     int p = sl;
     for (; p + 3 * P < HW; p += 4 * P) {
       float q0[8], q1[8], q2[8], q3[8];
-      load8(x, base + (long long)p * Cs, bf16, q0);
-      load8(x, base + (long long)(p + P) * Cs, bf16, q1);
-      load8(x, base + (long long)(p + 2 * P) * Cs, bf16, q2);
-      load8(x, base + (long long)(p + 3 * P) * Cs, bf16, q3);
+      load8_stream(x, base + (long long)p * Cs, bf16, q0);
+      load8_stream(x, base + (long long)(p + P) * Cs, bf16, q1);
+      load8_stream(x, base + (long long)(p + 2 * P) * Cs, bf16, q2);
+      load8_stream(x, base + (long long)(p + 3 * P) * Cs, bf16, q3);
       fold(q0); fold(q1); fold(q2); fold(q3);
     }
     for (; p < HW; p += P) {
       float q[8];
-      load8(x, base + (long long)p * Cs, bf16, q);
+      load8_stream(x, base + (long long)p * Cs, bf16, q);
       fold(q);
     }
   }
