@@ -500,6 +500,8 @@ def layers_main(args, dev):
         if m >= 0 and li >= 0:
             L = specs[m].layers[li]
             desc = f"{OP_NAMES[L.op]} {L.c_in}->{L.c_out} {L.kh}x{L.kw}/{L.stride}"
+            if OP_NAMES[L.op] == "concat" and kind != "concat":   # branches fused into one GEMM + max
+                desc = f"conv1d_maxtime branches -> concat {L.c_out}"
         tile = f"{a['cfg']} / {a['splits']}" if a["cfg"] >= 0 else ""
         print(f"| {specs[m].name if m >= 0 else '-'} | {li} | {desc} | {kind} | {tile} | {a['ms'] * 1e3:.1f} | "
               f"{a['flops'] / a['ms'] / 1e9:.0f} | {a['bytes'] / a['ms'] / 1e6:.0f} | {bound} | {tb * 1e3:.1f} | "

@@ -76,9 +76,18 @@ hipError_t launch_stage_images(const float* x, void* y, int N, int C, int H, int
 // Max-pool k x k / stride / pad over NHWC (Cs channels).
 hipError_t launch_maxpool(const void* x, void* y, int N, int H, int W, int Cs, int Ho, int Wo, int k,
                           int stride, int pad, int bf16, hipStream_t s);
+// Channel segments of a reduction whose channels cover different numbers of
+// positions: channels [end[i-1], end[i]) (end[-1] = 0) reduce over their first len[i]
+// positions; channels at or past end[n - 1] over all HW.  n = 0: every channel over HW.
+constexpr int kMaxReduceSegs = 8;
+struct ReduceSegs {
+  int n;
+  int end[kMaxReduceSegs];
+  int len[kMaxReduceSegs];
+};
 // Global average pool NHWC [N][HW][Cs] -> [N][Cs]; also max over time when is_max.
 hipError_t launch_spatial_reduce(const void* x, void* y, int N, int HW, int Cs, int is_max, int bf16,
-                                 hipStream_t s);
+                                 hipStream_t s, const ReduceSegs* segs = nullptr);
 // Embedding gather: tokens [N][L] -> y [N][L][Cs] rows of table [vocab][Cs].
 hipError_t launch_embed_gather(const int32_t* tok, const void* table, void* y, int N, int L, int Cs,
                                int bf16, hipStream_t s);

@@ -143,14 +143,31 @@ hipError_t launch_maxpool(const void* x, void* y, int N, int H, int W, int Cs, i
 // The order is fixed, so results are deterministic; sums are fp32.
 constexpr int kReduceThreads = 256;
 
+// With channel segments (ReduceSegs) each of a thread's 8 channels stops at its own
+// position count: positions below the smallest of the 8 counts fold unmasked, the
+// few above it channel by channel.
 __global__ __launch_bounds__(kReduceThreads) void spatial_reduce_kernel(const void* __restrict__ x, void* y, int HW,
-                                                                        int Cs, int GB, int is_max, int bf16) {
+                                                                        int Cs, int GB, int is_max, int bf16,
+                                                                        ReduceSegs sg) {
   __shared__ float part[kReduceThreads * 8];
   const int G = Cs / 8, P = kReduceThreads / GB;
   const int t = threadIdx.x, gl = t % GB, sl = t / GB;
   const int g = blockIdx.y * GB + gl;
   const long long n = blockIdx.x;
   const float init = is_max ? -INFINITY : 0.f;
+  int lim[8];
+  int lo = HW, hi = HW;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    lim[j] = HW;
+    for (int i = 0; i < sg.n; ++i)
+      if (g * 8 + j < sg.end[i]) {
+        lim[j] = sg.len[i];
+        break;
+      }
+    lo = min(lo, lim[j]);
+    hi = max(hi, lim[j]);
+  }
   float acc[8];
 #pragma unroll
   for (int j = 0; j < 8; ++j) acc[j] = init;
@@ -161,7 +178,7 @@ __global__ __launch_bounds__(kReduceThreads) void spatial_reduce_kernel(const vo
   if (sl < P && g < G) {
     const long long base = n * HW * Cs + g * 8;
     int p = sl;
-    for (; p + 3 * P < HW; p += 4 * P) {
+    for (; p + 3 * P < lo; p += 4 * P) {
       float q0[8], q1[8], q2[8], q3[8];
       load8_stream(x, base + (long long)p * Cs, bf16, q0);
       load8_stream(x, base + (long long)(p + P) * Cs, bf16, q1);
@@ -169,10 +186,17 @@ __global__ __launch_bounds__(kReduceThreads) void spatial_reduce_kernel(const vo
       load8_stream(x, base + (long long)(p + 3 * P) * Cs, bf16, q3);
       fold(q0); fold(q1); fold(q2); fold(q3);
     }
-    for (; p < HW; p += P) {
+    for (; p < lo; p += P) {
       float q[8];
       load8_stream(x, base + (long long)p * Cs, bf16, q);
       fold(q);
+    }
+    for (; p < hi; p += P) {
+      float q[8];
+      load8_stream(x, base + (long long)p * Cs, bf16, q);
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        if (p < lim[j]) acc[j] = is_max ? fmaxf(acc[j], q[j]) : acc[j] + q[j];
     }
   }
 #pragma unroll
@@ -186,19 +210,26 @@ __global__ __launch_bounds__(kReduceThreads) void spatial_reduce_kernel(const vo
     fold(q);
   }
   if (!is_max) {
-    const float inv = 1.0f / (float)HW;
 #pragma unroll
-    for (int j = 0; j < 8; ++j) acc[j] = acc[j] * inv;
+    for (int j = 0; j < 8; ++j) acc[j] = acc[j] * (1.0f / (float)lim[j]);
   }
   store8(y, n * Cs + g * 8, bf16, acc);
 }
 
 hipError_t launch_spatial_reduce(const void* x, void* y, int N, int HW, int Cs, int is_max, int bf16,
-                                 hipStream_t s) {
+                                 hipStream_t s, const ReduceSegs* segs) {
+  ReduceSegs sg{};
+  if (segs) {
+    if (segs->n < 0 || segs->n > kMaxReduceSegs) return hipErrorInvalidValue;
+    for (int i = 0; i < segs->n; ++i)
+      if (segs->len[i] < 1 || segs->len[i] > HW || (i > 0 && segs->end[i] <= segs->end[i - 1]))
+        return hipErrorInvalidValue;
+    sg = *segs;
+  }
   const int G = Cs / 8;
   const int GB = G < 64 ? G : 64;
   const dim3 grid((unsigned)N, (unsigned)((G + GB - 1) / GB));
-  launch(spatial_reduce_kernel, grid, dim3(kReduceThreads), s, x, y, HW, Cs, GB, is_max, bf16);
+  launch(spatial_reduce_kernel, grid, dim3(kReduceThreads), s, x, y, HW, Cs, GB, is_max, bf16, sg);
   return hipGetLastError();
 }
 

@@ -76,6 +76,10 @@ struct Op {
   int pool2 = 0;
   // conv1d: pre-max scratch [n][T][Cs_out] in the arena
   size_t tmp_off = 0;
+  // conv1d running several fused branches (nseg > 0): branch i owns output channels
+  // [seg_end[i - 1], seg_end[i]) and has a kernel of seg_kw[i] taps
+  int nseg = 0;
+  int seg_end[kMaxReduceSegs] = {}, seg_kw[kMaxReduceSegs] = {};
   // concat
   int ca = 0, cb = 0;
 };
@@ -175,6 +179,7 @@ struct rafiki_ensemble_s {
   std::map<std::pair<int, uint32_t>, Sched> schedule;
   bool tune_schedule = true;
   bool autotune = true;
+  bool fuse_branches = true;        // fuse sibling max-over-time convolutions (bf16)
   int force_tile = -1;              // diagnostic override of the tuned configuration
   // Forward passes replayed as HIP graphs, one per (batch size, model subset): every
   // kernel argument inside them (weights, arenas, staged input, logits workspace,
@@ -290,8 +295,7 @@ int upload_weights(rafiki_ensemble_s* e, Op& op, const std::vector<float>& packe
 
 // Fold inference batch-norm and bias: y = s * conv + t, s = gamma / sqrt(var + eps),
 // t = beta - mean * s + s * bias, evaluated in fp64 and rounded once to fp32.
-int upload_fold(rafiki_ensemble_s* e, Op& op, const rafiki_layer& L) {
-  std::vector<float> s(op.Co_pad, 0.f), t(op.Co_pad, 0.f);
+void fold_into(const rafiki_layer& L, float* s, float* t) {
   const bool bn = L.bn_gamma != nullptr;
   for (int c = 0; c < L.c_out; ++c) {
     const double b = L.bias ? (double)L.bias[c] : 0.0;
@@ -304,6 +308,17 @@ int upload_fold(rafiki_ensemble_s* e, Op& op, const rafiki_layer& L) {
       t[c] = (float)b;
     }
   }
+}
+
+int upload_fold(rafiki_ensemble_s* e, Op& op, const std::vector<float>& s, const std::vector<float>& t) {
+  int rc = upload(e, (void**)&op.d_scale, s.data(), s.size() * 4);
+  if (rc) return rc;
+  return upload(e, (void**)&op.d_shift, t.data(), t.size() * 4);
+}
+
+int upload_fold(rafiki_ensemble_s* e, Op& op, const rafiki_layer& L) {
+  std::vector<float> s(op.Co_pad, 0.f), t(op.Co_pad, 0.f);
+  fold_into(L, s.data(), t.data());
   int rc = upload(e, (void**)&op.d_scale, s.data(), s.size() * 4);
   if (rc) return rc;
   return upload(e, (void**)&op.d_shift, t.data(), t.size() * 4);
@@ -320,6 +335,131 @@ int storage_channels(int c, bool bf16) {
 
 std::string lname(int m, int i) { return "model " + std::to_string(m) + " layer " + std::to_string(i) + ": "; }
 
+// Branches of a model that run as one GEMM: max-over-time convolutions reading one
+// sequence whose outputs meet only in a tree of concatenations (the TextCNN's kernel
+// widths 3, 4 and 5, joined in order).  The branches' filters become the rows of one
+// weight matrix over the widest kernel's taps, a narrower branch's missing taps holding
+// zero weights; past the end of the sequence the GEMM reads the hardware's zeros, so
+// it can run over the positions of the narrowest branch.  Every output sums its own
+// products in its own K order with only exact zero products added, so each value is
+// bitwise that of its separate branch.  The max over time then reduces each branch's
+// channels over that branch's W - kw + 1 positions and writes the concatenated vector
+// directly: the concatenations disappear.
+struct BranchGroup {
+  int root = -1;                  // the outermost concatenation
+  std::vector<int> branches;      // convolution layers, in channel order
+  std::vector<int> concats;       // the concatenations inside the tree
+};
+
+void branch_leaves(const rafiki_model_desc& md, const std::vector<int>& readers, int t, BranchGroup& g, bool& ok) {
+  const rafiki_layer& L = md.layers[t];
+  for (int src : {L.input, L.input2}) {
+    if (src < 0 || src >= t) {
+      ok = false;
+      return;
+    }
+    if (md.layers[src].op == RAFIKI_OP_CONCAT && readers[src] == 1) {
+      g.concats.push_back(src);
+      branch_leaves(md, readers, src, g, ok);
+      if (!ok) return;
+    } else {
+      g.branches.push_back(src);
+    }
+  }
+}
+
+std::vector<BranchGroup> find_branch_groups(const rafiki_model_desc& md) {
+  const int nl = md.n_layers;
+  std::vector<int> readers(nl, 0), reader(nl, -1);
+  for (int i = 0; i < nl; ++i)
+    for (int src : {md.layers[i].input, md.layers[i].input2})
+      if (src >= 0 && src < i) {
+        ++readers[src];
+        reader[src] = i;
+      }
+  std::vector<BranchGroup> groups;
+  for (int r = 0; r < nl; ++r) {
+    if (md.layers[r].op != RAFIKI_OP_CONCAT) continue;
+    if (readers[r] == 1 && md.layers[reader[r]].op == RAFIKI_OP_CONCAT) continue;   // inside a larger tree
+    BranchGroup g;
+    g.root = r;
+    bool ok = true;
+    branch_leaves(md, readers, r, g, ok);
+    if (!ok || g.branches.size() < 2 || g.branches.size() > (size_t)kMaxReduceSegs) continue;
+    const rafiki_layer& b0 = md.layers[g.branches[0]];
+    for (int b : g.branches) {
+      const rafiki_layer& L = md.layers[b];
+      ok = ok && L.op == RAFIKI_OP_CONV1D_MAXTIME && readers[b] == 1 && L.input == b0.input &&
+           L.c_in == b0.c_in && (L.relu != 0) == (b0.relu != 0) && L.weight && L.kw >= 1;
+    }
+    if (ok) groups.push_back(std::move(g));
+  }
+  return groups;
+}
+
+// Replace each group's branch convolutions and concatenations by one conv1d op that
+// writes the group's root tensor; packs and uploads its weights and folded scale and
+// shift unless the handle is in its validation pass.
+int fuse_branches(rafiki_ensemble_s* e, const rafiki_model_desc& md, Model& M, const std::vector<BranchGroup>& groups) {
+  std::vector<int> group_of(M.ops.size(), -1);
+  std::vector<Op> fused(groups.size());
+  for (size_t gi = 0; gi < groups.size(); ++gi) {
+    const BranchGroup& g = groups[gi];
+    group_of[g.root] = (int)gi;
+    for (int t : g.branches) group_of[t] = (int)gi;
+    for (int t : g.concats) group_of[t] = (int)gi;
+    Op m = M.ops[g.branches[0]];
+    m.out = g.root;
+    m.nseg = (int)g.branches.size();
+    int kw_max = 0, kw_min = 1 << 30, c = 0;
+    for (int i = 0; i < m.nseg; ++i) {
+      const Op& b = M.ops[g.branches[i]];
+      kw_max = std::max(kw_max, b.kw);
+      kw_min = std::min(kw_min, b.kw);
+      c += b.c_out;
+      m.seg_end[i] = c;
+      m.seg_kw[i] = b.kw;
+    }
+    if (c != M.tensors[g.root].c) return fail(RAFIKI_ERR_INVALID, "internal: fused branch channels");
+    m.kw = kw_max; m.Wo = m.W - kw_min + 1; m.c_out = c;
+    m.K = kw_max * m.Cs_in;
+    m.Co_pad = round_up(c, kCoPadBf16);
+    m.Kp = round_up(m.K, 64);
+    m.d_w = nullptr; m.d_scale = nullptr; m.d_shift = nullptr;
+    if (!e->dry) {
+      // K order as pack_weight's over kw_max taps: (channel block of 64, tap, channel)
+      // when aligned, else (tap, channel)
+      const bool aligned = m.Cs_in % 64 == 0;
+      std::vector<float> packed((size_t)m.Co_pad * m.Kp, 0.f), sc(m.Co_pad, 0.f), sh(m.Co_pad, 0.f);
+      int o = 0;
+      for (int i = 0; i < m.nseg; ++i) {
+        const rafiki_layer& L = md.layers[g.branches[i]];
+        const int cin = L.c_in, kw = L.kw;
+        for (int co = 0; co < L.c_out; ++co)
+          for (int v = 0; v < kw; ++v)
+            for (int ci = 0; ci < cin; ++ci) {
+              const size_t k = aligned ? ((size_t)(ci / 64) * kw_max + v) * 64 + ci % 64 : (size_t)v * m.Cs_in + ci;
+              packed[(size_t)(o + co) * m.Kp + k] = L.weight[((size_t)co * cin + ci) * kw + v];
+            }
+        fold_into(L, sc.data() + o, sh.data() + o);
+        o += L.c_out;
+      }
+      int rc = upload_weights(e, m, packed);
+      if (!rc) rc = upload_fold(e, m, sc, sh);
+      if (rc) return rc;
+    }
+    fused[gi] = m;
+  }
+  std::vector<Op> ops;
+  for (const Op& op : M.ops) {
+    const int gi = op.out >= 0 && op.out < (int)group_of.size() ? group_of[op.out] : -1;
+    if (gi < 0) ops.push_back(op);
+    else if (op.out == groups[gi].root) ops.push_back(fused[gi]);
+  }
+  M.ops.swap(ops);
+  return RAFIKI_OK;
+}
+
 // Validate one model, infer shapes, build its ops and upload its parameters.
 int build_model(rafiki_ensemble_s* e, int mi, const rafiki_model_desc& md, Model& M) {
   if (md.n_layers < 1 || !md.layers) return fail(RAFIKI_ERR_INVALID, "model " + std::to_string(mi) + ": no layers");
@@ -333,6 +473,11 @@ int build_model(rafiki_ensemble_s* e, int mi, const rafiki_model_desc& md, Model
   const bool bf = e->precision == RAFIKI_BF16;
   auto tin = [&](int id) -> const Tensor& { return id < 0 ? in : M.tensors[id]; };
   M.tensors.resize(md.n_layers);
+  const std::vector<BranchGroup> groups =
+      bf && e->fuse_branches ? find_branch_groups(md) : std::vector<BranchGroup>();
+  std::vector<char> in_group(md.n_layers, 0);
+  for (const BranchGroup& g : groups)
+    for (int b : g.branches) in_group[b] = 1;
   for (int i = 0; i < md.n_layers; ++i) {
     const rafiki_layer& L = md.layers[i];
     const std::string ln = lname(mi, i);
@@ -450,7 +595,7 @@ int build_model(rafiki_ensemble_s* e, int mi, const rafiki_model_desc& md, Model
         op.K = L.kw * x.Cs;
         op.Co_pad = bf ? round_up(L.c_out, kCoPadBf16) : round_up(L.c_out, 32);
         op.Kp = bf ? round_up(op.K, 64) : op.K;
-        if (e->dry) break;
+        if (e->dry || in_group[i]) break;   // a fused branch: packed with its group below
         const int cin = L.c_in, kw = L.kw;
         auto packed = pack_weight(L.c_out, cin, 1, kw, x.Cs, op.Co_pad, op.Kp,
                                   [=](int co, int ci, int, int v) { return ((size_t)co * cin + ci) * kw + v; },
@@ -484,6 +629,10 @@ int build_model(rafiki_ensemble_s* e, int mi, const rafiki_model_desc& md, Model
   if (last.op != RAFIKI_OP_FC || last.c_out != md.n_classes)
     return fail(RAFIKI_ERR_INVALID, "model " + std::to_string(mi) + ": the last layer must be an FC with n_classes outputs");
   M.tensors.back().is_logits = true;
+  if (!groups.empty()) {
+    int rc = fuse_branches(e, md, M, groups);
+    if (rc) return rc;
+  }
 
   // A 2x2 stride-2 max-pool whose input is a bf16 conv output read by nothing else is
   // fused into that conv: its epilogue writes the pooled tensor, and the full-size conv
@@ -627,10 +776,20 @@ TraceTile& trace_tile() {
 int run_gemm(const rafiki_ensemble_s* e, const Op& op, ConvArgs a, hipStream_t s, int mi, int li, int cfg) {
   const double es = (double)e->esz();
   const double kalg = (double)op.kh * op.kw * op.cin_l;
-  const double flops = 2.0 * a.M * op.c_out * kalg;
+  double flops = 2.0 * a.M * op.c_out * kalg;
+  double w_elems = (double)op.c_out * kalg;
+  if (op.nseg > 0) {   // fused branches: each branch's own positions and taps
+    flops = 0.0;
+    w_elems = 0.0;
+    for (int i = 0; i < op.nseg; ++i) {
+      const double ci = (double)(op.seg_end[i] - (i ? op.seg_end[i - 1] : 0)) * op.seg_kw[i] * op.cin_l;
+      flops += 2.0 * a.N * (op.W - op.seg_kw[i] + 1) * ci;
+      w_elems += ci;
+    }
+  }
   const double in_elems = (double)a.N * a.H * a.W * op.cin_l;   // FC: H = W = 1, cin_l = flattened size
   const double out_rows = a.pool2 ? a.M / 4.0 : (double)a.M;
-  const double bytes = in_elems * es + (double)op.c_out * kalg * es +
+  const double bytes = in_elems * es + w_elems * es +
                        out_rows * op.c_out * (a.out_f32 ? 4.0 : es) * (a.res ? 2.0 : 1.0);
   if (e->precision != RAFIKI_BF16) {
     TRACED(e, s, RAFIKI_K_CONV_F32, mi, li, flops, bytes, launch_conv_f32(a, s));
@@ -812,8 +971,19 @@ int run_model(const rafiki_ensemble_s* e, int mi, const void* in, int n, float* 
           a.y = tmp; a.c_write = round_up(op.c_out, 8); a.ldy = a.c_write; a.out_f32 = bf ? 0 : 1;
           int rc = run_gemm(e, op, a, s, mi, li, cfg);
           if (rc) return rc;
-          TRACED(e, s, RAFIKI_K_POOL, mi, li, 0.0, (double)n * op.Wo * op.c_out * es + (double)n * op.c_out * es,
-                 launch_spatial_reduce(tmp, yp, n, op.Wo, y.Cs, 1, bf, s));
+          ReduceSegs segs{};
+          double rows = (double)op.Wo * op.c_out;   // pre-max values read per request
+          if (op.nseg > 0) {
+            segs.n = op.nseg;
+            rows = 0.0;
+            for (int i = 0; i < op.nseg; ++i) {
+              segs.end[i] = op.seg_end[i];
+              segs.len[i] = op.W - op.seg_kw[i] + 1;
+              rows += (double)segs.len[i] * (op.seg_end[i] - (i ? op.seg_end[i - 1] : 0));
+            }
+          }
+          TRACED(e, s, RAFIKI_K_POOL, mi, li, 0.0, (double)n * rows * es + (double)n * op.c_out * es,
+                 launch_spatial_reduce(tmp, yp, n, op.Wo, y.Cs, 1, bf, s, op.nseg > 0 ? &segs : nullptr));
           break;
         }
         a.y = yp;
@@ -908,6 +1078,7 @@ int rafiki_ensemble_create(const rafiki_model_desc* models, int n_models, const 
   if (const char* t = std::getenv("RAFIKI_MODEL_STREAMS")) e->concurrent = std::atoi(t) != 0;
   if (const char* t = std::getenv("RAFIKI_GRAPHS")) e->use_graphs = std::atoi(t) != 0;
   if (const char* t = std::getenv("RAFIKI_SCHEDULE_TUNING")) e->tune_schedule = std::atoi(t) != 0;
+  if (const char* t = std::getenv("RAFIKI_FUSE_BRANCHES")) e->fuse_branches = std::atoi(t) != 0;
   // Pass 1: validate every model and infer shapes without touching the device.
   e->dry = true;
   e->models.resize(n_models);

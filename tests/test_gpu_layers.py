@@ -160,3 +160,67 @@ def test_textcnn_long_sequence():
     ref = oracle.run_model(spec, params, tok, act="bf16")
     err = np.abs(z - ref).max() / np.abs(ref).max()
     assert err <= 1e-2, err
+
+
+def _branch_probe(dim, seq_len, filters, widths, vocab=97, extra_reader=False, seed=11):
+    """Embedding, conv1d max-over-time branches of the given widths and filter
+    counts, their concatenation in order, then the identity FC: the logits are the
+    concatenated feature vector.  With extra_reader, the first branch is also
+    concatenated a second time, so that it has two readers and must not be fused."""
+    L = [Layer(op=EMBEDDING, input=-1, c_in=vocab, c_out=dim)]
+    feats = []
+    for f, w in zip(filters, widths):
+        L.append(Layer(op=CONV1D_MAXTIME, input=0, c_in=dim, c_out=f, kh=1, kw=w, relu=True, bias=True))
+        feats.append(len(L) - 1)
+    x, c = feats[0], filters[0]
+    for fi, f in zip(feats[1:], filters[1:]):
+        L.append(Layer(op=CONCAT, input=x, input2=fi, c_in=c, c_out=c + f))
+        x, c = len(L) - 1, c + f
+    if extra_reader:
+        L.append(Layer(op=CONCAT, input=x, input2=feats[0], c_in=c, c_out=c + filters[0]))
+        c += filters[0]
+    spec, params = probe(L, (seq_len,), c, seed=seed, vocab=vocab)
+    for Lr, P in zip(spec.layers, params.layers):
+        if Lr.bias and Lr.op == CONV1D_MAXTIME:
+            P.bias = np.linspace(-0.3, 0.2, Lr.c_out).astype(np.float32)
+    return spec, params
+
+
+@pytest.mark.parametrize("case", [
+    dict(dim=300, seq_len=256, filters=(100, 100, 100), widths=(3, 4, 5)),   # the TextCNN shape (aligned K)
+    dict(dim=70, seq_len=40, filters=(13, 21, 6), widths=(5, 2, 3)),         # unaligned K, ragged segments
+    dict(dim=24, seq_len=9, filters=(8, 16), widths=(9, 1)),                 # a branch as wide as the sequence
+    dict(dim=24, seq_len=30, filters=(5, 7, 9), widths=(2, 3, 4), extra_reader=True),   # not fusable
+])
+def test_fused_branches_bitwise(case, monkeypatch):
+    """Sibling max-over-time convolutions joined by concatenation run as one GEMM and
+    one segmented max: the feature vector is bitwise that of the separate branches
+    (RAFIKI_FUSE_BRANCHES=0) and within one bf16 step of the oracle's."""
+    spec, params = _branch_probe(**case)
+    tok = wl.gen_tokens(7, case["seq_len"], 97, seed=3)
+
+    def run():
+        n = tok.shape[0]
+        with Ensemble([spec], [params], precision="bf16", max_batch=n) as ens:
+            x = torch.from_numpy(tok).to(DEV)
+            out = torch.empty((n, spec.n_classes), dtype=torch.float32, device=DEV)
+            ens.trace(True)
+            ens.model_logits(0, x, n, out)
+            torch.cuda.synchronize()
+            kinds = [r["kind"] for r in ens.trace_read()]
+            return out.cpu().numpy(), kinds
+
+    fused, kf = run()
+    monkeypatch.setenv("RAFIKI_FUSE_BRANCHES", "0")
+    separate, ks = run()
+    nb = len(case["widths"])
+    assert ks.count("concat") == nb - 1 + (1 if case.get("extra_reader") else 0)
+    assert ks.count("pool") == nb
+    if case.get("extra_reader"):
+        assert kf == ks
+    else:
+        assert kf.count("concat") == 0 and kf.count("pool") == 1
+        assert kf.count("conv_mfma") == ks.count("conv_mfma") - (nb - 1)
+    assert np.array_equal(fused.view(np.uint32), separate.view(np.uint32))
+    ref = oracle.run_model(spec, params, tok, act="bf16")
+    check_bf16_tensor(fused, ref)
