@@ -63,9 +63,11 @@ __device__ __forceinline__ int swz(int r) {
 // one half of such a block).  The taps of one channel block are consecutive tiles:
 // they re-read the same input rows while those are still in L2.  Tap, channel block
 // and half are wave-uniform and advanced incrementally; per row only the
-// image-bounds test and one add remain.  Otherwise (Cs % 64 != 0) K is ordered
+// image-bounds test and one add remain.  A tile of fused conv1d branches runs only
+// the first `taps` taps of each channel block; its weight K tile then follows the
+// packed stride of tap_stride taps per block.  Otherwise (Cs % 64 != 0) K is ordered
 // (tap, channel) and each lane decodes its own (u, v, ci) with multiply-high division.
-template <int BM, int BN, int NW, bool ALIGNED, int KC>
+template <int BM, int BN, int NW, bool ALIGNED, int KC, bool TL>
 struct Loader {
   static constexpr int ROWS = 64 / KC;
   static constexpr int SUBS = 8 / KC;      // K tiles per 64-channel block
@@ -80,10 +82,14 @@ struct Loader {
   int a_off[RA];                       // aligned path: byte offset of (hi0, wi0, chunk) (may be virtual)
   unsigned b_off[RB];
   int nu, nv, ntap, ncb, nsub;         // aligned path: tap (u, v, index), channel block, half of the next tile
+  int taps, tstride;                   // TL: taps run per channel block; taps packed per block
 
-  __device__ __forceinline__ void init(const ConvArgs& a, int m0, int n0, int wave_, int lane, int kt_begin_) {
+  __device__ __forceinline__ void init(const ConvArgs& a, int m0, int n0, int wave_, int lane, int kt_begin_,
+                                       int taps_) {
     wave = wave_;
     kt_begin = kt_begin_;
+    taps = TL ? taps_ : a.kh * a.kw;
+    tstride = TL ? a.tap_stride : 0;
     const int lrow = lane / KC;
     chunk = KC == 8 ? ((lane & 7) ^ lrow ^ (wave & 1)) : ((lane & 3) ^ (lane >> 4));
     xr = __builtin_amdgcn_make_buffer_rsrc((void*)a.x, (short)0, a.x_bytes, 0x00020000);
@@ -121,7 +127,6 @@ struct Loader {
     for (int j = 0; j < RB; ++j)
       b_off[j] = (unsigned)(((n0 + (j * NW + wave) * ROWS + lrow) * a.Kp + chunk * 8) * 2);
     if (ALIGNED) {
-      const int taps = a.kh * a.kw;
       const int blk = kt_begin / SUBS;
       nsub = kt_begin - blk * SUBS;
       ncb = blk / taps;
@@ -140,6 +145,8 @@ struct Loader {
   __device__ __forceinline__ void issue(const ConvArgs& a, uint4* lds, int kt, int stage) {
     const int gk = kt_begin + kt;
     uint4* sbase = lds + stage * STAGE_CHUNKS;
+    // K tile of the packed weights: gk itself unless taps are skipped
+    const int kw_tile = TL ? (ncb * tstride + ntap) * SUBS + nsub : gk;
     if (ALIGNED) {
       const bool kvalid = gk * (8 * KC) < a.K;   // tiles past K (padding to Kp) read zeros
       const int delta = ((nu * a.W + nv) * a.Cs + ncb * 64 + nsub * (8 * KC)) * 2;
@@ -152,7 +159,7 @@ struct Loader {
       }
       if (P == NP - 1 && ++nsub == SUBS) {
         nsub = 0;
-        if (++ntap == a.kh * a.kw) {
+        if (++ntap == (TL ? taps : a.kh * a.kw)) {
           ntap = 0; nu = 0; nv = 0; ++ncb;
         } else if (++nv == a.kw) {
           nv = 0; ++nu;
@@ -176,7 +183,7 @@ struct Loader {
 #pragma unroll
     for (int j = P; j < RB; j += NP)
       __builtin_amdgcn_raw_ptr_buffer_load_lds(wr, (lds_void*)(sbase + BM * KC + (j * NW + wave) * 64), 16,
-                                               b_off[j], gk * (KC * 16), 0, 0);
+                                               b_off[j], kw_tile * (KC * 16), 0, 0);
   }
 };
 
@@ -195,14 +202,18 @@ __device__ __forceinline__ void wait_tiles(int n) {
 }
 
 // OCC > 0: registers are limited so that OCC waves fit on each SIMD (more workgroups
-// per CU, at the risk of spills).
-template <int BM, int BN, int WM, int WN, int STAGES, bool ALIGNED, int KC, bool SPLIT, bool SPREAD, int OCC>
+// per CU, at the risk of spills).  TAPS: the variant for fused conv1d branches
+// (tap_stride > 0, aligned K order only), compiled apart so that the other launches
+// keep their own code.
+template <int BM, int BN, int WM, int WN, int STAGES, bool ALIGNED, int KC, bool SPLIT, bool SPREAD, int OCC,
+          bool TAPS = false>
 __global__ __launch_bounds__(WM * WN * 64, OCC > 0 ? OCC : 1) void conv_mfma_kernel(ConvArgs a) {
   constexpr int NW = WM * WN;
   constexpr int WTM = BM / WM, WTN = BN / WN;      // wave tile: pixels x channels
   constexpr int TM = WTM / 32, TN = WTN / 32;
   constexpr int KS = KC / 2;                       // MFMA k-steps of 16 per K tile
-  using LoaderT = Loader<BM, BN, NW, ALIGNED, KC>;
+  constexpr bool TL = ALIGNED && TAPS;
+  using LoaderT = Loader<BM, BN, NW, ALIGNED, KC, TL>;
   constexpr int PER = LoaderT::RA + LoaderT::RB;   // load instructions per thread per tile
   constexpr int STAGE_CHUNKS = (BM + BN) * KC;     // 16-byte chunks per stage
   static_assert(TM >= 1 && TN >= 1 && LoaderT::RA >= 1 && LoaderT::RB >= 1, "tile shape");
@@ -231,13 +242,21 @@ __global__ __launch_bounds__(WM * WN * 64, OCC > 0 ? OCC : 1) void conv_mfma_ker
   // K tiles that hold any of the K real terms (Kp may pad K by up to 63 with zeros, a
   // whole 32-wide tile of them when KC = 4); skipping a tile of zero products leaves
   // every sum unchanged, bit for bit
-  const int ktiles = (a.K + 8 * KC - 1) / (8 * KC);
-  const int kps = a.kt_per_split * (8 / KC);      // kt_per_split counts 64-wide tiles
+  // With fused branches (TL) a tile runs the taps of its widest rows.
+  int taps = 0;
+  if constexpr (TL) {
+    taps = 1;
+    for (int b = n0 / 64; b <= (n0 + BN - 1) / 64 && b < 16; ++b) taps = max(taps, (int)a.taps_by_block[b]);
+  }
+  const int ktiles = TL ? (a.Cs / 64) * taps * (8 / KC) : (a.K + 8 * KC - 1) / (8 * KC);
+  // kt_per_split counts 64-wide tiles, or with fused branches whole channel blocks (of
+  // `taps` tiles each), so that a row's products split the same way in every tile
+  const int kps = a.kt_per_split * (8 / KC) * (TL ? taps : 1);
   const int kt_begin = blockIdx.y * kps;
   const int nk = min(kps, ktiles - kt_begin);
 
   LoaderT ld;
-  ld.init(a, m0, n0, wave, lane, kt_begin);
+  ld.init(a, m0, n0, wave, lane, kt_begin, taps);
 
   f32x16 acc[TN][TM];
 #pragma unroll
@@ -475,7 +494,13 @@ static hipError_t launch_mfma_cfg(const ConvArgs& a, int splits, hipStream_t s) 
   const int m_tiles = (a.M + BM - 1) / BM;
   dim3 grid(m_tiles * b.n_tiles, splits);
   const dim3 block(WM * WN * 64);
-  if (splits > 1) {
+  if (a.tap_stride > 0) {   // fused branches: aligned K order only
+    if (a.Cs % 64 != 0) return hipErrorInvalidValue;
+    if (splits > 1)
+      launch((conv_mfma_kernel<BM, BN, WM, WN, STAGES, true, KC, true, SP, OC, true>), grid, block, s, b);
+    else
+      launch((conv_mfma_kernel<BM, BN, WM, WN, STAGES, true, KC, false, SP, OC, true>), grid, block, s, b);
+  } else if (splits > 1) {
     if (a.Cs % 64 == 0)
       launch((conv_mfma_kernel<BM, BN, WM, WN, STAGES, true, KC, true, SP, OC>), grid, block, s, b);
     else
@@ -604,7 +629,9 @@ const MfmaConfig kMfmaConfigs[kNumMfmaConfigs] = {RAFIKI_MFMA_CONFIGS(RAFIKI_CFG
   template __global__ void conv_mfma_kernel<BM, BN, WM, WN, ST, true, KC, false, SP, OC>(ConvArgs);  \
   template __global__ void conv_mfma_kernel<BM, BN, WM, WN, ST, false, KC, false, SP, OC>(ConvArgs); \
   template __global__ void conv_mfma_kernel<BM, BN, WM, WN, ST, true, KC, true, SP, OC>(ConvArgs);   \
-  template __global__ void conv_mfma_kernel<BM, BN, WM, WN, ST, false, KC, true, SP, OC>(ConvArgs);
+  template __global__ void conv_mfma_kernel<BM, BN, WM, WN, ST, false, KC, true, SP, OC>(ConvArgs);  \
+  template __global__ void conv_mfma_kernel<BM, BN, WM, WN, ST, true, KC, false, SP, OC, true>(ConvArgs); \
+  template __global__ void conv_mfma_kernel<BM, BN, WM, WN, ST, true, KC, true, SP, OC, true>(ConvArgs);
 RAFIKI_MFMA_CONFIGS(RAFIKI_INSTANTIATE)
 #undef RAFIKI_INSTANTIATE
 

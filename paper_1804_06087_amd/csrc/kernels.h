@@ -58,6 +58,12 @@ struct ConvArgs {
   int Cs8, K8;          // Cs / 8, K / 8
   unsigned mag_cs8;     // floor(x / Cs8) = umulhi(x, mag_cs8) (0 when Cs8 == 1)
   unsigned mag_kw;      // floor(x / kw)  = umulhi(x, mag_kw)  (0 when kw == 1)
+  // Fused conv1d branches (aligned K order only; 0: off): every weight row is packed
+  // over tap_stride taps per 64-channel block, but the rows of 64-row block b use only
+  // their first taps_by_block[b] taps.  A tile runs the largest count over its rows and
+  // skips the K tiles of the other taps, whose weights are all zero.
+  int tap_stride;
+  unsigned char taps_by_block[16];
 };
 
 // Direct-to-LDS pipelined bf16 MFMA kernel; cfg selects the tile configuration
@@ -76,14 +82,15 @@ hipError_t launch_stage_images(const float* x, void* y, int N, int C, int H, int
 // Max-pool k x k / stride / pad over NHWC (Cs channels).
 hipError_t launch_maxpool(const void* x, void* y, int N, int H, int W, int Cs, int Ho, int Wo, int k,
                           int stride, int pad, int bf16, hipStream_t s);
-// Channel segments of a reduction whose channels cover different numbers of
-// positions: channels [end[i-1], end[i]) (end[-1] = 0) reduce over their first len[i]
-// positions; channels at or past end[n - 1] over all HW.  n = 0: every channel over HW.
+// Branches of a fused conv1d in the max/mean over positions: branch i occupies input
+// channels [src[i], src[i] + cnt[i]), reduces them over its first len[i] positions and
+// writes output channels [dst[i], dst[i] + cnt[i]) of rows ldy wide; output channels
+// zero_from .. ldy - 1 are set to zero; input channels in no branch are not written.
+// n = 0: every channel over all positions, the output laid out as the input.
 constexpr int kMaxReduceSegs = 8;
 struct ReduceSegs {
-  int n;
-  int end[kMaxReduceSegs];
-  int len[kMaxReduceSegs];
+  int n, ldy, zero_from;
+  int src[kMaxReduceSegs], dst[kMaxReduceSegs], cnt[kMaxReduceSegs], len[kMaxReduceSegs];
 };
 // Global average pool NHWC [N][HW][Cs] -> [N][Cs]; also max over time when is_max.
 hipError_t launch_spatial_reduce(const void* x, void* y, int N, int HW, int Cs, int is_max, int bf16,

@@ -143,30 +143,50 @@ hipError_t launch_maxpool(const void* x, void* y, int N, int H, int W, int Cs, i
 // The order is fixed, so results are deterministic; sums are fp32.
 constexpr int kReduceThreads = 256;
 
-// With channel segments (ReduceSegs) each of a thread's 8 channels stops at its own
-// position count: positions below the smallest of the 8 counts fold unmasked, the
-// few above it channel by channel.
-__global__ __launch_bounds__(kReduceThreads) void spatial_reduce_kernel(const void* __restrict__ x, void* y, int HW,
-                                                                        int Cs, int GB, int is_max, int bf16,
-                                                                        ReduceSegs sg) {
-  __shared__ float part[kReduceThreads * 8];
-  const int G = Cs / 8, P = kReduceThreads / GB;
+// With branches (ReduceSegs) each of a thread's 8 channels stops at its own position
+// count: positions below the smallest of the 8 counts fold unmasked, the few above it
+// channel by channel; channels in no branch are not read; results go out one element
+// at a time to the branch's place.  The fused branches' max runs 1024 threads per
+// request (one block per request, long position ranges).
+template <int THREADS>
+__global__ __launch_bounds__(THREADS) void spatial_reduce_kernel(const void* __restrict__ x, void* y, int HW, int Cs,
+                                                                 int GB, int is_max, int bf16, ReduceSegs sg) {
+  __shared__ float part[THREADS * 8];
+  const int G = Cs / 8, P = THREADS / GB;
   const int t = threadIdx.x, gl = t % GB, sl = t / GB;
   const int g = blockIdx.y * GB + gl;
   const long long n = blockIdx.x;
   const float init = is_max ? -INFINITY : 0.f;
-  int lim[8];
+  int lim[8], dst[8];   // positions of each channel; its output channel (-1: none)
   int lo = HW, hi = HW;
+  if (sg.n > 0) {
+    lo = HW;
+    hi = 0;
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    lim[j] = HW;
-    for (int i = 0; i < sg.n; ++i)
-      if (g * 8 + j < sg.end[i]) {
-        lim[j] = sg.len[i];
-        break;
+    for (int j = 0; j < 8; ++j) {
+      const int c = g * 8 + j;
+      lim[j] = 0;
+      dst[j] = -1;
+      for (int i = 0; i < sg.n; ++i)
+        if (c >= sg.src[i] && c < sg.src[i] + sg.cnt[i]) {
+          lim[j] = sg.len[i];
+          dst[j] = sg.dst[i] + (c - sg.src[i]);
+        }
+      if (dst[j] >= 0) {
+        lo = min(lo, lim[j]);
+        hi = max(hi, lim[j]);
       }
-    lo = min(lo, lim[j]);
-    hi = max(hi, lim[j]);
+    }
+    if (hi == 0) lo = 0;   // no channel of this group is in a branch
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      if (dst[j] < 0) lim[j] = lo;
+  } else {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      lim[j] = HW;
+      dst[j] = g * 8 + j;
+    }
   }
   float acc[8];
 #pragma unroll
@@ -201,6 +221,11 @@ __global__ __launch_bounds__(kReduceThreads) void spatial_reduce_kernel(const vo
   }
 #pragma unroll
   for (int j = 0; j < 8; ++j) part[t * 8 + j] = acc[j];
+  if (sg.n > 0 && blockIdx.y == 0)
+    for (int c = sg.zero_from + t; c < sg.ldy; c += THREADS) {
+      if (bf16) ((bf16_t*)y)[n * sg.ldy + c] = 0;
+      else ((float*)y)[n * sg.ldy + c] = 0.f;
+    }
   __syncthreads();
   if (sl != 0 || g >= G) return;
   for (int r = 1; r < P; ++r) {
@@ -213,23 +238,37 @@ __global__ __launch_bounds__(kReduceThreads) void spatial_reduce_kernel(const vo
 #pragma unroll
     for (int j = 0; j < 8; ++j) acc[j] = acc[j] * (1.0f / (float)lim[j]);
   }
-  store8(y, n * Cs + g * 8, bf16, acc);
+  if (sg.n == 0) {
+    store8(y, n * Cs + g * 8, bf16, acc);
+    return;
+  }
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    if (dst[j] < 0) continue;
+    if (bf16) ((bf16_t*)y)[n * sg.ldy + dst[j]] = (bf16_t)f2bf(acc[j]);
+    else ((float*)y)[n * sg.ldy + dst[j]] = acc[j];
+  }
 }
 
 hipError_t launch_spatial_reduce(const void* x, void* y, int N, int HW, int Cs, int is_max, int bf16,
                                  hipStream_t s, const ReduceSegs* segs) {
   ReduceSegs sg{};
   if (segs) {
-    if (segs->n < 0 || segs->n > kMaxReduceSegs) return hipErrorInvalidValue;
+    if (segs->n < 0 || segs->n > kMaxReduceSegs || segs->zero_from < 0 || segs->zero_from > segs->ldy)
+      return hipErrorInvalidValue;
     for (int i = 0; i < segs->n; ++i)
-      if (segs->len[i] < 1 || segs->len[i] > HW || (i > 0 && segs->end[i] <= segs->end[i - 1]))
+      if (segs->len[i] < 1 || segs->len[i] > HW || segs->cnt[i] < 1 || segs->src[i] < 0 ||
+          segs->src[i] + segs->cnt[i] > Cs || segs->dst[i] < 0 || segs->dst[i] + segs->cnt[i] > segs->zero_from)
         return hipErrorInvalidValue;
     sg = *segs;
   }
   const int G = Cs / 8;
   const int GB = G < 64 ? G : 64;
   const dim3 grid((unsigned)N, (unsigned)((G + GB - 1) / GB));
-  launch(spatial_reduce_kernel, grid, dim3(kReduceThreads), s, x, y, HW, Cs, GB, is_max, bf16, sg);
+  if (sg.n > 0)
+    launch(spatial_reduce_kernel<1024>, grid, dim3(1024), s, x, y, HW, Cs, GB, is_max, bf16, sg);
+  else
+    launch(spatial_reduce_kernel<kReduceThreads>, grid, dim3(kReduceThreads), s, x, y, HW, Cs, GB, is_max, bf16, sg);
   return hipGetLastError();
 }
 

@@ -77,9 +77,12 @@ struct Op {
   // conv1d: pre-max scratch [n][T][Cs_out] in the arena
   size_t tmp_off = 0;
   // conv1d running several fused branches (nseg > 0): branch i owns output channels
-  // [seg_end[i - 1], seg_end[i]) and has a kernel of seg_kw[i] taps
+  // [seg_end[i - 1], seg_end[i]), GEMM rows from seg_row[i] on, and has a kernel of
+  // seg_kw[i] taps; tap_stride / taps_by_block as in ConvArgs
   int nseg = 0;
-  int seg_end[kMaxReduceSegs] = {}, seg_kw[kMaxReduceSegs] = {};
+  int seg_end[kMaxReduceSegs] = {}, seg_kw[kMaxReduceSegs] = {}, seg_row[kMaxReduceSegs] = {};
+  int tap_stride = 0;
+  unsigned char taps_by_block[16] = {};
   // concat
   int ca = 0, cb = 0;
 };
@@ -411,7 +414,7 @@ int fuse_branches(rafiki_ensemble_s* e, const rafiki_model_desc& md, Model& M, c
     Op m = M.ops[g.branches[0]];
     m.out = g.root;
     m.nseg = (int)g.branches.size();
-    int kw_max = 0, kw_min = 1 << 30, c = 0;
+    int kw_max = 0, kw_min = 1 << 30, c = 0, rows_dense = 0, rows_64 = 0;
     for (int i = 0; i < m.nseg; ++i) {
       const Op& b = M.ops[g.branches[i]];
       kw_max = std::max(kw_max, b.kw);
@@ -419,22 +422,45 @@ int fuse_branches(rafiki_ensemble_s* e, const rafiki_model_desc& md, Model& M, c
       c += b.c_out;
       m.seg_end[i] = c;
       m.seg_kw[i] = b.kw;
+      rows_dense += b.c_out;
+      rows_64 = round_up(rows_64, 64) + b.c_out;
     }
     if (c != M.tensors[g.root].c) return fail(RAFIKI_ERR_INVALID, "internal: fused branch channels");
-    m.kw = kw_max; m.Wo = m.W - kw_min + 1; m.c_out = c;
+    // With the aligned K order a tile skips the taps its rows lack; branches start on
+    // 64-row blocks when that adds at most a third to the GEMM's rows, so that tiles
+    // seldom mix kernel widths.
+    const bool aligned = m.Cs_in % 64 == 0;
+    const bool pad64 = aligned && 3 * rows_64 <= 4 * rows_dense && round_up(rows_64, 64) <= 16 * 64;
+    int rows = 0;
+    for (int i = 0; i < m.nseg; ++i) {
+      if (pad64) rows = round_up(rows, 64);
+      m.seg_row[i] = rows;
+      rows += m.seg_end[i] - (i ? m.seg_end[i - 1] : 0);
+    }
+    m.kw = kw_max; m.Wo = m.W - kw_min + 1; m.c_out = rows;
     m.K = kw_max * m.Cs_in;
-    m.Co_pad = round_up(c, kCoPadBf16);
+    m.Co_pad = round_up(rows, kCoPadBf16);
     m.Kp = round_up(m.K, 64);
+    m.tap_stride = 0;
+    if (aligned && round_up(rows, 64) <= 16 * 64) {
+      m.tap_stride = kw_max;
+      for (int b = 0; b < 16; ++b) {
+        int t = 1;
+        for (int i = 0; i < m.nseg; ++i) {
+          const int r0 = m.seg_row[i], r1 = r0 + m.seg_end[i] - (i ? m.seg_end[i - 1] : 0);
+          if (r0 < 64 * (b + 1) && r1 > 64 * b) t = std::max(t, m.seg_kw[i]);
+        }
+        m.taps_by_block[b] = (unsigned char)t;
+      }
+    }
     m.d_w = nullptr; m.d_scale = nullptr; m.d_shift = nullptr;
     if (!e->dry) {
       // K order as pack_weight's over kw_max taps: (channel block of 64, tap, channel)
       // when aligned, else (tap, channel)
-      const bool aligned = m.Cs_in % 64 == 0;
       std::vector<float> packed((size_t)m.Co_pad * m.Kp, 0.f), sc(m.Co_pad, 0.f), sh(m.Co_pad, 0.f);
-      int o = 0;
       for (int i = 0; i < m.nseg; ++i) {
         const rafiki_layer& L = md.layers[g.branches[i]];
-        const int cin = L.c_in, kw = L.kw;
+        const int cin = L.c_in, kw = L.kw, o = m.seg_row[i];
         for (int co = 0; co < L.c_out; ++co)
           for (int v = 0; v < kw; ++v)
             for (int ci = 0; ci < cin; ++ci) {
@@ -442,7 +468,6 @@ int fuse_branches(rafiki_ensemble_s* e, const rafiki_model_desc& md, Model& M, c
               packed[(size_t)(o + co) * m.Kp + k] = L.weight[((size_t)co * cin + ci) * kw + v];
             }
         fold_into(L, sc.data() + o, sh.data() + o);
-        o += L.c_out;
       }
       int rc = upload_weights(e, m, packed);
       if (!rc) rc = upload_fold(e, m, sc, sh);
@@ -798,9 +823,16 @@ int run_gemm(const rafiki_ensemble_s* e, const Op& op, ConvArgs a, hipStream_t s
   if ((long long)a.N * a.H * a.W * a.Cs * 2 >= (1LL << 31) || (long long)a.Co_pad * a.Kp * 2 >= (1LL << 31))
     return fail(RAFIKI_ERR_UNSUPPORTED, "a layer's input or weights exceed 2 GiB; use a smaller max_batch");
   const int ktiles = a.Kp / 64;
-  const int splits = choose_splits(a.M, op.c_out, ktiles);
-  if (cfg < 0) cfg = splits > 1 ? split_cfg(op.c_out) : default_cfg(op.c_out);
+  int splits = choose_splits(a.M, op.c_out, ktiles);
   a.kt_per_split = (ktiles + splits - 1) / splits;
+  if (a.tap_stride > 0 && splits > 1) {
+    // fused branches: a split takes whole channel blocks, each with the taps of the
+    // tile, so that every row's products fall into the same splits whatever the tile
+    const int cb = a.Cs / 64, sp = std::min(splits, cb);
+    a.kt_per_split = (cb + sp - 1) / sp;
+    splits = (cb + a.kt_per_split - 1) / a.kt_per_split;
+  }
+  if (cfg < 0) cfg = splits > 1 ? split_cfg(op.c_out) : default_cfg(op.c_out);
   struct TileScope {
     TileScope(int c, int sp) { trace_tile() = {c, sp}; }
     ~TileScope() { trace_tile() = {}; }
@@ -834,6 +866,8 @@ ConvArgs gemm_args(const rafiki_ensemble_s* e, const Model& M, const Op& op, int
   a.w_bytes = (int)((long long)op.Co_pad * op.Kp * (long long)e->esz());
   a.Cs8 = op.Cs_in / 8; a.K8 = op.K / 8;
   a.mag_cs8 = magic_div(op.Cs_in / 8); a.mag_kw = magic_div(op.kw);
+  a.tap_stride = op.tap_stride;
+  for (int b = 0; b < 16; ++b) a.taps_by_block[b] = op.taps_by_block[b];
   return a;
 }
 
@@ -972,18 +1006,22 @@ int run_model(const rafiki_ensemble_s* e, int mi, const void* in, int n, float* 
           int rc = run_gemm(e, op, a, s, mi, li, cfg);
           if (rc) return rc;
           ReduceSegs segs{};
-          double rows = (double)op.Wo * op.c_out;   // pre-max values read per request
+          double vals = (double)op.Wo * op.c_out;   // pre-max values read per request
           if (op.nseg > 0) {
             segs.n = op.nseg;
-            rows = 0.0;
+            segs.ldy = y.Cs;
+            segs.zero_from = y.c;
+            vals = 0.0;
             for (int i = 0; i < op.nseg; ++i) {
-              segs.end[i] = op.seg_end[i];
+              segs.dst[i] = i ? op.seg_end[i - 1] : 0;
+              segs.cnt[i] = op.seg_end[i] - segs.dst[i];
+              segs.src[i] = op.seg_row[i];
               segs.len[i] = op.W - op.seg_kw[i] + 1;
-              rows += (double)segs.len[i] * (op.seg_end[i] - (i ? op.seg_end[i - 1] : 0));
+              vals += (double)segs.len[i] * segs.cnt[i];
             }
           }
-          TRACED(e, s, RAFIKI_K_POOL, mi, li, 0.0, (double)n * rows * es + (double)n * op.c_out * es,
-                 launch_spatial_reduce(tmp, yp, n, op.Wo, y.Cs, 1, bf, s, op.nseg > 0 ? &segs : nullptr));
+          TRACED(e, s, RAFIKI_K_POOL, mi, li, 0.0, (double)n * vals * es + (double)n * y.c * es,
+                 launch_spatial_reduce(tmp, yp, n, op.Wo, a.c_write, 1, bf, s, op.nseg > 0 ? &segs : nullptr));
           break;
         }
         a.y = yp;

@@ -186,36 +186,42 @@ def _branch_probe(dim, seq_len, filters, widths, vocab=97, extra_reader=False, s
     return spec, params
 
 
-@pytest.mark.parametrize("case", [
-    dict(dim=300, seq_len=256, filters=(100, 100, 100), widths=(3, 4, 5)),   # the TextCNN shape (aligned K)
-    dict(dim=70, seq_len=40, filters=(13, 21, 6), widths=(5, 2, 3)),         # unaligned K, ragged segments
-    dict(dim=24, seq_len=9, filters=(8, 16), widths=(9, 1)),                 # a branch as wide as the sequence
-    dict(dim=24, seq_len=30, filters=(5, 7, 9), widths=(2, 3, 4), extra_reader=True),   # not fusable
+def _run_traced(spec, params, tok, cfg=-1):
+    """Logits and traced kernel kinds of one forward pass (cfg >= 0: forced tile)."""
+    n = tok.shape[0]
+    with Ensemble([spec], [params], precision="bf16", max_batch=n) as ens:
+        if cfg >= 0:
+            ens.force_tile(cfg)
+        x = torch.from_numpy(tok).to(DEV)
+        out = torch.empty((n, spec.n_classes), dtype=torch.float32, device=DEV)
+        ens.trace(True)
+        ens.model_logits(0, x, n, out)
+        torch.cuda.synchronize()
+        return out.cpu().numpy(), [r["kind"] for r in ens.trace_read()]
+
+
+# Batches large enough that neither the fused GEMM nor any separate branch splits K
+# (a split sums a row's products in parts, which the two layouts cut differently).
+@pytest.mark.parametrize("n, case", [
+    (72, dict(dim=300, seq_len=256, filters=(100, 100, 100), widths=(3, 4, 5))),  # TextCNN: aligned K, 64-row blocks
+    (384, dict(dim=128, seq_len=50, filters=(70, 90), widths=(2, 6))),           # aligned, tiles mixing widths
+    (570, dict(dim=64, seq_len=33, filters=(13, 21, 6), widths=(5, 2, 3))),      # aligned, one 64-row block
+    (460, dict(dim=70, seq_len=40, filters=(13, 21, 6), widths=(5, 2, 3))),      # unaligned K, ragged segments
+    (7, dict(dim=24, seq_len=30, filters=(5, 7, 9), widths=(2, 3, 4), extra_reader=True)),   # not fusable
 ])
-def test_fused_branches_bitwise(case, monkeypatch):
+def test_fused_branches_bitwise(n, case, monkeypatch):
     """Sibling max-over-time convolutions joined by concatenation run as one GEMM and
     one segmented max: the feature vector is bitwise that of the separate branches
     (RAFIKI_FUSE_BRANCHES=0) and within one bf16 step of the oracle's."""
     spec, params = _branch_probe(**case)
-    tok = wl.gen_tokens(7, case["seq_len"], 97, seed=3)
-
-    def run():
-        n = tok.shape[0]
-        with Ensemble([spec], [params], precision="bf16", max_batch=n) as ens:
-            x = torch.from_numpy(tok).to(DEV)
-            out = torch.empty((n, spec.n_classes), dtype=torch.float32, device=DEV)
-            ens.trace(True)
-            ens.model_logits(0, x, n, out)
-            torch.cuda.synchronize()
-            kinds = [r["kind"] for r in ens.trace_read()]
-            return out.cpu().numpy(), kinds
-
-    fused, kf = run()
+    tok = wl.gen_tokens(n, case["seq_len"], 97, seed=3)
+    fused, kf = _run_traced(spec, params, tok)
     monkeypatch.setenv("RAFIKI_FUSE_BRANCHES", "0")
-    separate, ks = run()
+    separate, ks = _run_traced(spec, params, tok)
     nb = len(case["widths"])
     assert ks.count("concat") == nb - 1 + (1 if case.get("extra_reader") else 0)
     assert ks.count("pool") == nb
+    assert "splitk_reduce" not in ks and "splitk_reduce" not in kf
     if case.get("extra_reader"):
         assert kf == ks
     else:
@@ -224,3 +230,24 @@ def test_fused_branches_bitwise(case, monkeypatch):
     assert np.array_equal(fused.view(np.uint32), separate.view(np.uint32))
     ref = oracle.run_model(spec, params, tok, act="bf16")
     check_bf16_tensor(fused, ref)
+
+
+@pytest.mark.parametrize("n, case", [
+    (7, dict(dim=300, seq_len=256, filters=(100, 100, 100), widths=(3, 4, 5))),
+    (1, dict(dim=300, seq_len=256, filters=(100, 100, 100), widths=(3, 4, 5))),
+    (9, dict(dim=128, seq_len=50, filters=(70, 90), widths=(2, 6))),
+    (7, dict(dim=24, seq_len=9, filters=(8, 16), widths=(9, 1))),              # a branch as wide as the sequence
+])
+def test_fused_branches_tile_independent(n, case):
+    """At small batches the fused GEMM splits K; whichever tile runs it (each skips
+    the taps its rows lack), the feature vector is the same bit for bit, and within
+    one bf16 step of the oracle's."""
+    spec, params = _branch_probe(**case)
+    tok = wl.gen_tokens(n, case["seq_len"], 97, seed=4)
+    base, kinds = _run_traced(spec, params, tok)
+    assert kinds.count("concat") == 0 and kinds.count("pool") == 1
+    for cfg in (8, 6, 5, 3, 16, 38, 40):      # 64x64, 64x128, 128x128, 128x256, 128x256, 256x64, 128x128
+        z, _ = _run_traced(spec, params, tok, cfg)
+        assert np.array_equal(z.view(np.uint32), base.view(np.uint32)), cfg
+    ref = oracle.run_model(spec, params, tok, act="bf16")
+    check_bf16_tensor(base, ref)
