@@ -120,7 +120,11 @@ typedef struct {
  * n_classes.  Validates the layer lists, folds batch-norm into a per-channel fp32
  * scale and shift (computed in fp64), rounds weights to the compute precision,
  * packs them for the kernels, uploads them synchronously to the current device and
- * sizes the workspace for opts->max_batch.
+ * sizes the workspace for opts->max_batch.  In bf16, conv1d max-over-time layers that
+ * read one sequence and whose outputs are joined only by concatenations (the TextCNN's
+ * kernel widths) are packed as one GEMM whose max over time writes the concatenated
+ * vector; every output value is that of its own layer's sum of products (environment
+ * RAFIKI_FUSE_BRANCHES=0 at create keeps them apart).
  * Errors: RAFIKI_ERR_INVALID (null pointers, n_models out of range, mismatched
  * shapes or classes, malformed layers), RAFIKI_ERR_UNSUPPORTED, RAFIKI_ERR_NOMEM,
  * RAFIKI_ERR_HIP.  On error *out is set to NULL. */
