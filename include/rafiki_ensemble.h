@@ -31,8 +31,8 @@
  *   every call shares: issue the calls on one stream, or make each call's stream wait
  *   for the previous call's work (an event); calls from several threads at once are
  *   not supported.
- * - Inputs are not checked on the device: token ids must lie in [0, vocab) and image
- *   values must be finite.
+ * - Inputs are not checked on the device: token ids outside [0, vocab) read a zero
+ *   embedding row (no error), and image values must be finite.
  * - Results are deterministic: the same inputs, mask and n give bitwise-identical
  *   outputs (no unordered atomics in any reduction).
  */

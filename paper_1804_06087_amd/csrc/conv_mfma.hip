@@ -82,7 +82,11 @@ struct Loader {
   int a_off[RA];                       // aligned path: byte offset of (hi0, wi0, chunk) (may be virtual)
   unsigned b_off[RB];
   int nu, nv, ntap, ncb, nsub;         // aligned path: tap (u, v, index), channel block, half of the next tile
-  int taps, tstride;                   // TL: taps run per channel block; taps packed per block
+  int taps, tstride, cs;               // TL: taps run per channel block; taps packed per block; Cs
+  // TL with token ids: the table rows under taps 0-3 (tk0) and 4-7 (tk1) of row j,
+  // 16 bits each (0xFFFF: zeros).  Packed words selected by shifts keep them in
+  // registers (an array indexed by the tap would be moved to scratch memory).
+  uint64_t tk0[TL ? RA : 1], tk1[TL ? RA : 1];
 
   __device__ __forceinline__ void init(const ConvArgs& a, int m0, int n0, int wave_, int lane, int kt_begin_,
                                        int taps_) {
@@ -90,6 +94,7 @@ struct Loader {
     kt_begin = kt_begin_;
     taps = TL ? taps_ : a.kh * a.kw;
     tstride = TL ? a.tap_stride : 0;
+    cs = a.Cs;
     const int lrow = lane / KC;
     chunk = KC == 8 ? ((lane & 7) ^ lrow ^ (wave & 1)) : ((lane & 3) ^ (lane >> 4));
     xr = __builtin_amdgcn_make_buffer_rsrc((void*)a.x, (short)0, a.x_bytes, 0x00020000);
@@ -122,6 +127,22 @@ struct Loader {
         a_wi[j] = 0;
       }
       a_off[j] = ((a_img[j] + a_hi[j] * a.W + a_wi[j]) * a.Cs + chunk * 8) * 2;
+      if constexpr (TL) {
+        if (a.tok) {
+          const int rows = a.x_bytes / (a.Cs * 2);   // table rows (< 0xFFFF)
+          tk0[j] = 0;
+          tk1[j] = 0;
+#pragma unroll
+          for (int v = 0; v < kMaxGatherTaps; ++v) {
+            const int wi = a_wi[j] + v;
+            int id = -1;
+            if (a_hi[j] == 0 && v < a.kw && (unsigned)wi < (unsigned)a.W) id = a.tok[a_img[j] + wi];
+            const uint64_t f = (unsigned)id < (unsigned)rows ? (uint64_t)id : 0xFFFFull;
+            if (v < 4) tk0[j] |= f << (16 * v);
+            else tk1[j] |= f << (16 * (v - 4));
+          }
+        }
+      }
     }
 #pragma unroll
     for (int j = 0; j < RB; ++j)
@@ -136,6 +157,28 @@ struct Loader {
     }
   }
 
+  // Token gather (TL): the pixel rows of the next K tile come from the table rows of
+  // their tokens under tap ntap, at channel block ncb.
+  template <int P, int NP>
+  __device__ __forceinline__ void issue_gather(uint4* sbase) {
+    const int cdelta = (ncb * 64 + nsub * (8 * KC) + chunk * 8) * 2;
+    const int sh = 16 * (ntap & 3);
+#pragma unroll
+    for (int j = P; j < RA; j += NP) {
+      const uint64_t w = ntap < 4 ? tk0[j] : tk1[j];
+      const unsigned id = (unsigned)(w >> sh) & 0xFFFFu;
+      const unsigned off = id != 0xFFFFu ? id * (unsigned)(2 * cs) + (unsigned)cdelta : oob;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (lds_void*)(sbase + (j * NW + wave) * 64), 16, off, 0, 0, 0);
+    }
+    if (P == NP - 1 && ++nsub == SUBS) {
+      nsub = 0;
+      if (++ntap == taps) {
+        ntap = 0;
+        ++ncb;
+      }
+    }
+  }
+
   // Issue the loads of K tile kt (relative to the split's first tile) into LDS stage
   // `stage`, or only part P of NP of them (the loads j with j % NP == P), so that a
   // tile's loads can be spread over the k-steps of the running tile.  The parts of a
@@ -147,7 +190,9 @@ struct Loader {
     uint4* sbase = lds + stage * STAGE_CHUNKS;
     // K tile of the packed weights: gk itself unless taps are skipped
     const int kw_tile = TL ? (ncb * tstride + ntap) * SUBS + nsub : gk;
-    if (ALIGNED) {
+    if (TL && a.tok) {
+      if constexpr (TL) issue_gather<P, NP>(sbase);
+    } else if (ALIGNED) {
       const bool kvalid = gk * (8 * KC) < a.K;   // tiles past K (padding to Kp) read zeros
       const int delta = ((nu * a.W + nv) * a.Cs + ncb * 64 + nsub * (8 * KC)) * 2;
 #pragma unroll
@@ -246,7 +291,10 @@ __global__ __launch_bounds__(WM * WN * 64, OCC > 0 ? OCC : 1) void conv_mfma_ker
   int taps = 0;
   if constexpr (TL) {
     taps = 1;
-    for (int b = n0 / 64; b <= (n0 + BN - 1) / 64 && b < 16; ++b) taps = max(taps, (int)a.taps_by_block[b]);
+    const int b0 = n0 / 64, b1 = (n0 + BN - 1) / 64;
+#pragma unroll
+    for (int b = 0; b < 16; ++b)   // constant indices: the kernel arguments stay in registers
+      if (b >= b0 && b <= b1) taps = max(taps, (int)a.taps_by_block[b]);
   }
   const int ktiles = TL ? (a.Cs / 64) * taps * (8 / KC) : (a.K + 8 * KC - 1) / (8 * KC);
   // kt_per_split counts 64-wide tiles, or with fused branches whole channel blocks (of

@@ -64,7 +64,13 @@ struct ConvArgs {
   // skips the K tiles of the other taps, whose weights are all zero.
   int tap_stride;
   unsigned char taps_by_block[16];
+  // With tap_stride > 0 and at most kMaxGatherTaps taps: gather the conv1d input rows
+  // through token ids instead of reading a stored sequence.  Row (n, pos) of the input
+  // is row tok[n * W + pos] of x, the embedding table [x_bytes / (2 Cs)][Cs]; ids
+  // outside the table read zeros.  nullptr: x is the sequence itself.
+  const int32_t* tok;
 };
+constexpr int kMaxGatherTaps = 8;
 
 // Direct-to-LDS pipelined bf16 MFMA kernel; cfg selects the tile configuration
 // (kMfmaConfigs).  splits > 1 writes partial sums; finish with splitk_reduce.
@@ -95,8 +101,9 @@ struct ReduceSegs {
 // Global average pool NHWC [N][HW][Cs] -> [N][Cs]; also max over time when is_max.
 hipError_t launch_spatial_reduce(const void* x, void* y, int N, int HW, int Cs, int is_max, int bf16,
                                  hipStream_t s, const ReduceSegs* segs = nullptr);
-// Embedding gather: tokens [N][L] -> y [N][L][Cs] rows of table [vocab][Cs].
-hipError_t launch_embed_gather(const int32_t* tok, const void* table, void* y, int N, int L, int Cs,
+// Embedding gather: tokens [N][L] -> y [N][L][Cs] rows of table [vocab][Cs]; ids
+// outside [0, vocab) give zero rows.
+hipError_t launch_embed_gather(const int32_t* tok, const void* table, void* y, int N, int L, int Cs, int vocab,
                                int bf16, hipStream_t s);
 // Concatenate vectors: y[b, 0:c1] = a[b, 0:c1], y[b, c1:c1+c2] = b[b, 0:c2], zero after.
 hipError_t launch_concat(const void* a, int ca, int lda, const void* b, int cb, int ldb, void* y, int ldy,

@@ -274,28 +274,32 @@ hipError_t launch_spatial_reduce(const void* x, void* y, int N, int HW, int Cs, 
 
 // ---------------------------------------------------------------- embedding gather
 __global__ void embed_gather_kernel(const int32_t* __restrict__ tok, const void* __restrict__ table, void* y,
-                                    int N, int L, int Cs, int bf16) {
+                                    int N, int L, int Cs, int vocab, int bf16) {
   const int groups = Cs / 8;
   const long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= (long long)N * L * groups) return;
   const int g = (int)(idx % groups);
   const long long pos = idx / groups;
-  const long long row = tok[pos];
+  const int id = tok[pos];
+  const bool ok = (unsigned)id < (unsigned)vocab;
+  const long long row = ok ? id : 0;
   if (bf16) {
-    *((uint4*)((bf16_t*)y + pos * Cs) + g) = *((const uint4*)((const bf16_t*)table + row * Cs) + g);
+    *((uint4*)((bf16_t*)y + pos * Cs) + g) =
+        ok ? *((const uint4*)((const bf16_t*)table + row * Cs) + g) : make_uint4(0u, 0u, 0u, 0u);
   } else {
     const float4* src = (const float4*)((const float*)table + row * Cs + g * 8);
     float4* dst = (float4*)((float*)y + pos * Cs + g * 8);
-    dst[0] = src[0];
-    dst[1] = src[1];
+    const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
+    dst[0] = ok ? src[0] : z;
+    dst[1] = ok ? src[1] : z;
   }
 }
 
-hipError_t launch_embed_gather(const int32_t* tok, const void* table, void* y, int N, int L, int Cs, int bf16,
-                               hipStream_t s) {
+hipError_t launch_embed_gather(const int32_t* tok, const void* table, void* y, int N, int L, int Cs, int vocab,
+                               int bf16, hipStream_t s) {
   const long long total = (long long)N * L * (Cs / 8);
   launch(embed_gather_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), s, tok, table, y, N,
-                     L, Cs, bf16);
+                     L, Cs, vocab, bf16);
   return hipGetLastError();
 }
 

@@ -83,6 +83,8 @@ struct Op {
   int seg_end[kMaxReduceSegs] = {}, seg_kw[kMaxReduceSegs] = {}, seg_row[kMaxReduceSegs] = {};
   int tap_stride = 0;
   unsigned char taps_by_block[16] = {};
+  // fused branches reading the token ids: input rows gathered from this table
+  const void* table = nullptr;
   // concat
   int ca = 0, cb = 0;
 };
@@ -657,6 +659,28 @@ int build_model(rafiki_ensemble_s* e, int mi, const rafiki_model_desc& md, Model
   if (!groups.empty()) {
     int rc = fuse_branches(e, md, M, groups);
     if (rc) return rc;
+    // A fused GEMM that alone reads an embedding gathers the embedding rows through
+    // the token ids itself: the embedded sequence is never stored.
+    std::vector<int> readers(M.tensors.size(), 0), writer(M.tensors.size(), -1);
+    for (size_t i = 0; i < M.ops.size(); ++i) {
+      for (int src : {M.ops[i].in, M.ops[i].in2})
+        if (src >= 0) ++readers[src];
+      writer[M.ops[i].out] = (int)i;
+    }
+    std::vector<char> drop(M.ops.size(), 0);
+    for (Op& op : M.ops) {
+      if (op.nseg == 0 || op.tap_stride == 0 || op.kw > kMaxGatherTaps || op.in < 0 || readers[op.in] != 1) continue;
+      const int wi = writer[op.in];
+      if (wi < 0 || M.ops[wi].kind != O_EMBED) continue;
+      if (e->vocab >= 0xFFFF || (long long)e->vocab * op.Cs_in * (long long)e->esz() >= (1LL << 31)) continue;
+      op.table = M.ops[wi].d_w;
+      op.in = -1;
+      drop[wi] = 1;
+    }
+    std::vector<Op> kept;
+    for (size_t i = 0; i < M.ops.size(); ++i)
+      if (!drop[i]) kept.push_back(M.ops[i]);
+    M.ops.swap(kept);
   }
 
   // A 2x2 stride-2 max-pool whose input is a bf16 conv output read by nothing else is
@@ -868,6 +892,11 @@ ConvArgs gemm_args(const rafiki_ensemble_s* e, const Model& M, const Op& op, int
   a.mag_cs8 = magic_div(op.Cs_in / 8); a.mag_kw = magic_div(op.kw);
   a.tap_stride = op.tap_stride;
   for (int b = 0; b < 16; ++b) a.taps_by_block[b] = op.taps_by_block[b];
+  if (op.table) {   // token gather: x is the embedding table, rows picked by the ids
+    a.x = op.table;
+    a.tok = (const int32_t*)in;
+    a.x_bytes = (int)((long long)e->vocab * op.Cs_in * (long long)e->esz());
+  }
   return a;
 }
 
@@ -1042,7 +1071,7 @@ int run_model(const rafiki_ensemble_s* e, int mi, const void* in, int n, float* 
         break;
       case O_EMBED:
         TRACED(e, s, RAFIKI_K_EMBED, mi, li, 0.0, (double)n * op.W * (4.0 + 2.0 * op.cin_l * es),
-               launch_embed_gather((const int32_t*)in, op.d_w, yp, n, op.W, op.Cs_in, bf, s));
+               launch_embed_gather((const int32_t*)in, op.d_w, yp, n, op.W, op.Cs_in, e->vocab, bf, s));
         break;
       case O_CONCAT: {
         const Tensor& a = M.tensors[op.in];

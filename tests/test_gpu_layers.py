@@ -227,6 +227,9 @@ def test_fused_branches_bitwise(n, case, monkeypatch):
     else:
         assert kf.count("concat") == 0 and kf.count("pool") == 1
         assert kf.count("conv_mfma") == ks.count("conv_mfma") - (nb - 1)
+        # with 64-aligned storage channels the GEMM gathers the embedding rows itself
+        assert kf.count("embed") == (0 if case["dim"] % 64 == 0 or case["dim"] == 300 else 1)
+    assert ks.count("embed") == 1
     assert np.array_equal(fused.view(np.uint32), separate.view(np.uint32))
     ref = oracle.run_model(spec, params, tok, act="bf16")
     check_bf16_tensor(fused, ref)
@@ -246,8 +249,33 @@ def test_fused_branches_tile_independent(n, case):
     tok = wl.gen_tokens(n, case["seq_len"], 97, seed=4)
     base, kinds = _run_traced(spec, params, tok)
     assert kinds.count("concat") == 0 and kinds.count("pool") == 1
+    assert kinds.count("embed") == (0 if case["dim"] % 64 == 0 or case["dim"] == 300 else 1)
     for cfg in (8, 6, 5, 3, 16, 38, 40):      # 64x64, 64x128, 128x128, 128x256, 128x256, 256x64, 128x128
         z, _ = _run_traced(spec, params, tok, cfg)
         assert np.array_equal(z.view(np.uint32), base.view(np.uint32)), cfg
     ref = oracle.run_model(spec, params, tok, act="bf16")
     check_bf16_tensor(base, ref)
+
+
+def test_invalid_token_ids_read_zero_rows(monkeypatch):
+    """Token ids outside [0, vocab) read a zero embedding row, both in the embedding
+    kernel (branches apart) and in the GEMM that gathers the rows itself (fused)."""
+    import copy
+    case = dict(dim=128, seq_len=50, filters=(70, 90), widths=(2, 6))
+    spec, params = _branch_probe(**case)
+    vocab = spec.layers[0].c_in
+    tok = wl.gen_tokens(384, case["seq_len"], vocab, seed=5)
+    rng = np.random.default_rng(9)
+    bad = rng.random(tok.shape) < 0.05
+    tok[bad] = rng.choice(np.array([-1, vocab, vocab + 7, 2**31 - 1, -2**31], dtype=np.int64),
+                          size=int(bad.sum())).astype(np.int32)
+    fused, kf = _run_traced(spec, params, tok)
+    assert kf.count("embed") == 0
+    monkeypatch.setenv("RAFIKI_FUSE_BRANCHES", "0")
+    separate, ks = _run_traced(spec, params, tok)
+    assert ks.count("embed") == 1
+    assert np.array_equal(fused.view(np.uint32), separate.view(np.uint32))
+    p2 = copy.deepcopy(params)
+    p2.layers[0].weight = np.vstack([params.layers[0].weight, np.zeros((1, case["dim"]), np.float32)])
+    ref = oracle.run_model(spec, p2, np.where(bad, vocab, tok), act="bf16")
+    check_bf16_tensor(fused, ref)
