@@ -258,6 +258,7 @@ __global__ __launch_bounds__(WM * WN * 64, OCC > 0 ? OCC : 1) void conv_mfma_ker
   constexpr int TM = WTM / 32, TN = WTN / 32;
   constexpr int KS = KC / 2;                       // MFMA k-steps of 16 per K tile
   constexpr bool TL = ALIGNED && TAPS;
+  static_assert(!TL || WTM <= 128, "the epilogue max assumes a wave tile spans at most two requests");
   using LoaderT = Loader<BM, BN, NW, ALIGNED, KC, TL>;
   constexpr int PER = LoaderT::RA + LoaderT::RB;   // load instructions per thread per tile
   constexpr int STAGE_CHUNKS = (BM + BN) * KC;     // 16-byte chunks per stage
@@ -459,6 +460,71 @@ __global__ __launch_bounds__(WM * WN * 64, OCC > 0 ? OCC : 1) void conv_mfma_ker
     }
     __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): this wave's LDS writes have landed
     __builtin_amdgcn_wave_barrier();
+    if constexpr (TL) {
+      if (a.maxslot) {
+        // Max over positions: lane (r, o) = (lane % 16, lane / 16) folds rows
+        // pass * 16 + r of channels c .. c + 7 (octet o) into the running max of the
+        // wave tile's first request (A) or, if the tile reaches it, the next (B) (a
+        // wave tile has at most 128 rows and a request at least 128 positions).  The
+        // 16 lanes of one octet form a DPP row and reduce with four DPP steps; lane
+        // r = 0 merges the result with atomic max.  The values are the bf16-rounded
+        // outputs the stored path would write, so the max is the same.
+        const int r = lane & 15, o = lane >> 4;
+        const int cm = cb + 8 * o;
+        const int mw = m0 + wm * WTM;
+        const int nA = mw / a.Wo, rowB = (nA + 1) * a.Wo;
+        const bool has_b = rowB < min(mw + WTM, a.M);   // wave-uniform
+        int kwb = 1;
+#pragma unroll
+        for (int b = 0; b < 16; ++b)   // constant indices: the kernel arguments stay in registers
+          if (b == (cb >> 6)) kwb = a.taps_by_block[b];
+        const int len = a.W - kwb + 1;   // positions of this channel block's branch
+        float mA[8], mB[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) mA[j] = mB[j] = -INFINITY;
+#pragma unroll
+        for (int pass = 0; pass < NPASS; ++pass) {
+          const int p = pass * 16 + r;
+          const int m = mw + p;
+          const float4 lo = stg[p * 8 + ((2 * o) ^ swz<8>(p))];
+          const float4 hi = stg[p * 8 + ((2 * o + 1) ^ swz<8>(p))];
+          const float v[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+          const bool inB = m >= rowB;
+          const int wo = m - (inB ? rowB : rowB - a.Wo);
+          if (m >= a.M || wo >= len) continue;
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            const float t = bf2f_m(f2bf_m(a.relu ? fmaxf(v[j], 0.f) : v[j]));
+            if (inB) mB[j] = fmaxf(mB[j], t);
+            else mA[j] = fmaxf(mA[j], t);
+          }
+        }
+        auto row_max = [](float x) {   // max over the 16 lanes of a DPP row, in every lane
+          x = fmaxf(x, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0xB1, 0xF, 0xF, false)));
+          x = fmaxf(x, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x4E, 0xF, 0xF, false)));
+          x = fmaxf(x, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x141, 0xF, 0xF, false)));
+          x = fmaxf(x, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x140, 0xF, 0xF, false)));
+          return x;
+        };
+#pragma unroll
+        for (int j = 0; j < 8; ++j) mA[j] = row_max(mA[j]);
+        if (has_b) {
+#pragma unroll
+          for (int j = 0; j < 8; ++j) mB[j] = row_max(mB[j]);
+        }
+        if (r == 0 && cm < a.c_write) {
+          unsigned* sA = a.maxslot + (long long)nA * a.ldslot + cm;
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            if (mA[j] > -INFINITY) atomicMax(sA + j, max_key(mA[j]));
+            if (has_b && mB[j] > -INFINITY) atomicMax(sA + a.ldslot + j, max_key(mB[j]));
+          }
+        }
+        __builtin_amdgcn_s_waitcnt(0xC07F);   // reads done before the region is rewritten
+        __builtin_amdgcn_wave_barrier();
+        continue;
+      }
+    }
     if (a.pool2) {
       // fused 2x2 max-pool: rows 4w .. 4w + 3 of the wave tile form window w; lane
       // (pl, oq) takes window pass * 16 + pl.  The max of the four fp32 values, then

@@ -69,8 +69,23 @@ struct ConvArgs {
   // is row tok[n * W + pos] of x, the embedding table [x_bytes / (2 Cs)][Cs]; ids
   // outside the table read zeros.  nullptr: x is the sequence itself.
   const int32_t* tok;
+  // With tap_stride > 0, branches on 64-row blocks, Wo >= 128 and no split: the max
+  // over positions is taken in the epilogue.  Each output row block b keeps positions
+  // wo < W - taps_by_block[b] + 1; the bf16-rounded, ReLU'd values are max-reduced per
+  // (request, channel) and merged with atomic max into maxslot [N][ldslot] as
+  // order-preserving keys (max_key()), which start at 0.  nullptr: rows are stored.
+  unsigned* maxslot;
+  int ldslot;
 };
 constexpr int kMaxGatherTaps = 8;
+// Order-preserving key of a float for unsigned atomic max (0 is below every key).
+__device__ __forceinline__ unsigned max_key(float f) {
+  const unsigned u = __float_as_uint(f);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__device__ __forceinline__ float max_key_value(unsigned k) {
+  return __uint_as_float((k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k);
+}
 
 // Direct-to-LDS pipelined bf16 MFMA kernel; cfg selects the tile configuration
 // (kMfmaConfigs).  splits > 1 writes partial sums; finish with splitk_reduce.
@@ -101,6 +116,10 @@ struct ReduceSegs {
 // Global average pool NHWC [N][HW][Cs] -> [N][Cs]; also max over time when is_max.
 hipError_t launch_spatial_reduce(const void* x, void* y, int N, int HW, int Cs, int is_max, int bf16,
                                  hipStream_t s, const ReduceSegs* segs = nullptr);
+// Fused branches' max in the GEMM epilogue: y[n][dst_i + k] = bf16 of slot row n at
+// channel src_i + k for each branch, zeros from zero_from to ldy; every slot read is
+// reset to 0 for the next call.
+hipError_t launch_maxslot_finish(unsigned* slot, int ldslot, void* y, int N, const ReduceSegs& sg, hipStream_t s);
 // Embedding gather: tokens [N][L] -> y [N][L][Cs] rows of table [vocab][Cs]; ids
 // outside [0, vocab) give zero rows.
 hipError_t launch_embed_gather(const int32_t* tok, const void* table, void* y, int N, int L, int Cs, int vocab,

@@ -272,6 +272,32 @@ hipError_t launch_spatial_reduce(const void* x, void* y, int N, int HW, int Cs, 
   return hipGetLastError();
 }
 
+// ---------------------------------------------------------------- fused branches' max
+__global__ void maxslot_finish_kernel(unsigned* slot, int ldslot, void* y, int N, ReduceSegs sg) {
+  const int n = blockIdx.y;
+  const int c = blockIdx.x * blockDim.x + threadIdx.x;
+  if (n >= N || c >= sg.ldy) return;
+  float v = 0.f;
+  for (int i = 0; i < sg.n; ++i)
+    if (c >= sg.dst[i] && c < sg.dst[i] + sg.cnt[i]) {
+      unsigned* p = slot + (long long)n * ldslot + sg.src[i] + (c - sg.dst[i]);
+      v = max_key_value(*p);
+      *p = 0u;
+    }
+  ((bf16_t*)y)[(long long)n * sg.ldy + c] = (bf16_t)f2bf(v);
+}
+
+hipError_t launch_maxslot_finish(unsigned* slot, int ldslot, void* y, int N, const ReduceSegs& sg, hipStream_t s) {
+  if (sg.n < 1 || sg.n > kMaxReduceSegs || N < 1) return hipErrorInvalidValue;
+  for (int i = 0; i < sg.n; ++i)
+    if (sg.cnt[i] < 1 || sg.src[i] < 0 || sg.src[i] + sg.cnt[i] > ldslot || sg.dst[i] < 0 ||
+        sg.dst[i] + sg.cnt[i] > sg.zero_from || sg.zero_from > sg.ldy)
+      return hipErrorInvalidValue;
+  launch(maxslot_finish_kernel, dim3((unsigned)((sg.ldy + 255) / 256), (unsigned)N), dim3(256), s, slot, ldslot, y, N,
+         sg);
+  return hipGetLastError();
+}
+
 // ---------------------------------------------------------------- embedding gather
 __global__ void embed_gather_kernel(const int32_t* __restrict__ tok, const void* __restrict__ table, void* y,
                                     int N, int L, int Cs, int vocab, int bf16) {

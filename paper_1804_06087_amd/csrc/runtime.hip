@@ -85,6 +85,10 @@ struct Op {
   unsigned char taps_by_block[16] = {};
   // fused branches reading the token ids: input rows gathered from this table
   const void* table = nullptr;
+  // fused branches whose max is taken in the GEMM epilogue (unsplit launches): atomic
+  // max keys [max_batch][ldslot], zero between calls
+  unsigned* d_slot = nullptr;
+  int ldslot = 0;
   // concat
   int ca = 0, cb = 0;
 };
@@ -475,6 +479,19 @@ int fuse_branches(rafiki_ensemble_s* e, const rafiki_model_desc& md, Model& M, c
       if (!rc) rc = upload_fold(e, m, sc, sh);
       if (rc) return rc;
     }
+    // Branches on their own 64-row blocks and requests of at least 128 positions (a
+    // wave tile then spans at most two requests): the max can be taken in the GEMM
+    // epilogue, into slots that start at zero and are reset as they are read.
+    if (pad64 && m.tap_stride > 0 && m.Wo >= 128) {
+      m.ldslot = round_up(rows, 8);
+      const size_t bytes = (size_t)e->max_batch * m.ldslot * 4;
+      int rc = dev_alloc(e, (void**)&m.d_slot, bytes);
+      if (rc) return rc;
+      if (!e->dry) {
+        const hipError_t st = hipMemset(m.d_slot, 0, bytes);
+        if (st != hipSuccess) return fail(RAFIKI_ERR_HIP, std::string("hipMemset: ") + hipGetErrorString(st));
+      }
+    }
     fused[gi] = m;
   }
   std::vector<Op> ops;
@@ -839,7 +856,7 @@ int run_gemm(const rafiki_ensemble_s* e, const Op& op, ConvArgs a, hipStream_t s
   const double in_elems = (double)a.N * a.H * a.W * op.cin_l;   // FC: H = W = 1, cin_l = flattened size
   const double out_rows = a.pool2 ? a.M / 4.0 : (double)a.M;
   const double bytes = in_elems * es + w_elems * es +
-                       out_rows * op.c_out * (a.out_f32 ? 4.0 : es) * (a.res ? 2.0 : 1.0);
+                       (a.maxslot ? 0.0 : out_rows * op.c_out * (a.out_f32 ? 4.0 : es) * (a.res ? 2.0 : 1.0));
   if (e->precision != RAFIKI_BF16) {
     TRACED(e, s, RAFIKI_K_CONV_F32, mi, li, flops, bytes, launch_conv_f32(a, s));
     return RAFIKI_OK;
@@ -1032,8 +1049,23 @@ int run_model(const rafiki_ensemble_s* e, int mi, const void* in, int n, float* 
         if (op.kind == O_CONV1D) {
           void* tmp = M.d_arena + op.tmp_off;
           a.y = tmp; a.c_write = round_up(op.c_out, 8); a.ldy = a.c_write; a.out_f32 = bf ? 0 : 1;
+          const bool in_epilogue = op.d_slot && choose_splits(a.M, op.c_out, a.Kp / 64) == 1;
+          if (in_epilogue) { a.maxslot = op.d_slot; a.ldslot = op.ldslot; }
           int rc = run_gemm(e, op, a, s, mi, li, cfg);
           if (rc) return rc;
+          if (in_epilogue) {   // the GEMM took the max; write the concatenated vector
+            ReduceSegs segs{};
+            segs.n = op.nseg; segs.ldy = y.Cs; segs.zero_from = y.c;
+            for (int i = 0; i < op.nseg; ++i) {
+              segs.dst[i] = i ? op.seg_end[i - 1] : 0;
+              segs.cnt[i] = op.seg_end[i] - segs.dst[i];
+              segs.src[i] = op.seg_row[i];
+              segs.len[i] = op.W - op.seg_kw[i] + 1;
+            }
+            TRACED(e, s, RAFIKI_K_POOL, mi, li, 0.0, (double)n * op.ldslot * 4.0 * 2.0 + (double)n * y.Cs * es,
+                   launch_maxslot_finish(op.d_slot, op.ldslot, yp, n, segs, s));
+            break;
+          }
           ReduceSegs segs{};
           double vals = (double)op.Wo * op.c_out;   // pre-max values read per request
           if (op.nseg > 0) {

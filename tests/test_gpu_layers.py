@@ -194,10 +194,15 @@ def _run_traced(spec, params, tok, cfg=-1):
             ens.force_tile(cfg)
         x = torch.from_numpy(tok).to(DEV)
         out = torch.empty((n, spec.n_classes), dtype=torch.float32, device=DEV)
+        ens.model_logits(0, x, n, out)          # tunes the tiles; a second call must agree
+        torch.cuda.synchronize()
+        first = out.cpu().numpy()
         ens.trace(True)
         ens.model_logits(0, x, n, out)
         torch.cuda.synchronize()
-        return out.cpu().numpy(), [r["kind"] for r in ens.trace_read()]
+        z = out.cpu().numpy()
+        assert np.array_equal(z.view(np.uint32), first.view(np.uint32)), "repeated call differs"
+        return z, [r["kind"] for r in ens.trace_read()]
 
 
 # Batches large enough that neither the fused GEMM nor any separate branch splits K
@@ -206,6 +211,7 @@ def _run_traced(spec, params, tok, cfg=-1):
     (72, dict(dim=300, seq_len=256, filters=(100, 100, 100), widths=(3, 4, 5))),  # TextCNN: aligned K, 64-row blocks
     (384, dict(dim=128, seq_len=50, filters=(70, 90), widths=(2, 6))),           # aligned, tiles mixing widths
     (570, dict(dim=64, seq_len=33, filters=(13, 21, 6), widths=(5, 2, 3))),      # aligned, one 64-row block
+    (130, dict(dim=64, seq_len=130, filters=(64, 64), widths=(2, 3))),           # max in the epilogue, 129 positions
     (460, dict(dim=70, seq_len=40, filters=(13, 21, 6), widths=(5, 2, 3))),      # unaligned K, ragged segments
     (7, dict(dim=24, seq_len=30, filters=(5, 7, 9), widths=(2, 3, 4), extra_reader=True)),   # not fusable
 ])
@@ -238,13 +244,17 @@ def test_fused_branches_bitwise(n, case, monkeypatch):
 @pytest.mark.parametrize("n, case", [
     (7, dict(dim=300, seq_len=256, filters=(100, 100, 100), widths=(3, 4, 5))),
     (1, dict(dim=300, seq_len=256, filters=(100, 100, 100), widths=(3, 4, 5))),
+    (72, dict(dim=300, seq_len=256, filters=(100, 100, 100), widths=(3, 4, 5))),    # unsplit: max in the epilogue
+    (130, dict(dim=64, seq_len=130, filters=(64, 64), widths=(2, 3))),
     (9, dict(dim=128, seq_len=50, filters=(70, 90), widths=(2, 6))),
     (7, dict(dim=24, seq_len=9, filters=(8, 16), widths=(9, 1))),              # a branch as wide as the sequence
 ])
 def test_fused_branches_tile_independent(n, case):
-    """At small batches the fused GEMM splits K; whichever tile runs it (each skips
-    the taps its rows lack), the feature vector is the same bit for bit, and within
-    one bf16 step of the oracle's."""
+    """Whichever tile runs the fused GEMM (each skips the taps its rows lack; at small
+    batches it splits K, at large ones with long sequences it takes the max in its
+    epilogue), the feature vector is the same bit for bit, and within one bf16 step
+    of the oracle's; repeated calls on one handle agree too (the epilogue's slots are
+    reset as they are read)."""
     spec, params = _branch_probe(**case)
     tok = wl.gen_tokens(n, case["seq_len"], 97, seed=4)
     base, kinds = _run_traced(spec, params, tok)
