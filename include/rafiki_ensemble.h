@@ -34,7 +34,8 @@
  * - Inputs are not checked on the device: token ids outside [0, vocab) read a zero
  *   embedding row (no error), and image values must be finite.
  * - Results are deterministic: the same inputs, mask and n give bitwise-identical
- *   outputs (no unordered atomics in any reduction).
+ *   outputs (sums are taken in a fixed order; the only atomics are maxima, which do
+ *   not depend on order).
  */
 #ifndef RAFIKI_ENSEMBLE_H
 #define RAFIKI_ENSEMBLE_H
