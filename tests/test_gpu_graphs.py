@@ -92,6 +92,10 @@ def test_graph_replay_tokens():
         _replay_matches_eager(ens, [x, x_alt], 40, [0b11, 0b01], C)
         _infer(ens, x, 23, 0b11, C)                    # ragged batch size: tuned eagerly first
         _replay_matches_eager(ens, [x[:23], x_alt[:23]], 23, [0b11], C)
+        # n = 40 and 23: the fused branch GEMM takes the max over time in its epilogue
+        # (slots reset by the finishing kernel); n = 5 splits K and stores the rows
+        _infer(ens, x, 5, 0b11, C)
+        _replay_matches_eager(ens, [x[:5], x_alt[:5]], 5, [0b11, 0b10], C)
 
 
 def test_graph_dropped_by_force_tile():
