@@ -359,17 +359,22 @@ hipError_t launch_concat(const void* a, int ca, int lda, const void* b, int cb, 
 
 // ---------------------------------------------------------------- fp32 direct conv
 // One thread per (pixel, output channel); taps outer, channels inner (fp32 FMA).
+// One thread per (pixel, 4 consecutive output channels).  Weights are [Kp][Co_pad]
+// (K-major), so a lane's 4 weights of one K index are one 16-byte load and the lanes
+// of a wave read consecutive ones; the input chunk is shared by the lanes of a pixel.
+// Each output sums its products in (u, v, ci) order with fmaf.
 __global__ void conv_f32_kernel(ConvArgs a) {
+  const int groups = (a.c_write + 3) / 4;
   const long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= (long long)a.M * a.c_write) return;
-  const int m = (int)(idx / a.c_write);
-  const int co = (int)(idx - (long long)m * a.c_write);
+  if (idx >= (long long)a.M * groups) return;
+  const int m = (int)(idx / groups);
+  const int co = 4 * (int)(idx - (long long)m * groups);
   const int HoWo = a.Ho * a.Wo;
   const int n = m / HoWo, r = m - n * HoWo;
   const int ho = r / a.Wo, wo = r - ho * a.Wo;
   const float* X = (const float*)a.x;
-  const float* Wt = (const float*)a.w + (long long)co * a.Kp;
-  float s = 0.f;
+  const float* Wt = (const float*)a.w + co;
+  float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
   for (int u = 0; u < a.kh; ++u) {
     const int hi = ho * a.stride - a.pad + u;
     if (hi < 0 || hi >= a.H) continue;
@@ -377,19 +382,36 @@ __global__ void conv_f32_kernel(ConvArgs a) {
       const int wi = wo * a.stride - a.pad + v;
       if (wi < 0 || wi >= a.W) continue;
       const float* xp = X + (((long long)n * a.H + hi) * a.W + wi) * a.Cs;
-      const float* wp = Wt + (u * a.kw + v) * a.Cs;
-      for (int ci = 0; ci < a.Cs; ++ci) s = fmaf(xp[ci], wp[ci], s);
+      const float* wp = Wt + (long long)((u * a.kw + v) * a.Cs) * a.Co_pad;
+      for (int ci = 0; ci < a.Cs; ci += 4) {
+        const float4 x4 = *(const float4*)(xp + ci);
+        const float xv[4] = {x4.x, x4.y, x4.z, x4.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float4 w4 = *(const float4*)(wp + (long long)(ci + i) * a.Co_pad);
+          s0 = fmaf(xv[i], w4.x, s0);
+          s1 = fmaf(xv[i], w4.y, s1);
+          s2 = fmaf(xv[i], w4.z, s2);
+          s3 = fmaf(xv[i], w4.w, s3);
+        }
+      }
     }
   }
-  float y = s * a.scale[co] + a.shift[co];
+  const float sv[4] = {s0, s1, s2, s3};
   const long long o = (long long)m * a.ldy + co;
-  if (a.res) y += ((const float*)a.res)[o];
-  if (a.relu) y = fmaxf(y, 0.f);
-  ((float*)a.y)[o] = y;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    if (co + j >= a.c_write) break;
+    float y = sv[j] * a.scale[co + j] + a.shift[co + j];
+    if (a.res) y += ((const float*)a.res)[o + j];
+    if (a.relu) y = fmaxf(y, 0.f);
+    ((float*)a.y)[o + j] = y;
+  }
 }
 
 hipError_t launch_conv_f32(const ConvArgs& a, hipStream_t s) {
-  const long long total = (long long)a.M * a.c_write;
+  if (a.Cs % 4 != 0 || a.Co_pad % 4 != 0 || a.c_write > a.Co_pad) return hipErrorInvalidValue;
+  const long long total = (long long)a.M * ((a.c_write + 3) / 4);
   launch(conv_f32_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), s, a);
   return hipGetLastError();
 }

@@ -274,13 +274,14 @@ int split_cfg(int c_out) { return c_out <= 32 ? 10 : (c_out <= 64 ? 8 : 6); }
 int default_cfg(int c_out) { return c_out <= 32 ? 10 : (c_out <= 64 ? 8 : 6); }
 
 // Pack a GEMM-like weight into [Co_pad][Kp] over Cs_in storage channels.  K order:
-// (channel block of 64, tap, channel) when Cs_in % 64 == 0 (the kernel's aligned
-// path), else (tap, channel).  `src_index(co, ci, u, v)` gives the canonical flat index.
+// (channel block of 64, tap, channel) for the bf16 kernel's aligned path (bf16 and
+// Cs_in % 64 == 0), else (tap, channel), the order the fp32 kernel reads.
+// `src_index(co, ci, u, v)` gives the canonical flat index.
 template <class F>
-std::vector<float> pack_weight(int c_out, int c_in, int kh, int kw, int Cs_in, int Co_pad, int Kp, F src_index,
-                               const float* w) {
+std::vector<float> pack_weight(bool bf16, int c_out, int c_in, int kh, int kw, int Cs_in, int Co_pad, int Kp,
+                               F src_index, const float* w) {
   std::vector<float> out((size_t)Co_pad * Kp, 0.f);
-  const bool aligned = Cs_in % 64 == 0;
+  const bool aligned = bf16 && Cs_in % 64 == 0;
   const int taps = kh * kw;
   for (int co = 0; co < c_out; ++co)
     for (int u = 0; u < kh; ++u)
@@ -300,6 +301,17 @@ int upload_weights(rafiki_ensemble_s* e, Op& op, const std::vector<float>& packe
     return upload(e, &op.d_w, b.data(), b.size() * 2);
   }
   return upload(e, &op.d_w, packed.data(), packed.size() * 4);
+}
+
+// GEMM weights packed as [Co_pad][Kp]: uploaded as they are for the bf16 kernel, and
+// transposed to [Kp][Co_pad] for the fp32 kernel, whose lanes read the weights of 4
+// consecutive output channels of one K index as one 16-byte load.
+int upload_gemm_weights(rafiki_ensemble_s* e, Op& op, const std::vector<float>& packed) {
+  if (e->precision == RAFIKI_BF16) return upload_weights(e, op, packed);
+  std::vector<float> t(packed.size());
+  for (int co = 0; co < op.Co_pad; ++co)
+    for (int k = 0; k < op.Kp; ++k) t[(size_t)k * op.Co_pad + co] = packed[(size_t)co * op.Kp + k];
+  return upload_weights(e, op, t);
 }
 
 // Fold inference batch-norm and bias: y = s * conv + t, s = gamma / sqrt(var + eps),
@@ -559,11 +571,11 @@ int build_model(rafiki_ensemble_s* e, int mi, const rafiki_model_desc& md, Model
         op.Co_pad = bf ? round_up(L.c_out, kCoPadBf16) : round_up(L.c_out, 32);
         op.Kp = bf ? round_up(op.K, 64) : op.K;
         if (e->dry) break;
-        auto packed = pack_weight(L.c_out, c_in, kh, kw, x.Cs, op.Co_pad, op.Kp,
+        auto packed = pack_weight(bf, L.c_out, c_in, kh, kw, x.Cs, op.Co_pad, op.Kp,
                                   [=](int co, int ci, int u, int v) {
                                     return (((size_t)co * c_in + ci) * kh + u) * kw + v;
                                   }, L.weight);
-        int rc = upload_weights(e, op, packed);
+        int rc = upload_gemm_weights(e, op, packed);
         if (!rc) rc = upload_fold(e, op, L);
         if (rc) return rc;
         break;
@@ -609,7 +621,7 @@ int build_model(rafiki_ensemble_s* e, int mi, const rafiki_model_desc& md, Model
               for (int c = 0; c < xc; ++c)
                 packed[(size_t)co * op.Kp + (size_t)(yy * xw + xx) * xCs + c] =
                     L.weight[(size_t)co * cin + (size_t)c * xh * xw + yy * xw + xx];
-        int rc = upload_weights(e, op, packed);
+        int rc = upload_gemm_weights(e, op, packed);
         if (!rc) rc = upload_fold(e, op, L);
         if (rc) return rc;
         break;
@@ -641,10 +653,10 @@ int build_model(rafiki_ensemble_s* e, int mi, const rafiki_model_desc& md, Model
         op.Kp = bf ? round_up(op.K, 64) : op.K;
         if (e->dry || in_group[i]) break;   // a fused branch: packed with its group below
         const int cin = L.c_in, kw = L.kw;
-        auto packed = pack_weight(L.c_out, cin, 1, kw, x.Cs, op.Co_pad, op.Kp,
+        auto packed = pack_weight(bf, L.c_out, cin, 1, kw, x.Cs, op.Co_pad, op.Kp,
                                   [=](int co, int ci, int, int v) { return ((size_t)co * cin + ci) * kw + v; },
                                   L.weight);
-        int rc = upload_weights(e, op, packed);
+        int rc = upload_gemm_weights(e, op, packed);
         if (!rc) rc = upload_fold(e, op, L);
         if (rc) return rc;
         break;

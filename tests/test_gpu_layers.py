@@ -72,6 +72,9 @@ CASES = {
                     (8, 8, 6), 2, 16 * 4 * 3),
     "gap": ([conv(-1, 8, 48, 3), Layer(op=GLOBAL_AVGPOOL, input=0, c_in=48, c_out=48)], (8, 7, 5), 6, 48),
     "many_tiles_ragged_m": ([conv(-1, 32, 16, 3)], (32, 7, 9), 37, 16 * 7 * 9),
+    # several 64-channel blocks under a 3x3 kernel: the bf16 kernel's channel-block K
+    # order, the fp32 kernel's (tap, channel) order
+    "cin192_3x3": ([conv(-1, 192, 24, 3)], (192, 5, 6), 3, 24 * 5 * 6),
     # image-input convolutions with few channels (input padded to 8 storage channels)
     "stem_3x3_cout32_ragged": ([conv(-1, 3, 32, 3)], (3, 5, 6), 7, 32 * 5 * 6),
     "stem_7x7_s2_cout128": ([conv(-1, 3, 128, 7, s=2, p=3)], (3, 4, 4), 3, 128 * 2 * 2),
@@ -105,7 +108,7 @@ def test_layer_bf16(name):
 
 
 @pytest.mark.parametrize("name", ["stem3x3_cin3", "s2_cin24_cout40_nonsquare", "residual_block", "maxpool3_s2_p1_odd",
-                                  "gap", "7x7_s2_p3_stem"])
+                                  "gap", "7x7_s2_p3_stem", "cin192_3x3", "pool2_fused_split_k"])
 def test_layer_fp32(name):
     layers, shape, n, out_elems = CASES[name]
     spec, params = probe(layers, shape, out_elems, bf16=False)
