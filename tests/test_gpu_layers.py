@@ -108,7 +108,8 @@ def test_layer_bf16(name):
 
 
 @pytest.mark.parametrize("name", ["stem3x3_cin3", "s2_cin24_cout40_nonsquare", "residual_block", "maxpool3_s2_p1_odd",
-                                  "gap", "7x7_s2_p3_stem", "cin192_3x3", "pool2_fused_split_k"])
+                                  "gap", "7x7_s2_p3_stem", "cin192_3x3", "pool2_fused_split_k", "maxpool2_s2",
+                                  "pool2_fused_ragged", "pool2_odd_unfused"])
 def test_layer_fp32(name):
     layers, shape, n, out_elems = CASES[name]
     spec, params = probe(layers, shape, out_elems, bf16=False)
