@@ -262,7 +262,7 @@ bool cfg_fits(int cfg, int c_out) {
 // compute units.  Depends only on the GEMM shape, so results do not depend on tuning.
 int choose_splits(int M, int c_out, int ktiles) {
   const int tiles = ((M + 63) / 64) * ((c_out + 127) / 128);
-  if (tiles >= 256) return 1;
+  if (tiles >= 256 || ktiles < 12) return 1;
   int s = std::min((512 + tiles - 1) / tiles, ktiles / 4);
   s = std::max(1, std::min(s, 64));
   const int per = (ktiles + s - 1) / s;
