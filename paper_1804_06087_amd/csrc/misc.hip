@@ -274,8 +274,8 @@ hipError_t launch_spatial_reduce(const void* x, void* y, int N, int HW, int Cs, 
 
 // ---------------------------------------------------------------- fused branches' max
 __global__ void maxslot_finish_kernel(unsigned* slot, int ldslot, void* y, int N, ReduceSegs sg) {
-  const int n = blockIdx.y;
-  const int c = blockIdx.x * blockDim.x + threadIdx.x;
+  const int n = blockIdx.x;
+  const int c = blockIdx.y * blockDim.x + threadIdx.x;
   if (n >= N || c >= sg.ldy) return;
   float v = 0.f;
   for (int i = 0; i < sg.n; ++i)
@@ -293,7 +293,7 @@ hipError_t launch_maxslot_finish(unsigned* slot, int ldslot, void* y, int N, con
     if (sg.cnt[i] < 1 || sg.src[i] < 0 || sg.src[i] + sg.cnt[i] > ldslot || sg.dst[i] < 0 ||
         sg.dst[i] + sg.cnt[i] > sg.zero_from || sg.zero_from > sg.ldy)
       return hipErrorInvalidValue;
-  launch(maxslot_finish_kernel, dim3((unsigned)((sg.ldy + 255) / 256), (unsigned)N), dim3(256), s, slot, ldslot, y, N,
+  launch(maxslot_finish_kernel, dim3((unsigned)N, (unsigned)((sg.ldy + 255) / 256)), dim3(256), s, slot, ldslot, y, N,
          sg);
   return hipGetLastError();
 }
