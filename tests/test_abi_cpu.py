@@ -162,3 +162,23 @@ def _light_params(spec):
             p.bn_gamma = p.bn_beta = p.bn_mean = p.bn_var = np.zeros(1, np.float32)
         lp.append(p)
     return wl.ModelParams(spec, lp, 0, True)
+
+
+def test_branch_fusion_keeps_validation_errors():
+    """The bf16 pre-pass that fuses a TextCNN's branches reads the layer list before it
+    is validated: malformed concatenations still fail validation, not the pre-pass."""
+    import copy
+    s = wl.textcnn(vocab=100, seq_len=16, dim=64, filters=8, widths=(2, 3, 4), n_classes=2)
+    opts = {"input_kind": 1, "c": 1, "h": 16, "w": 1, "vocab": 100}
+    # a concatenation whose c_out is not the sum of its inputs
+    bad = copy.deepcopy(s)
+    i = [k for k, L in enumerate(bad.layers) if L.op == wl.CONCAT][-1]
+    bad.layers[i].c_out += 1
+    rc, _ = _create([bad], [_light_params(bad)], precision=bd.RAFIKI_BF16, opts_over=opts)
+    assert rc == bd.RAFIKI_ERR_INVALID and "concat" in bd.last_error()
+    # a concatenation that reads a later layer
+    bad = copy.deepcopy(s)
+    i = [k for k, L in enumerate(bad.layers) if L.op == wl.CONCAT][0]
+    bad.layers[i].input2 = len(bad.layers) - 1
+    rc, _ = _create([bad], [_light_params(bad)], precision=bd.RAFIKI_BF16, opts_over=opts)
+    assert rc == bd.RAFIKI_ERR_INVALID and "out of range" in bd.last_error()
