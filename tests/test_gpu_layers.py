@@ -166,7 +166,7 @@ def test_textcnn_long_sequence():
     assert err <= 1e-2, err
 
 
-def _branch_probe(dim, seq_len, filters, widths, vocab=97, extra_reader=False, seed=11):
+def _branch_probe(dim, seq_len, filters, widths, vocab=97, extra_reader=False, seed=11, relu=True):
     """Embedding, conv1d max-over-time branches of the given widths and filter
     counts, their concatenation in order, then the identity FC: the logits are the
     concatenated feature vector.  With extra_reader, the first branch is also
@@ -174,7 +174,7 @@ def _branch_probe(dim, seq_len, filters, widths, vocab=97, extra_reader=False, s
     L = [Layer(op=EMBEDDING, input=-1, c_in=vocab, c_out=dim)]
     feats = []
     for f, w in zip(filters, widths):
-        L.append(Layer(op=CONV1D_MAXTIME, input=0, c_in=dim, c_out=f, kh=1, kw=w, relu=True, bias=True))
+        L.append(Layer(op=CONV1D_MAXTIME, input=0, c_in=dim, c_out=f, kh=1, kw=w, relu=relu, bias=True))
         feats.append(len(L) - 1)
     x, c = feats[0], filters[0]
     for fi, f in zip(feats[1:], filters[1:]):
@@ -216,6 +216,7 @@ def _run_traced(spec, params, tok, cfg=-1):
     (384, dict(dim=128, seq_len=50, filters=(70, 90), widths=(2, 6))),           # aligned, tiles mixing widths
     (570, dict(dim=64, seq_len=33, filters=(13, 21, 6), widths=(5, 2, 3))),      # aligned, one 64-row block
     (130, dict(dim=64, seq_len=130, filters=(64, 64), widths=(2, 3))),           # max in the epilogue, 129 positions
+    (72, dict(dim=300, seq_len=256, filters=(100, 100, 100), widths=(3, 4, 5), relu=False)),  # negative maxima
     (460, dict(dim=70, seq_len=40, filters=(13, 21, 6), widths=(5, 2, 3))),      # unaligned K, ragged segments
     (7, dict(dim=24, seq_len=30, filters=(5, 7, 9), widths=(2, 3, 4), extra_reader=True)),   # not fusable
 ])
@@ -249,6 +250,7 @@ def test_fused_branches_bitwise(n, case, monkeypatch):
     (7, dict(dim=300, seq_len=256, filters=(100, 100, 100), widths=(3, 4, 5))),
     (1, dict(dim=300, seq_len=256, filters=(100, 100, 100), widths=(3, 4, 5))),
     (72, dict(dim=300, seq_len=256, filters=(100, 100, 100), widths=(3, 4, 5))),    # unsplit: max in the epilogue
+    (72, dict(dim=300, seq_len=256, filters=(100, 100, 100), widths=(3, 4, 5), relu=False)),
     (130, dict(dim=64, seq_len=130, filters=(64, 64), widths=(2, 3))),
     (9, dict(dim=128, seq_len=50, filters=(70, 90), widths=(2, 6))),
     (7, dict(dim=24, seq_len=9, filters=(8, 16), widths=(9, 1))),              # a branch as wide as the sequence
