@@ -578,9 +578,20 @@ __global__ __launch_bounds__(256) void vote_kernel(CombineArgs a) {
     if (bidx == 0x7fffffff) bidx = 0;        // a row with no value above -inf
     if (lane == s) pred_mine = bidx;
   }
-  // votes for this lane's prediction
+  // one broadcast per model's prediction: the votes for this lane's prediction, and
+  // for each class this lane writes
   int count = 0;
-  for (int t = 0; t < a.S; ++t) count += (__shfl(pred_mine, t, 64) == pred_mine) ? 1 : 0;
+  int votes[kCombineMaxPerLane];
+#pragma unroll
+  for (int e = 0; e < kCombineMaxPerLane; ++e) votes[e] = 0;
+  for (int t = 0; t < a.S; ++t) {
+    const int p = __shfl(pred_mine, t, 64);
+    count += p == pred_mine ? 1 : 0;
+#pragma unroll
+    for (int i = 0; i < R; ++i)
+#pragma unroll
+      for (int j = 0; j < VEC; ++j) votes[i * VEC + j] += class_of<VEC>(i, j, lane) == p ? 1 : 0;
+  }
   int key = lane < a.S ? count * 64 + (63 - lane) : -1;   // most votes, then lowest s
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) key = max(key, __shfl_xor(key, o, 64));
@@ -592,12 +603,7 @@ __global__ __launch_bounds__(256) void vote_kernel(CombineArgs a) {
   for (int i = 0; i < R; ++i) {
     float f[VEC];
 #pragma unroll
-    for (int j = 0; j < VEC; ++j) {
-      const int c = class_of<VEC>(i, j, lane);
-      int votes = 0;
-      for (int t = 0; t < a.S; ++t) votes += (__shfl(pred_mine, t, 64) == c) ? 1 : 0;
-      f[j] = (float)votes * invS;
-    }
+    for (int j = 0; j < VEC; ++j) f[j] = (float)votes[i * VEC + j] * invS;
     const int c0 = class_of<VEC>(i, 0, lane);
     if (c0 < a.C) {
       if constexpr (VEC == 4) __builtin_nontemporal_store(nt_f4{f[0], f[1], f[2], f[3]}, (nt_f4*)(prow + c0));
