@@ -116,3 +116,41 @@ def greedy_busy_loop(arrivals, B, cost, tau, delta, t_end):
             head += b
             busy_until = t + cost[b]
     return lat, disp
+
+
+def greedy_multi_busy_loop(arrivals, policies, t_end):
+    """Several servers sharing one FIFO queue, stepped literally one microsecond per
+    iteration until t_end.  At each microsecond every free server, in index order,
+    tests the two conditions of Algorithm "Inference" with its own (B, cost, tau, delta)
+    on the current queue, and the round of tests is repeated while any server
+    dispatched.  Returns (latency per request or -1, dispatch list of (start, b, server))."""
+    n = len(arrivals)
+    lat = [-1] * n
+    disp = []
+    head, arrived = 0, 0
+    busy_until = [-1] * len(policies)
+    for t in range(int(arrivals[0]) if n else 0, int(t_end) + 1):
+        while arrived < n and arrivals[arrived] <= t:
+            arrived += 1
+        again = True
+        while again:
+            again = False
+            for k, (B, cost, tau, delta) in enumerate(policies):
+                if t < busy_until[k]:
+                    continue
+                q = arrived - head
+                b = 0
+                if q >= max(B):
+                    b = max(B)
+                elif q > 0:
+                    smaller = [x for x in B if x <= q]
+                    if smaller and cost[max(smaller)] + (t - arrivals[head]) + delta >= tau:
+                        b = max(smaller)
+                if b:
+                    disp.append((t, b, k))
+                    for i in range(head, head + b):
+                        lat[i] = t + cost[b] - arrivals[i]
+                    head += b
+                    busy_until[k] = t + cost[b]
+                    again = True
+    return lat, disp

@@ -91,11 +91,16 @@ def serving_stats(latency: Sequence[int], tau: int) -> dict:
 
 
 def simulate_greedy_multi(arrivals: Sequence[int], policies) -> Tuple[List[int], list]:
-    """Several independent servers (one model each) sharing the FIFO queue: whenever a
-    server is free, visited in index order, its own greedy policy (B, cost dict, tau,
-    delta) decides a batch of the oldest queued requests for it.  Returns (latency
-    per request or -1, dispatches (start, batch size, queue length, oldest wait,
-    server))."""
+    """Several independent servers (one model each) sharing the FIFO queue (Section 5.2:
+    each model an independent server; Section 5.1: each applies the greedy policy of
+    Algorithm "Inference" whenever it is free).  At each instant the free servers are
+    visited in index order, and the visit is repeated until none of them dispatches: a
+    dispatch changes the queue (its length and its oldest request), and a server that
+    declined before it must see the new queue at the same instant.  Each takes a batch
+    of the oldest queued requests chosen by its own policy (B, cost dict, tau, delta).
+
+    Returns (latency per request or -1, dispatches (start, batch size, queue length,
+    oldest wait, server))."""
     a = [int(x) for x in arrivals]
     n = len(a)
     lat = [-1] * n
@@ -106,17 +111,21 @@ def simulate_greedy_multi(arrivals: Sequence[int], policies) -> Tuple[List[int],
     while head < n:
         while arrived < n and a[arrived] <= t:
             arrived += 1
-        for k, (B, cost, tau, delta) in enumerate(policies):
-            if (free_at[k] is not None and free_at[k] > t) or arrived == head:
-                continue
-            b = greedy_decide(B, cost, arrived - head, t - a[head], tau, delta)
-            if b == 0:
-                continue
-            disp.append((t, b, arrived - head, t - a[head], k))
-            for i in range(head, head + b):
-                lat[i] = t + cost[b] - a[i]
-            head += b
-            free_at[k] = t + cost[b]
+        again = True
+        while again:
+            again = False
+            for k, (B, cost, tau, delta) in enumerate(policies):
+                if (free_at[k] is not None and free_at[k] > t) or arrived == head:
+                    continue
+                b = greedy_decide(B, cost, arrived - head, t - a[head], tau, delta)
+                if b == 0:
+                    continue
+                disp.append((t, b, arrived - head, t - a[head], k))
+                for i in range(head, head + b):
+                    lat[i] = t + cost[b] - a[i]
+                head += b
+                free_at[k] = t + cost[b]
+                again = True
         if head >= n:
             break
         cands = [a[arrived]] if arrived < n else []
@@ -129,5 +138,7 @@ def simulate_greedy_multi(arrivals: Sequence[int], policies) -> Tuple[List[int],
                     cands.append(a[head] + tau - delta - cost[max(fitting)])
         if not cands:
             break
+        # every free server declined the final queue at t, so its deadline lies after t
+        assert min(cands) > t, (min(cands), t)
         t = min(cands)
     return lat, disp

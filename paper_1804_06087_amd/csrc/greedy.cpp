@@ -142,21 +142,28 @@ int rafiki_greedy_simulate_multi(const rafiki_greedy_policy* policies, int n_ser
   int64_t nd = 0, t = n ? a[0] : 0, head = 0, arrived = 0;
   while (head < n) {
     while (arrived < n && a[arrived] <= t) ++arrived;
-    for (int k = 0; k < n_servers; ++k) {   // free servers in index order
-      if (free_at[k] > t || arrived == head) continue;
-      const rafiki_greedy_policy& p = policies[k];
-      const int64_t qlen = arrived - head, wait = t - a[head];
-      const int32_t b = greedy_decide(p, qlen, wait);
-      if (b == 0) continue;
-      int64_t cost = 0;
-      for (int i = 0; i < p.n_sizes; ++i)
-        if (p.batch_sizes[i] == b) cost = p.cost_us[i];
-      const int64_t done = t + cost;
-      for (int64_t i = head; i < head + b; ++i) out_latency_us[i] = done - a[i];
-      if (nd < dispatch_cap) out_dispatch[nd] = {t, done, head, qlen, wait, b, k};
-      ++nd;
-      head += b;
-      free_at[k] = done;
+    // Free servers in index order, again until none dispatches: a dispatch changes the
+    // queue's length and oldest request, which a server that declined before it must
+    // see at the same instant (with costs that fall as b grows, it may now accept).
+    for (bool again = true; again;) {
+      again = false;
+      for (int k = 0; k < n_servers; ++k) {
+        if (free_at[k] > t || arrived == head) continue;
+        const rafiki_greedy_policy& p = policies[k];
+        const int64_t qlen = arrived - head, wait = t - a[head];
+        const int32_t b = greedy_decide(p, qlen, wait);
+        if (b == 0) continue;
+        int64_t cost = 0;
+        for (int i = 0; i < p.n_sizes; ++i)
+          if (p.batch_sizes[i] == b) cost = p.cost_us[i];
+        const int64_t done = t + cost;
+        for (int64_t i = head; i < head + b; ++i) out_latency_us[i] = done - a[i];
+        if (nd < dispatch_cap) out_dispatch[nd] = {t, done, head, qlen, wait, b, k};
+        ++nd;
+        head += b;
+        free_at[k] = done;
+        again = true;
+      }
     }
     if (head >= n) break;
     int64_t next = arrived < n ? a[arrived] : INT64_MAX;
@@ -165,6 +172,8 @@ int rafiki_greedy_simulate_multi(const rafiki_greedy_policy* policies, int n_ser
       else if (arrived > head) next = std::min(next, greedy_deadline(policies[k], arrived - head, a[head]));
     }
     if (next == INT64_MAX) break;   // nothing running, nothing servable, nothing arriving
+    // every free server declined the final queue at t, so each deadline lies after t
+    if (next <= t) return set_error(RAFIKI_ERR_INVALID, "internal: simulation clock did not advance");
     t = next;
   }
   *out_n_dispatch = nd;

@@ -115,3 +115,72 @@ def test_sine_arrivals_counts():
     assert np.all(np.diff(arr) >= 0) and arr.dtype == np.int64
     arr2 = wl.sine_arrivals(r_ref, T, 2 * T, 1000, seed=3)
     assert abs(len(arr2) / len(arr) - 1) < 0.02               # noise has mean zero
+
+
+# ---------------------------------------------------------------- several servers
+def _multi_golden():
+    g = json.load(open(os.path.join(GOLDEN, "greedy_multi_small.json")))
+    pols = [(p["B"], {int(k): v for k, v in p["cost"].items()}, p["tau"], p["delta"]) for p in g["policies"]]
+    return g, pols
+
+
+def test_greedy_multi_golden_example():
+    """Hand-worked two-server example, including a server whose costs fall as b grows
+    and that accepts at the same instant after the other server shrank the queue."""
+    g, pols = _multi_golden()
+    lat, disp = oracle.simulate_greedy_multi(g["arrivals"], pols)
+    assert [list(d) for d in disp] == g["expected_dispatches"]
+    assert lat == g["expected_latency"]
+
+
+def test_greedy_multi_golden_brute_force():
+    g, pols = _multi_golden()
+    lat, disp = brute.greedy_multi_busy_loop(g["arrivals"], pols, 400)
+    assert disp == [(d[0], d[1], d[4]) for d in g["expected_dispatches"]]
+    assert lat == g["expected_latency"]
+
+
+def test_greedy_multi_one_server_is_greedy():
+    """With one server the shared-queue simulation is the single-model simulation."""
+    g, cost = _golden()
+    lat, disp = oracle.simulate_greedy_multi(g["arrivals"], [(g["B"], cost, g["tau"], g["delta"])])
+    lat1, disp1 = oracle.simulate_greedy(g["arrivals"], g["B"], cost, g["tau"], g["delta"])
+    assert lat == lat1 and [d[:4] for d in disp] == [tuple(d) for d in disp1]
+    assert all(d[4] == 0 for d in disp)
+    B, cost = [16, 32, 48, 64], {16: 700, 32: 1200, 48: 1800, 64: 2300}
+    tau = 2 * cost[64]
+    for seed in (0, 4):
+        arr = wl.sine_arrivals(r_ref=64 / 2300e-6, period_us=100 * tau, duration_us=60_000, step_us=100,
+                               seed=seed)
+        lat, disp = oracle.simulate_greedy_multi(arr, [(B, cost, tau, tau // 10)])
+        lat1, disp1 = oracle.simulate_greedy(arr, B, cost, tau, tau // 10)
+        assert len(disp1) > 10
+        assert lat == lat1 and [d[:4] for d in disp] == disp1
+
+
+def _nonmonotone_policies():
+    # server 0's batch of 1 costs more than its batch of 2 or 4; server 2 is slow
+    return [([1, 2, 4], {1: 460, 2: 150, 4: 210}, 600, 50),
+            ([2, 4, 8], {2: 120, 4: 180, 8: 300}, 700, 60),
+            ([4], {4: 520}, 900, 80)]
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2, 3])
+def test_greedy_multi_matches_literal_loop(seed):
+    """Event-driven multi-server oracle == every server's loop stepped every
+    microsecond, on sine arrivals and on random bursts, with non-monotone costs."""
+    pols = _nonmonotone_policies()
+    if seed < 2:
+        arr = wl.sine_arrivals(r_ref=40_000.0, period_us=20_000, duration_us=15_000, step_us=50, seed=seed)
+    else:
+        rng = np.random.default_rng(seed)
+        arr = np.sort(np.concatenate([rng.integers(0, 12_000, size=300), np.full(7, 3000), np.full(5, 9000)]))
+    lat, disp = oracle.simulate_greedy_multi(arr, pols)
+    lat2, disp2 = brute.greedy_multi_busy_loop(arr, pols, 40_000)
+    assert len(disp) > 10 and len({d[4] for d in disp}) == 3
+    assert [(d[0], d[1], d[4]) for d in disp] == disp2 and lat == lat2
+    starts = [d[0] for d in disp]
+    assert starts == sorted(starts)                               # the clock never goes back
+    for t, b, q, w, k in disp:
+        B, cost, tau, delta = pols[k]
+        assert oracle.greedy_decide(B, cost, q, w, tau, delta) == b

@@ -147,3 +147,26 @@ def test_argument_errors():
     lib = pkg.load_library()
     assert lib.rafiki_rl_info(None, None, None, None) == RAFIKI_ERR_INVALID
     assert lib.rafiki_rl_destroy(None) == 0
+
+
+def test_multi_server_greedy_golden_native():
+    """The hand-worked two-server example (a server whose costs fall as b grows accepts
+    at the same instant after the other server shrank the queue)."""
+    g = json.load(open(os.path.join(GOLDEN, "greedy_multi_small.json")))
+    pols = [(p["B"], [p["cost"][str(b)] for b in p["B"]], p["tau"], p["delta"]) for p in g["policies"]]
+    lat, disp = pkg.greedy_simulate_multi(g["arrivals"], pols)
+    assert lat.tolist() == g["expected_latency"]
+    assert [[int(d["start_us"]), int(d["b"]), int(d["queue_len"]), int(d["oldest_wait_us"]), int(d["model"])]
+            for d in disp] == g["expected_dispatches"]
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_multi_server_greedy_nonmonotone_costs(seed):
+    pols = [([1, 2, 4], [460, 150, 210], 600, 50), ([2, 4, 8], [120, 180, 300], 700, 60), ([4], [520], 900, 80)]
+    arr = wl.sine_arrivals(r_ref=40_000.0, period_us=20_000, duration_us=15_000, step_us=50, seed=seed)
+    lat, disp = pkg.greedy_simulate_multi(arr, pols)
+    lat_o, disp_o = oracle.simulate_greedy_multi(arr, [(B, dict(zip(B, c)), t, d) for B, c, t, d in pols])
+    assert lat.tolist() == lat_o
+    assert [(int(d["start_us"]), int(d["b"]), int(d["queue_len"]), int(d["oldest_wait_us"]), int(d["model"]))
+            for d in disp] == disp_o
+    assert np.all(np.diff(disp["start_us"]) >= 0)
