@@ -324,3 +324,37 @@ def test_vote_two_models_equal_the_priority_model():
     assert (np.argmax(za, 1) != np.argmax(zb, 1)).sum() > 100
     assert np.array_equal(oracle.combine_vote([za, zb])[1], np.argmax(za, 1))
     assert np.array_equal(oracle.combine_vote([zb, za])[1], np.argmax(zb, 1))
+
+
+def test_tiny_textcnn_brute():
+    """Embedding -> three conv1d max-over-time branches -> concatenations -> FC through
+    run_model vs scalar loops: the table gather as list indexing, each branch through
+    the scalar conv1d, the joins as explicit list concatenation in width order, then the
+    scalar FC.  Non-zero biases and unequal widths make any mis-wiring visible."""
+    spec = wl.textcnn(vocab=11, seq_len=9, dim=3, filters=2, widths=(2, 3, 4), n_classes=3)
+    P = wl.gen_params(spec, 5, False, "random")
+    r = np.random.default_rng(12)
+    for lp in P.layers:
+        if lp.bias is not None:
+            lp.bias = r.standard_normal(lp.bias.shape).astype(np.float32)
+    tok = r.integers(0, 11, size=(2, 9)).astype(np.int32)
+    got = oracle.run_model(spec, P, tok)
+    table = P.layers[0].weight.tolist()
+    emb = [[table[t] for t in row] for row in tok.tolist()]
+    branches = [brute.conv1d_maxtime(emb, P.layers[i].weight.tolist(), P.layers[i].bias.tolist(), True)
+                for i in (1, 2, 3)]
+    feats = [branches[0][n] + branches[1][n] + branches[2][n] for n in range(2)]
+    ref = brute.fc(feats, P.layers[-1].weight.tolist(), P.layers[-1].bias.tolist())
+    assert got.shape == (2, 3)
+    assert np.allclose(got, np.array(ref), atol=1e-12)
+    # a wrong join order is visible at this size
+    swapped = [branches[1][n] + branches[0][n] + branches[2][n] for n in range(2)]
+    assert not np.allclose(got, np.array(brute.fc(swapped, P.layers[-1].weight.tolist(),
+                                                  P.layers[-1].bias.tolist())), atol=1e-6)
+
+
+def test_concat_brute():
+    a = rng.standard_normal((3, 4))
+    b = rng.standard_normal((3, 2))
+    ref = [list(a[i]) + list(b[i]) for i in range(3)]
+    assert np.array_equal(oracle.concat(a, b), np.array(ref))
