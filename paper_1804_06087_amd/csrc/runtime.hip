@@ -851,6 +851,29 @@ TraceTile& trace_tile() {
                                  trace_tile().cfg, trace_tile().splits});                           \
   } while (0)
 
+// Size limits of the kernels at max_batch, checked by create's validation pass so
+// that no infer meets one partway through a forward pass.  The bf16 GEMM addresses its
+// input and weights through 32-bit buffer offsets (each below 2 GiB), and every kernel
+// numbers the GEMM rows n * Ho * Wo with int.  (A GEMM that gathers embedding rows reads
+// only the table, but is checked against the embedded sequence it replaces, which the
+// validation pass cannot tell apart.)
+int check_limits(const rafiki_ensemble_s* e, int mi, const Model& M) {
+  const long long nb = e->max_batch, es = (long long)e->esz();
+  for (size_t i = 0; i < M.ops.size(); ++i) {
+    const Op& op = M.ops[i];
+    if (op.kind != O_CONV && op.kind != O_CONV1D) continue;
+    const std::string ln = lname(mi, op.out);
+    if (nb * op.Ho * op.Wo >= (1LL << 31))
+      return fail(RAFIKI_ERR_UNSUPPORTED, ln + "max_batch * output positions exceeds 2^31 rows; use a smaller max_batch");
+    if (e->precision != RAFIKI_BF16) continue;
+    if (nb * op.H * op.W * op.Cs_in * es >= (1LL << 31))
+      return fail(RAFIKI_ERR_UNSUPPORTED, ln + "the layer's input at max_batch exceeds 2 GiB; use a smaller max_batch");
+    if ((long long)op.Co_pad * op.Kp * es >= (1LL << 31))
+      return fail(RAFIKI_ERR_UNSUPPORTED, ln + "the layer's weights exceed 2 GiB");
+  }
+  return RAFIKI_OK;
+}
+
 int run_gemm(const rafiki_ensemble_s* e, const Op& op, ConvArgs a, hipStream_t s, int mi, int li, int cfg) {
   const double es = (double)e->esz();
   const double kalg = (double)op.kh * op.kw * op.cin_l;
@@ -1195,6 +1218,7 @@ int rafiki_ensemble_create(const rafiki_model_desc* models, int n_models, const 
   e->models.resize(n_models);
   for (int m = 0; m < n_models; ++m) {
     int rc = build_model(e.get(), m, models[m], e->models[m]);
+    if (!rc) rc = check_limits(e.get(), m, e->models[m]);
     if (rc) return rc;
   }
   int ndev = 0;
@@ -1287,6 +1311,15 @@ static int forward(rafiki_ensemble_t h, const CombineArgs& ca, const void* in, i
       if (prev[m] < 0) HIPCHK(hipStreamWaitEvent(h->models[m].stream, h->staged_ev, 0));
       rounds = std::max(rounds, h->models[m].ops.size() + off[m]);
     }
+    // On an error partway, the caller's stream still waits for whatever the model
+    // streams already hold (they may read the caller's batch) before it is returned.
+    auto join_after_error = [&](int code) {
+      for (int i = 0; i < ca.S; ++i) {
+        Model& M = h->models[ca.sel[i]];
+        if (hipEventRecord(M.done, M.stream) == hipSuccess) (void)hipStreamWaitEvent(s, M.done, 0);
+      }
+      return code;
+    };
     for (size_t r = 0; r < rounds; ++r)
       for (int i = 0; i < ca.S; ++i) {
         const int m = ca.sel[i];
@@ -1294,10 +1327,15 @@ static int forward(rafiki_ensemble_t h, const CombineArgs& ca, const void* in, i
         if (r < off[m]) continue;
         const size_t oi = r - off[m];
         if (oi >= M.ops.size()) continue;
-        if (oi == 0 && prev[m] >= 0) HIPCHK(hipStreamWaitEvent(M.stream, h->models[prev[m]].done, 0));
+        hipError_t st = hipSuccess;
+        if (oi == 0 && prev[m] >= 0) st = hipStreamWaitEvent(M.stream, h->models[prev[m]].done, 0);
+        if (st != hipSuccess)
+          return join_after_error(fail(RAFIKI_ERR_HIP, std::string("hipStreamWaitEvent: ") + hipGetErrorString(st)));
         rc = run_model(h, m, in, n, h->d_logits + (size_t)m * ca.ld_model, M.stream, oi, oi + 1);
-        if (rc) return rc;
-        if (oi + 1 == M.ops.size()) HIPCHK(hipEventRecord(M.done, M.stream));
+        if (rc) return join_after_error(rc);
+        if (oi + 1 == M.ops.size()) st = hipEventRecord(M.done, M.stream);
+        if (st != hipSuccess)
+          return join_after_error(fail(RAFIKI_ERR_HIP, std::string("hipEventRecord: ") + hipGetErrorString(st)));
       }
     for (int i = 0; i < ca.S; ++i) HIPCHK(hipStreamWaitEvent(s, h->models[ca.sel[i]].done, 0));
   } else {

@@ -182,3 +182,20 @@ def test_branch_fusion_keeps_validation_errors():
     bad.layers[i].input2 = len(bad.layers) - 1
     rc, _ = _create([bad], [_light_params(bad)], precision=bd.RAFIKI_BF16, opts_over=opts)
     assert rc == bd.RAFIKI_ERR_INVALID and "out of range" in bd.last_error()
+
+
+def test_oversize_max_batch_rejected_at_create():
+    """The bf16 GEMM addresses a layer's input through 32-bit offsets: VGG-16's
+    224 x 224 x 64 activations exceed 2 GiB above about 334 requests.  create rejects
+    such a max_batch before any device call (so no infer meets it partway); a
+    max_batch just below the limit passes validation."""
+    s = wl.vgg16()
+    c, hh, w = s.input_shape
+    opts = {"c": c, "h": hh, "w": w}
+    rc, h = _create([s], [_light_params(s)], precision=bd.RAFIKI_BF16, max_batch=512, opts_over=opts)
+    assert rc == bd.RAFIKI_ERR_UNSUPPORTED and h.value is None
+    assert "max_batch" in bd.last_error() and "2 GiB" in bd.last_error()
+    import torch
+    if not torch.cuda.is_available():
+        rc, _ = _create([s], [_light_params(s)], precision=bd.RAFIKI_BF16, max_batch=333, opts_over=opts)
+        assert rc == bd.RAFIKI_ERR_HIP, bd.last_error()
