@@ -162,6 +162,24 @@ int rafiki_ensemble_infer(rafiki_ensemble_t h, const void* batch, int n, uint32_
 int rafiki_ensemble_infer_vote(rafiki_ensemble_t h, const void* batch, int n, uint32_t model_subset_mask,
                                float* out_votes, int32_t* out_labels, void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc): serve one batch exactly like
+ * rafiki_ensemble_infer (same arguments, rules, kernels and bitwise-identical
+ * results), but the call's scratch -- the split-K partial sums of every selected
+ * model's GEMMs and the keys of the fused max-over-time epilogues -- lives in a static
+ * device array of the library (64 MiB per GPU, allocated when the library's code is
+ * loaded on that GPU and held until the process ends) instead of the handle's
+ * workspace.  It calls no hipMalloc / hipFree.  A call whose scratch exceeds 64 MiB
+ * returns RAFIKI_ERR_UNSUPPORTED before enqueueing anything (the largest needs are
+ * deep split-K layers at large n: use infer there).  The keys are cleared on `stream`
+ * at the start of every call; the array otherwise keeps the last call's contents.
+ * Every call on one GPU, from any handle, shares that GPU's array: calls whose work
+ * overlaps on the device race (issue them on one stream, or order them with events).
+ * Like infer, the first call with a new n (or a new (n, mask) with three or more
+ * models) blocks while it tunes. */
+int rafiki_ensemble_infer_noalloc(rafiki_ensemble_t h, const void* batch, int n, uint32_t model_subset_mask,
+                                  float* out_probs, int32_t* out_labels, void* stream);
+
 /* Run model `model` alone and write its fp32 logits [n, n_classes] to out_logits.
  * Same argument rules as infer.  Enqueue-only on `stream`. */
 int rafiki_ensemble_model_logits(rafiki_ensemble_t h, int model, const void* batch, int n,

@@ -20,7 +20,7 @@ RAFIKI_OK, RAFIKI_ERR_INVALID, RAFIKI_ERR_UNSUPPORTED, RAFIKI_ERR_NOMEM, RAFIKI_
 RAFIKI_FP32, RAFIKI_BF16 = 0, 1
 RAFIKI_INPUT_IMAGE_NCHW_F32, RAFIKI_INPUT_TOKENS_I32 = 0, 1
 EXPORTED = ("rafiki_ensemble_create", "rafiki_ensemble_infer", "rafiki_ensemble_infer_vote",
-            "rafiki_ensemble_model_logits",
+            "rafiki_ensemble_infer_noalloc", "rafiki_ensemble_model_logits",
             "rafiki_ensemble_info", "rafiki_ensemble_trace", "rafiki_ensemble_trace_read",
             "rafiki_tile_config", "rafiki_ensemble_force_tile", "rafiki_ensemble_get_schedule",
             "rafiki_ensemble_set_schedule", "rafiki_ensemble_use_graphs",
@@ -99,6 +99,8 @@ def load_library(path: str = LIB_PATH):
                                           C.c_void_p]
     lib.rafiki_ensemble_infer_vote.argtypes = [C.c_void_p, C.c_void_p, C.c_int, C.c_uint32, C.c_void_p,
                                                C.c_void_p, C.c_void_p]
+    lib.rafiki_ensemble_infer_noalloc.argtypes = [C.c_void_p, C.c_void_p, C.c_int, C.c_uint32, C.c_void_p,
+                                                  C.c_void_p, C.c_void_p]
     lib.rafiki_ensemble_model_logits.argtypes = [C.c_void_p, C.c_int, C.c_void_p, C.c_int, C.c_void_p, C.c_void_p]
     lib.rafiki_ensemble_info.argtypes = [C.c_void_p, C.POINTER(C.c_int), C.POINTER(C.c_int), C.POINTER(C.c_int)]
     lib.rafiki_ensemble_destroy.argtypes = [C.c_void_p]
@@ -473,6 +475,11 @@ class Ensemble:
         lowest-numbered selected model's class."""
         _check(self._lib.rafiki_ensemble_infer_vote(self._h, _ptr(batch), n, mask, _ptr(out_votes),
                                                     _ptr(out_labels), _stream(stream)))
+
+    def infer_noalloc(self, batch, n: int, mask: int, out_probs, out_labels, stream=None):
+        """infer with the call's scratch in the library's static device array (no allocation)."""
+        _check(self._lib.rafiki_ensemble_infer_noalloc(self._h, _ptr(batch), n, mask, _ptr(out_probs),
+                                                       _ptr(out_labels), _stream(stream)))
 
     def model_logits(self, model: int, batch, n: int, out_logits, stream=None):
         _check(self._lib.rafiki_ensemble_model_logits(self._h, model, _ptr(batch), n, _ptr(out_logits),

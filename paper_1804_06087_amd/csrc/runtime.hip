@@ -21,6 +21,7 @@
 #include <cstdlib>
 #include <map>
 #include <memory>
+#include <mutex>
 #include <string>
 #include <thread>
 #include <vector>
@@ -203,6 +204,10 @@ struct rafiki_ensemble_s {
   hipStream_t capture_stream = nullptr;
   void* d_tokens = nullptr;         // token ids copied here when a graph reads them
   long long graph_replays = 0, graph_failures = 0;
+  // Device address of the library's static scratch array on this handle's device
+  // (resolved at create; null with the reason in scratch_err if that failed).
+  void* scratch = nullptr;
+  std::string scratch_err;
   size_t esz() const { return precision == RAFIKI_BF16 ? 2 : 4; }
   void drop_graphs() {
     for (auto& kv : graphs) {
@@ -851,6 +856,16 @@ TraceTile& trace_tile() {
                                  trace_tile().cfg, trace_tile().splits});                           \
   } while (0)
 
+// Per-call scratch placed outside the handle (rafiki_ensemble_infer_noalloc): for each
+// model, the split-K partial sums of its GEMMs and the keys of its epilogue maxima
+// (n rows of ldslot keys per fused op, in op order).  Null when a call uses the
+// handle's own buffers.
+struct CallScratch {
+  float* partial[32] = {};
+  size_t partial_bytes[32] = {};
+  unsigned* slot[32] = {};
+};
+
 // Size limits of the kernels at max_batch, checked by create's validation pass so
 // that no infer meets one partway through a forward pass.  The bf16 GEMM addresses its
 // input and weights through 32-bit buffer offsets (each below 2 GiB), and every kernel
@@ -874,7 +889,8 @@ int check_limits(const rafiki_ensemble_s* e, int mi, const Model& M) {
   return RAFIKI_OK;
 }
 
-int run_gemm(const rafiki_ensemble_s* e, const Op& op, ConvArgs a, hipStream_t s, int mi, int li, int cfg) {
+int run_gemm(const rafiki_ensemble_s* e, const Op& op, ConvArgs a, hipStream_t s, int mi, int li, int cfg,
+             const CallScratch* ws = nullptr) {
   const double es = (double)e->esz();
   const double kalg = (double)op.kh * op.kw * op.cin_l;
   double flops = 2.0 * a.M * op.c_out * kalg;
@@ -915,9 +931,10 @@ int run_gemm(const rafiki_ensemble_s* e, const Op& op, ConvArgs a, hipStream_t s
   } tile_scope(cfg, splits);
   if (splits > 1) {
     const Model& Mo = e->models[mi];
-    if ((size_t)splits * a.M * a.Co_pad * 4 > Mo.partial_bytes)
+    const size_t cap = ws ? ws->partial_bytes[mi] : Mo.partial_bytes;
+    if ((size_t)splits * a.M * a.Co_pad * 4 > cap)
       return fail(RAFIKI_ERR_INVALID, "internal: split-K workspace too small");
-    a.partial = Mo.d_partial;
+    a.partial = ws ? ws->partial[mi] : Mo.d_partial;
     TRACED(e, s, RAFIKI_K_CONV_MFMA, mi, li, flops, bytes, launch_conv_mfma(a, cfg, splits, s));
     TRACED(e, s, RAFIKI_K_SPLITK_REDUCE, mi, li, 0.0,
            (double)splits * a.M * a.c_write * 4.0 + out_rows * a.c_write * (a.out_f32 ? 4.0 : es),
@@ -953,7 +970,7 @@ ConvArgs gemm_args(const rafiki_ensemble_s* e, const Model& M, const Op& op, int
 }
 
 int run_model(const rafiki_ensemble_s* e, int mi, const void* in, int n, float* logits, hipStream_t s,
-              size_t op_begin = 0, size_t op_end = SIZE_MAX);
+              size_t op_begin = 0, size_t op_end = SIZE_MAX, const CallScratch* ws = nullptr);
 
 // Choose each GEMM op's tile configuration for batch size n (once per n; blocks the
 // caller).  The candidates are timed where they will run: inside forward passes of
@@ -1061,7 +1078,7 @@ int tune(rafiki_ensemble_s* e, int n, const void* in, hipStream_t s) {
 // Only ops [op_begin, op_end) are enqueued, so that the launches of several models
 // can be interleaved.
 int run_model(const rafiki_ensemble_s* e, int mi, const void* in, int n, float* logits, hipStream_t s,
-              size_t op_begin, size_t op_end) {
+              size_t op_begin, size_t op_end, const CallScratch* ws) {
   const Model& M = e->models[mi];
   const auto it = e->tuned.find(n);
   const std::vector<int> empty;
@@ -1085,8 +1102,14 @@ int run_model(const rafiki_ensemble_s* e, int mi, const void* in, int n, float* 
           void* tmp = M.d_arena + op.tmp_off;
           a.y = tmp; a.c_write = round_up(op.c_out, 8); a.ldy = a.c_write; a.out_f32 = bf ? 0 : 1;
           const bool in_epilogue = op.d_slot && choose_splits(a.M, op.c_out, a.Kp / 64) == 1;
-          if (in_epilogue) { a.maxslot = op.d_slot; a.ldslot = op.ldslot; }
-          int rc = run_gemm(e, op, a, s, mi, li, cfg);
+          unsigned* slot = op.d_slot;
+          if (ws) {   // this op's keys follow those of the model's earlier fused ops
+            slot = ws->slot[mi];
+            for (size_t j = 0; j < oi; ++j)
+              if (M.ops[j].d_slot) slot += (size_t)n * M.ops[j].ldslot;
+          }
+          if (in_epilogue) { a.maxslot = slot; a.ldslot = op.ldslot; }
+          int rc = run_gemm(e, op, a, s, mi, li, cfg, ws);
           if (rc) return rc;
           if (in_epilogue) {   // the GEMM took the max; write the concatenated vector
             ReduceSegs segs{};
@@ -1098,7 +1121,7 @@ int run_model(const rafiki_ensemble_s* e, int mi, const void* in, int n, float* 
               segs.len[i] = op.W - op.seg_kw[i] + 1;
             }
             TRACED(e, s, RAFIKI_K_POOL, mi, li, 0.0, (double)n * op.ldslot * 4.0 * 2.0 + (double)n * y.Cs * es,
-                   launch_maxslot_finish(op.d_slot, op.ldslot, yp, n, segs, s));
+                   launch_maxslot_finish(slot, op.ldslot, yp, n, segs, s));
             break;
           }
           ReduceSegs segs{};
@@ -1123,7 +1146,7 @@ int run_model(const rafiki_ensemble_s* e, int mi, const void* in, int n, float* 
         a.y = yp;
         if (y.is_logits) { a.c_write = y.c; a.ldy = y.c; a.out_f32 = 1; }
         else { a.c_write = y.Cs; a.ldy = y.Cs; a.out_f32 = bf ? 0 : 1; }
-        int rc = run_gemm(e, op, a, s, mi, li, cfg);
+        int rc = run_gemm(e, op, a, s, mi, li, cfg, ws);
         if (rc) return rc;
         break;
       }
@@ -1177,6 +1200,48 @@ int stage(const rafiki_ensemble_s* e, const void* batch, int n, hipStream_t s, v
 
 namespace rafiki {
 int set_error(int code, const std::string& msg) { return fail(code, msg); }
+
+// Scratch of rafiki_ensemble_infer_noalloc: a file-scope device array, one copy per
+// GPU, held until the process ends.  Host code never uses the array's name as an
+// address (on the host it is only a stand-in for the symbol): each device's address
+// comes from hipGetSymbolAddress, taken once per device by scratch_on_device().
+constexpr size_t kNoAllocScratchBytes = (size_t)64 << 20;
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+constexpr int kMaxScratchDevices = 64;
+
+// Address of `scratch` on the current device, resolved on the first call for that
+// device (with it current) and kept; null with *err set if the device index is out
+// of range or the lookup failed (the failure is kept too and reported again).
+void* scratch_on_device(int device, std::string* err) {
+  static std::mutex mu;
+  static void* ptr[kMaxScratchDevices] = {};
+  static std::string why[kMaxScratchDevices];
+  static bool done[kMaxScratchDevices] = {};
+  if (device < 0 || device >= kMaxScratchDevices) {
+    *err = "device index " + std::to_string(device) + " beyond the scratch table";
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> lock(mu);
+  if (!done[device]) {
+    void* p = nullptr;
+    const hipError_t st = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (st != hipSuccess || !p) {
+      (void)hipGetLastError();
+      why[device] = std::string("hipGetSymbolAddress(scratch): ") + hipGetErrorString(st);
+      p = nullptr;
+    }
+    ptr[device] = p;
+    done[device] = true;
+  }
+  if (!ptr[device]) *err = why[device];
+  return ptr[device];
+}
+
+__global__ void zero_u32_kernel(unsigned* p, long long count) {
+  const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < count) p[i] = 0u;
+}
 }  // namespace rafiki
 
 extern "C" {
@@ -1259,6 +1324,8 @@ int rafiki_ensemble_create(const rafiki_model_desc* models, int n_models, const 
     rc = dev_alloc(e.get(), &e->d_tokens, (size_t)e->max_batch * e->H * 4);
     if (rc) return rc;
   }
+  // the no-alloc variant's scratch on this device (a failure only disables that call)
+  e->scratch = scratch_on_device(e->device, &e->scratch_err);
   {
     hipError_t st2 = hipEventCreateWithFlags(&e->staged_ev, hipEventDisableTiming);
     if (st2 == hipSuccess) st2 = hipStreamCreateWithFlags(&e->capture_stream, hipStreamNonBlocking);
@@ -1279,7 +1346,7 @@ int rafiki_ensemble_create(const rafiki_model_desc* models, int n_models, const 
 // that every model stream has work from the start even when enqueueing is slower than
 // the device.
 static int forward(rafiki_ensemble_t h, const CombineArgs& ca, const void* in, int n, hipStream_t s,
-                   rafiki_ensemble_s::Sched sched) {
+                   rafiki_ensemble_s::Sched sched, const CallScratch* ws = nullptr) {
   const int solo = sched.solo;
   int rc = RAFIKI_OK;
   const bool fork = h->concurrent && (!h->trace.on || h->trace.concurrent) && ca.S > 1;
@@ -1331,7 +1398,7 @@ static int forward(rafiki_ensemble_t h, const CombineArgs& ca, const void* in, i
         if (oi == 0 && prev[m] >= 0) st = hipStreamWaitEvent(M.stream, h->models[prev[m]].done, 0);
         if (st != hipSuccess)
           return join_after_error(fail(RAFIKI_ERR_HIP, std::string("hipStreamWaitEvent: ") + hipGetErrorString(st)));
-        rc = run_model(h, m, in, n, h->d_logits + (size_t)m * ca.ld_model, M.stream, oi, oi + 1);
+        rc = run_model(h, m, in, n, h->d_logits + (size_t)m * ca.ld_model, M.stream, oi, oi + 1, ws);
         if (rc) return join_after_error(rc);
         if (oi + 1 == M.ops.size()) st = hipEventRecord(M.done, M.stream);
         if (st != hipSuccess)
@@ -1341,7 +1408,7 @@ static int forward(rafiki_ensemble_t h, const CombineArgs& ca, const void* in, i
   } else {
     for (int i = 0; i < ca.S; ++i) {
       const int m = ca.sel[i];
-      rc = run_model(h, m, in, n, h->d_logits + (size_t)m * ca.ld_model, s);
+      rc = run_model(h, m, in, n, h->d_logits + (size_t)m * ca.ld_model, s, 0, SIZE_MAX, ws);
       if (rc) return rc;
     }
   }
@@ -1355,7 +1422,7 @@ static int forward(rafiki_ensemble_t h, const CombineArgs& ca, const void* in, i
 // the choice never changes a result.  With fewer than three models, when tracing, or
 // with model streams off, the models run as before (all concurrent).
 static int pick_schedule(rafiki_ensemble_t h, const CombineArgs& ca, const void* in, int n, uint32_t mask,
-                         hipStream_t s, rafiki_ensemble_s::Sched* sched) {
+                         hipStream_t s, rafiki_ensemble_s::Sched* sched, const CallScratch* ws = nullptr) {
   *sched = {};
   if (ca.S < 3 || !h->concurrent || (h->trace.on && !h->trace.concurrent)) return RAFIKI_OK;
   const auto key = std::make_pair(n, mask);
@@ -1384,7 +1451,7 @@ static int pick_schedule(rafiki_ensemble_t h, const CombineArgs& ca, const void*
     float t = 1e30f;
     for (int rep = 0; rep < 3 && rc == RAFIKI_OK; ++rep) {   // best of three
       st = hipEventRecord(ev[0], s);
-      if (st == hipSuccess) rc = forward(h, ca, in, n, s, cand);
+      if (st == hipSuccess) rc = forward(h, ca, in, n, s, cand, ws);
       if (st == hipSuccess && rc == RAFIKI_OK) st = hipEventRecord(ev[1], s);
       if (st == hipSuccess && rc == RAFIKI_OK) st = hipEventSynchronize(ev[1]);
       float ms = 0.f;
@@ -1446,7 +1513,7 @@ static int graph_for(rafiki_ensemble_t h, int n, uint32_t mask, const CombineArg
 // One scheduled batch through the selected models, then the mean (vote = false) or
 // majority-vote (vote = true) combine into out / out_labels.
 static int serve(rafiki_ensemble_t h, const void* batch, int n, uint32_t model_subset_mask, float* out,
-                 int32_t* out_labels, void* stream, bool vote) {
+                 int32_t* out_labels, void* stream, bool vote, const CallScratch* ws = nullptr) {
   int rc = check_call(h, batch, n);
   if (rc) return rc;
   if (!out || !out_labels) return fail(RAFIKI_ERR_INVALID, "null output pointer");
@@ -1462,7 +1529,7 @@ static int serve(rafiki_ensemble_t h, const void* batch, int n, uint32_t model_s
     if ((model_subset_mask >> m) & 1u) ca.sel[ca.S++] = m;
   // With graphs on, a graph replays the forward passes once this batch size is tuned;
   // tracing, and a batch size seen for the first time, run them eagerly.
-  const bool graph = h->use_graphs && !h->trace.on && h->tuned.count(n);
+  const bool graph = h->use_graphs && !h->trace.on && h->tuned.count(n) && !ws;
   if (graph) {
     const void* in = h->input_kind == RAFIKI_INPUT_IMAGE_NCHW_F32 ? h->d_staged : h->d_tokens;
     rc = stage(h, batch, n, s, h->d_staged);
@@ -1487,8 +1554,8 @@ static int serve(rafiki_ensemble_t h, const void* batch, int n, uint32_t model_s
     rc = stage(h, batch, n, s, h->d_staged);
     if (!rc) rc = tune(h, n, in, s);
     rafiki_ensemble_s::Sched sched;
-    if (!rc) rc = pick_schedule(h, ca, in, n, model_subset_mask, s, &sched);
-    if (!rc) rc = forward(h, ca, in, n, s, sched);
+    if (!rc) rc = pick_schedule(h, ca, in, n, model_subset_mask, s, &sched, ws);
+    if (!rc) rc = forward(h, ca, in, n, s, sched, ws);
     if (rc) return rc;
   }
   const double cbytes = (double)n * h->n_classes * 4.0 * (ca.S + 1) + 4.0 * n;
@@ -1510,6 +1577,52 @@ int rafiki_ensemble_infer(rafiki_ensemble_t h, const void* batch, int n, uint32_
 int rafiki_ensemble_infer_vote(rafiki_ensemble_t h, const void* batch, int n, uint32_t model_subset_mask,
                                float* out_votes, int32_t* out_labels, void* stream) {
   return serve(h, batch, n, model_subset_mask, out_votes, out_labels, stream, true);
+}
+
+int rafiki_ensemble_infer_noalloc(rafiki_ensemble_t h, const void* batch, int n, uint32_t model_subset_mask,
+                                  float* out_probs, int32_t* out_labels, void* stream) {
+  int rc = check_call(h, batch, n);
+  if (rc) return rc;
+  if (model_subset_mask == 0) return fail(RAFIKI_ERR_INVALID, "model_subset_mask must select at least one model");
+  if (h->n_models < 32 && (model_subset_mask >> h->n_models) != 0)
+    return fail(RAFIKI_ERR_INVALID, "model_subset_mask selects a model that does not exist");
+  if (!h->scratch) return fail(RAFIKI_ERR_HIP, "no-alloc scratch unavailable: " + h->scratch_err);
+  // Layout for this call: every selected model's epilogue-max keys first (one range,
+  // cleared below), then each model's split-K partial sums, 256-byte aligned.
+  CallScratch ws;
+  char* base = (char*)h->scratch;
+  size_t off = 0;
+  for (int m = 0; m < h->n_models; ++m) {
+    if (!((model_subset_mask >> m) & 1u)) continue;
+    ws.slot[m] = (unsigned*)(base + off);
+    for (const Op& op : h->models[m].ops)
+      if (op.d_slot) off += (size_t)n * op.ldslot * 4;
+    off = round_up_sz(off, 256);
+  }
+  const size_t slot_bytes = off;
+  for (int m = 0; m < h->n_models; ++m) {
+    if (!((model_subset_mask >> m) & 1u) || h->precision != RAFIKI_BF16) continue;
+    size_t need = 0;
+    for (const Op& op : h->models[m].ops) {
+      if (op.kind != O_CONV && op.kind != O_CONV1D) continue;
+      const int rows = n * op.Ho * op.Wo;
+      const int sp = choose_splits(rows, op.c_out, op.Kp / 64);
+      if (sp > 1) need = std::max(need, (size_t)sp * rows * op.Co_pad * 4);
+    }
+    ws.partial[m] = (float*)(base + off);
+    ws.partial_bytes[m] = need;
+    off = round_up_sz(off + need, 256);
+  }
+  if (off > kNoAllocScratchBytes)
+    return fail(RAFIKI_ERR_UNSUPPORTED, "this call needs " + std::to_string(off) + " bytes of scratch; the no-alloc "
+                "scratch holds " + std::to_string(kNoAllocScratchBytes) + " (use a smaller n or fewer models, or infer)");
+  hipStream_t s = (hipStream_t)stream;
+  if (slot_bytes) {   // the maxima start from the zero key; the array keeps the last call's contents
+    const long long words = (long long)(slot_bytes / 4);
+    launch(zero_u32_kernel, dim3((unsigned)((words + 255) / 256)), dim3(256), s, (unsigned*)base, words);
+    HIPCHK(hipGetLastError());
+  }
+  return serve(h, batch, n, model_subset_mask, out_probs, out_labels, stream, false, &ws);
 }
 
 int rafiki_ensemble_model_logits(rafiki_ensemble_t h, int model, const void* batch, int n, float* out_logits,
