@@ -15,6 +15,17 @@ pytestmark = pytest.mark.gpu
 DEV = torch.device("cuda:0")
 
 
+def labels_vs_oracle(lab, p_ref):
+    """Labels equal the oracle's first-index argmax of its fp64 mean probabilities,
+    except where its top-2 differ by < 1e-3; there the label must be within 1e-3 of
+    the top."""
+    srt = np.sort(p_ref, 1)
+    ref = oracle.argmax_first(p_ref)
+    mism = np.nonzero(lab != ref)[0]
+    assert ((srt[mism, -1] - srt[mism, -2]) < 1e-3).all(), f"label mismatches at rows {mism}"
+    assert (p_ref[mism, lab[mism]] >= srt[mism, -1] - 1e-3).all()
+
+
 @pytest.mark.parametrize("S,n,C", [(3, 37, 1000), (1, 5, 10), (32, 9, 7), (2, 130, 1024)])
 def test_combine_mean_and_vote(S, n, C):
     rng = np.random.Generator(np.random.PCG64(S * 1000 + n))
@@ -27,9 +38,8 @@ def test_combine_mean_and_vote(S, n, C):
     torch.cuda.synchronize()
     p_ref = oracle.combine_mean([oracle.softmax(z[s].astype(np.float64)) for s in range(S)])
     assert np.abs(p.cpu().numpy() - p_ref).max() <= 1e-6
-    # first-index argmax of the fp32 result itself (ties are real in row 0)
-    assert np.array_equal(lab.cpu().numpy(), oracle.argmax_first(p.cpu().numpy().astype(np.float64)))
-    assert lab[0].item() == 0
+    labels_vs_oracle(lab.cpu().numpy(), p_ref)
+    assert lab[0].item() == 0                         # exact ties: the lowest index
     v = torch.empty((n, C), dtype=torch.float32, device=DEV)
     combine_vote(zt, v, lab)
     torch.cuda.synchronize()
@@ -53,7 +63,7 @@ def test_combine_unaligned_buffers():
     torch.cuda.synchronize()
     p_ref = oracle.combine_mean([oracle.softmax(z[s].astype(np.float64)) for s in range(S)])
     assert np.abs(p.cpu().numpy() - p_ref).max() <= 1e-6
-    assert np.array_equal(lab.cpu().numpy(), oracle.argmax_first(p.cpu().numpy().astype(np.float64)))
+    labels_vs_oracle(lab.cpu().numpy(), p_ref)
     combine_vote(zt, p, lab)
     torch.cuda.synchronize()
     v_ref, l_ref = oracle.combine_vote([z[s] for s in range(S)])

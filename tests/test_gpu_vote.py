@@ -8,6 +8,8 @@ The vote is integer work on top of each model's logits, so it is checked in two 
   except on rows whose oracle top-2 logit gap lies within twice the logit tolerance
   (fp32: 1e-4, bf16: 2e-2, row-normwise), where rounding may legitimately flip it.
 """
+import os
+
 import numpy as np
 import pytest
 import torch
@@ -143,11 +145,14 @@ def test_vote_32_models_full_mask():
 
 
 def test_vote_c3_full_batch(c3_vote_ens):
-    ens, specs, params, batch, rows, zb = c3_vote_ens
+    """Every row of the batch of 64: each model's prediction against the oracle's
+    (stored fp64 logits, both modes), then the exact vote."""
+    ens, specs, params, batch, ref = c3_vote_ens
     n, C = 64, 1000
     zg = [run_logits(ens, batch, n, m, C) for m in range(3)]
     for m in range(3):
-        check_predictions(zg[m][rows], zb[m], 2e-2)
+        for mode in ("bf16", "exact"):
+            check_predictions(zg[m], ref[f"{mode}_m{m}"][:n], 2e-2)
     for mask in (0b111, 0b101, 0b011):
         v, lab = run_vote(ens, batch, n, mask, C)
         check_combine_exact(v, lab, [zg[m] for m in range(3) if (mask >> m) & 1])
@@ -156,10 +161,10 @@ def test_vote_c3_full_batch(c3_vote_ens):
 @pytest.fixture(scope="module")
 def c3_vote_ens():
     cfg, specs, params, batch = wl.build_config(3)
-    rows = [0, 17, 63]
-    zb = [oracle.run_model(s, p, batch[rows], act="bf16", chunk=2) for s, p in zip(specs, params)]
+    ref = np.load(os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden",
+                               "oracle_logits_r50_vgg16_r101_n256.npz"))
     ens = Ensemble(specs, params, precision="bf16", max_batch=64)
-    yield ens, specs, params, batch, rows, zb
+    yield ens, specs, params, batch, ref
     ens.close()
 
 
