@@ -76,6 +76,10 @@ def parse():
                     help="HBM bandwidth of the path's memory-bound kernels called on their own (combine, vote, "
                          "max-pool, global average pool) at ImageNet-shaped sizes, against the 8 TB/s peak and a "
                          "plain device copy; one JSON line per kernel")
+    ap.add_argument("--peaks", action="store_true",
+                    help="the device's own ceilings: a register-resident bf16 MFMA loop (TFLOP/s) at 1, 2 and 4 "
+                         "wavefronts per SIMD, a 4 GiB streaming read and a 2 GiB device copy (GB/s); one JSON "
+                         "line each")
     ap.add_argument("--layers", action="store_true",
                     help="per-launch roofline of one workload (--workload, --n): traced steps with the models "
                          "one after another; for every launch its own bound max(FLOPs / 2.5 PFLOP/s, bytes / 8 TB/s) "
@@ -383,13 +387,92 @@ def memory_main(args, dev):
         del x, y
 
 
+def peaks_main(args, dev):
+    """Measured ceilings of this MI355X: the kernels' rooflines use the published peaks
+    (2.5 PFLOP/s bf16 dense, 8 TB/s); these probes show what the device delivers to a
+    kernel that does nothing else.  MFMA: 256 workgroups x 4 wavefronts per pass over the
+    256 compute units (1, 2 or 4 wavefronts per SIMD), each wavefront 8 independent
+    32x32x16 bf16 MFMAs per iteration on register operands.  HBM: one 16-byte streaming
+    read pass over 4 GiB (16x the last-level cache), and a device-to-device copy of
+    2 GiB (read + write).  Best of 10 timings after 2 warm-ups, HIP events."""
+    import torch
+
+    from paper_1804_06087_amd.binding import probe_mfma_bf16, probe_hbm_read
+
+    def best_ms(fn, reps=10):
+        for _ in range(2):
+            fn()
+        torch.cuda.synchronize()
+        t = 1e30
+        for _ in range(reps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            fn()
+            b.record()
+            b.synchronize()
+            t = min(t, a.elapsed_time(b))
+        return t
+
+    def emit(name, value, unit, peak, cfg, ms):
+        print(json.dumps({"metric": f"measured ceiling: {name}", "value": round(value, 1), "unit": unit,
+                          "higher_is_better": True, "n_gpus": 1, "dtype": "bf16" if "MFMA" in name else "u8",
+                          "data": "synthetic", "config": cfg, "ms": round(ms, 4),
+                          "of_published_peak": round(value / peak, 4), "published_peak": peak}), flush=True)
+
+    iters = 20000
+    for per_simd in (1, 2, 4):
+        blocks = 256 * per_simd
+        out = torch.empty(blocks * 4, dtype=torch.float32, device=dev)
+        ms = best_ms(lambda: probe_mfma_bf16(blocks, iters, out))
+        flops = blocks * 4 * iters * 8 * 32768.0
+        emit("register-resident bf16 MFMA loop", flops / (ms / 1e3) / 1e12, "TFLOP/s", PEAK_BF16_TFLOPS,
+             {"kernel": "v_mfma_f32_32x32x16_bf16", "workgroups": blocks, "waves_per_simd": per_simd,
+              "iterations": iters}, ms)
+    nbytes = 4 << 30
+    x = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    x.fill_(7)
+    blocks = 256 * 8
+    out = torch.empty(blocks * 4, dtype=torch.int32, device=dev)
+    ms = best_ms(lambda: probe_hbm_read(x, blocks, out))
+    emit("HBM streaming read", nbytes / (ms / 1e3) / 1e9, "GB/s", PEAK_HBM_GBS,
+         {"kernel": "16-byte nontemporal loads", "bytes": nbytes, "workgroups": blocks}, ms)
+    del x
+    src = torch.empty(1 << 29, dtype=torch.float32, device=dev).fill_(1.0)
+    dst = torch.empty_like(src)
+    ms = best_ms(lambda: dst.copy_(src))
+    emit("device copy (read + write)", 2 * src.numel() * 4 / (ms / 1e3) / 1e9, "GB/s", PEAK_HBM_GBS,
+         {"kernel": "torch copy_", "bytes_read": src.numel() * 4, "bytes_written": src.numel() * 4}, ms)
+
+
+def sweep_cpu_baseline(specs, params, pool, n, mask):
+    """The fp64 oracle (as is) over the first n requests and the selected models: one
+    timed run after a one-request warm-up; images/s on the host cores."""
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:
+        cores = os.cpu_count() or 1
+    oracle.ensemble(specs, params, pool[:1], mask)
+    t0 = time.perf_counter()
+    oracle.ensemble(specs, params, pool[:n], mask)
+    dt = time.perf_counter() - t0
+    return {"value": round(n / dt, 4), "unit": "images/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"all {n} requests of the point, selected models, fp64 NumPy oracle, one run of {dt:.1f} s"}
+
+
 def sweep_main(args, dev):
     """Latency/accuracy trade-off grid (Section 5.2): every subset of the ImageNet-shaped
     ensemble at every batch size, one handle (max batch 256) over one 256-image draw whose
     prefixes are the batches.  Per point: 20 warm-up calls, then timed calls each bracketed
     by events on the launch stream and synchronised; p50/p99 latency, images/s = n / p50.
     At n <= 4 also the cold latency: before each of 50 timed calls a 1 GiB buffer is
-    written (outside the events), which evicts the weights from the last-level cache."""
+    written (outside the events), which evicts the weights from the last-level cache.
+    Roofline per point: the algorithmic FLOPs and bytes of the call's launches (from one
+    traced call) against p50 -- the MFMA fraction, and the fraction of the sum of the
+    launches' own bounds max(FLOPs / 2.5 PFLOP/s, bytes / 8 TB/s).  CPU baseline at n =
+    1, 16 and 64: the fp64 oracle over the same n requests and subset, timed once after
+    a one-request warm-up (the n <= 64 points only; nothing is extrapolated)."""
     import numpy as np
     import torch
 
@@ -422,6 +505,24 @@ def sweep_main(args, dev):
                 lat.append(a.elapsed_time(b))
             lat = np.array(lat)
             p50 = float(np.percentile(lat, 50))
+            # algorithmic work of one call (launches traced one after another)
+            ens.trace(True)
+            ens.infer(x, n, mask, probs, labels, stream)
+            torch.cuda.synchronize()
+            recs = ens.trace_read()
+            ens.trace(False)
+            flops = sum(r["flops"] for r in recs)
+            nbytes = sum(r["bytes"] for r in recs)
+            bound_ms = sum(max(r["flops"] / (PEAK_BF16_TFLOPS * 1e9), r["bytes"] / (PEAK_HBM_GBS * 1e6))
+                           for r in recs)
+            tflops = flops / (p50 / 1e3) / 1e12
+            roof = {"bound": "mfma" if flops / (PEAK_BF16_TFLOPS * 1e9) >= nbytes / (PEAK_HBM_GBS * 1e6) else "hbm",
+                    "achieved": round(tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                    "frac": round(tflops / PEAK_BF16_TFLOPS, 4), "alg_gflop": round(flops / 1e9, 2),
+                    "alg_gbytes": round(nbytes / 1e9, 3), "of_launch_roofline": round(bound_ms / p50, 4)}
+            cpu = None
+            if n in (1, 16, 64) and not args.no_cpu_baseline:
+                cpu = sweep_cpu_baseline(specs, params, pool, n, mask)
             cold = None
             if n <= 4:
                 cl = []
@@ -443,7 +544,7 @@ def sweep_main(args, dev):
                            + f", batch {n} of 3x224x224", "mask": mask, "global_batch": n,
                            "schedule": schedule_desc(ens, n, mask, names)},
                 "p50_ms": round(p50, 4), "p99_ms": round(float(np.percentile(lat, 99)), 4),
-                "calls": int(lat.size), "cold": cold}), flush=True)
+                "calls": int(lat.size), "cold": cold, "roofline": roof, "cpu_baseline": cpu}), flush=True)
     del flush
     ens.close()
 
@@ -568,6 +669,9 @@ def main():
         return
     if args.memory_kernels:
         memory_main(args, dev)
+        return
+    if args.peaks:
+        peaks_main(args, dev)
         return
     if args.layers:
         layers_main(args, dev)

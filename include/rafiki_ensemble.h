@@ -256,6 +256,18 @@ int rafiki_maxpool_nhwc_bf16(const void* x, void* y, int n, int h, int w, int c,
  * order, one rounding to bf16).  c a multiple of 8. */
 int rafiki_global_avgpool_nhwc_bf16(const void* x, void* y, int n, int h, int w, int c, void* stream);
 
+/* Diagnostics: the device's own ceilings, against which the kernels are judged.
+ * rafiki_probe_mfma_bf16: `blocks` workgroups of 4 wavefronts; each wavefront issues
+ * iters x 8 independent v_mfma_f32_32x32x16_bf16 on register-resident operands
+ * (32768 FLOP each; nothing is loaded in the loop) and writes one fp32 checksum to
+ * out[block * 4 + wave] (device, >= blocks * 4 floats).
+ * rafiki_probe_hbm_read: reads `bytes` (a multiple of 16) of device memory at x
+ * (16-byte aligned) once with 16-byte streaming loads over `blocks` workgroups of
+ * 256 threads and writes one checksum per wavefront to out (device, >= blocks * 4
+ * words).  Both enqueue on `stream` only; time them with events. */
+int rafiki_probe_mfma_bf16(int blocks, int iters, float* out, void* stream);
+int rafiki_probe_hbm_read(const void* x, long long bytes, int blocks, unsigned* out, void* stream);
+
 /* Diagnostics: tile configurations of the bf16 GEMM kernel.  Configuration `cfg`
  * (0 .. count - 1) computes output tiles of bm pixels x bn channels with `waves`
  * wavefronts, `stages` K tiles of bk channels in flight.  Every configuration sums each

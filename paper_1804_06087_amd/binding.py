@@ -25,7 +25,8 @@ EXPORTED = ("rafiki_ensemble_create", "rafiki_ensemble_infer", "rafiki_ensemble_
             "rafiki_tile_config", "rafiki_ensemble_force_tile", "rafiki_ensemble_get_schedule",
             "rafiki_ensemble_set_schedule", "rafiki_ensemble_use_graphs",
             "rafiki_ensemble_graph_stats", "rafiki_combine_mean", "rafiki_combine_vote",
-            "rafiki_maxpool_nhwc_bf16", "rafiki_global_avgpool_nhwc_bf16",
+            "rafiki_maxpool_nhwc_bf16", "rafiki_global_avgpool_nhwc_bf16", "rafiki_probe_mfma_bf16",
+            "rafiki_probe_hbm_read",
             "rafiki_ensemble_destroy", "rafiki_greedy_decide", "rafiki_greedy_simulate", "rafiki_greedy_simulate_multi",
             "rafiki_ensemble_profile", "rafiki_ensemble_serve_greedy", "rafiki_ensemble_serve_greedy_async",
             "rafiki_rl_create", "rafiki_rl_destroy", "rafiki_rl_info", "rafiki_rl_get_params", "rafiki_rl_set_params",
@@ -117,6 +118,8 @@ def load_library(path: str = LIB_PATH):
     lib.rafiki_combine_mean.argtypes = [C.c_void_p, C.c_int, C.c_int, C.c_int, C.c_void_p, C.c_void_p, C.c_void_p]
     lib.rafiki_combine_vote.argtypes = [C.c_void_p, C.c_int, C.c_int, C.c_int, C.c_void_p, C.c_void_p, C.c_void_p]
     lib.rafiki_maxpool_nhwc_bf16.argtypes = [C.c_void_p, C.c_void_p] + [C.c_int] * 7 + [C.c_void_p]
+    lib.rafiki_probe_mfma_bf16.argtypes = [C.c_int, C.c_int, C.c_void_p, C.c_void_p]
+    lib.rafiki_probe_hbm_read.argtypes = [C.c_void_p, C.c_longlong, C.c_int, C.c_void_p, C.c_void_p]
     lib.rafiki_global_avgpool_nhwc_bf16.argtypes = [C.c_void_p, C.c_void_p] + [C.c_int] * 4 + [C.c_void_p]
     P = C.POINTER
     lib.rafiki_greedy_decide.argtypes = [P(RafikiGreedyPolicy), C.c_int64, C.c_int64, P(C.c_int32)]
@@ -413,6 +416,17 @@ def maxpool_nhwc_bf16(x, y, k: int, stride: int, pad: int, stream=None):
     _expect(x, (n, h, w, c), torch.bfloat16, "x")
     _expect(y, (n, (h + 2 * pad - k) // stride + 1, (w + 2 * pad - k) // stride + 1, c), torch.bfloat16, "y")
     _check(load_library().rafiki_maxpool_nhwc_bf16(_ptr(x), _ptr(y), n, h, w, c, k, stride, pad, _stream(stream)))
+
+
+def probe_mfma_bf16(blocks: int, iters: int, out, stream=None):
+    """Register-resident bf16 MFMA loop: blocks x 4 wavefronts x iters x 8 x 32768 FLOP."""
+    _check(load_library().rafiki_probe_mfma_bf16(blocks, iters, _ptr(out), _stream(stream)))
+
+
+def probe_hbm_read(x, blocks: int, out, stream=None):
+    """One streaming pass of 16-byte loads over the bytes of device tensor x."""
+    _check(load_library().rafiki_probe_hbm_read(_ptr(x), x.numel() * x.element_size(), blocks, _ptr(out),
+                                                 _stream(stream)))
 
 
 def global_avgpool_nhwc_bf16(x, y, stream=None):

@@ -142,4 +142,9 @@ hipError_t launch_combine(const CombineArgs& a, hipStream_t s);
 // Majority vote over the same slots: probs <- vote fractions, labels <- winner.
 hipError_t launch_vote(const CombineArgs& a, hipStream_t s);
 
+// Peak probes: register-resident bf16 MFMA loop (out [blocks * 4] checksums) and a
+// streaming 16-byte read of words16 words (out [blocks * 4]).
+hipError_t launch_probe_mfma(int blocks, int iters, float* out, hipStream_t s);
+hipError_t launch_probe_read(const void* x, long long words16, int blocks, unsigned* out, hipStream_t s);
+
 }  // namespace rafiki

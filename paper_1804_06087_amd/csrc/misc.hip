@@ -620,4 +620,69 @@ hipError_t launch_vote(const CombineArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
+// ---------------------------------------------------------------- peak probes
+// Matrix-core ceiling: each wave keeps 8 independent 32x32 fp32 accumulators and
+// issues `iters` rounds of 8 v_mfma_f32_32x32x16_bf16 on register-resident operands
+// (nothing is loaded inside the loop); one checksum per wave keeps the work alive.
+typedef __bf16 probe_bf16x8 __attribute__((ext_vector_type(8)));
+typedef float probe_f32x16 __attribute__((ext_vector_type(16)));
+
+__global__ __launch_bounds__(256) void probe_mfma_kernel(int iters, float* out) {
+  probe_bf16x8 a, b;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    a[i] = (__bf16)(0.001f * (float)((threadIdx.x + i) & 7));
+    b[i] = (__bf16)(0.002f * (float)((threadIdx.x * 3 + i) & 7));
+  }
+  probe_f32x16 acc[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc[j][e] = 0.f;
+  for (int it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc[j], 0, 0, 0);
+  }
+  float t = 0.f;
+#pragma unroll
+  for (int j = 0; j < 8; ++j)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) t += acc[j][e];
+  if ((threadIdx.x & 63) == 0) out[blockIdx.x * 4 + (threadIdx.x >> 6)] = t;
+}
+
+hipError_t launch_probe_mfma(int blocks, int iters, float* out, hipStream_t s) {
+  launch(probe_mfma_kernel, dim3(blocks), dim3(256), s, iters, out);
+  return hipGetLastError();
+}
+
+// HBM read ceiling: a grid-stride pass of 16-byte streaming loads over `words16`
+// 16-byte words, folded into one value per block.
+typedef unsigned probe_u4 __attribute__((ext_vector_type(4)));
+
+__global__ __launch_bounds__(256) void probe_read_kernel(const probe_u4* __restrict__ x, long long words16,
+                                                         unsigned* out) {
+  unsigned acc = 0;
+  const long long stride = (long long)gridDim.x * blockDim.x;
+  long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  for (; i + 3 * stride < words16; i += 4 * stride) {
+    const probe_u4 v0 = __builtin_nontemporal_load(x + i), v1 = __builtin_nontemporal_load(x + i + stride);
+    const probe_u4 v2 = __builtin_nontemporal_load(x + i + 2 * stride);
+    const probe_u4 v3 = __builtin_nontemporal_load(x + i + 3 * stride);
+    const probe_u4 v = v0 ^ v1 ^ v2 ^ v3;
+    acc ^= v.x ^ v.y ^ v.z ^ v.w;
+  }
+  for (; i < words16; i += stride) {
+    const probe_u4 v = __builtin_nontemporal_load(x + i);
+    acc ^= v.x ^ v.y ^ v.z ^ v.w;
+  }
+  for (int o = 32; o > 0; o >>= 1) acc ^= __shfl_xor(acc, o, 64);
+  if ((threadIdx.x & 63) == 0) out[blockIdx.x * 4 + (threadIdx.x >> 6)] = acc;
+}
+
+hipError_t launch_probe_read(const void* x, long long words16, int blocks, unsigned* out, hipStream_t s) {
+  launch(probe_read_kernel, dim3(blocks), dim3(256), s, (const probe_u4*)x, words16, out);
+  return hipGetLastError();
+}
+
 }  // namespace rafiki

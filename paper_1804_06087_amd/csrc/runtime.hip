@@ -1732,6 +1732,23 @@ int rafiki_global_avgpool_nhwc_bf16(const void* x, void* y, int n, int h, int w,
   return RAFIKI_OK;
 }
 
+int rafiki_probe_mfma_bf16(int blocks, int iters, float* out, void* stream) {
+  if (!out) return fail(RAFIKI_ERR_INVALID, "null pointer");
+  if (blocks < 1 || iters < 1) return fail(RAFIKI_ERR_INVALID, "blocks and iters must be positive");
+  const hipError_t st = launch_probe_mfma(blocks, iters, out, (hipStream_t)stream);
+  if (st != hipSuccess) return fail(RAFIKI_ERR_HIP, std::string("probe launch: ") + hipGetErrorString(st));
+  return RAFIKI_OK;
+}
+
+int rafiki_probe_hbm_read(const void* x, long long bytes, int blocks, unsigned* out, void* stream) {
+  if (!x || !out) return fail(RAFIKI_ERR_INVALID, "null pointer");
+  if (bytes < 16 || bytes % 16 || ((uintptr_t)x & 15) || blocks < 1)
+    return fail(RAFIKI_ERR_INVALID, "bytes must be a positive multiple of 16, x 16-byte aligned, blocks >= 1");
+  const hipError_t st = launch_probe_read(x, bytes / 16, blocks, out, (hipStream_t)stream);
+  if (st != hipSuccess) return fail(RAFIKI_ERR_HIP, std::string("probe launch: ") + hipGetErrorString(st));
+  return RAFIKI_OK;
+}
+
 int rafiki_tile_config(int cfg, int* bm, int* bn, int* waves, int* stages, int* bk) {
   if (cfg < 0 || cfg >= kNumMfmaConfigs) return fail(RAFIKI_ERR_INVALID, "no such tile configuration");
   const MfmaConfig& c = kMfmaConfigs[cfg];
