@@ -36,6 +36,7 @@
 #include <stdint.h>
 
 #include "rafiki_ensemble.h"
+#include "rafiki_sched.h"
 
 #ifdef __cplusplus
 extern "C" {
@@ -100,6 +101,30 @@ int rafiki_rl_run_episode(rafiki_rl_t h, const int64_t* arrival_us, int64_t n, i
  * out_episode_reward [episodes] (may be NULL) receives each episode's total reward. */
 int rafiki_rl_train(rafiki_rl_t h, const int64_t* arrival_us, int64_t n, int episodes, double gamma, double lr,
                     double c_v, double c_e, uint64_t seed, double* out_episode_reward);
+
+/* Serve requests in real time with the agent choosing each batch (Section 5.2): at
+ * every decision the state is built from the live queue (the waits of the oldest
+ * queued requests at that instant, the agent's c(m, b) table, each model's time left),
+ * the agent picks (v, b) (mode 1: sampled with the splitmix64 stream seeded with
+ * `seed`, one uniform draw per decision; mode 2: the most probable action, lowest index
+ * on ties), and the oldest min(b, queue length) requests run through
+ * rafiki_ensemble_infer with mask v on `stream`; their output rows go to out_probs /
+ * out_labels (device, [n_requests, n_classes] / [n_requests]).  The selected models of
+ * a batch run concurrently on the one GPU inside that call and the host waits for it
+ * to complete before the next decision, so every decision sees all models free (the
+ * time-left features are zero).  Request i is row i of `requests` (device, resident
+ * before the call) and arrives arrival_us[i] microseconds after serving starts (host,
+ * non-decreasing).  Before the clock starts every subset runs once at every batch
+ * size from 1 to max(B), the sizes min(b, queue length) can take (tuning).  Logs (host, first `cap` decisions): out_dispatch[k] (start = the
+ * decision instant, end, first request, queue length, oldest wait, batch size served,
+ * model -1), out_actions[k] and out_states[k * state_dim ...]; *out_steps = the number
+ * of decisions.  out_latency_us[n_requests] (host) = completion minus arrival.  The
+ * agent must schedule n_models models and its largest size must not exceed max_batch
+ * (else RAFIKI_ERR_INVALID).  Blocks the caller until every request is served. */
+int rafiki_ensemble_serve_rl(rafiki_ensemble_t h, rafiki_rl_t agent, const void* requests, const int64_t* arrival_us,
+                             int64_t n_requests, int mode, uint64_t seed, float* out_probs, int32_t* out_labels,
+                             int64_t* out_latency_us, rafiki_dispatch* out_dispatch, int32_t* out_actions,
+                             double* out_states, int64_t cap, int64_t* out_steps, void* stream);
 
 #ifdef __cplusplus
 }

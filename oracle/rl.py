@@ -100,6 +100,44 @@ class Env:
         return self.acc[mask] * (nb - self.beta * over)
 
 
+# ---------------------------------------------------------------- sampling
+class SplitMix64:
+    """splitmix64 (Steele, Lea and Flood, "Fast splittable pseudorandom number
+    generators", 2014): the state advances by the golden-ratio increment 0x9E3779B97F4A7C15
+    and each output is the state passed through two xor-shift-multiply rounds and a final
+    xor-shift; uniform doubles in [0, 1) take the top 53 bits."""
+    M64 = (1 << 64) - 1
+
+    def __init__(self, seed: int):
+        self.x = seed & self.M64
+
+    def next(self) -> int:
+        self.x = (self.x + 0x9E3779B97F4A7C15) & self.M64
+        z = self.x
+        z = ((z ^ (z >> 30)) * 0xBF58476D1CE4E5B9) & self.M64
+        z = ((z ^ (z >> 27)) * 0x94D049BB133111EB) & self.M64
+        return z ^ (z >> 31)
+
+    def uniform(self) -> float:
+        return (self.next() >> 11) * (1.0 / 9007199254740992.0)
+
+
+def sample_action(pi: Sequence[float], u: float) -> int:
+    """Inverse-CDF draw: the first action whose running sum of probabilities (in action
+    order) exceeds u; the last action if rounding leaves the sum at or below u."""
+    c = 0.0
+    for i, p in enumerate(pi):
+        c += float(p)
+        if u < c:
+            return i
+    return len(pi) - 1
+
+
+def argmax_action(pi: Sequence[float]) -> int:
+    """The most probable action, lowest index on ties."""
+    return int(np.argmax(np.asarray(pi)))
+
+
 # ---------------------------------------------------------------- network
 def param_shapes(D: int, H: int, A: int):
     return [("W1", (H, D)), ("b1", (H,)), ("W2", (H, H)), ("b2", (H,)), ("Wp", (A, H)), ("bp", (A,)),

@@ -29,6 +29,7 @@ EXPORTED = ("rafiki_ensemble_create", "rafiki_ensemble_infer", "rafiki_ensemble_
             "rafiki_probe_hbm_read",
             "rafiki_ensemble_destroy", "rafiki_greedy_decide", "rafiki_greedy_simulate", "rafiki_greedy_simulate_multi",
             "rafiki_ensemble_profile", "rafiki_ensemble_serve_greedy", "rafiki_ensemble_serve_greedy_async",
+            "rafiki_ensemble_serve_rl",
             "rafiki_rl_create", "rafiki_rl_destroy", "rafiki_rl_info", "rafiki_rl_get_params", "rafiki_rl_set_params",
             "rafiki_rl_forward", "rafiki_rl_gradient", "rafiki_rl_adam_step", "rafiki_rl_run_episode",
             "rafiki_rl_train", "rafiki_last_error")
@@ -128,6 +129,10 @@ def load_library(path: str = LIB_PATH):
     lib.rafiki_greedy_simulate_multi.argtypes = [P(RafikiGreedyPolicy), C.c_int, P(C.c_int64), C.c_int64,
                                                  P(C.c_int64), P(RafikiDispatch), C.c_int64, P(C.c_int64)]
     D = P(C.c_double)
+    lib.rafiki_ensemble_serve_rl.argtypes = [C.c_void_p, C.c_void_p, C.c_void_p, P(C.c_int64), C.c_int64, C.c_int,
+                                             C.c_uint64, C.c_void_p, C.c_void_p, P(C.c_int64),
+                                             P(RafikiDispatch), P(C.c_int32), D, C.c_int64, P(C.c_int64),
+                                             C.c_void_p]
     lib.rafiki_rl_create.argtypes = [P(RafikiRLConfig), C.c_uint64, P(C.c_void_p)]
     lib.rafiki_rl_destroy.argtypes = [C.c_void_p]
     lib.rafiki_rl_info.argtypes = [C.c_void_p, P(C.c_int), P(C.c_int), P(C.c_int64)]
@@ -544,6 +549,26 @@ class Ensemble:
                                                             _ptr(out_probs), _ptr(out_labels), _i64p(lat), disp, cap,
                                                             C.byref(nd), _stream(stream)))
         return lat, dispatches_to_array(disp, nd.value)
+
+    def serve_rl(self, agent, requests, arrival_us, out_probs, out_labels, mode: str = "argmax", seed: int = 0,
+                 stream=None):
+        """Real-time serving with the actor-critic agent choosing (subset, batch size) per
+        decision.  Returns a dict: latency (per request), dispatches, actions and states
+        (per decision)."""
+        a = np.ascontiguousarray(arrival_us, dtype=np.int64)
+        lat = np.zeros(a.size, dtype=np.int64)
+        cap = a.size + 1
+        disp = (RafikiDispatch * cap)()
+        acts = np.zeros(cap, dtype=np.int32)
+        states = np.zeros((cap, agent.state_dim))
+        steps = C.c_int64(0)
+        _check(self._lib.rafiki_ensemble_serve_rl(self._h, agent._h, _ptr(requests), _i64p(a), a.size,
+                                                  {"sample": 1, "argmax": 2}[mode], seed, _ptr(out_probs),
+                                                  _ptr(out_labels), _i64p(lat), disp, _i32p(acts), _f64p(states),
+                                                  cap, C.byref(steps), _stream(stream)))
+        k = steps.value
+        return {"latency": lat, "dispatches": dispatches_to_array(disp, k), "actions": acts[:k],
+                "states": states[:k]}
 
     def trace(self, enable, concurrent: bool = False):
         """Per-launch timing on (models one after another, or concurrent=True: on their

@@ -5,6 +5,7 @@
 #include <string>
 
 #include "rafiki_sched.h"
+#include "rafiki_rl.h"
 
 namespace rafiki {
 
@@ -24,5 +25,21 @@ int64_t greedy_deadline(const rafiki_greedy_policy& p, int64_t queue_len, int64_
 
 // Arrival times must be non-decreasing and in [0, 2^61).
 int check_arrivals(const int64_t* a, int64_t n);
+
+// The actor-critic scheduler's pieces used by the real-time serving loop.
+struct RlAgentView {
+  int n_models, n_sizes, queue_features, state_dim, n_actions;
+  const int32_t* batch_sizes;
+  int64_t tau_us;
+};
+RlAgentView rl_view(const rafiki_rl_s* h);
+// The state of Section 5.2 from live quantities: waits [nq] of the queued requests
+// (oldest first) and each model's time left on dispatched work busy_left [n_models].
+void rl_live_state(const rafiki_rl_s* h, const int64_t* waits, int64_t nq, const int64_t* busy_left, double* s);
+// mode 1: sample from the policy with one uniform draw of the splitmix64 stream *rng;
+// mode 2: the most probable action (lowest index on ties).
+int rl_choose(const rafiki_rl_s* h, const double* s, int mode, uint64_t* rng);
+// Action index -> (subset mask, index into the batch sizes).
+void rl_action(const rafiki_rl_s* h, int action, int* mask, int* size_index);
 
 }  // namespace rafiki

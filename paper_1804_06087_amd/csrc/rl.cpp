@@ -214,7 +214,53 @@ struct Env {
 
 int check_handle(rafiki_rl_t h) { return h ? RAFIKI_OK : set_error(RAFIKI_ERR_INVALID, "null handle"); }
 
+// One action of the policy at state s (mode 1: sampled with the uniform draw u; mode 2:
+// the most probable, lowest index on ties).
+int pick_action(const rafiki_rl_s* h, const Acts& o, int mode, double u) {
+  if (mode == 2) return (int)(std::max_element(o.pi.begin(), o.pi.end()) - o.pi.begin());
+  double c = 0;
+  for (int i = 0; i < h->A; ++i) {
+    c += o.pi[i];
+    if (u < c) return i;
+  }
+  return h->A - 1;
+}
+
 }  // namespace
+
+namespace rafiki {
+
+RlAgentView rl_view(const rafiki_rl_s* h) {
+  return {h->M, h->nB, h->Lq, h->D, h->A, h->B.data(), h->tau};
+}
+
+void rl_live_state(const rafiki_rl_s* h, const int64_t* waits, int64_t nq, const int64_t* busy_left, double* s) {
+  const double tau = (double)h->tau;
+  int k = 0;
+  for (int64_t i = 0; i < std::min<int64_t>(nq, h->Lq); ++i) s[k++] = (double)waits[i] / tau;
+  while (k < h->Lq) s[k++] = 0.0;
+  for (int64_t c : h->cost) s[k++] = (double)c / tau;
+  for (int m = 0; m < h->M; ++m) s[k++] = (double)std::max<int64_t>(busy_left[m], 0) / tau;
+}
+
+int rl_choose(const rafiki_rl_s* h, const double* s, int mode, uint64_t* rng) {
+  Acts o;
+  forward(h->lay, h->theta.data(), s, o);
+  double u = 0.0;
+  if (mode == 1) {
+    SplitMix r{*rng};
+    u = r.uniform();
+    *rng = r.x;
+  }
+  return pick_action(h, o, mode, u);
+}
+
+void rl_action(const rafiki_rl_s* h, int action, int* mask, int* size_index) {
+  *mask = h->act_mask[action];
+  *size_index = h->act_j[action];
+}
+
+}  // namespace rafiki
 
 extern "C" {
 
@@ -374,17 +420,7 @@ int rafiki_rl_run_episode(rafiki_rl_t h, const int64_t* arrival_us, int64_t n, i
       act = actions_in[k];
     } else {
       forward(h->lay, h->theta.data(), s.data(), o);
-      if (mode == 2) {
-        act = (int)(std::max_element(o.pi.begin(), o.pi.end()) - o.pi.begin());
-      } else {
-        const double u = rng.uniform();
-        double c = 0;
-        act = h->A - 1;
-        for (int i = 0; i < h->A; ++i) {
-          c += o.pi[i];
-          if (u < c) { act = i; break; }
-        }
-      }
+      act = pick_action(h, o, mode, mode == 1 ? rng.uniform() : 0.0);
     }
     const int64_t t0 = env.t;
     const double r = env.step(act);

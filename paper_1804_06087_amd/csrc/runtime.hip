@@ -2002,6 +2002,74 @@ int rafiki_ensemble_serve_greedy(rafiki_ensemble_t h, const void* requests, cons
   return RAFIKI_OK;
 }
 
+int rafiki_ensemble_serve_rl(rafiki_ensemble_t h, rafiki_rl_t agent, const void* requests, const int64_t* arrival_us,
+                             int64_t n_requests, int mode, uint64_t seed, float* out_probs, int32_t* out_labels,
+                             int64_t* out_latency_us, rafiki_dispatch* out_dispatch, int32_t* out_actions,
+                             double* out_states, int64_t cap, int64_t* out_steps, void* stream) {
+  if (!h || !agent) return fail(RAFIKI_ERR_INVALID, "null handle or agent");
+  if (mode != 1 && mode != 2) return fail(RAFIKI_ERR_INVALID, "mode must be 1 (sample) or 2 (most probable)");
+  int rc = check_arrivals(arrival_us, n_requests);
+  if (!rc) rc = check_serve_outputs(requests, n_requests, out_probs, out_labels, out_latency_us, out_dispatch, cap,
+                                    out_steps);
+  if (rc) return rc;
+  if (cap > 0 && (!out_actions || !out_states)) return fail(RAFIKI_ERR_INVALID, "null action or state log");
+  const RlAgentView ag = rl_view(agent);
+  if (ag.n_models != h->n_models) return fail(RAFIKI_ERR_INVALID, "the agent schedules a different number of models");
+  if (ag.batch_sizes[ag.n_sizes - 1] > h->max_batch)
+    return fail(RAFIKI_ERR_INVALID, "the agent's largest batch size exceeds max_batch");
+  const int64_t n = n_requests;
+  const int C = h->n_classes;
+  hipStream_t s = (hipStream_t)stream;
+  std::fill(out_latency_us, out_latency_us + n, int64_t(-1));
+  *out_steps = 0;
+  // Warm up (and tune) every subset at every size a batch can take -- min(b, queue
+  // length) is any of 1 .. max(B) -- before the clock starts.
+  for (int b = 1; b <= ag.batch_sizes[ag.n_sizes - 1] && b <= n; ++b)
+    for (int v = 1; v < (1 << h->n_models); ++v) {
+      rc = serve(h, requests, b, (uint32_t)v, out_probs, out_labels, stream, false);
+      if (rc) return rc;
+    }
+  HIPCHK(hipStreamSynchronize(s));
+  std::vector<double> state(ag.state_dim);
+  std::vector<int64_t> waits((size_t)ag.queue_features), busy_left(h->n_models, 0);
+  uint64_t rng = seed;
+  int64_t k = 0, head = 0, arrived = 0;
+  const int64_t* a = arrival_us;
+  ServeClock clk;
+  while (head < n) {
+    const int64_t t = clk.now();
+    while (arrived < n && a[arrived] <= t) ++arrived;
+    const int64_t qlen = arrived - head;
+    if (qlen == 0) {
+      clk.wait_until(a[arrived]);
+      continue;
+    }
+    // Every model is free here: the previous batch has completed on the device.
+    const int64_t nq = std::min<int64_t>(qlen, ag.queue_features);
+    for (int64_t i = 0; i < nq; ++i) waits[i] = t - a[head + i];
+    rl_live_state(agent, waits.data(), nq, busy_left.data(), state.data());
+    const int act = rl_choose(agent, state.data(), mode, &rng);
+    int mask = 0, j = 0;
+    rl_action(agent, act, &mask, &j);
+    const int b = (int)std::min<int64_t>(ag.batch_sizes[j], qlen);
+    rc = serve(h, request_row(h, requests, head), b, (uint32_t)mask, out_probs + (size_t)head * C, out_labels + head,
+               stream, false);
+    if (rc) return rc;
+    HIPCHK(hipStreamSynchronize(s));
+    const int64_t done = clk.now();
+    for (int64_t i = head; i < head + b; ++i) out_latency_us[i] = done - a[i];
+    if (k < cap) {
+      out_dispatch[k] = {t, done, head, qlen, t - a[head], b, -1};
+      out_actions[k] = act;
+      std::copy(state.begin(), state.end(), out_states + (size_t)k * ag.state_dim);
+    }
+    ++k;
+    head += b;
+  }
+  *out_steps = k;
+  return RAFIKI_OK;
+}
+
 int rafiki_ensemble_serve_greedy_async(rafiki_ensemble_t h, const void* requests, const int64_t* arrival_us,
                                        int64_t n_requests, const rafiki_greedy_policy* policies, uint32_t mask,
                                        float* out_probs, int32_t* out_labels, int64_t* out_latency_us,

@@ -78,3 +78,20 @@ def test_first_adam_step_closed_form():
 def test_discounted_returns():
     assert np.allclose(rl.discounted_returns([1.0] * 5, 0.5), [(1 - 0.5 ** k) / 0.5 for k in range(5, 0, -1)])
     assert rl.discounted_returns([2.0, 0.0, 1.0], 0.9).tolist() == pytest.approx([2.0 + 0.81, 0.9, 1.0])
+
+
+def test_splitmix64_reference_sequence():
+    """The generator's published reference outputs for seed 0 (the sequence used to
+    seed the xorshift/xoroshiro family), and uniforms in [0, 1) from the top 53 bits."""
+    g = rl.SplitMix64(0)
+    assert [g.next() for _ in range(4)] == [0xE220A8397B1DCDAF, 0x6E789E6AA1B965F4, 0x06C45D188009454F,
+                                            0xF88BB8A8724C81EC]
+    g = rl.SplitMix64(0)
+    assert g.uniform() == (0xE220A8397B1DCDAF >> 11) / 2.0 ** 53
+
+
+def test_action_selection():
+    pi = [0.1, 0.2, 0.3, 0.4]
+    assert [rl.sample_action(pi, u) for u in (0.0, 0.099, 0.1, 0.35, 0.61, 0.999)] == [0, 0, 1, 2, 3, 3]
+    assert rl.sample_action([0.5, 0.5 - 1e-17], 1.0 - 1e-17) == 1       # rounding leaves the sum short: last
+    assert rl.argmax_action([0.2, 0.4, 0.4]) == 1                      # ties: lowest index

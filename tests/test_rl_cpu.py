@@ -170,3 +170,24 @@ def test_multi_server_greedy_nonmonotone_costs(seed):
     assert [(int(d["start_us"]), int(d["b"]), int(d["queue_len"]), int(d["oldest_wait_us"]), int(d["model"]))
             for d in disp] == disp_o
     assert np.all(np.diff(disp["start_us"]) >= 0)
+
+
+@pytest.mark.parametrize("seed", [0, 5])
+def test_sampled_episode_replays_with_the_oracle_generator(seed):
+    """A sampled episode's actions are the inverse-CDF draws of the policy with one
+    splitmix64 uniform per decision: replayed with the oracle's environment, the native
+    policy probabilities and the oracle's generator."""
+    cost, acc, tau, arr = _scenario(seed)
+    B = B4
+    ag = RLScheduler(B, cost, acc, tau, 1.0, queue_features=16, hidden=8, seed=seed)
+    ag.train(arr[:200], 3, seed=seed)
+    ep = ag.run_episode(arr, mode="sample", seed=1000 + seed)
+    env = rl.Env(arr, B, cost, acc, tau, 1.0, 16)
+    g = rl.SplitMix64(1000 + seed)
+    for k, a in enumerate(ep["actions"]):
+        s = env.state()
+        assert np.array_equal(s, ep["states"][k])
+        pi, _ = ag.forward(s)
+        assert rl.sample_action(pi, g.uniform()) == a
+        env.step(int(a))
+    assert env.done() and len(ep["actions"]) > 10
