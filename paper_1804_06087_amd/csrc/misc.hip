@@ -127,8 +127,62 @@ __global__ void maxpool_kernel(const void* __restrict__ x, void* y, int N, int H
   store8(y, pix * Cs + g * 8, bf16, m);
 }
 
+// 3x3 stride-2 windows (bf16): a thread takes one 8-channel group of two vertically
+// adjacent outputs (rows 2r, 2r + 1), whose windows cover input rows 4r - pad .. 4r - pad
+// + 4; all 15 loads of the 5 x 3 block are issued before any max (positions outside the
+// image are clamped into it and masked out).  Max is exact, so the result is that of
+// the one-output kernel above.
+__global__ __launch_bounds__(256) void maxpool3s2_kernel(const uint4* __restrict__ x, uint4* y, int N, int H, int W,
+                                                         int G, int Ho, int Wo, int pad) {
+  const int Hr = (Ho + 1) / 2;
+  const long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (long long)N * Hr * Wo * G) return;
+  const int g = (int)(idx % G);
+  const long long pix = idx / G;
+  const int wo = (int)(pix % Wo);
+  const long long t = pix / Wo;
+  const int r = (int)(t % Hr);
+  const long long n = t / Hr;
+  uint4 q[15];
+  bool ok[15];
+#pragma unroll
+  for (int u = 0; u < 5; ++u)
+#pragma unroll
+    for (int v = 0; v < 3; ++v) {
+      const int hi = 4 * r - pad + u, wi = 2 * wo - pad + v;
+      ok[u * 3 + v] = hi >= 0 && hi < H && wi >= 0 && wi < W;
+      const int hc = min(max(hi, 0), H - 1), wc = min(max(wi, 0), W - 1);
+      q[u * 3 + v] = x[((n * H + hc) * W + wc) * G + g];
+    }
+  float a[8], b[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) a[j] = b[j] = -INFINITY;
+#pragma unroll
+  for (int u = 0; u < 5; ++u)
+#pragma unroll
+    for (int v = 0; v < 3; ++v) {
+      if (!ok[u * 3 + v]) continue;
+      const uint4 w = q[u * 3 + v];
+      const float f[8] = {bf2f(w.x & 0xFFFFu), bf2f(w.x >> 16), bf2f(w.y & 0xFFFFu), bf2f(w.y >> 16),
+                          bf2f(w.z & 0xFFFFu), bf2f(w.z >> 16), bf2f(w.w & 0xFFFFu), bf2f(w.w >> 16)};
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        if (u <= 2) a[j] = fmaxf(a[j], f[j]);
+        if (u >= 2) b[j] = fmaxf(b[j], f[j]);
+      }
+    }
+  store8(y, ((n * Ho + 2 * r) * Wo + wo) * G * 8 + g * 8, 1, a);
+  if (2 * r + 1 < Ho) store8(y, ((n * Ho + 2 * r + 1) * Wo + wo) * G * 8 + g * 8, 1, b);
+}
+
 hipError_t launch_maxpool(const void* x, void* y, int N, int H, int W, int Cs, int Ho, int Wo, int k, int stride,
                           int pad, int bf16, hipStream_t s) {
+  if (bf16 && k == 3 && stride == 2) {
+    const long long total = (long long)N * ((Ho + 1) / 2) * Wo * (Cs / 8);
+    launch(maxpool3s2_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), s, (const uint4*)x, (uint4*)y, N, H,
+           W, Cs / 8, Ho, Wo, pad);
+    return hipGetLastError();
+  }
   const long long total = (long long)N * Ho * Wo * (Cs / 8);
   launch(maxpool_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), s, x, y, N, H, W, Cs, Ho,
                      Wo, k, stride, pad, bf16, stride >= k ? 1 : 0);
@@ -250,8 +304,57 @@ __global__ __launch_bounds__(THREADS) void spatial_reduce_kernel(const void* __r
   }
 }
 
+// Without branches and with at least 16,384 (image, 8-channel group) pairs: one thread
+// per pair reduces the positions 0 .. HW - 1 in increasing order, eight 16-byte
+// streaming loads in flight (fp32 sums; the order is fixed, so results are
+// deterministic).  Enough pairs fill the device without splitting positions, and no
+// block-level fold is needed.
+template <typename T>
+__global__ __launch_bounds__(256) void spatial_reduce_rows_kernel(const T* __restrict__ x, T* y, int N, int HW,
+                                                                  int G, int is_max) {
+  const long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (long long)N * G) return;
+  const int g = (int)(idx % G);
+  const long long n = idx / G;
+  const bool bf = sizeof(T) == 2;
+  const long long base = n * HW * (long long)G * 8 + g * 8;
+  const long long step = (long long)G * 8;
+  float acc[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) acc[j] = is_max ? -INFINITY : 0.f;
+  int p = 0;
+  for (; p + 8 <= HW; p += 8) {
+    float q[8][8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) load8_stream(x, base + (p + u) * step, bf, q[u]);
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) acc[j] = is_max ? fmaxf(acc[j], q[u][j]) : acc[j] + q[u][j];
+  }
+  for (; p < HW; ++p) {
+    float q[8];
+    load8_stream(x, base + p * step, bf, q);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[j] = is_max ? fmaxf(acc[j], q[j]) : acc[j] + q[j];
+  }
+  if (!is_max) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[j] = acc[j] * (1.0f / (float)HW);
+  }
+  store8(y, n * G * 8 + g * 8, bf, acc);
+}
+
 hipError_t launch_spatial_reduce(const void* x, void* y, int N, int HW, int Cs, int is_max, int bf16,
                                  hipStream_t s, const ReduceSegs* segs) {
+  if (!segs && (long long)N * (Cs / 8) >= 16384) {
+    const long long total = (long long)N * (Cs / 8);
+    const dim3 grid((unsigned)((total + 255) / 256));
+    if (bf16) launch(spatial_reduce_rows_kernel<bf16_t>, grid, dim3(256), s, (const bf16_t*)x, (bf16_t*)y, N, HW, Cs / 8,
+                     is_max);
+    else launch(spatial_reduce_rows_kernel<float>, grid, dim3(256), s, (const float*)x, (float*)y, N, HW, Cs / 8, is_max);
+    return hipGetLastError();
+  }
   ReduceSegs sg{};
   if (segs) {
     if (segs->n < 0 || segs->n > kMaxReduceSegs || segs->zero_from < 0 || segs->zero_from > segs->ldy)

@@ -78,7 +78,9 @@ def _nhwc_bf16(n, h, w, c, seed):
 
 
 @pytest.mark.parametrize("shape,k,s,p", [((3, 9, 11, 16), 3, 2, 1), ((2, 8, 6, 64), 2, 2, 0),
-                                         ((1, 5, 5, 8), 5, 1, 2), ((4, 13, 7, 24), 3, 3, 0)])
+                                         ((1, 5, 5, 8), 5, 1, 2), ((4, 13, 7, 24), 3, 3, 0),
+                                         ((2, 10, 10, 8), 3, 2, 0), ((1, 112, 112, 64), 3, 2, 1),
+                                         ((2, 7, 13, 72), 3, 2, 1), ((3, 8, 5, 16), 3, 2, 2)])
 def test_maxpool(shape, k, s, p):
     n, h, w, c = shape
     x, xt = _nhwc_bf16(n, h, w, c, seed=k * 10 + s)
@@ -90,7 +92,8 @@ def test_maxpool(shape, k, s, p):
     assert np.array_equal(y.float().cpu().numpy(), ref.astype(np.float32))   # max is exact
 
 
-@pytest.mark.parametrize("shape", [(3, 7, 7, 2048), (5, 1, 1, 8), (2, 16, 16, 24), (1, 254, 1, 104)])
+@pytest.mark.parametrize("shape", [(3, 7, 7, 2048), (5, 1, 1, 8), (2, 16, 16, 24), (1, 254, 1, 104),
+                                   (64, 7, 7, 2048), (70, 3, 5, 2048), (2048, 1, 3, 64)])
 def test_global_avgpool(shape):
     n, h, w, c = shape
     x, xt = _nhwc_bf16(n, h, w, c, seed=h * w)
