@@ -624,6 +624,9 @@ def schedule_desc(ens, n, mask, names):
     members = [m for m in range(len(names)) if (mask >> m) & 1]
     if len(members) == 1:
         return names[members[0]]
+    kinds = {names[m].split("#")[0] for m in members}
+    if len(kinds) == 1 and os.environ.get("RAFIKI_GROUPED", "1") != "0":
+        return f"grouped: one launch per layer for the {len(members)} {kinds.pop()} members"
     try:
         solo, asc = ens.get_schedule(n, mask)
     except Exception:

@@ -253,6 +253,7 @@ __device__ __forceinline__ void wait_tiles(int n) {
 template <int BM, int BN, int WM, int WN, int STAGES, bool ALIGNED, int KC, bool SPLIT, bool SPREAD, int OCC,
           bool TAPS = false>
 __global__ __launch_bounds__(WM * WN * 64, OCC > 0 ? OCC : 1) void conv_mfma_kernel(ConvArgs a) {
+  use_member(a);
   constexpr int NW = WM * WN;
   constexpr int WTM = BM / WM, WTN = BN / WN;      // wave tile: pixels x channels
   constexpr int TM = WTM / 32, TN = WTN / 32;
@@ -606,7 +607,8 @@ static hipError_t launch_mfma_cfg(const ConvArgs& a, int splits, hipStream_t s) 
   ConvArgs b = a;
   b.n_tiles = (a.Nc + BN - 1) / BN;
   const int m_tiles = (a.M + BM - 1) / BM;
-  dim3 grid(m_tiles * b.n_tiles, splits);
+  if (a.n_members > kMaxGroup) return hipErrorInvalidValue;
+  dim3 grid(m_tiles * b.n_tiles, splits, a.n_members > 1 ? a.n_members : 1);
   const dim3 block(WM * WN * 64);
   if (a.tap_stride > 0) {   // fused branches: aligned K order only
     if (a.Cs % 64 != 0) return hipErrorInvalidValue;
@@ -631,6 +633,7 @@ static hipError_t launch_mfma_cfg(const ConvArgs& a, int splits, hipStream_t s) 
 // One thread per (output row, 4-channel group); with a fused 2x2 max-pool an output row
 // is window q, the max over GEMM rows 4q .. 4q + 3.
 __global__ void splitk_reduce_kernel(ConvArgs a, int splits, int in_bf16) {
+  use_member(a);
   const int groups = (a.c_write + 3) / 4;
   const long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x;
   if (a.pool2) {
@@ -763,7 +766,9 @@ hipError_t launch_splitk_reduce(const ConvArgs& a, int splits, int in_bf16, hipS
   const long long total = (long long)(a.pool2 ? a.M / 4 : a.M) * ((a.c_write + 3) / 4);
   const int threads = 256;
   const long long blocks = (total + threads - 1) / threads;
-  launch(splitk_reduce_kernel, dim3((unsigned)blocks), dim3(threads), s, a, splits, in_bf16);
+  if (a.n_members > kMaxGroup) return hipErrorInvalidValue;
+  launch(splitk_reduce_kernel, dim3((unsigned)blocks, 1, a.n_members > 1 ? a.n_members : 1), dim3(threads), s, a, splits,
+         in_bf16);
   return hipGetLastError();
 }
 

@@ -28,6 +28,37 @@ inline void launch(F kernel, dim3 grid, dim3 block, hipStream_t s, Args... args)
 
 typedef uint16_t bf16_t;   // bfloat16 storage (upper half of an IEEE float)
 
+// Grouped launches: models with identical layer lists run each layer as one launch,
+// member k (up to kMaxGroup) on grid z = k with its own pointers; everything else
+// (shapes, tile, splits) is shared, so every member's outputs are those of its own
+// launch, bit for bit.
+constexpr int kMaxGroup = 4;
+struct GroupMember {
+  const void* x;
+  const void* w;
+  const float* scale;
+  const float* shift;
+  const void* res;
+  void* y;
+  float* partial;
+  unsigned* maxslot;
+};
+// Per-member input / output of the memory-bound kernels (n = 1: one tensor).
+struct GroupIO {
+  const void* x[kMaxGroup];
+  void* y[kMaxGroup];
+  unsigned* slot[kMaxGroup];
+  int n;
+};
+inline GroupIO single_io(const void* x, void* y, unsigned* slot = nullptr) {
+  GroupIO io{};
+  io.x[0] = x;
+  io.y[0] = y;
+  io.slot[0] = slot;
+  io.n = 1;
+  return io;
+}
+
 // Implicit-GEMM convolution (also FC = 1x1 conv on a 1x1 image).
 //   out[m, co] = epilogue( sum_k X[m, k] * Wp[co, k] )
 //   m = (n, ho, wo) output pixel, k = (u, v, ci) kernel tap and input channel,
@@ -76,7 +107,42 @@ struct ConvArgs {
   // order-preserving keys (max_key()), which start at 0.  nullptr: rows are stored.
   unsigned* maxslot;
   int ldslot;
+  // Grouped launch: n_members > 1 replaces x, w, scale, shift, res, y, partial and
+  // maxslot with members[blockIdx.z]'s (0 or 1: the fields above).
+  int n_members;
+  GroupMember members[kMaxGroup];
 };
+// The pointers of this workgroup's member of a grouped launch.  The members are
+// picked with constant indices only: an index computed at run time into the argument
+// struct would make the compiler copy the whole struct to scratch memory.
+__device__ __forceinline__ void use_member(ConvArgs& a) {
+  if (a.n_members > 1) {
+    const unsigned z = blockIdx.z;
+#pragma unroll
+    for (int k = 1; k < kMaxGroup; ++k) {
+      if (z == (unsigned)k) {
+        a.x = a.members[k].x;
+        a.w = a.members[k].w;
+        a.scale = a.members[k].scale;
+        a.shift = a.members[k].shift;
+        a.res = a.members[k].res;
+        a.y = a.members[k].y;
+        a.partial = a.members[k].partial;
+        a.maxslot = a.members[k].maxslot;
+      }
+    }
+    if (z == 0) {
+      a.x = a.members[0].x;
+      a.w = a.members[0].w;
+      a.scale = a.members[0].scale;
+      a.shift = a.members[0].shift;
+      a.res = a.members[0].res;
+      a.y = a.members[0].y;
+      a.partial = a.members[0].partial;
+      a.maxslot = a.members[0].maxslot;
+    }
+  }
+}
 constexpr int kMaxGatherTaps = 8;
 // Order-preserving key of a float for unsigned atomic max (0 is below every key).
 __device__ __forceinline__ unsigned max_key(float f) {
@@ -101,8 +167,12 @@ hipError_t launch_conv_f32(const ConvArgs& a, hipStream_t s);
 hipError_t launch_stage_images(const float* x, void* y, int N, int C, int H, int W, int Cs, int to_bf16,
                                hipStream_t s);
 // Max-pool k x k / stride / pad over NHWC (Cs channels).
-hipError_t launch_maxpool(const void* x, void* y, int N, int H, int W, int Cs, int Ho, int Wo, int k,
-                          int stride, int pad, int bf16, hipStream_t s);
+hipError_t launch_maxpool(const GroupIO& io, int N, int H, int W, int Cs, int Ho, int Wo, int k, int stride, int pad,
+                          int bf16, hipStream_t s);
+inline hipError_t launch_maxpool(const void* x, void* y, int N, int H, int W, int Cs, int Ho, int Wo, int k,
+                                 int stride, int pad, int bf16, hipStream_t s) {
+  return launch_maxpool(single_io(x, y), N, H, W, Cs, Ho, Wo, k, stride, pad, bf16, s);
+}
 // Branches of a fused conv1d in the max/mean over positions: branch i occupies input
 // channels [src[i], src[i] + cnt[i]), reduces them over its first len[i] positions and
 // writes output channels [dst[i], dst[i] + cnt[i]) of rows ldy wide; output channels
@@ -114,12 +184,20 @@ struct ReduceSegs {
   int src[kMaxReduceSegs], dst[kMaxReduceSegs], cnt[kMaxReduceSegs], len[kMaxReduceSegs];
 };
 // Global average pool NHWC [N][HW][Cs] -> [N][Cs]; also max over time when is_max.
-hipError_t launch_spatial_reduce(const void* x, void* y, int N, int HW, int Cs, int is_max, int bf16,
-                                 hipStream_t s, const ReduceSegs* segs = nullptr);
+hipError_t launch_spatial_reduce(const GroupIO& io, int N, int HW, int Cs, int is_max, int bf16, hipStream_t s,
+                                 const ReduceSegs* segs = nullptr);
+inline hipError_t launch_spatial_reduce(const void* x, void* y, int N, int HW, int Cs, int is_max, int bf16,
+                                        hipStream_t s, const ReduceSegs* segs = nullptr) {
+  return launch_spatial_reduce(single_io(x, y), N, HW, Cs, is_max, bf16, s, segs);
+}
 // Fused branches' max in the GEMM epilogue: y[n][dst_i + k] = bf16 of slot row n at
 // channel src_i + k for each branch, zeros from zero_from to ldy; every slot read is
 // reset to 0 for the next call.
-hipError_t launch_maxslot_finish(unsigned* slot, int ldslot, void* y, int N, const ReduceSegs& sg, hipStream_t s);
+hipError_t launch_maxslot_finish(const GroupIO& io, int ldslot, int N, const ReduceSegs& sg, hipStream_t s);
+inline hipError_t launch_maxslot_finish(unsigned* slot, int ldslot, void* y, int N, const ReduceSegs& sg,
+                                        hipStream_t s) {
+  return launch_maxslot_finish(single_io(nullptr, y, slot), ldslot, N, sg, s);
+}
 // Embedding gather: tokens [N][L] -> y [N][L][Cs] rows of table [vocab][Cs]; ids
 // outside [0, vocab) give zero rows.
 hipError_t launch_embed_gather(const int32_t* tok, const void* table, void* y, int N, int L, int Cs, int vocab,

@@ -95,8 +95,10 @@ hipError_t launch_stage_images(const float* x, void* y, int N, int C, int H, int
 // ---------------------------------------------------------------- max-pool
 // stream = 1 (windows do not overlap, stride >= k): every input value is read once, with
 // streaming loads; overlapping windows re-read neighbours from cache and load normally.
-__global__ void maxpool_kernel(const void* __restrict__ x, void* y, int N, int H, int W, int Cs, int Ho, int Wo,
-                               int k, int stride, int pad, int bf16, int stream) {
+__global__ void maxpool_kernel(GroupIO io, int N, int H, int W, int Cs, int Ho, int Wo, int k, int stride, int pad,
+                               int bf16, int stream) {
+  const void* __restrict__ x = io.x[blockIdx.z];
+  void* y = io.y[blockIdx.z];
   const int groups = Cs / 8;
   const long long total = (long long)N * Ho * Wo * groups;
   const long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x;
@@ -132,8 +134,10 @@ __global__ void maxpool_kernel(const void* __restrict__ x, void* y, int N, int H
 // + 4; all 15 loads of the 5 x 3 block are issued before any max (positions outside the
 // image are clamped into it and masked out).  Max is exact, so the result is that of
 // the one-output kernel above.
-__global__ __launch_bounds__(256) void maxpool3s2_kernel(const uint4* __restrict__ x, uint4* y, int N, int H, int W,
-                                                         int G, int Ho, int Wo, int pad) {
+__global__ __launch_bounds__(256) void maxpool3s2_kernel(GroupIO io, int N, int H, int W, int G, int Ho, int Wo,
+                                                         int pad) {
+  const uint4* __restrict__ x = (const uint4*)io.x[blockIdx.z];
+  uint4* y = (uint4*)io.y[blockIdx.z];
   const int Hr = (Ho + 1) / 2;
   const long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= (long long)N * Hr * Wo * G) return;
@@ -175,17 +179,18 @@ __global__ __launch_bounds__(256) void maxpool3s2_kernel(const uint4* __restrict
   if (2 * r + 1 < Ho) store8(y, ((n * Ho + 2 * r + 1) * Wo + wo) * G * 8 + g * 8, 1, b);
 }
 
-hipError_t launch_maxpool(const void* x, void* y, int N, int H, int W, int Cs, int Ho, int Wo, int k, int stride,
-                          int pad, int bf16, hipStream_t s) {
+hipError_t launch_maxpool(const GroupIO& io, int N, int H, int W, int Cs, int Ho, int Wo, int k, int stride, int pad,
+                          int bf16, hipStream_t s) {
+  if (io.n < 1 || io.n > kMaxGroup) return hipErrorInvalidValue;
   if (bf16 && k == 3 && stride == 2) {
     const long long total = (long long)N * ((Ho + 1) / 2) * Wo * (Cs / 8);
-    launch(maxpool3s2_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), s, (const uint4*)x, (uint4*)y, N, H,
-           W, Cs / 8, Ho, Wo, pad);
+    launch(maxpool3s2_kernel, dim3((unsigned)((total + 255) / 256), 1, io.n), dim3(256), s, io, N, H, W, Cs / 8, Ho,
+           Wo, pad);
     return hipGetLastError();
   }
   const long long total = (long long)N * Ho * Wo * (Cs / 8);
-  launch(maxpool_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), s, x, y, N, H, W, Cs, Ho,
-                     Wo, k, stride, pad, bf16, stride >= k ? 1 : 0);
+  launch(maxpool_kernel, dim3((unsigned)((total + 255) / 256), 1, io.n), dim3(256), s, io, N, H, W, Cs, Ho, Wo, k,
+         stride, pad, bf16, stride >= k ? 1 : 0);
   return hipGetLastError();
 }
 
@@ -203,8 +208,10 @@ constexpr int kReduceThreads = 256;
 // at a time to the branch's place.  The fused branches' max runs 1024 threads per
 // request (one block per request, long position ranges).
 template <int THREADS>
-__global__ __launch_bounds__(THREADS) void spatial_reduce_kernel(const void* __restrict__ x, void* y, int HW, int Cs,
-                                                                 int GB, int is_max, int bf16, ReduceSegs sg) {
+__global__ __launch_bounds__(THREADS) void spatial_reduce_kernel(GroupIO io, int HW, int Cs, int GB, int is_max,
+                                                                 int bf16, ReduceSegs sg) {
+  const void* __restrict__ x = io.x[blockIdx.z];
+  void* y = io.y[blockIdx.z];
   __shared__ float part[THREADS * 8];
   const int G = Cs / 8, P = THREADS / GB;
   const int t = threadIdx.x, gl = t % GB, sl = t / GB;
@@ -310,8 +317,9 @@ __global__ __launch_bounds__(THREADS) void spatial_reduce_kernel(const void* __r
 // deterministic).  Enough pairs fill the device without splitting positions, and no
 // block-level fold is needed.
 template <typename T>
-__global__ __launch_bounds__(256) void spatial_reduce_rows_kernel(const T* __restrict__ x, T* y, int N, int HW,
-                                                                  int G, int is_max) {
+__global__ __launch_bounds__(256) void spatial_reduce_rows_kernel(GroupIO io, int N, int HW, int G, int is_max) {
+  const T* __restrict__ x = (const T*)io.x[blockIdx.z];
+  T* y = (T*)io.y[blockIdx.z];
   const long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= (long long)N * G) return;
   const int g = (int)(idx % G);
@@ -345,14 +353,14 @@ __global__ __launch_bounds__(256) void spatial_reduce_rows_kernel(const T* __res
   store8(y, n * G * 8 + g * 8, bf, acc);
 }
 
-hipError_t launch_spatial_reduce(const void* x, void* y, int N, int HW, int Cs, int is_max, int bf16,
-                                 hipStream_t s, const ReduceSegs* segs) {
+hipError_t launch_spatial_reduce(const GroupIO& io, int N, int HW, int Cs, int is_max, int bf16, hipStream_t s,
+                                 const ReduceSegs* segs) {
+  if (io.n < 1 || io.n > kMaxGroup) return hipErrorInvalidValue;
   if (!segs && (long long)N * (Cs / 8) >= 16384) {
     const long long total = (long long)N * (Cs / 8);
-    const dim3 grid((unsigned)((total + 255) / 256));
-    if (bf16) launch(spatial_reduce_rows_kernel<bf16_t>, grid, dim3(256), s, (const bf16_t*)x, (bf16_t*)y, N, HW, Cs / 8,
-                     is_max);
-    else launch(spatial_reduce_rows_kernel<float>, grid, dim3(256), s, (const float*)x, (float*)y, N, HW, Cs / 8, is_max);
+    const dim3 grid((unsigned)((total + 255) / 256), 1, io.n);
+    if (bf16) launch(spatial_reduce_rows_kernel<bf16_t>, grid, dim3(256), s, io, N, HW, Cs / 8, is_max);
+    else launch(spatial_reduce_rows_kernel<float>, grid, dim3(256), s, io, N, HW, Cs / 8, is_max);
     return hipGetLastError();
   }
   ReduceSegs sg{};
@@ -367,16 +375,18 @@ hipError_t launch_spatial_reduce(const void* x, void* y, int N, int HW, int Cs, 
   }
   const int G = Cs / 8;
   const int GB = G < 64 ? G : 64;
-  const dim3 grid((unsigned)N, (unsigned)((G + GB - 1) / GB));
+  const dim3 grid((unsigned)N, (unsigned)((G + GB - 1) / GB), io.n);
   if (sg.n > 0)
-    launch(spatial_reduce_kernel<1024>, grid, dim3(1024), s, x, y, HW, Cs, GB, is_max, bf16, sg);
+    launch(spatial_reduce_kernel<1024>, grid, dim3(1024), s, io, HW, Cs, GB, is_max, bf16, sg);
   else
-    launch(spatial_reduce_kernel<kReduceThreads>, grid, dim3(kReduceThreads), s, x, y, HW, Cs, GB, is_max, bf16, sg);
+    launch(spatial_reduce_kernel<kReduceThreads>, grid, dim3(kReduceThreads), s, io, HW, Cs, GB, is_max, bf16, sg);
   return hipGetLastError();
 }
 
 // ---------------------------------------------------------------- fused branches' max
-__global__ void maxslot_finish_kernel(unsigned* slot, int ldslot, void* y, int N, ReduceSegs sg) {
+__global__ void maxslot_finish_kernel(GroupIO io, int ldslot, int N, ReduceSegs sg) {
+  unsigned* slot = io.slot[blockIdx.z];
+  void* y = io.y[blockIdx.z];
   const int n = blockIdx.x;
   const int c = blockIdx.y * blockDim.x + threadIdx.x;
   if (n >= N || c >= sg.ldy) return;
@@ -390,13 +400,13 @@ __global__ void maxslot_finish_kernel(unsigned* slot, int ldslot, void* y, int N
   ((bf16_t*)y)[(long long)n * sg.ldy + c] = (bf16_t)f2bf(v);
 }
 
-hipError_t launch_maxslot_finish(unsigned* slot, int ldslot, void* y, int N, const ReduceSegs& sg, hipStream_t s) {
-  if (sg.n < 1 || sg.n > kMaxReduceSegs || N < 1) return hipErrorInvalidValue;
+hipError_t launch_maxslot_finish(const GroupIO& io, int ldslot, int N, const ReduceSegs& sg, hipStream_t s) {
+  if (sg.n < 1 || sg.n > kMaxReduceSegs || N < 1 || io.n < 1 || io.n > kMaxGroup) return hipErrorInvalidValue;
   for (int i = 0; i < sg.n; ++i)
     if (sg.cnt[i] < 1 || sg.src[i] < 0 || sg.src[i] + sg.cnt[i] > ldslot || sg.dst[i] < 0 ||
         sg.dst[i] + sg.cnt[i] > sg.zero_from || sg.zero_from > sg.ldy)
       return hipErrorInvalidValue;
-  launch(maxslot_finish_kernel, dim3((unsigned)N, (unsigned)((sg.ldy + 255) / 256)), dim3(256), s, slot, ldslot, y, N,
+  launch(maxslot_finish_kernel, dim3((unsigned)N, (unsigned)((sg.ldy + 255) / 256), io.n), dim3(256), s, io, ldslot, N,
          sg);
   return hipGetLastError();
 }
@@ -467,6 +477,7 @@ hipError_t launch_concat(const void* a, int ca, int lda, const void* b, int cb, 
 // of a wave read consecutive ones; the input chunk is shared by the lanes of a pixel.
 // Each output sums its products in (u, v, ci) order with fmaf.
 __global__ void conv_f32_kernel(ConvArgs a) {
+  use_member(a);
   const int groups = (a.c_write + 3) / 4;
   const long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= (long long)a.M * groups) return;
@@ -515,7 +526,8 @@ __global__ void conv_f32_kernel(ConvArgs a) {
 hipError_t launch_conv_f32(const ConvArgs& a, hipStream_t s) {
   if (a.Cs % 4 != 0 || a.Co_pad % 4 != 0 || a.c_write > a.Co_pad) return hipErrorInvalidValue;
   const long long total = (long long)a.M * ((a.c_write + 3) / 4);
-  launch(conv_f32_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), s, a);
+  if (a.n_members > kMaxGroup) return hipErrorInvalidValue;
+  launch(conv_f32_kernel, dim3((unsigned)((total + 255) / 256), 1, a.n_members > 1 ? a.n_members : 1), dim3(256), s, a);
   return hipGetLastError();
 }
 

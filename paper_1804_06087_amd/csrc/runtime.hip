@@ -190,6 +190,10 @@ struct rafiki_ensemble_s {
   bool tune_schedule = true;
   bool autotune = true;
   bool fuse_branches = true;        // fuse sibling max-over-time convolutions (bf16)
+  // Models with identical layer lists share a group id (the lowest index among them);
+  // a selection within one group runs as grouped launches (RAFIKI_GROUPED=0: never).
+  std::vector<int> group_of;
+  bool grouped = true;
   int force_tile = -1;              // diagnostic override of the tuned configuration
   // Forward passes replayed as HIP graphs, one per (batch size, model subset): every
   // kernel argument inside them (weights, arenas, staged input, logits workspace,
@@ -890,7 +894,8 @@ int check_limits(const rafiki_ensemble_s* e, int mi, const Model& M) {
 }
 
 int run_gemm(const rafiki_ensemble_s* e, const Op& op, ConvArgs a, hipStream_t s, int mi, int li, int cfg,
-             const CallScratch* ws = nullptr) {
+             const CallScratch* ws = nullptr, const int* mis = nullptr) {
+  const int nm = a.n_members > 1 ? a.n_members : 1;   // grouped launch: members mis[0 .. nm)
   const double es = (double)e->esz();
   const double kalg = (double)op.kh * op.kw * op.cin_l;
   double flops = 2.0 * a.M * op.c_out * kalg;
@@ -906,8 +911,10 @@ int run_gemm(const rafiki_ensemble_s* e, const Op& op, ConvArgs a, hipStream_t s
   }
   const double in_elems = (double)a.N * a.H * a.W * op.cin_l;   // FC: H = W = 1, cin_l = flattened size
   const double out_rows = a.pool2 ? a.M / 4.0 : (double)a.M;
-  const double bytes = in_elems * es + w_elems * es +
-                       (a.maxslot ? 0.0 : out_rows * op.c_out * (a.out_f32 ? 4.0 : es) * (a.res ? 2.0 : 1.0));
+  double bytes = in_elems * es + w_elems * es +
+                 (a.maxslot ? 0.0 : out_rows * op.c_out * (a.out_f32 ? 4.0 : es) * (a.res ? 2.0 : 1.0));
+  flops *= nm;
+  bytes *= nm;
   if (e->precision != RAFIKI_BF16) {
     TRACED(e, s, RAFIKI_K_CONV_F32, mi, li, flops, bytes, launch_conv_f32(a, s));
     return RAFIKI_OK;
@@ -930,14 +937,19 @@ int run_gemm(const rafiki_ensemble_s* e, const Op& op, ConvArgs a, hipStream_t s
     ~TileScope() { trace_tile() = {}; }
   } tile_scope(cfg, splits);
   if (splits > 1) {
-    const Model& Mo = e->models[mi];
-    const size_t cap = ws ? ws->partial_bytes[mi] : Mo.partial_bytes;
-    if ((size_t)splits * a.M * a.Co_pad * 4 > cap)
-      return fail(RAFIKI_ERR_INVALID, "internal: split-K workspace too small");
-    a.partial = ws ? ws->partial[mi] : Mo.d_partial;
+    for (int k = 0; k < nm; ++k) {
+      const int m = nm > 1 ? mis[k] : mi;
+      const Model& Mo = e->models[m];
+      const size_t cap = ws ? ws->partial_bytes[m] : Mo.partial_bytes;
+      if ((size_t)splits * a.M * a.Co_pad * 4 > cap)
+        return fail(RAFIKI_ERR_INVALID, "internal: split-K workspace too small");
+      float* part = ws ? ws->partial[m] : Mo.d_partial;
+      if (nm > 1) a.members[k].partial = part;
+      else a.partial = part;
+    }
     TRACED(e, s, RAFIKI_K_CONV_MFMA, mi, li, flops, bytes, launch_conv_mfma(a, cfg, splits, s));
     TRACED(e, s, RAFIKI_K_SPLITK_REDUCE, mi, li, 0.0,
-           (double)splits * a.M * a.c_write * 4.0 + out_rows * a.c_write * (a.out_f32 ? 4.0 : es),
+           nm * ((double)splits * a.M * a.c_write * 4.0 + out_rows * a.c_write * (a.out_f32 ? 4.0 : es)),
            launch_splitk_reduce(a, splits, 1, s));
   } else {
     TRACED(e, s, RAFIKI_K_CONV_MFMA, mi, li, flops, bytes, launch_conv_mfma(a, cfg, 1, s));
@@ -969,8 +981,12 @@ ConvArgs gemm_args(const rafiki_ensemble_s* e, const Model& M, const Op& op, int
   return a;
 }
 
-int run_model(const rafiki_ensemble_s* e, int mi, const void* in, int n, float* logits, hipStream_t s,
-              size_t op_begin = 0, size_t op_end = SIZE_MAX, const CallScratch* ws = nullptr);
+int run_models(const rafiki_ensemble_s* e, const int* mis, int nm, const void* in, int n, float* const* logits,
+               hipStream_t s, size_t op_begin = 0, size_t op_end = SIZE_MAX, const CallScratch* ws = nullptr);
+inline int run_model(const rafiki_ensemble_s* e, int mi, const void* in, int n, float* logits, hipStream_t s,
+                     size_t op_begin = 0, size_t op_end = SIZE_MAX, const CallScratch* ws = nullptr) {
+  return run_models(e, &mi, 1, in, n, &logits, s, op_begin, op_end, ws);
+}
 
 // Choose each GEMM op's tile configuration for batch size n (once per n; blocks the
 // caller).  The candidates are timed where they will run: inside forward passes of
@@ -1074,11 +1090,16 @@ int tune(rafiki_ensemble_s* e, int n, const void* in, hipStream_t s) {
 }
 
 // Forward pass of model `mi` over n requests whose model input is `in` (staged images
-// or token ids); logits [n][n_classes] to `logits`.
+// or token ids); logits [n][n_classes] to `logits`.  Several models with identical
+// layer lists (mis[0 .. nm), nm <= kMaxGroup) run as one grouped launch per op, member
+// k writing its logits to logits[k]; ops without a grouped kernel (embedding gather,
+// concatenation) are launched once per member.
 // Only ops [op_begin, op_end) are enqueued, so that the launches of several models
 // can be interleaved.
-int run_model(const rafiki_ensemble_s* e, int mi, const void* in, int n, float* logits, hipStream_t s,
-              size_t op_begin, size_t op_end, const CallScratch* ws) {
+int run_models(const rafiki_ensemble_s* e, const int* mis, int nm, const void* in, int n, float* const* logits,
+               hipStream_t s, size_t op_begin, size_t op_end, const CallScratch* ws) {
+  if (nm < 1 || nm > kMaxGroup) return fail(RAFIKI_ERR_INVALID, "internal: group size");
+  const int mi = mis[0];
   const Model& M = e->models[mi];
   const auto it = e->tuned.find(n);
   const std::vector<int> empty;
@@ -1089,27 +1110,61 @@ int run_model(const rafiki_ensemble_s* e, int mi, const void* in, int n, float* 
   for (size_t oi = op_begin; oi < op_end; ++oi) {
     const Op& op = M.ops[oi];
     const int li = op.out;
+    // member k's op, tensors and pointers (k = 0 is model mi)
+    auto mop = [&](int k) -> const Op& { return e->models[mis[k]].ops[oi]; };
+    auto yptr = [&](int k) -> void* {
+      const Model& Mk = e->models[mis[k]];
+      const Tensor& y = Mk.tensors[Mk.ops[oi].out];
+      return y.is_logits ? (void*)logits[k] : (void*)(Mk.d_arena + y.off);
+    };
+    auto xptr = [&](int k, int id) { return tptr(e, e->models[mis[k]], id, in); };
+    // this op's epilogue-max keys of member k (ws: after those of the model's earlier fused ops)
+    auto slotptr = [&](int k) -> unsigned* {
+      const Model& Mk = e->models[mis[k]];
+      if (!ws) return Mk.ops[oi].d_slot;
+      unsigned* p = ws->slot[mis[k]];
+      for (size_t j = 0; j < oi; ++j)
+        if (Mk.ops[j].d_slot) p += (size_t)n * Mk.ops[j].ldslot;
+      return p;
+    };
+    void* yp = yptr(0);
     const Tensor& y = M.tensors[op.out];
-    void* yp = y.is_logits ? (void*)logits : (void*)(M.d_arena + y.off);
-    const void* xp = tptr(e, M, op.in, in);
     switch (op.kind) {
       case O_CONV:
       case O_CONV1D: {
         ConvArgs a = gemm_args(e, M, op, n, in);
-        int cfg = cfgs.empty() ? -1 : cfgs[&op - M.ops.data()];
+        int cfg = cfgs.empty() ? -1 : cfgs[oi];
         if (e->force_tile >= 0 && cfg_fits(e->force_tile, op.c_out)) cfg = e->force_tile;
+        if (nm > 1) {
+          a.n_members = nm;
+          for (int k = 0; k < nm; ++k) {
+            const Op& ok = mop(k);
+            GroupMember& g = a.members[k];
+            g.x = ok.table ? ok.table : xptr(k, ok.in);
+            g.w = ok.d_w;
+            g.scale = ok.d_scale;
+            g.shift = ok.d_shift;
+            g.res = ok.in2 >= 0 ? xptr(k, ok.in2) : nullptr;
+          }
+        }
         if (op.kind == O_CONV1D) {
           void* tmp = M.d_arena + op.tmp_off;
           a.y = tmp; a.c_write = round_up(op.c_out, 8); a.ldy = a.c_write; a.out_f32 = bf ? 0 : 1;
           const bool in_epilogue = op.d_slot && choose_splits(a.M, op.c_out, a.Kp / 64) == 1;
-          unsigned* slot = op.d_slot;
-          if (ws) {   // this op's keys follow those of the model's earlier fused ops
-            slot = ws->slot[mi];
-            for (size_t j = 0; j < oi; ++j)
-              if (M.ops[j].d_slot) slot += (size_t)n * M.ops[j].ldslot;
+          GroupIO fin{};   // per member: slots, pre-max rows and the concatenated vector
+          fin.n = nm;
+          for (int k = 0; k < nm; ++k) {
+            const Model& Mk = e->models[mis[k]];
+            fin.slot[k] = slotptr(k);
+            fin.x[k] = Mk.d_arena + mop(k).tmp_off;
+            fin.y[k] = yptr(k);
+            if (nm > 1) {
+              a.members[k].y = (void*)fin.x[k];
+              a.members[k].maxslot = in_epilogue ? fin.slot[k] : nullptr;
+            }
           }
-          if (in_epilogue) { a.maxslot = slot; a.ldslot = op.ldslot; }
-          int rc = run_gemm(e, op, a, s, mi, li, cfg, ws);
+          if (in_epilogue) { a.maxslot = fin.slot[0]; a.ldslot = op.ldslot; }
+          int rc = run_gemm(e, op, a, s, mi, li, cfg, ws, mis);
           if (rc) return rc;
           if (in_epilogue) {   // the GEMM took the max; write the concatenated vector
             ReduceSegs segs{};
@@ -1120,8 +1175,9 @@ int run_model(const rafiki_ensemble_s* e, int mi, const void* in, int n, float* 
               segs.src[i] = op.seg_row[i];
               segs.len[i] = op.W - op.seg_kw[i] + 1;
             }
-            TRACED(e, s, RAFIKI_K_POOL, mi, li, 0.0, (double)n * op.ldslot * 4.0 * 2.0 + (double)n * y.Cs * es,
-                   launch_maxslot_finish(slot, op.ldslot, yp, n, segs, s));
+            TRACED(e, s, RAFIKI_K_POOL, mi, li, 0.0,
+                   nm * ((double)n * op.ldslot * 4.0 * 2.0 + (double)n * y.Cs * es),
+                   launch_maxslot_finish(fin, op.ldslot, n, segs, s));
             break;
           }
           ReduceSegs segs{};
@@ -1139,37 +1195,51 @@ int run_model(const rafiki_ensemble_s* e, int mi, const void* in, int n, float* 
               vals += (double)segs.len[i] * segs.cnt[i];
             }
           }
-          TRACED(e, s, RAFIKI_K_POOL, mi, li, 0.0, (double)n * vals * es + (double)n * y.c * es,
-                 launch_spatial_reduce(tmp, yp, n, op.Wo, a.c_write, 1, bf, s, op.nseg > 0 ? &segs : nullptr));
+          TRACED(e, s, RAFIKI_K_POOL, mi, li, 0.0, nm * ((double)n * vals * es + (double)n * y.c * es),
+                 launch_spatial_reduce(fin, n, op.Wo, a.c_write, 1, bf, s, op.nseg > 0 ? &segs : nullptr));
           break;
         }
         a.y = yp;
+        if (nm > 1)
+          for (int k = 0; k < nm; ++k) a.members[k].y = yptr(k);
         if (y.is_logits) { a.c_write = y.c; a.ldy = y.c; a.out_f32 = 1; }
         else { a.c_write = y.Cs; a.ldy = y.Cs; a.out_f32 = bf ? 0 : 1; }
-        int rc = run_gemm(e, op, a, s, mi, li, cfg, ws);
+        int rc = run_gemm(e, op, a, s, mi, li, cfg, ws, mis);
         if (rc) return rc;
         break;
       }
       case O_MAXPOOL:
-        TRACED(e, s, RAFIKI_K_POOL, mi, li, 0.0,
-               ((double)op.H * op.W + (double)op.Ho * op.Wo) * n * op.cin_l * es,
-               launch_maxpool(xp, yp, n, op.H, op.W, op.Cs_in, op.Ho, op.Wo, op.k, op.stride, op.pad, bf, s));
-        break;
-      case O_GAP:
-        TRACED(e, s, RAFIKI_K_POOL, mi, li, 0.0, ((double)op.H * op.W + 1.0) * n * op.cin_l * es,
-               launch_spatial_reduce(xp, yp, n, op.H * op.W, op.Cs_in, 0, bf, s));
-        break;
-      case O_EMBED:
-        TRACED(e, s, RAFIKI_K_EMBED, mi, li, 0.0, (double)n * op.W * (4.0 + 2.0 * op.cin_l * es),
-               launch_embed_gather((const int32_t*)in, op.d_w, yp, n, op.W, op.Cs_in, e->vocab, bf, s));
-        break;
-      case O_CONCAT: {
-        const Tensor& a = M.tensors[op.in];
-        const Tensor& b = M.tensors[op.in2];
-        TRACED(e, s, RAFIKI_K_CONCAT, mi, li, 0.0, 2.0 * n * (op.ca + op.cb) * es,
-               launch_concat(xp, op.ca, a.Cs, tptr(e, M, op.in2, in), op.cb, b.Cs, yp, y.Cs, n, bf, s));
+      case O_GAP: {
+        GroupIO io{};
+        io.n = nm;
+        for (int k = 0; k < nm; ++k) {
+          io.x[k] = xptr(k, mop(k).in);
+          io.y[k] = yptr(k);
+        }
+        if (op.kind == O_MAXPOOL)
+          TRACED(e, s, RAFIKI_K_POOL, mi, li, 0.0,
+                 nm * ((double)op.H * op.W + (double)op.Ho * op.Wo) * n * op.cin_l * es,
+                 launch_maxpool(io, n, op.H, op.W, op.Cs_in, op.Ho, op.Wo, op.k, op.stride, op.pad, bf, s));
+        else
+          TRACED(e, s, RAFIKI_K_POOL, mi, li, 0.0, nm * ((double)op.H * op.W + 1.0) * n * op.cin_l * es,
+                 launch_spatial_reduce(io, n, op.H * op.W, op.Cs_in, 0, bf, s));
         break;
       }
+      case O_EMBED:
+        for (int k = 0; k < nm; ++k)
+          TRACED(e, s, RAFIKI_K_EMBED, mis[k], li, 0.0, (double)n * op.W * (4.0 + 2.0 * op.cin_l * es),
+                 launch_embed_gather((const int32_t*)in, mop(k).d_w, yptr(k), n, op.W, op.Cs_in, e->vocab, bf, s));
+        break;
+      case O_CONCAT:
+        for (int k = 0; k < nm; ++k) {
+          const Model& Mk = e->models[mis[k]];
+          const Tensor& ta = Mk.tensors[op.in];
+          const Tensor& tb = Mk.tensors[op.in2];
+          TRACED(e, s, RAFIKI_K_CONCAT, mis[k], li, 0.0, 2.0 * n * (op.ca + op.cb) * es,
+                 launch_concat(xptr(k, op.in), op.ca, ta.Cs, xptr(k, op.in2), op.cb, tb.Cs, yptr(k), Mk.tensors[op.out].Cs,
+                               n, bf, s));
+        }
+        break;
     }
   }
   return RAFIKI_OK;
@@ -1200,6 +1270,34 @@ int stage(const rafiki_ensemble_s* e, const void* batch, int n, hipStream_t s, v
 
 namespace rafiki {
 int set_error(int code, const std::string& msg) { return fail(code, msg); }
+
+// Two models whose layer lists differ only in their parameters: every op and tensor
+// has the same kind, wiring, shapes, padding, tiling fields and arena offsets.
+bool same_structure(const Model& A, const Model& B) {
+  if (A.ops.size() != B.ops.size() || A.tensors.size() != B.tensors.size() || A.arena_bytes != B.arena_bytes)
+    return false;
+  for (size_t i = 0; i < A.tensors.size(); ++i) {
+    const Tensor &a = A.tensors[i], &b = B.tensors[i];
+    if (a.kind != b.kind || a.c != b.c || a.h != b.h || a.w != b.w || a.Cs != b.Cs || a.off != b.off ||
+        a.is_logits != b.is_logits)
+      return false;
+  }
+  for (size_t i = 0; i < A.ops.size(); ++i) {
+    const Op &a = A.ops[i], &b = B.ops[i];
+    const int fa[] = {a.kind, a.in, a.in2, a.out, a.H, a.W, a.Cs_in, a.Ho, a.Wo, a.kh, a.kw, a.stride, a.pad, a.relu,
+                      a.K, a.Kp, a.Co_pad, a.c_out, a.cin_l, a.k, a.pool2, a.nseg, a.tap_stride, a.ldslot, a.ca, a.cb,
+                      a.table != nullptr, a.d_slot != nullptr};
+    const int fb[] = {b.kind, b.in, b.in2, b.out, b.H, b.W, b.Cs_in, b.Ho, b.Wo, b.kh, b.kw, b.stride, b.pad, b.relu,
+                      b.K, b.Kp, b.Co_pad, b.c_out, b.cin_l, b.k, b.pool2, b.nseg, b.tap_stride, b.ldslot, b.ca, b.cb,
+                      b.table != nullptr, b.d_slot != nullptr};
+    if (std::memcmp(fa, fb, sizeof(fa)) != 0 || a.tmp_off != b.tmp_off) return false;
+    for (int j = 0; j < kMaxReduceSegs; ++j)
+      if (a.seg_end[j] != b.seg_end[j] || a.seg_kw[j] != b.seg_kw[j] || a.seg_row[j] != b.seg_row[j]) return false;
+    for (int j = 0; j < 16; ++j)
+      if (a.taps_by_block[j] != b.taps_by_block[j]) return false;
+  }
+  return true;
+}
 
 // Scratch of rafiki_ensemble_infer_noalloc: a file-scope device array, one copy per
 // GPU, held until the process ends.  Host code never uses the array's name as an
@@ -1278,6 +1376,7 @@ int rafiki_ensemble_create(const rafiki_model_desc* models, int n_models, const 
   if (const char* t = std::getenv("RAFIKI_GRAPHS")) e->use_graphs = std::atoi(t) != 0;
   if (const char* t = std::getenv("RAFIKI_SCHEDULE_TUNING")) e->tune_schedule = std::atoi(t) != 0;
   if (const char* t = std::getenv("RAFIKI_FUSE_BRANCHES")) e->fuse_branches = std::atoi(t) != 0;
+  if (const char* t = std::getenv("RAFIKI_GROUPED")) e->grouped = std::atoi(t) != 0;
   // Pass 1: validate every model and infer shapes without touching the device.
   e->dry = true;
   e->models.resize(n_models);
@@ -1301,6 +1400,15 @@ int rafiki_ensemble_create(const rafiki_model_desc* models, int n_models, const 
   for (int m = 0; m < n_models; ++m) {
     int rc = build_model(e.get(), m, models[m], e->models[m]);
     if (rc) return rc;
+  }
+  e->group_of.resize(n_models);
+  for (int m = 0; m < n_models; ++m) {
+    e->group_of[m] = m;
+    for (int j = 0; j < m; ++j)
+      if (same_structure(e->models[j], e->models[m])) {
+        e->group_of[m] = j;
+        break;
+      }
   }
   int rc;
   if (e->input_kind == RAFIKI_INPUT_IMAGE_NCHW_F32) {
@@ -1345,10 +1453,32 @@ int rafiki_ensemble_create(const rafiki_model_desc* models, int n_models, const 
 // itself).  Forked launches are enqueued interleaved, one op of each model in turn, so
 // that every model stream has work from the start even when enqueueing is slower than
 // the device.
+// The selection runs as grouped launches: two or more models of one group.
+static bool grouped_selection(const rafiki_ensemble_s* h, const CombineArgs& ca) {
+  if (!h->grouped || ca.S < 2) return false;
+  for (int i = 1; i < ca.S; ++i)
+    if (h->group_of[ca.sel[i]] != h->group_of[ca.sel[0]]) return false;
+  return true;
+}
+
 static int forward(rafiki_ensemble_t h, const CombineArgs& ca, const void* in, int n, hipStream_t s,
                    rafiki_ensemble_s::Sched sched, const CallScratch* ws = nullptr) {
   const int solo = sched.solo;
   int rc = RAFIKI_OK;
+  if (grouped_selection(h, ca)) {   // one launch per op for up to kMaxGroup members, on the caller's stream
+    for (int c0 = 0; c0 < ca.S; c0 += kMaxGroup) {
+      const int nm = std::min(kMaxGroup, ca.S - c0);
+      int mis[kMaxGroup];
+      float* lg[kMaxGroup];
+      for (int k = 0; k < nm; ++k) {
+        mis[k] = ca.sel[c0 + k];
+        lg[k] = h->d_logits + (size_t)mis[k] * ca.ld_model;
+      }
+      rc = run_models(h, mis, nm, in, n, lg, s, 0, SIZE_MAX, ws);
+      if (rc) return rc;
+    }
+    return RAFIKI_OK;
+  }
   const bool fork = h->concurrent && (!h->trace.on || h->trace.concurrent) && ca.S > 1;
   if (fork) {
     HIPCHK(hipEventRecord(h->staged_ev, s));
@@ -1424,7 +1554,8 @@ static int forward(rafiki_ensemble_t h, const CombineArgs& ca, const void* in, i
 static int pick_schedule(rafiki_ensemble_t h, const CombineArgs& ca, const void* in, int n, uint32_t mask,
                          hipStream_t s, rafiki_ensemble_s::Sched* sched, const CallScratch* ws = nullptr) {
   *sched = {};
-  if (ca.S < 3 || !h->concurrent || (h->trace.on && !h->trace.concurrent)) return RAFIKI_OK;
+  if (ca.S < 3 || !h->concurrent || (h->trace.on && !h->trace.concurrent) || grouped_selection(h, ca))
+    return RAFIKI_OK;
   const auto key = std::make_pair(n, mask);
   const auto it = h->schedule.find(key);
   if (it != h->schedule.end()) {

@@ -7,6 +7,8 @@ eager result of the same input, with eager work, other inputs and synchronisatio
 between replays (a graph that read a stale staged input, or skipped a node, would
 differ).  One case is also checked against the oracle.
 """
+import os
+
 import numpy as np
 import pytest
 import torch
@@ -123,7 +125,16 @@ def test_graph_replay_under_each_schedule(solo, asc):
     cfg, specs, params, batch = wl.build_config(2, n=24)
     C = 10
     x = torch.from_numpy(batch).to(DEV)
-    with Ensemble(specs, params, precision="bf16", max_batch=24) as ens:
+    old = os.environ.get("RAFIKI_GROUPED")
+    os.environ["RAFIKI_GROUPED"] = "0"   # schedules order the models' own streams (no grouped launches)
+    try:
+        ens = Ensemble(specs, params, precision="bf16", max_batch=24)
+    finally:
+        if old is None:
+            del os.environ["RAFIKI_GROUPED"]
+        else:
+            os.environ["RAFIKI_GROUPED"] = old
+    with ens:
         _infer(ens, x, 24, 0b111, C)                   # tunes n = 24
         ens.set_schedule(24, 0b111, solo, asc)
         ens.use_graphs(False)

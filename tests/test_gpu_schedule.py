@@ -5,6 +5,8 @@ one model alone on a lane while the others run one after another on a second lan
 every schedule must give bit-identical probabilities and labels; the one chosen by
 timing on the first call must be a valid candidate.
 """
+import os
+
 import numpy as np
 import pytest
 import torch
@@ -14,6 +16,20 @@ from paper_1804_06087_amd import Ensemble, RafikiError, RAFIKI_ERR_INVALID
 
 pytestmark = pytest.mark.gpu
 DEV = torch.device("cuda:0")
+
+
+def _ungrouped(specs, params, max_batch):
+    """Schedules order the models' own streams, so identical members (which otherwise
+    run as grouped launches on one stream) are created with grouping off."""
+    old = os.environ.get("RAFIKI_GROUPED")
+    os.environ["RAFIKI_GROUPED"] = "0"
+    try:
+        return Ensemble(specs, params, precision="bf16", max_batch=max_batch)
+    finally:
+        if old is None:
+            del os.environ["RAFIKI_GROUPED"]
+        else:
+            os.environ["RAFIKI_GROUPED"] = old
 
 
 def _infer(ens, x, n, mask, C, vote=False):
@@ -29,7 +45,7 @@ def test_every_schedule_gives_the_same_bits(cid, n, mask):
     cfg, specs, params, batch = wl.build_config(cid, n=n)
     C = specs[0].n_classes
     x = torch.from_numpy(batch).to(DEV)
-    with Ensemble(specs, params, precision="bf16", max_batch=n) as ens:
+    with _ungrouped(specs, params, n) as ens:
         p0, l0 = _infer(ens, x, n, mask, C)
         chosen, asc = ens.get_schedule(n, mask)
         members = [m for m in range(len(specs)) if (mask >> m) & 1]
@@ -49,7 +65,7 @@ def test_every_schedule_gives_the_same_bits(cid, n, mask):
 
 def test_schedule_arguments():
     cfg, specs, params, batch = wl.build_config(2, n=8)
-    with Ensemble(specs, params, precision="bf16", max_batch=8) as ens:
+    with _ungrouped(specs, params, 8) as ens:
         with pytest.raises(RafikiError) as e:
             ens.get_schedule(8, 0b111)                 # nothing chosen yet
         assert e.value.code == RAFIKI_ERR_INVALID
