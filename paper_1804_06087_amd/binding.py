@@ -14,7 +14,8 @@ from typing import List, Optional, Sequence
 import numpy as np
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_PKG, "librafiki_ensemble.so")
+# RAFIKI_LIBRARY names another build of the same sources (the host-sanitizer build)
+LIB_PATH = os.environ.get("RAFIKI_LIBRARY") or os.path.join(_PKG, "librafiki_ensemble.so")
 
 RAFIKI_OK, RAFIKI_ERR_INVALID, RAFIKI_ERR_UNSUPPORTED, RAFIKI_ERR_NOMEM, RAFIKI_ERR_HIP = 0, -1, -2, -3, -4
 RAFIKI_FP32, RAFIKI_BF16 = 0, 1
