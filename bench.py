@@ -619,9 +619,13 @@ def layers_main(args, dev):
         print(f"| {kind} | {ms:.3f} | {tb:.3f} | {tb / ms:.2f} |")
 
 
-def schedule_desc(ens, n, mask, names):
-    """How the selected models' forward passes were scheduled for (n, mask)."""
+def schedule_desc(ens, n, mask, names, kinds=()):
+    """How the selected models' forward passes were scheduled for (n, mask); `kinds`
+    are the kernel classes a traced pass launched."""
     members = [m for m in range(len(names)) if (mask >> m) & 1]
+    if "fused_net" in kinds:
+        return (f"whole-network kernel: one launch for the {len(members)} selected models, one workgroup per "
+                "image and model, activations in LDS")
     if len(members) == 1:
         return names[members[0]]
     kinds = {names[m].split("#")[0] for m in members}
@@ -835,7 +839,8 @@ def main():
         "data": "synthetic (seeded inputs and random-init weights of the named architectures)",
         "config": {"workload": desc, "global_batch": n, "mask": mask, "n_classes": C, "combine": args.combine,
                    "input": "int32 tokens [n, 256]" if tokens else "float32 NCHW images",
-                   "schedule": schedule_desc(ens, n, mask, [f"{sp.name}#{i}" for i, sp in enumerate(specs)])},
+                   "schedule": schedule_desc(ens, n, mask, [f"{sp.name}#{i}" for i, sp in enumerate(specs)],
+                                             tuple(classes))},
         "p50_ms": round(float(np.percentile(lat, 50)), 4),
         "p99_ms": round(float(np.percentile(lat, 99)), 4),
         "host_enqueue_ms": round(float(np.median(host)), 4),

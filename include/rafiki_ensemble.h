@@ -198,7 +198,8 @@ enum {
   RAFIKI_K_EMBED = 5,          /* embedding gather */
   RAFIKI_K_CONCAT = 6,         /* vector concatenation */
   RAFIKI_K_COMBINE = 7,        /* softmax + ensemble mean + argmax */
-  RAFIKI_K_VOTE = 8            /* per-model argmax + majority vote */
+  RAFIKI_K_VOTE = 8,           /* per-model argmax + majority vote */
+  RAFIKI_K_FUSED_NET = 9       /* whole forward pass of small CNNs, one workgroup per image and model */
 };
 typedef struct {
   int kind;                     /* RAFIKI_K_* */

@@ -34,7 +34,8 @@ EXPORTED = ("rafiki_ensemble_create", "rafiki_ensemble_infer", "rafiki_ensemble_
             "rafiki_rl_create", "rafiki_rl_destroy", "rafiki_rl_info", "rafiki_rl_get_params", "rafiki_rl_set_params",
             "rafiki_rl_forward", "rafiki_rl_gradient", "rafiki_rl_adam_step", "rafiki_rl_run_episode",
             "rafiki_rl_train", "rafiki_last_error")
-KERNEL_CLASSES = ("conv_mfma", "splitk_reduce", "conv_f32", "stage", "pool", "embed", "concat", "combine", "vote")
+KERNEL_CLASSES = ("conv_mfma", "splitk_reduce", "conv_f32", "stage", "pool", "embed", "concat", "combine", "vote",
+                  "fused_net")
 
 _fp = C.POINTER(C.c_float)
 

@@ -19,7 +19,7 @@ from . import build as b
 SAN_DIR = os.path.join(b.OBJ, "san")
 SAN_LIB = os.path.join(SAN_DIR, "librafiki_ensemble_san.so")
 HOST_SOURCES = ["runtime.hip", "greedy.cpp", "rl.cpp"]      # instrumented
-KERNEL_SOURCES = ["conv_mfma.hip", "misc.hip"]              # linked as built
+KERNEL_SOURCES = ["conv_mfma.hip", "misc.hip", "fused_net.hip"]   # linked as built
 SAN_FLAGS = "-Xarch_host -fsanitize=address -Xarch_host -fsanitize=undefined".split()
 HOST_DEBUG = "-Xarch_host -fno-omit-frame-pointer -Xarch_host -g".split()
 
@@ -43,12 +43,13 @@ def _compile(src: str, flags) -> str:
 def build_sanitized() -> str:
     os.makedirs(SAN_DIR, exist_ok=True)
     jobs = [(s, SAN_FLAGS + HOST_DEBUG) for s in HOST_SOURCES]
-    # kernel-only sources: reuse the ordinary objects when they are newer than every source
-    newest = max(os.path.getmtime(p) for p in glob.glob(os.path.join(b.SRC, "*")) +
-                 glob.glob(os.path.join(b.ROOT, "include", "*.h")))
+    # kernel-only sources: reuse the ordinary objects when they are newer than their
+    # source and every header
+    headers = glob.glob(os.path.join(b.SRC, "*.h")) + glob.glob(os.path.join(b.ROOT, "include", "*.h"))
     objs = []
     for s in KERNEL_SOURCES:
         o = os.path.join(b.OBJ, os.path.splitext(s)[0] + ".o")
+        newest = max(os.path.getmtime(p) for p in headers + [os.path.join(b.SRC, s)])
         if os.path.exists(o) and os.path.getmtime(o) >= newest:
             objs.append(o)
         else:

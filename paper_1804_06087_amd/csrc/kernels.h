@@ -220,6 +220,44 @@ hipError_t launch_combine(const CombineArgs& a, hipStream_t s);
 // Majority vote over the same slots: probs <- vote fractions, labels <- winner.
 hipError_t launch_vote(const CombineArgs& a, hipStream_t s);
 
+// Whole-network kernel for small image CNNs (fused_net.hip): one workgroup of
+// kFusedWaves waves runs one model's layer program on one image, the activations in
+// an LDS arena of kFusedLdsBytes (tensors [pixel][Cs] bf16, 8 <= Cs <= 64 a power of
+// two, in a swizzled chunk order), followed in LDS by 128 zero bytes and the model's
+// folded scale / shift table of at most kFusedTableBytes.
+constexpr int kFusedWaves = 4;
+constexpr int kFusedLdsBytes = 64 * 1024;
+constexpr int kFusedTableBytes = 8 * 1024;
+constexpr int kFusedMaxLayers = 64;
+// F_INPUT copies the staged image [Ho * Wo][Cso] to out_off and the scale / shift
+// table (`scale`, c_write bytes) to ss_off; F_END ends a program.
+enum FusedOpKind { F_END = 0, F_INPUT = 1, F_CONV = 2, F_GAP = 3, F_FC = 4 };
+struct FusedLayer {
+  int op;                        // FusedOpKind
+  int in_off, res_off, out_off;  // LDS byte offsets of the input, residual (-1: none) and output
+  int H, W, Cs;                  // input geometry, storage channels
+  int Ho, Wo, Cso;               // output geometry; Cso = output row stride (FC: logits row length)
+  int c_write;                   // output channels written
+  int kh, kw, stride, pad, relu;
+  int K, Kp;                     // K = kh * kw * Cs terms, packed weight row length
+  int n_cb, n_pb, ch;            // 32-channel blocks, 32-pixel blocks, pixel blocks per wave task
+  int lwo;                       // log2(Wo)
+  int ss_off;                    // LDS offset of this layer's scale [c4] then shift [c4], c4 = c_write rounded to 4
+  int tmp_off;                   // GAP: LDS scratch of the partial sums
+  const bf16_t* w;               // weights in fragment order [n_cb][ceil(K / 16)][64 lanes][8]: lane
+                                 // fk * 32 + r holds row cb * 32 + r, terms 16 g + 8 fk .. + 7, K in
+                                 // (tap, channel) order
+  const float* scale;            // F_INPUT: the model's scale / shift table in global memory
+};
+struct FusedNetArgs {
+  const FusedLayer* progs;   // [n_models][kFusedMaxLayers] programs, each ended by F_END
+  float* logits;             // model m's logits at logits + m * ld_model, rows of the FC's Cso
+  long long ld_model;
+  unsigned mask;             // selected models; grid y = the y-th set bit
+  const bf16_t* in;          // staged images [n][Ho * Wo][Cso] of the programs' F_INPUT
+};
+hipError_t launch_fused_net(const FusedNetArgs& a, int n, int n_models, hipStream_t s);
+
 // Peak probes: register-resident bf16 MFMA loop (out [blocks * 4] checksums) and a
 // streaming 16-byte read of words16 words (out [blocks * 4]).
 hipError_t launch_probe_mfma(int blocks, int iters, float* out, hipStream_t s);

@@ -104,6 +104,8 @@ struct Model {
   hipStream_t stream = nullptr;   // the model's own stream for concurrent ensembles
   hipEvent_t done = nullptr;      // recorded on `stream` after the model's last kernel
   void* d_staged_own = nullptr;   // the model's own staged input (asynchronous serving)
+  // Whole-network program (fused_net.hip) when every layer fits that kernel; empty if not.
+  std::vector<FusedLayer> fprog;
 };
 
 struct FreeList {
@@ -212,6 +214,10 @@ struct rafiki_ensemble_s {
   // (resolved at create; null with the reason in scratch_err if that failed).
   void* scratch = nullptr;
   std::string scratch_err;
+  // Whole-network kernel: the models' programs [n_models][kFusedMaxLayers] on the
+  // device (null if no model fits it); RAFIKI_FUSED_NET=0 at create turns it off.
+  bool fused_net = true;
+  FusedLayer* d_fprog = nullptr;
   size_t esz() const { return precision == RAFIKI_BF16 ? 2 : 4; }
   void drop_graphs() {
     for (auto& kv : graphs) {
@@ -790,6 +796,224 @@ size_t partial_need(const rafiki_ensemble_s* e, const Model& M) {
   return need;
 }
 
+// The whole-network program of model M (bf16 image models only), or false if a layer
+// does not fit the kernel: convolutions 1x1 (pad 0) or 3x3 (pad 1) of stride 1 or 2
+// over 8..64 storage channels (a power of two) to at most 64 output channels, with
+// Wo a power of two, Ho * Wo a multiple of 32 and no split K at any batch size, then a
+// global average pool and the final FC over at most 64 inputs and 32 * kFusedWaves
+// classes; the layers' folded scale / shift (copied from the layer kernels' device
+// arrays, so bitwise the same) within kFusedTableBytes.  Tensors get
+// LDS offsets by liveness; a convolution whose residual is read for the last time
+// writes its output over it (each output element replaces the residual element that
+// the same lane has just read).  The plan needs at most kFusedLdsBytes.
+// LDS arena of one workgroup: live intervals, placed lowest-first (or highest-first)
+// in the first gap that fits; sizes rounded to 256 bytes.
+struct LdsArena {
+  std::vector<std::pair<size_t, size_t>> live;   // (offset, size), sorted by offset
+  size_t cap, peak = 0;
+  explicit LdsArena(size_t c) : cap(c) {}
+  long long place(size_t n, bool high) {
+    n = round_up_sz(std::max<size_t>(n, 1), 256);
+    long long at = -1;
+    if (!high) {
+      size_t o = 0;
+      for (const auto& iv : live) {
+        if (o + n <= iv.first) break;
+        o = std::max(o, iv.first + iv.second);
+      }
+      if (o + n <= cap) at = (long long)o;
+    } else {
+      long long o = (long long)cap - (long long)n;
+      for (auto it = live.rbegin(); it != live.rend(); ++it) {
+        if (o >= (long long)(it->first + it->second)) break;
+        o = std::min(o, (long long)it->first - (long long)n);
+      }
+      if (o >= 0) at = o;
+    }
+    if (at < 0) return -1;
+    live.push_back({(size_t)at, n});
+    std::sort(live.begin(), live.end());
+    peak = std::max(peak, (size_t)at + n);
+    return at;
+  }
+  void release(long long off) {
+    for (size_t i = 0; i < live.size(); ++i)
+      if ((long long)live[i].first == off) {
+        live.erase(live.begin() + i);
+        return;
+      }
+  }
+};
+
+// The whole-network program of model M (bf16 image models only), or false if a layer
+// does not fit the kernel: convolutions 1x1 (pad 0) or 3x3 (pad 1) of stride 1 or 2
+// over 8..64 storage channels (a power of two) to at most 64 output channels, with
+// Wo a power of two, Ho * Wo a multiple of 32 and no split K at any batch size, then a
+// global average pool and the final FC over at most 64 inputs and 32 * kFusedWaves
+// classes; the layers' folded scale / shift (copied from the layer kernels' device
+// arrays, so bitwise the same) within kFusedTableBytes.  Tensors get
+// LDS offsets by liveness in an arena of kFusedLdsBytes, the model input at its top,
+// every other tensor as low as it fits; a convolution whose residual is read for the
+// last time writes its output over it (each output element replaces the residual
+// element that the same lane has just read).
+bool plan_fused(rafiki_ensemble_s* e, Model& M) {
+  M.fprog.clear();
+  if (e->precision != RAFIKI_BF16 || e->input_kind != RAFIKI_INPUT_IMAGE_NCHW_F32 || !e->fused_net) return false;
+  auto cs_ok = [](int cs) { return cs == 8 || cs == 16 || cs == 32 || cs == 64; };
+  if (!cs_ok(e->in_Cs) || M.ops.empty()) return false;
+  Tensor in_t;
+  in_t.kind = T_IMG; in_t.c = e->C; in_t.h = e->H; in_t.w = e->W; in_t.Cs = e->in_Cs;
+  auto tens = [&](int id) -> const Tensor& { return id < 0 ? in_t : M.tensors[id]; };
+  auto nbytes = [](const Tensor& t) { return (size_t)t.h * t.w * t.Cs * 2; };
+  int in_last = -1;
+  for (size_t i = 0; i < M.ops.size(); ++i)
+    if (M.ops[i].in == -1) in_last = (int)i;
+  std::vector<int> writer(M.tensors.size(), -1);
+  for (size_t i = 0; i < M.ops.size(); ++i) writer[M.ops[i].out] = (int)i;
+  LdsArena ar(kFusedLdsBytes);
+  std::vector<long long> off(M.tensors.size(), -1);
+  const long long in_off = ar.place(nbytes(in_t), true);
+  if (in_off < 0) return false;
+  auto loff = [&](int id) { return id < 0 ? in_off : off[id]; };
+  std::vector<FusedLayer> prog;
+  FusedLayer I{};
+  I.op = F_INPUT;
+  I.out_off = (int)in_off;
+  I.Cso = e->in_Cs;
+  I.Ho = e->H; I.Wo = e->W;
+  I.ss_off = kFusedLdsBytes + 128;
+  prog.push_back(I);
+  std::vector<float> table;   // per layer: scale [c4], shift [c4]
+  // The weights in fragment order: for channel block cb and K group g, the 64 lanes'
+  // 16-byte A fragments (lane fk * 32 + r: row cb * 32 + r, terms 16 g + 8 fk ..
+  // + 7) are one contiguous kilobyte, so a wave's fragment load reads whole lines.
+  auto frag_weights = [&](FusedLayer& L, const Op& op) -> bool {
+    if (e->dry) return true;
+    const int NG = (L.K + 15) / 16, rows = L.n_cb * 32;
+    std::vector<uint16_t> src((size_t)rows * op.Kp), dst((size_t)L.n_cb * NG * 64 * 8);
+    if (hipMemcpy(src.data(), op.d_w, src.size() * 2, hipMemcpyDeviceToHost) != hipSuccess) return false;
+    for (int cb = 0; cb < L.n_cb; ++cb)
+      for (int g = 0; g < NG; ++g)
+        for (int lane = 0; lane < 64; ++lane)
+          for (int i = 0; i < 8; ++i)
+            dst[(((size_t)cb * NG + g) * 64 + lane) * 8 + i] =
+                src[(size_t)(cb * 32 + (lane & 31)) * op.Kp + 16 * g + 8 * (lane >> 5) + i];
+    void* d = nullptr;
+    if (upload(e, &d, dst.data(), dst.size() * 2)) return false;
+    L.w = (const bf16_t*)d;
+    return true;
+  };
+  auto add_table = [&](FusedLayer& L, const Op& op) -> bool {
+    const int c4 = (L.c_write + 3) & ~3;
+    L.ss_off = I.ss_off + (int)table.size() * 4;
+    const size_t at = table.size();
+    table.resize(at + 2 * (size_t)c4, 0.f);
+    if (e->dry) return true;
+    return hipMemcpy(&table[at], op.d_scale, (size_t)L.c_write * 4, hipMemcpyDeviceToHost) == hipSuccess &&
+           hipMemcpy(&table[at + c4], op.d_shift, (size_t)L.c_write * 4, hipMemcpyDeviceToHost) == hipSuccess;
+  };
+  for (size_t i = 0; i < M.ops.size(); ++i) {
+    const Op& op = M.ops[i];
+    const Tensor& x = tens(op.in);
+    const Tensor& y = M.tensors[op.out];
+    FusedLayer L{};
+    bool aliased = false;
+    if (op.kind == O_CONV && !y.is_logits) {
+      if (x.kind != T_IMG || op.pool2 || op.kh != op.kw || (op.kh != 1 && op.kh != 3) || op.pad != op.kh / 2 ||
+          (op.stride != 1 && op.stride != 2) || !cs_ok(op.Cs_in) || !cs_ok(y.Cs) || op.c_out > 64 ||
+          (op.Wo & (op.Wo - 1)) != 0 || (op.Ho * op.Wo) % 32 != 0 || op.Kp / 64 >= 12 ||
+          (op.in2 >= 0 && op.in2 == op.in))
+        return false;
+      L.op = F_CONV;
+      L.res_off = -1;
+      if (op.in2 >= 0) {
+        const Tensor& r = M.tensors[op.in2];
+        L.res_off = (int)off[op.in2];
+        if (r.last_use == (int)i && nbytes(r) == nbytes(y)) {
+          off[op.out] = off[op.in2];
+          aliased = true;
+        }
+      }
+      if (!aliased) off[op.out] = ar.place(nbytes(y), false);
+      if (off[op.out] < 0) return false;
+      L.in_off = (int)loff(op.in);
+      L.out_off = (int)off[op.out];
+      L.H = op.H; L.W = op.W; L.Cs = op.Cs_in; L.Ho = op.Ho; L.Wo = op.Wo; L.Cso = y.Cs; L.c_write = y.Cs;
+      L.kh = op.kh; L.kw = op.kw; L.stride = op.stride; L.pad = op.pad; L.relu = op.relu;
+      L.K = op.K; L.Kp = op.Kp;
+      L.lwo = 31 - __builtin_clz((unsigned)op.Wo);
+      L.n_cb = (y.Cs + 31) / 32;
+      L.n_pb = op.Ho * op.Wo / 32;
+      // pixel blocks per wave task: enough tasks for every wave, the A fragments reused
+      // over up to 4 blocks; a divisor of n_pb
+      const int want = std::max(1, std::min(4, L.n_pb * L.n_cb / kFusedWaves));
+      L.ch = 1;
+      for (int c = 4; c >= 1; c /= 2)
+        if (c <= want && L.n_pb % c == 0) { L.ch = c; break; }
+    } else if (op.kind == O_GAP) {
+      if (x.kind != T_IMG || !cs_ok(op.Cs_in)) return false;
+      L.op = F_GAP;
+      off[op.out] = ar.place((size_t)op.Cs_in * 2, false);
+      if (off[op.out] < 0) return false;
+      L.in_off = (int)loff(op.in);
+      L.out_off = (int)off[op.out];
+      L.H = op.H; L.W = op.W; L.Cs = op.Cs_in;
+      // strided partial sums [P][Cs] (fp32) for the block summation order
+      const int G = op.Cs_in / 8, P = 256 / std::min(G, 64);
+      const long long tmp = ar.place((size_t)P * op.Cs_in * 4, false);
+      if (tmp < 0) return false;
+      L.tmp_off = (int)tmp;
+      ar.release(tmp);
+    } else if (op.kind == O_CONV && y.is_logits) {
+      if (i + 1 != M.ops.size() || op.in < 0 || writer[op.in] < 0 || M.ops[writer[op.in]].kind != O_GAP ||
+          op.Cs_in > 64 || op.K != op.Cs_in || op.c_out > 32 * kFusedWaves || op.Kp / 64 >= 12)
+        return false;
+      L.op = F_FC;
+      L.in_off = (int)off[op.in];
+      L.Cs = op.Cs_in; L.K = op.K; L.Kp = op.Kp;
+      L.Cso = y.c; L.c_write = y.c; L.relu = op.relu;
+      L.n_cb = (op.c_out + 31) / 32;
+    } else {
+      return false;
+    }
+    if (L.op != F_GAP && !add_table(L, op)) return false;
+    if (L.op != F_GAP && !frag_weights(L, op)) return false;
+    if (op.in == -1 && in_last == (int)i) ar.release(in_off);
+    for (int src : {op.in, op.in2})
+      if (src >= 0 && M.tensors[src].last_use == (int)i && !(aliased && src == op.in2)) ar.release(off[src]);
+    prog.push_back(L);
+  }
+  const size_t tbytes = round_up_sz(table.size() * 4, 16);
+  if (ar.peak > (size_t)kFusedLdsBytes || prog.size() + 1 > (size_t)kFusedMaxLayers || tbytes > (size_t)kFusedTableBytes)
+    return false;
+  table.resize(tbytes / 4, 0.f);
+  void* d_table = nullptr;
+  if (upload(e, &d_table, table.data(), tbytes)) {
+    (void)hipGetLastError();
+    return false;
+  }
+  prog[0].scale = (const float*)d_table;
+  prog[0].c_write = (int)tbytes;
+  prog.push_back(FusedLayer{});   // F_END
+  M.fprog.swap(prog);
+  return true;
+}
+
+// Algorithmic FLOPs and bytes of model M's forward pass over n requests (the sums of
+// its launches' counts; weights read once).
+void model_alg(const rafiki_ensemble_s* e, const Model& M, int n, double* flops, double* bytes) {
+  const double es = (double)e->esz();
+  double f = 0.0, wb = 0.0;
+  for (const Op& op : M.ops) {
+    if (op.kind != O_CONV) continue;
+    const double kalg = (double)op.kh * op.kw * op.cin_l;
+    f += 2.0 * n * op.Ho * op.Wo * (double)op.c_out * kalg;
+    wb += (double)op.c_out * kalg * es;
+  }
+  *flops = f;
+  *bytes = wb + (double)n * e->H * e->W * e->C * es + (double)n * e->n_classes * 4.0;
+}
+
 unsigned magic_div(int d) { return d == 1 ? 0u : (unsigned)((((unsigned long long)1 << 32) + d - 1) / d); }
 
 // Tensor `id` of model M; id -1 is the model input `in` (staged images or the token batch).
@@ -1004,7 +1228,9 @@ int tune(rafiki_ensemble_s* e, int n, const void* in, hipStream_t s) {
   std::vector<std::vector<int>> choice(NM);
   std::vector<std::vector<std::vector<int>>> cand(NM);
   std::vector<double> est(NM, 0.0);
-  const bool timing = e->autotune && e->precision == RAFIKI_BF16;
+  bool all_fused = e->d_fprog != nullptr;
+  for (const Model& M : e->models) all_fused = all_fused && !M.fprog.empty();
+  const bool timing = e->autotune && e->precision == RAFIKI_BF16 && !all_fused;
   for (size_t mi = 0; mi < NM; ++mi) {
     const Model& M = e->models[mi];
     choice[mi].assign(M.ops.size(), -1);
@@ -1377,6 +1603,7 @@ int rafiki_ensemble_create(const rafiki_model_desc* models, int n_models, const 
   if (const char* t = std::getenv("RAFIKI_SCHEDULE_TUNING")) e->tune_schedule = std::atoi(t) != 0;
   if (const char* t = std::getenv("RAFIKI_FUSE_BRANCHES")) e->fuse_branches = std::atoi(t) != 0;
   if (const char* t = std::getenv("RAFIKI_GROUPED")) e->grouped = std::atoi(t) != 0;
+  if (const char* t = std::getenv("RAFIKI_FUSED_NET")) e->fused_net = std::atoi(t) != 0;
   // Pass 1: validate every model and infer shapes without touching the device.
   e->dry = true;
   e->models.resize(n_models);
@@ -1411,6 +1638,19 @@ int rafiki_ensemble_create(const rafiki_model_desc* models, int n_models, const 
       }
   }
   int rc;
+  {   // whole-network programs of the models that fit the kernel
+    std::vector<FusedLayer> progs((size_t)n_models * kFusedMaxLayers, FusedLayer{});
+    bool any = false;
+    for (int m = 0; m < n_models; ++m)
+      if (plan_fused(e.get(), e->models[m])) {
+        std::copy(e->models[m].fprog.begin(), e->models[m].fprog.end(), progs.begin() + (size_t)m * kFusedMaxLayers);
+        any = true;
+      }
+    if (any) {
+      rc = upload(e.get(), (void**)&e->d_fprog, progs.data(), progs.size() * sizeof(FusedLayer));
+      if (rc) return rc;
+    }
+  }
   if (e->input_kind == RAFIKI_INPUT_IMAGE_NCHW_F32) {
     rc = dev_alloc(e.get(), &e->d_staged, (size_t)e->max_batch * e->H * e->W * e->in_Cs * e->esz());
     if (rc) return rc;
@@ -1461,10 +1701,45 @@ static bool grouped_selection(const rafiki_ensemble_s* h, const CombineArgs& ca)
   return true;
 }
 
+// Model m runs as the whole-network kernel.
+static bool fused_model(const rafiki_ensemble_s* h, int m) { return h->d_fprog && !h->models[m].fprog.empty(); }
+static bool fused_selection(const rafiki_ensemble_s* h, const CombineArgs& ca) {
+  for (int i = 0; i < ca.S; ++i)
+    if (!fused_model(h, ca.sel[i])) return false;
+  return ca.S > 0;
+}
+
+// One launch of the whole-network kernel: the models of `mask` over n staged images,
+// model m's logits at logits + m * ld_model.
+static int run_fused(const rafiki_ensemble_s* h, uint32_t mask, const void* in, int n, float* logits,
+                     long long ld_model, hipStream_t s) {
+  FusedNetArgs a{};
+  a.progs = h->d_fprog;
+  a.logits = logits;
+  a.ld_model = ld_model;
+  a.mask = mask;
+  a.in = (const bf16_t*)in;
+  double flops = 0.0, bytes = 0.0;
+  for (int m = 0; m < h->n_models; ++m)
+    if ((mask >> m) & 1u) {
+      double f, b;
+      model_alg(h, h->models[m], n, &f, &b);
+      flops += f;
+      bytes += b;
+    }
+  TRACED(h, s, RAFIKI_K_FUSED_NET, -1, -1, flops, bytes, launch_fused_net(a, n, __builtin_popcount(mask), s));
+  return RAFIKI_OK;
+}
+
 static int forward(rafiki_ensemble_t h, const CombineArgs& ca, const void* in, int n, hipStream_t s,
                    rafiki_ensemble_s::Sched sched, const CallScratch* ws = nullptr) {
   const int solo = sched.solo;
   int rc = RAFIKI_OK;
+  if (fused_selection(h, ca)) {   // every selected model in one launch
+    uint32_t mask = 0;
+    for (int i = 0; i < ca.S; ++i) mask |= 1u << ca.sel[i];
+    return run_fused(h, mask, in, n, h->d_logits, ca.ld_model, s);
+  }
   if (grouped_selection(h, ca)) {   // one launch per op for up to kMaxGroup members, on the caller's stream
     for (int c0 = 0; c0 < ca.S; c0 += kMaxGroup) {
       const int nm = std::min(kMaxGroup, ca.S - c0);
@@ -1554,7 +1829,8 @@ static int forward(rafiki_ensemble_t h, const CombineArgs& ca, const void* in, i
 static int pick_schedule(rafiki_ensemble_t h, const CombineArgs& ca, const void* in, int n, uint32_t mask,
                          hipStream_t s, rafiki_ensemble_s::Sched* sched, const CallScratch* ws = nullptr) {
   *sched = {};
-  if (ca.S < 3 || !h->concurrent || (h->trace.on && !h->trace.concurrent) || grouped_selection(h, ca))
+  if (ca.S < 3 || !h->concurrent || (h->trace.on && !h->trace.concurrent) || grouped_selection(h, ca) ||
+      fused_selection(h, ca))
     return RAFIKI_OK;
   const auto key = std::make_pair(n, mask);
   const auto it = h->schedule.find(key);
@@ -1765,7 +2041,9 @@ int rafiki_ensemble_model_logits(rafiki_ensemble_t h, int model, const void* bat
   hipStream_t s = (hipStream_t)stream;
   const void* in = model_input(h, batch, h->d_staged);
   rc = stage(h, batch, n, s, h->d_staged);
-  if (!rc) rc = tune(h, n, in, s);
+  if (rc) return rc;
+  if (fused_model(h, model)) return run_fused(h, 1u << model, in, n, out_logits, 0, s);
+  rc = tune(h, n, in, s);
   if (rc) return rc;
   return run_model(h, model, in, n, out_logits, s);
 }

@@ -14,6 +14,7 @@ import pytest
 import torch
 
 import oracle
+import envutil
 import workloads as wl
 from paper_1804_06087_amd import Ensemble
 
@@ -104,7 +105,7 @@ def test_graph_dropped_by_force_tile():
     cfg, specs, params, batch = wl.build_config(2, n=16)
     C = 10
     x = torch.from_numpy(batch).to(DEV)
-    with Ensemble(specs, params, precision="bf16", max_batch=16) as ens:
+    with envutil.create({"RAFIKI_FUSED_NET": "0"}, specs, params, "bf16", 16) as ens:   # tiles: the layer path
         ens.use_graphs(True)
         base = _infer(ens, x, 16, 0b111, C)
         p, lab = _infer(ens, x, 16, 0b111, C)          # captured
@@ -125,16 +126,8 @@ def test_graph_replay_under_each_schedule(solo, asc):
     cfg, specs, params, batch = wl.build_config(2, n=24)
     C = 10
     x = torch.from_numpy(batch).to(DEV)
-    old = os.environ.get("RAFIKI_GROUPED")
-    os.environ["RAFIKI_GROUPED"] = "0"   # schedules order the models' own streams (no grouped launches)
-    try:
-        ens = Ensemble(specs, params, precision="bf16", max_batch=24)
-    finally:
-        if old is None:
-            del os.environ["RAFIKI_GROUPED"]
-        else:
-            os.environ["RAFIKI_GROUPED"] = old
-    with ens:
+    # schedules order the models' own streams (no grouped or whole-network launches)
+    with envutil.create(envutil.LAYER_PATH, specs, params, "bf16", 24) as ens:
         _infer(ens, x, 24, 0b111, C)                   # tunes n = 24
         ens.set_schedule(24, 0b111, solo, asc)
         ens.use_graphs(False)

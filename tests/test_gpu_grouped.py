@@ -14,25 +14,19 @@ import numpy as np
 import pytest
 import torch
 
+import envutil
 import oracle
 import workloads as wl
 from workloads import ModelSpec
-from paper_1804_06087_amd import Ensemble
 
 pytestmark = pytest.mark.gpu
 DEV = torch.device("cuda:0")
 
 
 def make(specs, params, precision, max_batch, grouped):
-    old = os.environ.get("RAFIKI_GROUPED")
-    os.environ["RAFIKI_GROUPED"] = "1" if grouped else "0"
-    try:
-        return Ensemble(specs, params, precision=precision, max_batch=max_batch)
-    finally:
-        if old is None:
-            del os.environ["RAFIKI_GROUPED"]
-        else:
-            os.environ["RAFIKI_GROUPED"] = old
+    # the layer-by-layer path (the whole-network kernel would run the ResNets in one launch)
+    return envutil.create({"RAFIKI_GROUPED": "1" if grouped else "0", "RAFIKI_FUSED_NET": "0"}, specs, params,
+                          precision, max_batch)
 
 
 def run(ens, x, n, mask, C):

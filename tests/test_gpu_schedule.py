@@ -11,6 +11,7 @@ import numpy as np
 import pytest
 import torch
 
+import envutil
 import workloads as wl
 from paper_1804_06087_amd import Ensemble, RafikiError, RAFIKI_ERR_INVALID
 
@@ -20,16 +21,9 @@ DEV = torch.device("cuda:0")
 
 def _ungrouped(specs, params, max_batch):
     """Schedules order the models' own streams, so identical members (which otherwise
-    run as grouped launches on one stream) are created with grouping off."""
-    old = os.environ.get("RAFIKI_GROUPED")
-    os.environ["RAFIKI_GROUPED"] = "0"
-    try:
-        return Ensemble(specs, params, precision="bf16", max_batch=max_batch)
-    finally:
-        if old is None:
-            del os.environ["RAFIKI_GROUPED"]
-        else:
-            os.environ["RAFIKI_GROUPED"] = old
+    run as grouped launches on one stream, or the ResNets as one whole-network launch)
+    are created on the layer-by-layer path with grouping off."""
+    return envutil.create(envutil.LAYER_PATH, specs, params, "bf16", max_batch)
 
 
 def _infer(ens, x, n, mask, C, vote=False):

@@ -130,11 +130,18 @@ def resnet20() -> ModelSpec:
     The first block of stages 2 and 3 strides by 2 and uses a 1x1 stride-2 conv + BN
     projection shortcut.  Within a block the layer order is [projection], conv_a, conv_b.
     """
+    return resnet_cifar(3)
+
+
+def resnet_cifar(blocks: int, widths: Tuple[int, int, int] = (16, 32, 64), n_classes: int = 10,
+                 name: Optional[str] = None) -> ModelSpec:
+    """CIFAR ResNet of 6 * blocks + 2 layers (blocks = 3: ResNet-20, 5: ResNet-32, ...),
+    the stem and first stage at widths[0], stages 2 and 3 at widths[1] and widths[2]."""
     b = _Builder()
-    x = b.conv(-1, 3, 16, 3)
-    c_prev = 16
-    for stage, width in enumerate((16, 32, 64)):
-        for blk in range(3):
+    x = b.conv(-1, 3, widths[0], 3)
+    c_prev = widths[0]
+    for stage, width in enumerate(widths):
+        for blk in range(blocks):
             stride = 2 if (stage > 0 and blk == 0) else 1
             if stride != 1 or c_prev != width:
                 sc = b.conv(x, c_prev, width, 1, stride=stride, pad=0, relu=False)
@@ -143,9 +150,9 @@ def resnet20() -> ModelSpec:
             a = b.conv(x, c_prev, width, 3, stride=stride)
             x = b.conv(a, width, width, 3, relu=True, residual=sc)
             c_prev = width
-    x = b.add(op=GLOBAL_AVGPOOL, input=x, c_in=64, c_out=64)
-    b.add(op=FC, input=x, c_in=64, c_out=10, bias=True)
-    return ModelSpec("resnet20", b.layers, 10, (3, 32, 32))
+    x = b.add(op=GLOBAL_AVGPOOL, input=x, c_in=c_prev, c_out=c_prev)
+    b.add(op=FC, input=x, c_in=c_prev, c_out=n_classes, bias=True)
+    return ModelSpec(name or f"resnet{6 * blocks + 2}", b.layers, n_classes, (3, 32, 32))
 
 
 def _resnet_bottleneck(name: str, blocks: Tuple[int, int, int, int]) -> ModelSpec:
