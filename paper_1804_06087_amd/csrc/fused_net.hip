@@ -20,8 +20,8 @@
 //   with Ho * Wo a multiple of 32, so its column is p % 32; the FC's row is the image
 //   index n); groups past K hold only zero products and are not run;
 // * the epilogue is fma(acc, scale, shift), + residual, ReLU, one round to nearest
-//   even bf16 (v_cvt_pk_bf16_f32 rounds as the integer form of the layer kernels does
-//   for every finite value);
+//   even bf16 (v_cvt_pk_bf16_f32 rounds as the integer form of the layer kernels does,
+//   and the integer-max ReLU equals their fmaxf, for every finite value);
 // * the average pool sums in the order of the batched kernel chosen for this batch
 //   size (positions in sequence, or strided partial sums folded in order), then
 //   multiplies by 1 / HW;
@@ -83,19 +83,46 @@ __device__ __forceinline__ void conv_chunk(const FusedLayer& L, char* lds, int c
   const int lr = 28 - __builtin_clz(L.Cs), sh = 4 - lr;
   const int fx = CPT > 0 ? fk : 0;
   int q[CH][NQ];
+  if ((L.Wo & 31) == 0 && (L.W & 15) == 0) {
+    // Each pixel block lies in one output row (wave-uniform ho), and the swizzle slot
+    // of an input pixel depends on its column alone (W % 16 == 0): a tap's address is
+    // a uniform row offset plus one of KH per-lane column parts.
 #pragma unroll
-  for (int j = 0; j < CH; ++j) {
-    const int p = (pb0 + j) * 32 + frow;
-    const int ho = p >> L.lwo, wo = p & (L.Wo - 1);
-    const int hi0 = ho * L.stride - L.pad, wi0 = wo * L.stride - L.pad;
-    const int pin0 = hi0 * L.W + wi0;
+    for (int j = 0; j < CH; ++j) {
+      const int m0 = (pb0 + j) * 32;
+      const int ho = m0 >> L.lwo;
+      const int wi0 = ((m0 & (L.Wo - 1)) + frow) * L.stride - L.pad;
+      int cpart[KH];
+      bool cok[KH];
 #pragma unroll
-    for (int t = 0; t < NQ; ++t) {
-      const int u = t / KH, v = t % KH;
-      const int pin = pin0 + u * L.W + v;
-      const int a = L.in_off + pin * R16 + (((int)__builtin_amdgcn_ubfe((unsigned)pin, sh, lr) ^ fx) << 4);
-      const bool ok = t < TAPS && (unsigned)(hi0 + u) < (unsigned)L.H && (unsigned)(wi0 + v) < (unsigned)L.W;
-      q[j][t] = ok ? a : kZeroOff;
+      for (int v = 0; v < KH; ++v) {
+        const int wi = wi0 + v;
+        cok[v] = (unsigned)wi < (unsigned)L.W;
+        cpart[v] = L.in_off + wi * R16 + (((int)__builtin_amdgcn_ubfe((unsigned)wi, sh, lr) ^ fx) << 4);
+      }
+#pragma unroll
+      for (int t = 0; t < NQ; ++t) {
+        const int u = t / KH, v = t % KH;
+        const int hi = ho * L.stride - L.pad + u;
+        const bool rowok = t < TAPS && (unsigned)hi < (unsigned)L.H;   // wave-uniform
+        q[j][t] = rowok && cok[v] ? cpart[v] + hi * L.W * R16 : kZeroOff;
+      }
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < CH; ++j) {
+      const int p = (pb0 + j) * 32 + frow;
+      const int ho = p >> L.lwo, wo = p & (L.Wo - 1);
+      const int hi0 = ho * L.stride - L.pad, wi0 = wo * L.stride - L.pad;
+      const int pin0 = hi0 * L.W + wi0;
+#pragma unroll
+      for (int t = 0; t < NQ; ++t) {
+        const int u = t / KH, v = t % KH;
+        const int pin = pin0 + u * L.W + v;
+        const int a = L.in_off + pin * R16 + (((int)__builtin_amdgcn_ubfe((unsigned)pin, sh, lr) ^ fx) << 4);
+        const bool ok = t < TAPS && (unsigned)(hi0 + u) < (unsigned)L.H && (unsigned)(wi0 + v) < (unsigned)L.W;
+        q[j][t] = ok ? a : kZeroOff;
+      }
     }
   }
   f32x16 acc[CH];
@@ -133,36 +160,53 @@ __device__ __forceinline__ void conv_chunk(const FusedLayer& L, char* lds, int c
 
   // Epilogue: lane (frow, fk) holds channels cb * 32 + 8 qq + 4 fk + r (qq, r < 4) of
   // pixel (pb0 + j) * 32 + frow: 8 bytes of logical chunk cb * 4 + qq of that pixel.
+  // Every LDS read (scale / shift, residual) is issued before the first write: the
+  // output may replace the residual in place, and each (pixel, channel) is read and
+  // written by this lane alone.  ReLU as an integer max with 0 equals fmaxf(v, 0) for
+  // every value but NaN (-0 and negative values give +0).
   const int R16o = L.Cso << 1, c4 = (L.c_write + 3) & ~3;
-  int ro[CH], rr[CH], sw[CH];
+  constexpr int NQQ = 4;
+  int ro[CH], sw[CH];
+  f32x4 sc[NQQ], sf[NQQ];
+  uint2 rv[NQQ][CH];
 #pragma unroll
   for (int j = 0; j < CH; ++j) {
     const int p = (pb0 + j) * 32 + frow;
-    ro[j] = L.out_off + p * R16o + 8 * fk;
-    rr[j] = L.res_off + p * R16o + 8 * fk;
+    ro[j] = p * R16o + 8 * fk;
     sw[j] = swz(p, L.Cso);
   }
 #pragma unroll
-  for (int qq = 0; qq < 4; ++qq) {
+  for (int qq = 0; qq < NQQ; ++qq) {
     const int c = cb * 32 + 8 * qq + 4 * fk;
     if (c >= L.c_write) continue;
-    const f32x4 sc = *(const f32x4*)(lds + L.ss_off + 4 * c);
-    const f32x4 sf = *(const f32x4*)(lds + L.ss_off + 4 * (c4 + c));
+    sc[qq] = *(const f32x4*)(lds + L.ss_off + 4 * c);
+    sf[qq] = *(const f32x4*)(lds + L.ss_off + 4 * (c4 + c));
+    if (L.res_off >= 0) {
+#pragma unroll
+      for (int j = 0; j < CH; ++j) rv[qq][j] = *(const uint2*)(lds + L.res_off + ro[j] + (((cb * 4 + qq) ^ sw[j]) << 4));
+    }
+  }
+#pragma unroll
+  for (int qq = 0; qq < NQQ; ++qq) {
+    const int c = cb * 32 + 8 * qq + 4 * fk;
+    if (c >= L.c_write) continue;
 #pragma unroll
     for (int j = 0; j < CH; ++j) {
-      const int slot = ((cb * 4 + qq) ^ sw[j]) << 4;
-      float v[4] = {__builtin_fmaf(acc[j][4 * qq + 0], sc[0], sf[0]), __builtin_fmaf(acc[j][4 * qq + 1], sc[1], sf[1]),
-                    __builtin_fmaf(acc[j][4 * qq + 2], sc[2], sf[2]), __builtin_fmaf(acc[j][4 * qq + 3], sc[3], sf[3])};
+      float v[4] = {__builtin_fmaf(acc[j][4 * qq + 0], sc[qq][0], sf[qq][0]),
+                    __builtin_fmaf(acc[j][4 * qq + 1], sc[qq][1], sf[qq][1]),
+                    __builtin_fmaf(acc[j][4 * qq + 2], sc[qq][2], sf[qq][2]),
+                    __builtin_fmaf(acc[j][4 * qq + 3], sc[qq][3], sf[qq][3])};
       if (L.res_off >= 0) {
-        const uint2 r = *(const uint2*)(lds + rr[j] + slot);
+        const uint2 r = rv[qq][j];
         v[0] += fbf2f(r.x & 0xFFFFu); v[1] += fbf2f(r.x >> 16);
         v[2] += fbf2f(r.y & 0xFFFFu); v[3] += fbf2f(r.y >> 16);
       }
       if (L.relu) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) v[r] = fmaxf(v[r], 0.f);
+        for (int r = 0; r < 4; ++r) v[r] = __int_as_float(max(__float_as_int(v[r]), 0));
       }
-      *(uint2*)(lds + ro[j] + slot) = make_uint2(pack_bf16(v[0], v[1]), pack_bf16(v[2], v[3]));
+      *(uint2*)(lds + L.out_off + ro[j] + (((cb * 4 + qq) ^ sw[j]) << 4)) =
+          make_uint2(pack_bf16(v[0], v[1]), pack_bf16(v[2], v[3]));
     }
   }
 }
