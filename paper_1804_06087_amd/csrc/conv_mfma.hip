@@ -28,6 +28,16 @@ __device__ __forceinline__ uint32_t f2bf_m(float f) {   // nearest, ties to even
   u += 0x7FFFu + ((u >> 16) & 1u);
   return u >> 16;
 }
+// Two values rounded to bf16 by v_cvt_pk_bf16_f32 (nearest even: the same bits as
+// f2bf_m for every finite value), a in the low half.
+typedef __bf16 bf16x2_m __attribute__((ext_vector_type(2)));
+typedef float f32x2_m __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t pack2_bf16(float a, float b) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_m{a, b}, bf16x2_m));
+}
+// ReLU as an integer max with 0: the same bits as fmaxf(v, 0) for every value but NaN
+// (negative values and -0 give +0, as fmaxf does on this hardware), in one instruction.
+__device__ __forceinline__ float relu_m(float v) { return __int_as_float(max(__float_as_int(v), 0)); }
 
 // s_waitcnt with only the vector-memory counter constrained (gfx9 encoding).
 template <int N>
@@ -547,13 +557,13 @@ __global__ __launch_bounds__(WM * WN * 64, OCC > 0 ? OCC : 1) void conv_mfma_ker
         }
         if (a.relu) {
 #pragma unroll
-          for (int j = 0; j < 8; ++j) v[j] = fmaxf(v[j], 0.f);
+          for (int j = 0; j < 8; ++j) v[j] = relu_m(v[j]);
         }
         uint4 w;
-        w.x = f2bf_m(v[0]) | (f2bf_m(v[1]) << 16);
-        w.y = f2bf_m(v[2]) | (f2bf_m(v[3]) << 16);
-        w.z = f2bf_m(v[4]) | (f2bf_m(v[5]) << 16);
-        w.w = f2bf_m(v[6]) | (f2bf_m(v[7]) << 16);
+        w.x = pack2_bf16(v[0], v[1]);
+        w.y = pack2_bf16(v[2], v[3]);
+        w.z = pack2_bf16(v[4], v[5]);
+        w.w = pack2_bf16(v[6], v[7]);
         *(uint4*)((bf16_t*)a.y + (long long)(mb >> 2) * a.ldy + c) = w;
       }
       __builtin_amdgcn_s_waitcnt(0xC07F);   // reads done before the region is rewritten
@@ -588,13 +598,13 @@ __global__ __launch_bounds__(WM * WN * 64, OCC > 0 ? OCC : 1) void conv_mfma_ker
       }
       if (a.relu) {
 #pragma unroll
-        for (int j = 0; j < 8; ++j) v[j] = fmaxf(v[j], 0.f);
+        for (int j = 0; j < 8; ++j) v[j] = relu_m(v[j]);
       }
       uint4 w;
-      w.x = f2bf_m(v[0]) | (f2bf_m(v[1]) << 16);
-      w.y = f2bf_m(v[2]) | (f2bf_m(v[3]) << 16);
-      w.z = f2bf_m(v[4]) | (f2bf_m(v[5]) << 16);
-      w.w = f2bf_m(v[6]) | (f2bf_m(v[7]) << 16);
+      w.x = pack2_bf16(v[0], v[1]);
+      w.y = pack2_bf16(v[2], v[3]);
+      w.z = pack2_bf16(v[4], v[5]);
+      w.w = pack2_bf16(v[6], v[7]);
       *(uint4*)((bf16_t*)a.y + o) = w;
     }
     __builtin_amdgcn_s_waitcnt(0xC07F);   // reads done before the region is rewritten
