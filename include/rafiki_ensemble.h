@@ -299,6 +299,24 @@ int rafiki_ensemble_force_tile(rafiki_ensemble_t h, int cfg);
 int rafiki_ensemble_get_schedule(rafiki_ensemble_t h, int n, uint32_t model_subset_mask, int* solo, int* ascending);
 int rafiki_ensemble_set_schedule(rafiki_ensemble_t h, int n, uint32_t model_subset_mask, int solo, int ascending);
 
+/* Paired layers of two different models (Section 5.1: the selected models all run the
+ * same batch).  At create, every two bf16 models with different layer lists whose ops
+ * align for at least half of the shorter list (a longest common subsequence under equal
+ * launch shapes: ResNet-50 within ResNet-101) are pairable.  A paired schedule runs such
+ * a pair on one lane, each aligned pair of ops as one launch with a member per model and
+ * the other ops alone in the merged order, while the other selected models run one after
+ * another on a second lane.  Each member's outputs are those of its own launch, so the
+ * schedule never changes a result.  The schedule timing of infer (above) also times
+ * every pairable pair of the subset (with two selected models as well).
+ * get_schedule_pair: the kept choice's pair, or *pa = *pb = -1 if it is not paired;
+ * RAFIKI_ERR_INVALID if no schedule has been chosen yet.
+ * set_schedule_pair: pa < pb, a pairable pair of the subset, or pa = -1 (all models
+ * concurrent); synchronises the device and drops any kept graphs.
+ * pairing: the number of aligned ops of models a < b (0: not pairable). */
+int rafiki_ensemble_get_schedule_pair(rafiki_ensemble_t h, int n, uint32_t model_subset_mask, int* pa, int* pb);
+int rafiki_ensemble_set_schedule_pair(rafiki_ensemble_t h, int n, uint32_t model_subset_mask, int pa, int pb);
+int rafiki_ensemble_pairing(rafiki_ensemble_t h, int a, int b, int* aligned);
+
 /* Graph replay of the forward passes (off by default; environment RAFIKI_GRAPHS=1 turns
  * it on at create).  Measured on MI355X it is no faster than the eager launches for one
  * model and slower for several, whose branches the replay did not overlap as well as

@@ -24,7 +24,8 @@ EXPORTED = ("rafiki_ensemble_create", "rafiki_ensemble_infer", "rafiki_ensemble_
             "rafiki_ensemble_infer_noalloc", "rafiki_ensemble_model_logits",
             "rafiki_ensemble_info", "rafiki_ensemble_trace", "rafiki_ensemble_trace_read",
             "rafiki_tile_config", "rafiki_ensemble_force_tile", "rafiki_ensemble_get_schedule",
-            "rafiki_ensemble_set_schedule", "rafiki_ensemble_use_graphs",
+            "rafiki_ensemble_set_schedule", "rafiki_ensemble_get_schedule_pair", "rafiki_ensemble_set_schedule_pair",
+            "rafiki_ensemble_pairing", "rafiki_ensemble_use_graphs",
             "rafiki_ensemble_graph_stats", "rafiki_combine_mean", "rafiki_combine_vote",
             "rafiki_maxpool_nhwc_bf16", "rafiki_global_avgpool_nhwc_bf16", "rafiki_probe_mfma_bf16",
             "rafiki_probe_hbm_read",
@@ -115,6 +116,10 @@ def load_library(path: str = LIB_PATH):
     lib.rafiki_ensemble_get_schedule.argtypes = [C.c_void_p, C.c_int, C.c_uint32, C.POINTER(C.c_int),
                                                  C.POINTER(C.c_int)]
     lib.rafiki_ensemble_set_schedule.argtypes = [C.c_void_p, C.c_int, C.c_uint32, C.c_int, C.c_int]
+    lib.rafiki_ensemble_get_schedule_pair.argtypes = [C.c_void_p, C.c_int, C.c_uint32, C.POINTER(C.c_int),
+                                                      C.POINTER(C.c_int)]
+    lib.rafiki_ensemble_set_schedule_pair.argtypes = [C.c_void_p, C.c_int, C.c_uint32, C.c_int, C.c_int]
+    lib.rafiki_ensemble_pairing.argtypes = [C.c_void_p, C.c_int, C.c_int, C.POINTER(C.c_int)]
     lib.rafiki_ensemble_use_graphs.argtypes = [C.c_void_p, C.c_int]
     lib.rafiki_ensemble_graph_stats.argtypes = [C.c_void_p, C.POINTER(C.c_int), C.POINTER(C.c_longlong),
                                                 C.POINTER(C.c_longlong)]
@@ -591,6 +596,22 @@ class Ensemble:
 
     def set_schedule(self, n: int, mask: int, solo: int, ascending: int = 0):
         _check(self._lib.rafiki_ensemble_set_schedule(self._h, n, mask, solo, ascending))
+
+    def get_schedule_pair(self, n: int, mask: int):
+        """The pair (a, b) whose aligned layers the schedule kept for (n, mask) runs as
+        two-member launches, or (-1, -1)."""
+        a, b = C.c_int(0), C.c_int(0)
+        _check(self._lib.rafiki_ensemble_get_schedule_pair(self._h, n, mask, C.byref(a), C.byref(b)))
+        return a.value, b.value
+
+    def set_schedule_pair(self, n: int, mask: int, a: int, b: int = -1):
+        _check(self._lib.rafiki_ensemble_set_schedule_pair(self._h, n, mask, a, b))
+
+    def pairing(self, a: int, b: int) -> int:
+        """Number of aligned ops of models a < b (0: not pairable)."""
+        v = C.c_int(0)
+        _check(self._lib.rafiki_ensemble_pairing(self._h, a, b, C.byref(v)))
+        return v.value
 
     def use_graphs(self, enable: bool):
         """Turn graph replay of the forward passes on or off (drops every kept graph)."""

@@ -185,10 +185,17 @@ struct rafiki_ensemble_s {
   // chosen by timing (solo -1: all concurrent; solo m: model m alone on one lane, the
   // others one after another on a second lane, longest estimated alone time first, or
   // shortest first when `ascending`).
+  // pa >= 0: models pa and pb run paired on one lane (their aligned ops as two-member
+  // launches) and the other selected models one after another on a second lane; solo
+  // and ascending are then unused.
   struct Sched {
-    int solo = -1, ascending = 0;
+    int solo = -1, ascending = 0, pa = -1, pb = -1;
   };
   std::map<std::pair<int, uint32_t>, Sched> schedule;
+  // Pairable models (a < b) of different layer lists: the merged op order of the two,
+  // each step (i, j) an op of a and an op of b with the same launch signature, or one of
+  // them -1 (that model's op alone).
+  std::map<std::pair<int, int>, std::vector<std::pair<int, int>>> pairing;
   bool tune_schedule = true;
   bool autotune = true;
   bool fuse_branches = true;        // fuse sibling max-over-time convolutions (bf16)
@@ -1322,8 +1329,12 @@ int tune(rafiki_ensemble_s* e, int n, const void* in, hipStream_t s) {
 // concatenation) are launched once per member.
 // Only ops [op_begin, op_end) are enqueued, so that the launches of several models
 // can be interleaved.
-int run_models(const rafiki_ensemble_s* e, const int* mis, int nm, const void* in, int n, float* const* logits,
-               hipStream_t s, size_t op_begin, size_t op_end, const CallScratch* ws) {
+// One op of several members in one launch: member k is op ois[k] of model mis[k]; every
+// member's op has the same launch signature (same_launch), so the launch shares shapes,
+// tile and K splits and each member's outputs are those of its own launch.  The tile
+// is member 0's tuned one (every tile gives the same sums).
+int run_op(const rafiki_ensemble_s* e, const int* mis, const int* ois, int nm, const void* in, int n,
+           float* const* logits, hipStream_t s, const CallScratch* ws) {
   if (nm < 1 || nm > kMaxGroup) return fail(RAFIKI_ERR_INVALID, "internal: group size");
   const int mi = mis[0];
   const Model& M = e->models[mi];
@@ -1332,24 +1343,24 @@ int run_models(const rafiki_ensemble_s* e, const int* mis, int nm, const void* i
   const std::vector<int>& cfgs = it == e->tuned.end() ? empty : it->second[mi];
   const int bf = e->precision == RAFIKI_BF16 ? 1 : 0;
   const double es = (double)e->esz();
-  op_end = std::min(op_end, M.ops.size());
-  for (size_t oi = op_begin; oi < op_end; ++oi) {
+  const size_t oi = (size_t)ois[0];
+  {
     const Op& op = M.ops[oi];
     const int li = op.out;
     // member k's op, tensors and pointers (k = 0 is model mi)
-    auto mop = [&](int k) -> const Op& { return e->models[mis[k]].ops[oi]; };
+    auto mop = [&](int k) -> const Op& { return e->models[mis[k]].ops[ois[k]]; };
     auto yptr = [&](int k) -> void* {
       const Model& Mk = e->models[mis[k]];
-      const Tensor& y = Mk.tensors[Mk.ops[oi].out];
+      const Tensor& y = Mk.tensors[Mk.ops[ois[k]].out];
       return y.is_logits ? (void*)logits[k] : (void*)(Mk.d_arena + y.off);
     };
     auto xptr = [&](int k, int id) { return tptr(e, e->models[mis[k]], id, in); };
     // this op's epilogue-max keys of member k (ws: after those of the model's earlier fused ops)
     auto slotptr = [&](int k) -> unsigned* {
       const Model& Mk = e->models[mis[k]];
-      if (!ws) return Mk.ops[oi].d_slot;
+      if (!ws) return Mk.ops[ois[k]].d_slot;
       unsigned* p = ws->slot[mis[k]];
-      for (size_t j = 0; j < oi; ++j)
+      for (int j = 0; j < ois[k]; ++j)
         if (Mk.ops[j].d_slot) p += (size_t)n * Mk.ops[j].ldslot;
       return p;
     };
@@ -1471,6 +1482,19 @@ int run_models(const rafiki_ensemble_s* e, const int* mis, int nm, const void* i
   return RAFIKI_OK;
 }
 
+int run_models(const rafiki_ensemble_s* e, const int* mis, int nm, const void* in, int n, float* const* logits,
+               hipStream_t s, size_t op_begin, size_t op_end, const CallScratch* ws) {
+  if (nm < 1 || nm > kMaxGroup) return fail(RAFIKI_ERR_INVALID, "internal: group size");
+  op_end = std::min(op_end, e->models[mis[0]].ops.size());
+  for (size_t oi = op_begin; oi < op_end; ++oi) {
+    int ois[kMaxGroup];
+    for (int k = 0; k < nm; ++k) ois[k] = (int)oi;
+    const int rc = run_op(e, mis, ois, nm, in, n, logits, s, ws);
+    if (rc) return rc;
+  }
+  return RAFIKI_OK;
+}
+
 int check_call(const rafiki_ensemble_s* h, const void* batch, int n) {
   if (!h) return fail(RAFIKI_ERR_INVALID, "null handle");
   if (!batch) return fail(RAFIKI_ERR_INVALID, "null batch pointer");
@@ -1523,6 +1547,42 @@ bool same_structure(const Model& A, const Model& B) {
       if (a.taps_by_block[j] != b.taps_by_block[j]) return false;
   }
   return true;
+}
+
+// Two ops whose launches can be one launch with a member each: the same kind, shapes,
+// K layout, padding, epilogue and output tensor layout (the tensors themselves differ).
+bool same_op(const Model& A, const Op& a, const Model& B, const Op& b) {
+  const Tensor &ya = A.tensors[a.out], &yb = B.tensors[b.out];
+  const int fa[] = {a.kind, a.H, a.W, a.Cs_in, a.Ho, a.Wo, a.kh, a.kw, a.stride, a.pad, a.relu, a.K, a.Kp, a.Co_pad,
+                    a.c_out, a.cin_l, a.k, a.pool2, a.nseg, a.tap_stride, a.ldslot, a.ca, a.cb, a.in2 >= 0,
+                    a.table != nullptr, a.d_slot != nullptr, ya.kind, ya.c, ya.h, ya.w, ya.Cs, ya.is_logits};
+  const int fb[] = {b.kind, b.H, b.W, b.Cs_in, b.Ho, b.Wo, b.kh, b.kw, b.stride, b.pad, b.relu, b.K, b.Kp, b.Co_pad,
+                    b.c_out, b.cin_l, b.k, b.pool2, b.nseg, b.tap_stride, b.ldslot, b.ca, b.cb, b.in2 >= 0,
+                    b.table != nullptr, b.d_slot != nullptr, yb.kind, yb.c, yb.h, yb.w, yb.Cs, yb.is_logits};
+  if (std::memcmp(fa, fb, sizeof(fa)) != 0 || a.nseg != 0 || a.kind == O_EMBED || a.kind == O_CONCAT) return false;
+  return true;
+}
+
+// The merged op order of two models: a longest common subsequence of their ops under
+// same_op (aligned steps), with each model's other ops in between in their own order.
+std::vector<std::pair<int, int>> align_ops(const Model& A, const Model& B) {
+  const int na = (int)A.ops.size(), nb = (int)B.ops.size();
+  std::vector<std::vector<int>> L(na + 1, std::vector<int>(nb + 1, 0));
+  for (int i = na - 1; i >= 0; --i)
+    for (int j = nb - 1; j >= 0; --j)
+      L[i][j] = same_op(A, A.ops[i], B, B.ops[j]) ? L[i + 1][j + 1] + 1 : std::max(L[i + 1][j], L[i][j + 1]);
+  std::vector<std::pair<int, int>> steps;
+  int i = 0, j = 0;
+  while (i < na || j < nb) {
+    if (i < na && j < nb && same_op(A, A.ops[i], B, B.ops[j]) && L[i][j] == L[i + 1][j + 1] + 1) {
+      steps.push_back({i++, j++});
+    } else if (j >= nb || (i < na && L[i + 1][j] >= L[i][j + 1])) {
+      steps.push_back({i++, -1});
+    } else {
+      steps.push_back({-1, j++});
+    }
+  }
+  return steps;
 }
 
 // Scratch of rafiki_ensemble_infer_noalloc: a file-scope device array, one copy per
@@ -1637,6 +1697,18 @@ int rafiki_ensemble_create(const rafiki_model_desc* models, int n_models, const 
         break;
       }
   }
+  // Pairable models: bf16, different layer lists, at least half of the shorter one's
+  // ops aligned with ops of the other.
+  if (e->precision == RAFIKI_BF16)
+    for (int a = 0; a < n_models; ++a)
+      for (int b = a + 1; b < n_models; ++b) {
+        if (e->group_of[a] == e->group_of[b]) continue;
+        std::vector<std::pair<int, int>> steps = align_ops(e->models[a], e->models[b]);
+        size_t matched = 0;
+        for (const auto& st : steps) matched += st.first >= 0 && st.second >= 0;
+        if (2 * matched >= std::min(e->models[a].ops.size(), e->models[b].ops.size()))
+          e->pairing[{a, b}] = std::move(steps);
+      }
   int rc;
   {   // whole-network programs of the models that fit the kernel
     std::vector<FusedLayer> progs((size_t)n_models * kFusedMaxLayers, FusedLayer{});
@@ -1731,6 +1803,77 @@ static int run_fused(const rafiki_ensemble_s* h, uint32_t mask, const void* in, 
   return RAFIKI_OK;
 }
 
+// The pairing of the selection's models pa and pb, or null.
+static const std::vector<std::pair<int, int>>* selected_pairing(const rafiki_ensemble_s* h, const CombineArgs& ca,
+                                                                int pa, int pb) {
+  if (pa < 0 || pb < 0) return nullptr;
+  bool a = false, b = false;
+  for (int i = 0; i < ca.S; ++i) {
+    a = a || ca.sel[i] == pa;
+    b = b || ca.sel[i] == pb;
+  }
+  const auto it = h->pairing.find({pa, pb});
+  return a && b && it != h->pairing.end() ? &it->second : nullptr;
+}
+
+// Forward passes with models pa and pb paired on one lane (each aligned pair of ops as
+// one two-member launch, their other ops alone, in the merged order) and the other
+// selected models one after another on a second lane, longest estimated alone time
+// first.  Launches are enqueued alternating between the lanes.
+static int forward_paired(rafiki_ensemble_t h, const CombineArgs& ca, const void* in, int n, hipStream_t s,
+                          int pa, int pb, const std::vector<std::pair<int, int>>& steps, const CallScratch* ws) {
+  std::vector<int> rest;
+  for (int i = 0; i < ca.S; ++i)
+    if (ca.sel[i] != pa && ca.sel[i] != pb) rest.push_back(ca.sel[i]);
+  std::vector<double> est(h->n_models, 1.0);
+  const auto mit = h->model_ms.find(n);
+  if (mit != h->model_ms.end()) est = mit->second;
+  std::stable_sort(rest.begin(), rest.end(), [&](int a, int b) { return est[a] > est[b]; });
+  std::vector<std::pair<int, int>> lane_b;   // (model, op) in order
+  for (int m : rest)
+    for (size_t oi = 0; oi < h->models[m].ops.size(); ++oi) lane_b.push_back({m, (int)oi});
+  Model& MA = h->models[pa];
+  Model* MB = rest.empty() ? nullptr : &h->models[rest[0]];
+  HIPCHK(hipEventRecord(h->staged_ev, s));
+  HIPCHK(hipStreamWaitEvent(MA.stream, h->staged_ev, 0));
+  if (MB) HIPCHK(hipStreamWaitEvent(MB->stream, h->staged_ev, 0));
+  auto join = [&]() {
+    hipError_t st = hipEventRecord(MA.done, MA.stream);
+    if (st == hipSuccess) st = hipStreamWaitEvent(s, MA.done, 0);
+    if (MB && st == hipSuccess) st = hipEventRecord(MB->done, MB->stream);
+    if (MB && st == hipSuccess) st = hipStreamWaitEvent(s, MB->done, 0);
+    return st;
+  };
+  float* lga = h->d_logits + (size_t)pa * ca.ld_model;
+  float* lgb = h->d_logits + (size_t)pb * ca.ld_model;
+  const size_t rounds = std::max(steps.size(), lane_b.size());
+  for (size_t r = 0; r < rounds; ++r) {
+    int rc = RAFIKI_OK;
+    if (r < steps.size()) {
+      const int i = steps[r].first, j = steps[r].second;
+      if (i >= 0 && j >= 0) {
+        const int mis[2] = {pa, pb}, ois[2] = {i, j};
+        float* lg[2] = {lga, lgb};
+        rc = run_op(h, mis, ois, 2, in, n, lg, MA.stream, ws);
+      } else {
+        const int mis[1] = {i >= 0 ? pa : pb}, ois[1] = {i >= 0 ? i : j};
+        float* lg[1] = {i >= 0 ? lga : lgb};
+        rc = run_op(h, mis, ois, 1, in, n, lg, MA.stream, ws);
+      }
+    }
+    if (rc == RAFIKI_OK && r < lane_b.size()) {
+      const int m = lane_b[r].first, oi = lane_b[r].second;
+      rc = run_model(h, m, in, n, h->d_logits + (size_t)m * ca.ld_model, MB->stream, oi, oi + 1, ws);
+    }
+    if (rc) {
+      (void)join();   // the caller's stream still waits for what the lanes already hold
+      return rc;
+    }
+  }
+  HIPCHK(join());
+  return RAFIKI_OK;
+}
+
 static int forward(rafiki_ensemble_t h, const CombineArgs& ca, const void* in, int n, hipStream_t s,
                    rafiki_ensemble_s::Sched sched, const CallScratch* ws = nullptr) {
   const int solo = sched.solo;
@@ -1755,6 +1898,10 @@ static int forward(rafiki_ensemble_t h, const CombineArgs& ca, const void* in, i
     return RAFIKI_OK;
   }
   const bool fork = h->concurrent && (!h->trace.on || h->trace.concurrent) && ca.S > 1;
+  if (fork && sched.pa >= 0) {
+    const auto* steps = selected_pairing(h, ca, sched.pa, sched.pb);
+    if (steps) return forward_paired(h, ca, in, n, s, sched.pa, sched.pb, *steps, ws);
+  }
   if (fork) {
     HIPCHK(hipEventRecord(h->staged_ev, s));
     // Lanes.  solo < 0: every model on its own lane.  solo = m: model m alone on one
@@ -1829,8 +1976,11 @@ static int forward(rafiki_ensemble_t h, const CombineArgs& ca, const void* in, i
 static int pick_schedule(rafiki_ensemble_t h, const CombineArgs& ca, const void* in, int n, uint32_t mask,
                          hipStream_t s, rafiki_ensemble_s::Sched* sched, const CallScratch* ws = nullptr) {
   *sched = {};
-  if (ca.S < 3 || !h->concurrent || (h->trace.on && !h->trace.concurrent) || grouped_selection(h, ca) ||
-      fused_selection(h, ca))
+  std::vector<std::pair<int, int>> pairs;   // pairable models of the selection
+  for (const auto& kv : h->pairing)
+    if (selected_pairing(h, ca, kv.first.first, kv.first.second)) pairs.push_back(kv.first);
+  if ((ca.S < 3 && pairs.empty()) || !h->concurrent || (h->trace.on && !h->trace.concurrent) ||
+      grouped_selection(h, ca) || fused_selection(h, ca))
     return RAFIKI_OK;
   const auto key = std::make_pair(n, mask);
   const auto it = h->schedule.find(key);
@@ -1840,10 +1990,12 @@ static int pick_schedule(rafiki_ensemble_t h, const CombineArgs& ca, const void*
   }
   if (!h->tune_schedule || h->trace.on) return RAFIKI_OK;   // never time candidates while tracing
   std::vector<rafiki_ensemble_s::Sched> cands(1);
-  for (int i = 0; i < ca.S; ++i) {
-    cands.push_back({ca.sel[i], 0});
-    if (ca.S >= 3) cands.push_back({ca.sel[i], 1});
-  }
+  if (ca.S >= 3)
+    for (int i = 0; i < ca.S; ++i) {
+      cands.push_back({ca.sel[i], 0});
+      cands.push_back({ca.sel[i], 1});
+    }
+  for (const auto& pr : pairs) cands.push_back({-1, 0, pr.first, pr.second});
   hipEvent_t ev[2] = {nullptr, nullptr};
   HIPCHK(hipEventCreate(&ev[0]));
   hipError_t st = hipEventCreate(&ev[1]);
@@ -2198,6 +2350,43 @@ int rafiki_ensemble_set_schedule(rafiki_ensemble_t h, int n, uint32_t mask, int 
   HIPCHK(hipDeviceSynchronize());   // graphs built with the old schedule may still run
   h->drop_graphs();
   h->schedule[std::make_pair(n, mask)] = {solo, ascending ? 1 : 0};
+  return RAFIKI_OK;
+}
+
+int rafiki_ensemble_get_schedule_pair(rafiki_ensemble_t h, int n, uint32_t mask, int* pa, int* pb) {
+  if (!h || !pa || !pb) return fail(RAFIKI_ERR_INVALID, "null argument");
+  const auto it = h->schedule.find(std::make_pair(n, mask));
+  if (it == h->schedule.end()) return fail(RAFIKI_ERR_INVALID, "no schedule chosen for this batch size and subset");
+  *pa = it->second.pa;
+  *pb = it->second.pb;
+  return RAFIKI_OK;
+}
+
+int rafiki_ensemble_set_schedule_pair(rafiki_ensemble_t h, int n, uint32_t mask, int pa, int pb) {
+  if (!h) return fail(RAFIKI_ERR_INVALID, "null handle");
+  if (n < 1 || n > h->max_batch || mask == 0 || (h->n_models < 32 && (mask >> h->n_models) != 0))
+    return fail(RAFIKI_ERR_INVALID, "batch size or subset mask out of range");
+  if (pa != -1 && (pa < 0 || pb <= pa || pb >= h->n_models || !((mask >> pa) & 1u) || !((mask >> pb) & 1u) ||
+                   !h->pairing.count({pa, pb})))
+    return fail(RAFIKI_ERR_INVALID, "pa < pb must be a pairable pair of the subset, or pa = -1");
+  HIPCHK(hipDeviceSynchronize());   // graphs built with the old schedule may still run
+  h->drop_graphs();
+  rafiki_ensemble_s::Sched sc;
+  if (pa >= 0) {
+    sc.pa = pa;
+    sc.pb = pb;
+  }
+  h->schedule[std::make_pair(n, mask)] = sc;
+  return RAFIKI_OK;
+}
+
+int rafiki_ensemble_pairing(rafiki_ensemble_t h, int a, int b, int* aligned) {
+  if (!h || !aligned) return fail(RAFIKI_ERR_INVALID, "null argument");
+  if (a < 0 || b <= a || b >= h->n_models) return fail(RAFIKI_ERR_INVALID, "need 0 <= a < b < n_models");
+  *aligned = 0;
+  const auto it = h->pairing.find({a, b});
+  if (it != h->pairing.end())
+    for (const auto& st : it->second) *aligned += st.first >= 0 && st.second >= 0;
   return RAFIKI_OK;
 }
 
