@@ -1,6 +1,7 @@
 """bench.py's host-side contract, without a GPU: more than one GPU is refused with a
 message, and the HBM-traffic summary rescales each counter by what it read for the
-calibration copy and averages it over the conv launches that follow the copy."""
+calibration copy and averages it over the conv launches between the two copies that
+bench.py runs around its first traced pass."""
 import csv
 import json
 import os
@@ -36,12 +37,16 @@ def test_more_than_one_gpu_is_refused():
 
 def test_pmc_summary_rescales_by_the_copy(tmp_path):
     conv = "void rafiki::conv_mfma_kernel<128, 128, 2, 2, 3, true, 8, false, false, 0>(rafiki::ConvArgs)"
+    copy = "void at::native::elementwise_kernel<mul>(x)"
+    fill = "void at::native::vectorized_elementwise_kernel<fill>(x)"
     copy_bytes = 1 << 20
-    # warm-up conv launches before the copy are ignored; the copy read half its bytes
-    _write(str(tmp_path / "f"), "FETCH_SIZE", [(conv, 999.0), ("__amd_rocclr_copyBuffer", 512.0),
-                                                (conv, 100.0), ("void rafiki::pool(x)", 7.0), (conv, 300.0)])
-    _write(str(tmp_path / "w"), "WRITE_SIZE", [(conv, 5.0), ("__amd_rocclr_copyBuffer", 1024.0),
-                                                (conv, 40.0), (conv, 60.0)])
+    # the buffer's fill (writes only), timed-step conv launches before the first copy and
+    # the concurrent traced pass after the second are ignored; the copy read half its bytes
+    _write(str(tmp_path / "f"), "FETCH_SIZE", [(conv, 999.0), (fill, 0.5), (conv, 777.0), (copy, 512.0),
+                                                (conv, 100.0), ("void rafiki::pool(x)", 7.0), (conv, 300.0),
+                                                (copy, 512.0), (conv, 5000.0)])
+    _write(str(tmp_path / "w"), "WRITE_SIZE", [(conv, 5.0), (fill, 1024.0), (conv, 77.0), (copy, 1024.0),
+                                                (conv, 40.0), (conv, 60.0), (copy, 1024.0), (conv, 900.0)])
     out = bench.summarize_pmc(str(tmp_path / "f"), str(tmp_path / "w"), copy_bytes)
     assert out["fetch"]["launches"] == 2 and out["write"]["launches"] == 2
     assert abs(out["fetch"]["scale"] - 2.0) < 1e-12 and abs(out["write"]["scale"] - 1.0) < 1e-12
@@ -49,3 +54,15 @@ def test_pmc_summary_rescales_by_the_copy(tmp_path):
     assert abs(out["write"]["bytes_per_launch"] - 50.0 * 1024) < 1e-6
     assert abs(out["traffic_bytes_per_launch"] - (400.0 + 50.0) * 1024) < 1e-6
     assert out["source_sha256"] == bench.kernel_source_sha()
+
+
+def test_pmc_summary_needs_both_marker_copies(tmp_path):
+    conv = "void rafiki::conv_mfma_kernel<128, 128, 2, 2, 3, true, 8, false, false, 0>(rafiki::ConvArgs)"
+    _write(str(tmp_path / "f"), "FETCH_SIZE", [("copy", 512.0), (conv, 100.0)])
+    _write(str(tmp_path / "w"), "WRITE_SIZE", [("copy", 1024.0), (conv, 40.0)])
+    try:
+        bench.summarize_pmc(str(tmp_path / "f"), str(tmp_path / "w"), 1 << 20)
+    except SystemExit as e:
+        assert "marker" in str(e)
+    else:
+        raise AssertionError("a single copy was accepted")
