@@ -402,7 +402,10 @@ def peaks_main(args, dev):
     256 compute units (1, 2 or 4 wavefronts per SIMD), each wavefront 8 independent
     32x32x16 bf16 MFMAs per iteration on register operands.  HBM: one 16-byte streaming
     read pass over 4 GiB (16x the last-level cache), and a device-to-device copy of
-    2 GiB (read + write).  Best of 10 timings after 2 warm-ups, HIP events."""
+    2 GiB (read + write).  Main-loop skeleton: the GEMM kernel's LDS fragment reads and
+    MFMAs for four wave layouts, alone and with each K tile's LDS writes and barrier, one
+    workgroup per compute unit.  Best of 10 (skeleton: 5) timings after 2 warm-ups, HIP
+    events."""
     import torch
 
     from paper_1804_06087_amd.binding import probe_mfma_bf16, probe_hbm_read
@@ -436,6 +439,18 @@ def peaks_main(args, dev):
         emit("register-resident bf16 MFMA loop", flops / (ms / 1e3) / 1e12, "TFLOP/s", PEAK_BF16_TFLOPS,
              {"kernel": "v_mfma_f32_32x32x16_bf16", "workgroups": blocks, "waves_per_simd": per_simd,
               "iterations": iters}, ms)
+    # the GEMM kernel's main loop without memory loads (one workgroup per compute unit)
+    from paper_1804_06087_amd.binding import MAINLOOP_VARIANTS, probe_mainloop
+    ktiles, blocks = 2000, 256
+    out = torch.empty(blocks * 8, dtype=torch.float32, device=dev)
+    for variant, (waves, wtile, tile, mf) in MAINLOOP_VARIANTS.items():
+        for sync in (False, True):
+            ms = best_ms(lambda: probe_mainloop(variant, sync, blocks, ktiles, out), reps=5)
+            flops = blocks * waves * ktiles * 4 * mf * 32768.0
+            emit("GEMM main-loop skeleton (LDS fragment reads + MFMA" + (", tile writes + barrier" if sync else "") + ")",
+                 flops / (ms / 1e3) / 1e12, "TFLOP/s", PEAK_BF16_TFLOPS,
+                 {"kernel": "probe_mainloop", "waves": waves, "wave_tile": wtile, "workgroup_tile": tile,
+                  "k_tiles": ktiles, "workgroups": blocks, "lds_writes_and_barrier_per_k_tile": sync}, ms)
     nbytes = 4 << 30
     x = torch.empty(nbytes, dtype=torch.uint8, device=dev)
     x.fill_(7)

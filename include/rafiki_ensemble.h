@@ -269,6 +269,18 @@ int rafiki_global_avgpool_nhwc_bf16(const void* x, void* y, int n, int h, int w,
 int rafiki_probe_mfma_bf16(int blocks, int iters, float* out, void* stream);
 int rafiki_probe_hbm_read(const void* x, long long bytes, int blocks, unsigned* out, void* stream);
 
+/* Diagnostics: the GEMM kernel's main loop with nothing loaded from memory, to separate
+ * what its LDS fragment reads, LDS writes and barriers cost from what its loads cost.
+ * Each of `blocks` workgroups runs `ktiles` K tiles of 64; per K tile every wavefront
+ * reads its fragments from LDS and issues its 32x32x16 bf16 MFMAs (4 k-steps of
+ * TM x TN MFMAs, 32768 FLOP each).  variant 0: 8 wavefronts of 64x128 outputs
+ * (TM = 2, TN = 4; the 256x256 8-wavefront tile); 1: 4 wavefronts of 128x128 (4, 4);
+ * 2: 4 wavefronts of 64x64 (2, 2); 3: 8 wavefronts of 64x32 (2, 1).  sync != 0: each
+ * K tile also writes the tile's (BM + BN) x 64 bf16 into LDS and passes a workgroup
+ * barrier.  One fp32 checksum per wavefront goes to out[block * 8 + wave] (device,
+ * >= blocks * 8 floats).  Enqueues on `stream` only. */
+int rafiki_probe_mainloop(int variant, int sync, int blocks, int ktiles, float* out, void* stream);
+
 /* Diagnostics: tile configurations of the bf16 GEMM kernel.  Configuration `cfg`
  * (0 .. count - 1) computes output tiles of bm pixels x bn channels with `waves`
  * wavefronts, `stages` K tiles of bk channels in flight.  Every configuration sums each

@@ -28,7 +28,7 @@ EXPORTED = ("rafiki_ensemble_create", "rafiki_ensemble_infer", "rafiki_ensemble_
             "rafiki_ensemble_pairing", "rafiki_ensemble_use_graphs",
             "rafiki_ensemble_graph_stats", "rafiki_combine_mean", "rafiki_combine_vote",
             "rafiki_maxpool_nhwc_bf16", "rafiki_global_avgpool_nhwc_bf16", "rafiki_probe_mfma_bf16",
-            "rafiki_probe_hbm_read",
+            "rafiki_probe_hbm_read", "rafiki_probe_mainloop",
             "rafiki_ensemble_destroy", "rafiki_greedy_decide", "rafiki_greedy_simulate", "rafiki_greedy_simulate_multi",
             "rafiki_ensemble_profile", "rafiki_ensemble_serve_greedy", "rafiki_ensemble_serve_greedy_async",
             "rafiki_ensemble_serve_rl",
@@ -128,6 +128,7 @@ def load_library(path: str = LIB_PATH):
     lib.rafiki_maxpool_nhwc_bf16.argtypes = [C.c_void_p, C.c_void_p] + [C.c_int] * 7 + [C.c_void_p]
     lib.rafiki_probe_mfma_bf16.argtypes = [C.c_int, C.c_int, C.c_void_p, C.c_void_p]
     lib.rafiki_probe_hbm_read.argtypes = [C.c_void_p, C.c_longlong, C.c_int, C.c_void_p, C.c_void_p]
+    lib.rafiki_probe_mainloop.argtypes = [C.c_int, C.c_int, C.c_int, C.c_int, C.c_void_p, C.c_void_p]
     lib.rafiki_global_avgpool_nhwc_bf16.argtypes = [C.c_void_p, C.c_void_p] + [C.c_int] * 4 + [C.c_void_p]
     P = C.POINTER
     lib.rafiki_greedy_decide.argtypes = [P(RafikiGreedyPolicy), C.c_int64, C.c_int64, P(C.c_int32)]
@@ -439,6 +440,19 @@ def probe_hbm_read(x, blocks: int, out, stream=None):
     """One streaming pass of 16-byte loads over the bytes of device tensor x."""
     _check(load_library().rafiki_probe_hbm_read(_ptr(x), x.numel() * x.element_size(), blocks, _ptr(out),
                                                  _stream(stream)))
+
+
+# (waves, wave tile, workgroup tile, TM x TN MFMA blocks per wave) of each main-loop variant
+MAINLOOP_VARIANTS = {0: (8, "64x128", "256x256", 8), 1: (4, "128x128", "256x256", 16),
+                     2: (4, "64x64", "128x128", 4), 3: (8, "64x32", "128x128", 2)}
+
+
+def probe_mainloop(variant: int, sync: bool, blocks: int, ktiles: int, out, stream=None):
+    """The GEMM main loop without memory loads: LDS fragment reads and MFMAs, with
+    (sync) or without each K tile's LDS writes and barrier.  FLOP per launch:
+    blocks x waves x ktiles x 4 x (TM x TN) x 32768."""
+    _check(load_library().rafiki_probe_mainloop(variant, 1 if sync else 0, blocks, ktiles, _ptr(out),
+                                                _stream(stream)))
 
 
 def global_avgpool_nhwc_bf16(x, y, stream=None):

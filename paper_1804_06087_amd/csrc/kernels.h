@@ -262,5 +262,6 @@ hipError_t launch_fused_net(const FusedNetArgs& a, int n, int n_models, hipStrea
 // streaming 16-byte read of words16 words (out [blocks * 4]).
 hipError_t launch_probe_mfma(int blocks, int iters, float* out, hipStream_t s);
 hipError_t launch_probe_read(const void* x, long long words16, int blocks, unsigned* out, hipStream_t s);
+hipError_t launch_probe_mainloop(int variant, bool sync, int blocks, int ktiles, float* out, hipStream_t s);
 
 }  // namespace rafiki

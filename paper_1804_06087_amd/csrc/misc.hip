@@ -800,4 +800,94 @@ hipError_t launch_probe_read(const void* x, long long words16, int blocks, unsig
   return hipGetLastError();
 }
 
+// Main-loop skeleton of the GEMM kernel, nothing loaded from memory: per K tile of 64,
+// four k-steps in which each wave reads its TM + TN fragments from LDS (the conv
+// kernel's conflict-free swizzle; the next step's reads issued ahead of this step's
+// MFMAs) and runs its TM x TN v_mfma_f32_32x32x16_bf16.  With SYNC each K tile also
+// writes the tile's volume, (BM + BN) rows x 64 bf16, into LDS from registers and passes
+// a workgroup barrier, as the refill of a stage does.  Every LDS index stays inside the
+// 80 KB array: fragment rows r < 256 of 8 chunks for each operand, writes to the last
+// 1024 chunks.  The addresses alternate with the tile so that no read is loop-invariant.
+template <int NW, int WM, int TM, int TN, bool SYNC>
+__global__ __launch_bounds__(NW * 64, 1) void probe_mainloop_kernel(int ktiles, float* out) {
+  __shared__ probe_u4 lds[5120];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // bf16 values in [2^-7, 2^-6): sums over any number of tiles here stay finite
+  for (int i = tid; i < 5120; i += NW * 64) {
+    const unsigned u = (unsigned)i;
+    lds[i] = probe_u4{0x3C003C00u | (u & 0x7F) | ((3 * u & 0x7F) << 16), 0x3C003C00u | (5 * u & 0x7F),
+                      0x3C003C00u | ((7 * u & 0x7F) << 16), 0x3C003C00u | (11 * u & 0x7F)};
+  }
+  __syncthreads();
+  probe_f32x16 acc[TN][TM];
+#pragma unroll
+  for (int i = 0; i < TN; ++i)
+#pragma unroll
+    for (int j = 0; j < TM; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+  const int frow = lane & 31, fk = lane >> 5;
+  const int wm = wave % WM, wn = wave / WM;
+  auto frag = [&](int base, int r, int kc) {
+    r &= 255;
+    return __builtin_bit_cast(probe_bf16x8, lds[base + r * 8 + (kc ^ (r & 7) ^ ((r >> 3) & 1))]);
+  };
+  probe_bf16x8 xf[2][TM], wf[2][TN];
+#pragma unroll
+  for (int tm = 0; tm < TM; ++tm) xf[0][tm] = frag(0, wm * 32 * TM + tm * 32 + frow, fk);
+#pragma unroll
+  for (int tn = 0; tn < TN; ++tn) wf[0][tn] = frag(2048, wn * 32 * TN + tn * 32 + frow, fk);
+  for (int kt = 0; kt < ktiles; ++kt) {
+    const int ro = (kt & 1) * 32;
+#pragma unroll
+    for (int st = 0; st < 4; ++st) {
+      const int b = st & 1, nx = 2 * ((st + 1) & 3) + fk;
+#pragma unroll
+      for (int tm = 0; tm < TM; ++tm) xf[b ^ 1][tm] = frag(0, ro + wm * 32 * TM + tm * 32 + frow, nx);
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn) wf[b ^ 1][tn] = frag(2048, ro + wn * 32 * TN + tn * 32 + frow, nx);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn)
+#pragma unroll
+        for (int tm = 0; tm < TM; ++tm)
+          acc[tn][tm] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[b][tn], xf[b][tm], acc[tn][tm], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    if constexpr (SYNC) {
+      constexpr int BM = 32 * TM * WM, BN = 32 * TN * (NW / WM);
+      constexpr int PT = (BM + BN) * 8 / (NW * 64);   // 16-byte chunks per thread
+#pragma unroll
+      for (int i = 0; i < PT; ++i)
+        lds[4096 + ((i * NW * 64 + tid) & 1023)] = probe_u4{(unsigned)kt, (unsigned)i, (unsigned)tid, 1u};
+      __syncthreads();
+    }
+  }
+  float t = 0.f;
+#pragma unroll
+  for (int i = 0; i < TN; ++i)
+#pragma unroll
+    for (int j = 0; j < TM; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) t += acc[i][j][e];
+  if (lane == 0) out[blockIdx.x * 8 + wave] = t;
+}
+
+// Variants: 0 = 8 waves of 64x128 (the 256x256 tile's layout), 1 = 4 waves of 128x128,
+// 2 = 4 waves of 64x64 (128x128 tile), 3 = 8 waves of 64x32 (128x128 tile).
+hipError_t launch_probe_mainloop(int variant, bool sync, int blocks, int ktiles, float* out, hipStream_t s) {
+#define RAFIKI_PROBE_ML(NW, WM, TM, TN)                                                              \
+  if (sync) launch(probe_mainloop_kernel<NW, WM, TM, TN, true>, dim3(blocks), dim3(NW * 64), s, ktiles, out); \
+  else launch(probe_mainloop_kernel<NW, WM, TM, TN, false>, dim3(blocks), dim3(NW * 64), s, ktiles, out);
+  switch (variant) {
+    case 0: RAFIKI_PROBE_ML(8, 4, 2, 4) break;
+    case 1: RAFIKI_PROBE_ML(4, 2, 4, 4) break;
+    case 2: RAFIKI_PROBE_ML(4, 2, 2, 2) break;
+    case 3: RAFIKI_PROBE_ML(8, 2, 2, 1) break;
+    default: return hipErrorInvalidValue;
+  }
+#undef RAFIKI_PROBE_ML
+  return hipGetLastError();
+}
+
 }  // namespace rafiki

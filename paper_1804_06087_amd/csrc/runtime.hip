@@ -2310,6 +2310,15 @@ int rafiki_probe_hbm_read(const void* x, long long bytes, int blocks, unsigned* 
   return RAFIKI_OK;
 }
 
+int rafiki_probe_mainloop(int variant, int sync, int blocks, int ktiles, float* out, void* stream) {
+  if (!out) return fail(RAFIKI_ERR_INVALID, "null pointer");
+  if (variant < 0 || variant > 3) return fail(RAFIKI_ERR_INVALID, "variant must be 0..3");
+  if (blocks < 1 || ktiles < 1) return fail(RAFIKI_ERR_INVALID, "blocks and ktiles must be positive");
+  const hipError_t st = launch_probe_mainloop(variant, sync != 0, blocks, ktiles, out, (hipStream_t)stream);
+  if (st != hipSuccess) return fail(RAFIKI_ERR_HIP, std::string("probe launch: ") + hipGetErrorString(st));
+  return RAFIKI_OK;
+}
+
 int rafiki_tile_config(int cfg, int* bm, int* bn, int* waves, int* stages, int* bk) {
   if (cfg < 0 || cfg >= kNumMfmaConfigs) return fail(RAFIKI_ERR_INVALID, "no such tile configuration");
   const MfmaConfig& c = kMfmaConfigs[cfg];

@@ -125,3 +125,26 @@ def test_standalone_argument_errors():
         maxpool_nhwc_bf16(x, y, 2, 2, 0)                 # output buffer of the wrong shape
     with pytest.raises(ValueError):
         combine_mean(z[:3], p.to(torch.float64), lab)    # output of the wrong dtype
+
+
+def test_mainloop_probe_checksums_and_arguments():
+    """The main-loop probe (a diagnostic, not part of the path): its per-K-tile LDS writes
+    go to chunks that no fragment read touches, so each wave's checksum is the same with
+    and without them; every wave of every workgroup writes a finite checksum."""
+    from paper_1804_06087_amd.binding import MAINLOOP_VARIANTS, probe_mainloop
+    blocks = 300
+    for v, (waves, *_rest) in MAINLOOP_VARIANTS.items():
+        res = []
+        for sync in (False, True):
+            out = torch.full((blocks * 8,), float("nan"), dtype=torch.float32, device=DEV)
+            probe_mainloop(v, sync, blocks, 5, out)
+            torch.cuda.synchronize()
+            o = out.view(blocks, 8)[:, :waves].cpu()
+            assert torch.isfinite(o).all(), (v, sync)
+            res.append(o)
+        assert torch.equal(res[0], res[1]), v
+    out = torch.empty((8,), dtype=torch.float32, device=DEV)
+    for bad in ((4, False, 1, 1), (0, False, 0, 1), (0, True, 1, 0)):
+        with pytest.raises(RafikiError) as e:
+            probe_mainloop(*bad, out)
+        assert e.value.code == RAFIKI_ERR_INVALID
