@@ -275,6 +275,7 @@ constexpr int kCoPadBf16 = 256;
 
 // Configurations whose channel tile suits c_out (at most one partly used tile row).
 bool cfg_fits(int cfg, int c_out) {
+  if (cfg < 0 || cfg >= kNumMfmaConfigs) return false;
   const int bn = kMfmaConfigs[cfg].bn;
   if (c_out <= 32) return bn == 32;
   if (c_out <= 64) return bn <= 64;
@@ -1162,6 +1163,7 @@ int run_gemm(const rafiki_ensemble_s* e, const Op& op, ConvArgs a, hipStream_t s
     a.kt_per_split = (cb + sp - 1) / sp;
     splits = (cb + a.kt_per_split - 1) / a.kt_per_split;
   }
+  if (cfg == kCfgDirect3x3 && (splits > 1 || !conv3x3_direct_fits(a))) cfg = -1;   // e.g. a grouped launch
   if (cfg < 0) cfg = splits > 1 ? split_cfg(op.c_out) : default_cfg(op.c_out);
   struct TileScope {
     TileScope(int c, int sp) { trace_tile() = {c, sp}; }
@@ -1182,10 +1184,22 @@ int run_gemm(const rafiki_ensemble_s* e, const Op& op, ConvArgs a, hipStream_t s
     TRACED(e, s, RAFIKI_K_SPLITK_REDUCE, mi, li, 0.0,
            nm * ((double)splits * a.M * a.c_write * 4.0 + out_rows * a.c_write * (a.out_f32 ? 4.0 : es)),
            launch_splitk_reduce(a, splits, 1, s));
+  } else if (cfg == kCfgDirect3x3) {
+    TRACED(e, s, RAFIKI_K_CONV_MFMA, mi, li, flops, bytes, launch_conv3x3_direct(a, s));
   } else {
     TRACED(e, s, RAFIKI_K_CONV_MFMA, mi, li, flops, bytes, launch_conv_mfma(a, cfg, 1, s));
   }
   return RAFIKI_OK;
+}
+
+// Whether op (of model M) is one the direct 3x3 kernel takes when launched alone: the
+// op-level form of conv3x3_direct_fits for the tuner's candidate list.
+bool direct3x3_op_fits(const rafiki_ensemble_s* e, const Model& M, const Op& op) {
+  if (e->precision != RAFIKI_BF16 || op.kind != O_CONV || op.nseg > 0 || op.table || op.in2 >= 0) return false;
+  const Tensor& y = M.tensors[op.out];
+  return op.kh == 3 && op.kw == 3 && op.stride == 1 && op.pad == 1 && op.Cs_in == 64 && op.K == 576 &&
+         op.Kp == 576 && op.c_out == 64 && op.Ho == op.H && op.Wo == op.W && !y.is_logits && y.Cs == 64 &&
+         op.tap_stride == 0 && (!op.pool2 || (op.H % 2 == 0 && op.W % 2 == 0));
 }
 
 // Kernel arguments of a GEMM-like op over n requests (output pointer set by the caller).
@@ -1252,6 +1266,7 @@ int tune(rafiki_ensemble_s* e, int n, const void* in, hipStream_t s) {
       if (!timing) continue;
       for (int cfg = 0; cfg < kNumMfmaConfigs; ++cfg)
         if (cfg_fits(cfg, op.c_out) && kMfmaConfigs[cfg].bm <= 2 * round_up(M_rows, 32)) cand[mi][oi].push_back(cfg);
+      if (splits == 1 && direct3x3_op_fits(e, M, op)) cand[mi][oi].push_back(kCfgDirect3x3);
     }
   }
   if (!timing) {
@@ -1270,7 +1285,7 @@ int tune(rafiki_ensemble_s* e, int n, const void* in, hipStream_t s) {
   e->trace.on = false;
   for (size_t mi = 0; mi < NM && rc == RAFIKI_OK; ++mi) {
     const Model& M = e->models[mi];
-    best[mi].assign(M.ops.size(), std::vector<float>(kNumMfmaConfigs, 1e30f));
+    best[mi].assign(M.ops.size(), std::vector<float>(kNumMfmaConfigs + 1, 1e30f));
     std::vector<int> out_to_op(M.tensors.size(), -1);
     size_t J = 0;
     for (size_t oi = 0; oi < M.ops.size(); ++oi) {
@@ -1299,7 +1314,7 @@ int tune(rafiki_ensemble_s* e, int n, const void* in, hipStream_t s) {
             break;
           }
           const int oi = r.layer >= 0 && r.layer < (int)out_to_op.size() ? out_to_op[r.layer] : -1;
-          if (oi >= 0 && r.cfg >= 0 && r.cfg < kNumMfmaConfigs)
+          if (oi >= 0 && r.cfg >= 0 && r.cfg <= kCfgDirect3x3)
             best[mi][oi][r.cfg] = std::min(best[mi][oi][r.cfg], ms);
         }
       }
@@ -1371,7 +1386,11 @@ int run_op(const rafiki_ensemble_s* e, const int* mis, const int* ois, int nm, c
       case O_CONV1D: {
         ConvArgs a = gemm_args(e, M, op, n, in);
         int cfg = cfgs.empty() ? -1 : cfgs[oi];
-        if (e->force_tile >= 0 && cfg_fits(e->force_tile, op.c_out)) cfg = e->force_tile;
+        if (e->force_tile == kCfgDirect3x3) {
+          if (direct3x3_op_fits(e, M, op)) cfg = kCfgDirect3x3;
+        } else if (e->force_tile >= 0 && cfg_fits(e->force_tile, op.c_out)) {
+          cfg = e->force_tile;
+        }
         if (nm > 1) {
           a.n_members = nm;
           for (int k = 0; k < nm; ++k) {
@@ -2332,7 +2351,8 @@ int rafiki_tile_config(int cfg, int* bm, int* bn, int* waves, int* stages, int* 
 
 int rafiki_ensemble_force_tile(rafiki_ensemble_t h, int cfg) {
   if (!h) return fail(RAFIKI_ERR_INVALID, "null handle");
-  if (cfg < -1 || cfg >= kNumMfmaConfigs) return fail(RAFIKI_ERR_INVALID, "no such tile configuration");
+  if (cfg == RAFIKI_TILE_DIRECT3X3) cfg = kCfgDirect3x3;
+  else if (cfg < -1 || cfg >= kNumMfmaConfigs) return fail(RAFIKI_ERR_INVALID, "no such tile configuration");
   if (cfg != h->force_tile) {
     HIPCHK(hipDeviceSynchronize());   // graphs holding the old tiles may still be running
     h->drop_graphs();

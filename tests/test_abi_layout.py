@@ -47,3 +47,22 @@ def test_ctypes_layout_matches_headers(tmp_path):
         assert got[(cname, "size")] == C.sizeof(py), cname
         for fname, _ in py._fields_:
             assert got[(cname, fname)] == getattr(py, fname).offset, f"{cname}.{fname}"
+
+
+@pytest.mark.skipif(shutil.which("gcc") is None, reason="needs gcc")
+def test_binding_constants_match_headers(tmp_path):
+    """Status codes, precisions and the direct-kernel tile id as the header defines them."""
+    names = ["RAFIKI_OK", "RAFIKI_ERR_INVALID", "RAFIKI_ERR_UNSUPPORTED", "RAFIKI_ERR_NOMEM", "RAFIKI_ERR_HIP",
+             "RAFIKI_FP32", "RAFIKI_BF16", "RAFIKI_TILE_DIRECT3X3"]
+    lines = ['#include <stdio.h>', '#include "rafiki_ensemble.h"', "int main(void) {"]
+    lines += [f'  printf("{nm} %d\\n", (int)({nm}));' for nm in names]
+    lines += ["  return 0;", "}"]
+    src = tmp_path / "consts.c"
+    src.write_text("\n".join(lines) + "\n")
+    exe = tmp_path / "consts"
+    subprocess.run(["gcc", "-std=c99", "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)],
+                   check=True, capture_output=True)
+    out = subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout.split("\n")
+    got = dict((ln.split()[0], int(ln.split()[1])) for ln in out if ln)
+    for nm in names:
+        assert got[nm] == getattr(bd, nm), nm
