@@ -87,12 +87,17 @@ def parse():
     return ap.parse_args()
 
 
-CONV_SOURCE = os.path.join(ROOT, "paper_1804_06087_amd", "csrc", "conv_mfma.hip")
+# the bf16 conv launches (trace class conv_mfma): the GEMM kernel and the direct 3x3 kernel
+CONV_SOURCES = [os.path.join(ROOT, "paper_1804_06087_amd", "csrc", f) for f in ("conv_mfma.hip", "conv3x3_direct.hip")]
+CONV_KERNEL_NAMES = ("conv_mfma_kernel", "conv3x3_direct_kernel")
 
 
 def kernel_source_sha() -> str:
     import hashlib
-    return hashlib.sha256(open(CONV_SOURCE, "rb").read()).hexdigest()
+    h = hashlib.sha256()
+    for f in CONV_SOURCES:
+        h.update(open(f, "rb").read())
+    return h.hexdigest()
 
 
 def _pmc_rows(d, counter):
@@ -128,7 +133,7 @@ def summarize_pmc(fetch_dir, write_dir, copy_bytes):
         a, b = marks[-2], marks[-1]
         c = b
         scale = copy_bytes / rows[c][1] if rows[c][1] > 0 else float("nan")
-        conv = [v for k, v in rows[a + 1:b] if "conv_mfma_kernel" in k]
+        conv = [v for k, v in rows[a + 1:b] if any(nm in k for nm in CONV_KERNEL_NAMES)]
         out[name] = {"scale": scale, "launches": len(conv), "bytes_per_launch": scale * sum(conv) / max(len(conv), 1),
                      "copy_counter_bytes": rows[c][1]}
     return {"kernel": "conv_mfma", "source_sha256": kernel_source_sha(), "copy_bytes": copy_bytes,
@@ -611,6 +616,8 @@ def layers_main(args, dev):
         a["ms"] += r["ms"] / T
     tot_ms = sum(a["ms"] for a in agg.values())
     tot_bound = 0.0
+    from paper_1804_06087_amd.binding import tile_configs
+    n_gemm_cfgs = len(tile_configs())   # the trace's tile id of the direct 3x3 kernel
     print(f"# Per-launch roofline: {cfg.name}, batch {n}, mask {mask:#b}\n")
     print(f"Command: `python bench.py --layers --workload {args.workload}"
           + (f" --n {args.n}" if args.n else "") + (f" --mask {args.mask}" if args.mask else "") + "`\n")
@@ -631,7 +638,7 @@ def layers_main(args, dev):
             desc = f"{OP_NAMES[L.op]} {L.c_in}->{L.c_out} {L.kh}x{L.kw}/{L.stride}"
             if OP_NAMES[L.op] == "concat" and kind != "concat":   # branches fused into one GEMM + max
                 desc = f"conv1d_maxtime branches -> concat {L.c_out}"
-        tile = f"{a['cfg']} / {a['splits']}" if a["cfg"] >= 0 else ""
+        tile = ("direct 3x3" if a["cfg"] == n_gemm_cfgs else f"{a['cfg']} / {a['splits']}") if a["cfg"] >= 0 else ""
         print(f"| {specs[m].name if m >= 0 else '-'} | {li} | {desc} | {kind} | {tile} | {a['ms'] * 1e3:.1f} | "
               f"{a['flops'] / a['ms'] / 1e9:.0f} | {a['bytes'] / a['ms'] / 1e6:.0f} | {bound} | {tb * 1e3:.1f} | "
               f"{tb / a['ms']:.2f} |")

@@ -66,3 +66,17 @@ def test_pmc_summary_needs_both_marker_copies(tmp_path):
         assert "marker" in str(e)
     else:
         raise AssertionError("a single copy was accepted")
+
+
+def test_pmc_summary_counts_both_conv_kernels(tmp_path):
+    """The traced class conv_mfma holds the GEMM and the direct 3x3 launches; the
+    counter summary averages over both."""
+    gemm = "void rafiki::conv_mfma_kernel<128, 128, 2, 2, 3, true, 8, false, false, 0>(rafiki::ConvArgs)"
+    direct = "rafiki::conv3x3_direct_kernel(rafiki::ConvArgs)"
+    copy = "void at::native::elementwise_kernel<mul>(x)"
+    _write(str(tmp_path / "f"), "FETCH_SIZE", [(copy, 512.0), (gemm, 100.0), (direct, 300.0), (copy, 512.0)])
+    _write(str(tmp_path / "w"), "WRITE_SIZE", [(copy, 1024.0), (gemm, 10.0), (direct, 30.0), (copy, 1024.0)])
+    out = bench.summarize_pmc(str(tmp_path / "f"), str(tmp_path / "w"), 1 << 20)
+    assert out["fetch"]["launches"] == 2 and out["write"]["launches"] == 2
+    assert abs(out["fetch"]["bytes_per_launch"] - 2.0 * 200.0 * 1024) < 1e-6
+    assert abs(out["write"]["bytes_per_launch"] - 20.0 * 1024) < 1e-6
