@@ -18,6 +18,9 @@
 // holding k-range 8 * (l / 32) .. +8 of row l % 32; then fma(acc, scale, shift), the
 // fp32 max over each 2x2 window when pooling, integer-max ReLU and one rounding to
 // bf16.  The outputs are therefore bitwise those of the GEMM kernel, whatever its tile.
+#include <algorithm>
+#include <atomic>
+
 #include "kernels.h"
 
 namespace rafiki {
@@ -235,19 +238,21 @@ bool conv3x3_direct_fits(const ConvArgs& a) {
 
 hipError_t launch_conv3x3_direct(const ConvArgs& a, hipStream_t s) {
   if (!conv3x3_direct_fits(a)) return hipErrorInvalidValue;
-  static int cus[64] = {};
+  // compute units per device, queried once (concurrent first calls store the same value)
+  static std::atomic<int> cus[64];
   int dev = 0;
   hipError_t st = hipGetDevice(&dev);
   if (st != hipSuccess) return st;
   if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
-  if (cus[dev] <= 0) {
-    int c = 0;
-    st = hipDeviceGetAttribute(&c, hipDeviceAttributeMultiprocessorCount, dev);
+  int n_cu = cus[dev].load(std::memory_order_relaxed);
+  if (n_cu <= 0) {
+    st = hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev);
     if (st != hipSuccess) return st;
-    cus[dev] = c > 0 ? c : 1;
+    n_cu = n_cu > 0 ? n_cu : 1;
+    cus[dev].store(n_cu, std::memory_order_relaxed);
   }
   const long long tiles = (long long)a.N * ((a.H + kTile - 1) / kTile) * ((a.W + kTile - 1) / kTile);
-  const int grid = (int)std::min<long long>(tiles, cus[dev]);
+  const int grid = (int)std::min<long long>(tiles, n_cu);
   launch(conv3x3_direct_kernel, dim3(grid), dim3(256), s, a);
   return hipGetLastError();
 }
