@@ -1,23 +1,24 @@
-// Direct 3x3 convolution (stride 1, zero padding 1) of bf16 NHWC layers with 64 input
-// and 64 output channels on gfx950 matrix cores, optionally with the 2x2 stride-2
-// max-pool fused (the conv layers of a network's full-resolution stage: VGG-16's
-// conv1_2, the 56x56 3x3 layers of ResNet-50/101; Section 5.1, each model's forward
-// pass over the batch).
+// Direct convolution of bf16 NHWC layers with 64 output channels on gfx950 matrix
+// cores, for the layers where the implicit GEMM is bound by its loads (Section 5.1,
+// each model's forward pass over the batch):
+//   - 3x3, stride 1, 64 input channels (VGG-16's conv1_2 with its fused 2x2 max-pool, the
+//     56x56 3x3 layers of ResNet-50/101): the GEMM brings every input pixel into LDS nine
+//     times, once per tap, and with 64 output channels each 16-byte chunk it loads feeds
+//     just two MFMAs;
+//   - 3x3, stride 1, and 7x7, stride 2, on the 8 storage channels of an RGB image (VGG-16's
+//     conv1_1, the ResNet stems): 9 or 49 taps re-read each pixel as often.
+// A persistent workgroup (one or two per compute unit) keeps the layer's weights in LDS
+// for its whole life, and two input patches (a 16 x 16 output tile plus its halo): the
+// taps read the patch in place, and the next tile's patch loads while the current one is
+// computed.
 //
-// Why a kernel of its own: the implicit GEMM brings every input pixel into LDS nine
-// times, once per tap, and with only 64 output channels each 16-byte chunk it loads
-// feeds just two MFMAs, so these layers are bound by the L2 -> LDS load path.  Here a
-// persistent workgroup (one per compute unit) keeps the layer's weights (64 x 576 bf16,
-// 72 KB) in LDS for its whole life, and two input patches of 18 x 18 pixels (a 16 x 16
-// output tile plus the halo): the nine taps read the patch in place, and the next
-// patch loads while the current one is computed.
-//
-// The sums are formed exactly as conv_mfma_kernel forms them for this layer: K in the
-// packed order (tap u * 3 + v, then channel), 36 k-steps of v_mfma_f32_32x32x16_bf16
-// in increasing K with the weights as A operand and the pixels as B operand, lane l
-// holding k-range 8 * (l / 32) .. +8 of row l % 32; then fma(acc, scale, shift), the
-// fp32 max over each 2x2 window when pooling, integer-max ReLU and one rounding to
-// bf16.  The outputs are therefore bitwise those of the GEMM kernel, whatever its tile.
+// The sums are formed exactly as conv_mfma_kernel forms them for these layers: K in the
+// packed order (tap u * kw + v, then channel), k-steps of v_mfma_f32_32x32x16_bf16 in
+// increasing K with the weights as A operand and the pixels as B operand, lane l holding
+// k-range 8 * (l / 32) .. +8 of row l % 32 (with 8 channels, k-step s covers taps 2s and
+// 2s + 1; a tap past the last is zero on both sides); then fma(acc, scale, shift), the
+// fp32 max over each 2x2 window when pooling, integer-max ReLU and one rounding to bf16.
+// The outputs are therefore bitwise those of the GEMM kernel, whatever its tile.
 #include <algorithm>
 #include <atomic>
 
@@ -32,19 +33,35 @@ typedef __attribute__((address_space(3))) void d3_lds_void;
 typedef __bf16 d3_bf16x2 __attribute__((ext_vector_type(2)));
 typedef float d3_f32x2 __attribute__((ext_vector_type(2)));
 
-constexpr int kTile = 16;                     // output tile: 16 x 16 pixels
-constexpr int kPatch = kTile + 2;             // input patch side with the halo
-constexpr int kPatchPix = kPatch * kPatch;    // 324
-constexpr int kPatchLoads = (kPatchPix + 7) / 8;   // one load instruction moves 8 pixels
-constexpr int kPatchChunks = kPatchLoads * 64;     // 16-byte chunks per patch buffer (328 pixels)
-constexpr int kWChunks = 9 * 64 * 8;               // weights: [tap][channel][8 chunks]
-constexpr int kLdsChunks = kWChunks + 2 * kPatchChunks;
-constexpr int kDepth = 3;   // k-steps of fragment reads in flight ahead of the MFMAs
-static_assert(kLdsChunks * 16 <= 160 * 1024, "LDS budget");
+constexpr int kTile = 16;    // output tile: 16 x 16 pixels
+constexpr int kDepth = 3;    // k-steps of fragment reads in flight ahead of the MFMAs
+
+// Geometry of one instance: CS storage input channels (64 or 8), KS x KS taps, stride ST.
+template <int CS, int KS, int ST>
+struct DGeo {
+  static constexpr int CC = CS / 8;                         // 16-byte chunks per pixel
+  static constexpr int PAD = KS / 2;
+  static constexpr int PS = (kTile - 1) * ST + KS;          // patch side
+  static constexpr int PPIX = PS * PS;
+  static constexpr int PIX_PER_LOAD = 64 / CC;              // one load instruction: 64 chunks
+  static constexpr int PLOADS = (PPIX + PIX_PER_LOAD - 1) / PIX_PER_LOAD;
+  static constexpr int PCHUNKS = PLOADS * 64;               // per patch buffer
+  static constexpr int TAPS = KS * KS;
+  static constexpr int NK = (TAPS * CS + 15) / 16;          // k-steps of 16
+  static constexpr int WTAPS = CS == 64 ? TAPS : 2 * NK;    // weight rows per channel (8 channels: even)
+  static constexpr int WCHUNKS = WTAPS * 64 * CC;           // weights: [tap][channel][CC chunks]
+  static constexpr int ZERO = WCHUNKS + 2 * PCHUNKS;        // one zero chunk (taps past the last)
+  // 8 channels: each wave's 64 output pixels x 8 chunks, staged for whole-pixel stores
+  static constexpr int STG = ZERO + 1;
+  static constexpr int LDS_CHUNKS = STG + (CS == 8 ? 4 * 64 * 8 : 0);
+  static_assert(CS == 64 || CS == 8, "64 or 8 input channels");
+  static_assert(LDS_CHUNKS * 16 <= 160 * 1024, "LDS budget");
+};
 
 // Row r keeps logical 16-byte chunk q in slot q ^ swz(r): over any 16 consecutive rows
 // (r % 2, slot) is distinct, so a ds_read_b128 of one chunk from 16 consecutive rows is
-// bank-conflict free.  Patch pixels are rows here, as are weight rows (channels).
+// bank-conflict free.  Patch pixels are rows here, as are weight rows (channels).  With
+// one chunk per row (8 channels) rows are 16 bytes apart and need no swizzle.
 __device__ __forceinline__ int d3_swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
 
 __device__ __forceinline__ uint32_t d3_pack2(float a, float b) {   // nearest even, a low
@@ -68,38 +85,55 @@ __device__ __forceinline__ TileGeo tile_geo(int t, int per_img, int tw) {
 
 }  // namespace
 
-__global__ __launch_bounds__(256, 1) void conv3x3_direct_kernel(ConvArgs a) {
-  __shared__ uint4 lds[kLdsChunks];
+template <int CS, int KS, int ST, int OCC>
+__global__ __launch_bounds__(256, OCC) void conv_direct_kernel(ConvArgs a) {
+  using D = DGeo<CS, KS, ST>;
+  __shared__ uint4 lds[D::LDS_CHUNKS];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc((void*)a.x, (short)0, a.x_bytes, 0x00020000);
   const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc((void*)a.w, (short)0, a.w_bytes, 0x00020000);
   const unsigned oob = (unsigned)a.x_bytes;   // offset at num_records: the hardware returns zeros
-  const int tw = (a.W + kTile - 1) / kTile, per_img = ((a.H + kTile - 1) / kTile) * tw;
+  const int tw = (a.Wo + kTile - 1) / kTile, per_img = ((a.Ho + kTile - 1) / kTile) * tw;
   const int ntiles = a.N * per_img;
   const int G = gridDim.x;
 
-  // Weights, once: load i moves tap i / 8, channels 8 * (i % 8) .. +8 (all 8 chunks);
-  // lane l carries chunk (l % 8) ^ swz(channel) into slot l % 8 of row (tap, channel).
-  for (int i = wave; i < 72; i += 4) {
-    const int t = i >> 3, co = (i & 7) * 8 + (lane >> 3);
-    const int q = (lane & 7) ^ d3_swz(co);
-    const unsigned off = (unsigned)((co * a.Kp + t * 64 + q * 8) * 2);
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(wr, (d3_lds_void*)(lds + i * 64), 16, off, 0, 0, 0);
+  // Weights, once.  64 channels: load i moves tap i / 8, channels 8 * (i % 8) .. +8 (all
+  // 8 chunks), lane l carrying chunk (l % 8) ^ swz(channel) into slot l % 8 of row (tap,
+  // channel).  8 channels: load i moves tap i of the 64 channels, one chunk each (the
+  // padded taps read the packed array's zeros).
+  if constexpr (CS == 64) {
+    for (int i = wave; i < D::TAPS * 8; i += 4) {
+      const int t = i >> 3, co = (i & 7) * 8 + (lane >> 3);
+      const int q = (lane & 7) ^ d3_swz(co);
+      const unsigned off = (unsigned)((co * a.Kp + t * 64 + q * 8) * 2);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(wr, (d3_lds_void*)(lds + i * 64), 16, off, 0, 0, 0);
+    }
+  } else {
+    for (int i = wave; i < D::WTAPS; i += 4) {
+      const unsigned off = (unsigned)((lane * a.Kp + i * 8) * 2);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(wr, (d3_lds_void*)(lds + i * 64), 16, off, 0, 0, 0);
+    }
   }
-  // Patch of tile t into buffer b: load i moves patch pixels 8i .. 8i + 7 (pixel p is
-  // input row oh0 - 1 + p / 18, column ow0 - 1 + p % 18); pixels outside the image, and
-  // the 4 past the patch, read zeros.
+  if (tid == 0) lds[D::ZERO] = make_uint4(0u, 0u, 0u, 0u);
+  // Patch of tile t into buffer b: patch pixel p is input row oh0 * ST - PAD + p / PS,
+  // column ow0 * ST - PAD + p % PS; pixels outside the image, and those past the patch,
+  // read zeros.
   auto load_patch = [&](int t, int b) {
     const TileGeo g = tile_geo(t, per_img, tw);
-    uint4* base = lds + kWChunks + b * kPatchChunks;
-    for (int i = wave; i < kPatchLoads; i += 4) {
-      const int p = i * 8 + (lane >> 3);
-      const int ph = p / kPatch, pw = p - ph * kPatch;
-      const int hi = g.oh0 - 1 + ph, wi = g.ow0 - 1 + pw;
-      const int q = (lane & 7) ^ d3_swz(p);
-      const bool ok = p < kPatchPix && (unsigned)hi < (unsigned)a.H && (unsigned)wi < (unsigned)a.W;
-      const unsigned off = ok ? (unsigned)((((g.n * a.H + hi) * a.W + wi) * 64 + q * 8) * 2) : oob;
+    uint4* base = lds + D::WCHUNKS + b * D::PCHUNKS;
+    for (int i = wave; i < D::PLOADS; i += 4) {
+      const int p = i * D::PIX_PER_LOAD + lane / D::CC;
+      const int ph = p / D::PS, pw = p - ph * D::PS;
+      const int hi = g.oh0 * ST - D::PAD + ph, wi = g.ow0 * ST - D::PAD + pw;
+      const bool ok = p < D::PPIX && (unsigned)hi < (unsigned)a.H && (unsigned)wi < (unsigned)a.W;
+      unsigned off;
+      if constexpr (CS == 64) {
+        const int q = (lane & 7) ^ d3_swz(p);
+        off = ok ? (unsigned)((((g.n * a.H + hi) * a.W + wi) * 64 + q * 8) * 2) : oob;
+      } else {
+        off = ok ? (unsigned)(((g.n * a.H + hi) * a.W + wi) * 16) : oob;
+      }
       __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (d3_lds_void*)(base + i * 64), 16, off, 0, 0, 0);
     }
   };
@@ -111,9 +145,9 @@ __global__ __launch_bounds__(256, 1) void conv3x3_direct_kernel(ConvArgs a) {
   // window sit in four adjacent lanes (a DPP quad).  Which pixel a column holds does
   // not change its sum.
   const int prow = (frow >> 1) & 1, pcol = 2 * (frow >> 2) + (frow & 1);
-  int pix0[2];   // patch pixel of this lane's output in block tm under tap (0, 0)
+  int pix0[2];   // patch pixel under tap (0, 0) of this lane's output in block tm
 #pragma unroll
-  for (int tm = 0; tm < 2; ++tm) pix0[tm] = (4 * wave + 2 * tm + prow) * kPatch + pcol;
+  for (int tm = 0; tm < 2; ++tm) pix0[tm] = (4 * wave + 2 * tm + prow) * ST * D::PS + pcol * ST;
   // scale and shift of this lane's output channels tn * 32 + 8q + 4fk + j, kept in
   // registers for the workgroup's life
   float4 sc[2][4], sh[2][4];
@@ -132,7 +166,7 @@ __global__ __launch_bounds__(256, 1) void conv3x3_direct_kernel(ConvArgs a) {
   for (int it = 0; t < ntiles; ++it, t += G) {
     const int b = it & 1;
     if (t + G < ntiles) load_patch(t + G, b ^ 1);
-    const uint4* P = lds + kWChunks + b * kPatchChunks;
+    const int pbase = D::WCHUNKS + b * D::PCHUNKS;   // the patch being computed
 
     d3_f32x16 acc[2][2];
 #pragma unroll
@@ -142,30 +176,44 @@ __global__ __launch_bounds__(256, 1) void conv3x3_direct_kernel(ConvArgs a) {
 #pragma unroll
         for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
     // Fragments run kDepth k-steps ahead of the MFMAs (ring of kDepth + 1 register
-    // sets): with one wave per SIMD nothing else hides the LDS latency, which under the
-    // four waves' reads is about three k-steps of MFMAs.
+    // sets): with one wave per SIMD nothing else hides the LDS latency.
     d3_bf16x8 xf[kDepth + 1][2], wf[kDepth + 1][2];
-    // fragments of k-step ks (tap ks / 4, channels 16 * (ks % 4) .. +16) into set s
+    // fragments of k-step ks into set s
     auto rd = [&](int ks, int s) {
-      const int tap = ks >> 2, u = tap / 3, v = tap - 3 * u;
-      const int q = 2 * (ks & 3) + fk;
+      if constexpr (CS == 64) {   // tap ks / 4, channels 16 * (ks % 4) .. +16
+        const int tap = ks >> 2, u = tap / KS, v = tap - KS * u;
+        const int q = 2 * (ks & 3) + fk;
 #pragma unroll
-      for (int tm = 0; tm < 2; ++tm) {
-        const int p = pix0[tm] + u * kPatch + v;
-        xf[s][tm] = __builtin_bit_cast(d3_bf16x8, P[p * 8 + (q ^ d3_swz(p))]);
-      }
+        for (int tm = 0; tm < 2; ++tm) {
+          const int p = pix0[tm] + u * D::PS + v;
+          xf[s][tm] = __builtin_bit_cast(d3_bf16x8, lds[pbase + p * 8 + (q ^ d3_swz(p))]);
+        }
 #pragma unroll
-      for (int tn = 0; tn < 2; ++tn) {
-        const int co = tn * 32 + frow;
-        wf[s][tn] = __builtin_bit_cast(d3_bf16x8, lds[(tap * 64 + co) * 8 + (q ^ d3_swz(co))]);
+        for (int tn = 0; tn < 2; ++tn) {
+          const int co = tn * 32 + frow;
+          wf[s][tn] = __builtin_bit_cast(d3_bf16x8, lds[(tap * 64 + co) * 8 + (q ^ d3_swz(co))]);
+        }
+      } else {   // taps 2 ks (lanes fk = 0) and 2 ks + 1 (fk = 1), 8 channels each
+        const int t0 = 2 * ks, t1 = 2 * ks + 1;
+        const int o0 = (t0 / KS) * D::PS + t0 % KS, o1 = (t1 / KS) * D::PS + t1 % KS;
+        const bool real = fk ? t1 < D::TAPS : t0 < D::TAPS;
+        const int off = fk ? o1 : o0;
+#pragma unroll
+        for (int tm = 0; tm < 2; ++tm) {
+          const int idx = real ? pbase + pix0[tm] + off : D::ZERO;
+          xf[s][tm] = __builtin_bit_cast(d3_bf16x8, lds[idx]);
+        }
+#pragma unroll
+        for (int tn = 0; tn < 2; ++tn)
+          wf[s][tn] = __builtin_bit_cast(d3_bf16x8, lds[(2 * ks + fk) * 64 + tn * 32 + frow]);
       }
     };
 #pragma unroll
     for (int ks = 0; ks < kDepth; ++ks) rd(ks, ks);
 #pragma unroll
-    for (int ks = 0; ks < 36; ++ks) {
+    for (int ks = 0; ks < D::NK; ++ks) {
       const int s = ks % (kDepth + 1);
-      if (ks + kDepth < 36) rd(ks + kDepth, (ks + kDepth) % (kDepth + 1));
+      if (ks + kDepth < D::NK) rd(ks + kDepth, (ks + kDepth) % (kDepth + 1));
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int tn = 0; tn < 2; ++tn)
@@ -174,70 +222,108 @@ __global__ __launch_bounds__(256, 1) void conv3x3_direct_kernel(ConvArgs a) {
           acc[tn][tm] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[s][tn], xf[s][tm], acc[tn][tm], 0, 0, 0);
       __builtin_amdgcn_sched_barrier(0);
     }
-    // This wave's loads of the next patch have landed, and every wave is done with P:
-    // the next iteration may compute from the other buffer and refill this one.
+    // This wave's loads of the next patch have landed, and every wave is done with this
+    // patch: the next iteration may compute from the other buffer and refill this one.
     d3_wait_vmcnt<0>();
     __syncthreads();
 
     // Epilogue from the accumulators: lane (frow, fk) holds, for block (tn, tm),
-    // channels tn * 32 + 8g + 4fk + j (g, j in 0..3) of its pixel.
+    // channels tn * 32 + 8q + 4fk + j (q, j in 0..3) of its pixel.
     const TileGeo g = tile_geo(t, per_img, tw);
+    if (CS == 64 && a.pool2) {
+      // Fused 2x2 max-pool: the max over each window's quad of lanes (DPP quad_perm
+      // [1,0,3,2], then [2,3,0,1]); the quad's first lane stores the pooled pixel's 16
+      // channels as 8-byte pieces (a quarter of the pixels: staging them for whole-pixel
+      // stores cost more in synchronisation than it saved).
 #pragma unroll
-    for (int tn = 0; tn < 2; ++tn) {
+      for (int tn = 0; tn < 2; ++tn)
 #pragma unroll
-      for (int tm = 0; tm < 2; ++tm) {
-        const int oh = g.oh0 + 4 * wave + 2 * tm + prow, ow = g.ow0 + pcol;
-        float v[16];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          v[4 * q + 0] = __builtin_fmaf(acc[tn][tm][4 * q + 0], sc[tn][q].x, sh[tn][q].x);
-          v[4 * q + 1] = __builtin_fmaf(acc[tn][tm][4 * q + 1], sc[tn][q].y, sh[tn][q].y);
-          v[4 * q + 2] = __builtin_fmaf(acc[tn][tm][4 * q + 2], sc[tn][q].z, sh[tn][q].z);
-          v[4 * q + 3] = __builtin_fmaf(acc[tn][tm][4 * q + 3], sc[tn][q].w, sh[tn][q].w);
-        }
-        if (a.pool2) {
-          // max over the window's quad of lanes (DPP quad_perm [1,0,3,2], then [2,3,0,1])
+        for (int tm = 0; tm < 2; ++tm) {
+          const int oh = g.oh0 + 4 * wave + 2 * tm + prow, ow = g.ow0 + pcol;
+          float v[16];
 #pragma unroll
           for (int e = 0; e < 16; ++e) {
+            v[e] = __builtin_fmaf(acc[tn][tm][e], (&sc[tn][e >> 2].x)[e & 3], (&sh[tn][e >> 2].x)[e & 3]);
             v[e] = fmaxf(v[e], __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v[e]), 0xB1, 0xF, 0xF, false)));
             v[e] = fmaxf(v[e], __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v[e]), 0x4E, 0xF, 0xF, false)));
           }
-          if ((frow & 3) != 0 || oh >= a.H || ow >= a.W) continue;
+          if ((frow & 3) != 0 || oh >= a.Ho || ow >= a.Wo) continue;
           if (a.relu) {
 #pragma unroll
             for (int e = 0; e < 16; ++e) v[e] = d3_relu(v[e]);
           }
-          bf16_t* y = (bf16_t*)a.y + ((long long)(g.n * (a.H >> 1) + (oh >> 1)) * (a.W >> 1) + (ow >> 1)) * a.ldy;
+          bf16_t* y = (bf16_t*)a.y + ((long long)(g.n * (a.Ho >> 1) + (oh >> 1)) * (a.Wo >> 1) + (ow >> 1)) * a.ldy +
+                      tn * 32 + 4 * fk;
 #pragma unroll
           for (int q = 0; q < 4; ++q)
-            *(uint2*)(y + tn * 32 + 8 * q + 4 * fk) =
-                make_uint2(d3_pack2(v[4 * q], v[4 * q + 1]), d3_pack2(v[4 * q + 2], v[4 * q + 3]));
-        } else {
-          if (oh >= a.H || ow >= a.W) continue;
-          if (a.relu) {
-#pragma unroll
-            for (int e = 0; e < 16; ++e) v[e] = d3_relu(v[e]);
-          }
-          bf16_t* y = (bf16_t*)a.y + ((long long)(g.n * a.H + oh) * a.W + ow) * a.ldy;
-#pragma unroll
-          for (int q = 0; q < 4; ++q)
-            *(uint2*)(y + tn * 32 + 8 * q + 4 * fk) =
-                make_uint2(d3_pack2(v[4 * q], v[4 * q + 1]), d3_pack2(v[4 * q + 2], v[4 * q + 3]));
+            *(uint2*)(y + 8 * q) = make_uint2(d3_pack2(v[4 * q], v[4 * q + 1]), d3_pack2(v[4 * q + 2], v[4 * q + 3]));
         }
-      }
+      continue;
     }
+    // Without pool the wave's 64 rounded pixels go to an LDS region as [pixel][8 chunks]
+    // (chunk c in slot c ^ swz(pixel)), then out with 16-byte stores of whole 128-byte
+    // pixel rows, 8 lanes per pixel.  The region is the wave's share of the patch buffer
+    // this tile was computed from (free until the next tile refills it), or with 8 input
+    // channels a region of its own.
+    uint4* stg = lds + (CS == 8 ? D::STG : pbase) + wave * 64 * 8;
+#pragma unroll
+    for (int tn = 0; tn < 2; ++tn)
+#pragma unroll
+      for (int tm = 0; tm < 2; ++tm)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          float v[4];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) v[j] = __builtin_fmaf(acc[tn][tm][4 * q + j], (&sc[tn][q].x)[j], (&sh[tn][q].x)[j]);
+          if (a.relu) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) v[j] = d3_relu(v[j]);
+          }
+          const int p = tm * 32 + frow, c = tn * 4 + q;
+          *(uint2*)((char*)(stg + p * 8 + (c ^ d3_swz(p))) + 8 * fk) = make_uint2(d3_pack2(v[0], v[1]), d3_pack2(v[2], v[3]));
+        }
+    __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): the wave's staging writes have landed
+    __builtin_amdgcn_wave_barrier();
+#pragma unroll
+    for (int r = 0; r < 8; ++r) {
+      const int p = r * 8 + (lane >> 3), c = lane & 7, f = p & 31;
+      const uint4 val = stg[p * 8 + (c ^ d3_swz(p))];
+      const int oh = g.oh0 + 4 * wave + 2 * (p >> 5) + ((f >> 1) & 1), ow = g.ow0 + 2 * (f >> 2) + (f & 1);
+      if (oh < a.Ho && ow < a.Wo)
+        *(uint4*)((bf16_t*)a.y + ((long long)(g.n * a.Ho + oh) * a.Wo + ow) * a.ldy + c * 8) = val;
+    }
+    __builtin_amdgcn_s_waitcnt(0xC07F);   // reads done before the region is rewritten
+    if constexpr (CS == 64) __syncthreads();   // every wave is done before the next tile refills the buffer
+    else __builtin_amdgcn_wave_barrier();
   }
 }
 
-bool conv3x3_direct_fits(const ConvArgs& a) {
-  return a.kh == 3 && a.kw == 3 && a.stride == 1 && a.pad == 1 && a.Cs == 64 && a.K == 576 && a.Kp == 576 &&
-         a.Nc == 64 && a.Co_pad >= 64 && a.c_write == 64 && a.ldy >= 64 && a.ldy % 4 == 0 && a.Ho == a.H &&
-         a.Wo == a.W && a.res == nullptr && !a.out_f32 && a.tap_stride == 0 && a.maxslot == nullptr &&
-         a.n_members <= 1 && (!a.pool2 || (a.H % 2 == 0 && a.W % 2 == 0)) && a.N >= 1;
+// Which instance takes this launch: 1 = 64 channels 3x3, 2 = 8 channels 3x3, 3 = 8
+// channels 7x7 stride 2; 0 = none.  The 8-channel instances ask for ReLU (a tap past
+// the last adds exact zeros on either path, which can differ only in the sign of a zero
+// sum, and ReLU maps both zeros to +0) and no fused pool (their epilogue stores whole
+// pixels).
+int conv_direct_variant(const ConvArgs& a) {
+  if (a.res != nullptr || a.out_f32 || a.tap_stride != 0 || a.maxslot != nullptr || a.n_members > 1 ||
+      a.Nc != 64 || a.Co_pad < 64 || a.c_write != 64 || a.ldy < 64 || a.ldy % 4 != 0 || a.N < 1 ||
+      a.kh != a.kw || (a.pool2 && (a.Ho % 2 != 0 || a.Wo % 2 != 0)))
+    return 0;
+  auto out_ok = [&](int k, int st) {
+    const int pad = k / 2;
+    return a.pad == pad && a.stride == st && a.Ho == (a.H + 2 * pad - k) / st + 1 &&
+           a.Wo == (a.W + 2 * pad - k) / st + 1;
+  };
+  if (a.kh == 3 && a.Cs == 64 && a.K == 576 && a.Kp == 576 && out_ok(3, 1)) return 1;
+  if (a.kh == 3 && a.Cs == 8 && a.K == 72 && a.Kp >= 80 && a.relu && !a.pool2 && out_ok(3, 1)) return 2;
+  if (a.kh == 7 && a.Cs == 8 && a.K == 392 && a.Kp >= 400 && a.relu && !a.pool2 && out_ok(7, 2)) return 3;
+  return 0;
 }
 
+bool conv3x3_direct_fits(const ConvArgs& a) { return conv_direct_variant(a) != 0; }
+
 hipError_t launch_conv3x3_direct(const ConvArgs& a, hipStream_t s) {
-  if (!conv3x3_direct_fits(a)) return hipErrorInvalidValue;
+  const int variant = conv_direct_variant(a);
+  if (!variant) return hipErrorInvalidValue;
   // compute units per device, queried once (concurrent first calls store the same value)
   static std::atomic<int> cus[64];
   int dev = 0;
@@ -251,10 +337,17 @@ hipError_t launch_conv3x3_direct(const ConvArgs& a, hipStream_t s) {
     n_cu = n_cu > 0 ? n_cu : 1;
     cus[dev].store(n_cu, std::memory_order_relaxed);
   }
-  const long long tiles = (long long)a.N * ((a.H + kTile - 1) / kTile) * ((a.W + kTile - 1) / kTile);
-  const int grid = (int)std::min<long long>(tiles, n_cu);
-  launch(conv3x3_direct_kernel, dim3(grid), dim3(256), s, a);
+  const long long tiles = (long long)a.N * ((a.Ho + kTile - 1) / kTile) * ((a.Wo + kTile - 1) / kTile);
+  const int per_cu = variant == 2 ? 2 : 1;   // workgroups that fit on a compute unit
+  const int grid = (int)std::min<long long>(tiles, (long long)n_cu * per_cu);
+  if (variant == 1) launch((conv_direct_kernel<64, 3, 1, 1>), dim3(grid), dim3(256), s, a);
+  else if (variant == 2) launch((conv_direct_kernel<8, 3, 1, 2>), dim3(grid), dim3(256), s, a);
+  else launch((conv_direct_kernel<8, 7, 2, 1>), dim3(grid), dim3(256), s, a);
   return hipGetLastError();
 }
+
+template __global__ void conv_direct_kernel<64, 3, 1, 1>(ConvArgs);
+template __global__ void conv_direct_kernel<8, 3, 1, 2>(ConvArgs);
+template __global__ void conv_direct_kernel<8, 7, 2, 1>(ConvArgs);
 
 }  // namespace rafiki

@@ -1192,14 +1192,24 @@ int run_gemm(const rafiki_ensemble_s* e, const Op& op, ConvArgs a, hipStream_t s
   return RAFIKI_OK;
 }
 
-// Whether op (of model M) is one the direct 3x3 kernel takes when launched alone: the
-// op-level form of conv3x3_direct_fits for the tuner's candidate list.
+// Whether op (of model M) is one the direct conv kernel takes when launched alone: the
+// op-level form of conv3x3_direct_fits (conv3x3_direct.hip) for the tuner's candidate
+// list: 64 output channels, no residual, and 3x3 stride 1 over 64 channels, or (with
+// ReLU, no fused pool) 3x3 stride 1 or 7x7 stride 2 over the 8 storage channels of an image.
 bool direct3x3_op_fits(const rafiki_ensemble_s* e, const Model& M, const Op& op) {
   if (e->precision != RAFIKI_BF16 || op.kind != O_CONV || op.nseg > 0 || op.table || op.in2 >= 0) return false;
   const Tensor& y = M.tensors[op.out];
-  return op.kh == 3 && op.kw == 3 && op.stride == 1 && op.pad == 1 && op.Cs_in == 64 && op.K == 576 &&
-         op.Kp == 576 && op.c_out == 64 && op.Ho == op.H && op.Wo == op.W && !y.is_logits && y.Cs == 64 &&
-         op.tap_stride == 0 && (!op.pool2 || (op.H % 2 == 0 && op.W % 2 == 0));
+  if (op.c_out != 64 || y.is_logits || y.Cs != 64 || op.tap_stride != 0 || op.kh != op.kw ||
+      (op.pool2 && (op.Ho % 2 != 0 || op.Wo % 2 != 0)))
+    return false;
+  auto out_ok = [&](int k, int st) {
+    const int pad = k / 2;
+    return op.pad == pad && op.stride == st && op.Ho == (op.H + 2 * pad - k) / st + 1 &&
+           op.Wo == (op.W + 2 * pad - k) / st + 1;
+  };
+  if (op.kh == 3 && op.Cs_in == 64 && op.K == 576 && op.Kp == 576 && out_ok(3, 1)) return true;
+  if (op.kh == 3 && op.Cs_in == 8 && op.K == 72 && op.Kp >= 80 && op.relu && !op.pool2 && out_ok(3, 1)) return true;
+  return op.kh == 7 && op.Cs_in == 8 && op.K == 392 && op.Kp >= 400 && op.relu && !op.pool2 && out_ok(7, 2);
 }
 
 // Kernel arguments of a GEMM-like op over n requests (output pointer set by the caller).

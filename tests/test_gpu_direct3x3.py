@@ -1,14 +1,16 @@
-"""The direct 3x3 kernel for 64-channel layers (weights and an 18 x 18 input patch per
-16 x 16 output tile held in LDS) gives the same bits as the bf16 GEMM kernel.
+"""The direct conv kernel (weights and an input patch per 16 x 16 output tile held in
+LDS) gives the same bits as the bf16 GEMM kernel.
 
-The tuner times it as one more candidate of the layers it takes (3x3, stride 1,
-padding 1, 64 -> 64 channels, no residual, optionally with the fused 2x2 max-pool), so
+The tuner times it as one more candidate of the layers it takes (64 output channels,
+no residual; 3x3 stride 1 over 64 channels, optionally with the fused 2x2 max-pool, or
+with ReLU 3x3 stride 1 and 7x7 stride 2 over the 8 storage channels of an image), so
 its results must not depend on the choice.  Each probe model ends in global average
 pooling and a random FC, as in the tile tests: equal logits mean equal conv outputs.
 Covered: maps that are not multiples of the 16 x 16 tile (ragged tiles in both
 directions, odd sizes), fewer tiles than compute units and many tiles per workgroup,
-the fused pool after a 3 -> 64 first layer, a 64 -> 64 layer after a strided one, and a
-layer the kernel does not take (residual) next to one it does.  Also against the oracle.
+the fused pool after a 3 -> 64 first layer, 7x7 stride-2 stems on odd sizes, a 64 -> 64
+layer after a strided one, and layers the kernel does not take (residual; an RGB layer
+without ReLU) next to ones it does.  Also against the oracle.
 """
 import numpy as np
 import pytest
@@ -38,7 +40,13 @@ CASES = {
     "ragged_20x36": ([conv(-1, 64, 64, 3)], (64, 20, 36), 5, 1),
     "odd_15x17": ([conv(-1, 64, 64, 3)], (64, 15, 17), 3, 1),
     "many_tiles_per_workgroup": ([conv(-1, 64, 64, 3)], (64, 32, 32), 300, 1),
-    "fused_pool_after_rgb": ([conv(-1, 3, 64, 3), conv(0, 64, 64, 3), pool(1, 64)], (3, 36, 28), 17, 1),
+    "fused_pool_after_rgb": ([conv(-1, 3, 64, 3), conv(0, 64, 64, 3), pool(1, 64)], (3, 36, 28), 17, 2),
+    # the 8 storage channels of an RGB image: 3x3 stride 1, 7x7 stride 2 (stems, odd sizes)
+    "rgb_3x3_many_tiles": ([conv(-1, 3, 64, 3)], (3, 40, 48), 90, 1),
+    "stem_7x7_s2_odd": ([conv(-1, 3, 64, 7, s=2)], (3, 45, 38), 5, 1),
+    "stem_7x7_s2_many_tiles": ([conv(-1, 3, 64, 7, s=2)], (3, 64, 64), 300, 1),
+    # without ReLU the 8-channel layers stay on the GEMM; the 64-channel one does not care
+    "rgb_no_relu_then_64": ([conv(-1, 3, 64, 3, relu=False), conv(0, 64, 64, 3, relu=False)], (3, 20, 20), 4, 1),
     "after_stride2_and_residual_next": ([conv(-1, 64, 64, 3, s=2), conv(0, 64, 64, 3), conv(1, 64, 64, 3, res=0)],
                                         (64, 34, 40), 6, 1),
     "relu_off_two_layers": ([conv(-1, 64, 64, 3, relu=False), conv(0, 64, 64, 3)], (64, 18, 16), 9, 2),
