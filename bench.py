@@ -87,9 +87,9 @@ def parse():
     return ap.parse_args()
 
 
-# the bf16 conv launches (trace class conv_mfma): the GEMM kernel and the direct 3x3 kernel
-CONV_SOURCES = [os.path.join(ROOT, "paper_1804_06087_amd", "csrc", f) for f in ("conv_mfma.hip", "conv3x3_direct.hip")]
-CONV_KERNEL_NAMES = ("conv_mfma_kernel", "conv3x3_direct_kernel")
+# the bf16 conv launches (trace class conv_mfma): the GEMM kernel and the direct conv kernel
+CONV_SOURCES = [os.path.join(ROOT, "paper_1804_06087_amd", "csrc", f) for f in ("conv_mfma.hip", "conv_direct.hip")]
+CONV_KERNEL_NAMES = ("conv_mfma_kernel", "conv_direct_kernel")
 
 
 def kernel_source_sha() -> str:
@@ -617,7 +617,7 @@ def layers_main(args, dev):
     tot_ms = sum(a["ms"] for a in agg.values())
     tot_bound = 0.0
     from paper_1804_06087_amd.binding import tile_configs
-    n_gemm_cfgs = len(tile_configs())   # the trace's tile id of the direct 3x3 kernel
+    n_gemm_cfgs = len(tile_configs())   # the trace's tile id of the direct conv kernel
     print(f"# Per-launch roofline: {cfg.name}, batch {n}, mask {mask:#b}\n")
     print(f"Command: `python bench.py --layers --workload {args.workload}"
           + (f" --n {args.n}" if args.n else "") + (f" --mask {args.mask}" if args.mask else "") + "`\n")
@@ -638,7 +638,7 @@ def layers_main(args, dev):
             desc = f"{OP_NAMES[L.op]} {L.c_in}->{L.c_out} {L.kh}x{L.kw}/{L.stride}"
             if OP_NAMES[L.op] == "concat" and kind != "concat":   # branches fused into one GEMM + max
                 desc = f"conv1d_maxtime branches -> concat {L.c_out}"
-        tile = ("direct 3x3" if a["cfg"] == n_gemm_cfgs else f"{a['cfg']} / {a['splits']}") if a["cfg"] >= 0 else ""
+        tile = ("direct" if a["cfg"] == n_gemm_cfgs else f"{a['cfg']} / {a['splits']}") if a["cfg"] >= 0 else ""
         print(f"| {specs[m].name if m >= 0 else '-'} | {li} | {desc} | {kind} | {tile} | {a['ms'] * 1e3:.1f} | "
               f"{a['flops'] / a['ms'] / 1e9:.0f} | {a['bytes'] / a['ms'] / 1e6:.0f} | {bound} | {tb * 1e3:.1f} | "
               f"{tb / a['ms']:.2f} |")

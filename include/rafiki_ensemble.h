@@ -291,11 +291,12 @@ int rafiki_tile_config(int cfg, int* bm, int* bn, int* waves, int* stages, int* 
 /* Diagnostics: make every subsequent unsplit bf16 GEMM launch of the handle use tile
  * configuration `cfg` wherever its channel tile suits the layer's output channels
  * (other layers keep their tuned choice); cfg = -1 restores the tuned choice.
- * cfg = RAFIKI_TILE_DIRECT3X3 runs every layer that the direct 3x3 kernel takes (bf16,
- * 3x3, stride 1, padding 1, 64 input and 64 output channels, no residual, optionally
- * with the fused 2x2 max-pool; one launch per model) with that kernel, which the tuner
+ * cfg = RAFIKI_TILE_DIRECT runs every layer that the direct conv kernel takes with that
+ * kernel (bf16, 64 output channels, no residual, one launch per model; 3x3 stride 1 over
+ * 64 input channels, optionally with the fused 2x2 max-pool, or with ReLU and no pool
+ * 3x3 stride 1 or 7x7 stride 2 over an image's 8 storage channels), which the tuner
  * otherwise times as one more candidate.  Results are unchanged; only speed differs. */
-#define RAFIKI_TILE_DIRECT3X3 1000
+#define RAFIKI_TILE_DIRECT 1000
 int rafiki_ensemble_force_tile(rafiki_ensemble_t h, int cfg);
 
 /* Schedule of the selected models' forward passes for one (n, model_subset_mask).

@@ -18,8 +18,8 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.environ.get("RAFIKI_LIBRARY") or os.path.join(_PKG, "librafiki_ensemble.so")
 
 RAFIKI_OK, RAFIKI_ERR_INVALID, RAFIKI_ERR_UNSUPPORTED, RAFIKI_ERR_NOMEM, RAFIKI_ERR_HIP = 0, -1, -2, -3, -4
-# force_tile: the direct 3x3 kernel wherever it applies (RAFIKI_TILE_DIRECT3X3 in the header)
-RAFIKI_TILE_DIRECT3X3 = 1000
+# force_tile: the direct conv kernel wherever it applies (RAFIKI_TILE_DIRECT in the header)
+RAFIKI_TILE_DIRECT = 1000
 RAFIKI_FP32, RAFIKI_BF16 = 0, 1
 RAFIKI_INPUT_IMAGE_NCHW_F32, RAFIKI_INPUT_TOKENS_I32 = 0, 1
 EXPORTED = ("rafiki_ensemble_create", "rafiki_ensemble_infer", "rafiki_ensemble_infer_vote",

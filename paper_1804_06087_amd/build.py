@@ -15,7 +15,7 @@ ROOT = os.path.dirname(PKG)
 SRC = os.path.join(PKG, "csrc")
 OBJ = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "librafiki_ensemble.so")
-SOURCES = ["conv_mfma.hip", "conv3x3_direct.hip", "misc.hip", "fused_net.hip", "runtime.hip", "greedy.cpp", "rl.cpp"]
+SOURCES = ["conv_mfma.hip", "conv_direct.hip", "misc.hip", "fused_net.hip", "runtime.hip", "greedy.cpp", "rl.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-I", os.path.join(ROOT, "include"),
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]

@@ -19,7 +19,7 @@ from . import build as b
 SAN_DIR = os.path.join(b.OBJ, "san")
 SAN_LIB = os.path.join(SAN_DIR, "librafiki_ensemble_san.so")
 HOST_SOURCES = ["runtime.hip", "greedy.cpp", "rl.cpp"]      # instrumented
-KERNEL_SOURCES = ["conv_mfma.hip", "conv3x3_direct.hip", "misc.hip", "fused_net.hip"]   # linked as built
+KERNEL_SOURCES = ["conv_mfma.hip", "conv_direct.hip", "misc.hip", "fused_net.hip"]   # linked as built
 SAN_FLAGS = "-Xarch_host -fsanitize=address -Xarch_host -fsanitize=undefined".split()
 HOST_DEBUG = "-Xarch_host -fno-omit-frame-pointer -Xarch_host -g".split()
 

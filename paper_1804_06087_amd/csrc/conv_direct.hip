@@ -319,9 +319,9 @@ int conv_direct_variant(const ConvArgs& a) {
   return 0;
 }
 
-bool conv3x3_direct_fits(const ConvArgs& a) { return conv_direct_variant(a) != 0; }
+bool conv_direct_fits(const ConvArgs& a) { return conv_direct_variant(a) != 0; }
 
-hipError_t launch_conv3x3_direct(const ConvArgs& a, hipStream_t s) {
+hipError_t launch_conv_direct(const ConvArgs& a, hipStream_t s) {
   const int variant = conv_direct_variant(a);
   if (!variant) return hipErrorInvalidValue;
   // compute units per device, queried once (concurrent first calls store the same value)

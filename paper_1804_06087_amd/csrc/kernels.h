@@ -159,11 +159,11 @@ struct MfmaConfig { int bm, bn, waves, stages, bk; };
 constexpr int kNumMfmaConfigs = 43;
 extern const MfmaConfig kMfmaConfigs[kNumMfmaConfigs];
 hipError_t launch_conv_mfma(const ConvArgs& a, int cfg, int splits, hipStream_t s);
-// Direct 3x3 convolution of 64-channel bf16 layers (conv3x3_direct.hip): the tuner's
-// candidate kCfgDirect3x3 beside the GEMM tiles, bitwise equal to them.
-constexpr int kCfgDirect3x3 = kNumMfmaConfigs;
-bool conv3x3_direct_fits(const ConvArgs& a);
-hipError_t launch_conv3x3_direct(const ConvArgs& a, hipStream_t s);
+// Direct convolution of bf16 layers with 64 output channels (conv_direct.hip): the tuner's
+// candidate kCfgDirect beside the GEMM tiles, bitwise equal to them.
+constexpr int kCfgDirect = kNumMfmaConfigs;
+bool conv_direct_fits(const ConvArgs& a);
+hipError_t launch_conv_direct(const ConvArgs& a, hipStream_t s);
 hipError_t launch_splitk_reduce(const ConvArgs& a, int splits, int in_bf16, hipStream_t s);
 // fp32 direct kernel (CUDA-core style FMA loops; used by the fp32 precision mode).
 hipError_t launch_conv_f32(const ConvArgs& a, hipStream_t s);

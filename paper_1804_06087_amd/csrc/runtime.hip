@@ -1163,7 +1163,7 @@ int run_gemm(const rafiki_ensemble_s* e, const Op& op, ConvArgs a, hipStream_t s
     a.kt_per_split = (cb + sp - 1) / sp;
     splits = (cb + a.kt_per_split - 1) / a.kt_per_split;
   }
-  if (cfg == kCfgDirect3x3 && (splits > 1 || !conv3x3_direct_fits(a))) cfg = -1;   // e.g. a grouped launch
+  if (cfg == kCfgDirect && (splits > 1 || !conv_direct_fits(a))) cfg = -1;   // e.g. a grouped launch
   if (cfg < 0) cfg = splits > 1 ? split_cfg(op.c_out) : default_cfg(op.c_out);
   struct TileScope {
     TileScope(int c, int sp) { trace_tile() = {c, sp}; }
@@ -1184,8 +1184,8 @@ int run_gemm(const rafiki_ensemble_s* e, const Op& op, ConvArgs a, hipStream_t s
     TRACED(e, s, RAFIKI_K_SPLITK_REDUCE, mi, li, 0.0,
            nm * ((double)splits * a.M * a.c_write * 4.0 + out_rows * a.c_write * (a.out_f32 ? 4.0 : es)),
            launch_splitk_reduce(a, splits, 1, s));
-  } else if (cfg == kCfgDirect3x3) {
-    TRACED(e, s, RAFIKI_K_CONV_MFMA, mi, li, flops, bytes, launch_conv3x3_direct(a, s));
+  } else if (cfg == kCfgDirect) {
+    TRACED(e, s, RAFIKI_K_CONV_MFMA, mi, li, flops, bytes, launch_conv_direct(a, s));
   } else {
     TRACED(e, s, RAFIKI_K_CONV_MFMA, mi, li, flops, bytes, launch_conv_mfma(a, cfg, 1, s));
   }
@@ -1193,10 +1193,10 @@ int run_gemm(const rafiki_ensemble_s* e, const Op& op, ConvArgs a, hipStream_t s
 }
 
 // Whether op (of model M) is one the direct conv kernel takes when launched alone: the
-// op-level form of conv3x3_direct_fits (conv3x3_direct.hip) for the tuner's candidate
+// op-level form of conv_direct_fits (conv_direct.hip) for the tuner's candidate
 // list: 64 output channels, no residual, and 3x3 stride 1 over 64 channels, or (with
 // ReLU, no fused pool) 3x3 stride 1 or 7x7 stride 2 over the 8 storage channels of an image.
-bool direct3x3_op_fits(const rafiki_ensemble_s* e, const Model& M, const Op& op) {
+bool direct_op_fits(const rafiki_ensemble_s* e, const Model& M, const Op& op) {
   if (e->precision != RAFIKI_BF16 || op.kind != O_CONV || op.nseg > 0 || op.table || op.in2 >= 0) return false;
   const Tensor& y = M.tensors[op.out];
   if (op.c_out != 64 || y.is_logits || y.Cs != 64 || op.tap_stride != 0 || op.kh != op.kw ||
@@ -1276,7 +1276,7 @@ int tune(rafiki_ensemble_s* e, int n, const void* in, hipStream_t s) {
       if (!timing) continue;
       for (int cfg = 0; cfg < kNumMfmaConfigs; ++cfg)
         if (cfg_fits(cfg, op.c_out) && kMfmaConfigs[cfg].bm <= 2 * round_up(M_rows, 32)) cand[mi][oi].push_back(cfg);
-      if (splits == 1 && direct3x3_op_fits(e, M, op)) cand[mi][oi].push_back(kCfgDirect3x3);
+      if (splits == 1 && direct_op_fits(e, M, op)) cand[mi][oi].push_back(kCfgDirect);
     }
   }
   if (!timing) {
@@ -1324,7 +1324,7 @@ int tune(rafiki_ensemble_s* e, int n, const void* in, hipStream_t s) {
             break;
           }
           const int oi = r.layer >= 0 && r.layer < (int)out_to_op.size() ? out_to_op[r.layer] : -1;
-          if (oi >= 0 && r.cfg >= 0 && r.cfg <= kCfgDirect3x3)
+          if (oi >= 0 && r.cfg >= 0 && r.cfg <= kCfgDirect)
             best[mi][oi][r.cfg] = std::min(best[mi][oi][r.cfg], ms);
         }
       }
@@ -1396,8 +1396,8 @@ int run_op(const rafiki_ensemble_s* e, const int* mis, const int* ois, int nm, c
       case O_CONV1D: {
         ConvArgs a = gemm_args(e, M, op, n, in);
         int cfg = cfgs.empty() ? -1 : cfgs[oi];
-        if (e->force_tile == kCfgDirect3x3) {
-          if (direct3x3_op_fits(e, M, op)) cfg = kCfgDirect3x3;
+        if (e->force_tile == kCfgDirect) {
+          if (direct_op_fits(e, M, op)) cfg = kCfgDirect;
         } else if (e->force_tile >= 0 && cfg_fits(e->force_tile, op.c_out)) {
           cfg = e->force_tile;
         }
@@ -2361,7 +2361,7 @@ int rafiki_tile_config(int cfg, int* bm, int* bn, int* waves, int* stages, int* 
 
 int rafiki_ensemble_force_tile(rafiki_ensemble_t h, int cfg) {
   if (!h) return fail(RAFIKI_ERR_INVALID, "null handle");
-  if (cfg == RAFIKI_TILE_DIRECT3X3) cfg = kCfgDirect3x3;
+  if (cfg == RAFIKI_TILE_DIRECT) cfg = kCfgDirect;
   else if (cfg < -1 || cfg >= kNumMfmaConfigs) return fail(RAFIKI_ERR_INVALID, "no such tile configuration");
   if (cfg != h->force_tile) {
     HIPCHK(hipDeviceSynchronize());   // graphs holding the old tiles may still be running

@@ -53,7 +53,7 @@ def test_ctypes_layout_matches_headers(tmp_path):
 def test_binding_constants_match_headers(tmp_path):
     """Status codes, precisions and the direct-kernel tile id as the header defines them."""
     names = ["RAFIKI_OK", "RAFIKI_ERR_INVALID", "RAFIKI_ERR_UNSUPPORTED", "RAFIKI_ERR_NOMEM", "RAFIKI_ERR_HIP",
-             "RAFIKI_FP32", "RAFIKI_BF16", "RAFIKI_TILE_DIRECT3X3"]
+             "RAFIKI_FP32", "RAFIKI_BF16", "RAFIKI_TILE_DIRECT"]
     lines = ['#include <stdio.h>', '#include "rafiki_ensemble.h"', "int main(void) {"]
     lines += [f'  printf("{nm} %d\\n", (int)({nm}));' for nm in names]
     lines += ["  return 0;", "}"]

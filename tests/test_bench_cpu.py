@@ -72,7 +72,7 @@ def test_pmc_summary_counts_both_conv_kernels(tmp_path):
     """The traced class conv_mfma holds the GEMM and the direct 3x3 launches; the
     counter summary averages over both."""
     gemm = "void rafiki::conv_mfma_kernel<128, 128, 2, 2, 3, true, 8, false, false, 0>(rafiki::ConvArgs)"
-    direct = "rafiki::conv3x3_direct_kernel(rafiki::ConvArgs)"
+    direct = "rafiki::conv_direct_kernel(rafiki::ConvArgs)"
     copy = "void at::native::elementwise_kernel<mul>(x)"
     _write(str(tmp_path / "f"), "FETCH_SIZE", [(copy, 512.0), (gemm, 100.0), (direct, 300.0), (copy, 512.0)])
     _write(str(tmp_path / "w"), "WRITE_SIZE", [(copy, 1024.0), (gemm, 10.0), (direct, 30.0), (copy, 1024.0)])

@@ -19,7 +19,7 @@ import torch
 import oracle
 import workloads as wl
 from workloads import Layer, ModelSpec, CONV2D, MAXPOOL2D, GLOBAL_AVGPOOL, FC
-from paper_1804_06087_amd import Ensemble, RAFIKI_TILE_DIRECT3X3
+from paper_1804_06087_amd import Ensemble, RAFIKI_TILE_DIRECT
 from paper_1804_06087_amd.binding import tile_configs
 
 pytestmark = pytest.mark.gpu
@@ -58,7 +58,7 @@ def build(layers, shape):
     c = L[-1].c_out
     L.append(Layer(op=GLOBAL_AVGPOOL, input=len(L) - 1, c_in=c, c_out=c))
     L.append(Layer(op=FC, input=len(L) - 1, c_in=c, c_out=10, bias=True))
-    return ModelSpec("direct3x3", L, 10, shape)
+    return ModelSpec("direct_conv", L, 10, shape)
 
 
 def logits_and_tiles(ens, x, n):
@@ -72,7 +72,7 @@ def logits_and_tiles(ens, x, n):
 
 
 @pytest.mark.parametrize("name", sorted(CASES))
-def test_direct3x3_bitwise_equal_to_gemm(name):
+def test_direct_conv_bitwise_equal_to_gemm(name):
     layers, shape, n, n_direct = CASES[name]
     spec = build(layers, shape)
     params = wl.gen_params(spec, 5, True, "random")
@@ -80,7 +80,7 @@ def test_direct3x3_bitwise_equal_to_gemm(name):
     x = torch.from_numpy(batch).to(DEV)
     direct_id = len(tile_configs())   # the trace's tile id of the direct kernel
     with Ensemble([spec], [params], precision="bf16", max_batch=n) as ens:
-        ens.force_tile(RAFIKI_TILE_DIRECT3X3)
+        ens.force_tile(RAFIKI_TILE_DIRECT)
         zd, tiles = logits_and_tiles(ens, x, n)
         assert tiles.count(direct_id) == n_direct, tiles
         results = {"direct": zd}
@@ -113,7 +113,7 @@ def test_force_direct_rejects_nothing_and_restores():
     direct_id = len(tile_configs())
     with Ensemble([spec], [params], precision="bf16", max_batch=4) as ens:
         z0, _ = logits_and_tiles(ens, x, 4)
-        ens.force_tile(RAFIKI_TILE_DIRECT3X3)
+        ens.force_tile(RAFIKI_TILE_DIRECT)
         z1, tiles = logits_and_tiles(ens, x, 4)
         assert direct_id not in tiles
         assert np.array_equal(z0.view(np.uint32), z1.view(np.uint32))
