@@ -292,9 +292,9 @@ int rafiki_tile_config(int cfg, int* bm, int* bn, int* waves, int* stages, int* 
  * configuration `cfg` wherever its channel tile suits the layer's output channels
  * (other layers keep their tuned choice); cfg = -1 restores the tuned choice.
  * cfg = RAFIKI_TILE_DIRECT runs every layer that the direct conv kernel takes with that
- * kernel (bf16, 64 output channels, no residual, one launch per model; 3x3 stride 1 over
- * 64 input channels, optionally with the fused 2x2 max-pool, or with ReLU and no pool
- * 3x3 stride 1 or 7x7 stride 2 over an image's 8 storage channels), which the tuner
+ * kernel (bf16, no residual, one launch per model; 3x3 stride 1 from 64 to 64 or 128
+ * channels, optionally with the fused 2x2 max-pool, or with 64 output channels, ReLU
+ * and no pool 3x3 stride 1 or 7x7 stride 2 over an image's 8 storage channels), which the tuner
  * otherwise times as one more candidate.  Results are unchanged; only speed differs. */
 #define RAFIKI_TILE_DIRECT 1000
 int rafiki_ensemble_force_tile(rafiki_ensemble_t h, int cfg);

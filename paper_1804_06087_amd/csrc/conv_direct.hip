@@ -96,7 +96,11 @@ __global__ __launch_bounds__(256, OCC) void conv_direct_kernel(ConvArgs a) {
   const unsigned oob = (unsigned)a.x_bytes;   // offset at num_records: the hardware returns zeros
   const int tw = (a.Wo + kTile - 1) / kTile, per_img = ((a.Ho + kTile - 1) / kTile) * tw;
   const int ntiles = a.N * per_img;
-  const int G = gridDim.x;
+  // 64-channel input with 128 output channels: workgroup b computes the 64-channel half
+  // h = b % 2 of its tiles (weights, scale, shift and outputs offset by 64 h)
+  const int NH = CS == 64 ? a.Nc / 64 : 1;
+  const int h = (int)blockIdx.x % NH, c0 = 64 * h;
+  const int G = gridDim.x / NH;
 
   // Weights, once.  64 channels: load i moves tap i / 8, channels 8 * (i % 8) .. +8 (all
   // 8 chunks), lane l carrying chunk (l % 8) ^ swz(channel) into slot l % 8 of row (tap,
@@ -106,7 +110,7 @@ __global__ __launch_bounds__(256, OCC) void conv_direct_kernel(ConvArgs a) {
     for (int i = wave; i < D::TAPS * 8; i += 4) {
       const int t = i >> 3, co = (i & 7) * 8 + (lane >> 3);
       const int q = (lane & 7) ^ d3_swz(co);
-      const unsigned off = (unsigned)((co * a.Kp + t * 64 + q * 8) * 2);
+      const unsigned off = (unsigned)(((c0 + co) * a.Kp + t * 64 + q * 8) * 2);
       __builtin_amdgcn_raw_ptr_buffer_load_lds(wr, (d3_lds_void*)(lds + i * 64), 16, off, 0, 0, 0);
     }
   } else {
@@ -155,11 +159,11 @@ __global__ __launch_bounds__(256, OCC) void conv_direct_kernel(ConvArgs a) {
   for (int tn = 0; tn < 2; ++tn)
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      sc[tn][q] = *(const float4*)(a.scale + tn * 32 + 8 * q + 4 * fk);
-      sh[tn][q] = *(const float4*)(a.shift + tn * 32 + 8 * q + 4 * fk);
+      sc[tn][q] = *(const float4*)(a.scale + c0 + tn * 32 + 8 * q + 4 * fk);
+      sh[tn][q] = *(const float4*)(a.shift + c0 + tn * 32 + 8 * q + 4 * fk);
     }
 
-  int t = blockIdx.x;
+  int t = blockIdx.x / NH;
   if (t < ntiles) load_patch(t, 0);
   d3_wait_vmcnt<0>();
   __syncthreads();
@@ -253,7 +257,7 @@ __global__ __launch_bounds__(256, OCC) void conv_direct_kernel(ConvArgs a) {
             for (int e = 0; e < 16; ++e) v[e] = d3_relu(v[e]);
           }
           bf16_t* y = (bf16_t*)a.y + ((long long)(g.n * (a.Ho >> 1) + (oh >> 1)) * (a.Wo >> 1) + (ow >> 1)) * a.ldy +
-                      tn * 32 + 4 * fk;
+                      c0 + tn * 32 + 4 * fk;
 #pragma unroll
           for (int q = 0; q < 4; ++q)
             *(uint2*)(y + 8 * q) = make_uint2(d3_pack2(v[4 * q], v[4 * q + 1]), d3_pack2(v[4 * q + 2], v[4 * q + 3]));
@@ -290,7 +294,7 @@ __global__ __launch_bounds__(256, OCC) void conv_direct_kernel(ConvArgs a) {
       const uint4 val = stg[p * 8 + (c ^ d3_swz(p))];
       const int oh = g.oh0 + 4 * wave + 2 * (p >> 5) + ((f >> 1) & 1), ow = g.ow0 + 2 * (f >> 2) + (f & 1);
       if (oh < a.Ho && ow < a.Wo)
-        *(uint4*)((bf16_t*)a.y + ((long long)(g.n * a.Ho + oh) * a.Wo + ow) * a.ldy + c * 8) = val;
+        *(uint4*)((bf16_t*)a.y + ((long long)(g.n * a.Ho + oh) * a.Wo + ow) * a.ldy + c0 + c * 8) = val;
     }
     __builtin_amdgcn_s_waitcnt(0xC07F);   // reads done before the region is rewritten
     if constexpr (CS == 64) __syncthreads();   // every wave is done before the next tile refills the buffer
@@ -298,14 +302,15 @@ __global__ __launch_bounds__(256, OCC) void conv_direct_kernel(ConvArgs a) {
   }
 }
 
-// Which instance takes this launch: 1 = 64 channels 3x3, 2 = 8 channels 3x3, 3 = 8
-// channels 7x7 stride 2; 0 = none.  The 8-channel instances ask for ReLU (a tap past
+// Which instance takes this launch: 1 = 64 channels 3x3 (64 or, as two halves, 128
+// output channels), 2 = 8 channels 3x3, 3 = 8 channels 7x7 stride 2; 0 = none.  The 8-channel instances ask for ReLU (a tap past
 // the last adds exact zeros on either path, which can differ only in the sign of a zero
 // sum, and ReLU maps both zeros to +0) and no fused pool (their epilogue stores whole
 // pixels).
 int conv_direct_variant(const ConvArgs& a) {
   if (a.res != nullptr || a.out_f32 || a.tap_stride != 0 || a.maxslot != nullptr || a.n_members > 1 ||
-      a.Nc != 64 || a.Co_pad < 64 || a.c_write != 64 || a.ldy < 64 || a.ldy % 4 != 0 || a.N < 1 ||
+      (a.Nc != 64 && !(a.Nc == 128 && a.Cs == 64)) || a.Co_pad < a.Nc || a.c_write != a.Nc || a.ldy < a.Nc ||
+      a.ldy % 4 != 0 || a.N < 1 ||
       a.kh != a.kw || (a.pool2 && (a.Ho % 2 != 0 || a.Wo % 2 != 0)))
     return 0;
   auto out_ok = [&](int k, int st) {
@@ -339,7 +344,8 @@ hipError_t launch_conv_direct(const ConvArgs& a, hipStream_t s) {
   }
   const long long tiles = (long long)a.N * ((a.Ho + kTile - 1) / kTile) * ((a.Wo + kTile - 1) / kTile);
   const int per_cu = variant == 2 ? 2 : 1;   // workgroups that fit on a compute unit
-  const int grid = (int)std::min<long long>(tiles, (long long)n_cu * per_cu);
+  const int halves = a.Nc / 64;               // 128 output channels: two workgroups per tile
+  const int grid = halves * (int)std::min<long long>(tiles, (long long)n_cu * per_cu / halves);
   if (variant == 1) launch((conv_direct_kernel<64, 3, 1, 1>), dim3(grid), dim3(256), s, a);
   else if (variant == 2) launch((conv_direct_kernel<8, 3, 1, 2>), dim3(grid), dim3(256), s, a);
   else launch((conv_direct_kernel<8, 7, 2, 1>), dim3(grid), dim3(256), s, a);

@@ -1194,13 +1194,14 @@ int run_gemm(const rafiki_ensemble_s* e, const Op& op, ConvArgs a, hipStream_t s
 
 // Whether op (of model M) is one the direct conv kernel takes when launched alone: the
 // op-level form of conv_direct_fits (conv_direct.hip) for the tuner's candidate
-// list: 64 output channels, no residual, and 3x3 stride 1 over 64 channels, or (with
-// ReLU, no fused pool) 3x3 stride 1 or 7x7 stride 2 over the 8 storage channels of an image.
+// list: no residual, and 3x3 stride 1 from 64 to 64 or 128 channels, or (64 output
+// channels, with ReLU, no fused pool) 3x3 stride 1 or 7x7 stride 2 over the 8 storage
+// channels of an image.
 bool direct_op_fits(const rafiki_ensemble_s* e, const Model& M, const Op& op) {
   if (e->precision != RAFIKI_BF16 || op.kind != O_CONV || op.nseg > 0 || op.table || op.in2 >= 0) return false;
   const Tensor& y = M.tensors[op.out];
-  if (op.c_out != 64 || y.is_logits || y.Cs != 64 || op.tap_stride != 0 || op.kh != op.kw ||
-      (op.pool2 && (op.Ho % 2 != 0 || op.Wo % 2 != 0)))
+  if ((op.c_out != 64 && !(op.c_out == 128 && op.Cs_in == 64)) || y.is_logits || y.Cs != op.c_out ||
+      op.tap_stride != 0 || op.kh != op.kw || (op.pool2 && (op.Ho % 2 != 0 || op.Wo % 2 != 0)))
     return false;
   auto out_ok = [&](int k, int st) {
     const int pad = k / 2;

@@ -1,16 +1,17 @@
 """The direct conv kernel (weights and an input patch per 16 x 16 output tile held in
 LDS) gives the same bits as the bf16 GEMM kernel.
 
-The tuner times it as one more candidate of the layers it takes (64 output channels,
-no residual; 3x3 stride 1 over 64 channels, optionally with the fused 2x2 max-pool, or
-with ReLU 3x3 stride 1 and 7x7 stride 2 over the 8 storage channels of an image), so
-its results must not depend on the choice.  Each probe model ends in global average
-pooling and a random FC, as in the tile tests: equal logits mean equal conv outputs.
-Covered: maps that are not multiples of the 16 x 16 tile (ragged tiles in both
-directions, odd sizes), fewer tiles than compute units and many tiles per workgroup,
-the fused pool after a 3 -> 64 first layer, 7x7 stride-2 stems on odd sizes, a 64 -> 64
-layer after a strided one, and layers the kernel does not take (residual; an RGB layer
-without ReLU) next to ones it does.  Also against the oracle.
+The tuner times it as one more candidate of the layers it takes (no residual; 3x3
+stride 1 from 64 to 64 or 128 channels, optionally with the fused 2x2 max-pool, or with
+64 output channels and ReLU 3x3 stride 1 and 7x7 stride 2 over the 8 storage channels
+of an image), so its results must not depend on the choice.  Each probe model ends in
+global average pooling and a random FC, as in the tile tests: equal logits mean equal
+conv outputs.  Covered: maps that are not multiples of the 16 x 16 tile (ragged tiles in
+both directions, odd sizes), fewer tiles than compute units and many tiles per
+workgroup, the fused pool after a 3 -> 64 first layer, 7x7 stride-2 stems on odd sizes,
+64 -> 128 channels as two halves (also pooled), a 64 -> 64 layer after a strided one,
+and layers the kernel does not take (residual; an RGB layer without ReLU) next to ones
+it does.  Also against the oracle.
 """
 import numpy as np
 import pytest
@@ -47,6 +48,9 @@ CASES = {
     "stem_7x7_s2_many_tiles": ([conv(-1, 3, 64, 7, s=2)], (3, 64, 64), 300, 1),
     # without ReLU the 8-channel layers stay on the GEMM; the 64-channel one does not care
     "rgb_no_relu_then_64": ([conv(-1, 3, 64, 3, relu=False), conv(0, 64, 64, 3, relu=False)], (3, 20, 20), 4, 1),
+    # 64 -> 128 channels: two workgroups per tile, one per 64-channel half (also pooled)
+    "cout128_ragged": ([conv(-1, 64, 128, 3)], (64, 20, 36), 7, 1),
+    "cout128_pool_many_tiles": ([conv(-1, 64, 128, 3), pool(0, 128)], (64, 32, 32), 200, 1),
     "after_stride2_and_residual_next": ([conv(-1, 64, 64, 3, s=2), conv(0, 64, 64, 3), conv(1, 64, 64, 3, res=0)],
                                         (64, 34, 40), 6, 1),
     "relu_off_two_layers": ([conv(-1, 64, 64, 3, relu=False), conv(0, 64, 64, 3)], (64, 18, 16), 9, 2),
