@@ -1,10 +1,10 @@
-// Direct convolution of bf16 NHWC layers with 64 output channels on gfx950 matrix
-// cores, for the layers where the implicit GEMM is bound by its loads (Section 5.1,
-// each model's forward pass over the batch):
-//   - 3x3, stride 1, 64 input channels (VGG-16's conv1_2 with its fused 2x2 max-pool, the
-//     56x56 3x3 layers of ResNet-50/101): the GEMM brings every input pixel into LDS nine
-//     times, once per tap, and with 64 output channels each 16-byte chunk it loads feeds
-//     just two MFMAs;
+// Direct convolution of bf16 NHWC layers with 64 output channels (or 128, as two halves)
+// on gfx950 matrix cores, for the layers where the implicit GEMM is bound by its loads
+// (Section 5.1, each model's forward pass over the batch):
+//   - 3x3, stride 1, 64 input channels (VGG-16's conv1_2 with its fused 2x2 max-pool and
+//     conv2_1, the 56x56 3x3 layers of ResNet-50/101): the GEMM brings every input pixel
+//     into LDS nine times, once per tap, and with 64 output channels each 16-byte chunk
+//     it loads feeds just two MFMAs;
 //   - 3x3, stride 1, and 7x7, stride 2, on the 8 storage channels of an RGB image (VGG-16's
 //     conv1_1, the ResNet stems): 9 or 49 taps re-read each pixel as often.
 // A persistent workgroup (one or two per compute unit) keeps the layer's weights in LDS
@@ -143,7 +143,7 @@ __global__ __launch_bounds__(256, OCC) void conv_direct_kernel(ConvArgs a) {
   };
 
   const int frow = lane & 31, fk = lane >> 5;
-  // Wave w computes tile rows 4w .. 4w + 3, all 64 channels; pixel block tm covers rows
+  // Wave w computes tile rows 4w .. 4w + 3, all 64 channels (of its half); pixel block tm covers rows
   // 4w + 2tm and 4w + 2tm + 1.  Column frow of a block is the pixel at row offset
   // (frow >> 1) & 1, column 2 (frow >> 2) + (frow & 1): the four pixels of each 2x2
   // window sit in four adjacent lanes (a DPP quad).  Which pixel a column holds does
