@@ -21,6 +21,7 @@
 // The outputs are therefore bitwise those of the GEMM kernel, whatever its tile.
 #include <algorithm>
 #include <atomic>
+#include <type_traits>
 
 #include "kernels.h"
 
@@ -32,6 +33,8 @@ typedef float d3_f32x16 __attribute__((ext_vector_type(16)));
 typedef __attribute__((address_space(3))) void d3_lds_void;
 typedef __bf16 d3_bf16x2 __attribute__((ext_vector_type(2)));
 typedef float d3_f32x2 __attribute__((ext_vector_type(2)));
+typedef unsigned d3_u32x2 __attribute__((ext_vector_type(2)));
+typedef unsigned d3_u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kTile = 16;    // output tile: 16 x 16 pixels
 constexpr int kDepth = 3;    // k-steps of fragment reads in flight ahead of the MFMAs
@@ -94,6 +97,11 @@ __global__ __launch_bounds__(256, OCC) void conv_direct_kernel(ConvArgs a) {
   const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc((void*)a.x, (short)0, a.x_bytes, 0x00020000);
   const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc((void*)a.w, (short)0, a.w_bytes, 0x00020000);
   const unsigned oob = (unsigned)a.x_bytes;   // offset at num_records: the hardware returns zeros
+  // Output through a buffer resource as well: the launcher takes only outputs below
+  // 4 GiB, so byte offsets fit 32 bits, and an offset at num_records (yoob) is dropped.
+  const int Hy = a.pool2 ? a.Ho >> 1 : a.Ho, Wy = a.pool2 ? a.Wo >> 1 : a.Wo;
+  const unsigned yoob = (unsigned)((unsigned long long)a.N * Hy * Wy * a.ldy * 2);
+  const __amdgpu_buffer_rsrc_t yr = __builtin_amdgcn_make_buffer_rsrc(a.y, (short)0, (int)yoob, 0x00020000);
   const int tw = (a.Wo + kTile - 1) / kTile, per_img = ((a.Ho + kTile - 1) / kTile) * tw;
   const int ntiles = a.N * per_img;
   // 64-channel input with 128 output channels: workgroup b computes the 64-channel half
@@ -120,38 +128,43 @@ __global__ __launch_bounds__(256, OCC) void conv_direct_kernel(ConvArgs a) {
     }
   }
   if (tid == 0) lds[D::ZERO] = make_uint4(0u, 0u, 0u, 0u);
-  // Patch of tile t into buffer b: patch pixel p is input row oh0 * ST - PAD + p / PS,
-  // column ow0 * ST - PAD + p % PS; pixels outside the image, and those past the patch,
-  // read zeros.
-  auto load_patch = [&](int t, int b) {
-    const TileGeo g = tile_geo(t, per_img, tw);
-    uint4* base = lds + D::WCHUNKS + b * D::PCHUNKS;
-    for (int i = wave; i < D::PLOADS; i += 4) {
-      const int p = i * D::PIX_PER_LOAD + lane / D::CC;
-      const int ph = p / D::PS, pw = p - ph * D::PS;
-      const int hi = g.oh0 * ST - D::PAD + ph, wi = g.ow0 * ST - D::PAD + pw;
-      const bool ok = p < D::PPIX && (unsigned)hi < (unsigned)a.H && (unsigned)wi < (unsigned)a.W;
-      unsigned off;
-      if constexpr (CS == 64) {
-        const int q = (lane & 7) ^ d3_swz(p);
-        off = ok ? (unsigned)((((g.n * a.H + hi) * a.W + wi) * 64 + q * 8) * 2) : oob;
-      } else {
-        off = ok ? (unsigned)(((g.n * a.H + hi) * a.W + wi) * 16) : oob;
-      }
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (d3_lds_void*)(base + i * 64), 16, off, 0, 0, 0);
-    }
+
+  // Patch of a tile: patch pixel p is input row oh0 * ST - PAD + p / PS, column
+  // ow0 * ST - PAD + p % PS; pixels outside the image, and those past the patch, read
+  // zeros.  Wave w issues loads i = w + 4j; a lane's patch row, column and offset within
+  // the image are the same for every tile (a pixel past the patch gets a row that fails
+  // the bounds check), so a load costs a few adds and compares.
+  constexpr int kLoads = (D::PLOADS + 3) / 4;   // loads per wave and patch
+  int lph[kLoads], lpw[kLoads], loff[kLoads];
+#pragma unroll
+  for (int j = 0; j < kLoads; ++j) {
+    const int i = wave + 4 * j;
+    const int p = i * D::PIX_PER_LOAD + lane / D::CC;
+    const int ph = p / D::PS, pw = p - ph * D::PS;
+    lph[j] = i < D::PLOADS && p < D::PPIX ? ph : 0x40000000;
+    lpw[j] = pw;
+    if constexpr (CS == 64) loff[j] = (ph * a.W + pw) * 128 + ((lane & 7) ^ d3_swz(p)) * 16;
+    else loff[j] = (ph * a.W + pw) * 16;
+  }
+  auto load_one = [&](const TileGeo& g, int b, int j) {
+    const int i = wave + 4 * j;
+    if (i >= D::PLOADS) return;
+    const int h0 = g.oh0 * ST - D::PAD, w0 = g.ow0 * ST - D::PAD;
+    const int base = ((g.n * a.H + h0) * a.W + w0) * (CS * 2);
+    const bool ok = (unsigned)(h0 + lph[j]) < (unsigned)a.H && (unsigned)(w0 + lpw[j]) < (unsigned)a.W;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (d3_lds_void*)(lds + D::WCHUNKS + b * D::PCHUNKS + i * 64), 16,
+                                             ok ? (unsigned)(base + loff[j]) : oob, 0, 0, 0);
   };
 
   const int frow = lane & 31, fk = lane >> 5;
-  // Wave w computes tile rows 4w .. 4w + 3, all 64 channels (of its half); pixel block tm covers rows
-  // 4w + 2tm and 4w + 2tm + 1.  Column frow of a block is the pixel at row offset
-  // (frow >> 1) & 1, column 2 (frow >> 2) + (frow & 1): the four pixels of each 2x2
-  // window sit in four adjacent lanes (a DPP quad).  Which pixel a column holds does
-  // not change its sum.
-  const int prow = (frow >> 1) & 1, pcol = 2 * (frow >> 2) + (frow & 1);
+  // Wave w computes tile rows 4w .. 4w + 3, all 64 channels (of its half).  Column frow
+  // of pixel block tm is the pixel at tile row 4w + 2 (frow / 16) + tm, column frow % 16:
+  // the two rows of each 2x2 window sit in one lane (blocks 0 and 1), its two columns in
+  // adjacent lanes.  Which pixel a column holds does not change its sum.
+  const int prow = 4 * wave + 2 * (frow >> 4), pcol = frow & 15;
   int pix0[2];   // patch pixel under tap (0, 0) of this lane's output in block tm
 #pragma unroll
-  for (int tm = 0; tm < 2; ++tm) pix0[tm] = (4 * wave + 2 * tm + prow) * ST * D::PS + pcol * ST;
+  for (int tm = 0; tm < 2; ++tm) pix0[tm] = (prow + tm) * ST * D::PS + pcol * ST;
   // scale and shift of this lane's output channels tn * 32 + 8q + 4fk + j, kept in
   // registers for the workgroup's life
   float4 sc[2][4], sh[2][4];
@@ -162,15 +175,27 @@ __global__ __launch_bounds__(256, OCC) void conv_direct_kernel(ConvArgs a) {
       sc[tn][q] = *(const float4*)(a.scale + c0 + tn * 32 + 8 * q + 4 * fk);
       sh[tn][q] = *(const float4*)(a.shift + c0 + tn * 32 + 8 * q + 4 * fk);
     }
+  // Byte offsets within a tile's output, per lane: the pooled pixel of a window's
+  // leading lane, or the pixel and 8-channel chunk of a whole-pixel store (8 lanes per
+  // pixel, the store of step r covering tile row 4w + 2 ((r % 4) / 2) + r / 4 and columns
+  // 8 (r % 2) .. + 8).
+  const int ylane = a.pool2 ? ((frow >> 4) * Wy + (pcol >> 1)) * a.ldy * 2 + (c0 + 4 * fk) * 2
+                            : ((lane >> 3) * a.ldy + c0 + (lane & 7) * 8) * 2;
 
   int t = blockIdx.x / NH;
-  if (t < ntiles) load_patch(t, 0);
+  if (t < ntiles) {
+    const TileGeo g = tile_geo(t, per_img, tw);
+#pragma unroll
+    for (int j = 0; j < kLoads; ++j) load_one(g, 0, j);
+  }
   d3_wait_vmcnt<0>();
   __syncthreads();
   for (int it = 0; t < ntiles; ++it, t += G) {
     const int b = it & 1;
-    if (t + G < ntiles) load_patch(t + G, b ^ 1);
     const int pbase = D::WCHUNKS + b * D::PCHUNKS;   // the patch being computed
+    // the next tile's patch goes into the other buffer, its loads spread over the k-steps
+    const bool more = t + G < ntiles;
+    const TileGeo gn = tile_geo(more ? t + G : t, per_img, tw);
 
     d3_f32x16 acc[2][2];
 #pragma unroll
@@ -214,17 +239,26 @@ __global__ __launch_bounds__(256, OCC) void conv_direct_kernel(ConvArgs a) {
     };
 #pragma unroll
     for (int ks = 0; ks < kDepth; ++ks) rd(ks, ks);
+    // one patch load every kEvery k-steps, all in the first half of the loop so that
+    // the second half covers their latency
+    constexpr int kEvery = D::NK / (2 * kLoads) > 1 ? D::NK / (2 * kLoads) : 1;
 #pragma unroll
     for (int ks = 0; ks < D::NK; ++ks) {
       const int s = ks % (kDepth + 1);
       if (ks + kDepth < D::NK) rd(ks + kDepth, (ks + kDepth) % (kDepth + 1));
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int tn = 0; tn < 2; ++tn)
+      for (int tn = 0; tn < 2; ++tn) {
 #pragma unroll
         for (int tm = 0; tm < 2; ++tm)
           acc[tn][tm] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[s][tn], xf[s][tm], acc[tn][tm], 0, 0, 0);
-      __builtin_amdgcn_sched_barrier(0);
+        // a patch load between two pairs of MFMAs, which run while it issues
+        if (tn == 0 && ks % kEvery == 0 && ks / kEvery < kLoads) {
+          __builtin_amdgcn_sched_barrier(0);
+          if (more) load_one(gn, b ^ 1, ks / kEvery);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
     }
     // This wave's loads of the next patch have landed, and every wave is done with this
     // patch: the next iteration may compute from the other buffer and refill this one.
@@ -235,33 +269,40 @@ __global__ __launch_bounds__(256, OCC) void conv_direct_kernel(ConvArgs a) {
     // channels tn * 32 + 8q + 4fk + j (q, j in 0..3) of its pixel.
     const TileGeo g = tile_geo(t, per_img, tw);
     if (CS == 64 && a.pool2) {
-      // Fused 2x2 max-pool: the max over each window's quad of lanes (DPP quad_perm
-      // [1,0,3,2], then [2,3,0,1]); the quad's first lane stores the pooled pixel's 16
-      // channels as 8-byte pieces (a quarter of the pixels: staging them for whole-pixel
-      // stores cost more in synchronisation than it saved).
+      // Fused 2x2 max-pool: the max of the lane's two rows, then of the two lanes
+      // (DPP quad_perm [1,0,3,2]); the window's even lane stores the pooled pixel's 16
+      // channels as 8-byte pieces.  With ReLU it is applied to each value first and the
+      // max taken on the bit patterns (non-negative floats order as their bits): for
+      // every non-NaN sum that is the max of the four values followed by ReLU.
+      const bool ok = (pcol & 1) == 0 && g.oh0 + prow < a.Ho && g.ow0 + pcol < a.Wo;
+      const unsigned ybase = (unsigned)((g.n * Hy + (g.oh0 >> 1) + 2 * wave) * Wy + (g.ow0 >> 1)) * (unsigned)a.ldy * 2u;
+      const unsigned yo = ok ? ybase + (unsigned)ylane : yoob;
+      auto fs = [&](int tn, int tm, int e) {
+        return __builtin_fmaf(acc[tn][tm][e], (&sc[tn][e >> 2].x)[e & 3], (&sh[tn][e >> 2].x)[e & 3]);
+      };
 #pragma unroll
-      for (int tn = 0; tn < 2; ++tn)
-#pragma unroll
-        for (int tm = 0; tm < 2; ++tm) {
-          const int oh = g.oh0 + 4 * wave + 2 * tm + prow, ow = g.ow0 + pcol;
-          float v[16];
+      for (int tn = 0; tn < 2; ++tn) {
+        int r[16];
+        if (a.relu) {
 #pragma unroll
           for (int e = 0; e < 16; ++e) {
-            v[e] = __builtin_fmaf(acc[tn][tm][e], (&sc[tn][e >> 2].x)[e & 3], (&sh[tn][e >> 2].x)[e & 3]);
-            v[e] = fmaxf(v[e], __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v[e]), 0xB1, 0xF, 0xF, false)));
-            v[e] = fmaxf(v[e], __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v[e]), 0x4E, 0xF, 0xF, false)));
+            r[e] = max(max(__float_as_int(fs(tn, 0, e)), 0), max(__float_as_int(fs(tn, 1, e)), 0));
+            r[e] = max(r[e], __builtin_amdgcn_mov_dpp(r[e], 0xB1, 0xF, 0xF, true));
           }
-          if ((frow & 3) != 0 || oh >= a.Ho || ow >= a.Wo) continue;
-          if (a.relu) {
+        } else {
 #pragma unroll
-            for (int e = 0; e < 16; ++e) v[e] = d3_relu(v[e]);
+          for (int e = 0; e < 16; ++e) {
+            const float v = fmaxf(fs(tn, 0, e), fs(tn, 1, e));
+            r[e] = __float_as_int(fmaxf(v, __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0xB1, 0xF, 0xF, true))));
           }
-          bf16_t* y = (bf16_t*)a.y + ((long long)(g.n * (a.Ho >> 1) + (oh >> 1)) * (a.Wo >> 1) + (ow >> 1)) * a.ldy +
-                      c0 + tn * 32 + 4 * fk;
-#pragma unroll
-          for (int q = 0; q < 4; ++q)
-            *(uint2*)(y + 8 * q) = make_uint2(d3_pack2(v[4 * q], v[4 * q + 1]), d3_pack2(v[4 * q + 2], v[4 * q + 3]));
         }
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const d3_u32x2 w = {d3_pack2(__int_as_float(r[4 * q]), __int_as_float(r[4 * q + 1])),
+                              d3_pack2(__int_as_float(r[4 * q + 2]), __int_as_float(r[4 * q + 3]))};
+          __builtin_amdgcn_raw_buffer_store_b64(w, yr, (int)(yo + tn * 64 + q * 16), 0, 0);
+        }
+      }
       continue;
     }
     // Without pool the wave's 64 rounded pixels go to an LDS region as [pixel][8 chunks]
@@ -270,31 +311,37 @@ __global__ __launch_bounds__(256, OCC) void conv_direct_kernel(ConvArgs a) {
     // this tile was computed from (free until the next tile refills it), or with 8 input
     // channels a region of its own.
     uint4* stg = lds + (CS == 8 ? D::STG : pbase) + wave * 64 * 8;
+    auto stage = [&](auto relu) {
 #pragma unroll
-    for (int tn = 0; tn < 2; ++tn)
+      for (int tn = 0; tn < 2; ++tn)
 #pragma unroll
-      for (int tm = 0; tm < 2; ++tm)
+        for (int tm = 0; tm < 2; ++tm)
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          float v[4];
+          for (int q = 0; q < 4; ++q) {
+            float v[4];
 #pragma unroll
-          for (int j = 0; j < 4; ++j) v[j] = __builtin_fmaf(acc[tn][tm][4 * q + j], (&sc[tn][q].x)[j], (&sh[tn][q].x)[j]);
-          if (a.relu) {
-#pragma unroll
-            for (int j = 0; j < 4; ++j) v[j] = d3_relu(v[j]);
+            for (int j = 0; j < 4; ++j) {
+              v[j] = __builtin_fmaf(acc[tn][tm][4 * q + j], (&sc[tn][q].x)[j], (&sh[tn][q].x)[j]);
+              if constexpr (decltype(relu)::value) v[j] = d3_relu(v[j]);
+            }
+            const int p = tm * 32 + frow, c = tn * 4 + q;
+            *(uint2*)((char*)(stg + p * 8 + (c ^ d3_swz(p))) + 8 * fk) = make_uint2(d3_pack2(v[0], v[1]), d3_pack2(v[2], v[3]));
           }
-          const int p = tm * 32 + frow, c = tn * 4 + q;
-          *(uint2*)((char*)(stg + p * 8 + (c ^ d3_swz(p))) + 8 * fk) = make_uint2(d3_pack2(v[0], v[1]), d3_pack2(v[2], v[3]));
-        }
+    };
+    if (a.relu) stage(std::true_type{});
+    else stage(std::false_type{});
     __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): the wave's staging writes have landed
     __builtin_amdgcn_wave_barrier();
+    const int hlim = a.Ho - g.oh0 - 4 * wave, wlim = a.Wo - g.ow0 - (lane >> 3);
+    const unsigned ybase = (unsigned)((g.n * a.Ho + g.oh0 + 4 * wave) * a.Wo + g.ow0) * (unsigned)a.ldy * 2u + (unsigned)ylane;
 #pragma unroll
     for (int r = 0; r < 8; ++r) {
-      const int p = r * 8 + (lane >> 3), c = lane & 7, f = p & 31;
+      const int p = r * 8 + (lane >> 3), c = lane & 7;
       const uint4 val = stg[p * 8 + (c ^ d3_swz(p))];
-      const int oh = g.oh0 + 4 * wave + 2 * (p >> 5) + ((f >> 1) & 1), ow = g.ow0 + 2 * (f >> 2) + (f & 1);
-      if (oh < a.Ho && ow < a.Wo)
-        *(uint4*)((bf16_t*)a.y + ((long long)(g.n * a.Ho + oh) * a.Wo + ow) * a.ldy + c0 + c * 8) = val;
+      const int dh = 2 * ((r & 3) >> 1) + (r >> 2), dw = 8 * (r & 1);   // step r's row and column in the wave's rows
+      const bool ok = dh < hlim && dw < wlim;
+      const unsigned yo = ok ? ybase + (unsigned)((dh * a.Wo + dw) * a.ldy * 2) : yoob;
+      __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(d3_u32x4, val), yr, (int)yo, 0, 0);
     }
     __builtin_amdgcn_s_waitcnt(0xC07F);   // reads done before the region is rewritten
     if constexpr (CS == 64) __syncthreads();   // every wave is done before the next tile refills the buffer
@@ -318,6 +365,10 @@ int conv_direct_variant(const ConvArgs& a) {
     return a.pad == pad && a.stride == st && a.Ho == (a.H + 2 * pad - k) / st + 1 &&
            a.Wo == (a.W + 2 * pad - k) / st + 1;
   };
+  // outputs are addressed with 32-bit byte offsets (plus at most 112 bytes of immediate)
+  const unsigned long long ybytes =
+      (unsigned long long)a.N * (a.pool2 ? (a.Ho / 2) * (a.Wo / 2) : a.Ho * a.Wo) * a.ldy * 2;
+  if (ybytes > 0xFFFFFF00ull) return 0;
   if (a.kh == 3 && a.Cs == 64 && a.K == 576 && a.Kp == 576 && out_ok(3, 1)) return 1;
   if (a.kh == 3 && a.Cs == 8 && a.K == 72 && a.Kp >= 80 && a.relu && !a.pool2 && out_ok(3, 1)) return 2;
   if (a.kh == 7 && a.Cs == 8 && a.K == 392 && a.Kp >= 400 && a.relu && !a.pool2 && out_ok(7, 2)) return 3;

@@ -9,7 +9,8 @@ global average pooling and a random FC, as in the tile tests: equal logits mean 
 conv outputs.  Covered: maps that are not multiples of the 16 x 16 tile (ragged tiles in
 both directions, odd sizes), fewer tiles than compute units and many tiles per
 workgroup, the fused pool after a 3 -> 64 first layer, 7x7 stride-2 stems on odd sizes,
-64 -> 128 channels as two halves (also pooled), a 64 -> 64 layer after a strided one,
+64 -> 128 channels as two halves (also pooled), the pool on ragged tiles with and
+without ReLU, a 64 -> 64 layer after a strided one,
 and layers the kernel does not take (residual; an RGB layer without ReLU) next to ones
 it does.  Also against the oracle.
 """
@@ -54,6 +55,9 @@ CASES = {
     "after_stride2_and_residual_next": ([conv(-1, 64, 64, 3, s=2), conv(0, 64, 64, 3), conv(1, 64, 64, 3, res=0)],
                                         (64, 34, 40), 6, 1),
     "relu_off_two_layers": ([conv(-1, 64, 64, 3, relu=False), conv(0, 64, 64, 3)], (64, 18, 16), 9, 2),
+    # the fused pool on ragged tiles, with ReLU (maximum on the bit patterns) and without
+    "pool_ragged_many_tiles": ([conv(-1, 64, 64, 3), pool(0, 64)], (64, 36, 52), 40, 1),
+    "pool_no_relu_ragged": ([conv(-1, 64, 64, 3, relu=False), pool(0, 64)], (64, 20, 36), 6, 1),
 }
 
 
