@@ -92,11 +92,22 @@ CONV_SOURCES = [os.path.join(ROOT, "paper_1804_06087_amd", "csrc", f) for f in (
 CONV_KERNEL_NAMES = ("conv_mfma_kernel", "conv_direct_kernel")
 
 
+def strip_comments(src: str) -> str:
+    """C++ source without its comments and blank space, so that editing a comment keeps
+    the hash of the code (string literals in the kernel sources hold no comment marks)."""
+    import re
+    src = re.sub(r"/\*.*?\*/", " ", src, flags=re.S)
+    src = re.sub(r"//[^\n]*", "", src)
+    return "\n".join(" ".join(line.split()) for line in src.splitlines() if line.strip())
+
+
 def kernel_source_sha() -> str:
+    """sha256 of the conv kernel sources' code (comments and layout ignored): the stored
+    traffic counters are reported only while it matches."""
     import hashlib
     h = hashlib.sha256()
     for f in CONV_SOURCES:
-        h.update(open(f, "rb").read())
+        h.update(strip_comments(open(f).read()).encode())
     return h.hexdigest()
 
 

@@ -17,8 +17,10 @@
 // increasing K with the weights as A operand and the pixels as B operand, lane l holding
 // k-range 8 * (l / 32) .. +8 of row l % 32 (with 8 channels, k-step s covers taps 2s and
 // 2s + 1; a tap past the last is zero on both sides); then fma(acc, scale, shift), the
-// fp32 max over each 2x2 window when pooling, integer-max ReLU and one rounding to bf16.
-// The outputs are therefore bitwise those of the GEMM kernel, whatever its tile.
+// max over each 2x2 window when pooling, integer-max ReLU and one rounding to bf16 (with
+// ReLU and pool, ReLU on each value and then the integer max, which equals ReLU of the
+// fp32 max for every non-NaN sum).  The outputs are therefore bitwise those of the GEMM
+// kernel, whatever its tile.
 #include <algorithm>
 #include <atomic>
 #include <type_traits>

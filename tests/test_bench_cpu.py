@@ -80,3 +80,12 @@ def test_pmc_summary_counts_both_conv_kernels(tmp_path):
     assert out["fetch"]["launches"] == 2 and out["write"]["launches"] == 2
     assert abs(out["fetch"]["bytes_per_launch"] - 2.0 * 200.0 * 1024) < 1e-6
     assert abs(out["write"]["bytes_per_launch"] - 20.0 * 1024) < 1e-6
+
+
+def test_source_hash_ignores_comments_not_code():
+    """The stored traffic counters stay valid across comment edits, not code edits."""
+    src = "int f(int a) {  // add one\n  /* the sum */ return a + 1;\n}\n"
+    assert bench.strip_comments(src) == bench.strip_comments("// header\nint f(int a) {\n\n  return a + 1;  }\n".replace("  }", "\n}"))
+    assert bench.strip_comments(src) != bench.strip_comments(src.replace("a + 1", "a + 2"))
+    assert "add one" not in bench.strip_comments(src) and "sum" not in bench.strip_comments(src)
+
