@@ -210,7 +210,8 @@ typedef struct {
                                    events the launch records at the kernel's start and end
                                    (hipExtLaunchKernelGGL start/stop events) */
   int tile_cfg;                 /* bf16 GEMM launches (conv_mfma, splitk_reduce): the tile
-                                   configuration used (rafiki_tile_config); -1 otherwise */
+                                   configuration used (rafiki_tile_config), or the number of
+                                   configurations for the direct conv kernel; -1 otherwise */
   int splits;                   /* the same launches: K splits (1 = unsplit); 0 otherwise */
 } rafiki_trace_rec;
 

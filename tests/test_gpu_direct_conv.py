@@ -58,6 +58,8 @@ CASES = {
     # the fused pool on ragged tiles, with ReLU (maximum on the bit patterns) and without
     "pool_ragged_many_tiles": ([conv(-1, 64, 64, 3), pool(0, 64)], (64, 36, 52), 40, 1),
     "pool_no_relu_ragged": ([conv(-1, 64, 64, 3, relu=False), pool(0, 64)], (64, 20, 36), 6, 1),
+    # an image smaller than one tile, pooled
+    "tiny_4x6_pool": ([conv(-1, 64, 64, 3), pool(0, 64)], (64, 4, 6), 3, 1),
 }
 
 
