@@ -674,13 +674,21 @@ def schedule_desc(ens, n, mask, names, kinds=()):
         return f"grouped: one launch per layer for the {len(members)} {kinds.pop()} members"
     try:
         solo, asc = ens.get_schedule(n, mask)
+        pa, pb = ens.get_schedule_pair(n, mask)
+        lean = ens.get_schedule_tiles(n, mask)
     except Exception:
-        solo, asc = -1, 0
+        solo, asc, pa, pb, lean = -1, 0, -1, -1, 0
+    tiles = "; the layers of maps up to 14x14 on their lean tiles" if lean else ""
+    if pa >= 0:
+        rest = [names[m] for m in members if m not in (pa, pb)]
+        return (f"{names[pa]} and {names[pb]} paired on one lane; {', '.join(rest) or 'nothing'} on a second lane"
+                + tiles)
     if solo < 0:
-        return "all concurrent"
+        return "all concurrent" + tiles
     rest = [names[m] for m in members if m != solo]
     order = "shortest" if asc else "longest"
-    return f"{names[solo]} alone; {', '.join(rest)} one after another on a second lane, {order} alone time first"
+    return (f"{names[solo]} alone; {', '.join(rest)} one after another on a second lane, {order} alone time first"
+            + tiles)
 
 
 def main():

@@ -317,6 +317,23 @@ int rafiki_ensemble_force_tile(rafiki_ensemble_t h, int cfg);
 int rafiki_ensemble_get_schedule(rafiki_ensemble_t h, int n, uint32_t model_subset_mask, int* solo, int* ascending);
 int rafiki_ensemble_set_schedule(rafiki_ensemble_t h, int n, uint32_t model_subset_mask, int solo, int ascending);
 
+/* Tile policy of a kept schedule (Section 5.1: the selected models share the GPU).  The
+ * tuner keeps, beside each layer's fastest tile alone, a lean choice for every unsplit
+ * GEMM layer with an output map of at most 14 x 14 pixels: its fastest tile among those
+ * of 8 waves, at least 128 x 128, K tiles of 64 and an LDS ring of at most 64 KB, which loads fewer
+ * bytes per FLOP than the small tiles such layers prefer alone and leaves room on each
+ * compute unit for the other models' workgroups.  The schedule timing of infer times
+ * every candidate schedule with both policies (when their tiles differ) and keeps the
+ * faster (environment RAFIKI_LEAN_TILES=0 at create: never tried).  Every tile gives
+ * the same bits, so the policy never changes a result.
+ * get_schedule_tiles: the kept choice's policy (*lean = 1: lean tiles); RAFIKI_ERR_INVALID
+ * if no schedule has been chosen yet.
+ * set_schedule_tiles: sets the policy of the kept schedule (lean = 0 or 1;
+ * RAFIKI_ERR_INVALID if none is kept); synchronises the device and drops any kept
+ * graphs.  set_schedule and set_schedule_pair reset it to 0. */
+int rafiki_ensemble_get_schedule_tiles(rafiki_ensemble_t h, int n, uint32_t model_subset_mask, int* lean);
+int rafiki_ensemble_set_schedule_tiles(rafiki_ensemble_t h, int n, uint32_t model_subset_mask, int lean);
+
 /* Paired layers of two different models (Section 5.1: the selected models all run the
  * same batch).  At create, every two bf16 models with different layer lists whose ops
  * align for at least half of the shorter list (a longest common subsequence under equal

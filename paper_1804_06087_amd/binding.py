@@ -27,6 +27,7 @@ EXPORTED = ("rafiki_ensemble_create", "rafiki_ensemble_infer", "rafiki_ensemble_
             "rafiki_ensemble_info", "rafiki_ensemble_trace", "rafiki_ensemble_trace_read",
             "rafiki_tile_config", "rafiki_ensemble_force_tile", "rafiki_ensemble_get_schedule",
             "rafiki_ensemble_set_schedule", "rafiki_ensemble_get_schedule_pair", "rafiki_ensemble_set_schedule_pair",
+            "rafiki_ensemble_get_schedule_tiles", "rafiki_ensemble_set_schedule_tiles",
             "rafiki_ensemble_pairing", "rafiki_ensemble_use_graphs",
             "rafiki_ensemble_graph_stats", "rafiki_combine_mean", "rafiki_combine_vote",
             "rafiki_maxpool_nhwc_bf16", "rafiki_global_avgpool_nhwc_bf16", "rafiki_probe_mfma_bf16",
@@ -121,6 +122,8 @@ def load_library(path: str = LIB_PATH):
     lib.rafiki_ensemble_get_schedule_pair.argtypes = [C.c_void_p, C.c_int, C.c_uint32, C.POINTER(C.c_int),
                                                       C.POINTER(C.c_int)]
     lib.rafiki_ensemble_set_schedule_pair.argtypes = [C.c_void_p, C.c_int, C.c_uint32, C.c_int, C.c_int]
+    lib.rafiki_ensemble_get_schedule_tiles.argtypes = [C.c_void_p, C.c_int, C.c_uint32, C.POINTER(C.c_int)]
+    lib.rafiki_ensemble_set_schedule_tiles.argtypes = [C.c_void_p, C.c_int, C.c_uint32, C.c_int]
     lib.rafiki_ensemble_pairing.argtypes = [C.c_void_p, C.c_int, C.c_int, C.POINTER(C.c_int)]
     lib.rafiki_ensemble_use_graphs.argtypes = [C.c_void_p, C.c_int]
     lib.rafiki_ensemble_graph_stats.argtypes = [C.c_void_p, C.POINTER(C.c_int), C.POINTER(C.c_longlong),
@@ -622,6 +625,16 @@ class Ensemble:
 
     def set_schedule_pair(self, n: int, mask: int, a: int, b: int = -1):
         _check(self._lib.rafiki_ensemble_set_schedule_pair(self._h, n, mask, a, b))
+
+    def get_schedule_tiles(self, n: int, mask: int) -> int:
+        """Tile policy of the schedule kept for (n, mask): 1 if the layers with output maps
+        of at most 14 x 14 pixels take their lean tiles, 0 for the fastest tiles alone."""
+        v = C.c_int(0)
+        _check(self._lib.rafiki_ensemble_get_schedule_tiles(self._h, n, mask, C.byref(v)))
+        return v.value
+
+    def set_schedule_tiles(self, n: int, mask: int, lean: int):
+        _check(self._lib.rafiki_ensemble_set_schedule_tiles(self._h, n, mask, lean))
 
     def pairing(self, a: int, b: int) -> int:
         """Number of aligned ops of models a < b (0: not pairable)."""

@@ -178,6 +178,12 @@ struct rafiki_ensemble_s {
   std::vector<void*> allocs;
   // Tuned tile configuration per batch size, model and op (-1: not a GEMM op).
   std::map<int, std::vector<std::vector<int>>> tuned;
+  // The same per batch size, except that each unsplit GEMM layer with an output map of at
+  // most 14 x 14 pixels takes its fastest lean tile (8 waves, at least 128 x 128, K tiles
+  // of 64, at most 64 KB of LDS ring): more FLOPs per loaded byte than the small tiles those layers
+  // prefer alone, and room on each compute unit for the other models' workgroups when
+  // models run concurrently.  Every tile gives the same bits.
+  std::map<int, std::vector<std::vector<int>>> tuned_lean;
   // Per batch size: each model's forward time alone, estimated when tuning (sum of the
   // chosen tiles' times; GEMM FLOPs / 1e12 when tiles are not timed).
   std::map<int, std::vector<double>> model_ms;
@@ -190,6 +196,7 @@ struct rafiki_ensemble_s {
   // and ascending are then unused.
   struct Sched {
     int solo = -1, ascending = 0, pa = -1, pb = -1;
+    int lean = 0;   // 1: the small-map layers take their lean tiles (tuned_lean)
   };
   std::map<std::pair<int, uint32_t>, Sched> schedule;
   // Pairable models (a < b) of different layer lists: the merged op order of the two,
@@ -199,6 +206,7 @@ struct rafiki_ensemble_s {
   bool tune_schedule = true;
   bool autotune = true;
   bool fuse_branches = true;        // fuse sibling max-over-time convolutions (bf16)
+  bool lean_policy = true;          // the schedule timing also tries the lean tiles
   // Models with identical layer lists share a group id (the lowest index among them);
   // a selection within one group runs as grouped launches (RAFIKI_GROUPED=0: never).
   std::vector<int> group_of;
@@ -1071,6 +1079,22 @@ TraceTile& trace_tile() {
   return t;
 }
 
+// Whether the forward pass being enqueued uses the lean tiles (set by forward()).
+bool& lean_tiles() {
+  thread_local bool on = false;
+  return on;
+}
+
+// A tile of the lean set: 8 waves, at least 128 x 128, K tiles of 64 (one barrier per 64
+// of K; the 32-wide tiles of the same footprint gained a third as much alongside other
+// models) and a ring of at most 64 KB.
+bool lean_cfg(int cfg) {
+  if (cfg < 0 || cfg >= kNumMfmaConfigs) return false;
+  const MfmaConfig& c = kMfmaConfigs[cfg];
+  return c.waves == 8 && c.bm * c.bn >= 128 * 128 && c.bk == 64 &&
+         (long long)c.stages * (c.bm + c.bn) * c.bk * 2 <= 64 * 1024;
+}
+
 #define TRACED(e, s, kind, model, layer, flops, bytes, expr)                                  \
   do {                                                                                        \
     hipEvent_t ta_ = nullptr, tb_ = nullptr, pa_ = nullptr, pb_ = nullptr;                    \
@@ -1281,6 +1305,7 @@ int tune(rafiki_ensemble_s* e, int n, const void* in, hipStream_t s) {
     }
   }
   if (!timing) {
+    e->tuned_lean[n] = choice;
     e->tuned[n] = std::move(choice);
     e->model_ms[n] = std::move(est);
     return RAFIKI_OK;
@@ -1334,15 +1359,25 @@ int tune(rafiki_ensemble_s* e, int n, const void* in, hipStream_t s) {
   e->force_tile = saved_force;
   e->trace.on = saved_trace;
   if (rc) return rc;
+  std::vector<std::vector<int>> lean(NM);
   for (size_t mi = 0; mi < NM; ++mi) {
     est[mi] = 0.0;
+    lean[mi] = choice[mi];
     for (size_t oi = 0; oi < cand[mi].size(); ++oi) {
       float t = 1e30f;
       for (int cfg : cand[mi][oi])
         if (best[mi][oi][cfg] < t) { t = best[mi][oi][cfg]; choice[mi][oi] = cfg; }
       if (t < 1e29f) est[mi] += t;
+      const Op& op = e->models[mi].ops[oi];
+      lean[mi][oi] = choice[mi][oi];
+      if (op.Ho * op.Wo > 196 || op.Ho * op.Wo < 2 || choose_splits(n * op.Ho * op.Wo, op.c_out, op.Kp / 64) > 1)
+        continue;
+      float tl = 1e30f;
+      for (int cfg : cand[mi][oi])
+        if (lean_cfg(cfg) && best[mi][oi][cfg] < tl) { tl = best[mi][oi][cfg]; lean[mi][oi] = cfg; }
     }
   }
+  e->tuned_lean[n] = std::move(lean);
   e->tuned[n] = std::move(choice);
   e->model_ms[n] = std::move(est);
   return RAFIKI_OK;
@@ -1364,9 +1399,10 @@ int run_op(const rafiki_ensemble_s* e, const int* mis, const int* ois, int nm, c
   if (nm < 1 || nm > kMaxGroup) return fail(RAFIKI_ERR_INVALID, "internal: group size");
   const int mi = mis[0];
   const Model& M = e->models[mi];
-  const auto it = e->tuned.find(n);
+  const auto& table = lean_tiles() ? e->tuned_lean : e->tuned;
+  const auto it = table.find(n);
   const std::vector<int> empty;
-  const std::vector<int>& cfgs = it == e->tuned.end() ? empty : it->second[mi];
+  const std::vector<int>& cfgs = it == table.end() ? empty : it->second[mi];
   const int bf = e->precision == RAFIKI_BF16 ? 1 : 0;
   const double es = (double)e->esz();
   const size_t oi = (size_t)ois[0];
@@ -1692,6 +1728,7 @@ int rafiki_ensemble_create(const rafiki_model_desc* models, int n_models, const 
   if (const char* t = std::getenv("RAFIKI_GRAPHS")) e->use_graphs = std::atoi(t) != 0;
   if (const char* t = std::getenv("RAFIKI_SCHEDULE_TUNING")) e->tune_schedule = std::atoi(t) != 0;
   if (const char* t = std::getenv("RAFIKI_FUSE_BRANCHES")) e->fuse_branches = std::atoi(t) != 0;
+  if (const char* t = std::getenv("RAFIKI_LEAN_TILES")) e->lean_policy = std::atoi(t) != 0;
   if (const char* t = std::getenv("RAFIKI_GROUPED")) e->grouped = std::atoi(t) != 0;
   if (const char* t = std::getenv("RAFIKI_FUSED_NET")) e->fused_net = std::atoi(t) != 0;
   // Pass 1: validate every model and infer shapes without touching the device.
@@ -1908,6 +1945,10 @@ static int forward(rafiki_ensemble_t h, const CombineArgs& ca, const void* in, i
                    rafiki_ensemble_s::Sched sched, const CallScratch* ws = nullptr) {
   const int solo = sched.solo;
   int rc = RAFIKI_OK;
+  struct LeanScope {   // the schedule's tile table for the launches enqueued below
+    explicit LeanScope(bool on) { lean_tiles() = on; }
+    ~LeanScope() { lean_tiles() = false; }
+  } lean_scope(sched.lean != 0);
   if (fused_selection(h, ca)) {   // every selected model in one launch
     uint32_t mask = 0;
     for (int i = 0; i < ca.S; ++i) mask |= 1u << ca.sel[i];
@@ -2026,6 +2067,19 @@ static int pick_schedule(rafiki_ensemble_t h, const CombineArgs& ca, const void*
       cands.push_back({ca.sel[i], 1});
     }
   for (const auto& pr : pairs) cands.push_back({-1, 0, pr.first, pr.second});
+  // each schedule also with the lean tiles, where they differ from the fastest alone
+  const auto tl = h->tuned_lean.find(n), tf = h->tuned.find(n);
+  bool differ = false;
+  if (tl != h->tuned_lean.end() && tf != h->tuned.end())
+    for (int i = 0; i < ca.S; ++i) differ = differ || tl->second[ca.sel[i]] != tf->second[ca.sel[i]];
+  if (differ && h->lean_policy) {
+    const size_t k = cands.size();
+    for (size_t i = 0; i < k; ++i) {
+      rafiki_ensemble_s::Sched c = cands[i];
+      c.lean = 1;
+      cands.push_back(c);
+    }
+  }
   hipEvent_t ev[2] = {nullptr, nullptr};
   HIPCHK(hipEventCreate(&ev[0]));
   hipError_t st = hipEventCreate(&ev[1]);
@@ -2390,6 +2444,25 @@ int rafiki_ensemble_set_schedule(rafiki_ensemble_t h, int n, uint32_t mask, int 
   HIPCHK(hipDeviceSynchronize());   // graphs built with the old schedule may still run
   h->drop_graphs();
   h->schedule[std::make_pair(n, mask)] = {solo, ascending ? 1 : 0};
+  return RAFIKI_OK;
+}
+
+int rafiki_ensemble_get_schedule_tiles(rafiki_ensemble_t h, int n, uint32_t mask, int* lean) {
+  if (!h || !lean) return fail(RAFIKI_ERR_INVALID, "null argument");
+  const auto it = h->schedule.find(std::make_pair(n, mask));
+  if (it == h->schedule.end()) return fail(RAFIKI_ERR_INVALID, "no schedule chosen for this batch size and subset");
+  *lean = it->second.lean;
+  return RAFIKI_OK;
+}
+
+int rafiki_ensemble_set_schedule_tiles(rafiki_ensemble_t h, int n, uint32_t mask, int lean) {
+  if (!h) return fail(RAFIKI_ERR_INVALID, "null handle");
+  if (lean != 0 && lean != 1) return fail(RAFIKI_ERR_INVALID, "lean must be 0 or 1");
+  const auto it = h->schedule.find(std::make_pair(n, mask));
+  if (it == h->schedule.end()) return fail(RAFIKI_ERR_INVALID, "no schedule chosen for this batch size and subset");
+  HIPCHK(hipDeviceSynchronize());   // graphs built with the old policy may still run
+  h->drop_graphs();
+  it->second.lean = lean;
   return RAFIKI_OK;
 }
 

@@ -71,3 +71,48 @@ def test_schedule_arguments():
             ens.set_schedule(8, 0b1000, -1)            # no such model
         ens.set_schedule(8, 0b111, 1, 1)
         assert ens.get_schedule(8, 0b111) == (1, 1)
+
+
+def test_lean_tiles_give_the_same_bits():
+    """The tile policy of a schedule (rafiki_ensemble_get/set_schedule_tiles): with the
+    lean tiles the layers of maps up to 14 x 14 run on 8-wave tiles of at least 128 x 128
+    with K tiles of 64 and at most 64 KB of LDS ring, and the results are bit-identical to the fastest
+    tiles alone; set_schedule resets the policy."""
+    from paper_1804_06087_amd.binding import tile_configs
+    n, mask = 8, 0b111
+    cfg, specs, params, batch = wl.build_config(3, n=n)   # ResNet-50, VGG-16, ResNet-101
+    C = specs[0].n_classes
+    x = torch.from_numpy(batch).to(DEV)
+    tiles = tile_configs()
+    lean_ids = {i for i, t in enumerate(tiles)
+                if t["waves"] == 8 and t["bm"] * t["bn"] >= 128 * 128 and t["bk"] == 64
+                and t["stages"] * (t["bm"] + t["bn"]) * t["bk"] * 2 <= 65536}
+    assert lean_ids
+    with Ensemble(specs, params, precision="bf16", max_batch=n) as ens:
+        with pytest.raises(RafikiError):
+            ens.get_schedule_tiles(n, mask)           # nothing chosen yet
+        p0, l0 = _infer(ens, x, n, mask, C)
+        assert ens.get_schedule_tiles(n, mask) in (0, 1)
+        with pytest.raises(RafikiError):
+            ens.set_schedule_tiles(n, mask, 2)
+        with pytest.raises(RafikiError):
+            ens.set_schedule_tiles(n, 0b011, 1)       # no schedule kept for this subset
+        for lean in (1, 0, 1):
+            ens.set_schedule_tiles(n, mask, lean)
+            assert ens.get_schedule_tiles(n, mask) == lean
+            for _ in range(2):
+                p, lab = _infer(ens, x, n, mask, C)
+                assert np.array_equal(p, p0), f"lean {lean}: probabilities differ"
+                assert np.array_equal(lab, l0), f"lean {lean}: labels differ"
+            ens.trace(True, concurrent=True)
+            _infer(ens, x, n, mask, C)
+            recs = ens.trace_read()
+            ens.trace(False)
+            small = [r for r in recs if r["kind"] == "conv_mfma" and r["splits"] == 1 and r["tile_cfg"] < len(tiles)
+                     and r["flops"] > 0]
+            used = {r["tile_cfg"] for r in small}
+            if lean:
+                assert used & lean_ids, used
+        solo, asc = ens.get_schedule(n, mask)
+        ens.set_schedule(n, mask, solo, asc)
+        assert ens.get_schedule_tiles(n, mask) == 0
