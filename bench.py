@@ -679,6 +679,8 @@ def schedule_desc(ens, n, mask, names, kinds=()):
     except Exception:
         solo, asc, pa, pb, lean = -1, 0, -1, -1, 0
     tiles = "; the layers of maps up to 14x14 on their lean tiles" if lean else ""
+    if lean == 2 and solo >= 0:
+        tiles += f", {names[solo]}'s direct-conv layers on GEMM tiles"
     if pa >= 0:
         rest = [names[m] for m in members if m not in (pa, pb)]
         return (f"{names[pa]} and {names[pb]} paired on one lane; {', '.join(rest) or 'nothing'} on a second lane"

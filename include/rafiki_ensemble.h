@@ -326,9 +326,15 @@ int rafiki_ensemble_set_schedule(rafiki_ensemble_t h, int n, uint32_t model_subs
  * every candidate schedule with both policies (when their tiles differ) and keeps the
  * faster (environment RAFIKI_LEAN_TILES=0 at create: never tried).  Every tile gives
  * the same bits, so the policy never changes a result.
- * get_schedule_tiles: the kept choice's policy (*lean = 1: lean tiles); RAFIKI_ERR_INVALID
- * if no schedule has been chosen yet.
- * set_schedule_tiles: sets the policy of the kept schedule (lean = 0 or 1;
+ * With a model alone on its lane there is a third policy: the lean tiles, and that
+ * model's layers that would take the direct conv kernel on their fastest GEMM tile
+ * instead (the direct kernel's persistent workgroups fill each compute unit's LDS and
+ * leave no room for the other lane's workgroups).
+ * get_schedule_tiles: the kept choice's policy (*lean = 0: the tiles fastest alone, 1:
+ * lean tiles, 2: lean tiles and GEMM tiles for the solo model); RAFIKI_ERR_INVALID if no
+ * schedule has been chosen yet.
+ * set_schedule_tiles: sets the policy of the kept schedule (lean = 0, 1 or 2, where 2
+ * acts as 1 without a solo model;
  * RAFIKI_ERR_INVALID if none is kept); synchronises the device and drops any kept
  * graphs.  set_schedule and set_schedule_pair reset it to 0. */
 int rafiki_ensemble_get_schedule_tiles(rafiki_ensemble_t h, int n, uint32_t model_subset_mask, int* lean);

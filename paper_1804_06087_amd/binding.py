@@ -627,8 +627,9 @@ class Ensemble:
         _check(self._lib.rafiki_ensemble_set_schedule_pair(self._h, n, mask, a, b))
 
     def get_schedule_tiles(self, n: int, mask: int) -> int:
-        """Tile policy of the schedule kept for (n, mask): 1 if the layers with output maps
-        of at most 14 x 14 pixels take their lean tiles, 0 for the fastest tiles alone."""
+        """Tile policy of the schedule kept for (n, mask): 0 the fastest tiles alone; 1 the
+        layers with output maps of at most 14 x 14 pixels on their lean tiles; 2 as 1, and
+        the model alone on its lane without the direct conv kernel (GEMM tiles)."""
         v = C.c_int(0)
         _check(self._lib.rafiki_ensemble_get_schedule_tiles(self._h, n, mask, C.byref(v)))
         return v.value

@@ -184,6 +184,10 @@ struct rafiki_ensemble_s {
   // prefer alone, and room on each compute unit for the other models' workgroups when
   // models run concurrently.  Every tile gives the same bits.
   std::map<int, std::vector<std::vector<int>>> tuned_lean;
+  // tuned_lean with every direct-conv choice replaced by the layer's fastest GEMM tile:
+  // the direct kernel's persistent workgroups fill each compute unit's LDS, which leaves
+  // no room for the other lane's workgroups while it runs.
+  std::map<int, std::vector<std::vector<int>>> tuned_lean_gemm;
   // Per batch size: each model's forward time alone, estimated when tuning (sum of the
   // chosen tiles' times; GEMM FLOPs / 1e12 when tiles are not timed).
   std::map<int, std::vector<double>> model_ms;
@@ -196,7 +200,8 @@ struct rafiki_ensemble_s {
   // and ascending are then unused.
   struct Sched {
     int solo = -1, ascending = 0, pa = -1, pb = -1;
-    int lean = 0;   // 1: the small-map layers take their lean tiles (tuned_lean)
+    int lean = 0;   // 1: the small-map layers take their lean tiles (tuned_lean); 2: also the
+                    // solo model's direct-conv layers take their fastest GEMM tile (tuned_lean_gemm)
   };
   std::map<std::pair<int, uint32_t>, Sched> schedule;
   // Pairable models (a < b) of different layer lists: the merged op order of the two,
@@ -1079,10 +1084,15 @@ TraceTile& trace_tile() {
   return t;
 }
 
-// Whether the forward pass being enqueued uses the lean tiles (set by forward()).
-bool& lean_tiles() {
-  thread_local bool on = false;
-  return on;
+// Tile policy of the forward pass being enqueued (set by forward()): 0 the tiles fastest
+// alone, 1 the lean tiles, 2 the lean tiles and GEMM tiles for model lean_gemm_model().
+int& lean_tiles() {
+  thread_local int level = 0;
+  return level;
+}
+int& lean_gemm_model() {
+  thread_local int m = -1;
+  return m;
 }
 
 // A tile of the lean set: 8 waves, at least 128 x 128, K tiles of 64 (one barrier per 64
@@ -1306,6 +1316,7 @@ int tune(rafiki_ensemble_s* e, int n, const void* in, hipStream_t s) {
   }
   if (!timing) {
     e->tuned_lean[n] = choice;
+    e->tuned_lean_gemm[n] = choice;
     e->tuned[n] = std::move(choice);
     e->model_ms[n] = std::move(est);
     return RAFIKI_OK;
@@ -1377,6 +1388,18 @@ int tune(rafiki_ensemble_s* e, int n, const void* in, hipStream_t s) {
         if (lean_cfg(cfg) && best[mi][oi][cfg] < tl) { tl = best[mi][oi][cfg]; lean[mi][oi] = cfg; }
     }
   }
+  std::vector<std::vector<int>> lean_gemm = lean;
+  for (size_t mi = 0; mi < NM; ++mi)
+    for (size_t oi = 0; oi < cand[mi].size(); ++oi) {
+      if (lean_gemm[mi][oi] != kCfgDirect) continue;
+      const Op& op = e->models[mi].ops[oi];
+      float t = 1e30f;
+      int pick = default_cfg(op.c_out);
+      for (int cfg : cand[mi][oi])
+        if (cfg != kCfgDirect && best[mi][oi][cfg] < t) { t = best[mi][oi][cfg]; pick = cfg; }
+      lean_gemm[mi][oi] = pick;
+    }
+  e->tuned_lean_gemm[n] = std::move(lean_gemm);
   e->tuned_lean[n] = std::move(lean);
   e->tuned[n] = std::move(choice);
   e->model_ms[n] = std::move(est);
@@ -1399,7 +1422,8 @@ int run_op(const rafiki_ensemble_s* e, const int* mis, const int* ois, int nm, c
   if (nm < 1 || nm > kMaxGroup) return fail(RAFIKI_ERR_INVALID, "internal: group size");
   const int mi = mis[0];
   const Model& M = e->models[mi];
-  const auto& table = lean_tiles() ? e->tuned_lean : e->tuned;
+  const auto& table = lean_tiles() == 2 && mi == lean_gemm_model() ? e->tuned_lean_gemm
+                      : lean_tiles() ? e->tuned_lean : e->tuned;
   const auto it = table.find(n);
   const std::vector<int> empty;
   const std::vector<int>& cfgs = it == table.end() ? empty : it->second[mi];
@@ -1945,10 +1969,10 @@ static int forward(rafiki_ensemble_t h, const CombineArgs& ca, const void* in, i
                    rafiki_ensemble_s::Sched sched, const CallScratch* ws = nullptr) {
   const int solo = sched.solo;
   int rc = RAFIKI_OK;
-  struct LeanScope {   // the schedule's tile table for the launches enqueued below
-    explicit LeanScope(bool on) { lean_tiles() = on; }
-    ~LeanScope() { lean_tiles() = false; }
-  } lean_scope(sched.lean != 0);
+  struct LeanScope {   // the schedule's tile tables for the launches enqueued below
+    LeanScope(int level, int solo) { lean_tiles() = level; lean_gemm_model() = solo; }
+    ~LeanScope() { lean_tiles() = 0; lean_gemm_model() = -1; }
+  } lean_scope(sched.lean, sched.solo);
   if (fused_selection(h, ca)) {   // every selected model in one launch
     uint32_t mask = 0;
     for (int i = 0; i < ca.S; ++i) mask |= 1u << ca.sel[i];
@@ -2072,12 +2096,21 @@ static int pick_schedule(rafiki_ensemble_t h, const CombineArgs& ca, const void*
   bool differ = false;
   if (tl != h->tuned_lean.end() && tf != h->tuned.end())
     for (int i = 0; i < ca.S; ++i) differ = differ || tl->second[ca.sel[i]] != tf->second[ca.sel[i]];
-  if (differ && h->lean_policy) {
+  // and a schedule with a model alone on its lane also with that model's direct-conv
+  // layers on GEMM tiles, where it has any
+  const auto tg = h->tuned_lean_gemm.find(n);
+  if (h->lean_policy && tl != h->tuned_lean.end() && tg != h->tuned_lean_gemm.end()) {
     const size_t k = cands.size();
     for (size_t i = 0; i < k; ++i) {
       rafiki_ensemble_s::Sched c = cands[i];
-      c.lean = 1;
-      cands.push_back(c);
+      if (differ) {
+        c.lean = 1;
+        cands.push_back(c);
+      }
+      if (c.solo >= 0 && tg->second[c.solo] != tl->second[c.solo]) {
+        c.lean = 2;
+        cands.push_back(c);
+      }
     }
   }
   hipEvent_t ev[2] = {nullptr, nullptr};
@@ -2457,7 +2490,7 @@ int rafiki_ensemble_get_schedule_tiles(rafiki_ensemble_t h, int n, uint32_t mask
 
 int rafiki_ensemble_set_schedule_tiles(rafiki_ensemble_t h, int n, uint32_t mask, int lean) {
   if (!h) return fail(RAFIKI_ERR_INVALID, "null handle");
-  if (lean != 0 && lean != 1) return fail(RAFIKI_ERR_INVALID, "lean must be 0 or 1");
+  if (lean < 0 || lean > 2) return fail(RAFIKI_ERR_INVALID, "lean must be 0, 1 or 2");
   const auto it = h->schedule.find(std::make_pair(n, mask));
   if (it == h->schedule.end()) return fail(RAFIKI_ERR_INVALID, "no schedule chosen for this batch size and subset");
   HIPCHK(hipDeviceSynchronize());   // graphs built with the old policy may still run

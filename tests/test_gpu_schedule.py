@@ -76,7 +76,8 @@ def test_schedule_arguments():
 def test_lean_tiles_give_the_same_bits():
     """The tile policy of a schedule (rafiki_ensemble_get/set_schedule_tiles): with the
     lean tiles the layers of maps up to 14 x 14 run on 8-wave tiles of at least 128 x 128
-    with K tiles of 64 and at most 64 KB of LDS ring, and the results are bit-identical to the fastest
+    with K tiles of 64 and at most 64 KB of LDS ring, with policy 2 also the solo model's
+    direct-conv layers on GEMM tiles, and the results are bit-identical to the fastest
     tiles alone; set_schedule resets the policy."""
     from paper_1804_06087_amd.binding import tile_configs
     n, mask = 8, 0b111
@@ -92,12 +93,13 @@ def test_lean_tiles_give_the_same_bits():
         with pytest.raises(RafikiError):
             ens.get_schedule_tiles(n, mask)           # nothing chosen yet
         p0, l0 = _infer(ens, x, n, mask, C)
-        assert ens.get_schedule_tiles(n, mask) in (0, 1)
+        assert ens.get_schedule_tiles(n, mask) in (0, 1, 2)
         with pytest.raises(RafikiError):
-            ens.set_schedule_tiles(n, mask, 2)
+            ens.set_schedule_tiles(n, mask, 3)
         with pytest.raises(RafikiError):
             ens.set_schedule_tiles(n, 0b011, 1)       # no schedule kept for this subset
-        for lean in (1, 0, 1):
+        ens.set_schedule(n, mask, 2, 0)                # ResNet-101 alone on a lane
+        for lean in (1, 0, 2, 1):
             ens.set_schedule_tiles(n, mask, lean)
             assert ens.get_schedule_tiles(n, mask) == lean
             for _ in range(2):
@@ -113,6 +115,9 @@ def test_lean_tiles_give_the_same_bits():
             used = {r["tile_cfg"] for r in small}
             if lean:
                 assert used & lean_ids, used
+            direct_r101 = [r for r in recs if r["kind"] == "conv_mfma" and r["model"] == 2 and r["tile_cfg"] == len(tiles)]
+            if lean == 2:
+                assert not direct_r101       # the solo model's direct-conv layers on GEMM tiles
         solo, asc = ens.get_schedule(n, mask)
         ens.set_schedule(n, mask, solo, asc)
         assert ens.get_schedule_tiles(n, mask) == 0
