@@ -303,8 +303,8 @@ int rafiki_ensemble_force_tile(rafiki_ensemble_t h, int cfg);
 /* Schedule of the selected models' forward passes for one (n, model_subset_mask).
  * The models are independent until the combine and run on their own streams.  With
  * three or more selected models, the first infer / infer_vote of a (n, mask) pair times
- * each candidate schedule on `stream` (best of three runs each; it blocks the caller
- * once) and keeps the fastest: solo = -1, all models concurrently; solo = m, model m
+ * each candidate schedule on `stream` (best of four runs each, the candidates in turn;
+ * it blocks the caller once) and keeps the fastest: solo = -1, all models concurrently; solo = m, model m
  * alone on one lane while the other selected models run one after another on a second
  * lane, longest estimated alone time first (ascending = 0) or shortest first
  * (ascending = 1).  A schedule only orders the same launches, so it never changes a

@@ -2121,23 +2121,24 @@ static int pick_schedule(rafiki_ensemble_t h, const CombineArgs& ca, const void*
     return fail(RAFIKI_ERR_HIP, std::string("hipEventCreate: ") + hipGetErrorString(st));
   }
   int rc = RAFIKI_OK;
-  rafiki_ensemble_s::Sched best_sched;
-  float best = 1e30f;
-  for (const auto& cand : cands) {
-    float t = 1e30f;
-    for (int rep = 0; rep < 3 && rc == RAFIKI_OK; ++rep) {   // best of three
+  // Best of four runs each, the candidates taken in turn in every round, so that a drift
+  // of the device's clocks during the timing affects them alike.
+  std::vector<float> tbest(cands.size(), 1e30f);
+  for (int rep = 0; rep < 4 && rc == RAFIKI_OK; ++rep)
+    for (size_t ci = 0; ci < cands.size() && rc == RAFIKI_OK; ++ci) {
       st = hipEventRecord(ev[0], s);
-      if (st == hipSuccess) rc = forward(h, ca, in, n, s, cand, ws);
+      if (st == hipSuccess) rc = forward(h, ca, in, n, s, cands[ci], ws);
       if (st == hipSuccess && rc == RAFIKI_OK) st = hipEventRecord(ev[1], s);
       if (st == hipSuccess && rc == RAFIKI_OK) st = hipEventSynchronize(ev[1]);
       float ms = 0.f;
       if (st == hipSuccess && rc == RAFIKI_OK) st = hipEventElapsedTime(&ms, ev[0], ev[1]);
       if (st != hipSuccess && rc == RAFIKI_OK) rc = fail(RAFIKI_ERR_HIP, std::string("schedule timing: ") + hipGetErrorString(st));
-      if (rc == RAFIKI_OK) t = std::min(t, ms);
+      if (rc == RAFIKI_OK) tbest[ci] = std::min(tbest[ci], ms);
     }
-    if (rc) break;
-    if (t < best) { best = t; best_sched = cand; }
-  }
+  rafiki_ensemble_s::Sched best_sched;
+  float best = 1e30f;
+  for (size_t ci = 0; ci < cands.size() && rc == RAFIKI_OK; ++ci)
+    if (tbest[ci] < best) { best = tbest[ci]; best_sched = cands[ci]; }
   (void)hipEventDestroy(ev[0]);
   (void)hipEventDestroy(ev[1]);
   if (rc) return rc;
